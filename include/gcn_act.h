@@ -1,0 +1,332 @@
+/*
+ * gcn_act.h - C ABI of the MI355X subgraph GCN training hot path.
+ *
+ * Method: GraphACT (Zeng & Prasanna, FPGA '20). A minibatch is a subgraph
+ * G_s induced on sampled vertices (Section 3.1); every layer aggregates
+ * neighbour features with D^-1 A and transforms them with two weight
+ * matrices (Eq. 1); gradients follow Eq. 2a-2c; the aggregation may run on
+ * the redundancy-reduced graph G_s^# whose extra vertices are pre-computed
+ * sums of neighbour pairs (Section 3.2, Algorithms 1-3; Section 4.2).
+ *
+ * Conventions (every entry point):
+ *   - Returns GCN_OK (0) or a negative status; gcn_last_error() gives a
+ *     thread-local message for the last failing call on this thread.
+ *   - All arguments are validated before anything is enqueued; on error no
+ *     device work is launched and no output is touched.
+ *   - Host objects (gcn_graph_t, gcn_reduced_t) are created and freed by the
+ *     library. Calls on distinct objects may run concurrently from different
+ *     threads.
+ *   - Device buffers are caller-owned. Dense matrices are row-major float32
+ *     with an explicit leading dimension ld (in elements): ld >= width,
+ *     ld % 4 == 0, base pointer 16-byte aligned. Weight matrices are dense
+ *     with ld == width. The library never allocates device memory; scratch
+ *     space is the caller's `ws` buffer (256-byte aligned) of `ws_bytes`.
+ *   - Device entry points take a stream (a hipStream_t passed as void*; NULL
+ *     is the null stream), only enqueue work on it, never synchronise, and
+ *     return before the work completes.
+ *   - Vertex indices are int32; sizes that can exceed 2^31 are int64.
+ *   - Columns of an output beyond its logical width are never written.
+ */
+#ifndef GCN_ACT_H
+#define GCN_ACT_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* ------------------------------------------------------------ status */
+#define GCN_OK              0
+#define GCN_E_INVALID_ARG  (-1)  /* bad pointer, size, layout or graph     */
+#define GCN_E_HIP          (-2)  /* a HIP runtime call failed              */
+#define GCN_E_OOM          (-3)  /* host allocation failed                 */
+#define GCN_E_UNSUPPORTED  (-4)  /* valid request this build cannot serve  */
+#define GCN_E_WORKSPACE    (-5)  /* ws_bytes below the required size       */
+#define GCN_E_INTERNAL     (-6)
+
+#define GCN_MAX_ROUNDS 64
+#define GCN_MAX_LAYERS 8
+
+#define GCN_LOSS_SOFTMAX_CE 0    /* labels: int32[n] class ids            */
+#define GCN_LOSS_SIGMOID_BCE 1   /* labels: uint8[n*C] 0/1, row-major     */
+
+#define GCN_PREC_FP32 0          /* fp32 MFMA for the dense products      */
+#define GCN_PREC_BF16 1          /* bf16 MFMA operands, fp32 accumulation */
+
+#define GCN_AGG_MEAN 0           /* Y = D^-1 A X        (forward, Eq. 1)   */
+#define GCN_AGG_TRANSPOSED 1     /* Y = A D^-1 X        (backward, Eq. 2c) */
+
+typedef void* gcn_stream_t;      /* hipStream_t */
+
+/* Message of the last failing call on this thread ("" if none). */
+const char* gcn_last_error(void);
+
+/* ABI version of this header (bumped on incompatible change). */
+int gcn_abi_version(void);
+#define GCN_ABI_VERSION 1
+
+/* ------------------------------------------------ subgraph (host, a1)
+ * gcn_subgraph_build - undirected simple subgraph in CSR form.
+ * Section 2.1: the input graph is undirected, A is its 0/1 adjacency and D
+ * the diagonal degree matrix. Section 3.1: a minibatch is the subgraph
+ * induced on a vertex subset, used by every layer.
+ *   n_full      vertices of the full graph (ids 0..n_full-1), < 2^31
+ *   src,dst     host int64[n_edges]; edge i joins src[i] and dst[i], either
+ *               direction; repeats and self-loops are allowed and dropped
+ *   vertices    host int64[n_vertices] subset (vertex vertices[k] becomes k)
+ *               or NULL for all n_full vertices
+ *   out         receives a new graph; free with gcn_graph_free
+ * Errors: GCN_E_INVALID_ARG for out-of-range or repeated ids, negative
+ * sizes or NULL pointers with nonzero sizes; GCN_E_OOM.
+ */
+typedef struct gcn_graph* gcn_graph_t;
+int gcn_subgraph_build(int64_t n_full, const int64_t* src, const int64_t* dst,
+                       int64_t n_edges, const int64_t* vertices,
+                       int64_t n_vertices, gcn_graph_t* out);
+
+/* Borrowed views (valid until gcn_graph_free): rowptr int32[n+1], col
+ * int32[nnz], each row sorted ascending, symmetric, no self-loops. */
+int gcn_graph_info(gcn_graph_t g, int32_t* n, int64_t* nnz,
+                   const int32_t** rowptr, const int32_t** col);
+void gcn_graph_free(gcn_graph_t g);
+
+/* ------------------------------------- redundancy reduction (host, a2)
+ * gcn_redundancy_reduce - rounds of Algorithms 1-3 (Section 3.2).
+ * Each round counts, for every pair of vertices, the neighbour lists that
+ * hold both (Alg. 1); takes pairs greedily by decreasing count while the
+ * count exceeds theta, skipping pairs with an endpoint already taken
+ * (Alg. 2; equal counts in ascending (smaller id, larger id) order); gives
+ * the k-th taken pair of the round the id n + (pairs of earlier rounds) + k
+ * and replaces the pair by that id in every list holding both (Alg. 3);
+ * lists stay sorted. Rounds stop at max_rounds, at an empty matching, or
+ * when max_aux new vertices exist (a pair is taken only while the total is
+ * below max_aux; < 0 means no cap). max_rounds == 0 gives the input graph
+ * unchanged (direct aggregation).
+ *   num_threads  host threads for the pair counting (0: all hardware
+ *                threads, capped at 64); results do not depend on it
+ * Errors: GCN_E_INVALID_ARG (theta < 0, max_rounds outside
+ * [0, GCN_MAX_ROUNDS], NULL); GCN_E_OOM.
+ */
+typedef struct {
+    int32_t theta;        /* default 2 */
+    int32_t max_rounds;   /* default 5 */
+    int64_t max_aux;      /* default -1 (no cap) */
+    int32_t num_threads;  /* default 0 */
+    int32_t reserved;
+} gcn_rr_params;
+
+typedef struct {
+    int64_t matched;      /* |M| of the round                        */
+    int64_t weight_sum;   /* sum of the taken pairs' counts          */
+    int64_t nnz;          /* numRead of the lists after the round    */
+    int64_t num_add;      /* numAdd of the lists after the round     */
+} gcn_rr_round;
+
+typedef struct gcn_reduced* gcn_reduced_t;
+int gcn_redundancy_reduce(gcn_graph_t g, const gcn_rr_params* params,
+                          gcn_reduced_t* out);
+
+/* Borrowed views (valid until gcn_reduced_free):
+ *   rowptr int32[n+1], col int32[nnz]  lists of G_s^# for the n original
+ *                     vertices; ids >= n name pair sums
+ *   pairs  int32[naux*2]  pair k = (pairs[2k], pairs[2k+1]), smaller first;
+ *                     its sum is vertex n+k
+ *   round_offsets int32[rounds+1]; per_round gcn_rr_round[rounds]
+ *   deg    int32[n]   degrees of the ORIGINAL subgraph (D of Eq. 1)      */
+int gcn_reduced_info(gcn_reduced_t r, int32_t* n, int32_t* naux,
+                     int32_t* rounds, int64_t* nnz, const int32_t** rowptr,
+                     const int32_t** col, const int32_t** pairs,
+                     const int32_t** round_offsets,
+                     const gcn_rr_round** per_round, const int32_t** deg);
+void gcn_reduced_free(gcn_reduced_t r);
+
+/* ------------------------------------------------ device graph image
+ * The device form of G_s^# (what the accelerator receives in Section 4.1:
+ * the lists, the pairs and D), plus a work list that splits long lists
+ * into segments of at most `seg_len` entries for load balance.
+ * gcn_graph_image_bytes - size of the packed image (host and device).
+ * gcn_graph_pack        - write the image into a caller host buffer (may
+ *                         be pinned); the reduced object may then be freed.
+ * gcn_graph_upload      - copy the image to a caller device buffer on
+ *                         `stream` (hipMemcpyAsync; the host buffer must
+ *                         stay valid until the copy completes) and fill the
+ *                         descriptor, whose pointers are into dev_buf.
+ * seg_len: 0 selects the default (64); otherwise 1..65536.
+ */
+typedef struct {
+    int32_t n, naux, rounds, seg_len;
+    int32_t nseg, nlong, nslots, max_row;
+    int64_t nnz;
+    const int32_t* rowptr;     /* device int32[n+1]                  */
+    const int32_t* col;        /* device int32[nnz]                  */
+    const int32_t* pairs;      /* device int32[2*naux]               */
+    const float* inv_deg;      /* device float[n], 1/d (0 if d == 0) */
+    const int32_t* seg;        /* device int32[4*nseg]               */
+    const int32_t* longrows;   /* device int32[4*nlong]              */
+    int32_t round_offsets[GCN_MAX_ROUNDS + 1];   /* host copy        */
+} gcn_dgraph;
+
+int gcn_graph_image_bytes(gcn_reduced_t r, int32_t seg_len, size_t* bytes);
+int gcn_graph_pack(gcn_reduced_t r, int32_t seg_len, void* host_buf,
+                   size_t bytes);
+int gcn_graph_upload(const void* host_image, size_t bytes, void* dev_buf,
+                     gcn_dgraph* out, gcn_stream_t stream);
+/* Fill the descriptor for an image already resident at dev_buf (host_image
+ * is the same image's host copy; nothing is copied). */
+int gcn_graph_describe(const void* host_image, size_t bytes,
+                       const void* dev_buf, gcn_dgraph* out);
+
+/* ------------------------------------------------------- scratch size
+ * Bytes of `ws` needed by gcn_aggregate / gcn_layer_fwd / gcn_layer_bwd /
+ * gcn_classifier_* / gcn_loss for widths up to max_width and row count of
+ * the graph (g may be NULL for the classifier and loss alone, then n is
+ * taken from `n`). */
+int gcn_scratch_bytes(const gcn_dgraph* g, int32_t n, int32_t max_width,
+                      size_t* bytes);
+
+/* ---------------------------------------------- aggregation (a3 a4 a10)
+ * gcn_aggregate - Y = D^-1 A X (GCN_AGG_MEAN, forward aggregation of Eq. 1)
+ * or Y = A D^-1 X (GCN_AGG_TRANSPOSED, the aggregation inside Eq. 2c), run
+ * on G_s^#: pair sums are formed round by round first (Section 4.2 step 1),
+ * then the lists are summed (step 2) and scaled by the original 1/d (step 3,
+ * after the sum for MEAN; on the gathered original rows for TRANSPOSED).
+ * Vertices with d == 0 get zero rows.
+ *   X  device [n x F] ld ldx;  Y  device [n x F] ld ldy (X and Y must not
+ *   overlap). Scratch: pair sums and partial sums of split lists.
+ */
+int gcn_aggregate(const gcn_dgraph* g, int32_t mode, int32_t F,
+                  const float* X, int64_t ldx, float* Y, int64_t ldy,
+                  void* ws, size_t ws_bytes, gcn_stream_t stream);
+
+/* ------------------------------------------------- layer forward (a3-a5)
+ * gcn_layer_fwd - one graph convolutional layer, Eq. 1:
+ *   AH    = D^-1 A H_in                         (saved for Eq. 2b)
+ *   H_out = ReLU( H_in W_self | AH W_neigh  (+ bias) )
+ *   H_in  [n x F] ld ld_in;  W_self, W_neigh [F x h];  bias [2h] or NULL
+ *   AH    [n x F] ld ld_ah;  H_out [n x 2h] ld ld_out (self half first)
+ *   precision GCN_PREC_FP32 (GCN_PREC_BF16: GCN_E_UNSUPPORTED until built)
+ */
+int gcn_layer_fwd(const gcn_dgraph* g, int32_t F, int32_t h,
+                  const float* H_in, int64_t ld_in, const float* W_self,
+                  const float* W_neigh, const float* bias, float* AH,
+                  int64_t ld_ah, float* H_out, int64_t ld_out,
+                  int32_t precision, void* ws, size_t ws_bytes,
+                  gcn_stream_t stream);
+
+/* --------------------------------------------- classifier + loss (a6)
+ * gcn_classifier_fwd - logits = H W_cls (+ b_cls), a linear layer on the
+ * last layer's output (Section 2.1, node classifier).
+ *   H [n x K] ld ldh; W_cls [K x C]; b_cls [C] or NULL; logits [n x C] ldz
+ */
+int gcn_classifier_fwd(int32_t n, int32_t K, int32_t C, const float* H,
+                       int64_t ldh, const float* W_cls, const float* b_cls,
+                       float* logits, int64_t ldz, int32_t precision,
+                       gcn_stream_t stream);
+
+/* gcn_loss - loss and its gradient w.r.t. the logits (Section 2.1: softmax
+ * with cross-entropy; its gradient is a subtraction).
+ *   SOFTMAX_CE : loss = mean_v (logsumexp(z_v) - z_v[y_v]),
+ *                dz   = (softmax(z) - onehot(y)) / n;   labels int32[n]
+ *   SIGMOID_BCE: loss = mean over n*C of
+ *                       max(z,0) - z y + log(1 + exp(-|z|)),
+ *                dz   = (sigmoid(z) - y) / (n C);        labels uint8[n*C]
+ *   logits, dlogits [n x C] (ld ldz, ldd; may be the same buffer);
+ *   loss_out device float[1]. Deterministic (fixed summation order).
+ * Errors: labels are not range-checked on the device; class ids outside
+ * [0, C) give an undefined loss but no out-of-bounds access. */
+int gcn_loss(int32_t n, int32_t C, int32_t kind, const float* logits,
+             int64_t ldz, const void* labels, float* dlogits, int64_t ldd,
+             float* loss_out, void* ws, size_t ws_bytes, gcn_stream_t stream);
+
+/* ---------------------------------------- classifier backward (a7, a12)
+ * gcn_classifier_bwd - with dZ = dL/dlogits:
+ *   G_out  = (dZ W_cls^T) * [H > 0]      (dL/dH masked by the ReLU that
+ *                                         produced H; NULL to skip)
+ *   dW_cls = H^T dZ,  db_cls = 1^T dZ
+ *   W_cls -= lr dW_cls, b_cls -= lr db_cls   (after G_out has read W_cls)
+ *   dW_cls_out / db_cls_out: optional copies of the gradients (NULL ok)
+ * Deterministic: split sums are combined in a fixed order. */
+int gcn_classifier_bwd(int32_t n, int32_t K, int32_t C, const float* dZ,
+                       int64_t ldd, const float* H, int64_t ldh, float* W_cls,
+                       float* b_cls, float lr, float* G_out, int64_t ldg,
+                       float* dW_cls_out, float* db_cls_out, int32_t precision,
+                       void* ws, size_t ws_bytes, gcn_stream_t stream);
+
+/* ---------------------------------------- layer backward (a8-a12)
+ * gcn_layer_bwd - Eq. 2a-2c for one layer. G is this layer's masked output
+ * gradient, G = dL/dH_out * [H_out > 0] (n x 2h, self half first).
+ *   dW_self  = H_in^T G[:, :h]                       (Eq. 2a)
+ *   dW_neigh = AH^T  G[:, h:]                        (Eq. 2b)
+ *   db       = 1^T G                                 (when bias != NULL)
+ *   G_in     = ( G[:, :h] W_self^T + A D^-1 G[:, h:] W_neigh^T ) * [H_in > 0]
+ *              (Eq. 2c, masked by the ReLU that produced H_in; NULL for the
+ *              first layer, whose input has no gradient)
+ *   W -= lr dW for W_self, W_neigh (and bias), after G_in has read them.
+ *   H_in [n x F] ld ld_in; AH [n x F] ld ld_ah; G [n x 2h] ld ldg;
+ *   G_in [n x F] ld ldgi; dW*_out optional gradient copies (NULL ok).
+ */
+int gcn_layer_bwd(const gcn_dgraph* g, int32_t F, int32_t h, const float* G,
+                  int64_t ldg, const float* H_in, int64_t ld_in,
+                  const float* AH, int64_t ld_ah, float* W_self,
+                  float* W_neigh, float* bias, float lr, float* G_in,
+                  int64_t ldgi, float* dW_self_out, float* dW_neigh_out,
+                  float* db_out, int32_t precision, void* ws, size_t ws_bytes,
+                  gcn_stream_t stream);
+
+/* ---------------------------------------------- full step (a3-a12)
+ * gcn_train_step - forward through L layers (Eq. 1), classifier, loss,
+ * backward (Eq. 2a-2c) and the gradient-descent update of every weight, on
+ * one subgraph. Weights in `params` are updated in place.
+ *   X       device [n x f_in] ld desc->ld_x
+ *   labels  device, as for gcn_loss
+ *   loss_out device float[1]
+ *   grads   optional device buffers receiving every gradient (NULL, or
+ *           individual NULL members, to skip)
+ *   ws      >= gcn_workspace_bytes(); activations live at the offsets
+ *           reported by gcn_workspace_layout (valid after the step).
+ */
+typedef struct {
+    int32_t L, f_in, h, C;
+    int32_t loss;         /* GCN_LOSS_*  */
+    int32_t precision;    /* GCN_PREC_*  */
+    int32_t has_bias;     /* biases on every layer and the classifier */
+    int32_t reserved;
+    int64_t ld_x;
+} gcn_model_desc;
+
+typedef struct {          /* device pointers, row-major, ld == width */
+    float* W_self[GCN_MAX_LAYERS];    /* layer l: [F_l x h]          */
+    float* W_neigh[GCN_MAX_LAYERS];   /* layer l: [F_l x h]          */
+    float* b[GCN_MAX_LAYERS];         /* layer l: [2h] (has_bias)    */
+    float* W_cls;                     /* [2h x C]                    */
+    float* b_cls;                     /* [C] (has_bias)              */
+} gcn_params;
+
+typedef struct {          /* byte offsets into ws, -1 when absent */
+    int64_t AH[GCN_MAX_LAYERS];       /* [n x F_l], ld ld_AH[l]      */
+    int64_t H[GCN_MAX_LAYERS];        /* layer outputs [n x 2h]      */
+    int64_t ld_AH[GCN_MAX_LAYERS];
+    int64_t ld_H;
+    int64_t logits, dlogits, ld_C;    /* [n x C]                     */
+    int64_t G[GCN_MAX_LAYERS];        /* masked grads of layer outputs;
+                                         ping-pong, so only the last
+                                         two written stay valid      */
+    int64_t scratch, scratch_bytes, total_bytes;
+} gcn_ws_layout;
+
+int gcn_workspace_layout(const gcn_dgraph* g, const gcn_model_desc* desc,
+                         gcn_ws_layout* out);
+int gcn_workspace_bytes(const gcn_dgraph* g, const gcn_model_desc* desc,
+                        size_t* bytes);
+int gcn_train_step(const gcn_dgraph* g, const gcn_model_desc* desc,
+                   const gcn_params* params, const float* X,
+                   const void* labels, float lr, float* loss_out,
+                   const gcn_params* grads, void* ws, size_t ws_bytes,
+                   gcn_stream_t stream);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* GCN_ACT_H */

@@ -1,0 +1,317 @@
+// Feature aggregation on G_s^# (Section 4.2): pair sums round by round
+// (step 1), list sums (step 2) and the degree scaling (step 3, fused).
+//
+// Work decomposition (gfx950, 64-lane wavefronts): a group of GL lanes
+// (16, 32 or 64, chosen from the feature width) owns one pair or one list
+// segment and sweeps the feature row in float4 chunks, NCH chunks per lane,
+// so every neighbour-row gather is a coalesced run of GL*16 bytes. The
+// group loads up to GL neighbour ids at once (one per lane) and broadcasts
+// them lane by lane (readlane for a full wavefront, a width-GL shuffle
+// otherwise). Lists longer than the segment length are split on the host;
+// their segments write partial sums to scratch slots that a second pass adds
+// in slot order, so the result is deterministic and no row serialises a
+// whole wavefront for thousands of neighbours.
+#include "kernels.h"
+
+namespace gcn {
+namespace {
+
+constexpr int kBlock = 256;
+
+__device__ __forceinline__ const float* row_of(const RowSource& s, int c) {
+    return c < s.n ? s.X + (int64_t)c * s.ldx
+                   : s.aux + (int64_t)(c - s.n) * s.ldaux;
+}
+
+__device__ __forceinline__ float4 ld4(const float* p) {
+    return *reinterpret_cast<const float4*>(p);
+}
+
+__device__ __forceinline__ void st4(float* p, float4 v) {
+    *reinterpret_cast<float4*>(p) = v;
+}
+
+// stores the first `valid` elements of v (valid >= 1)
+__device__ __forceinline__ void st4_masked(float* p, float4 v, int valid) {
+    if (valid >= 4) {
+        st4(p, v);
+        return;
+    }
+    p[0] = v.x;
+    if (valid > 1) p[1] = v.y;
+    if (valid > 2) p[2] = v.z;
+}
+
+__device__ __forceinline__ void fma4(float4& acc, float s, float4 v) {
+    acc.x = fmaf(s, v.x, acc.x);
+    acc.y = fmaf(s, v.y, acc.y);
+    acc.z = fmaf(s, v.z, acc.z);
+    acc.w = fmaf(s, v.w, acc.w);
+}
+
+__device__ __forceinline__ void add4(float4& acc, float4 v) {
+    acc.x += v.x;
+    acc.y += v.y;
+    acc.z += v.z;
+    acc.w += v.w;
+}
+
+template <int GL>
+__device__ __forceinline__ int bcast_i(int v, int t) {
+    if constexpr (GL == 64) {
+        return __builtin_amdgcn_readlane(v, t);
+    } else {
+        return __shfl(v, t, GL);
+    }
+}
+
+template <int GL>
+__device__ __forceinline__ float bcast_f(float v, int t) {
+    return __int_as_float(bcast_i<GL>(__float_as_int(v), t));
+}
+
+// group index, made wave-uniform when the group is the whole wavefront
+template <int GL>
+__device__ __forceinline__ int group_index() {
+    int g = blockIdx.x * (kBlock / GL) + (int)threadIdx.x / GL;
+    if constexpr (GL == 64) g = __builtin_amdgcn_readfirstlane(g);
+    return g;
+}
+
+template <int GL, int NCH, bool PRE>
+__global__ __launch_bounds__(kBlock) void pair_sums_kernel(
+    const int32_t* __restrict__ pairs, int k0, int k1, RowSource src,
+    const float* __restrict__ inv_deg, float* __restrict__ aux,
+    int64_t ldaux, int F) {
+    const int lane = (int)threadIdx.x % GL;
+    const int k = k0 + group_index<GL>();
+    if (k >= k1) return;
+    const int p = pairs[2 * k], q = pairs[2 * k + 1];
+    const float* rp = row_of(src, p);
+    const float* rq = row_of(src, q);
+    float sp = 1.0f, sq = 1.0f;
+    if (PRE) {
+        if (p < src.n) sp = inv_deg[p];
+        if (q < src.n) sq = inv_deg[q];
+    }
+    float* out = aux + (int64_t)k * ldaux;
+    const int nf4 = (F + 3) >> 2;
+    for (int base = 0; base < nf4; base += GL * NCH) {
+#pragma unroll
+        for (int j = 0; j < NCH; ++j) {
+            const int c4 = base + lane + j * GL;
+            if (c4 < nf4) {
+                float4 a = ld4(rp + 4 * c4), b = ld4(rq + 4 * c4), v;
+                if (PRE) {
+                    v.x = fmaf(sp, a.x, sq * b.x);
+                    v.y = fmaf(sp, a.y, sq * b.y);
+                    v.z = fmaf(sp, a.z, sq * b.z);
+                    v.w = fmaf(sp, a.w, sq * b.w);
+                } else {
+                    v = make_float4(a.x + b.x, a.y + b.y, a.z + b.z, a.w + b.w);
+                }
+                st4(out + 4 * c4, v);   // scratch rows: padding may be written
+            }
+        }
+    }
+}
+
+// One group per segment (row, begin, end, slot) of the work list.
+template <int GL, int NCH, bool PRE, bool POST>
+__global__ __launch_bounds__(kBlock) void list_sums_kernel(
+    const int4* __restrict__ seg, int nseg, const int32_t* __restrict__ col,
+    RowSource src, const float* __restrict__ inv_deg, float* __restrict__ Y,
+    int64_t ldy, float* __restrict__ partial, int64_t ldp, int F) {
+    const int lane = (int)threadIdx.x % GL;
+    const int sidx = group_index<GL>();
+    if (sidx >= nseg) return;
+    const int4 sg = seg[sidx];
+    const int row = sg.x, b = sg.y, e = sg.z, slot = sg.w;
+    const int nf4 = (F + 3) >> 2;
+    for (int base = 0; base < nf4; base += GL * NCH) {
+        float4 acc[NCH];
+#pragma unroll
+        for (int j = 0; j < NCH; ++j) acc[j] = make_float4(0.f, 0.f, 0.f, 0.f);
+        for (int i0 = b; i0 < e; i0 += GL) {
+            const int cnt = min(GL, e - i0);
+            int my_c = 0;
+            float my_s = 1.0f;
+            if (lane < cnt) {
+                my_c = col[i0 + lane];
+                if (PRE && my_c < src.n) my_s = inv_deg[my_c];
+            }
+            int t = 0;
+            // four neighbours in flight per step
+            for (; t + 4 <= cnt; t += 4) {
+                const float* r[4];
+                float s[4];
+#pragma unroll
+                for (int u = 0; u < 4; ++u) {
+                    r[u] = row_of(src, bcast_i<GL>(my_c, t + u));
+                    s[u] = PRE ? bcast_f<GL>(my_s, t + u) : 1.0f;
+                }
+#pragma unroll
+                for (int j = 0; j < NCH; ++j) {
+                    const int c4 = base + lane + j * GL;
+                    if (c4 < nf4) {
+                        float4 v[4];
+#pragma unroll
+                        for (int u = 0; u < 4; ++u) v[u] = ld4(r[u] + 4 * c4);
+#pragma unroll
+                        for (int u = 0; u < 4; ++u) {
+                            if (PRE) fma4(acc[j], s[u], v[u]);
+                            else add4(acc[j], v[u]);
+                        }
+                    }
+                }
+            }
+            for (; t < cnt; ++t) {
+                const float* r = row_of(src, bcast_i<GL>(my_c, t));
+                const float s = PRE ? bcast_f<GL>(my_s, t) : 1.0f;
+#pragma unroll
+                for (int j = 0; j < NCH; ++j) {
+                    const int c4 = base + lane + j * GL;
+                    if (c4 < nf4) {
+                        float4 v = ld4(r + 4 * c4);
+                        if (PRE) fma4(acc[j], s, v);
+                        else add4(acc[j], v);
+                    }
+                }
+            }
+        }
+        if (slot < 0) {
+            const float sc = POST ? inv_deg[row] : 1.0f;
+            float* out = Y + (int64_t)row * ldy;
+#pragma unroll
+            for (int j = 0; j < NCH; ++j) {
+                const int c4 = base + lane + j * GL;
+                if (c4 < nf4) {
+                    float4 v = acc[j];
+                    if (POST) v = make_float4(v.x * sc, v.y * sc, v.z * sc, v.w * sc);
+                    st4_masked(out + 4 * c4, v, F - 4 * c4);
+                }
+            }
+        } else {
+            float* out = partial + (int64_t)slot * ldp;
+#pragma unroll
+            for (int j = 0; j < NCH; ++j) {
+                const int c4 = base + lane + j * GL;
+                if (c4 < nf4) st4(out + 4 * c4, acc[j]);
+            }
+        }
+    }
+}
+
+// One group per split list: add its slots in order, scale, store.
+template <int GL, int NCH, bool POST>
+__global__ __launch_bounds__(kBlock) void fixup_kernel(
+    const int4* __restrict__ longrows, int nlong,
+    const float* __restrict__ partial, int64_t ldp,
+    const float* __restrict__ inv_deg, float* __restrict__ Y, int64_t ldy,
+    int F) {
+    const int lane = (int)threadIdx.x % GL;
+    const int li = group_index<GL>();
+    if (li >= nlong) return;
+    const int4 lr = longrows[li];
+    const int row = lr.x, first = lr.y, ns = lr.z;
+    const int nf4 = (F + 3) >> 2;
+    const float sc = POST ? inv_deg[row] : 1.0f;
+    float* out = Y + (int64_t)row * ldy;
+    for (int base = 0; base < nf4; base += GL * NCH) {
+#pragma unroll
+        for (int j = 0; j < NCH; ++j) {
+            const int c4 = base + lane + j * GL;
+            if (c4 < nf4) {
+                float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+                for (int sI = 0; sI < ns; ++sI)
+                    add4(acc, ld4(partial + (int64_t)(first + sI) * ldp + 4 * c4));
+                if (POST) acc = make_float4(acc.x * sc, acc.y * sc, acc.z * sc, acc.w * sc);
+                st4_masked(out + 4 * c4, acc, F - 4 * c4);
+            }
+        }
+    }
+}
+
+struct Shape {
+    int gl, nch;
+};
+
+Shape pick_shape(int F) {
+    const int nf4 = (F + 3) / 4;
+    if (nf4 <= 16) return {16, 1};
+    if (nf4 <= 32) return {32, 1};
+    if (nf4 <= 64) return {64, 1};
+    if (nf4 <= 128) return {64, 2};
+    if (nf4 <= 192) return {64, 3};
+    return {64, 4};
+}
+
+int blocks_for(int groups, int gl) {
+    const int per = kBlock / gl;
+    return (groups + per - 1) / per;
+}
+
+#define GCN_SHAPES(X) \
+    X(16, 1) X(32, 1) X(64, 1) X(64, 2) X(64, 3) X(64, 4)
+
+}  // namespace
+
+hipError_t launch_pair_sums(const int32_t* pairs, int32_t k0, int32_t k1,
+                            RowSource src, const float* inv_deg, bool prescale,
+                            float* aux, int64_t ldaux, int32_t F,
+                            hipStream_t s) {
+    if (k1 <= k0 || F <= 0) return hipSuccess;
+    const Shape sh = pick_shape(F);
+    const dim3 grid(blocks_for(k1 - k0, sh.gl)), block(kBlock);
+#define GCN_LAUNCH_PAIR(GL_, NCH_)                                                  \
+    if (sh.gl == GL_ && sh.nch == NCH_) {                                           \
+        if (prescale)                                                               \
+            pair_sums_kernel<GL_, NCH_, true><<<grid, block, 0, s>>>(               \
+                pairs, k0, k1, src, inv_deg, aux, ldaux, F);                        \
+        else                                                                        \
+            pair_sums_kernel<GL_, NCH_, false><<<grid, block, 0, s>>>(              \
+                pairs, k0, k1, src, inv_deg, aux, ldaux, F);                        \
+        return hipGetLastError();                                                   \
+    }
+    GCN_SHAPES(GCN_LAUNCH_PAIR)
+#undef GCN_LAUNCH_PAIR
+    return hipErrorInvalidValue;
+}
+
+hipError_t launch_list_sums(const gcn_dgraph* g, RowSource src, bool prescale,
+                            bool postscale, float* Y, int64_t ldy,
+                            float* partial, int64_t ldp, int32_t F,
+                            hipStream_t s) {
+    if (g->n <= 0 || F <= 0) return hipSuccess;
+    const Shape sh = pick_shape(F);
+    const int4* seg = reinterpret_cast<const int4*>(g->seg);
+    const int4* lr = reinterpret_cast<const int4*>(g->longrows);
+    const dim3 block(kBlock);
+    const dim3 grid(blocks_for(g->nseg, sh.gl));
+    const dim3 gfix(blocks_for(g->nlong, sh.gl));
+#define GCN_LAUNCH_LIST(GL_, NCH_)                                                    \
+    if (sh.gl == GL_ && sh.nch == NCH_) {                                             \
+        if (prescale && !postscale)                                                   \
+            list_sums_kernel<GL_, NCH_, true, false><<<grid, block, 0, s>>>(          \
+                seg, g->nseg, g->col, src, g->inv_deg, Y, ldy, partial, ldp, F);      \
+        else if (!prescale && postscale)                                              \
+            list_sums_kernel<GL_, NCH_, false, true><<<grid, block, 0, s>>>(          \
+                seg, g->nseg, g->col, src, g->inv_deg, Y, ldy, partial, ldp, F);      \
+        else                                                                          \
+            return hipErrorInvalidValue;                                              \
+        hipError_t e = hipGetLastError();                                             \
+        if (e != hipSuccess || g->nlong == 0) return e;                               \
+        if (postscale)                                                                \
+            fixup_kernel<GL_, NCH_, true><<<gfix, block, 0, s>>>(                     \
+                lr, g->nlong, partial, ldp, g->inv_deg, Y, ldy, F);                   \
+        else                                                                          \
+            fixup_kernel<GL_, NCH_, false><<<gfix, block, 0, s>>>(                    \
+                lr, g->nlong, partial, ldp, g->inv_deg, Y, ldy, F);                   \
+        return hipGetLastError();                                                     \
+    }
+    GCN_SHAPES(GCN_LAUNCH_LIST)
+#undef GCN_LAUNCH_LIST
+    return hipErrorInvalidValue;
+}
+
+}  // namespace gcn

@@ -1,0 +1,637 @@
+// Device entry points of gcn_act.h: argument validation, scratch planning
+// and the composition of aggregation, GEMMs, loss and update into layer and
+// training-step calls. Every check runs before the first launch.
+#include <algorithm>
+#include <cstring>
+
+#include "kernels.h"
+
+using namespace gcn;
+
+namespace {
+
+constexpr int64_t kAlign = 256;
+
+inline int64_t r4(int64_t x) { return round_up(x, 4); }
+
+// Scratch regions (bytes from the start of ws) for widths up to W.
+struct ScratchPlan {
+    int64_t aux, part_list, T, gemm_part, rowloss, total;
+    int64_t gemm_part_floats;   // per problem
+};
+
+int64_t gemm_part_bound(int64_t W) {
+    // split factor * tiles <= 512 + tiles, each tile 128 x 128 floats
+    const int64_t tiles = ((W + 1 + 127) / 128) * ((W + 127) / 128);
+    return (512 + tiles) * 128 * 128;
+}
+
+ScratchPlan plan_scratch(int64_t n, int64_t naux, int64_t nslots, int64_t W) {
+    ScratchPlan p{};
+    const int64_t ldW = r4(std::max<int64_t>(W, 1));
+    int64_t off = 0;
+    auto take = [&](int64_t bytes) {
+        int64_t o = off;
+        off = round_up(off + std::max<int64_t>(bytes, 1), kAlign);
+        return o;
+    };
+    p.aux = take(4 * naux * ldW);
+    p.part_list = take(4 * nslots * ldW);
+    p.T = take(4 * n * ldW);
+    p.gemm_part_floats = gemm_part_bound(W);
+    p.gemm_part = take(4 * 2 * p.gemm_part_floats);
+    p.rowloss = take(4 * std::max<int64_t>(n, 1));
+    p.total = off;
+    return p;
+}
+
+int hip_fail(hipError_t e, const char* where) {
+    set_error("%s: HIP error %d (%s)", where, (int)e, hipGetErrorString(e));
+    return GCN_E_HIP;
+}
+
+#define GCN_HIP(call, where)                          \
+    do {                                              \
+        hipError_t e_ = (call);                       \
+        if (e_ != hipSuccess) return hip_fail(e_, where); \
+    } while (0)
+
+// Dense matrix argument check: rows x width, leading dimension ld.
+int check_mat(const char* fn, const char* name, const void* p, int64_t rows,
+              int64_t width, int64_t ld) {
+    if (rows <= 0 || width <= 0) return GCN_OK;
+    GCN_CHECK_ARG(p != nullptr, "%s: %s is NULL", fn, name);
+    GCN_CHECK_ARG(((uintptr_t)p & 15) == 0, "%s: %s not 16-byte aligned", fn, name);
+    GCN_CHECK_ARG(ld >= width, "%s: ld of %s (%lld) < width %lld", fn, name,
+                  (long long)ld, (long long)width);
+    GCN_CHECK_ARG(ld % 4 == 0, "%s: ld of %s (%lld) not a multiple of 4", fn,
+                  name, (long long)ld);
+    return GCN_OK;
+}
+
+int check_vec(const char* fn, const char* name, const void* p, int64_t len) {
+    if (len <= 0) return GCN_OK;
+    GCN_CHECK_ARG(p != nullptr, "%s: %s is NULL", fn, name);
+    GCN_CHECK_ARG(((uintptr_t)p & 3) == 0, "%s: %s not 4-byte aligned", fn, name);
+    return GCN_OK;
+}
+
+int check_graph(const char* fn, const gcn_dgraph* g) {
+    GCN_CHECK_ARG(g != nullptr, "%s: graph descriptor is NULL", fn);
+    GCN_CHECK_ARG(g->n >= 0 && g->naux >= 0 && g->rounds >= 0 &&
+                      g->rounds <= GCN_MAX_ROUNDS && g->nseg >= 0 &&
+                      g->nlong >= 0 && g->nslots >= 0,
+                  "%s: malformed graph descriptor", fn);
+    GCN_CHECK_ARG(g->round_offsets[0] == 0 && g->round_offsets[g->rounds] == g->naux,
+                  "%s: graph descriptor round offsets inconsistent", fn);
+    GCN_CHECK_ARG(g->n == 0 || (g->rowptr && g->inv_deg && g->seg),
+                  "%s: graph descriptor has NULL arrays", fn);
+    return GCN_OK;
+}
+
+int check_ws(const char* fn, const void* ws, size_t ws_bytes, int64_t need) {
+    GCN_CHECK_ARG(ws != nullptr || need == 0, "%s: workspace is NULL", fn);
+    GCN_CHECK_ARG(((uintptr_t)ws % kAlign) == 0, "%s: workspace not 256-byte aligned", fn);
+    if ((int64_t)ws_bytes < need) {
+        set_error("%s: workspace of %zu bytes, need %lld", fn, ws_bytes, (long long)need);
+        return GCN_E_WORKSPACE;
+    }
+    return GCN_OK;
+}
+
+int check_precision(const char* fn, int32_t precision) {
+    GCN_CHECK_ARG(precision == GCN_PREC_FP32 || precision == GCN_PREC_BF16,
+                  "%s: unknown precision %d", fn, precision);
+    if (precision != GCN_PREC_FP32) {
+        set_error("%s: bf16 MFMA path not built", fn);
+        return GCN_E_UNSUPPORTED;
+    }
+    return GCN_OK;
+}
+
+#define GCN_TRY(x)                \
+    do {                          \
+        int rc_ = (x);            \
+        if (rc_ != GCN_OK) return rc_; \
+    } while (0)
+
+float* fptr(void* ws, int64_t off) {
+    return reinterpret_cast<float*>(static_cast<char*>(ws) + off);
+}
+
+// ------------------------------------------------------------ internals
+// (arguments already validated)
+
+int do_aggregate(const char* fn, const gcn_dgraph* g, bool transposed, int32_t F,
+                 const float* X, int64_t ldx, float* Y, int64_t ldy,
+                 const ScratchPlan& sp, void* ws, hipStream_t s) {
+    const int64_t ldaux = r4(F);
+    float* aux = fptr(ws, sp.aux);
+    float* part = fptr(ws, sp.part_list);
+    RowSource src{X, ldx, aux, ldaux, g->n};
+    for (int r = 0; r < g->rounds; ++r)
+        GCN_HIP(launch_pair_sums(g->pairs, g->round_offsets[r], g->round_offsets[r + 1],
+                                 src, g->inv_deg, transposed, aux, ldaux, F, s),
+                fn);
+    GCN_HIP(launch_list_sums(g, src, transposed, !transposed, Y, ldy, part, ldaux, F, s), fn);
+    return GCN_OK;
+}
+
+GemmProblem gp_zero() {
+    GemmProblem p;
+    std::memset(&p, 0, sizeof(p));
+    p.splits = 1;
+    return p;
+}
+
+int do_layer_fwd(const char* fn, const gcn_dgraph* g, int32_t F, int32_t h,
+                 const float* H_in, int64_t ld_in, const float* Ws,
+                 const float* Wn, const float* bias, float* AH, int64_t ld_ah,
+                 float* H_out, int64_t ld_out, const ScratchPlan& sp, void* ws,
+                 hipStream_t s) {
+    GCN_TRY(do_aggregate(fn, g, false, F, H_in, ld_in, AH, ld_ah, sp, ws, s));
+    GemmBatch b;
+    std::memset(&b, 0, sizeof(b));
+    b.nprob = 2;
+    for (int i = 0; i < 2; ++i) {
+        GemmProblem p = gp_zero();
+        p.M = g->n;
+        p.N = h;
+        p.K = F;
+        p.A0 = p.A1 = i == 0 ? H_in : AH;
+        p.lda0 = p.lda1 = i == 0 ? ld_in : ld_ah;
+        p.ksplitA = F;
+        p.B0 = p.B1 = i == 0 ? Ws : Wn;
+        p.ldb0 = p.ldb1 = h;
+        p.ksplitB = F;
+        p.C = H_out + (i == 0 ? 0 : h);
+        p.ldc = ld_out;
+        p.bias = bias ? bias + (i == 0 ? 0 : h) : nullptr;
+        b.p[i] = p;
+    }
+    GCN_HIP(launch_gemm(b, A_MK, B_KN, EPI_BIAS_RELU, s), fn);
+    return GCN_OK;
+}
+
+int do_classifier_fwd(const char* fn, int32_t n, int32_t K, int32_t C,
+                      const float* H, int64_t ldh, const float* Wc,
+                      const float* bc, float* Z, int64_t ldz, hipStream_t s) {
+    GemmBatch b;
+    std::memset(&b, 0, sizeof(b));
+    b.nprob = 1;
+    GemmProblem p = gp_zero();
+    p.M = n;
+    p.N = C;
+    p.K = K;
+    p.A0 = p.A1 = H;
+    p.lda0 = p.lda1 = ldh;
+    p.ksplitA = K;
+    p.B0 = p.B1 = Wc;
+    p.ldb0 = p.ldb1 = C;
+    p.ksplitB = K;
+    p.C = Z;
+    p.ldc = ldz;
+    p.bias = bc;
+    b.p[0] = p;
+    GCN_HIP(launch_gemm(b, A_MK, B_KN, EPI_BIAS, s), fn);
+    return GCN_OK;
+}
+
+// dW = A^T B over K = n rows with split-K slices in scratch slot `which`.
+GemmProblem dw_problem(int32_t n, int32_t Mw, bool ones, int32_t N,
+                       const float* A, int64_t lda, const float* B, int64_t ldb,
+                       float* part) {
+    GemmProblem p = gp_zero();
+    p.M = Mw + (ones ? 1 : 0);
+    p.N = N;
+    p.K = n;
+    p.A0 = p.A1 = A;
+    p.lda0 = p.lda1 = lda;
+    p.ones_row = ones ? 1 : 0;
+    p.B0 = p.B1 = B;
+    p.ldb0 = p.ldb1 = ldb;
+    gemm_split_plan(p.M, p.N, p.K, &p.splits, &p.kchunk);
+    p.C = part;
+    p.ldc = r4(N);
+    p.part_stride = (int64_t)p.M * p.ldc;
+    return p;
+}
+
+SgdProblem sgd_problem(const GemmProblem& gpb, int32_t Mw, int32_t N, float* W,
+                       float* b, float* dW_out, float* db_out) {
+    SgdProblem q;
+    q.part = gpb.C;
+    q.part_stride = gpb.part_stride;
+    q.ldp = gpb.ldc;
+    q.splits = gpb.splits;
+    q.Mw = Mw;
+    q.N = N;
+    q.W = W;
+    q.b = b;
+    q.dW_out = dW_out;
+    q.db_out = db_out;
+    return q;
+}
+
+int do_classifier_bwd(const char* fn, int32_t n, int32_t K, int32_t C,
+                      const float* dZ, int64_t ldd, const float* H, int64_t ldh,
+                      float* Wc, float* bc, float lr, float* G_out, int64_t ldg,
+                      float* dWc_out, float* dbc_out, const ScratchPlan& sp,
+                      void* ws, hipStream_t s) {
+    if (G_out) {
+        GemmBatch b;
+        std::memset(&b, 0, sizeof(b));
+        b.nprob = 1;
+        GemmProblem p = gp_zero();
+        p.M = n;
+        p.N = K;
+        p.K = C;
+        p.A0 = p.A1 = dZ;
+        p.lda0 = p.lda1 = ldd;
+        p.ksplitA = C;
+        p.B0 = p.B1 = Wc;       // B(k=c, n=j) = W_cls[j][c]
+        p.ldb0 = p.ldb1 = C;
+        p.ksplitB = C;
+        p.mask = H;
+        p.ldmask = ldh;
+        p.C = G_out;
+        p.ldc = ldg;
+        b.p[0] = p;
+        GCN_HIP(launch_gemm(b, A_MK, B_NK, EPI_MASK, s), fn);
+    }
+    GemmBatch b;
+    std::memset(&b, 0, sizeof(b));
+    b.nprob = 1;
+    b.p[0] = dw_problem(n, K, bc != nullptr, C, H, ldh, dZ, ldd, fptr(ws, sp.gemm_part));
+    GCN_HIP(launch_gemm(b, A_KM, B_KN, EPI_PARTIAL, s), fn);
+    SgdProblem q = sgd_problem(b.p[0], K, C, Wc, bc, dWc_out, dbc_out);
+    GCN_HIP(launch_sgd_reduce(&q, 1, lr, s), fn);
+    return GCN_OK;
+}
+
+int do_layer_bwd(const char* fn, const gcn_dgraph* g, int32_t F, int32_t h,
+                 const float* G, int64_t ldg, const float* H_in, int64_t ld_in,
+                 const float* AH, int64_t ld_ah, float* Ws, float* Wn,
+                 float* bias, float lr, float* G_in, int64_t ldgi,
+                 float* dWs_out, float* dWn_out, float* db_out,
+                 const ScratchPlan& sp, void* ws, hipStream_t s) {
+    const int32_t n = g->n;
+    if (G_in) {
+        // T = A D^-1 G[:, h:]  (Eq. 2c), then G_in = [G_self | T] [W_self; W_neigh]^T
+        float* T = fptr(ws, sp.T);
+        const int64_t ldt = r4(h);
+        GCN_TRY(do_aggregate(fn, g, true, h, G + h, ldg, T, ldt, sp, ws, s));
+        GemmBatch b;
+        std::memset(&b, 0, sizeof(b));
+        b.nprob = 1;
+        GemmProblem p = gp_zero();
+        p.M = n;
+        p.N = F;
+        p.K = 2 * h;
+        p.A0 = G;
+        p.lda0 = ldg;
+        p.A1 = T;
+        p.lda1 = ldt;
+        p.ksplitA = h;
+        p.B0 = Ws;
+        p.ldb0 = h;
+        p.B1 = Wn;
+        p.ldb1 = h;
+        p.ksplitB = h;
+        p.mask = H_in;
+        p.ldmask = ld_in;
+        p.C = G_in;
+        p.ldc = ldgi;
+        b.p[0] = p;
+        GCN_HIP(launch_gemm(b, A_MK, B_NK, EPI_MASK, s), fn);
+    }
+    GemmBatch b;
+    std::memset(&b, 0, sizeof(b));
+    b.nprob = 2;
+    float* part0 = fptr(ws, sp.gemm_part);
+    float* part1 = part0 + sp.gemm_part_floats;
+    const bool ones = bias != nullptr;
+    b.p[0] = dw_problem(n, F, ones, h, H_in, ld_in, G, ldg, part0);
+    b.p[1] = dw_problem(n, F, ones, h, AH, ld_ah, G + h, ldg, part1);
+    GCN_HIP(launch_gemm(b, A_KM, B_KN, EPI_PARTIAL, s), fn);
+    SgdProblem q[2] = {
+        sgd_problem(b.p[0], F, h, Ws, bias, dWs_out, db_out),
+        sgd_problem(b.p[1], F, h, Wn, bias ? bias + h : nullptr, dWn_out,
+                    db_out ? db_out + h : nullptr)};
+    GCN_HIP(launch_sgd_reduce(q, 2, lr, s), fn);
+    return GCN_OK;
+}
+
+struct StepLayout {
+    gcn_ws_layout pub;
+    ScratchPlan sp;
+};
+
+int plan_step(const gcn_dgraph* g, const gcn_model_desc* d, StepLayout* out) {
+    const int64_t n = g->n;
+    std::memset(&out->pub, 0, sizeof(out->pub));
+    for (int i = 0; i < GCN_MAX_LAYERS; ++i)
+        out->pub.AH[i] = out->pub.H[i] = out->pub.G[i] = out->pub.ld_AH[i] = -1;
+    int64_t off = 0;
+    auto take = [&](int64_t bytes) {
+        int64_t o = off;
+        off = round_up(off + std::max<int64_t>(bytes, 1), kAlign);
+        return o;
+    };
+    const int64_t ldH = r4(2 * (int64_t)d->h);
+    const int64_t ldC = r4(d->C);
+    for (int l = 0; l < d->L; ++l) {
+        const int64_t F = l == 0 ? d->f_in : 2 * (int64_t)d->h;
+        out->pub.ld_AH[l] = r4(F);
+        out->pub.AH[l] = take(4 * n * r4(F));
+        out->pub.H[l] = take(4 * n * ldH);
+    }
+    out->pub.ld_H = ldH;
+    out->pub.logits = take(4 * n * ldC);
+    out->pub.dlogits = take(4 * n * ldC);
+    out->pub.ld_C = ldC;
+    const int64_t g0 = take(4 * n * ldH), g1 = take(4 * n * ldH);
+    // G[l] is the masked gradient of layer l's output; layers alternate
+    for (int l = 0; l < d->L; ++l) out->pub.G[l] = ((d->L - 1 - l) % 2 == 0) ? g0 : g1;
+    const int64_t W = std::max<int64_t>({(int64_t)d->f_in, 2 * (int64_t)d->h, (int64_t)d->C});
+    out->sp = plan_scratch(n, g->naux, g->nslots, W);
+    out->pub.scratch = off;
+    out->pub.scratch_bytes = out->sp.total;
+    out->pub.total_bytes = off + out->sp.total;
+    return GCN_OK;
+}
+
+int check_desc(const char* fn, const gcn_model_desc* d) {
+    GCN_CHECK_ARG(d != nullptr, "%s: model descriptor is NULL", fn);
+    GCN_CHECK_ARG(d->L >= 1 && d->L <= GCN_MAX_LAYERS, "%s: L=%d outside [1, %d]",
+                  fn, d->L, GCN_MAX_LAYERS);
+    GCN_CHECK_ARG(d->f_in >= 1, "%s: f_in < 1", fn);
+    GCN_CHECK_ARG(d->h >= 4 && d->h % 4 == 0, "%s: h=%d must be a positive multiple of 4", fn, d->h);
+    GCN_CHECK_ARG(d->C >= 1, "%s: C < 1", fn);
+    GCN_CHECK_ARG(d->loss == GCN_LOSS_SOFTMAX_CE || d->loss == GCN_LOSS_SIGMOID_BCE,
+                  "%s: unknown loss %d", fn, d->loss);
+    GCN_CHECK_ARG(d->ld_x >= d->f_in && d->ld_x % 4 == 0,
+                  "%s: ld_x=%lld must be >= f_in and a multiple of 4", fn, (long long)d->ld_x);
+    return check_precision(fn, d->precision);
+}
+
+}  // namespace
+
+extern "C" {
+
+int gcn_graph_upload(const void* host_image, size_t bytes, void* dev_buf,
+                     gcn_dgraph* out, gcn_stream_t stream) {
+    gcn_dgraph tmp;
+    int rc = gcn_graph_describe(host_image, bytes, dev_buf, &tmp);
+    if (rc) return rc;
+    ImageHeader h;
+    std::memcpy(&h, host_image, sizeof(h));
+    GCN_HIP(hipMemcpyAsync(dev_buf, host_image, (size_t)h.total, hipMemcpyHostToDevice,
+                           (hipStream_t)stream),
+            "gcn_graph_upload");
+    *out = tmp;
+    return GCN_OK;
+}
+
+int gcn_scratch_bytes(const gcn_dgraph* g, int32_t n, int32_t max_width, size_t* bytes) {
+    GCN_CHECK_ARG(bytes != nullptr, "gcn_scratch_bytes: bytes is NULL");
+    GCN_CHECK_ARG(max_width >= 1, "gcn_scratch_bytes: max_width < 1");
+    if (g) GCN_TRY(check_graph("gcn_scratch_bytes", g));
+    const ScratchPlan sp = g ? plan_scratch(g->n, g->naux, g->nslots, max_width)
+                             : plan_scratch(std::max(n, 0), 0, 0, max_width);
+    *bytes = (size_t)sp.total;
+    return GCN_OK;
+}
+
+int gcn_aggregate(const gcn_dgraph* g, int32_t mode, int32_t F, const float* X,
+                  int64_t ldx, float* Y, int64_t ldy, void* ws, size_t ws_bytes,
+                  gcn_stream_t stream) {
+    const char* fn = "gcn_aggregate";
+    GCN_TRY(check_graph(fn, g));
+    GCN_CHECK_ARG(mode == GCN_AGG_MEAN || mode == GCN_AGG_TRANSPOSED, "%s: unknown mode", fn);
+    GCN_CHECK_ARG(F >= 1, "%s: F < 1", fn);
+    GCN_TRY(check_mat(fn, "X", X, g->n, F, ldx));
+    GCN_TRY(check_mat(fn, "Y", Y, g->n, F, ldy));
+    GCN_CHECK_ARG(g->n == 0 || X != Y, "%s: X and Y must not overlap", fn);
+    const ScratchPlan sp = plan_scratch(g->n, g->naux, g->nslots, F);
+    GCN_TRY(check_ws(fn, ws, ws_bytes, sp.total));
+    return do_aggregate(fn, g, mode == GCN_AGG_TRANSPOSED, F, X, ldx, Y, ldy, sp, ws,
+                        (hipStream_t)stream);
+}
+
+int gcn_layer_fwd(const gcn_dgraph* g, int32_t F, int32_t h, const float* H_in,
+                  int64_t ld_in, const float* W_self, const float* W_neigh,
+                  const float* bias, float* AH, int64_t ld_ah, float* H_out,
+                  int64_t ld_out, int32_t precision, void* ws, size_t ws_bytes,
+                  gcn_stream_t stream) {
+    const char* fn = "gcn_layer_fwd";
+    GCN_TRY(check_graph(fn, g));
+    GCN_CHECK_ARG(F >= 1, "%s: F < 1", fn);
+    GCN_CHECK_ARG(h >= 4 && h % 4 == 0, "%s: h=%d must be a positive multiple of 4", fn, h);
+    GCN_TRY(check_precision(fn, precision));
+    const int64_t n = g->n;
+    GCN_TRY(check_mat(fn, "H_in", H_in, n, F, ld_in));
+    GCN_TRY(check_mat(fn, "AH", AH, n, F, ld_ah));
+    GCN_TRY(check_mat(fn, "H_out", H_out, n, 2 * (int64_t)h, ld_out));
+    GCN_TRY(check_mat(fn, "W_self", W_self, F, h, h));
+    GCN_TRY(check_mat(fn, "W_neigh", W_neigh, F, h, h));
+    if (bias) GCN_TRY(check_vec(fn, "bias", bias, 2 * (int64_t)h));
+    const ScratchPlan sp = plan_scratch(n, g->naux, g->nslots, std::max(F, 2 * h));
+    GCN_TRY(check_ws(fn, ws, ws_bytes, sp.total));
+    return do_layer_fwd(fn, g, F, h, H_in, ld_in, W_self, W_neigh, bias, AH, ld_ah,
+                        H_out, ld_out, sp, ws, (hipStream_t)stream);
+}
+
+int gcn_classifier_fwd(int32_t n, int32_t K, int32_t C, const float* H, int64_t ldh,
+                       const float* W_cls, const float* b_cls, float* logits,
+                       int64_t ldz, int32_t precision, gcn_stream_t stream) {
+    const char* fn = "gcn_classifier_fwd";
+    GCN_CHECK_ARG(n >= 0 && K >= 1 && C >= 1, "%s: bad sizes", fn);
+    GCN_TRY(check_precision(fn, precision));
+    GCN_TRY(check_mat(fn, "H", H, n, K, ldh));
+    GCN_TRY(check_vec(fn, "W_cls", W_cls, (int64_t)K * C));
+    if (b_cls) GCN_TRY(check_vec(fn, "b_cls", b_cls, C));
+    GCN_TRY(check_mat(fn, "logits", logits, n, C, ldz));
+    return do_classifier_fwd(fn, n, K, C, H, ldh, W_cls, b_cls, logits, ldz,
+                             (hipStream_t)stream);
+}
+
+int gcn_loss(int32_t n, int32_t C, int32_t kind, const float* logits, int64_t ldz,
+             const void* labels, float* dlogits, int64_t ldd, float* loss_out, void* ws,
+             size_t ws_bytes, gcn_stream_t stream) {
+    const char* fn = "gcn_loss";
+    GCN_CHECK_ARG(n >= 0 && C >= 1, "%s: bad sizes", fn);
+    GCN_CHECK_ARG(kind == GCN_LOSS_SOFTMAX_CE || kind == GCN_LOSS_SIGMOID_BCE,
+                  "%s: unknown loss %d", fn, kind);
+    GCN_TRY(check_mat(fn, "logits", logits, n, C, ldz));
+    GCN_TRY(check_mat(fn, "dlogits", dlogits, n, C, ldd));
+    GCN_CHECK_ARG(n == 0 || labels != nullptr, "%s: labels is NULL", fn);
+    GCN_CHECK_ARG(kind != GCN_LOSS_SOFTMAX_CE || ((uintptr_t)labels & 3) == 0,
+                  "%s: int32 labels not 4-byte aligned", fn);
+    GCN_CHECK_ARG(logits != dlogits || ldz == ldd, "%s: in-place loss needs ldz == ldd", fn);
+    GCN_TRY(check_vec(fn, "loss_out", loss_out, 1));
+    const ScratchPlan sp = plan_scratch(n, 0, 0, C);
+    GCN_TRY(check_ws(fn, ws, ws_bytes, sp.total));
+    GCN_HIP(launch_loss(n, C, kind, logits, ldz, labels, dlogits, ldd, fptr(ws, sp.rowloss),
+                        loss_out, (hipStream_t)stream),
+            fn);
+    return GCN_OK;
+}
+
+int gcn_classifier_bwd(int32_t n, int32_t K, int32_t C, const float* dZ, int64_t ldd,
+                       const float* H, int64_t ldh, float* W_cls, float* b_cls, float lr,
+                       float* G_out, int64_t ldg, float* dW_cls_out, float* db_cls_out,
+                       int32_t precision, void* ws, size_t ws_bytes, gcn_stream_t stream) {
+    const char* fn = "gcn_classifier_bwd";
+    GCN_CHECK_ARG(n >= 0 && K >= 1 && C >= 1, "%s: bad sizes", fn);
+    GCN_TRY(check_precision(fn, precision));
+    GCN_TRY(check_mat(fn, "dZ", dZ, n, C, ldd));
+    GCN_TRY(check_mat(fn, "H", H, n, K, ldh));
+    GCN_TRY(check_vec(fn, "W_cls", W_cls, (int64_t)K * C));
+    if (b_cls) GCN_TRY(check_vec(fn, "b_cls", b_cls, C));
+    if (G_out) GCN_TRY(check_mat(fn, "G_out", G_out, n, K, ldg));
+    if (dW_cls_out) GCN_TRY(check_vec(fn, "dW_cls_out", dW_cls_out, (int64_t)K * C));
+    if (db_cls_out) GCN_TRY(check_vec(fn, "db_cls_out", db_cls_out, C));
+    const ScratchPlan sp = plan_scratch(n, 0, 0, std::max(K, C));
+    GCN_TRY(check_ws(fn, ws, ws_bytes, sp.total));
+    return do_classifier_bwd(fn, n, K, C, dZ, ldd, H, ldh, W_cls, b_cls, lr, G_out, ldg,
+                             dW_cls_out, db_cls_out, sp, ws, (hipStream_t)stream);
+}
+
+int gcn_layer_bwd(const gcn_dgraph* g, int32_t F, int32_t h, const float* G, int64_t ldg,
+                  const float* H_in, int64_t ld_in, const float* AH, int64_t ld_ah,
+                  float* W_self, float* W_neigh, float* bias, float lr, float* G_in,
+                  int64_t ldgi, float* dW_self_out, float* dW_neigh_out, float* db_out,
+                  int32_t precision, void* ws, size_t ws_bytes, gcn_stream_t stream) {
+    const char* fn = "gcn_layer_bwd";
+    GCN_TRY(check_graph(fn, g));
+    GCN_CHECK_ARG(F >= 1, "%s: F < 1", fn);
+    GCN_CHECK_ARG(h >= 4 && h % 4 == 0, "%s: h=%d must be a positive multiple of 4", fn, h);
+    GCN_TRY(check_precision(fn, precision));
+    const int64_t n = g->n;
+    GCN_TRY(check_mat(fn, "G", G, n, 2 * (int64_t)h, ldg));
+    GCN_TRY(check_mat(fn, "H_in", H_in, n, F, ld_in));
+    GCN_TRY(check_mat(fn, "AH", AH, n, F, ld_ah));
+    GCN_TRY(check_mat(fn, "W_self", W_self, F, h, h));
+    GCN_TRY(check_mat(fn, "W_neigh", W_neigh, F, h, h));
+    if (bias) GCN_TRY(check_vec(fn, "bias", bias, 2 * (int64_t)h));
+    if (G_in) GCN_TRY(check_mat(fn, "G_in", G_in, n, F, ldgi));
+    if (dW_self_out) GCN_TRY(check_vec(fn, "dW_self_out", dW_self_out, (int64_t)F * h));
+    if (dW_neigh_out) GCN_TRY(check_vec(fn, "dW_neigh_out", dW_neigh_out, (int64_t)F * h));
+    if (db_out) GCN_TRY(check_vec(fn, "db_out", db_out, 2 * (int64_t)h));
+    GCN_CHECK_ARG(db_out == nullptr || bias != nullptr, "%s: db_out without bias", fn);
+    const ScratchPlan sp = plan_scratch(n, g->naux, g->nslots, std::max(F, 2 * h));
+    GCN_TRY(check_ws(fn, ws, ws_bytes, sp.total));
+    return do_layer_bwd(fn, g, F, h, G, ldg, H_in, ld_in, AH, ld_ah, W_self, W_neigh, bias,
+                        lr, G_in, ldgi, dW_self_out, dW_neigh_out, db_out, sp, ws,
+                        (hipStream_t)stream);
+}
+
+int gcn_workspace_layout(const gcn_dgraph* g, const gcn_model_desc* desc,
+                         gcn_ws_layout* out) {
+    const char* fn = "gcn_workspace_layout";
+    GCN_TRY(check_graph(fn, g));
+    GCN_TRY(check_desc(fn, desc));
+    GCN_CHECK_ARG(out != nullptr, "%s: out is NULL", fn);
+    StepLayout sl;
+    GCN_TRY(plan_step(g, desc, &sl));
+    *out = sl.pub;
+    return GCN_OK;
+}
+
+int gcn_workspace_bytes(const gcn_dgraph* g, const gcn_model_desc* desc, size_t* bytes) {
+    gcn_ws_layout l;
+    GCN_TRY(gcn_workspace_layout(g, desc, &l));
+    GCN_CHECK_ARG(bytes != nullptr, "gcn_workspace_bytes: bytes is NULL");
+    *bytes = (size_t)l.total_bytes;
+    return GCN_OK;
+}
+
+int gcn_train_step(const gcn_dgraph* g, const gcn_model_desc* d, const gcn_params* P,
+                   const float* X, const void* labels, float lr, float* loss_out,
+                   const gcn_params* grads, void* ws, size_t ws_bytes,
+                   gcn_stream_t stream) {
+    const char* fn = "gcn_train_step";
+    GCN_TRY(check_graph(fn, g));
+    GCN_TRY(check_desc(fn, d));
+    GCN_CHECK_ARG(P != nullptr, "%s: params is NULL", fn);
+    const int64_t n = g->n;
+    const int32_t h = d->h, C = d->C, L = d->L;
+    GCN_TRY(check_mat(fn, "X", X, n, d->f_in, d->ld_x));
+    GCN_CHECK_ARG(n == 0 || labels != nullptr, "%s: labels is NULL", fn);
+    GCN_TRY(check_vec(fn, "loss_out", loss_out, 1));
+    for (int l = 0; l < L; ++l) {
+        const int64_t F = l == 0 ? d->f_in : 2 * (int64_t)h;
+        GCN_TRY(check_mat(fn, "W_self[l]", P->W_self[l], F, h, h));
+        GCN_TRY(check_mat(fn, "W_neigh[l]", P->W_neigh[l], F, h, h));
+        if (d->has_bias) GCN_TRY(check_vec(fn, "b[l]", P->b[l], 2 * (int64_t)h));
+        if (grads) {
+            if (grads->W_self[l]) GCN_TRY(check_vec(fn, "grads W_self[l]", grads->W_self[l], F * h));
+            if (grads->W_neigh[l]) GCN_TRY(check_vec(fn, "grads W_neigh[l]", grads->W_neigh[l], F * h));
+            if (grads->b[l]) {
+                GCN_CHECK_ARG(d->has_bias, "%s: bias gradient requested without biases", fn);
+                GCN_TRY(check_vec(fn, "grads b[l]", grads->b[l], 2 * (int64_t)h));
+            }
+        }
+    }
+    GCN_TRY(check_vec(fn, "W_cls", P->W_cls, 2 * (int64_t)h * C));
+    if (d->has_bias) GCN_TRY(check_vec(fn, "b_cls", P->b_cls, C));
+    if (grads) {
+        if (grads->W_cls) GCN_TRY(check_vec(fn, "grads W_cls", grads->W_cls, 2 * (int64_t)h * C));
+        if (grads->b_cls) {
+            GCN_CHECK_ARG(d->has_bias, "%s: bias gradient requested without biases", fn);
+            GCN_TRY(check_vec(fn, "grads b_cls", grads->b_cls, C));
+        }
+    }
+    StepLayout sl;
+    GCN_TRY(plan_step(g, d, &sl));
+    GCN_TRY(check_ws(fn, ws, ws_bytes, sl.pub.total_bytes));
+
+    hipStream_t s = (hipStream_t)stream;
+    void* scratch = static_cast<char*>(ws) + sl.pub.scratch;
+    const ScratchPlan& sp = sl.sp;
+    const int64_t ldH = sl.pub.ld_H, ldC = sl.pub.ld_C;
+    auto act = [&](int64_t off) { return fptr(ws, off); };
+
+    // forward (Eq. 1, every layer)
+    const float* Hprev = X;
+    int64_t ldprev = d->ld_x;
+    for (int l = 0; l < L; ++l) {
+        const int32_t F = l == 0 ? d->f_in : 2 * h;
+        GCN_TRY(do_layer_fwd(fn, g, F, h, Hprev, ldprev, P->W_self[l], P->W_neigh[l],
+                             d->has_bias ? P->b[l] : nullptr, act(sl.pub.AH[l]),
+                             sl.pub.ld_AH[l], act(sl.pub.H[l]), ldH, sp, scratch, s));
+        Hprev = act(sl.pub.H[l]);
+        ldprev = ldH;
+    }
+    // classifier + loss
+    float* Z = act(sl.pub.logits);
+    float* dZ = act(sl.pub.dlogits);
+    GCN_TRY(do_classifier_fwd(fn, (int32_t)n, 2 * h, C, Hprev, ldH, P->W_cls,
+                              d->has_bias ? P->b_cls : nullptr, Z, ldC, s));
+    GCN_HIP(launch_loss((int32_t)n, C, d->loss, Z, ldC, labels, dZ, ldC,
+                        fptr(scratch, sp.rowloss), loss_out, s),
+            fn);
+    // backward (classifier, then Eq. 2a-2c layer by layer)
+    float* Gcur = act(sl.pub.G[L - 1]);
+    GCN_TRY(do_classifier_bwd(fn, (int32_t)n, 2 * h, C, dZ, ldC, Hprev, ldH, P->W_cls,
+                              d->has_bias ? P->b_cls : nullptr, lr, Gcur, ldH,
+                              grads ? grads->W_cls : nullptr,
+                              grads ? grads->b_cls : nullptr, sp, scratch, s));
+    for (int l = L - 1; l >= 0; --l) {
+        const int32_t F = l == 0 ? d->f_in : 2 * h;
+        const float* Hin = l == 0 ? X : act(sl.pub.H[l - 1]);
+        const int64_t ldin = l == 0 ? d->ld_x : ldH;
+        float* Gnext = l > 0 ? act(sl.pub.G[l - 1]) : nullptr;
+        GCN_TRY(do_layer_bwd(fn, g, F, h, Gcur, ldH, Hin, ldin, act(sl.pub.AH[l]),
+                             sl.pub.ld_AH[l], P->W_self[l], P->W_neigh[l],
+                             d->has_bias ? P->b[l] : nullptr, lr, Gnext, ldH,
+                             grads ? grads->W_self[l] : nullptr,
+                             grads ? grads->W_neigh[l] : nullptr,
+                             grads ? grads->b[l] : nullptr, sp, scratch, s));
+        Gcur = Gnext;
+    }
+    return GCN_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,42 @@
+// Internal helpers shared by the host and device halves of the library.
+#pragma once
+
+#include <cstdarg>
+#include <cstdint>
+#include <cstdio>
+#include <string>
+
+#include "../../include/gcn_act.h"
+
+namespace gcn {
+
+void set_error(const char* fmt, ...);
+void clear_error();
+
+// Fails the calling entry point with GCN_E_INVALID_ARG and a message.
+#define GCN_CHECK_ARG(cond, ...)                 \
+    do {                                         \
+        if (!(cond)) {                           \
+            ::gcn::set_error(__VA_ARGS__);       \
+            return GCN_E_INVALID_ARG;            \
+        }                                        \
+    } while (0)
+
+inline int64_t round_up(int64_t x, int64_t a) { return (x + a - 1) / a * a; }
+
+// Layout of the packed device image of a reduced graph. All sections start
+// on 256-byte boundaries; the header is stored at offset 0.
+struct ImageHeader {
+    uint32_t magic;
+    int32_t n, naux, rounds, seg_len;
+    int32_t nseg, nlong, nslots, max_row;
+    int32_t pad0;
+    int64_t nnz;
+    int64_t off_rowptr, off_col, off_pairs, off_inv_deg, off_seg, off_longrows;
+    int64_t total;
+    int32_t round_offsets[GCN_MAX_ROUNDS + 1];
+};
+constexpr uint32_t kImageMagic = 0x47434e31u;  // "GCN1"
+constexpr int kDefaultSegLen = 64;
+
+}  // namespace gcn

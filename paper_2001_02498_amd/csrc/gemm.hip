@@ -1,0 +1,335 @@
+// Dense products of the layer (Eq. 1 transforms, Eq. 2 gradients) on the
+// gfx950 matrix cores: v_mfma_f32_32x32x2_f32, fp32 in and out.
+//
+// Tile: 128 x 128 per 256-thread workgroup, K step 16; four wavefronts in a
+// 2 x 2 grid each own a 64 x 64 block = 2 x 2 MFMA 32x32 accumulators.
+// Operands are staged k-major in LDS (double-buffered, one barrier per K
+// step), so every fragment read is 32 consecutive floats per half-wave.
+// Global loads are float4 along whichever dimension is contiguous in HBM;
+// ragged M / N / K edges are zero-filled. Epilogues fuse what the layer
+// needs next: bias + ReLU + placement into one half of the concatenated
+// output (forward), the ReLU mask of the previous layer (input gradient),
+// or a split-K slice (weight gradient, summed later in fixed order).
+// Tiles are renumbered so consecutive tiles (sharing A rows or a K range)
+// land on the same XCD, whose L2 then serves their common operand.
+#include <algorithm>
+
+#include "kernels.h"
+
+namespace gcn {
+namespace {
+
+typedef float floatx16 __attribute__((ext_vector_type(16)));
+
+constexpr int BM = 128, BN = 128, BK = 16;
+constexpr int kThreads = 256;
+constexpr int kStride = BM + 4;   // LDS row stride (floats), 16-byte aligned
+constexpr int kXcds = 8;
+
+__device__ __forceinline__ float4 ld4(const float* p) {
+    return *reinterpret_cast<const float4*>(p);
+}
+
+__device__ __forceinline__ void zero_from(float4& v, int valid) {
+    // keep the first `valid` elements (valid may be <= 0 or >= 4)
+    if (valid < 4) v.w = 0.f;
+    if (valid < 3) v.z = 0.f;
+    if (valid < 2) v.y = 0.f;
+    if (valid < 1) v.x = 0.f;
+}
+
+// Row-contiguous operand (A_MK rows = m, or B_NK rows = n), K-concatenated:
+// element (r, k) at P0[r*ld0 + k] for k < ksplit, else P1[r*ld1 + k-ksplit].
+// vec: rows are 16-byte aligned, so one float4 load (its tail past the
+// logical width stays inside the padded row); else element loads.
+__device__ __forceinline__ float4 load_rowk(const float* P0, const float* P1,
+                                            int64_t ld0, int64_t ld1,
+                                            int ksplit, int rows, int r, int k,
+                                            int kend, bool vec) {
+    float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+    if (r < rows && k < kend) {
+        const float* p = k < ksplit ? P0 + (int64_t)r * ld0 + k
+                                    : P1 + (int64_t)r * ld1 + (k - ksplit);
+        const int valid = kend - k;
+        if (vec) {
+            v = ld4(p);
+            zero_from(v, valid);
+        } else {
+            v.x = p[0];
+            if (valid > 1) v.y = p[1];
+            if (valid > 2) v.z = p[2];
+            if (valid > 3) v.w = p[3];
+        }
+    }
+    return v;
+}
+
+// K-major operand (A_KM or B_KN): element (c, k) at P[k*ld + c], c < cols;
+// with ones, column c == cols is an implicit 1 (bias gradient row).
+__device__ __forceinline__ float4 load_kcol(const float* P, int64_t ld,
+                                            int cols, bool ones, int c, int k,
+                                            int kend, bool vec) {
+    float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+    if (k < kend) {
+        if (c < cols) {
+            const float* p = P + (int64_t)k * ld + c;
+            const int valid = cols - c;
+            if (vec) {
+                v = ld4(p);
+                zero_from(v, valid);
+            } else {
+                v.x = p[0];
+                if (valid > 1) v.y = p[1];
+                if (valid > 2) v.z = p[2];
+                if (valid > 3) v.w = p[3];
+            }
+        }
+        if (ones) {
+            const int o = cols - c;
+            if (o == 0) v.x = 1.f;
+            if (o == 1) v.y = 1.f;
+            if (o == 2) v.z = 1.f;
+            if (o == 3) v.w = 1.f;
+        }
+    }
+    return v;
+}
+
+template <ALayout AL, BLayout BL, Epilogue EP>
+__global__ __launch_bounds__(kThreads, 2) void gemm_kernel(GemmBatch batch) {
+    __shared__ float As[2][BK][kStride];
+    __shared__ float Bs[2][BK][kStride];
+
+    // XCD-aware renumbering: workgroup b runs on XCD b % 8; give each XCD a
+    // contiguous range of logical tiles.
+    const int T = batch.total_tiles;
+    const int bid = blockIdx.x;
+    const int xcd = bid % kXcds, slot = bid / kXcds;
+    const int per = T / kXcds, rem = T % kXcds;
+    const int tile = xcd * per + min(xcd, rem) + slot;
+
+    const int pi = (batch.nprob > 1 && tile >= batch.p[1].tile_begin) ? 1 : 0;
+    const GemmProblem& P = batch.p[pi];
+    int local = tile - P.tile_begin;
+    const int per_split = P.tiles_m * P.tiles_n;
+    const int split = local / per_split;
+    local -= split * per_split;
+    const int m0 = (local / P.tiles_n) * BM;
+    const int n0 = (local % P.tiles_n) * BN;
+    const int kbeg = split * P.kchunk;
+    const int kend = min(P.K, kbeg + P.kchunk);
+    const int nk = kend > kbeg ? (kend - kbeg + BK - 1) / BK : 0;
+
+    const int t = threadIdx.x;
+    const int lane = t & 63, wave = t >> 6;
+    const int wm = wave >> 1, wn = wave & 1;
+
+    const int Areal = P.M - P.ones_row;   // rows of A backed by memory
+
+    float4 ra[2], rb[2];
+    auto gload = [&](int k0) {
+#pragma unroll
+        for (int i = 0; i < 2; ++i) {
+            if constexpr (AL == A_MK) {
+                ra[i] = load_rowk(P.A0, P.A1, P.lda0, P.lda1, P.ksplitA, P.M,
+                                  m0 + (t >> 2) + 64 * i, k0 + 4 * (t & 3), kend,
+                                  P.a_vec != 0);
+            } else {
+                ra[i] = load_kcol(P.A0, P.lda0, Areal, P.ones_row != 0,
+                                  m0 + 4 * (t & 31), k0 + (t >> 5) + 8 * i, kend,
+                                  P.a_vec != 0);
+            }
+            if constexpr (BL == B_NK) {
+                rb[i] = load_rowk(P.B0, P.B1, P.ldb0, P.ldb1, P.ksplitB, P.N,
+                                  n0 + (t >> 2) + 64 * i, k0 + 4 * (t & 3), kend,
+                                  P.b_vec != 0);
+            } else {
+                rb[i] = load_kcol(P.B0, P.ldb0, P.N, false, n0 + 4 * (t & 31),
+                                  k0 + (t >> 5) + 8 * i, kend, P.b_vec != 0);
+            }
+        }
+    };
+    auto sstore = [&](int buf) {
+#pragma unroll
+        for (int i = 0; i < 2; ++i) {
+            if constexpr (AL == A_MK) {
+                const int r = (t >> 2) + 64 * i, kq = 4 * (t & 3);
+                As[buf][kq + 0][r] = ra[i].x;
+                As[buf][kq + 1][r] = ra[i].y;
+                As[buf][kq + 2][r] = ra[i].z;
+                As[buf][kq + 3][r] = ra[i].w;
+            } else {
+                *reinterpret_cast<float4*>(&As[buf][(t >> 5) + 8 * i][4 * (t & 31)]) = ra[i];
+            }
+            if constexpr (BL == B_NK) {
+                const int r = (t >> 2) + 64 * i, kq = 4 * (t & 3);
+                Bs[buf][kq + 0][r] = rb[i].x;
+                Bs[buf][kq + 1][r] = rb[i].y;
+                Bs[buf][kq + 2][r] = rb[i].z;
+                Bs[buf][kq + 3][r] = rb[i].w;
+            } else {
+                *reinterpret_cast<float4*>(&Bs[buf][(t >> 5) + 8 * i][4 * (t & 31)]) = rb[i];
+            }
+        }
+    };
+
+    floatx16 acc[2][2];
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+
+    if (nk > 0) {
+        gload(kbeg);
+        sstore(0);
+        __syncthreads();
+    }
+    const int half = lane >> 5, l32 = lane & 31;
+    for (int kt = 0; kt < nk; ++kt) {
+        const int buf = kt & 1;
+        if (kt + 1 < nk) gload(kbeg + (kt + 1) * BK);
+#pragma unroll
+        for (int kk = 0; kk < BK / 2; ++kk) {
+            const int kr = 2 * kk + half;
+            const float a0 = As[buf][kr][wm * 64 + l32];
+            const float a1 = As[buf][kr][wm * 64 + 32 + l32];
+            const float b0 = Bs[buf][kr][wn * 64 + l32];
+            const float b1 = Bs[buf][kr][wn * 64 + 32 + l32];
+            acc[0][0] = __builtin_amdgcn_mfma_f32_32x32x2f32(a0, b0, acc[0][0], 0, 0, 0);
+            acc[0][1] = __builtin_amdgcn_mfma_f32_32x32x2f32(a0, b1, acc[0][1], 0, 0, 0);
+            acc[1][0] = __builtin_amdgcn_mfma_f32_32x32x2f32(a1, b0, acc[1][0], 0, 0, 0);
+            acc[1][1] = __builtin_amdgcn_mfma_f32_32x32x2f32(a1, b1, acc[1][1], 0, 0, 0);
+        }
+        if (kt + 1 < nk) sstore(buf ^ 1);
+        __syncthreads();
+    }
+
+    // Epilogue. Accumulator element r of lane l is C[i][j] of the 32x32
+    // block with j = l % 32, i = (r % 4) + 8 (r / 4) + 4 (l / 32).
+    float* C = P.C;
+    if constexpr (EP == EPI_PARTIAL) C += (int64_t)split * P.part_stride;
+#pragma unroll
+    for (int bi = 0; bi < 2; ++bi) {
+#pragma unroll
+        for (int bj = 0; bj < 2; ++bj) {
+            const int n = n0 + wn * 64 + bj * 32 + l32;
+            if (n >= P.N) continue;
+            float bv = 0.f;
+            if constexpr (EP == EPI_BIAS_RELU || EP == EPI_BIAS) {
+                if (P.bias) bv = P.bias[n];
+            }
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+                const int m = m0 + wm * 64 + bi * 32 + (r & 3) + 8 * (r >> 2) + 4 * half;
+                if (m >= P.M) continue;
+                float v = acc[bi][bj][r];
+                if constexpr (EP == EPI_BIAS_RELU) {
+                    v += bv;
+                    v = v > 0.f ? v : 0.f;
+                } else if constexpr (EP == EPI_BIAS) {
+                    v += bv;
+                } else if constexpr (EP == EPI_MASK) {
+                    v = P.mask[(int64_t)m * P.ldmask + n] > 0.f ? v : 0.f;
+                }
+                C[(int64_t)m * P.ldc + n] = v;
+            }
+        }
+    }
+}
+
+__global__ __launch_bounds__(256) void sgd_reduce_kernel(SgdProblem p0,
+                                                         SgdProblem p1,
+                                                         int64_t total0,
+                                                         int64_t total,
+                                                         float lr) {
+    const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (idx >= total) return;
+    const bool second = idx >= total0;
+    const SgdProblem& p = second ? p1 : p0;
+    const int64_t e = second ? idx - total0 : idx;
+    const int m = (int)(e / p.N), nn = (int)(e % p.N);
+    const float* src = p.part + (int64_t)m * p.ldp + nn;
+    float d = 0.f;
+    for (int j = 0; j < p.splits; ++j) d += src[(int64_t)j * p.part_stride];
+    if (m < p.Mw) {
+        const int64_t w = (int64_t)m * p.N + nn;
+        p.W[w] = fmaf(-lr, d, p.W[w]);
+        if (p.dW_out) p.dW_out[w] = d;
+    } else {
+        p.b[nn] = fmaf(-lr, d, p.b[nn]);
+        if (p.db_out) p.db_out[nn] = d;
+    }
+}
+
+}  // namespace
+
+void gemm_split_plan(int32_t M, int32_t N, int32_t K, int32_t* splits,
+                     int32_t* kchunk) {
+    const int64_t tiles = (int64_t)((M + BM - 1) / BM) * ((N + BN - 1) / BN);
+    int64_t s = (512 + tiles - 1) / std::max<int64_t>(tiles, 1);
+    s = std::min<int64_t>(s, 32);
+    s = std::min<int64_t>(s, std::max(1, (K + 127) / 128));
+    s = std::max<int64_t>(s, 1);
+    const int64_t kc = (K + s - 1) / s;
+    const int64_t chunk = std::max<int64_t>(BK, (kc + BK - 1) / BK * BK);
+    *kchunk = (int32_t)chunk;
+    *splits = K > 0 ? (int32_t)((K + chunk - 1) / chunk) : 1;
+}
+
+hipError_t launch_gemm(GemmBatch& b, ALayout al, BLayout bl, Epilogue ep,
+                       hipStream_t s) {
+    int total = 0;
+    for (int i = 0; i < b.nprob; ++i) {
+        GemmProblem& p = b.p[i];
+        p.tiles_m = (p.M + BM - 1) / BM;
+        p.tiles_n = (p.N + BN - 1) / BN;
+        if (ep != EPI_PARTIAL) {
+            p.splits = 1;
+            p.kchunk = std::max(BK, (p.K + BK - 1) / BK * BK);
+        } else if (p.splits < 1 || p.kchunk < BK || p.kchunk % BK != 0) {
+            return hipErrorInvalidValue;
+        }
+        p.tile_begin = total;
+        auto aligned = [](const float* q, int64_t ld) {
+            return q == nullptr || (((uintptr_t)q & 15) == 0 && (ld & 3) == 0);
+        };
+        p.a_vec = aligned(p.A0, p.lda0) && aligned(p.A1, p.lda1);
+        p.b_vec = aligned(p.B0, p.ldb0) && aligned(p.B1, p.ldb1);
+        if (p.M > 0 && p.N > 0) total += p.tiles_m * p.tiles_n * p.splits;
+    }
+    b.total_tiles = total;
+    if (total == 0) return hipSuccess;
+    const dim3 grid(total), block(kThreads);
+#define GCN_GEMM_CASE(AL_, BL_, EP_)                                        \
+    if (al == AL_ && bl == BL_ && ep == EP_) {                               \
+        gemm_kernel<AL_, BL_, EP_><<<grid, block, 0, s>>>(b);                \
+        return hipGetLastError();                                           \
+    }
+    GCN_GEMM_CASE(A_MK, B_KN, EPI_BIAS_RELU)
+    GCN_GEMM_CASE(A_MK, B_KN, EPI_BIAS)
+    GCN_GEMM_CASE(A_MK, B_KN, EPI_STORE)
+    GCN_GEMM_CASE(A_MK, B_NK, EPI_MASK)
+    GCN_GEMM_CASE(A_MK, B_NK, EPI_STORE)
+    GCN_GEMM_CASE(A_KM, B_KN, EPI_PARTIAL)
+#undef GCN_GEMM_CASE
+    return hipErrorInvalidValue;
+}
+
+hipError_t launch_sgd_reduce(const SgdProblem* p, int nprob, float lr,
+                             hipStream_t s) {
+    if (nprob <= 0) return hipSuccess;
+    auto count = [](const SgdProblem& q) {
+        return (int64_t)(q.Mw + (q.b ? 1 : 0)) * q.N;
+    };
+    const int64_t t0 = count(p[0]);
+    const int64_t total = t0 + (nprob > 1 ? count(p[1]) : 0);
+    if (total == 0) return hipSuccess;
+    const SgdProblem second = nprob > 1 ? p[1] : p[0];
+    const int64_t blocks = (total + 255) / 256;
+    sgd_reduce_kernel<<<dim3((unsigned)blocks), dim3(256), 0, s>>>(p[0], second, t0, total, lr);
+    return hipGetLastError();
+}
+
+}  // namespace gcn

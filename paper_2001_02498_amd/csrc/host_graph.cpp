@@ -1,0 +1,564 @@
+// Host-side graph preprocessing: subgraph construction (Section 2.1,
+// Section 3.1) and the redundancy reduction of Section 3.2 (Algorithms 1-3
+// applied in rounds), plus packing of the device image. CPU only: nothing
+// here calls the HIP runtime, so it also builds and runs without a GPU.
+#include <algorithm>
+#include <atomic>
+#include <cstring>
+#include <exception>
+#include <new>
+#include <numeric>
+#include <thread>
+#include <vector>
+
+#include "common.h"
+
+namespace gcn {
+
+static thread_local std::string g_err;
+
+void set_error(const char* fmt, ...) {
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof(buf), fmt, ap);
+    va_end(ap);
+    g_err = buf;
+}
+
+void clear_error() { g_err.clear(); }
+
+}  // namespace gcn
+
+using gcn::set_error;
+
+struct gcn_graph {
+    int32_t n = 0;
+    std::vector<int32_t> rowptr;  // n + 1
+    std::vector<int32_t> col;
+};
+
+struct gcn_reduced {
+    int32_t n = 0, naux = 0, rounds = 0;
+    std::vector<int32_t> rowptr, col, pairs, round_offsets, deg;
+    std::vector<gcn_rr_round> stats;
+};
+
+namespace {
+
+// Runs body(t) on `threads` threads (inline when threads == 1).
+template <class F>
+void parallel_run(int threads, F&& body) {
+    if (threads <= 1) {
+        body(0);
+        return;
+    }
+    std::vector<std::thread> pool;
+    pool.reserve(threads);
+    for (int t = 0; t < threads; ++t) pool.emplace_back([&, t] { body(t); });
+    for (auto& th : pool) th.join();
+}
+
+int pick_threads(int requested, int64_t work) {
+    int hw = (int)std::thread::hardware_concurrency();
+    if (hw <= 0) hw = 1;
+    int t = requested > 0 ? requested : hw;
+    t = std::min(t, 64);
+    // small problems are not worth the thread start-up
+    int64_t cap = std::max<int64_t>(1, work / 200000);
+    return (int)std::max<int64_t>(1, std::min<int64_t>(t, cap));
+}
+
+struct Candidate {
+    int64_t w;
+    int32_t x, y;
+};
+
+// Lists of the aggregators in CSR form; ids in [0, ncols).
+struct Lists {
+    int32_t n = 0, ncols = 0;
+    std::vector<int64_t> ptr;
+    std::vector<int32_t> col;
+};
+
+// Algorithm 1, keeping only pairs whose count exceeds theta: for each x,
+// walk the lists that hold x and count every larger id y that follows x in
+// the same (sorted) list; the count of {x, y} is the number of lists holding
+// both. A dense counter per thread plays the hash table.
+std::vector<Candidate> count_pairs(const Lists& L, int theta, int threads) {
+    const int32_t ncols = L.ncols;
+    // transposed index: for each id, the (list, position) pairs holding it
+    std::vector<int64_t> tptr(ncols + 1, 0);
+    for (int64_t e = 0; e < L.ptr[L.n]; ++e) tptr[L.col[e] + 1]++;
+    for (int32_t c = 0; c < ncols; ++c) tptr[c + 1] += tptr[c];
+    std::vector<int32_t> tlist(L.ptr[L.n]), tpos(L.ptr[L.n]);
+    {
+        std::vector<int64_t> fill(tptr.begin(), tptr.end() - 1);
+        for (int32_t w = 0; w < L.n; ++w)
+            for (int64_t e = L.ptr[w]; e < L.ptr[w + 1]; ++e) {
+                int64_t k = fill[L.col[e]]++;
+                tlist[k] = w;
+                tpos[k] = (int32_t)(e - L.ptr[w]);
+            }
+    }
+    int64_t work = 0;
+    for (int32_t w = 0; w < L.n; ++w) {
+        int64_t d = L.ptr[w + 1] - L.ptr[w];
+        work += d * (d - 1) / 2;
+    }
+    int nt = pick_threads(threads, work);
+    std::vector<std::vector<Candidate>> out(nt);
+    std::atomic<int32_t> next{0};
+    const int32_t chunk = 32;
+    parallel_run(nt, [&](int t) {
+        std::vector<int32_t> cnt(ncols, 0);
+        std::vector<int32_t> touched;
+        touched.reserve(1024);
+        auto& mine = out[t];
+        for (;;) {
+            int32_t x0 = next.fetch_add(chunk);
+            if (x0 >= ncols) break;
+            int32_t x1 = std::min(ncols, x0 + chunk);
+            for (int32_t x = x0; x < x1; ++x) {
+                for (int64_t k = tptr[x]; k < tptr[x + 1]; ++k) {
+                    int32_t w = tlist[k];
+                    const int32_t* row = L.col.data() + L.ptr[w];
+                    int32_t d = (int32_t)(L.ptr[w + 1] - L.ptr[w]);
+                    for (int32_t p = tpos[k] + 1; p < d; ++p) {
+                        int32_t y = row[p];
+                        if (cnt[y]++ == 0) touched.push_back(y);
+                    }
+                }
+                for (int32_t y : touched) {
+                    // weight-1 pairs are not edges of G_a (Alg. 1 drops them)
+                    if (cnt[y] > theta && cnt[y] >= 2) mine.push_back({cnt[y], x, y});
+                    cnt[y] = 0;
+                }
+                touched.clear();
+            }
+        }
+    });
+    std::vector<Candidate> all;
+    size_t total = 0;
+    for (auto& v : out) total += v.size();
+    all.reserve(total);
+    for (auto& v : out) all.insert(all.end(), v.begin(), v.end());
+    return all;
+}
+
+// Algorithm 3 for one round: rewrite every list, replacing each matched pair
+// it holds by the pair's new id; lists stay sorted (new ids exceed all older
+// ones, and the few new ids of a list are sorted among themselves).
+Lists rewrite(const Lists& L, const std::vector<int32_t>& partner,
+              const std::vector<int32_t>& newid, int32_t ncols_new,
+              int threads) {
+    Lists out;
+    out.n = L.n;
+    out.ncols = ncols_new;
+    out.ptr.assign(L.n + 1, 0);
+    int nt = pick_threads(threads, L.ptr[L.n] * 4);
+    auto pass = [&](bool fill) {
+        std::atomic<int32_t> next{0};
+        parallel_run(nt, [&](int) {
+            std::vector<int32_t> stamp(L.ncols, -1);
+            std::vector<int32_t> added;
+            for (;;) {
+                int32_t w0 = next.fetch_add(256);
+                if (w0 >= L.n) break;
+                int32_t w1 = std::min(L.n, w0 + 256);
+                for (int32_t w = w0; w < w1; ++w) {
+                    const int32_t* row = L.col.data() + L.ptr[w];
+                    int32_t d = (int32_t)(L.ptr[w + 1] - L.ptr[w]);
+                    for (int32_t i = 0; i < d; ++i) stamp[row[i]] = w;
+                    int32_t* dst = fill ? out.col.data() + out.ptr[w] : nullptr;
+                    int32_t kept = 0;
+                    added.clear();
+                    for (int32_t i = 0; i < d; ++i) {
+                        int32_t c = row[i];
+                        int32_t p = partner[c];
+                        if (p >= 0 && stamp[p] == w) {
+                            if (c < p) added.push_back(newid[c]);
+                            continue;
+                        }
+                        if (fill) dst[kept] = c;
+                        ++kept;
+                    }
+                    if (fill) {
+                        std::sort(added.begin(), added.end());
+                        std::copy(added.begin(), added.end(), dst + kept);
+                    } else {
+                        out.ptr[w + 1] = kept + (int32_t)added.size();
+                    }
+                }
+            }
+        });
+    };
+    pass(false);
+    for (int32_t w = 0; w < L.n; ++w) out.ptr[w + 1] += out.ptr[w];
+    out.col.resize(out.ptr[L.n]);
+    pass(true);
+    return out;
+}
+
+int64_t num_add(const Lists& L) {
+    int64_t s = 0;
+    for (int32_t w = 0; w < L.n; ++w) {
+        int64_t d = L.ptr[w + 1] - L.ptr[w];
+        if (d >= 1) s += d - 1;
+    }
+    return s;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* gcn_last_error(void) { return gcn::g_err.c_str(); }
+
+int gcn_abi_version(void) { return GCN_ABI_VERSION; }
+
+int gcn_subgraph_build(int64_t n_full, const int64_t* src, const int64_t* dst,
+                       int64_t n_edges, const int64_t* vertices,
+                       int64_t n_vertices, gcn_graph_t* out) {
+    GCN_CHECK_ARG(out != nullptr, "gcn_subgraph_build: out is NULL");
+    GCN_CHECK_ARG(n_full >= 0 && n_full < INT32_MAX,
+                  "gcn_subgraph_build: n_full %lld outside [0, 2^31-1)",
+                  (long long)n_full);
+    GCN_CHECK_ARG(n_edges >= 0, "gcn_subgraph_build: negative n_edges");
+    GCN_CHECK_ARG(n_edges == 0 || (src && dst),
+                  "gcn_subgraph_build: src/dst NULL with n_edges > 0");
+    GCN_CHECK_ARG(vertices == nullptr || (n_vertices >= 0 && n_vertices <= n_full),
+                  "gcn_subgraph_build: n_vertices outside [0, n_full]");
+    try {
+        const int32_t n = vertices ? (int32_t)n_vertices : (int32_t)n_full;
+        std::vector<int32_t> relabel;
+        if (vertices) {
+            relabel.assign((size_t)n_full, -1);
+            for (int64_t k = 0; k < n_vertices; ++k) {
+                int64_t v = vertices[k];
+                GCN_CHECK_ARG(v >= 0 && v < n_full,
+                              "gcn_subgraph_build: vertex %lld out of range",
+                              (long long)v);
+                GCN_CHECK_ARG(relabel[v] < 0,
+                              "gcn_subgraph_build: vertex %lld repeated",
+                              (long long)v);
+                relabel[v] = (int32_t)k;
+            }
+        }
+        std::vector<int64_t> cnt((size_t)n + 1, 0);
+        for (int64_t i = 0; i < n_edges; ++i) {
+            int64_t a = src[i], b = dst[i];
+            GCN_CHECK_ARG(a >= 0 && a < n_full && b >= 0 && b < n_full,
+                          "gcn_subgraph_build: edge %lld (%lld, %lld) out of range",
+                          (long long)i, (long long)a, (long long)b);
+        }
+        auto map = [&](int64_t v) -> int32_t {
+            return vertices ? relabel[v] : (int32_t)v;
+        };
+        for (int64_t i = 0; i < n_edges; ++i) {
+            int32_t a = map(src[i]), b = map(dst[i]);
+            if (a < 0 || b < 0 || a == b) continue;
+            cnt[a + 1]++;
+            cnt[b + 1]++;
+        }
+        for (int32_t v = 0; v < n; ++v) cnt[v + 1] += cnt[v];
+        std::vector<int32_t> adj(cnt[n]);
+        std::vector<int64_t> fill(cnt.begin(), cnt.end() - 1);
+        for (int64_t i = 0; i < n_edges; ++i) {
+            int32_t a = map(src[i]), b = map(dst[i]);
+            if (a < 0 || b < 0 || a == b) continue;
+            adj[fill[a]++] = b;
+            adj[fill[b]++] = a;
+        }
+        auto* g = new gcn_graph;
+        g->n = n;
+        g->rowptr.assign((size_t)n + 1, 0);
+        int64_t total = 0;
+        for (int32_t v = 0; v < n; ++v) {
+            auto b = adj.begin() + cnt[v], e = adj.begin() + cnt[v + 1];
+            std::sort(b, e);
+            auto last = std::unique(b, e);
+            total += last - b;
+            if (total >= INT32_MAX) {
+                delete g;
+                set_error("gcn_subgraph_build: more than 2^31-1 list entries");
+                return GCN_E_INVALID_ARG;
+            }
+            g->rowptr[v + 1] = (int32_t)total;
+        }
+        g->col.resize(total);
+        for (int32_t v = 0; v < n; ++v) {
+            int64_t d = g->rowptr[v + 1] - g->rowptr[v];
+            std::copy(adj.begin() + cnt[v], adj.begin() + cnt[v] + d,
+                      g->col.begin() + g->rowptr[v]);
+        }
+        *out = g;
+        gcn::clear_error();
+        return GCN_OK;
+    } catch (const std::bad_alloc&) {
+        set_error("gcn_subgraph_build: out of host memory");
+        return GCN_E_OOM;
+    }
+}
+
+int gcn_graph_info(gcn_graph_t g, int32_t* n, int64_t* nnz,
+                   const int32_t** rowptr, const int32_t** col) {
+    GCN_CHECK_ARG(g != nullptr, "gcn_graph_info: NULL graph");
+    if (n) *n = g->n;
+    if (nnz) *nnz = g->rowptr[g->n];
+    if (rowptr) *rowptr = g->rowptr.data();
+    if (col) *col = g->col.data();
+    return GCN_OK;
+}
+
+void gcn_graph_free(gcn_graph_t g) { delete g; }
+
+int gcn_redundancy_reduce(gcn_graph_t g, const gcn_rr_params* params,
+                          gcn_reduced_t* out) {
+    GCN_CHECK_ARG(g != nullptr && params != nullptr && out != nullptr,
+                  "gcn_redundancy_reduce: NULL argument");
+    GCN_CHECK_ARG(params->theta >= 0, "gcn_redundancy_reduce: theta < 0");
+    GCN_CHECK_ARG(params->max_rounds >= 0 && params->max_rounds <= GCN_MAX_ROUNDS,
+                  "gcn_redundancy_reduce: max_rounds %d outside [0, %d]",
+                  params->max_rounds, GCN_MAX_ROUNDS);
+    GCN_CHECK_ARG(params->num_threads >= 0, "gcn_redundancy_reduce: num_threads < 0");
+    try {
+        const int32_t n = g->n;
+        Lists L;
+        L.n = n;
+        L.ncols = n;
+        L.ptr.assign(g->rowptr.begin(), g->rowptr.end());
+        L.col = g->col;
+        auto* r = new gcn_reduced;
+        r->n = n;
+        r->deg.resize(n);
+        for (int32_t v = 0; v < n; ++v) r->deg[v] = g->rowptr[v + 1] - g->rowptr[v];
+        r->round_offsets.push_back(0);
+        const int64_t max_aux = params->max_aux;
+        for (int round = 0; round < params->max_rounds; ++round) {
+            int64_t naux = (int64_t)r->pairs.size() / 2;
+            int64_t budget_left = max_aux < 0 ? INT64_MAX : max_aux - naux;
+            if (budget_left <= 0) break;
+            if ((int64_t)L.ncols + std::min<int64_t>(budget_left, L.ncols) >= INT32_MAX) {
+                delete r;
+                set_error("gcn_redundancy_reduce: vertex ids would exceed 2^31-1");
+                return GCN_E_INVALID_ARG;
+            }
+            // Algorithm 1 (candidates above theta only)
+            std::vector<Candidate> cand = count_pairs(L, params->theta, params->num_threads);
+            // Algorithm 2: decreasing weight, then (x, y) ascending
+            std::sort(cand.begin(), cand.end(), [](const Candidate& a, const Candidate& b) {
+                if (a.w != b.w) return a.w > b.w;
+                if (a.x != b.x) return a.x < b.x;
+                return a.y < b.y;
+            });
+            std::vector<char> used(L.ncols, 0);
+            std::vector<int32_t> partner(L.ncols, -1), newid(L.ncols, -1);
+            int64_t taken = 0, wsum = 0;
+            bool exhausted = false;
+            for (const Candidate& c : cand) {
+                if (taken >= budget_left) {
+                    exhausted = true;
+                    break;
+                }
+                if (used[c.x] || used[c.y]) continue;
+                used[c.x] = used[c.y] = 1;
+                int32_t id = L.ncols + (int32_t)taken;
+                partner[c.x] = c.y;
+                partner[c.y] = c.x;
+                newid[c.x] = newid[c.y] = id;
+                r->pairs.push_back(c.x);
+                r->pairs.push_back(c.y);
+                wsum += c.w;
+                ++taken;
+            }
+            if (taken == 0) break;
+            // Algorithm 3
+            L = rewrite(L, partner, newid, L.ncols + (int32_t)taken, params->num_threads);
+            r->round_offsets.push_back((int32_t)(r->pairs.size() / 2));
+            r->stats.push_back({taken, wsum, L.ptr[n], num_add(L)});
+            if (exhausted) break;
+        }
+        r->naux = (int32_t)(r->pairs.size() / 2);
+        r->rounds = (int32_t)r->stats.size();
+        if (L.ptr[n] >= INT32_MAX) {
+            delete r;
+            set_error("gcn_redundancy_reduce: list entries exceed 2^31-1");
+            return GCN_E_INVALID_ARG;
+        }
+        r->rowptr.resize(n + 1);
+        for (int32_t v = 0; v <= n; ++v) r->rowptr[v] = (int32_t)L.ptr[v];
+        r->col = std::move(L.col);
+        *out = r;
+        gcn::clear_error();
+        return GCN_OK;
+    } catch (const std::bad_alloc&) {
+        set_error("gcn_redundancy_reduce: out of host memory");
+        return GCN_E_OOM;
+    }
+}
+
+int gcn_reduced_info(gcn_reduced_t r, int32_t* n, int32_t* naux,
+                     int32_t* rounds, int64_t* nnz, const int32_t** rowptr,
+                     const int32_t** col, const int32_t** pairs,
+                     const int32_t** round_offsets,
+                     const gcn_rr_round** per_round, const int32_t** deg) {
+    GCN_CHECK_ARG(r != nullptr, "gcn_reduced_info: NULL handle");
+    if (n) *n = r->n;
+    if (naux) *naux = r->naux;
+    if (rounds) *rounds = r->rounds;
+    if (nnz) *nnz = r->rowptr[r->n];
+    if (rowptr) *rowptr = r->rowptr.data();
+    if (col) *col = r->col.data();
+    if (pairs) *pairs = r->pairs.data();
+    if (round_offsets) *round_offsets = r->round_offsets.data();
+    if (per_round) *per_round = r->stats.data();
+    if (deg) *deg = r->deg.data();
+    return GCN_OK;
+}
+
+void gcn_reduced_free(gcn_reduced_t r) { delete r; }
+
+// ----------------------------------------------------------- device image
+
+static int plan_image(gcn_reduced_t r, int32_t seg_len, gcn::ImageHeader* h) {
+    GCN_CHECK_ARG(r != nullptr, "graph image: NULL reduced graph");
+    if (seg_len == 0) seg_len = gcn::kDefaultSegLen;
+    GCN_CHECK_ARG(seg_len >= 1 && seg_len <= 65536,
+                  "graph image: seg_len %d outside [1, 65536]", seg_len);
+    std::memset(h, 0, sizeof(*h));
+    h->magic = gcn::kImageMagic;
+    h->n = r->n;
+    h->naux = r->naux;
+    h->rounds = r->rounds;
+    h->seg_len = seg_len;
+    h->nnz = r->rowptr[r->n];
+    int64_t nseg = 0, nlong = 0, nslots = 0;
+    int32_t max_row = 0;
+    for (int32_t w = 0; w < r->n; ++w) {
+        int32_t d = r->rowptr[w + 1] - r->rowptr[w];
+        max_row = std::max(max_row, d);
+        if (d <= seg_len) {
+            ++nseg;
+        } else {
+            int32_t k = (d + seg_len - 1) / seg_len;
+            nseg += k;
+            nslots += k;
+            ++nlong;
+        }
+    }
+    GCN_CHECK_ARG(nseg < INT32_MAX, "graph image: too many segments");
+    h->nseg = (int32_t)nseg;
+    h->nlong = (int32_t)nlong;
+    h->nslots = (int32_t)nslots;
+    h->max_row = max_row;
+    int64_t off = gcn::round_up(sizeof(gcn::ImageHeader), 256);
+    auto take = [&](int64_t bytes) {
+        int64_t o = off;
+        off = gcn::round_up(off + std::max<int64_t>(bytes, 1), 256);
+        return o;
+    };
+    h->off_rowptr = take(4 * ((int64_t)r->n + 1));
+    h->off_col = take(4 * h->nnz);
+    h->off_pairs = take(8 * (int64_t)r->naux);
+    h->off_inv_deg = take(4 * (int64_t)r->n);
+    h->off_seg = take(16 * nseg);
+    h->off_longrows = take(16 * nlong);
+    h->total = off;
+    for (int i = 0; i <= r->rounds; ++i) h->round_offsets[i] = r->round_offsets[i];
+    return GCN_OK;
+}
+
+int gcn_graph_image_bytes(gcn_reduced_t r, int32_t seg_len, size_t* bytes) {
+    GCN_CHECK_ARG(bytes != nullptr, "gcn_graph_image_bytes: NULL bytes");
+    gcn::ImageHeader h;
+    int rc = plan_image(r, seg_len, &h);
+    if (rc) return rc;
+    *bytes = (size_t)h.total;
+    return GCN_OK;
+}
+
+int gcn_graph_pack(gcn_reduced_t r, int32_t seg_len, void* host_buf,
+                   size_t bytes) {
+    GCN_CHECK_ARG(host_buf != nullptr, "gcn_graph_pack: NULL buffer");
+    gcn::ImageHeader h;
+    int rc = plan_image(r, seg_len, &h);
+    if (rc) return rc;
+    GCN_CHECK_ARG(bytes >= (size_t)h.total,
+                  "gcn_graph_pack: buffer of %zu bytes, image needs %lld",
+                  bytes, (long long)h.total);
+    char* base = static_cast<char*>(host_buf);
+    std::memset(base, 0, (size_t)h.total);
+    std::memcpy(base, &h, sizeof(h));
+    std::memcpy(base + h.off_rowptr, r->rowptr.data(), 4 * ((size_t)r->n + 1));
+    if (h.nnz) std::memcpy(base + h.off_col, r->col.data(), 4 * (size_t)h.nnz);
+    if (r->naux) std::memcpy(base + h.off_pairs, r->pairs.data(), 8 * (size_t)r->naux);
+    float* inv = reinterpret_cast<float*>(base + h.off_inv_deg);
+    for (int32_t v = 0; v < r->n; ++v)
+        inv[v] = r->deg[v] > 0 ? (float)(1.0 / (double)r->deg[v]) : 0.0f;
+    // Work list: long lists first (split into seg_len pieces whose partial
+    // sums land in consecutive slots), then the short lists in row order.
+    int32_t* seg = reinterpret_cast<int32_t*>(base + h.off_seg);
+    int32_t* lr = reinterpret_cast<int32_t*>(base + h.off_longrows);
+    int64_t s = 0, slot = 0, li = 0;
+    for (int32_t w = 0; w < r->n; ++w) {
+        int32_t b = r->rowptr[w], e = r->rowptr[w + 1];
+        if (e - b <= h.seg_len) continue;
+        int32_t k = (e - b + h.seg_len - 1) / h.seg_len;
+        lr[4 * li + 0] = w;
+        lr[4 * li + 1] = (int32_t)slot;
+        lr[4 * li + 2] = k;
+        lr[4 * li + 3] = 0;
+        ++li;
+        for (int32_t j = 0; j < k; ++j) {
+            seg[4 * s + 0] = w;
+            seg[4 * s + 1] = b + j * h.seg_len;
+            seg[4 * s + 2] = std::min(e, b + (j + 1) * h.seg_len);
+            seg[4 * s + 3] = (int32_t)slot++;
+            ++s;
+        }
+    }
+    for (int32_t w = 0; w < r->n; ++w) {
+        int32_t b = r->rowptr[w], e = r->rowptr[w + 1];
+        if (e - b > h.seg_len) continue;
+        seg[4 * s + 0] = w;
+        seg[4 * s + 1] = b;
+        seg[4 * s + 2] = e;
+        seg[4 * s + 3] = -1;
+        ++s;
+    }
+    return GCN_OK;
+}
+
+int gcn_graph_describe(const void* host_image, size_t bytes,
+                       const void* dev_buf, gcn_dgraph* out) {
+    GCN_CHECK_ARG(host_image && dev_buf && out, "gcn_graph_describe: NULL argument");
+    GCN_CHECK_ARG(bytes >= sizeof(gcn::ImageHeader), "gcn_graph_describe: image too small");
+    gcn::ImageHeader h;
+    std::memcpy(&h, host_image, sizeof(h));
+    GCN_CHECK_ARG(h.magic == gcn::kImageMagic, "gcn_graph_describe: not a graph image");
+    GCN_CHECK_ARG((size_t)h.total <= bytes, "gcn_graph_describe: image truncated");
+    GCN_CHECK_ARG(((uintptr_t)dev_buf & 255) == 0,
+                  "gcn_graph_describe: device buffer not 256-byte aligned");
+    const char* d = static_cast<const char*>(dev_buf);
+    std::memset(out, 0, sizeof(*out));
+    out->n = h.n;
+    out->naux = h.naux;
+    out->rounds = h.rounds;
+    out->seg_len = h.seg_len;
+    out->nseg = h.nseg;
+    out->nlong = h.nlong;
+    out->nslots = h.nslots;
+    out->max_row = h.max_row;
+    out->nnz = h.nnz;
+    out->rowptr = reinterpret_cast<const int32_t*>(d + h.off_rowptr);
+    out->col = reinterpret_cast<const int32_t*>(d + h.off_col);
+    out->pairs = reinterpret_cast<const int32_t*>(d + h.off_pairs);
+    out->inv_deg = reinterpret_cast<const float*>(d + h.off_inv_deg);
+    out->seg = reinterpret_cast<const int32_t*>(d + h.off_seg);
+    out->longrows = reinterpret_cast<const int32_t*>(d + h.off_longrows);
+    for (int i = 0; i <= h.rounds; ++i) out->round_offsets[i] = h.round_offsets[i];
+    return GCN_OK;
+}
+
+}  // extern "C"

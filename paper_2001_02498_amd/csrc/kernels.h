@@ -1,0 +1,111 @@
+// Internal launch interface between the entry points (api.hip) and the
+// kernel files. Every launcher only enqueues work on `s` and returns the
+// hipGetLastError() status of its launches.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include "common.h"
+
+namespace gcn {
+
+// ---------------------------------------------------------------- aggregation
+// Extended row source: vertex c < n reads X row c, c >= n reads aux row c-n.
+struct RowSource {
+    const float* X;
+    int64_t ldx;
+    const float* aux;
+    int64_t ldaux;
+    int32_t n;
+};
+
+// Pair sums of one reduction round: aux[k] = s(p_k) src(p_k) + s(q_k) src(q_k)
+// for k in [k0, k1), s(c) = 1/d_c for original vertices when prescale, else 1.
+hipError_t launch_pair_sums(const int32_t* pairs, int32_t k0, int32_t k1,
+                            RowSource src, const float* inv_deg, bool prescale,
+                            float* aux, int64_t ldaux, int32_t F, hipStream_t s);
+
+// Segment sums of G_s^# lists (see the work list of gcn_graph_pack), then the
+// fix-up of split lists. postscale: Y_w = (1/d_w) * sum; prescale: gathered
+// original rows are multiplied by their 1/d.
+hipError_t launch_list_sums(const gcn_dgraph* g, RowSource src, bool prescale,
+                            bool postscale, float* Y, int64_t ldy,
+                            float* partial, int64_t ldp, int32_t F,
+                            hipStream_t s);
+
+// ---------------------------------------------------------------- GEMM
+enum ALayout : int { A_MK = 0, A_KM = 1 };   // A(m,k) = A[m*lda+k] | A[k*lda+m]
+enum BLayout : int { B_KN = 0, B_NK = 1 };   // B(k,n) = B[k*ldb+n] | B[n*ldb+k]
+enum Epilogue : int {
+    EPI_STORE = 0,      // C = acc
+    EPI_BIAS_RELU = 1,  // C = max(acc + bias[n], 0)   (bias may be NULL)
+    EPI_BIAS = 2,       // C = acc + bias[n]            (bias may be NULL)
+    EPI_MASK = 3,       // C = acc * [mask[m,n] > 0]
+    EPI_PARTIAL = 4,    // C + split*part_stride = acc over the split's K range
+};
+
+struct GemmProblem {
+    int32_t M, N, K;
+    // A, optionally concatenated along K: k < ksplitA reads A0, else A1 at
+    // k - ksplitA (ksplitA % 4 == 0); A_KM may append a row of ones (m == M-1)
+    const float* A0;
+    const float* A1;
+    int64_t lda0, lda1;
+    int32_t ksplitA;
+    int32_t ones_row;
+    const float* B0;
+    const float* B1;
+    int64_t ldb0, ldb1;
+    int32_t ksplitB;
+    int32_t splits;       // split-K factor (EPI_PARTIAL: from gemm_split_plan)
+    float* C;
+    int64_t ldc;
+    const float* bias;
+    const float* mask;
+    int64_t ldmask;
+    int64_t part_stride;  // floats between split slices
+    int32_t kchunk;       // K per split (EPI_PARTIAL: from gemm_split_plan)
+    int32_t tiles_m, tiles_n, tile_begin;
+    int32_t a_vec, b_vec; // operand rows 16-byte aligned: float4 loads
+};
+
+constexpr int kMaxProblems = 2;
+struct GemmBatch {
+    GemmProblem p[kMaxProblems];
+    int32_t nprob;
+    int32_t total_tiles;
+};
+
+// Split-K plan for a weight-gradient problem (deterministic in the shapes):
+// K is cut into `splits` ranges of `kchunk` (a multiple of the K tile), the
+// last one possibly shorter; every range is non-empty when K > 0.
+void gemm_split_plan(int32_t M, int32_t N, int32_t K, int32_t* splits,
+                     int32_t* kchunk);
+
+// Launch C = A B for 1-2 problems of identical layouts / epilogue.
+hipError_t launch_gemm(GemmBatch& b, ALayout al, BLayout bl, Epilogue ep,
+                       hipStream_t s);
+
+// Deterministic sum of split-K slices + gradient-descent update:
+//   d = sum_j part[j] (j ascending);  W[m][n] -= lr d  (m < Mw);
+//   bias row m == Mw (when b != NULL): b[n] -= lr d.  Optional copies of d.
+struct SgdProblem {
+    const float* part;
+    int64_t part_stride;
+    int64_t ldp;
+    int32_t splits, Mw, N;
+    float* W;
+    float* b;
+    float* dW_out;
+    float* db_out;
+};
+hipError_t launch_sgd_reduce(const SgdProblem* p, int nprob, float lr,
+                             hipStream_t s);
+
+// ---------------------------------------------------------------- loss
+hipError_t launch_loss(int32_t n, int32_t C, int32_t kind, const float* z,
+                       int64_t ldz, const void* labels, float* dz,
+                       int64_t ldd, float* rowloss, float* loss_out,
+                       hipStream_t s);
+
+}  // namespace gcn

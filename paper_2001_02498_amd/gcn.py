@@ -1,0 +1,401 @@
+"""ctypes binding of libgcnact.so (the C ABI of include/gcn_act.h).
+
+Argument marshalling only: every computation runs in the library (host C++
+for graph preprocessing, HIP kernels for the training step). Device buffers
+are torch tensors, passed by data pointer; streams are torch streams,
+passed by handle. If the library has not been built this module raises on
+import; there is no fallback path.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "_lib", "libgcnact.so")
+
+if not os.path.exists(LIB_PATH):
+    raise ImportError(f"{LIB_PATH} is missing: build it with "
+                      "`python -m paper_2001_02498_amd.build`")
+_lib = C.CDLL(LIB_PATH)
+
+OK = 0
+E_INVALID_ARG = -1
+E_HIP = -2
+E_OOM = -3
+E_UNSUPPORTED = -4
+E_WORKSPACE = -5
+E_INTERNAL = -6
+MAX_ROUNDS = 64
+MAX_LAYERS = 8
+LOSS_SOFTMAX_CE = 0
+LOSS_SIGMOID_BCE = 1
+PREC_FP32 = 0
+PREC_BF16 = 1
+AGG_MEAN = 0
+AGG_TRANSPOSED = 1
+ABI_VERSION = 1
+
+_i32, _i64, _f32 = C.c_int32, C.c_int64, C.c_float
+_vp, _sz = C.c_void_p, C.c_size_t
+_pi32 = C.POINTER(C.c_int32)
+_pi64 = C.POINTER(C.c_int64)
+_pf32 = C.POINTER(C.c_float)
+
+
+class GcnError(RuntimeError):
+    def __init__(self, code, msg):
+        super().__init__(f"[{code}] {msg}")
+        self.code = code
+
+
+class RrParams(C.Structure):
+    _fields_ = [("theta", _i32), ("max_rounds", _i32), ("max_aux", _i64),
+                ("num_threads", _i32), ("reserved", _i32)]
+
+
+class RrRound(C.Structure):
+    _fields_ = [("matched", _i64), ("weight_sum", _i64), ("nnz", _i64),
+                ("num_add", _i64)]
+
+
+class DGraph(C.Structure):
+    _fields_ = [("n", _i32), ("naux", _i32), ("rounds", _i32), ("seg_len", _i32),
+                ("nseg", _i32), ("nlong", _i32), ("nslots", _i32), ("max_row", _i32),
+                ("nnz", _i64),
+                ("rowptr", _vp), ("col", _vp), ("pairs", _vp), ("inv_deg", _vp),
+                ("seg", _vp), ("longrows", _vp),
+                ("round_offsets", _i32 * (MAX_ROUNDS + 1))]
+
+
+class ModelDesc(C.Structure):
+    _fields_ = [("L", _i32), ("f_in", _i32), ("h", _i32), ("C", _i32),
+                ("loss", _i32), ("precision", _i32), ("has_bias", _i32),
+                ("reserved", _i32), ("ld_x", _i64)]
+
+
+class Params(C.Structure):
+    _fields_ = [("W_self", _vp * MAX_LAYERS), ("W_neigh", _vp * MAX_LAYERS),
+                ("b", _vp * MAX_LAYERS), ("W_cls", _vp), ("b_cls", _vp)]
+
+
+class WsLayout(C.Structure):
+    _fields_ = [("AH", _i64 * MAX_LAYERS), ("H", _i64 * MAX_LAYERS),
+                ("ld_AH", _i64 * MAX_LAYERS), ("ld_H", _i64),
+                ("logits", _i64), ("dlogits", _i64), ("ld_C", _i64),
+                ("G", _i64 * MAX_LAYERS),
+                ("scratch", _i64), ("scratch_bytes", _i64), ("total_bytes", _i64)]
+
+
+def _proto(name, args, res=C.c_int):
+    f = getattr(_lib, name)
+    f.argtypes = args
+    f.restype = res
+    return f
+
+
+_last_error = _proto("gcn_last_error", [], C.c_char_p)
+_abi_version = _proto("gcn_abi_version", [])
+_subgraph_build = _proto("gcn_subgraph_build", [_i64, _vp, _vp, _i64, _vp, _i64, C.POINTER(_vp)])
+_graph_info = _proto("gcn_graph_info", [_vp, _pi32, _pi64, C.POINTER(_pi32), C.POINTER(_pi32)])
+_graph_free = _proto("gcn_graph_free", [_vp], None)
+_reduce = _proto("gcn_redundancy_reduce", [_vp, C.POINTER(RrParams), C.POINTER(_vp)])
+_reduced_info = _proto("gcn_reduced_info", [_vp, _pi32, _pi32, _pi32, _pi64,
+                                            C.POINTER(_pi32), C.POINTER(_pi32), C.POINTER(_pi32),
+                                            C.POINTER(_pi32), C.POINTER(C.POINTER(RrRound)),
+                                            C.POINTER(_pi32)])
+_reduced_free = _proto("gcn_reduced_free", [_vp], None)
+_image_bytes = _proto("gcn_graph_image_bytes", [_vp, _i32, C.POINTER(_sz)])
+_pack = _proto("gcn_graph_pack", [_vp, _i32, _vp, _sz])
+_upload = _proto("gcn_graph_upload", [_vp, _sz, _vp, C.POINTER(DGraph), _vp])
+_describe = _proto("gcn_graph_describe", [_vp, _sz, _vp, C.POINTER(DGraph)])
+_scratch_bytes = _proto("gcn_scratch_bytes", [C.POINTER(DGraph), _i32, _i32, C.POINTER(_sz)])
+_aggregate = _proto("gcn_aggregate", [C.POINTER(DGraph), _i32, _i32, _vp, _i64, _vp, _i64,
+                                      _vp, _sz, _vp])
+_layer_fwd = _proto("gcn_layer_fwd", [C.POINTER(DGraph), _i32, _i32, _vp, _i64, _vp, _vp, _vp,
+                                      _vp, _i64, _vp, _i64, _i32, _vp, _sz, _vp])
+_classifier_fwd = _proto("gcn_classifier_fwd", [_i32, _i32, _i32, _vp, _i64, _vp, _vp, _vp,
+                                                _i64, _i32, _vp])
+_loss = _proto("gcn_loss", [_i32, _i32, _i32, _vp, _i64, _vp, _vp, _i64, _vp, _vp, _sz, _vp])
+_classifier_bwd = _proto("gcn_classifier_bwd", [_i32, _i32, _i32, _vp, _i64, _vp, _i64, _vp,
+                                                _vp, _f32, _vp, _i64, _vp, _vp, _i32, _vp,
+                                                _sz, _vp])
+_layer_bwd = _proto("gcn_layer_bwd", [C.POINTER(DGraph), _i32, _i32, _vp, _i64, _vp, _i64, _vp,
+                                      _i64, _vp, _vp, _vp, _f32, _vp, _i64, _vp, _vp, _vp,
+                                      _i32, _vp, _sz, _vp])
+_ws_layout = _proto("gcn_workspace_layout", [C.POINTER(DGraph), C.POINTER(ModelDesc),
+                                             C.POINTER(WsLayout)])
+_ws_bytes = _proto("gcn_workspace_bytes", [C.POINTER(DGraph), C.POINTER(ModelDesc),
+                                           C.POINTER(_sz)])
+_train_step = _proto("gcn_train_step", [C.POINTER(DGraph), C.POINTER(ModelDesc),
+                                        C.POINTER(Params), _vp, _vp, _f32, _vp,
+                                        C.POINTER(Params), _vp, _sz, _vp])
+
+EXPORTS = [
+    "gcn_last_error", "gcn_abi_version", "gcn_subgraph_build", "gcn_graph_info",
+    "gcn_graph_free", "gcn_redundancy_reduce", "gcn_reduced_info", "gcn_reduced_free",
+    "gcn_graph_image_bytes", "gcn_graph_pack", "gcn_graph_upload", "gcn_graph_describe",
+    "gcn_scratch_bytes", "gcn_aggregate", "gcn_layer_fwd", "gcn_classifier_fwd",
+    "gcn_loss", "gcn_classifier_bwd", "gcn_layer_bwd", "gcn_workspace_layout",
+    "gcn_workspace_bytes", "gcn_train_step",
+]
+
+
+def last_error() -> str:
+    return _last_error().decode()
+
+
+def _check(rc):
+    if rc != OK:
+        raise GcnError(rc, last_error())
+
+
+def abi_version() -> int:
+    return _abi_version()
+
+
+# ------------------------------------------------------------------ host side
+
+def _np_ptr(a):
+    return a.ctypes.data_as(_vp) if a is not None and a.size else None
+
+
+class Graph:
+    """Undirected simple subgraph in CSR form (owned by the library)."""
+
+    def __init__(self, handle):
+        self._h = _vp(handle)
+
+    def __del__(self):
+        if getattr(self, "_h", None) and self._h.value:
+            _graph_free(self._h)
+            self._h = _vp()
+
+    def _info(self):
+        n, nnz = _i32(), _i64()
+        rp, cl = _pi32(), _pi32()
+        _check(_graph_info(self._h, C.byref(n), C.byref(nnz), C.byref(rp), C.byref(cl)))
+        return n.value, nnz.value, rp, cl
+
+    @property
+    def n(self):
+        return self._info()[0]
+
+    @property
+    def nnz(self):
+        return self._info()[1]
+
+    def csr(self):
+        n, nnz, rp, cl = self._info()
+        rowptr = np.ctypeslib.as_array(rp, shape=(n + 1,)).copy()
+        col = np.ctypeslib.as_array(cl, shape=(nnz,)).copy() if nnz else np.zeros(0, np.int32)
+        return rowptr, col
+
+
+def subgraph_build(n_full, src, dst, vertices=None) -> Graph:
+    src = np.ascontiguousarray(src, dtype=np.int64)
+    dst = np.ascontiguousarray(dst, dtype=np.int64)
+    if src.shape != dst.shape:
+        raise ValueError("src and dst differ in length")
+    v = None if vertices is None else np.ascontiguousarray(vertices, dtype=np.int64)
+    out = _vp()
+    _check(_subgraph_build(int(n_full), _np_ptr(src), _np_ptr(dst), src.size,
+                           _np_ptr(v) if v is not None else None,
+                           0 if v is None else v.size, C.byref(out)))
+    return Graph(out.value)
+
+
+class Reduced:
+    """Output of the redundancy reduction (owned by the library)."""
+
+    def __init__(self, handle):
+        self._h = _vp(handle)
+
+    def __del__(self):
+        if getattr(self, "_h", None) and self._h.value:
+            _reduced_free(self._h)
+            self._h = _vp()
+
+    def info(self):
+        n, naux, rounds, nnz = _i32(), _i32(), _i32(), _i64()
+        rp, cl, pr, ro, dg = _pi32(), _pi32(), _pi32(), _pi32(), _pi32()
+        st = C.POINTER(RrRound)()
+        _check(_reduced_info(self._h, C.byref(n), C.byref(naux), C.byref(rounds),
+                             C.byref(nnz), C.byref(rp), C.byref(cl), C.byref(pr),
+                             C.byref(ro), C.byref(st), C.byref(dg)))
+        n, naux, rounds, nnz = n.value, naux.value, rounds.value, nnz.value
+
+        def arr(p, k):
+            return np.ctypeslib.as_array(p, shape=(k,)).copy() if k else np.zeros(0, np.int32)
+        stats = [(st[i].matched, st[i].weight_sum, st[i].nnz, st[i].num_add)
+                 for i in range(rounds)]
+        return dict(n=n, naux=naux, rounds=rounds, nnz=nnz,
+                    rowptr=arr(rp, n + 1), col=arr(cl, nnz),
+                    pairs=arr(pr, 2 * naux).reshape(-1, 2),
+                    round_offsets=arr(ro, rounds + 1), stats=stats, deg=arr(dg, n))
+
+
+def redundancy_reduce(g: Graph, theta=2, max_rounds=5, max_aux=-1, num_threads=0) -> Reduced:
+    p = RrParams(int(theta), int(max_rounds), int(max_aux), int(num_threads), 0)
+    out = _vp()
+    _check(_reduce(g._h, C.byref(p), C.byref(out)))
+    return Reduced(out.value)
+
+
+def image_bytes(r: Reduced, seg_len=0) -> int:
+    b = _sz()
+    _check(_image_bytes(r._h, int(seg_len), C.byref(b)))
+    return b.value
+
+
+def pack(r: Reduced, buf_ptr: int, nbytes: int, seg_len=0):
+    _check(_pack(r._h, int(seg_len), _vp(buf_ptr), nbytes))
+
+
+def describe(host_ptr: int, nbytes: int, dev_ptr: int) -> DGraph:
+    d = DGraph()
+    _check(_describe(_vp(host_ptr), nbytes, _vp(dev_ptr), C.byref(d)))
+    return d
+
+
+# ---------------------------------------------------------------- device side
+
+def _torch():
+    import torch
+    return torch
+
+
+def _stream(stream):
+    if stream is None:
+        return _vp(_torch().cuda.current_stream().cuda_stream)
+    return _vp(stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream))
+
+
+def _ptr(t):
+    return None if t is None else _vp(t.data_ptr())
+
+
+def _ld(t):
+    if t is None:
+        return 0
+    if t.dim() != 2 or t.stride(1) != 1:
+        raise ValueError("matrix must be 2-D with unit column stride")
+    return t.stride(0)
+
+
+class DeviceGraph:
+    """A reduced graph resident in device memory (torch-owned buffer)."""
+
+    def __init__(self, reduced: Reduced, seg_len=0, stream=None, device="cuda"):
+        torch = _torch()
+        nbytes = image_bytes(reduced, seg_len)
+        self.host = torch.empty(nbytes, dtype=torch.uint8, pin_memory=True)
+        pack(reduced, self.host.data_ptr(), nbytes, seg_len)
+        self.dev = torch.empty(nbytes + 256, dtype=torch.uint8, device=device)
+        off = (-self.dev.data_ptr()) % 256
+        self.dev_view = self.dev[off:off + nbytes]
+        self.nbytes = nbytes
+        self.desc = DGraph()
+        _check(_upload(_vp(self.host.data_ptr()), nbytes, _vp(self.dev_view.data_ptr()),
+                       C.byref(self.desc), _stream(stream)))
+
+    @property
+    def n(self):
+        return self.desc.n
+
+
+def alloc_ws(nbytes, device="cuda"):
+    """256-byte-aligned device workspace as a uint8 tensor view."""
+    torch = _torch()
+    raw = torch.empty(int(nbytes) + 256, dtype=torch.uint8, device=device)
+    off = (-raw.data_ptr()) % 256
+    view = raw[off:off + int(nbytes)]
+    view._raw = raw
+    return view
+
+
+def scratch_bytes(dg: DeviceGraph | None, max_width: int, n: int = 0) -> int:
+    b = _sz()
+    _check(_scratch_bytes(C.byref(dg.desc) if dg is not None else None, n, int(max_width),
+                          C.byref(b)))
+    return b.value
+
+
+def aggregate(dg, mode, X, Y, ws, stream=None):
+    _check(_aggregate(C.byref(dg.desc), mode, X.shape[1], _ptr(X), _ld(X), _ptr(Y), _ld(Y),
+                      _ptr(ws), ws.numel(), _stream(stream)))
+
+
+def layer_fwd(dg, H_in, W_self, W_neigh, bias, AH, H_out, ws, precision=PREC_FP32,
+              stream=None):
+    F, h = W_self.shape
+    _check(_layer_fwd(C.byref(dg.desc), F, h, _ptr(H_in), _ld(H_in), _ptr(W_self),
+                      _ptr(W_neigh), _ptr(bias), _ptr(AH), _ld(AH), _ptr(H_out),
+                      _ld(H_out), precision, _ptr(ws), ws.numel(), _stream(stream)))
+
+
+def classifier_fwd(H, K, W_cls, b_cls, logits, precision=PREC_FP32, stream=None):
+    n = H.shape[0]
+    Cn = W_cls.shape[1]
+    _check(_classifier_fwd(n, K, Cn, _ptr(H), _ld(H), _ptr(W_cls), _ptr(b_cls),
+                           _ptr(logits), _ld(logits), precision, _stream(stream)))
+
+
+def loss(kind, logits, C_, labels, dlogits, loss_out, ws, stream=None):
+    n = logits.shape[0]
+    _check(_loss(n, C_, kind, _ptr(logits), _ld(logits), _ptr(labels), _ptr(dlogits),
+                 _ld(dlogits), _ptr(loss_out), _ptr(ws), ws.numel(), _stream(stream)))
+
+
+def classifier_bwd(dZ, C_, H, K, W_cls, b_cls, lr, G_out, dW_out, db_out, ws,
+                   precision=PREC_FP32, stream=None):
+    n = dZ.shape[0]
+    _check(_classifier_bwd(n, K, C_, _ptr(dZ), _ld(dZ), _ptr(H), _ld(H), _ptr(W_cls),
+                           _ptr(b_cls), float(lr), _ptr(G_out), _ld(G_out), _ptr(dW_out),
+                           _ptr(db_out), precision, _ptr(ws), ws.numel(), _stream(stream)))
+
+
+def layer_bwd(dg, G, H_in, AH, W_self, W_neigh, bias, lr, G_in, dW_self, dW_neigh, db, ws,
+              precision=PREC_FP32, stream=None):
+    F, h = W_self.shape
+    _check(_layer_bwd(C.byref(dg.desc), F, h, _ptr(G), _ld(G), _ptr(H_in), _ld(H_in),
+                      _ptr(AH), _ld(AH), _ptr(W_self), _ptr(W_neigh), _ptr(bias),
+                      float(lr), _ptr(G_in), _ld(G_in), _ptr(dW_self), _ptr(dW_neigh),
+                      _ptr(db), precision, _ptr(ws), ws.numel(), _stream(stream)))
+
+
+def model_desc(L, f_in, h, C_, loss_kind, ld_x, precision=PREC_FP32, has_bias=False):
+    return ModelDesc(L, f_in, h, C_, loss_kind, precision, 1 if has_bias else 0, 0, ld_x)
+
+
+def make_params(W_self, W_neigh, W_cls, b=None, b_cls=None):
+    p = Params()
+    for l, (ws_, wn_) in enumerate(zip(W_self, W_neigh)):
+        p.W_self[l] = None if ws_ is None else ws_.data_ptr()
+        p.W_neigh[l] = None if wn_ is None else wn_.data_ptr()
+        if b is not None and b[l] is not None:
+            p.b[l] = b[l].data_ptr()
+    p.W_cls = None if W_cls is None else W_cls.data_ptr()
+    p.b_cls = None if b_cls is None else b_cls.data_ptr()
+    return p
+
+
+def workspace_layout(dg, desc) -> WsLayout:
+    out = WsLayout()
+    _check(_ws_layout(C.byref(dg.desc), C.byref(desc), C.byref(out)))
+    return out
+
+
+def workspace_bytes(dg, desc) -> int:
+    b = _sz()
+    _check(_ws_bytes(C.byref(dg.desc), C.byref(desc), C.byref(b)))
+    return b.value
+
+
+def train_step(dg, desc, params, X, labels, lr, loss_out, ws, grads=None, stream=None):
+    _check(_train_step(C.byref(dg.desc), C.byref(desc), C.byref(params), _ptr(X),
+                       _ptr(labels), float(lr), _ptr(loss_out),
+                       C.byref(grads) if grads is not None else None, _ptr(ws), ws.numel(),
+                       _stream(stream)))

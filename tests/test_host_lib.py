@@ -1,0 +1,237 @@
+"""The C-ABI library on the CPU: symbol exports, and the host preprocessing
+(subgraph build, redundancy reduction, device-image packing) bit-exact
+against the oracle. No GPU needed: these entry points never touch HIP."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+from oracle import graph as gr
+from oracle import reduction as rd
+from paper_2001_02498_amd import synth
+
+gcn = pytest.importorskip("paper_2001_02498_amd.gcn")
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _declared_symbols():
+    txt = open(os.path.join(ROOT, "include", "gcn_act.h")).read()
+    txt = re.sub(r"/\*.*?\*/", "", txt, flags=re.S)
+    return sorted(set(re.findall(r"\b(gcn_[a-z_]+)\s*\(", txt)))
+
+
+def test_library_exports_every_declared_symbol():
+    lib = ctypes.CDLL(gcn.LIB_PATH)
+    syms = _declared_symbols()
+    assert len(syms) >= 20
+    for s in syms:
+        assert hasattr(lib, s), s
+    assert sorted(gcn.EXPORTS) == syms
+
+
+def test_abi_version():
+    assert gcn.abi_version() == gcn.ABI_VERSION
+
+
+def _same_graph(lib_graph, rp, cl):
+    r2, c2 = lib_graph.csr()
+    assert np.array_equal(r2, rp) and np.array_equal(c2, cl)
+
+
+def test_subgraph_build_matches_oracle():
+    rng = np.random.default_rng(17)
+    for trial in range(60):
+        n = int(rng.integers(1, 80))
+        s, d = synth.random_edges(n, int(rng.integers(0, 6 * n)), rng)
+        rp, cl = gr.subgraph_build(n, s, d)
+        _same_graph(gcn.subgraph_build(n, s, d), rp, cl)
+        if n > 3:
+            sub = rng.choice(n, size=n // 2, replace=False)
+            rp, cl = gr.subgraph_build(n, s, d, vertices=sub)
+            _same_graph(gcn.subgraph_build(n, s, d, vertices=sub), rp, cl)
+
+
+def test_subgraph_build_figures(golden):
+    g1 = golden("fig1_aggregation.json")
+    g2 = golden("fig2_reduction.json")
+    e = np.array(g1["edges"])
+    g = gcn.subgraph_build(g1["n"], e[:, 0], e[:, 1])
+    rp, cl = g.csr()
+    assert gr.rows_of(rp, cl) == g1["neighbours"]
+    g = gcn.subgraph_build(g1["n"], e[:, 0], e[:, 1], vertices=g2["subset"])
+    rp, cl = g.csr()
+    assert gr.rows_of(rp, cl) == g2["neighbours_before"]
+
+
+def test_subgraph_build_errors():
+    with pytest.raises(gcn.GcnError) as ei:
+        gcn.subgraph_build(3, [0, 7], [1, 2])
+    assert ei.value.code == gcn.E_INVALID_ARG and "out of range" in str(ei.value)
+    with pytest.raises(gcn.GcnError):
+        gcn.subgraph_build(3, [0], [1], vertices=[1, 1])
+    with pytest.raises(gcn.GcnError):
+        gcn.subgraph_build(3, [0], [1], vertices=[5])
+    with pytest.raises(gcn.GcnError):
+        gcn.subgraph_build(-1, [], [])
+    g = gcn.subgraph_build(0, [], [])
+    assert g.n == 0 and g.nnz == 0
+
+
+def _compare_reduction(lib_red, ora):
+    info = lib_red.info()
+    assert info["naux"] == ora["naux"]
+    assert np.array_equal(info["pairs"], ora["pairs"].astype(np.int32).reshape(-1, 2))
+    assert np.array_equal(info["round_offsets"], ora["round_offsets"])
+    assert np.array_equal(info["rowptr"], ora["rowptr"])
+    assert np.array_equal(info["col"], ora["col"])
+    assert [tuple(s) for s in info["stats"]] == [tuple(s) for s in ora["stats"]]
+    return info
+
+
+def test_reduction_figures_exact(golden):
+    g1 = golden("fig1_aggregation.json")
+    g2 = golden("fig2_reduction.json")
+    e = np.array(g1["edges"])
+    g = gcn.subgraph_build(g1["n"], e[:, 0], e[:, 1], vertices=g2["subset"])
+    info = gcn.redundancy_reduce(g, theta=1).info()
+    assert info["pairs"].tolist() == g2["pairs"]
+    assert info["rowptr"].tolist() == g2["rowptr"]
+    assert info["col"].tolist() == g2["col"]
+    want = golden("fig1_reduction.json")
+    g = gcn.subgraph_build(g1["n"], e[:, 0], e[:, 1])
+    info = gcn.redundancy_reduce(g, theta=1).info()
+    assert info["pairs"].tolist() == want["pairs"]
+    assert info["rowptr"].tolist() == want["rowptr"]
+    assert info["col"].tolist() == want["col"]
+    assert info["deg"].tolist() == [3, 2, 3, 4, 2, 2]
+
+
+def test_reduction_random_graphs_bit_exact():
+    rng = np.random.default_rng(23)
+    for trial in range(200):
+        n = int(rng.integers(1, 70))
+        s, d = synth.random_edges(n, int(rng.integers(0, 10 * n)), rng)
+        rp, cl = gr.subgraph_build(n, s, d)
+        theta = int(rng.integers(0, 4))
+        rounds = int(rng.integers(0, 7))
+        max_aux = int(rng.integers(-1, 12))
+        ora = rd.reduce(rp, cl, theta=theta, max_rounds=rounds, max_aux=max_aux)
+        red = gcn.redundancy_reduce(gcn.subgraph_build(n, s, d), theta=theta,
+                                    max_rounds=rounds, max_aux=max_aux)
+        _compare_reduction(red, ora)
+
+
+@pytest.mark.parametrize("name", ["tiny", "ppi8k", "stream8k"])
+def test_reduction_workloads_bit_exact(name):
+    wl = synth.WORKLOADS[name]
+    inp = synth.make_inputs(wl)
+    rp, cl = gr.subgraph_build(wl.n, inp.src, inp.dst)
+    ora = rd.reduce(rp, cl, theta=wl.theta, max_rounds=wl.rounds, max_aux=wl.max_aux)
+    g = gcn.subgraph_build(wl.n, inp.src, inp.dst)
+    _same_graph(g, rp, cl)
+    red = gcn.redundancy_reduce(g, theta=wl.theta, max_rounds=wl.rounds,
+                                max_aux=wl.max_aux)
+    info = _compare_reduction(red, ora)
+    assert info["naux"] > 0
+
+
+@pytest.mark.slow
+def test_reduction_yelp_bit_exact():
+    wl = synth.WORKLOADS["yelp10k"]
+    inp = synth.make_inputs(wl)
+    rp, cl = gr.subgraph_build(wl.n, inp.src, inp.dst)
+    ora = rd.reduce(rp, cl, theta=wl.theta, max_rounds=wl.rounds, max_aux=wl.max_aux)
+    red = gcn.redundancy_reduce(gcn.subgraph_build(wl.n, inp.src, inp.dst),
+                                theta=wl.theta, max_rounds=wl.rounds, max_aux=wl.max_aux)
+    _compare_reduction(red, ora)
+
+
+def test_reduction_independent_of_thread_count():
+    wl = synth.WORKLOADS["ppi8k"]
+    inp = synth.make_inputs(wl)
+    g = gcn.subgraph_build(wl.n, inp.src, inp.dst)
+    a = gcn.redundancy_reduce(g, num_threads=1).info()
+    b = gcn.redundancy_reduce(g, num_threads=7).info()
+    for k in ("pairs", "round_offsets", "rowptr", "col"):
+        assert np.array_equal(a[k], b[k])
+
+
+def test_reduction_errors():
+    g = gcn.subgraph_build(4, [0, 1], [1, 2])
+    with pytest.raises(gcn.GcnError):
+        gcn.redundancy_reduce(g, theta=-1)
+    with pytest.raises(gcn.GcnError):
+        gcn.redundancy_reduce(g, max_rounds=gcn.MAX_ROUNDS + 1)
+    with pytest.raises(gcn.GcnError):
+        gcn.redundancy_reduce(g, num_threads=-2)
+
+
+def _unpack_image(buf, nbytes):
+    """Reads the packed image's sections through gcn_graph_describe, using
+    the host buffer as the 'device' address (CPU-only inspection)."""
+    addr = buf.ctypes.data
+    d = gcn.describe(addr, nbytes, addr)
+
+    def view(ptr, count, dtype):
+        off = ptr - addr
+        return np.frombuffer(buf, dtype=dtype, count=count, offset=off)
+    return d, dict(
+        rowptr=view(d.rowptr, d.n + 1, np.int32),
+        col=view(d.col, d.nnz, np.int32) if d.nnz else np.zeros(0, np.int32),
+        pairs=view(d.pairs, 2 * d.naux, np.int32) if d.naux else np.zeros(0, np.int32),
+        inv_deg=view(d.inv_deg, d.n, np.float32),
+        seg=view(d.seg, 4 * d.nseg, np.int32).reshape(-1, 4),
+        longrows=view(d.longrows, 4 * d.nlong, np.int32).reshape(-1, 4) if d.nlong
+        else np.zeros((0, 4), np.int32))
+
+
+@pytest.mark.parametrize("seg_len", [0, 1, 3, 64])
+def test_device_image_work_list(seg_len):
+    wl = synth.WORKLOADS["tiny"]
+    inp = synth.make_inputs(wl)
+    g = gcn.subgraph_build(wl.n, inp.src, inp.dst)
+    red = gcn.redundancy_reduce(g)
+    info = red.info()
+    nbytes = gcn.image_bytes(red, seg_len)
+    buf = np.zeros(nbytes + 256, dtype=np.uint8)
+    off = (-buf.ctypes.data) % 256
+    buf = buf[off:off + nbytes]
+    gcn.pack(red, buf.ctypes.data, nbytes, seg_len)
+    d, sec = _unpack_image(buf, nbytes)
+    L = seg_len or 64
+    assert d.seg_len == L and d.n == wl.n and d.naux == info["naux"]
+    assert np.array_equal(sec["rowptr"], info["rowptr"])
+    assert np.array_equal(sec["col"], info["col"])
+    assert np.array_equal(sec["pairs"], info["pairs"].ravel())
+    deg = info["deg"]
+    want_inv = np.where(deg > 0, 1.0 / np.maximum(deg, 1), 0.0).astype(np.float32)
+    assert np.array_equal(sec["inv_deg"], want_inv)
+    assert list(d.round_offsets[:d.rounds + 1]) == info["round_offsets"].tolist()
+    # every list entry covered exactly once; segments never exceed seg_len;
+    # split lists write consecutive slots recorded in the long-row table
+    covered = np.zeros(info["nnz"], dtype=np.int64)
+    rows_seen = np.zeros(wl.n, dtype=np.int64)
+    slots = {}
+    for row, b, e, slot in sec["seg"]:
+        assert info["rowptr"][row] <= b <= e <= info["rowptr"][row + 1]
+        assert e - b <= L
+        covered[b:e] += 1
+        rows_seen[row] += 1
+        if slot >= 0:
+            slots.setdefault(row, []).append(slot)
+    assert np.all(covered == 1)
+    assert np.all(rows_seen >= 1)
+    lens = np.diff(info["rowptr"])
+    assert d.max_row == lens.max()
+    assert d.nlong == int((lens > L).sum())
+    for row, first, ns, _ in sec["longrows"]:
+        assert slots[row] == list(range(first, first + ns))
+    assert d.nslots == sum(len(v) for v in slots.values())
+    # image corruption is rejected
+    bad = buf.copy()
+    bad[:4] = 0
+    with pytest.raises(gcn.GcnError):
+        gcn.describe(bad.ctypes.data, nbytes, bad.ctypes.data)
