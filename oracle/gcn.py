@@ -154,8 +154,14 @@ def forward(rowptr, col, X, params):
     return dict(H=Hs, AH=AHs, Z=Zs, logits=logits)
 
 
-def backward(rowptr, col, params, fw, dlogits):
+def backward(rowptr, col, params, fw, dlogits, masks=None):
     """Eq. 2a-2c for every layer, plus the classifier's gradients.
+
+    masks: optional list of 0/1 arrays, one per layer, taking the ReLU
+    decision [Z_l > 0] from elsewhere. The paper computes in single
+    precision (Section 6); a comparison against a float32 implementation
+    passes the float32 decision here so both sides mask the same entries
+    (an entry with |Z| near 1e-7 may otherwise fall on different sides).
 
     Returns dict with dW_self, dW_neigh, db (lists, layer order), dW_cls,
     db_cls, G (masked gradients per layer) and dH (dL/dH_l for l = 1..L).
@@ -170,7 +176,8 @@ def backward(rowptr, col, params, fw, dlogits):
     dH = dZc @ Wc.T
     for l in range(L - 1, -1, -1):
         out["dH"][l] = dH
-        G = dH * (fw["Z"][l] > 0.0)
+        mask = fw["Z"][l] > 0.0 if masks is None else np.asarray(masks[l], bool)
+        G = dH * mask
         h = G.shape[1] // 2
         Gs, Gn = G[:, :h], G[:, h:]
         out["G"][l] = G
@@ -202,11 +209,11 @@ def sgd(params, grads, lr):
     return new
 
 
-def train_step(rowptr, col, X, params, labels, loss_kind, lr):
+def train_step(rowptr, col, X, params, labels, loss_kind, lr, masks=None):
     """One forward + loss + backward + gradient-descent step."""
     fw = forward(rowptr, col, X, params)
     loss, dlogits = loss_and_grad(loss_kind, fw["logits"], labels)
-    grads = backward(rowptr, col, params, fw, dlogits)
+    grads = backward(rowptr, col, params, fw, dlogits, masks)
     new = sgd(params, grads, lr)
     return dict(fw=fw, loss=loss, dlogits=dlogits, grads=grads, params=new)
 

@@ -1,0 +1,180 @@
+"""GPU parity of the full training step (gcn_train_step) against the oracle,
+on the seeded workloads at full size and on small ragged cases.
+
+The ReLU decisions of the backward pass are taken from the kernel's float32
+activations on both sides (the paper computes in single precision); the
+forward activations themselves are compared within tolerance. The updated
+weights are compared as W_new - W_old against -lr dW, with the float32
+rounding of storing W added to the tolerance (lr dW can sit below the
+spacing of W's float32 values)."""
+import numpy as np
+import pytest
+
+from oracle import gcn as og
+from oracle import graph as gr
+from paper_2001_02498_amd import synth
+from tests.gpu_helpers import FP32_TOL, GraphCase, dev, need_gpu, rel, say, torch
+
+pytestmark = pytest.mark.gpu
+
+
+class StepRun:
+    """Runs one gcn_train_step on a workload and keeps every tensor."""
+
+    def __init__(self, wl, inp=None, bias=False, seg_len=0):
+        from paper_2001_02498_amd import gcn
+        self.gcn, self.wl = gcn, wl
+        self.inp = inp or synth.make_inputs(wl)
+        rounds = wl.rounds if wl.reduce else 0
+        self.case = GraphCase(wl.n, self.inp.src, self.inp.dst, theta=wl.theta,
+                              rounds=rounds, max_aux=wl.max_aux, seg_len=seg_len)
+        rng = np.random.default_rng(7)
+        self.b = [(rng.standard_normal(2 * wl.h) * 0.1).astype(np.float32)
+                  for _ in range(wl.L)] if bias else None
+        self.bc = (rng.standard_normal(wl.C) * 0.1).astype(np.float32) if bias else None
+        self.bias = bias
+
+    def params_dev(self):
+        wl, inp = self.wl, self.inp
+        Ws = [dev(w, wl.h) for w in inp.W_self]
+        Wn = [dev(w, wl.h) for w in inp.W_neigh]
+        Wc = torch.from_numpy(inp.W_cls.copy()).cuda()
+        b = [dev(x) for x in self.b] if self.bias else None
+        bc = dev(self.bc) if self.bias else None
+        return Ws, Wn, Wc, b, bc
+
+    def run(self):
+        gcn, wl, inp = self.gcn, self.wl, self.inp
+        X = dev(inp.X)
+        self.X = X
+        Ws, Wn, Wc, b, bc = self.params_dev()
+        self.dev_params = (Ws, Wn, Wc, b, bc)
+        P = gcn.make_params(Ws, Wn, Wc, b, bc)
+        gWs = [torch.zeros_like(w) for w in Ws]
+        gWn = [torch.zeros_like(w) for w in Wn]
+        gWc = torch.zeros_like(Wc)
+        gb = [torch.zeros_like(x) for x in b] if self.bias else None
+        gbc = torch.zeros_like(bc) if self.bias else None
+        self.grads_dev = (gWs, gWn, gWc, gb, gbc)
+        Gp = gcn.make_params(gWs, gWn, gWc, gb, gbc)
+        desc = gcn.model_desc(wl.L, wl.f_in, wl.h, wl.C, wl.loss, X.stride(0),
+                              has_bias=self.bias)
+        self.layout = gcn.workspace_layout(self.case.dg, desc)
+        ws = gcn.alloc_ws(gcn.workspace_bytes(self.case.dg, desc))
+        self.ws = ws
+        labels = torch.from_numpy(inp.labels).cuda()
+        loss = torch.zeros(1, device="cuda")
+        say("train_step", wl.name, "n", wl.n, "L", wl.L, "f_in", wl.f_in, "h", wl.h,
+            "C", wl.C, "naux", self.case.info["naux"], "bias", self.bias)
+        gcn.train_step(self.case.dg, desc, P, X, labels, wl.lr, loss, ws, grads=Gp)
+        torch.cuda.synchronize()
+        self.loss = loss.item()
+        return self
+
+    def act(self, off, rows, cols, ld):
+        t = self.ws[off:off + 4 * rows * ld].view(torch.float32).view(rows, ld)
+        return t[:, :cols]
+
+    def oracle(self):
+        wl, inp = self.wl, self.inp
+        lay = self.layout
+        masks = [self.act(lay.H[l], wl.n, 2 * wl.h, lay.ld_H).cpu().numpy() > 0
+                 for l in range(wl.L)]
+        params = dict(W_self=inp.W_self, W_neigh=inp.W_neigh,
+                      b=self.b if self.bias else [None] * wl.L, W_cls=inp.W_cls,
+                      b_cls=self.bc)
+        return og.train_step(self.case.rp, self.case.cl, inp.X, params, inp.labels,
+                             wl.loss, wl.lr, masks=masks)
+
+
+def _update_err(new_dev, old, d_ref, lr):
+    """max|(W_new - W_old) - (-lr dW)| relative to max|lr dW|, after removing
+    the half-ulp of float32 storage of W_new."""
+    new = new_dev.detach().cpu().double().numpy()
+    want = old.astype(np.float64) - lr * d_ref
+    ulp = np.spacing(np.abs(want).astype(np.float32)).astype(np.float64)
+    excess = np.maximum(np.abs(new - want) - ulp, 0.0)
+    return float(excess.max() / max(np.abs(lr * d_ref).max(), 1e-30))
+
+
+def check_step(run, tol=FP32_TOL):
+    ref = run.oracle()
+    wl, lay = run.wl, run.layout
+    errs = {}
+    for l in range(wl.L):
+        F = wl.f_in if l == 0 else 2 * wl.h
+        errs[f"AH{l}"] = rel(run.act(lay.AH[l], wl.n, F, lay.ld_AH[l]), ref["fw"]["AH"][l])
+        errs[f"H{l}"] = rel(run.act(lay.H[l], wl.n, 2 * wl.h, lay.ld_H), ref["fw"]["H"][l + 1])
+    errs["logits"] = rel(run.act(lay.logits, wl.n, wl.C, lay.ld_C), ref["fw"]["logits"])
+    errs["dlogits"] = rel(run.act(lay.dlogits, wl.n, wl.C, lay.ld_C), ref["dlogits"])
+    errs["loss"] = abs(run.loss - ref["loss"]) / abs(ref["loss"])
+    # masked gradients still resident: the last two written (layers 0 and 1)
+    for l in range(min(2, wl.L)):
+        errs[f"G{l}"] = rel(run.act(lay.G[l], wl.n, 2 * wl.h, lay.ld_H), ref["grads"]["G"][l])
+    gWs, gWn, gWc, gb, gbc = run.grads_dev
+    Ws, Wn, Wc, b, bc = run.dev_params
+    g = ref["grads"]
+    for l in range(wl.L):
+        errs[f"dWs{l}"] = rel(gWs[l], g["dW_self"][l])
+        errs[f"dWn{l}"] = rel(gWn[l], g["dW_neigh"][l])
+        errs[f"Ws{l}"] = rel(Ws[l], ref["params"]["W_self"][l])
+        errs[f"dWs_upd{l}"] = _update_err(Ws[l], run.inp.W_self[l], g["dW_self"][l], wl.lr)
+        errs[f"dWn_upd{l}"] = _update_err(Wn[l], run.inp.W_neigh[l], g["dW_neigh"][l], wl.lr)
+        if run.bias:
+            errs[f"db{l}"] = rel(gb[l], g["db"][l])
+            errs[f"db_upd{l}"] = _update_err(b[l], run.b[l], g["db"][l], wl.lr)
+    errs["dWc"] = rel(gWc, g["dW_cls"])
+    errs["dWc_upd"] = _update_err(Wc, run.inp.W_cls, g["dW_cls"], wl.lr)
+    if run.bias:
+        errs["dbc"] = rel(gbc, g["db_cls"])
+    worst = max(errs, key=errs.get)
+    say("max error", worst, errs[worst])
+    bad = {k: v for k, v in errs.items() if not v < tol}
+    assert not bad, bad
+    return errs
+
+
+def test_step_tiny_reduced():
+    need_gpu()
+    check_step(StepRun(synth.WORKLOADS["tiny"]).run())
+
+
+@pytest.mark.parametrize("L,loss,bias", [(2, synth.SIGMOID_BCE, True),
+                                         (3, synth.SOFTMAX_CE, False),
+                                         (1, synth.SOFTMAX_CE, True)])
+def test_step_ragged_small(L, loss, bias):
+    need_gpu()
+    wl = synth.small_workload(437, 9, L, 29, 36, 7, loss, (L, loss, int(bias)))
+    check_step(StepRun(wl, bias=bias, seg_len=4).run())
+
+
+@pytest.mark.parametrize("name", ["ppi8k", "reddit8k", "yelp10k", "stream8k"])
+def test_step_workloads(name):
+    need_gpu()
+    check_step(StepRun(synth.WORKLOADS[name]).run())
+
+
+def test_step_ppi_direct_matches_reduced():
+    """The same step on G_s and on G_s^#: both within tolerance of the oracle
+    and of each other."""
+    need_gpu()
+    import dataclasses
+    wl = synth.WORKLOADS["ppi8k"]
+    inp = synth.make_inputs(wl)
+    a = StepRun(dataclasses.replace(wl, reduce=False), inp=inp).run()
+    b = StepRun(wl, inp=inp).run()
+    assert a.case.info["naux"] == 0 and b.case.info["naux"] > 0
+    assert abs(a.loss - b.loss) <= 1e-5 * abs(a.loss)
+    for l in range(wl.L):
+        assert rel(a.grads_dev[0][l], b.grads_dev[0][l].cpu().double().numpy()) < FP32_TOL
+
+
+def test_step_deterministic():
+    need_gpu()
+    wl = synth.WORKLOADS["tiny"]
+    a = StepRun(wl).run()
+    b = StepRun(wl).run()
+    assert a.loss == b.loss
+    for x, y in zip(a.grads_dev[0] + a.grads_dev[1] + [a.grads_dev[2]],
+                    b.grads_dev[0] + b.grads_dev[1] + [b.grads_dev[2]]):
+        assert torch.equal(x, y)
