@@ -326,6 +326,35 @@ int gcn_train_step(const gcn_dgraph* g, const gcn_model_desc* desc,
                    const gcn_params* grads, void* ws, size_t ws_bytes,
                    gcn_stream_t stream);
 
+/* ---------------------------------------------------- launch timing
+ * Tracing for measurement: when enabled, every kernel launch made by the
+ * entry points above is bracketed by two HIP events on its own stream and
+ * labelled with its kernel class and algorithmic work.
+ * gcn_profile_enable - start timing with room for `capacity` launches
+ *   (1..2^20); clears earlier records; creates the events (host call, not
+ *   for use while another thread launches through the library).
+ * gcn_profile_disable - stop timing new launches (records are kept).
+ * gcn_profile_read - wait for the timed launches and report, per kernel
+ *   class with at least one launch: launches, total / min / max
+ *   milliseconds, and the summed algorithmic flops and bytes (bytes: each
+ *   operand element read or written once, list gathers counted per list
+ *   entry). Writes up to max_entries entries and sets *count to the number
+ *   of classes; reset != 0 clears the records. Returns GCN_E_INTERNAL if
+ *   launches went untimed because the capacity ran out.
+ */
+typedef struct {
+    int32_t kind;
+    int32_t launches;
+    const char* name;     /* static string, e.g. "gemm_dw" */
+    double total_ms, min_ms, max_ms;
+    double flops, bytes;
+} gcn_profile_entry;
+
+int gcn_profile_enable(int32_t capacity);
+int gcn_profile_disable(void);
+int gcn_profile_read(gcn_profile_entry* out, int32_t max_entries,
+                     int32_t* count, int32_t reset);
+
 #ifdef __cplusplus
 }
 #endif

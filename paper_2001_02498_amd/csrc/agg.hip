@@ -12,6 +12,7 @@
 // in slot order, so the result is deterministic and no row serialises a
 // whole wavefront for thousands of neighbours.
 #include "kernels.h"
+#include "prof.h"
 
 namespace gcn {
 namespace {
@@ -263,6 +264,8 @@ hipError_t launch_pair_sums(const int32_t* pairs, int32_t k0, int32_t k1,
     if (k1 <= k0 || F <= 0) return hipSuccess;
     const Shape sh = pick_shape(F);
     const dim3 grid(blocks_for(k1 - k0, sh.gl)), block(kBlock);
+    const double np_ = (double)(k1 - k0);
+    ProfScope prof(s, K_PAIR_SUMS, np_ * F * (prescale ? 3.0 : 1.0), np_ * (12.0 * F + 8.0));
 #define GCN_LAUNCH_PAIR(GL_, NCH_)                                                  \
     if (sh.gl == GL_ && sh.nch == NCH_) {                                           \
         if (prescale)                                                               \
@@ -283,35 +286,47 @@ hipError_t launch_list_sums(const gcn_dgraph* g, RowSource src, bool prescale,
                             float* partial, int64_t ldp, int32_t F,
                             hipStream_t s) {
     if (g->n <= 0 || F <= 0) return hipSuccess;
+    if (prescale == postscale) return hipErrorInvalidValue;
     const Shape sh = pick_shape(F);
     const int4* seg = reinterpret_cast<const int4*>(g->seg);
     const int4* lr = reinterpret_cast<const int4*>(g->longrows);
     const dim3 block(kBlock);
     const dim3 grid(blocks_for(g->nseg, sh.gl));
     const dim3 gfix(blocks_for(g->nlong, sh.gl));
+    const double nnz = (double)g->nnz, n = (double)g->n;
+    {
+        // algorithmic: one gather per list entry, its id, one write per row
+        ProfScope prof(s, K_LIST_SUMS, nnz * F * (prescale ? 2.0 : 1.0) + (postscale ? n * F : 0.0),
+                       4.0 * F * nnz + 4.0 * nnz + 4.0 * F * n);
 #define GCN_LAUNCH_LIST(GL_, NCH_)                                                    \
+        if (sh.gl == GL_ && sh.nch == NCH_) {                                         \
+            if (prescale)                                                             \
+                list_sums_kernel<GL_, NCH_, true, false><<<grid, block, 0, s>>>(      \
+                    seg, g->nseg, g->col, src, g->inv_deg, Y, ldy, partial, ldp, F);  \
+            else                                                                      \
+                list_sums_kernel<GL_, NCH_, false, true><<<grid, block, 0, s>>>(      \
+                    seg, g->nseg, g->col, src, g->inv_deg, Y, ldy, partial, ldp, F);  \
+        } else
+        GCN_SHAPES(GCN_LAUNCH_LIST) { return hipErrorInvalidValue; }
+#undef GCN_LAUNCH_LIST
+        hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+    }
+    if (g->nlong == 0) return hipSuccess;
+    ProfScope prof(s, K_LIST_FIXUP, (double)g->nslots * F,
+                   4.0 * F * ((double)g->nslots + g->nlong));
+#define GCN_LAUNCH_FIX(GL_, NCH_)                                                     \
     if (sh.gl == GL_ && sh.nch == NCH_) {                                             \
-        if (prescale && !postscale)                                                   \
-            list_sums_kernel<GL_, NCH_, true, false><<<grid, block, 0, s>>>(          \
-                seg, g->nseg, g->col, src, g->inv_deg, Y, ldy, partial, ldp, F);      \
-        else if (!prescale && postscale)                                              \
-            list_sums_kernel<GL_, NCH_, false, true><<<grid, block, 0, s>>>(          \
-                seg, g->nseg, g->col, src, g->inv_deg, Y, ldy, partial, ldp, F);      \
-        else                                                                          \
-            return hipErrorInvalidValue;                                              \
-        hipError_t e = hipGetLastError();                                             \
-        if (e != hipSuccess || g->nlong == 0) return e;                               \
         if (postscale)                                                                \
             fixup_kernel<GL_, NCH_, true><<<gfix, block, 0, s>>>(                     \
                 lr, g->nlong, partial, ldp, g->inv_deg, Y, ldy, F);                   \
         else                                                                          \
             fixup_kernel<GL_, NCH_, false><<<gfix, block, 0, s>>>(                    \
                 lr, g->nlong, partial, ldp, g->inv_deg, Y, ldy, F);                   \
-        return hipGetLastError();                                                     \
-    }
-    GCN_SHAPES(GCN_LAUNCH_LIST)
-#undef GCN_LAUNCH_LIST
-    return hipErrorInvalidValue;
+    } else
+    GCN_SHAPES(GCN_LAUNCH_FIX) { return hipErrorInvalidValue; }
+#undef GCN_LAUNCH_FIX
+    return hipGetLastError();
 }
 
 }  // namespace gcn

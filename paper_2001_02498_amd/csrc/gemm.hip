@@ -15,6 +15,7 @@
 #include <algorithm>
 
 #include "kernels.h"
+#include "prof.h"
 
 namespace gcn {
 namespace {
@@ -302,6 +303,19 @@ hipError_t launch_gemm(GemmBatch& b, ALayout al, BLayout bl, Epilogue ep,
     b.total_tiles = total;
     if (total == 0) return hipSuccess;
     const dim3 grid(total), block(kThreads);
+    double flops = 0, bytes = 0;
+    for (int i = 0; i < b.nprob; ++i) {
+        const GemmProblem& p = b.p[i];
+        const double M = p.M, N = p.N, K = p.K;
+        flops += 2.0 * M * N * K;
+        bytes += 4.0 * (M * K + K * N + M * N) + (ep == EPI_MASK ? 4.0 * M * N : 0.0);
+    }
+    const int kind = ep == EPI_BIAS_RELU ? K_GEMM_FWD
+                   : ep == EPI_BIAS      ? K_GEMM_CLS
+                   : ep == EPI_MASK      ? K_GEMM_DX
+                   : ep == EPI_PARTIAL   ? K_GEMM_DW
+                                         : K_GEMM_CLS;
+    ProfScope prof(s, kind, flops, bytes);
 #define GCN_GEMM_CASE(AL_, BL_, EP_)                                        \
     if (al == AL_ && bl == BL_ && ep == EP_) {                               \
         gemm_kernel<AL_, BL_, EP_><<<grid, block, 0, s>>>(b);                \
@@ -328,6 +342,13 @@ hipError_t launch_sgd_reduce(const SgdProblem* p, int nprob, float lr,
     if (total == 0) return hipSuccess;
     const SgdProblem second = nprob > 1 ? p[1] : p[0];
     const int64_t blocks = (total + 255) / 256;
+    double flops = 0, bytes = 0;
+    for (int i = 0; i < nprob; ++i) {
+        const double cells = (double)(p[i].Mw + (p[i].b ? 1 : 0)) * p[i].N;
+        flops += cells * (p[i].splits + 1.0);
+        bytes += 4.0 * cells * (p[i].splits + 2.0);
+    }
+    ProfScope prof(s, K_SGD, flops, bytes);
     sgd_reduce_kernel<<<dim3((unsigned)blocks), dim3(256), 0, s>>>(p[0], second, t0, total, lr);
     return hipGetLastError();
 }

@@ -4,6 +4,7 @@
 // vertex row; per-row losses are then summed by a single workgroup in a
 // fixed order, so the scalar loss is bitwise reproducible.
 #include "kernels.h"
+#include "prof.h"
 
 namespace gcn {
 namespace {
@@ -92,6 +93,7 @@ hipError_t launch_loss(int32_t n, int32_t C, int32_t kind, const float* z,
                        float* rowloss, float* loss_out, hipStream_t s) {
     if (n > 0) {
         const dim3 grid((n + 3) / 4), block(256);
+        ProfScope prof(s, K_LOSS_ROWS, 8.0 * n * C, 8.0 * n * C + 4.0 * n);
         if (kind == GCN_LOSS_SOFTMAX_CE)
             softmax_ce_kernel<<<grid, block, 0, s>>>(
                 n, C, z, ldz, static_cast<const int32_t*>(labels), dz, ldd, rowloss);
@@ -102,6 +104,7 @@ hipError_t launch_loss(int32_t n, int32_t C, int32_t kind, const float* z,
         if (e != hipSuccess) return e;
     }
     const float denom = kind == GCN_LOSS_SOFTMAX_CE ? (float)n : (float)n * (float)C;
+    ProfScope prof(s, K_LOSS_MEAN, (double)n, 4.0 * n);
     mean_kernel<<<dim3(1), dim3(256), 0, s>>>(n, rowloss, denom > 0 ? denom : 1.0f, loss_out);
     return hipGetLastError();
 }

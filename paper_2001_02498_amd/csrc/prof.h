@@ -1,0 +1,40 @@
+// Launch timing scopes (see prof.hip).
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include "common.h"
+
+namespace gcn {
+
+enum Kind : int {
+    K_PAIR_SUMS = 0,
+    K_LIST_SUMS,
+    K_LIST_FIXUP,
+    K_GEMM_FWD,
+    K_GEMM_CLS,
+    K_GEMM_DX,
+    K_GEMM_DW,
+    K_SGD,
+    K_LOSS_ROWS,
+    K_LOSS_MEAN,
+    K_COUNT
+};
+
+const char* kind_name(int k);
+
+// Records an event pair around the launches made during its lifetime when
+// timing is enabled; a no-op otherwise.
+class ProfScope {
+   public:
+    ProfScope(hipStream_t s, int kind, double flops, double bytes);
+    ~ProfScope();
+    ProfScope(const ProfScope&) = delete;
+    ProfScope& operator=(const ProfScope&) = delete;
+
+   private:
+    hipStream_t s_;
+    int64_t idx_;
+};
+
+}  // namespace gcn

@@ -133,13 +133,24 @@ _train_step = _proto("gcn_train_step", [C.POINTER(DGraph), C.POINTER(ModelDesc),
                                         C.POINTER(Params), _vp, _vp, _f32, _vp,
                                         C.POINTER(Params), _vp, _sz, _vp])
 
+class ProfileEntry(C.Structure):
+    _fields_ = [("kind", _i32), ("launches", _i32), ("name", C.c_char_p),
+                ("total_ms", C.c_double), ("min_ms", C.c_double), ("max_ms", C.c_double),
+                ("flops", C.c_double), ("bytes", C.c_double)]
+
+
+_prof_enable = _proto("gcn_profile_enable", [_i32])
+_prof_disable = _proto("gcn_profile_disable", [])
+_prof_read = _proto("gcn_profile_read", [C.POINTER(ProfileEntry), _i32, _pi32, _i32])
+
 EXPORTS = [
     "gcn_last_error", "gcn_abi_version", "gcn_subgraph_build", "gcn_graph_info",
     "gcn_graph_free", "gcn_redundancy_reduce", "gcn_reduced_info", "gcn_reduced_free",
     "gcn_graph_image_bytes", "gcn_graph_pack", "gcn_graph_upload", "gcn_graph_describe",
     "gcn_scratch_bytes", "gcn_aggregate", "gcn_layer_fwd", "gcn_classifier_fwd",
     "gcn_loss", "gcn_classifier_bwd", "gcn_layer_bwd", "gcn_workspace_layout",
-    "gcn_workspace_bytes", "gcn_train_step",
+    "gcn_workspace_bytes", "gcn_train_step", "gcn_profile_enable", "gcn_profile_disable",
+    "gcn_profile_read",
 ]
 
 
@@ -399,3 +410,24 @@ def train_step(dg, desc, params, X, labels, lr, loss_out, ws, grads=None, stream
                        _ptr(labels), float(lr), _ptr(loss_out),
                        C.byref(grads) if grads is not None else None, _ptr(ws), ws.numel(),
                        _stream(stream)))
+
+
+# ------------------------------------------------------------ launch timing
+
+def profile_enable(capacity=4096):
+    _check(_prof_enable(int(capacity)))
+
+
+def profile_disable():
+    _check(_prof_disable())
+
+
+def profile_read(reset=True):
+    """Per kernel class: dict(launches, total_ms, min_ms, max_ms, flops, bytes)."""
+    buf = (ProfileEntry * 32)()
+    cnt = _i32()
+    _check(_prof_read(buf, 32, C.byref(cnt), 1 if reset else 0))
+    return {buf[i].name.decode(): dict(launches=buf[i].launches, total_ms=buf[i].total_ms,
+                                       min_ms=buf[i].min_ms, max_ms=buf[i].max_ms,
+                                       flops=buf[i].flops, bytes=buf[i].bytes)
+            for i in range(min(cnt.value, 32))}
