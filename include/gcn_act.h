@@ -219,11 +219,13 @@ int gcn_layer_fwd(const gcn_dgraph* g, int32_t F, int32_t h,
  * gcn_classifier_fwd - logits = H W_cls (+ b_cls), a linear layer on the
  * last layer's output (Section 2.1, node classifier).
  *   H [n x K] ld ldh; W_cls [K x C]; b_cls [C] or NULL; logits [n x C] ldz
+ *   Scratch (split-K slices when n x C is too small to fill the GPU):
+ *   gcn_scratch_bytes(NULL, n, max(K, C)).
  */
 int gcn_classifier_fwd(int32_t n, int32_t K, int32_t C, const float* H,
                        int64_t ldh, const float* W_cls, const float* b_cls,
                        float* logits, int64_t ldz, int32_t precision,
-                       gcn_stream_t stream);
+                       void* ws, size_t ws_bytes, gcn_stream_t stream);
 
 /* gcn_loss - loss and its gradient w.r.t. the logits (Section 2.1: softmax
  * with cross-entropy; its gradient is a subtraction).

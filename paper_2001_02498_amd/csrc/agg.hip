@@ -223,9 +223,18 @@ __global__ __launch_bounds__(kBlock) void fixup_kernel(
         for (int j = 0; j < NCH; ++j) {
             const int c4 = base + lane + j * GL;
             if (c4 < nf4) {
+                // eight slots in flight, added in slot order
+                const float* src = partial + (int64_t)first * ldp + 4 * c4;
                 float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
-                for (int sI = 0; sI < ns; ++sI)
-                    add4(acc, ld4(partial + (int64_t)(first + sI) * ldp + 4 * c4));
+                int sI = 0;
+                for (; sI + 8 <= ns; sI += 8) {
+                    float4 v[8];
+#pragma unroll
+                    for (int u = 0; u < 8; ++u) v[u] = ld4(src + (int64_t)(sI + u) * ldp);
+#pragma unroll
+                    for (int u = 0; u < 8; ++u) add4(acc, v[u]);
+                }
+                for (; sI < ns; ++sI) add4(acc, ld4(src + (int64_t)sI * ldp));
                 if (POST) acc = make_float4(acc.x * sc, acc.y * sc, acc.z * sc, acc.w * sc);
                 st4_masked(out + 4 * c4, acc, F - 4 * c4);
             }

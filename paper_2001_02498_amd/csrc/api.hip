@@ -175,7 +175,8 @@ int do_layer_fwd(const char* fn, const gcn_dgraph* g, int32_t F, int32_t h,
 
 int do_classifier_fwd(const char* fn, int32_t n, int32_t K, int32_t C,
                       const float* H, int64_t ldh, const float* Wc,
-                      const float* bc, float* Z, int64_t ldz, hipStream_t s) {
+                      const float* bc, float* Z, int64_t ldz, const ScratchPlan& sp,
+                      void* ws, hipStream_t s) {
     GemmBatch b;
     std::memset(&b, 0, sizeof(b));
     b.nprob = 1;
@@ -189,6 +190,21 @@ int do_classifier_fwd(const char* fn, int32_t n, int32_t K, int32_t C,
     p.B0 = p.B1 = Wc;
     p.ldb0 = p.ldb1 = C;
     p.ksplitB = K;
+    // A few output tiles cannot fill the GPU: split K, then sum the slices.
+    const int64_t tiles = (int64_t)((n + 127) / 128) * ((C + 127) / 128);
+    int32_t splits = 1, kchunk = 0;
+    if (tiles < 192) gemm_split_plan(n, C, K, &splits, &kchunk);
+    if (splits > 1) {
+        p.splits = splits;
+        p.kchunk = kchunk;
+        p.C = fptr(ws, sp.gemm_part);
+        p.ldc = r4(C);
+        p.part_stride = (int64_t)n * p.ldc;
+        b.p[0] = p;
+        GCN_HIP(launch_gemm(b, A_MK, B_KN, EPI_PARTIAL, s), fn);
+        GCN_HIP(launch_splitk_finish(p.C, p.part_stride, p.ldc, splits, n, C, bc, Z, ldz, s), fn);
+        return GCN_OK;
+    }
     p.C = Z;
     p.ldc = ldz;
     p.bias = bc;
@@ -444,7 +460,8 @@ int gcn_layer_fwd(const gcn_dgraph* g, int32_t F, int32_t h, const float* H_in,
 
 int gcn_classifier_fwd(int32_t n, int32_t K, int32_t C, const float* H, int64_t ldh,
                        const float* W_cls, const float* b_cls, float* logits,
-                       int64_t ldz, int32_t precision, gcn_stream_t stream) {
+                       int64_t ldz, int32_t precision, void* ws, size_t ws_bytes,
+                       gcn_stream_t stream) {
     const char* fn = "gcn_classifier_fwd";
     GCN_CHECK_ARG(n >= 0 && K >= 1 && C >= 1, "%s: bad sizes", fn);
     GCN_TRY(check_precision(fn, precision));
@@ -452,7 +469,9 @@ int gcn_classifier_fwd(int32_t n, int32_t K, int32_t C, const float* H, int64_t 
     GCN_TRY(check_vec(fn, "W_cls", W_cls, (int64_t)K * C));
     if (b_cls) GCN_TRY(check_vec(fn, "b_cls", b_cls, C));
     GCN_TRY(check_mat(fn, "logits", logits, n, C, ldz));
-    return do_classifier_fwd(fn, n, K, C, H, ldh, W_cls, b_cls, logits, ldz,
+    const ScratchPlan sp = plan_scratch(n, 0, 0, std::max(K, C));
+    GCN_TRY(check_ws(fn, ws, ws_bytes, sp.total));
+    return do_classifier_fwd(fn, n, K, C, H, ldh, W_cls, b_cls, logits, ldz, sp, ws,
                              (hipStream_t)stream);
 }
 
@@ -608,7 +627,7 @@ int gcn_train_step(const gcn_dgraph* g, const gcn_model_desc* d, const gcn_param
     float* Z = act(sl.pub.logits);
     float* dZ = act(sl.pub.dlogits);
     GCN_TRY(do_classifier_fwd(fn, (int32_t)n, 2 * h, C, Hprev, ldH, P->W_cls,
-                              d->has_bias ? P->b_cls : nullptr, Z, ldC, s));
+                              d->has_bias ? P->b_cls : nullptr, Z, ldC, sp, scratch, s));
     GCN_HIP(launch_loss((int32_t)n, C, d->loss, Z, ldC, labels, dZ, ldC,
                         fptr(scratch, sp.rowloss), loss_out, s),
             fn);

@@ -39,64 +39,67 @@ __device__ __forceinline__ void zero_from(float4& v, int valid) {
     if (valid < 1) v.x = 0.f;
 }
 
+// Operand loads are split in two halves so that prefetching never waits:
+// the load half only issues memory reads (predicated on bounds) and records
+// how many of the four elements are valid; the store half, run after the
+// MFMA work of the current K step, zero-fills the invalid tail and writes
+// LDS. Out-of-range elements inside a float4 stay inside the padded row.
+struct Quad {
+    float4 v;
+    int valid;   // elements [0, valid) are real; the rest become 0
+    int one;     // element index that is an implicit 1, or -1
+};
+
+__device__ __forceinline__ float4 finish(Quad q) {
+    float4 v = q.v;
+    zero_from(v, q.valid);
+    if (q.one == 0) v.x = 1.f;
+    if (q.one == 1) v.y = 1.f;
+    if (q.one == 2) v.z = 1.f;
+    if (q.one == 3) v.w = 1.f;
+    return v;
+}
+
+template <bool VEC>
+__device__ __forceinline__ void issue(Quad& q, const float* p, int valid) {
+    q.valid = valid;
+    q.v = make_float4(0.f, 0.f, 0.f, 0.f);
+    if constexpr (VEC) {
+        if (valid > 0) q.v = ld4(p);
+    } else {
+        if (valid > 0) q.v.x = p[0];
+        if (valid > 1) q.v.y = p[1];
+        if (valid > 2) q.v.z = p[2];
+        if (valid > 3) q.v.w = p[3];
+    }
+}
+
 // Row-contiguous operand (A_MK rows = m, or B_NK rows = n), K-concatenated:
 // element (r, k) at P0[r*ld0 + k] for k < ksplit, else P1[r*ld1 + k-ksplit].
-// vec: rows are 16-byte aligned, so one float4 load (its tail past the
-// logical width stays inside the padded row); else element loads.
-__device__ __forceinline__ float4 load_rowk(const float* P0, const float* P1,
-                                            int64_t ld0, int64_t ld1,
-                                            int ksplit, int rows, int r, int k,
-                                            int kend, bool vec) {
-    float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
-    if (r < rows && k < kend) {
-        const float* p = k < ksplit ? P0 + (int64_t)r * ld0 + k
-                                    : P1 + (int64_t)r * ld1 + (k - ksplit);
-        const int valid = kend - k;
-        if (vec) {
-            v = ld4(p);
-            zero_from(v, valid);
-        } else {
-            v.x = p[0];
-            if (valid > 1) v.y = p[1];
-            if (valid > 2) v.z = p[2];
-            if (valid > 3) v.w = p[3];
-        }
-    }
-    return v;
+template <bool VEC>
+__device__ __forceinline__ void load_rowk(Quad& q, const float* P0, const float* P1,
+                                          int64_t ld0, int64_t ld1, int ksplit,
+                                          int rows, int r, int k, int kend) {
+    q.one = -1;
+    const bool live = r < rows && k < kend;
+    const float* p = k < ksplit ? P0 + (int64_t)r * ld0 + k
+                                : P1 + (int64_t)r * ld1 + (k - ksplit);
+    issue<VEC>(q, p, live ? kend - k : 0);
 }
 
 // K-major operand (A_KM or B_KN): element (c, k) at P[k*ld + c], c < cols;
 // with ones, column c == cols is an implicit 1 (bias gradient row).
-__device__ __forceinline__ float4 load_kcol(const float* P, int64_t ld,
-                                            int cols, bool ones, int c, int k,
-                                            int kend, bool vec) {
-    float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
-    if (k < kend) {
-        if (c < cols) {
-            const float* p = P + (int64_t)k * ld + c;
-            const int valid = cols - c;
-            if (vec) {
-                v = ld4(p);
-                zero_from(v, valid);
-            } else {
-                v.x = p[0];
-                if (valid > 1) v.y = p[1];
-                if (valid > 2) v.z = p[2];
-                if (valid > 3) v.w = p[3];
-            }
-        }
-        if (ones) {
-            const int o = cols - c;
-            if (o == 0) v.x = 1.f;
-            if (o == 1) v.y = 1.f;
-            if (o == 2) v.z = 1.f;
-            if (o == 3) v.w = 1.f;
-        }
-    }
-    return v;
+template <bool VEC>
+__device__ __forceinline__ void load_kcol(Quad& q, const float* P, int64_t ld, int cols,
+                                          bool ones, int c, int k, int kend) {
+    const bool krow = k < kend;
+    q.one = (ones && krow && cols - c >= 0 && cols - c < 4) ? cols - c : -1;
+    issue<VEC>(q, P + (int64_t)k * ld + c, (krow && c < cols) ? cols - c : 0);
 }
 
-template <ALayout AL, BLayout BL, Epilogue EP>
+// A rows are always 16-byte aligned (checked on the host); BVEC selects
+// float4 or element loads for B (the classifier weight has any width C).
+template <ALayout AL, BLayout BL, Epilogue EP, bool BVEC>
 __global__ __launch_bounds__(kThreads, 2) void gemm_kernel(GemmBatch batch) {
     __shared__ float As[2][BK][kStride];
     __shared__ float Bs[2][BK][kStride];
@@ -127,49 +130,48 @@ __global__ __launch_bounds__(kThreads, 2) void gemm_kernel(GemmBatch batch) {
 
     const int Areal = P.M - P.ones_row;   // rows of A backed by memory
 
-    float4 ra[2], rb[2];
+    Quad ra[2], rb[2];
     auto gload = [&](int k0) {
 #pragma unroll
         for (int i = 0; i < 2; ++i) {
             if constexpr (AL == A_MK) {
-                ra[i] = load_rowk(P.A0, P.A1, P.lda0, P.lda1, P.ksplitA, P.M,
-                                  m0 + (t >> 2) + 64 * i, k0 + 4 * (t & 3), kend,
-                                  P.a_vec != 0);
+                load_rowk<true>(ra[i], P.A0, P.A1, P.lda0, P.lda1, P.ksplitA, P.M,
+                                m0 + (t >> 2) + 64 * i, k0 + 4 * (t & 3), kend);
             } else {
-                ra[i] = load_kcol(P.A0, P.lda0, Areal, P.ones_row != 0,
-                                  m0 + 4 * (t & 31), k0 + (t >> 5) + 8 * i, kend,
-                                  P.a_vec != 0);
+                load_kcol<true>(ra[i], P.A0, P.lda0, Areal, P.ones_row != 0,
+                                m0 + 4 * (t & 31), k0 + (t >> 5) + 8 * i, kend);
             }
             if constexpr (BL == B_NK) {
-                rb[i] = load_rowk(P.B0, P.B1, P.ldb0, P.ldb1, P.ksplitB, P.N,
-                                  n0 + (t >> 2) + 64 * i, k0 + 4 * (t & 3), kend,
-                                  P.b_vec != 0);
+                load_rowk<BVEC>(rb[i], P.B0, P.B1, P.ldb0, P.ldb1, P.ksplitB, P.N,
+                                n0 + (t >> 2) + 64 * i, k0 + 4 * (t & 3), kend);
             } else {
-                rb[i] = load_kcol(P.B0, P.ldb0, P.N, false, n0 + 4 * (t & 31),
-                                  k0 + (t >> 5) + 8 * i, kend, P.b_vec != 0);
+                load_kcol<BVEC>(rb[i], P.B0, P.ldb0, P.N, false, n0 + 4 * (t & 31),
+                                k0 + (t >> 5) + 8 * i, kend);
             }
         }
     };
     auto sstore = [&](int buf) {
 #pragma unroll
         for (int i = 0; i < 2; ++i) {
+            const float4 a = finish(ra[i]);
+            const float4 b = finish(rb[i]);
             if constexpr (AL == A_MK) {
                 const int r = (t >> 2) + 64 * i, kq = 4 * (t & 3);
-                As[buf][kq + 0][r] = ra[i].x;
-                As[buf][kq + 1][r] = ra[i].y;
-                As[buf][kq + 2][r] = ra[i].z;
-                As[buf][kq + 3][r] = ra[i].w;
+                As[buf][kq + 0][r] = a.x;
+                As[buf][kq + 1][r] = a.y;
+                As[buf][kq + 2][r] = a.z;
+                As[buf][kq + 3][r] = a.w;
             } else {
-                *reinterpret_cast<float4*>(&As[buf][(t >> 5) + 8 * i][4 * (t & 31)]) = ra[i];
+                *reinterpret_cast<float4*>(&As[buf][(t >> 5) + 8 * i][4 * (t & 31)]) = a;
             }
             if constexpr (BL == B_NK) {
                 const int r = (t >> 2) + 64 * i, kq = 4 * (t & 3);
-                Bs[buf][kq + 0][r] = rb[i].x;
-                Bs[buf][kq + 1][r] = rb[i].y;
-                Bs[buf][kq + 2][r] = rb[i].z;
-                Bs[buf][kq + 3][r] = rb[i].w;
+                Bs[buf][kq + 0][r] = b.x;
+                Bs[buf][kq + 1][r] = b.y;
+                Bs[buf][kq + 2][r] = b.z;
+                Bs[buf][kq + 3][r] = b.w;
             } else {
-                *reinterpret_cast<float4*>(&Bs[buf][(t >> 5) + 8 * i][4 * (t & 31)]) = rb[i];
+                *reinterpret_cast<float4*>(&Bs[buf][(t >> 5) + 8 * i][4 * (t & 31)]) = b;
             }
         }
     };
@@ -264,7 +266,32 @@ __global__ __launch_bounds__(256) void sgd_reduce_kernel(SgdProblem p0,
     }
 }
 
+__global__ __launch_bounds__(256) void splitk_finish_kernel(
+    const float* __restrict__ part, int64_t part_stride, int64_t ldp, int splits, int M,
+    int N, const float* __restrict__ bias, float* __restrict__ C, int64_t ldc) {
+    const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (idx >= (int64_t)M * N) return;
+    const int m = (int)(idx / N), nn = (int)(idx % N);
+    const float* src = part + (int64_t)m * ldp + nn;
+    float d = 0.f;
+    for (int j = 0; j < splits; ++j) d += src[(int64_t)j * part_stride];
+    if (bias) d += bias[nn];
+    C[(int64_t)m * ldc + nn] = d;
+}
+
 }  // namespace
+
+hipError_t launch_splitk_finish(const float* part, int64_t part_stride, int64_t ldp,
+                                int32_t splits, int32_t M, int32_t N, const float* bias,
+                                float* C, int64_t ldc, hipStream_t s) {
+    const int64_t total = (int64_t)M * N;
+    if (total == 0) return hipSuccess;
+    ProfScope prof(s, K_SPLITK_FINISH, (double)total * splits,
+                   4.0 * (double)total * (splits + 1));
+    splitk_finish_kernel<<<dim3((unsigned)((total + 255) / 256)), dim3(256), 0, s>>>(
+        part, part_stride, ldp, splits, M, N, bias, C, ldc);
+    return hipGetLastError();
+}
 
 void gemm_split_plan(int32_t M, int32_t N, int32_t K, int32_t* splits,
                      int32_t* kchunk) {
@@ -310,23 +337,29 @@ hipError_t launch_gemm(GemmBatch& b, ALayout al, BLayout bl, Epilogue ep,
         flops += 2.0 * M * N * K;
         bytes += 4.0 * (M * K + K * N + M * N) + (ep == EPI_MASK ? 4.0 * M * N : 0.0);
     }
-    const int kind = ep == EPI_BIAS_RELU ? K_GEMM_FWD
-                   : ep == EPI_BIAS      ? K_GEMM_CLS
-                   : ep == EPI_MASK      ? K_GEMM_DX
-                   : ep == EPI_PARTIAL   ? K_GEMM_DW
-                                         : K_GEMM_CLS;
+    const int kind = ep == EPI_BIAS_RELU            ? K_GEMM_FWD
+                   : ep == EPI_MASK                 ? K_GEMM_DX
+                   : ep == EPI_PARTIAL && al == A_KM ? K_GEMM_DW
+                                                    : K_GEMM_CLS;
     ProfScope prof(s, kind, flops, bytes);
+    bool bvec = true;
+    for (int i = 0; i < b.nprob; ++i) {
+        if (!b.p[i].a_vec) return hipErrorInvalidValue;   // A rows must be aligned
+        bvec = bvec && b.p[i].b_vec;
+    }
 #define GCN_GEMM_CASE(AL_, BL_, EP_)                                        \
     if (al == AL_ && bl == BL_ && ep == EP_) {                               \
-        gemm_kernel<AL_, BL_, EP_><<<grid, block, 0, s>>>(b);                \
+        if (bvec)                                                           \
+            gemm_kernel<AL_, BL_, EP_, true><<<grid, block, 0, s>>>(b);      \
+        else                                                                \
+            gemm_kernel<AL_, BL_, EP_, false><<<grid, block, 0, s>>>(b);     \
         return hipGetLastError();                                           \
     }
     GCN_GEMM_CASE(A_MK, B_KN, EPI_BIAS_RELU)
     GCN_GEMM_CASE(A_MK, B_KN, EPI_BIAS)
-    GCN_GEMM_CASE(A_MK, B_KN, EPI_STORE)
     GCN_GEMM_CASE(A_MK, B_NK, EPI_MASK)
-    GCN_GEMM_CASE(A_MK, B_NK, EPI_STORE)
     GCN_GEMM_CASE(A_KM, B_KN, EPI_PARTIAL)
+    GCN_GEMM_CASE(A_MK, B_KN, EPI_PARTIAL)
 #undef GCN_GEMM_CASE
     return hipErrorInvalidValue;
 }

@@ -86,6 +86,12 @@ void gemm_split_plan(int32_t M, int32_t N, int32_t K, int32_t* splits,
 hipError_t launch_gemm(GemmBatch& b, ALayout al, BLayout bl, Epilogue ep,
                        hipStream_t s);
 
+// Sum of split-K slices in slice order plus an optional bias:
+//   C[m][n] = sum_j part[j*stride + m*ldp + n] (+ bias[n]).
+hipError_t launch_splitk_finish(const float* part, int64_t part_stride, int64_t ldp,
+                                int32_t splits, int32_t M, int32_t N, const float* bias,
+                                float* C, int64_t ldc, hipStream_t s);
+
 // Deterministic sum of split-K slices + gradient-descent update:
 //   d = sum_j part[j] (j ascending);  W[m][n] -= lr d  (m < Mw);
 //   bias row m == Mw (when b != NULL): b[n] -= lr d.  Optional copies of d.

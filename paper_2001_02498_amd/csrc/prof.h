@@ -18,6 +18,7 @@ enum Kind : int {
     K_SGD,
     K_LOSS_ROWS,
     K_LOSS_MEAN,
+    K_SPLITK_FINISH,
     K_COUNT
 };
 

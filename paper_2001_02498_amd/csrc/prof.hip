@@ -39,6 +39,7 @@ const char* kind_name(int k) {
         case K_SGD: return "sgd_reduce";
         case K_LOSS_ROWS: return "loss_rows";
         case K_LOSS_MEAN: return "loss_mean";
+        case K_SPLITK_FINISH: return "splitk_finish";
         default: return "other";
     }
 }

@@ -117,7 +117,7 @@ _aggregate = _proto("gcn_aggregate", [C.POINTER(DGraph), _i32, _i32, _vp, _i64, 
 _layer_fwd = _proto("gcn_layer_fwd", [C.POINTER(DGraph), _i32, _i32, _vp, _i64, _vp, _vp, _vp,
                                       _vp, _i64, _vp, _i64, _i32, _vp, _sz, _vp])
 _classifier_fwd = _proto("gcn_classifier_fwd", [_i32, _i32, _i32, _vp, _i64, _vp, _vp, _vp,
-                                                _i64, _i32, _vp])
+                                                _i64, _i32, _vp, _sz, _vp])
 _loss = _proto("gcn_loss", [_i32, _i32, _i32, _vp, _i64, _vp, _vp, _i64, _vp, _vp, _sz, _vp])
 _classifier_bwd = _proto("gcn_classifier_bwd", [_i32, _i32, _i32, _vp, _i64, _vp, _i64, _vp,
                                                 _vp, _f32, _vp, _i64, _vp, _vp, _i32, _vp,
@@ -347,11 +347,12 @@ def layer_fwd(dg, H_in, W_self, W_neigh, bias, AH, H_out, ws, precision=PREC_FP3
                       _ld(H_out), precision, _ptr(ws), ws.numel(), _stream(stream)))
 
 
-def classifier_fwd(H, K, W_cls, b_cls, logits, precision=PREC_FP32, stream=None):
+def classifier_fwd(H, K, W_cls, b_cls, logits, ws, precision=PREC_FP32, stream=None):
     n = H.shape[0]
     Cn = W_cls.shape[1]
     _check(_classifier_fwd(n, K, Cn, _ptr(H), _ld(H), _ptr(W_cls), _ptr(b_cls),
-                           _ptr(logits), _ld(logits), precision, _stream(stream)))
+                           _ptr(logits), _ld(logits), precision, _ptr(ws), ws.numel(),
+                           _stream(stream)))
 
 
 def loss(kind, logits, C_, labels, dlogits, loss_out, ws, stream=None):

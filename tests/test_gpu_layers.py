@@ -63,11 +63,12 @@ def test_classifier_fwd_loss_bwd(n, K, C, bias):
     Hd, Wd = dev(H), torch.from_numpy(Wc.copy()).cuda()
     bd = torch.from_numpy(bc.copy()).cuda() if bias else None
     Z = empty(n, C)
-    gcn.classifier_fwd(Hd, K, Wd, bd, Z)
+    ws = gcn.alloc_ws(gcn.scratch_bytes(None, max(K, C), n=n))
+    gcn.classifier_fwd(Hd, K, Wd, bd, Z, ws)
     Zref = H.astype(float) @ Wc + (bc if bias else 0)
     torch.cuda.synchronize()
     assert rel(Z, Zref) < FP32_TOL
-    ws = gcn.alloc_ws(gcn.scratch_bytes(None, max(K, C), n=n))
+    assert torch.isnan(padding_of(Z)).all()
     for kind in (og.SOFTMAX_CE, og.SIGMOID_BCE):
         if kind == og.SOFTMAX_CE:
             y = rng.integers(0, C, n).astype(np.int32)
