@@ -37,6 +37,8 @@ def parse():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="ppi8k")
     ap.add_argument("--profile-steps", type=int, default=10)
+    ap.add_argument("--seg-len", type=int, default=0,
+                    help="list segment length of the device work list (0: library default)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
                     help="CPU oracle sample budget (seconds of work)")
@@ -49,7 +51,7 @@ def parse():
 class Setup:
     """Inputs of one workload on the device, ready for timed steps."""
 
-    def __init__(self, wl, reduce, inp):
+    def __init__(self, wl, reduce, inp, seg_len=0):
         import torch
         from paper_2001_02498_amd import gcn
         self.gcn, self.wl = gcn, wl
@@ -61,7 +63,7 @@ class Setup:
         t2 = time.perf_counter()
         self.host_ms = dict(subgraph_build=1e3 * (t1 - t0), reduction=1e3 * (t2 - t1))
         self.info = red.info()
-        self.dg = gcn.DeviceGraph(red)
+        self.dg = gcn.DeviceGraph(red, seg_len=seg_len)
 
         def mat(x, ld=None):
             import numpy as np
@@ -180,12 +182,12 @@ def main():
     inp = synth.make_inputs(wl)
     print(f"[bench] workload {wl.name}: inputs ready", file=sys.stderr, flush=True)
 
-    red = Setup(wl, wl.reduce, inp)
+    red = Setup(wl, wl.reduce, inp, args.seg_len)
     ms = 1e3 * red.timed(args.steps, args.warmup)
     print(f"[bench] timed {args.steps} steps: {ms:.3f} ms/step", file=sys.stderr, flush=True)
     direct = None
     if wl.reduce:
-        d = Setup(dataclasses.replace(wl, reduce=False), False, inp)
+        d = Setup(dataclasses.replace(wl, reduce=False), False, inp, args.seg_len)
         direct = 1e3 * d.timed(args.steps, args.warmup)
         print(f"[bench] direct aggregation: {direct:.3f} ms/step", file=sys.stderr, flush=True)
         del d

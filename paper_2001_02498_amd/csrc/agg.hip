@@ -11,6 +11,10 @@
 // their segments write partial sums to scratch slots that a second pass adds
 // in slot order, so the result is deterministic and no row serialises a
 // whole wavefront for thousands of neighbours.
+// Wide rows (F >= 512) are cut into 8 column slices and workgroup b works on
+// slice b % 8, which is also the XCD it runs on: each XCD then gathers only
+// its slice of every feature row, so its 4 MB L2 holds that slice of the
+// whole matrix instead of every XCD streaming all of it.
 #include "kernels.h"
 #include "prof.h"
 
@@ -71,21 +75,33 @@ __device__ __forceinline__ float bcast_f(float v, int t) {
     return __int_as_float(bcast_i<GL>(__float_as_int(v), t));
 }
 
-// group index, made wave-uniform when the group is the whole wavefront
+// Column slice and group index of this thread: workgroup b covers slice
+// b % nsl; the group index is made wave-uniform when the group is a whole
+// wavefront.
+struct Slice {
+    int c4_begin, c4_end;   // float4 columns [begin, end)
+};
+
 template <int GL>
-__device__ __forceinline__ int group_index() {
-    int g = blockIdx.x * (kBlock / GL) + (int)threadIdx.x / GL;
+__device__ __forceinline__ int group_index(int nsl) {
+    int g = (int)(blockIdx.x / nsl) * (kBlock / GL) + (int)threadIdx.x / GL;
     if constexpr (GL == 64) g = __builtin_amdgcn_readfirstlane(g);
     return g;
+}
+
+__device__ __forceinline__ Slice slice_of(int nsl, int slice_f4, int nf4) {
+    const int sl = (int)(blockIdx.x % nsl);
+    const int b = sl * slice_f4;
+    return {b, min(nf4, b + slice_f4)};
 }
 
 template <int GL, int NCH, bool PRE>
 __global__ __launch_bounds__(kBlock) void pair_sums_kernel(
     const int32_t* __restrict__ pairs, int k0, int k1, RowSource src,
     const float* __restrict__ inv_deg, float* __restrict__ aux,
-    int64_t ldaux, int F) {
+    int64_t ldaux, int F, int nsl, int slice_f4) {
     const int lane = (int)threadIdx.x % GL;
-    const int k = k0 + group_index<GL>();
+    const int k = k0 + group_index<GL>(nsl);
     if (k >= k1) return;
     const int p = pairs[2 * k], q = pairs[2 * k + 1];
     const float* rp = row_of(src, p);
@@ -96,12 +112,12 @@ __global__ __launch_bounds__(kBlock) void pair_sums_kernel(
         if (q < src.n) sq = inv_deg[q];
     }
     float* out = aux + (int64_t)k * ldaux;
-    const int nf4 = (F + 3) >> 2;
-    for (int base = 0; base < nf4; base += GL * NCH) {
+    const Slice sl = slice_of(nsl, slice_f4, (F + 3) >> 2);
+    for (int base = sl.c4_begin; base < sl.c4_end; base += GL * NCH) {
 #pragma unroll
         for (int j = 0; j < NCH; ++j) {
             const int c4 = base + lane + j * GL;
-            if (c4 < nf4) {
+            if (c4 < sl.c4_end) {
                 float4 a = ld4(rp + 4 * c4), b = ld4(rq + 4 * c4), v;
                 if (PRE) {
                     v.x = fmaf(sp, a.x, sq * b.x);
@@ -122,14 +138,15 @@ template <int GL, int NCH, bool PRE, bool POST>
 __global__ __launch_bounds__(kBlock) void list_sums_kernel(
     const int4* __restrict__ seg, int nseg, const int32_t* __restrict__ col,
     RowSource src, const float* __restrict__ inv_deg, float* __restrict__ Y,
-    int64_t ldy, float* __restrict__ partial, int64_t ldp, int F) {
+    int64_t ldy, float* __restrict__ partial, int64_t ldp, int F, int nsl, int slice_f4) {
     const int lane = (int)threadIdx.x % GL;
-    const int sidx = group_index<GL>();
+    const int sidx = group_index<GL>(nsl);
     if (sidx >= nseg) return;
     const int4 sg = seg[sidx];
     const int row = sg.x, b = sg.y, e = sg.z, slot = sg.w;
-    const int nf4 = (F + 3) >> 2;
-    for (int base = 0; base < nf4; base += GL * NCH) {
+    const Slice sl = slice_of(nsl, slice_f4, (F + 3) >> 2);
+    const int nf4 = sl.c4_end;
+    for (int base = sl.c4_begin; base < nf4; base += GL * NCH) {
         float4 acc[NCH];
 #pragma unroll
         for (int j = 0; j < NCH; ++j) acc[j] = make_float4(0.f, 0.f, 0.f, 0.f);
@@ -209,16 +226,17 @@ __global__ __launch_bounds__(kBlock) void fixup_kernel(
     const int4* __restrict__ longrows, int nlong,
     const float* __restrict__ partial, int64_t ldp,
     const float* __restrict__ inv_deg, float* __restrict__ Y, int64_t ldy,
-    int F) {
+    int F, int nsl, int slice_f4) {
     const int lane = (int)threadIdx.x % GL;
-    const int li = group_index<GL>();
+    const int li = group_index<GL>(nsl);
     if (li >= nlong) return;
     const int4 lr = longrows[li];
     const int row = lr.x, first = lr.y, ns = lr.z;
-    const int nf4 = (F + 3) >> 2;
+    const Slice sl = slice_of(nsl, slice_f4, (F + 3) >> 2);
+    const int nf4 = sl.c4_end;
     const float sc = POST ? inv_deg[row] : 1.0f;
     float* out = Y + (int64_t)row * ldy;
-    for (int base = 0; base < nf4; base += GL * NCH) {
+    for (int base = sl.c4_begin; base < nf4; base += GL * NCH) {
 #pragma unroll
         for (int j = 0; j < NCH; ++j) {
             const int c4 = base + lane + j * GL;
@@ -243,22 +261,33 @@ __global__ __launch_bounds__(kBlock) void fixup_kernel(
 }
 
 struct Shape {
-    int gl, nch;
+    int gl, nch;      // lanes per group, float4 per lane per pass
+    int nsl;          // column slices (8: one per XCD)
+    int slice_f4;     // float4 columns per slice
 };
+
+Shape lanes_for(int f4) {
+    if (f4 <= 16) return {16, 1, 1, f4};
+    if (f4 <= 32) return {32, 1, 1, f4};
+    if (f4 <= 64) return {64, 1, 1, f4};
+    if (f4 <= 128) return {64, 2, 1, f4};
+    if (f4 <= 192) return {64, 3, 1, f4};
+    return {64, 4, 1, f4};
+}
 
 Shape pick_shape(int F) {
     const int nf4 = (F + 3) / 4;
-    if (nf4 <= 16) return {16, 1};
-    if (nf4 <= 32) return {32, 1};
-    if (nf4 <= 64) return {64, 1};
-    if (nf4 <= 128) return {64, 2};
-    if (nf4 <= 192) return {64, 3};
-    return {64, 4};
+    if (nf4 < 128) return lanes_for(nf4);
+    const int slice = (nf4 + 7) / 8;
+    Shape sh = lanes_for(slice);
+    sh.nsl = 8;
+    sh.slice_f4 = slice;
+    return sh;
 }
 
-int blocks_for(int groups, int gl) {
-    const int per = kBlock / gl;
-    return (groups + per - 1) / per;
+int blocks_for(int groups, const Shape& sh) {
+    const int per = kBlock / sh.gl;
+    return ((groups + per - 1) / per) * sh.nsl;
 }
 
 #define GCN_SHAPES(X) \
@@ -272,17 +301,17 @@ hipError_t launch_pair_sums(const int32_t* pairs, int32_t k0, int32_t k1,
                             hipStream_t s) {
     if (k1 <= k0 || F <= 0) return hipSuccess;
     const Shape sh = pick_shape(F);
-    const dim3 grid(blocks_for(k1 - k0, sh.gl)), block(kBlock);
+    const dim3 grid(blocks_for(k1 - k0, sh)), block(kBlock);
     const double np_ = (double)(k1 - k0);
     ProfScope prof(s, K_PAIR_SUMS, np_ * F * (prescale ? 3.0 : 1.0), np_ * (12.0 * F + 8.0));
 #define GCN_LAUNCH_PAIR(GL_, NCH_)                                                  \
     if (sh.gl == GL_ && sh.nch == NCH_) {                                           \
         if (prescale)                                                               \
             pair_sums_kernel<GL_, NCH_, true><<<grid, block, 0, s>>>(               \
-                pairs, k0, k1, src, inv_deg, aux, ldaux, F);                        \
+                pairs, k0, k1, src, inv_deg, aux, ldaux, F, sh.nsl, sh.slice_f4);   \
         else                                                                        \
             pair_sums_kernel<GL_, NCH_, false><<<grid, block, 0, s>>>(              \
-                pairs, k0, k1, src, inv_deg, aux, ldaux, F);                        \
+                pairs, k0, k1, src, inv_deg, aux, ldaux, F, sh.nsl, sh.slice_f4);   \
         return hipGetLastError();                                                   \
     }
     GCN_SHAPES(GCN_LAUNCH_PAIR)
@@ -300,8 +329,8 @@ hipError_t launch_list_sums(const gcn_dgraph* g, RowSource src, bool prescale,
     const int4* seg = reinterpret_cast<const int4*>(g->seg);
     const int4* lr = reinterpret_cast<const int4*>(g->longrows);
     const dim3 block(kBlock);
-    const dim3 grid(blocks_for(g->nseg, sh.gl));
-    const dim3 gfix(blocks_for(g->nlong, sh.gl));
+    const dim3 grid(blocks_for(g->nseg, sh));
+    const dim3 gfix(blocks_for(g->nlong, sh));
     const double nnz = (double)g->nnz, n = (double)g->n;
     {
         // algorithmic: one gather per list entry, its id, one write per row
@@ -311,10 +340,12 @@ hipError_t launch_list_sums(const gcn_dgraph* g, RowSource src, bool prescale,
         if (sh.gl == GL_ && sh.nch == NCH_) {                                         \
             if (prescale)                                                             \
                 list_sums_kernel<GL_, NCH_, true, false><<<grid, block, 0, s>>>(      \
-                    seg, g->nseg, g->col, src, g->inv_deg, Y, ldy, partial, ldp, F);  \
+                    seg, g->nseg, g->col, src, g->inv_deg, Y, ldy, partial, ldp, F,   \
+                    sh.nsl, sh.slice_f4);                                             \
             else                                                                      \
                 list_sums_kernel<GL_, NCH_, false, true><<<grid, block, 0, s>>>(      \
-                    seg, g->nseg, g->col, src, g->inv_deg, Y, ldy, partial, ldp, F);  \
+                    seg, g->nseg, g->col, src, g->inv_deg, Y, ldy, partial, ldp, F,   \
+                    sh.nsl, sh.slice_f4);                                             \
         } else
         GCN_SHAPES(GCN_LAUNCH_LIST) { return hipErrorInvalidValue; }
 #undef GCN_LAUNCH_LIST
@@ -328,10 +359,10 @@ hipError_t launch_list_sums(const gcn_dgraph* g, RowSource src, bool prescale,
     if (sh.gl == GL_ && sh.nch == NCH_) {                                             \
         if (postscale)                                                                \
             fixup_kernel<GL_, NCH_, true><<<gfix, block, 0, s>>>(                     \
-                lr, g->nlong, partial, ldp, g->inv_deg, Y, ldy, F);                   \
+                lr, g->nlong, partial, ldp, g->inv_deg, Y, ldy, F, sh.nsl, sh.slice_f4); \
         else                                                                          \
             fixup_kernel<GL_, NCH_, false><<<gfix, block, 0, s>>>(                    \
-                lr, g->nlong, partial, ldp, g->inv_deg, Y, ldy, F);                   \
+                lr, g->nlong, partial, ldp, g->inv_deg, Y, ldy, F, sh.nsl, sh.slice_f4); \
     } else
     GCN_SHAPES(GCN_LAUNCH_FIX) { return hipErrorInvalidValue; }
 #undef GCN_LAUNCH_FIX

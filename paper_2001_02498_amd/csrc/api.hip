@@ -193,7 +193,7 @@ int do_classifier_fwd(const char* fn, int32_t n, int32_t K, int32_t C,
     // A few output tiles cannot fill the GPU: split K, then sum the slices.
     const int64_t tiles = (int64_t)((n + 127) / 128) * ((C + 127) / 128);
     int32_t splits = 1, kchunk = 0;
-    if (tiles < 192) gemm_split_plan(n, C, K, &splits, &kchunk);
+    if (tiles < 192) gemm_split_plan(n, C, K, 1, &splits, &kchunk);
     if (splits > 1) {
         p.splits = splits;
         p.kchunk = kchunk;
@@ -216,7 +216,7 @@ int do_classifier_fwd(const char* fn, int32_t n, int32_t K, int32_t C,
 // dW = A^T B over K = n rows with split-K slices in scratch slot `which`.
 GemmProblem dw_problem(int32_t n, int32_t Mw, bool ones, int32_t N,
                        const float* A, int64_t lda, const float* B, int64_t ldb,
-                       float* part) {
+                       float* part, int32_t nprob) {
     GemmProblem p = gp_zero();
     p.M = Mw + (ones ? 1 : 0);
     p.N = N;
@@ -226,7 +226,7 @@ GemmProblem dw_problem(int32_t n, int32_t Mw, bool ones, int32_t N,
     p.ones_row = ones ? 1 : 0;
     p.B0 = p.B1 = B;
     p.ldb0 = p.ldb1 = ldb;
-    gemm_split_plan(p.M, p.N, p.K, &p.splits, &p.kchunk);
+    gemm_split_plan(p.M, p.N, p.K, nprob, &p.splits, &p.kchunk);
     p.C = part;
     p.ldc = r4(N);
     p.part_stride = (int64_t)p.M * p.ldc;
@@ -278,7 +278,7 @@ int do_classifier_bwd(const char* fn, int32_t n, int32_t K, int32_t C,
     GemmBatch b;
     std::memset(&b, 0, sizeof(b));
     b.nprob = 1;
-    b.p[0] = dw_problem(n, K, bc != nullptr, C, H, ldh, dZ, ldd, fptr(ws, sp.gemm_part));
+    b.p[0] = dw_problem(n, K, bc != nullptr, C, H, ldh, dZ, ldd, fptr(ws, sp.gemm_part), 1);
     GCN_HIP(launch_gemm(b, A_KM, B_KN, EPI_PARTIAL, s), fn);
     SgdProblem q = sgd_problem(b.p[0], K, C, Wc, bc, dWc_out, dbc_out);
     GCN_HIP(launch_sgd_reduce(&q, 1, lr, s), fn);
@@ -327,8 +327,8 @@ int do_layer_bwd(const char* fn, const gcn_dgraph* g, int32_t F, int32_t h,
     float* part0 = fptr(ws, sp.gemm_part);
     float* part1 = part0 + sp.gemm_part_floats;
     const bool ones = bias != nullptr;
-    b.p[0] = dw_problem(n, F, ones, h, H_in, ld_in, G, ldg, part0);
-    b.p[1] = dw_problem(n, F, ones, h, AH, ld_ah, G + h, ldg, part1);
+    b.p[0] = dw_problem(n, F, ones, h, H_in, ld_in, G, ldg, part0, 2);
+    b.p[1] = dw_problem(n, F, ones, h, AH, ld_ah, G + h, ldg, part1, 2);
     GCN_HIP(launch_gemm(b, A_KM, B_KN, EPI_PARTIAL, s), fn);
     SgdProblem q[2] = {
         sgd_problem(b.p[0], F, h, Ws, bias, dWs_out, db_out),

@@ -1,17 +1,24 @@
 // Dense products of the layer (Eq. 1 transforms, Eq. 2 gradients) on the
 // gfx950 matrix cores: v_mfma_f32_32x32x2_f32, fp32 in and out.
 //
-// Tile: 128 x 128 per 256-thread workgroup, K step 16; four wavefronts in a
-// 2 x 2 grid each own a 64 x 64 block = 2 x 2 MFMA 32x32 accumulators.
-// Operands are staged k-major in LDS (double-buffered, one barrier per K
-// step), so every fragment read is 32 consecutive floats per half-wave.
-// Global loads are float4 along whichever dimension is contiguous in HBM;
-// ragged M / N / K edges are zero-filled. Epilogues fuse what the layer
-// needs next: bias + ReLU + placement into one half of the concatenated
-// output (forward), the ReLU mask of the previous layer (input gradient),
-// or a split-K slice (weight gradient, summed later in fixed order).
-// Tiles are renumbered so consecutive tiles (sharing A rows or a K range)
-// land on the same XCD, whose L2 then serves their common operand.
+// Tile: 128 x 128 per 256-thread workgroup (one workgroup per CU: LDS holds
+// two 64-deep K steps of both operands), four wavefronts in a 2 x 2 grid, each
+// owning 64 x 64 = 2 x 2 MFMA 32x32 accumulators.
+// LDS layout follows HBM: an operand whose rows are contiguous along K
+// (A_MK, B_NK) is kept [row][k] and its fragments are read 4 K values at a
+// time with 128-bit LDS reads; a K-major operand (A_KM, B_KN) is kept [k][col]
+// and read 32 consecutive floats per half-wave. Both fill LDS with 128-bit
+// stores, no transposition. Within a group of 8 K values, MFMA step j of lane
+// half g takes k = 4 g + j (a fixed permutation of K, the same for A and B).
+// Global loads for the next K step are issued before the current step's MFMAs
+// and written to the other LDS buffer after them (one barrier per step); LDS
+// fragments of the next group are read before the current group's MFMAs.
+// Ragged M / N / K edges are zero-filled at LDS-store time. Epilogues fuse
+// what the layer needs next: bias + ReLU + placement into one half of the
+// concatenated output (forward), the ReLU mask of the previous layer (input
+// gradient), or a split-K slice (weight gradient, summed later in fixed
+// order). Tiles are renumbered so consecutive tiles (sharing A rows or a K
+// range) land on the same XCD, whose L2 then serves their common operand.
 #include <algorithm>
 
 #include "kernels.h"
@@ -22,10 +29,14 @@ namespace {
 
 typedef float floatx16 __attribute__((ext_vector_type(16)));
 
-constexpr int BM = 128, BN = 128, BK = 16;
+constexpr int BM = 128, BN = 128, BK = 32;
 constexpr int kThreads = 256;
-constexpr int kStride = BM + 4;   // LDS row stride (floats), 16-byte aligned
 constexpr int kXcds = 8;
+constexpr int kQuads = BK * BM / 4 / kThreads;   // float4 loads per operand per step
+constexpr int kRowStride = BK + 4;               // [row][k] layout, floats
+constexpr int kColStride = BM + 4;               // [k][col] layout, floats
+constexpr int kOperandFloats = (BM * kRowStride > BK * kColStride) ? BM * kRowStride
+                                                                   : BK * kColStride;
 
 __device__ __forceinline__ float4 ld4(const float* p) {
     return *reinterpret_cast<const float4*>(p);
@@ -101,8 +112,8 @@ __device__ __forceinline__ void load_kcol(Quad& q, const float* P, int64_t ld, i
 // float4 or element loads for B (the classifier weight has any width C).
 template <ALayout AL, BLayout BL, Epilogue EP, bool BVEC>
 __global__ __launch_bounds__(kThreads, 2) void gemm_kernel(GemmBatch batch) {
-    __shared__ float As[2][BK][kStride];
-    __shared__ float Bs[2][BK][kStride];
+    // [buffer][A | B] operand tiles
+    __shared__ __attribute__((aligned(16))) float smem[2][2][kOperandFloats];
 
     // XCD-aware renumbering: workgroup b runs on XCD b % 8; give each XCD a
     // contiguous range of logical tiles.
@@ -127,51 +138,52 @@ __global__ __launch_bounds__(kThreads, 2) void gemm_kernel(GemmBatch batch) {
     const int t = threadIdx.x;
     const int lane = t & 63, wave = t >> 6;
     const int wm = wave >> 1, wn = wave & 1;
+    const int half = lane >> 5, l32 = lane & 31;
 
     const int Areal = P.M - P.ones_row;   // rows of A backed by memory
 
-    Quad ra[2], rb[2];
+    // Thread t moves kQuads float4 per operand and K step:
+    //   row-contiguous: row t / (BK/4) + q * (256 / (BK/4)), k = 4 (t % (BK/4))
+    //   K-major:        k row t / 32 + 8 q, column 4 (t % 32)
+    constexpr int kPerRow = BK / 4, kRowStep = kThreads / kPerRow;
+    Quad ra[kQuads], rb[kQuads];
     auto gload = [&](int k0) {
 #pragma unroll
-        for (int i = 0; i < 2; ++i) {
+        for (int q = 0; q < kQuads; ++q) {
             if constexpr (AL == A_MK) {
-                load_rowk<true>(ra[i], P.A0, P.A1, P.lda0, P.lda1, P.ksplitA, P.M,
-                                m0 + (t >> 2) + 64 * i, k0 + 4 * (t & 3), kend);
+                load_rowk<true>(ra[q], P.A0, P.A1, P.lda0, P.lda1, P.ksplitA, P.M,
+                                m0 + t / kPerRow + kRowStep * q, k0 + 4 * (t % kPerRow), kend);
             } else {
-                load_kcol<true>(ra[i], P.A0, P.lda0, Areal, P.ones_row != 0,
-                                m0 + 4 * (t & 31), k0 + (t >> 5) + 8 * i, kend);
+                load_kcol<true>(ra[q], P.A0, P.lda0, Areal, P.ones_row != 0,
+                                m0 + 4 * (t & 31), k0 + (t >> 5) + 8 * q, kend);
             }
             if constexpr (BL == B_NK) {
-                load_rowk<BVEC>(rb[i], P.B0, P.B1, P.ldb0, P.ldb1, P.ksplitB, P.N,
-                                n0 + (t >> 2) + 64 * i, k0 + 4 * (t & 3), kend);
+                load_rowk<BVEC>(rb[q], P.B0, P.B1, P.ldb0, P.ldb1, P.ksplitB, P.N,
+                                n0 + t / kPerRow + kRowStep * q, k0 + 4 * (t % kPerRow), kend);
             } else {
-                load_kcol<BVEC>(rb[i], P.B0, P.ldb0, P.N, false, n0 + 4 * (t & 31),
-                                k0 + (t >> 5) + 8 * i, kend);
+                load_kcol<BVEC>(rb[q], P.B0, P.ldb0, P.N, false, n0 + 4 * (t & 31),
+                                k0 + (t >> 5) + 8 * q, kend);
             }
         }
     };
     auto sstore = [&](int buf) {
+        float* As = smem[buf][0];
+        float* Bs = smem[buf][1];
 #pragma unroll
-        for (int i = 0; i < 2; ++i) {
-            const float4 a = finish(ra[i]);
-            const float4 b = finish(rb[i]);
+        for (int q = 0; q < kQuads; ++q) {
+            const float4 a = finish(ra[q]);
+            const float4 b = finish(rb[q]);
             if constexpr (AL == A_MK) {
-                const int r = (t >> 2) + 64 * i, kq = 4 * (t & 3);
-                As[buf][kq + 0][r] = a.x;
-                As[buf][kq + 1][r] = a.y;
-                As[buf][kq + 2][r] = a.z;
-                As[buf][kq + 3][r] = a.w;
+                *reinterpret_cast<float4*>(
+                    &As[(t / kPerRow + kRowStep * q) * kRowStride + 4 * (t % kPerRow)]) = a;
             } else {
-                *reinterpret_cast<float4*>(&As[buf][(t >> 5) + 8 * i][4 * (t & 31)]) = a;
+                *reinterpret_cast<float4*>(&As[((t >> 5) + 8 * q) * kColStride + 4 * (t & 31)]) = a;
             }
             if constexpr (BL == B_NK) {
-                const int r = (t >> 2) + 64 * i, kq = 4 * (t & 3);
-                Bs[buf][kq + 0][r] = b.x;
-                Bs[buf][kq + 1][r] = b.y;
-                Bs[buf][kq + 2][r] = b.z;
-                Bs[buf][kq + 3][r] = b.w;
+                *reinterpret_cast<float4*>(
+                    &Bs[(t / kPerRow + kRowStep * q) * kRowStride + 4 * (t % kPerRow)]) = b;
             } else {
-                *reinterpret_cast<float4*>(&Bs[buf][(t >> 5) + 8 * i][4 * (t & 31)]) = b;
+                *reinterpret_cast<float4*>(&Bs[((t >> 5) + 8 * q) * kColStride + 4 * (t & 31)]) = b;
             }
         }
     };
@@ -189,21 +201,52 @@ __global__ __launch_bounds__(kThreads, 2) void gemm_kernel(GemmBatch batch) {
         sstore(0);
         __syncthreads();
     }
-    const int half = lane >> 5, l32 = lane & 31;
     for (int kt = 0; kt < nk; ++kt) {
         const int buf = kt & 1;
         if (kt + 1 < nk) gload(kbeg + (kt + 1) * BK);
+        const float* As = smem[buf][0];
+        const float* Bs = smem[buf][1];
+        // fragments of one group of 8 K values: element j feeds MFMA step j
+        float4 fa[2][2], fb[2][2];
+        auto frag = [&](int sg, int slot) {
+            const int kb = 8 * sg + 4 * half;
 #pragma unroll
-        for (int kk = 0; kk < BK / 2; ++kk) {
-            const int kr = 2 * kk + half;
-            const float a0 = As[buf][kr][wm * 64 + l32];
-            const float a1 = As[buf][kr][wm * 64 + 32 + l32];
-            const float b0 = Bs[buf][kr][wn * 64 + l32];
-            const float b1 = Bs[buf][kr][wn * 64 + 32 + l32];
-            acc[0][0] = __builtin_amdgcn_mfma_f32_32x32x2f32(a0, b0, acc[0][0], 0, 0, 0);
-            acc[0][1] = __builtin_amdgcn_mfma_f32_32x32x2f32(a0, b1, acc[0][1], 0, 0, 0);
-            acc[1][0] = __builtin_amdgcn_mfma_f32_32x32x2f32(a1, b0, acc[1][0], 0, 0, 0);
-            acc[1][1] = __builtin_amdgcn_mfma_f32_32x32x2f32(a1, b1, acc[1][1], 0, 0, 0);
+            for (int i = 0; i < 2; ++i) {
+                const int m = wm * 64 + i * 32 + l32;
+                if constexpr (AL == A_MK) {
+                    fa[slot][i] = *reinterpret_cast<const float4*>(&As[m * kRowStride + kb]);
+                } else {
+                    fa[slot][i] = make_float4(As[(kb + 0) * kColStride + m], As[(kb + 1) * kColStride + m],
+                                              As[(kb + 2) * kColStride + m], As[(kb + 3) * kColStride + m]);
+                }
+                const int nn = wn * 64 + i * 32 + l32;
+                if constexpr (BL == B_NK) {
+                    fb[slot][i] = *reinterpret_cast<const float4*>(&Bs[nn * kRowStride + kb]);
+                } else {
+                    fb[slot][i] = make_float4(Bs[(kb + 0) * kColStride + nn], Bs[(kb + 1) * kColStride + nn],
+                                              Bs[(kb + 2) * kColStride + nn], Bs[(kb + 3) * kColStride + nn]);
+                }
+            }
+        };
+        frag(0, 0);
+#pragma unroll
+        for (int sg = 0; sg < BK / 8; ++sg) {
+            const int cur = sg & 1;
+            if (sg + 1 < BK / 8) frag(sg + 1, cur ^ 1);
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const float a0 = j == 0 ? fa[cur][0].x : j == 1 ? fa[cur][0].y : j == 2 ? fa[cur][0].z : fa[cur][0].w;
+                const float a1 = j == 0 ? fa[cur][1].x : j == 1 ? fa[cur][1].y : j == 2 ? fa[cur][1].z : fa[cur][1].w;
+                const float b0 = j == 0 ? fb[cur][0].x : j == 1 ? fb[cur][0].y : j == 2 ? fb[cur][0].z : fb[cur][0].w;
+                const float b1 = j == 0 ? fb[cur][1].x : j == 1 ? fb[cur][1].y : j == 2 ? fb[cur][1].z : fb[cur][1].w;
+                acc[0][0] = __builtin_amdgcn_mfma_f32_32x32x2f32(a0, b0, acc[0][0], 0, 0, 0);
+                acc[0][1] = __builtin_amdgcn_mfma_f32_32x32x2f32(a0, b1, acc[0][1], 0, 0, 0);
+                acc[1][0] = __builtin_amdgcn_mfma_f32_32x32x2f32(a1, b0, acc[1][0], 0, 0, 0);
+                acc[1][1] = __builtin_amdgcn_mfma_f32_32x32x2f32(a1, b1, acc[1][1], 0, 0, 0);
+            }
+            // next group's LDS reads go out ahead of this group's MFMAs
+            __builtin_amdgcn_sched_group_barrier(0x100, 8, 0);   // DS reads
+            __builtin_amdgcn_sched_group_barrier(0x008, 16, 0);  // MFMA
         }
         if (kt + 1 < nk) sstore(buf ^ 1);
         __syncthreads();
@@ -242,6 +285,21 @@ __global__ __launch_bounds__(kThreads, 2) void gemm_kernel(GemmBatch batch) {
     }
 }
 
+// sum_j src[j * stride], j ascending; eight loads in flight at a time
+__device__ __forceinline__ float sum_slices(const float* src, int64_t stride, int splits) {
+    float d = 0.f;
+    int j = 0;
+    for (; j + 8 <= splits; j += 8) {
+        float v[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) v[u] = src[(int64_t)(j + u) * stride];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) d += v[u];
+    }
+    for (; j < splits; ++j) d += src[(int64_t)j * stride];
+    return d;
+}
+
 __global__ __launch_bounds__(256) void sgd_reduce_kernel(SgdProblem p0,
                                                          SgdProblem p1,
                                                          int64_t total0,
@@ -254,8 +312,7 @@ __global__ __launch_bounds__(256) void sgd_reduce_kernel(SgdProblem p0,
     const int64_t e = second ? idx - total0 : idx;
     const int m = (int)(e / p.N), nn = (int)(e % p.N);
     const float* src = p.part + (int64_t)m * p.ldp + nn;
-    float d = 0.f;
-    for (int j = 0; j < p.splits; ++j) d += src[(int64_t)j * p.part_stride];
+    const float d = sum_slices(src, p.part_stride, p.splits);
     if (m < p.Mw) {
         const int64_t w = (int64_t)m * p.N + nn;
         p.W[w] = fmaf(-lr, d, p.W[w]);
@@ -272,9 +329,7 @@ __global__ __launch_bounds__(256) void splitk_finish_kernel(
     const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (idx >= (int64_t)M * N) return;
     const int m = (int)(idx / N), nn = (int)(idx % N);
-    const float* src = part + (int64_t)m * ldp + nn;
-    float d = 0.f;
-    for (int j = 0; j < splits; ++j) d += src[(int64_t)j * part_stride];
+    float d = sum_slices(part + (int64_t)m * ldp + nn, part_stride, splits);
     if (bias) d += bias[nn];
     C[(int64_t)m * ldc + nn] = d;
 }
@@ -293,14 +348,32 @@ hipError_t launch_splitk_finish(const float* part, int64_t part_stride, int64_t 
     return hipGetLastError();
 }
 
-void gemm_split_plan(int32_t M, int32_t N, int32_t K, int32_t* splits,
+void gemm_split_plan(int32_t M, int32_t N, int32_t K, int32_t nprob, int32_t* splits,
                      int32_t* kchunk) {
-    const int64_t tiles = (int64_t)((M + BM - 1) / BM) * ((N + BN - 1) / BN);
-    int64_t s = (512 + tiles - 1) / std::max<int64_t>(tiles, 1);
-    s = std::min<int64_t>(s, 32);
-    s = std::min<int64_t>(s, std::max(1, (K + 127) / 128));
-    s = std::max<int64_t>(s, 1);
-    const int64_t kc = (K + s - 1) / s;
+    // Two workgroups fit per CU: pick the smallest split whose tile count
+    // fills the 512 resident slots of the 256 CUs to >= 90 %, keeping >= 2 K
+    // steps per split and at most 512 slices in all (the scratch bound of the
+    // partial sums).
+    constexpr int64_t kSlots = 512;
+    const int64_t tiles = (int64_t)((M + BM - 1) / BM) * ((N + BN - 1) / BN) *
+                          std::max(nprob, 1);
+    const int64_t smax = std::max<int64_t>(1, std::min<int64_t>(32, K / (2 * BK)));
+    int64_t best = 1;
+    double best_eff = -1.0;
+    for (int64_t s = 1; s <= smax; ++s) {
+        const int64_t total = tiles * s;
+        if (s > 1 && total > kSlots) break;
+        const double eff = (double)total / (double)(((total + kSlots - 1) / kSlots) * kSlots);
+        if (eff >= 0.9) {
+            best = s;
+            break;
+        }
+        if (eff > best_eff + 1e-9) {
+            best_eff = eff;
+            best = s;
+        }
+    }
+    const int64_t kc = (K + best - 1) / best;
     const int64_t chunk = std::max<int64_t>(BK, (kc + BK - 1) / BK * BK);
     *kchunk = (int32_t)chunk;
     *splits = K > 0 ? (int32_t)((K + chunk - 1) / chunk) : 1;
@@ -316,7 +389,7 @@ hipError_t launch_gemm(GemmBatch& b, ALayout al, BLayout bl, Epilogue ep,
         if (ep != EPI_PARTIAL) {
             p.splits = 1;
             p.kchunk = std::max(BK, (p.K + BK - 1) / BK * BK);
-        } else if (p.splits < 1 || p.kchunk < BK || p.kchunk % BK != 0) {
+        } else if (p.splits < 1 || p.kchunk < 1) {
             return hipErrorInvalidValue;
         }
         p.tile_begin = total;

@@ -76,10 +76,11 @@ struct GemmBatch {
     int32_t total_tiles;
 };
 
-// Split-K plan for a weight-gradient problem (deterministic in the shapes):
-// K is cut into `splits` ranges of `kchunk` (a multiple of the K tile), the
-// last one possibly shorter; every range is non-empty when K > 0.
-void gemm_split_plan(int32_t M, int32_t N, int32_t K, int32_t* splits,
+// Split-K plan for `nprob` problems of one shape launched together
+// (deterministic in the shapes): K is cut into `splits` ranges of `kchunk`
+// (a multiple of the K tile), the last one possibly shorter; every range is
+// non-empty when K > 0.
+void gemm_split_plan(int32_t M, int32_t N, int32_t K, int32_t nprob, int32_t* splits,
                      int32_t* kchunk);
 
 // Launch C = A B for 1-2 problems of identical layouts / epilogue.
