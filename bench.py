@@ -39,6 +39,8 @@ def parse():
     ap.add_argument("--profile-steps", type=int, default=10)
     ap.add_argument("--seg-len", type=int, default=0,
                     help="list segment length of the device work list (0: library default)")
+    ap.add_argument("--graph", action="store_true",
+                    help="replay the step from a captured HIP graph")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
                     help="CPU oracle sample budget (seconds of work)")
@@ -88,14 +90,31 @@ class Setup:
         self.gcn.train_step(self.dg, self.desc, self.P, self.X, self.labels, self.wl.lr,
                             self.loss, self.ws)
 
-    def timed(self, steps, warmup):
+    def capture(self):
+        """Record one step into a HIP graph (stream capture on a side stream)."""
         import torch
-        for _ in range(warmup):
+        self.step()                       # warm: first launches load code objects
+        torch.cuda.synchronize()
+        self.graph = torch.cuda.CUDAGraph()
+        s = torch.cuda.Stream()
+        with torch.cuda.stream(s):
+            self.graph.capture_begin()
             self.step()
+            self.graph.capture_end()
+        torch.cuda.synchronize()
+
+    def timed(self, steps, warmup, graph=False):
+        import torch
+        run = self.step
+        if graph:
+            self.capture()
+            run = self.graph.replay
+        for _ in range(warmup):
+            run()
         torch.cuda.synchronize()
         t0 = time.perf_counter()
         for _ in range(steps):
-            self.step()
+            run()
         torch.cuda.synchronize()
         return (time.perf_counter() - t0) / steps
 
@@ -183,12 +202,12 @@ def main():
     print(f"[bench] workload {wl.name}: inputs ready", file=sys.stderr, flush=True)
 
     red = Setup(wl, wl.reduce, inp, args.seg_len)
-    ms = 1e3 * red.timed(args.steps, args.warmup)
+    ms = 1e3 * red.timed(args.steps, args.warmup, args.graph)
     print(f"[bench] timed {args.steps} steps: {ms:.3f} ms/step", file=sys.stderr, flush=True)
     direct = None
     if wl.reduce:
         d = Setup(dataclasses.replace(wl, reduce=False), False, inp, args.seg_len)
-        direct = 1e3 * d.timed(args.steps, args.warmup)
+        direct = 1e3 * d.timed(args.steps, args.warmup, args.graph)
         print(f"[bench] direct aggregation: {direct:.3f} ms/step", file=sys.stderr, flush=True)
         del d
     prof = red.profile(args.profile_steps)
@@ -226,6 +245,7 @@ def main():
         "scaling": "weak",
         "vs_baseline": None,
         "dtype": "f32",
+        "launch": "hip-graph replay" if args.graph else "eager stream launches",
         "data": "synthetic",
         "config": {
             "workload": (f"{wl.name}: {wl.L}-layer GCN step on a {wl.n}-vertex Chung-Lu "

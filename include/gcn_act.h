@@ -65,7 +65,7 @@ const char* gcn_last_error(void);
 
 /* ABI version of this header (bumped on incompatible change). */
 int gcn_abi_version(void);
-#define GCN_ABI_VERSION 1
+#define GCN_ABI_VERSION 2
 
 /* ------------------------------------------------ subgraph (host, a1)
  * gcn_subgraph_build - undirected simple subgraph in CSR form.
@@ -145,7 +145,10 @@ void gcn_reduced_free(gcn_reduced_t r);
 /* ------------------------------------------------ device graph image
  * The device form of G_s^# (what the accelerator receives in Section 4.1:
  * the lists, the pairs and D), plus a work list that splits long lists
- * into segments of at most `seg_len` entries for load balance.
+ * into segments of at most `seg_len` entries for load balance, and each pair
+ * sum's expansion into original vertices (the pair sum of Section 4.2 step 1
+ * is the sum of those rows), so that all pair sums of all rounds can be
+ * formed in one pass instead of one dependent pass per round.
  * gcn_graph_image_bytes - size of the packed image (host and device).
  * gcn_graph_pack        - write the image into a caller host buffer (may
  *                         be pinned); the reduced object may then be freed.
@@ -153,18 +156,23 @@ void gcn_reduced_free(gcn_reduced_t r);
  *                         `stream` (hipMemcpyAsync; the host buffer must
  *                         stay valid until the copy completes) and fill the
  *                         descriptor, whose pointers are into dev_buf.
- * seg_len: 0 selects the default (64); otherwise 1..65536.
+ * seg_len: 0 selects the default (32); otherwise 1..65536.
  */
 typedef struct {
     int32_t n, naux, rounds, seg_len;
     int32_t nseg, nlong, nslots, max_row;
     int64_t nnz;
+    int64_t exp_nnz;           /* total expansion length             */
     const int32_t* rowptr;     /* device int32[n+1]                  */
     const int32_t* col;        /* device int32[nnz]                  */
     const int32_t* pairs;      /* device int32[2*naux]               */
     const float* inv_deg;      /* device float[n], 1/d (0 if d == 0) */
     const int32_t* seg;        /* device int32[4*nseg]               */
     const int32_t* longrows;   /* device int32[4*nlong]              */
+    const int32_t* exp_col;    /* device int32[exp_nnz]: original
+                                  vertices of pair sum k, ascending  */
+    const int32_t* exp_seg;    /* device int32[4*naux]: (k, begin,
+                                  end, -1) into exp_col              */
     int32_t round_offsets[GCN_MAX_ROUNDS + 1];   /* host copy        */
 } gcn_dgraph;
 
@@ -189,9 +197,10 @@ int gcn_scratch_bytes(const gcn_dgraph* g, int32_t n, int32_t max_width,
 /* ---------------------------------------------- aggregation (a3 a4 a10)
  * gcn_aggregate - Y = D^-1 A X (GCN_AGG_MEAN, forward aggregation of Eq. 1)
  * or Y = A D^-1 X (GCN_AGG_TRANSPOSED, the aggregation inside Eq. 2c), run
- * on G_s^#: pair sums are formed round by round first (Section 4.2 step 1),
- * then the lists are summed (step 2) and scaled by the original 1/d (step 3,
- * after the sum for MEAN; on the gathered original rows for TRANSPOSED).
+ * on G_s^#: the pair sums of every round are formed first (Section 4.2 step
+ * 1; each from its expansion into original rows, in one pass), then the
+ * lists are summed (step 2) and scaled by the original 1/d (step 3, after
+ * the sum for MEAN; on the gathered original rows for TRANSPOSED).
  * Vertices with d == 0 get zero rows.
  *   X  device [n x F] ld ldx;  Y  device [n x F] ld ldy (X and Y must not
  *   overlap). Scratch: pair sums and partial sums of split lists.

@@ -1,8 +1,10 @@
-// Feature aggregation on G_s^# (Section 4.2): pair sums round by round
-// (step 1), list sums (step 2) and the degree scaling (step 3, fused).
+// Feature aggregation on G_s^# (Section 4.2): pair sums (step 1), list sums
+// (step 2) and the degree scaling (step 3, fused). The pair sums of all
+// rounds are formed in one launch, each from its expansion into original
+// rows (a list like any other), so no launch waits on an earlier round.
 //
 // Work decomposition (gfx950, 64-lane wavefronts): a group of GL lanes
-// (16, 32 or 64, chosen from the feature width) owns one pair or one list
+// (16, 32 or 64, chosen from the feature width) owns one pair sum or one list
 // segment and sweeps the feature row in float4 chunks, NCH chunks per lane,
 // so every neighbour-row gather is a coalesced run of GL*16 bytes. The
 // group loads up to GL neighbour ids at once (one per lane) and broadcasts
@@ -93,44 +95,6 @@ __device__ __forceinline__ Slice slice_of(int nsl, int slice_f4, int nf4) {
     const int sl = (int)(blockIdx.x % nsl);
     const int b = sl * slice_f4;
     return {b, min(nf4, b + slice_f4)};
-}
-
-template <int GL, int NCH, bool PRE>
-__global__ __launch_bounds__(kBlock) void pair_sums_kernel(
-    const int32_t* __restrict__ pairs, int k0, int k1, RowSource src,
-    const float* __restrict__ inv_deg, float* __restrict__ aux,
-    int64_t ldaux, int F, int nsl, int slice_f4) {
-    const int lane = (int)threadIdx.x % GL;
-    const int k = k0 + group_index<GL>(nsl);
-    if (k >= k1) return;
-    const int p = pairs[2 * k], q = pairs[2 * k + 1];
-    const float* rp = row_of(src, p);
-    const float* rq = row_of(src, q);
-    float sp = 1.0f, sq = 1.0f;
-    if (PRE) {
-        if (p < src.n) sp = inv_deg[p];
-        if (q < src.n) sq = inv_deg[q];
-    }
-    float* out = aux + (int64_t)k * ldaux;
-    const Slice sl = slice_of(nsl, slice_f4, (F + 3) >> 2);
-    for (int base = sl.c4_begin; base < sl.c4_end; base += GL * NCH) {
-#pragma unroll
-        for (int j = 0; j < NCH; ++j) {
-            const int c4 = base + lane + j * GL;
-            if (c4 < sl.c4_end) {
-                float4 a = ld4(rp + 4 * c4), b = ld4(rq + 4 * c4), v;
-                if (PRE) {
-                    v.x = fmaf(sp, a.x, sq * b.x);
-                    v.y = fmaf(sp, a.y, sq * b.y);
-                    v.z = fmaf(sp, a.z, sq * b.z);
-                    v.w = fmaf(sp, a.w, sq * b.w);
-                } else {
-                    v = make_float4(a.x + b.x, a.y + b.y, a.z + b.z, a.w + b.w);
-                }
-                st4(out + 4 * c4, v);   // scratch rows: padding may be written
-            }
-        }
-    }
 }
 
 // One group per segment (row, begin, end, slot) of the work list.
@@ -295,24 +259,26 @@ int blocks_for(int groups, const Shape& sh) {
 
 }  // namespace
 
-hipError_t launch_pair_sums(const int32_t* pairs, int32_t k0, int32_t k1,
-                            RowSource src, const float* inv_deg, bool prescale,
-                            float* aux, int64_t ldaux, int32_t F,
-                            hipStream_t s) {
-    if (k1 <= k0 || F <= 0) return hipSuccess;
+hipError_t launch_pair_sums(const gcn_dgraph* g, RowSource src, bool prescale,
+                            float* aux, int64_t ldaux, int32_t F, hipStream_t s) {
+    if (g->naux <= 0 || F <= 0) return hipSuccess;
     const Shape sh = pick_shape(F);
-    const dim3 grid(blocks_for(k1 - k0, sh)), block(kBlock);
-    const double np_ = (double)(k1 - k0);
-    ProfScope prof(s, K_PAIR_SUMS, np_ * F * (prescale ? 3.0 : 1.0), np_ * (12.0 * F + 8.0));
-#define GCN_LAUNCH_PAIR(GL_, NCH_)                                                  \
-    if (sh.gl == GL_ && sh.nch == NCH_) {                                           \
-        if (prescale)                                                               \
-            pair_sums_kernel<GL_, NCH_, true><<<grid, block, 0, s>>>(               \
-                pairs, k0, k1, src, inv_deg, aux, ldaux, F, sh.nsl, sh.slice_f4);   \
-        else                                                                        \
-            pair_sums_kernel<GL_, NCH_, false><<<grid, block, 0, s>>>(              \
-                pairs, k0, k1, src, inv_deg, aux, ldaux, F, sh.nsl, sh.slice_f4);   \
-        return hipGetLastError();                                                   \
+    const int4* seg = reinterpret_cast<const int4*>(g->exp_seg);
+    const dim3 grid(blocks_for(g->naux, sh)), block(kBlock);
+    const double e = (double)g->exp_nnz, k = (double)g->naux;
+    // one gather per expansion entry, its id, one write per pair sum
+    ProfScope prof(s, K_PAIR_SUMS, e * F * (prescale ? 2.0 : 1.0), 4.0 * F * e + 4.0 * e + 4.0 * F * k);
+#define GCN_LAUNCH_PAIR(GL_, NCH_)                                                    \
+    if (sh.gl == GL_ && sh.nch == NCH_) {                                             \
+        if (prescale)                                                                 \
+            list_sums_kernel<GL_, NCH_, true, false><<<grid, block, 0, s>>>(          \
+                seg, g->naux, g->exp_col, src, g->inv_deg, aux, ldaux, nullptr, 0, F, \
+                sh.nsl, sh.slice_f4);                                                 \
+        else                                                                          \
+            list_sums_kernel<GL_, NCH_, false, false><<<grid, block, 0, s>>>(         \
+                seg, g->naux, g->exp_col, src, g->inv_deg, aux, ldaux, nullptr, 0, F, \
+                sh.nsl, sh.slice_f4);                                                 \
+        return hipGetLastError();                                                     \
     }
     GCN_SHAPES(GCN_LAUNCH_PAIR)
 #undef GCN_LAUNCH_PAIR

@@ -86,6 +86,8 @@ int check_graph(const char* fn, const gcn_dgraph* g) {
                   "%s: graph descriptor round offsets inconsistent", fn);
     GCN_CHECK_ARG(g->n == 0 || (g->rowptr && g->inv_deg && g->seg),
                   "%s: graph descriptor has NULL arrays", fn);
+    GCN_CHECK_ARG(g->naux == 0 || (g->exp_col && g->exp_seg && g->exp_nnz >= 2 * (int64_t)g->naux),
+                  "%s: graph descriptor lacks pair-sum expansions", fn);
     return GCN_OK;
 }
 
@@ -129,10 +131,7 @@ int do_aggregate(const char* fn, const gcn_dgraph* g, bool transposed, int32_t F
     float* aux = fptr(ws, sp.aux);
     float* part = fptr(ws, sp.part_list);
     RowSource src{X, ldx, aux, ldaux, g->n};
-    for (int r = 0; r < g->rounds; ++r)
-        GCN_HIP(launch_pair_sums(g->pairs, g->round_offsets[r], g->round_offsets[r + 1],
-                                 src, g->inv_deg, transposed, aux, ldaux, F, s),
-                fn);
+    GCN_HIP(launch_pair_sums(g, src, transposed, aux, ldaux, F, s), fn);
     GCN_HIP(launch_list_sums(g, src, transposed, !transposed, Y, ldy, part, ldaux, F, s), fn);
     return GCN_OK;
 }

@@ -31,12 +31,13 @@ struct ImageHeader {
     int32_t n, naux, rounds, seg_len;
     int32_t nseg, nlong, nslots, max_row;
     int32_t pad0;
-    int64_t nnz;
+    int64_t nnz, exp_nnz;
     int64_t off_rowptr, off_col, off_pairs, off_inv_deg, off_seg, off_longrows;
+    int64_t off_exp_col, off_exp_seg;
     int64_t total;
     int32_t round_offsets[GCN_MAX_ROUNDS + 1];
 };
-constexpr uint32_t kImageMagic = 0x47434e31u;  // "GCN1"
-constexpr int kDefaultSegLen = 64;
+constexpr uint32_t kImageMagic = 0x47434e32u;  // "GCN2"
+constexpr int kDefaultSegLen = 32;
 
 }  // namespace gcn

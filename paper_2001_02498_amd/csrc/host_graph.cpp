@@ -464,6 +464,24 @@ static int plan_image(gcn_reduced_t r, int32_t seg_len, gcn::ImageHeader* h) {
     h->off_inv_deg = take(4 * (int64_t)r->n);
     h->off_seg = take(16 * nseg);
     h->off_longrows = take(16 * nlong);
+    // expansion sizes: |E(k)| = |E(p_k)| + |E(q_k)|, originals count 1
+    int64_t exp_nnz = 0;
+    {
+        std::vector<int64_t> sz(r->naux);
+        for (int32_t k = 0; k < r->naux; ++k) {
+            int64_t t = 0;
+            for (int e = 0; e < 2; ++e) {
+                const int32_t c = r->pairs[2 * k + e];
+                t += c < r->n ? 1 : sz[c - r->n];
+            }
+            sz[k] = t;
+            exp_nnz += t;
+        }
+    }
+    GCN_CHECK_ARG(exp_nnz < INT32_MAX, "graph image: pair-sum expansions too long");
+    h->exp_nnz = exp_nnz;
+    h->off_exp_col = take(4 * exp_nnz);
+    h->off_exp_seg = take(16 * (int64_t)r->naux);
     h->total = off;
     for (int i = 0; i <= r->rounds; ++i) h->round_offsets[i] = r->round_offsets[i];
     return GCN_OK;
@@ -527,6 +545,28 @@ int gcn_graph_pack(gcn_reduced_t r, int32_t seg_len, void* host_buf,
         seg[4 * s + 3] = -1;
         ++s;
     }
+    // Expansion of every pair sum into original vertices, ascending: the
+    // members of pair k are the members of its two parts (earlier ids).
+    int32_t* ecol = reinterpret_cast<int32_t*>(base + h.off_exp_col);
+    int32_t* eseg = reinterpret_cast<int32_t*>(base + h.off_exp_seg);
+    int32_t pos = 0;
+    for (int32_t k = 0; k < r->naux; ++k) {
+        const int32_t b = pos;
+        for (int e = 0; e < 2; ++e) {
+            const int32_t c = r->pairs[2 * k + e];
+            if (c < r->n) {
+                ecol[pos++] = c;
+            } else {
+                const int32_t* src = eseg + 4 * (c - r->n);
+                for (int32_t i = src[1]; i < src[2]; ++i) ecol[pos++] = ecol[i];
+            }
+        }
+        std::sort(ecol + b, ecol + pos);
+        eseg[4 * k + 0] = k;
+        eseg[4 * k + 1] = b;
+        eseg[4 * k + 2] = pos;
+        eseg[4 * k + 3] = -1;
+    }
     return GCN_OK;
 }
 
@@ -557,6 +597,9 @@ int gcn_graph_describe(const void* host_image, size_t bytes,
     out->inv_deg = reinterpret_cast<const float*>(d + h.off_inv_deg);
     out->seg = reinterpret_cast<const int32_t*>(d + h.off_seg);
     out->longrows = reinterpret_cast<const int32_t*>(d + h.off_longrows);
+    out->exp_nnz = h.exp_nnz;
+    out->exp_col = reinterpret_cast<const int32_t*>(d + h.off_exp_col);
+    out->exp_seg = reinterpret_cast<const int32_t*>(d + h.off_exp_seg);
     for (int i = 0; i <= h.rounds; ++i) out->round_offsets[i] = h.round_offsets[i];
     return GCN_OK;
 }

@@ -19,10 +19,10 @@ struct RowSource {
     int32_t n;
 };
 
-// Pair sums of one reduction round: aux[k] = s(p_k) src(p_k) + s(q_k) src(q_k)
-// for k in [k0, k1), s(c) = 1/d_c for original vertices when prescale, else 1.
-hipError_t launch_pair_sums(const int32_t* pairs, int32_t k0, int32_t k1,
-                            RowSource src, const float* inv_deg, bool prescale,
+// Pair sums of all rounds in one pass: aux[k] = sum over the original
+// vertices v of pair k's expansion of s(v) X[v], s(v) = 1/d_v when
+// prescale, else 1.
+hipError_t launch_pair_sums(const gcn_dgraph* g, RowSource src, bool prescale,
                             float* aux, int64_t ldaux, int32_t F, hipStream_t s);
 
 // Segment sums of G_s^# lists (see the work list of gcn_graph_pack), then the

@@ -36,7 +36,7 @@ PREC_FP32 = 0
 PREC_BF16 = 1
 AGG_MEAN = 0
 AGG_TRANSPOSED = 1
-ABI_VERSION = 1
+ABI_VERSION = 2
 
 _i32, _i64, _f32 = C.c_int32, C.c_int64, C.c_float
 _vp, _sz = C.c_void_p, C.c_size_t
@@ -64,9 +64,9 @@ class RrRound(C.Structure):
 class DGraph(C.Structure):
     _fields_ = [("n", _i32), ("naux", _i32), ("rounds", _i32), ("seg_len", _i32),
                 ("nseg", _i32), ("nlong", _i32), ("nslots", _i32), ("max_row", _i32),
-                ("nnz", _i64),
+                ("nnz", _i64), ("exp_nnz", _i64),
                 ("rowptr", _vp), ("col", _vp), ("pairs", _vp), ("inv_deg", _vp),
-                ("seg", _vp), ("longrows", _vp),
+                ("seg", _vp), ("longrows", _vp), ("exp_col", _vp), ("exp_seg", _vp),
                 ("round_offsets", _i32 * (MAX_ROUNDS + 1))]
 
 

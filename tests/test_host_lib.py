@@ -185,6 +185,9 @@ def _unpack_image(buf, nbytes):
         inv_deg=view(d.inv_deg, d.n, np.float32),
         seg=view(d.seg, 4 * d.nseg, np.int32).reshape(-1, 4),
         longrows=view(d.longrows, 4 * d.nlong, np.int32).reshape(-1, 4) if d.nlong
+        else np.zeros((0, 4), np.int32),
+        exp_col=view(d.exp_col, d.exp_nnz, np.int32) if d.exp_nnz else np.zeros(0, np.int32),
+        exp_seg=view(d.exp_seg, 4 * d.naux, np.int32).reshape(-1, 4) if d.naux
         else np.zeros((0, 4), np.int32))
 
 
@@ -201,7 +204,7 @@ def test_device_image_work_list(seg_len):
     buf = buf[off:off + nbytes]
     gcn.pack(red, buf.ctypes.data, nbytes, seg_len)
     d, sec = _unpack_image(buf, nbytes)
-    L = seg_len or 64
+    L = seg_len or 32
     assert d.seg_len == L and d.n == wl.n and d.naux == info["naux"]
     assert np.array_equal(sec["rowptr"], info["rowptr"])
     assert np.array_equal(sec["col"], info["col"])
@@ -230,6 +233,13 @@ def test_device_image_work_list(seg_len):
     for row, first, ns, _ in sec["longrows"]:
         assert slots[row] == list(range(first, first + ns))
     assert d.nslots == sum(len(v) for v in slots.values())
+    # pair sum k expands into the original vertices of the oracle's expansion
+    assert d.naux > 0
+    for k, (kk, b, e, slot) in enumerate(sec["exp_seg"]):
+        assert kk == k and slot == -1
+        want = sorted(rd.expand(wl.n + k, wl.n, info["pairs"]))
+        assert sec["exp_col"][b:e].tolist() == want
+    assert sec["exp_seg"][-1][2] == d.exp_nnz
     # image corruption is rejected
     bad = buf.copy()
     bad[:4] = 0
