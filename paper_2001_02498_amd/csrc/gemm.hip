@@ -51,17 +51,18 @@ __device__ __forceinline__ void zero_from(float4& v, int valid) {
 }
 
 // Operand loads are split in two halves so that prefetching never waits:
-// the load half only issues memory reads (predicated on bounds) and records
-// how many of the four elements are valid; the store half, run after the
-// MFMA work of the current K step, zero-fills the invalid tail and writes
-// LDS. Out-of-range elements inside a float4 stay inside the padded row.
+// the load half only issues memory reads and records how many of the four
+// elements are valid; the store half, run during the MFMA work of the
+// current K step, zero-fills the invalid tail and writes LDS. Vector loads
+// are branchless (an empty quad reads the operand's first 16 bytes instead)
+// so that a whole K step is one basic block the scheduler can interleave.
 struct Quad {
     float4 v;
     int valid;   // elements [0, valid) are real; the rest become 0
     int one;     // element index that is an implicit 1, or -1
 };
 
-__device__ __forceinline__ float4 finish(Quad q) {
+__device__ __forceinline__ float4 finish(const Quad& q) {
     float4 v = q.v;
     zero_from(v, q.valid);
     if (q.one == 0) v.x = 1.f;
@@ -72,12 +73,12 @@ __device__ __forceinline__ float4 finish(Quad q) {
 }
 
 template <bool VEC>
-__device__ __forceinline__ void issue(Quad& q, const float* p, int valid) {
+__device__ __forceinline__ void issue(Quad& q, const float* p, const float* safe, int valid) {
     q.valid = valid;
-    q.v = make_float4(0.f, 0.f, 0.f, 0.f);
     if constexpr (VEC) {
-        if (valid > 0) q.v = ld4(p);
+        q.v = ld4(valid > 0 ? p : safe);
     } else {
+        q.v = make_float4(0.f, 0.f, 0.f, 0.f);
         if (valid > 0) q.v.x = p[0];
         if (valid > 1) q.v.y = p[1];
         if (valid > 2) q.v.z = p[2];
@@ -85,28 +86,16 @@ __device__ __forceinline__ void issue(Quad& q, const float* p, int valid) {
     }
 }
 
-// Row-contiguous operand (A_MK rows = m, or B_NK rows = n), K-concatenated:
-// element (r, k) at P0[r*ld0 + k] for k < ksplit, else P1[r*ld1 + k-ksplit].
-template <bool VEC>
-__device__ __forceinline__ void load_rowk(Quad& q, const float* P0, const float* P1,
-                                          int64_t ld0, int64_t ld1, int ksplit,
-                                          int rows, int r, int k, int kend) {
-    q.one = -1;
-    const bool live = r < rows && k < kend;
-    const float* p = k < ksplit ? P0 + (int64_t)r * ld0 + k
-                                : P1 + (int64_t)r * ld1 + (k - ksplit);
-    issue<VEC>(q, p, live ? kend - k : 0);
-}
+// Per-thread view of one operand quad: which row / column it covers.
+struct RowQuad {      // row-contiguous operand: row r, K offset kofs
+    const float* p0;  // row r of the first K-concatenated part
+    const float* p1;  // row r of the second part
+    bool live;        // r inside the operand
+};
 
-// K-major operand (A_KM or B_KN): element (c, k) at P[k*ld + c], c < cols;
-// with ones, column c == cols is an implicit 1 (bias gradient row).
-template <bool VEC>
-__device__ __forceinline__ void load_kcol(Quad& q, const float* P, int64_t ld, int cols,
-                                          bool ones, int c, int k, int kend) {
-    const bool krow = k < kend;
-    q.one = (ones && krow && cols - c >= 0 && cols - c < 4) ? cols - c : -1;
-    issue<VEC>(q, P + (int64_t)k * ld + c, (krow && c < cols) ? cols - c : 0);
-}
+struct ColQuad {      // K-major operand: columns c..c+3 of K row kofs + k0
+    int c;
+};
 
 // A rows are always 16-byte aligned (checked on the host); BVEC selects
 // float4 or element loads for B (the classifier weight has any width C).
@@ -140,51 +129,86 @@ __global__ __launch_bounds__(kThreads, 2) void gemm_kernel(GemmBatch batch) {
     const int wm = wave >> 1, wn = wave & 1;
     const int half = lane >> 5, l32 = lane & 31;
 
-    const int Areal = P.M - P.ones_row;   // rows of A backed by memory
+    // operand descriptors, fixed for the whole K loop
+    const float* const A0 = P.A0;
+    const float* const B0 = P.B0;
+    const int M = P.M, N = P.N;
+    const int Areal = M - P.ones_row;   // rows of A backed by memory
+    const bool ones = P.ones_row != 0;
+    const int ksplitA = P.ksplitA, ksplitB = P.ksplitB;
+    const int64_t lda0 = P.lda0, ldb0 = P.ldb0;
 
     // Thread t moves kQuads float4 per operand and K step:
     //   row-contiguous: row t / (BK/4) + q * (256 / (BK/4)), k = 4 (t % (BK/4))
     //   K-major:        k row t / 32 + 8 q, column 4 (t % 32)
     constexpr int kPerRow = BK / 4, kRowStep = kThreads / kPerRow;
-    Quad ra[kQuads], rb[kQuads];
-    auto gload = [&](int k0) {
+    const int rk = 4 * (t % kPerRow);   // K offset of a row-contiguous quad
+    const int kr = t >> 5;              // K row of a K-major quad (+ 8 q)
+    RowQuad arow[kQuads], brow[kQuads];
+    ColQuad acol, bcol;
+    acol.c = m0 + 4 * (t & 31);
+    bcol.c = n0 + 4 * (t & 31);
 #pragma unroll
-        for (int q = 0; q < kQuads; ++q) {
-            if constexpr (AL == A_MK) {
-                load_rowk<true>(ra[q], P.A0, P.A1, P.lda0, P.lda1, P.ksplitA, P.M,
-                                m0 + t / kPerRow + kRowStep * q, k0 + 4 * (t % kPerRow), kend);
-            } else {
-                load_kcol<true>(ra[q], P.A0, P.lda0, Areal, P.ones_row != 0,
-                                m0 + 4 * (t & 31), k0 + (t >> 5) + 8 * q, kend);
-            }
-            if constexpr (BL == B_NK) {
-                load_rowk<BVEC>(rb[q], P.B0, P.B1, P.ldb0, P.ldb1, P.ksplitB, P.N,
-                                n0 + t / kPerRow + kRowStep * q, k0 + 4 * (t % kPerRow), kend);
-            } else {
-                load_kcol<BVEC>(rb[q], P.B0, P.ldb0, P.N, false, n0 + 4 * (t & 31),
-                                k0 + (t >> 5) + 8 * q, kend);
-            }
+    for (int q = 0; q < kQuads; ++q) {
+        if constexpr (AL == A_MK) {
+            const int r = m0 + t / kPerRow + kRowStep * q;
+            arow[q].live = r < M;
+            const int rr = arow[q].live ? r : 0;
+            arow[q].p0 = A0 + (int64_t)rr * lda0;
+            arow[q].p1 = P.A1 + (int64_t)rr * P.lda1;
+        }
+        if constexpr (BL == B_NK) {
+            const int r = n0 + t / kPerRow + kRowStep * q;
+            brow[q].live = r < N;
+            const int rr = brow[q].live ? r : 0;
+            brow[q].p0 = B0 + (int64_t)rr * ldb0;
+            brow[q].p1 = P.B1 + (int64_t)rr * P.ldb1;
+        }
+    }
+
+    Quad ra[kQuads], rb[kQuads];
+    auto gload_a = [&](int k0, int q) {
+        if constexpr (AL == A_MK) {
+            const int k = k0 + rk;
+            const float* p = k < ksplitA ? arow[q].p0 + k : arow[q].p1 + (k - ksplitA);
+            ra[q].one = -1;
+            issue<true>(ra[q], p, A0, (arow[q].live && k < kend) ? kend - k : 0);
+        } else {
+            const int k = k0 + kr + 8 * q;
+            const int c = acol.c;
+            const bool krow = k < kend;
+            ra[q].one = (ones && krow && Areal - c >= 0 && Areal - c < 4) ? Areal - c : -1;
+            issue<true>(ra[q], A0 + (int64_t)k * lda0 + c, A0, (krow && c < Areal) ? Areal - c : 0);
         }
     };
-    auto sstore = [&](int buf) {
+    auto gload_b = [&](int k0, int q) {
+        if constexpr (BL == B_NK) {
+            const int k = k0 + rk;
+            const float* p = k < ksplitB ? brow[q].p0 + k : brow[q].p1 + (k - ksplitB);
+            rb[q].one = -1;
+            issue<BVEC>(rb[q], p, B0, (brow[q].live && k < kend) ? kend - k : 0);
+        } else {
+            const int k = k0 + kr + 8 * q;
+            const int c = bcol.c;
+            const bool krow = k < kend;
+            rb[q].one = -1;
+            issue<BVEC>(rb[q], B0 + (int64_t)k * ldb0 + c, B0, (krow && c < N) ? N - c : 0);
+        }
+    };
+    auto sstore = [&](int buf, int q) {
         float* As = smem[buf][0];
         float* Bs = smem[buf][1];
-#pragma unroll
-        for (int q = 0; q < kQuads; ++q) {
-            const float4 a = finish(ra[q]);
-            const float4 b = finish(rb[q]);
-            if constexpr (AL == A_MK) {
-                *reinterpret_cast<float4*>(
-                    &As[(t / kPerRow + kRowStep * q) * kRowStride + 4 * (t % kPerRow)]) = a;
-            } else {
-                *reinterpret_cast<float4*>(&As[((t >> 5) + 8 * q) * kColStride + 4 * (t & 31)]) = a;
-            }
-            if constexpr (BL == B_NK) {
-                *reinterpret_cast<float4*>(
-                    &Bs[(t / kPerRow + kRowStep * q) * kRowStride + 4 * (t % kPerRow)]) = b;
-            } else {
-                *reinterpret_cast<float4*>(&Bs[((t >> 5) + 8 * q) * kColStride + 4 * (t & 31)]) = b;
-            }
+        const float4 a = finish(ra[q]);
+        const float4 b = finish(rb[q]);
+        if constexpr (AL == A_MK) {
+            *reinterpret_cast<float4*>(&As[(t / kPerRow + kRowStep * q) * kRowStride + rk]) = a;
+        } else {
+            *reinterpret_cast<float4*>(&As[(kr + 8 * q) * kColStride + 4 * (t & 31)]) = a;
+        }
+        if constexpr (BL == B_NK) {
+            *reinterpret_cast<float4*>(&Bs[(t / kPerRow + kRowStep * q) * kRowStride + rk]) = b;
+        } else {
+            *reinterpret_cast<float4*>(&Bs[(kr + 8 * q) * kColStride + 4 * (t & 31)]) = b;
         }
     };
 
@@ -196,60 +220,93 @@ __global__ __launch_bounds__(kThreads, 2) void gemm_kernel(GemmBatch batch) {
 #pragma unroll
             for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
+    // fragments of one group of 8 K values: element j feeds MFMA step j
+    float4 fa[2][2], fb[2][2];
+    auto frag = [&](const float* As, const float* Bs, int sg, int fslot) {
+        const int kb = 8 * sg + 4 * half;
+#pragma unroll
+        for (int i = 0; i < 2; ++i) {
+            const int m = wm * 64 + i * 32 + l32;
+            if constexpr (AL == A_MK) {
+                fa[fslot][i] = *reinterpret_cast<const float4*>(&As[m * kRowStride + kb]);
+            } else {
+                fa[fslot][i] = make_float4(As[(kb + 0) * kColStride + m], As[(kb + 1) * kColStride + m],
+                                           As[(kb + 2) * kColStride + m], As[(kb + 3) * kColStride + m]);
+            }
+            const int nn = wn * 64 + i * 32 + l32;
+            if constexpr (BL == B_NK) {
+                fb[fslot][i] = *reinterpret_cast<const float4*>(&Bs[nn * kRowStride + kb]);
+            } else {
+                fb[fslot][i] = make_float4(Bs[(kb + 0) * kColStride + nn], Bs[(kb + 1) * kColStride + nn],
+                                           Bs[(kb + 2) * kColStride + nn], Bs[(kb + 3) * kColStride + nn]);
+            }
+        }
+    };
+    auto mfma_group = [&](int fslot) {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const float a0 = j == 0 ? fa[fslot][0].x : j == 1 ? fa[fslot][0].y : j == 2 ? fa[fslot][0].z : fa[fslot][0].w;
+            const float a1 = j == 0 ? fa[fslot][1].x : j == 1 ? fa[fslot][1].y : j == 2 ? fa[fslot][1].z : fa[fslot][1].w;
+            const float b0 = j == 0 ? fb[fslot][0].x : j == 1 ? fb[fslot][0].y : j == 2 ? fb[fslot][0].z : fb[fslot][0].w;
+            const float b1 = j == 0 ? fb[fslot][1].x : j == 1 ? fb[fslot][1].y : j == 2 ? fb[fslot][1].z : fb[fslot][1].w;
+            acc[0][0] = __builtin_amdgcn_mfma_f32_32x32x2f32(a0, b0, acc[0][0], 0, 0, 0);
+            acc[0][1] = __builtin_amdgcn_mfma_f32_32x32x2f32(a0, b1, acc[0][1], 0, 0, 0);
+            acc[1][0] = __builtin_amdgcn_mfma_f32_32x32x2f32(a1, b0, acc[1][0], 0, 0, 0);
+            acc[1][1] = __builtin_amdgcn_mfma_f32_32x32x2f32(a1, b1, acc[1][1], 0, 0, 0);
+        }
+    };
+
+    static_assert(BK / 8 == 4, "the K step is laid out as four groups of 8");
     if (nk > 0) {
-        gload(kbeg);
-        sstore(0);
+#pragma unroll
+        for (int q = 0; q < kQuads; ++q) {
+            gload_a(kbeg, q);
+            gload_b(kbeg, q);
+            sstore(0, q);
+        }
         __syncthreads();
+        frag(smem[0][0], smem[0][1], 0, 0);
     }
     for (int kt = 0; kt < nk; ++kt) {
         const int buf = kt & 1;
-        if (kt + 1 < nk) gload(kbeg + (kt + 1) * BK);
         const float* As = smem[buf][0];
         const float* Bs = smem[buf][1];
-        // fragments of one group of 8 K values: element j feeds MFMA step j
-        float4 fa[2][2], fb[2][2];
-        auto frag = [&](int sg, int slot) {
-            const int kb = 8 * sg + 4 * half;
+        const int knext = kbeg + (kt + 1) * BK;   // past kend on the last step: empty quads
+        // group 0: next group's fragments, the next K step's global loads
+        frag(As, Bs, 1, 1);
 #pragma unroll
-            for (int i = 0; i < 2; ++i) {
-                const int m = wm * 64 + i * 32 + l32;
-                if constexpr (AL == A_MK) {
-                    fa[slot][i] = *reinterpret_cast<const float4*>(&As[m * kRowStride + kb]);
-                } else {
-                    fa[slot][i] = make_float4(As[(kb + 0) * kColStride + m], As[(kb + 1) * kColStride + m],
-                                              As[(kb + 2) * kColStride + m], As[(kb + 3) * kColStride + m]);
-                }
-                const int nn = wn * 64 + i * 32 + l32;
-                if constexpr (BL == B_NK) {
-                    fb[slot][i] = *reinterpret_cast<const float4*>(&Bs[nn * kRowStride + kb]);
-                } else {
-                    fb[slot][i] = make_float4(Bs[(kb + 0) * kColStride + nn], Bs[(kb + 1) * kColStride + nn],
-                                              Bs[(kb + 2) * kColStride + nn], Bs[(kb + 3) * kColStride + nn]);
-                }
-            }
-        };
-        frag(0, 0);
-#pragma unroll
-        for (int sg = 0; sg < BK / 8; ++sg) {
-            const int cur = sg & 1;
-            if (sg + 1 < BK / 8) frag(sg + 1, cur ^ 1);
-#pragma unroll
-            for (int j = 0; j < 4; ++j) {
-                const float a0 = j == 0 ? fa[cur][0].x : j == 1 ? fa[cur][0].y : j == 2 ? fa[cur][0].z : fa[cur][0].w;
-                const float a1 = j == 0 ? fa[cur][1].x : j == 1 ? fa[cur][1].y : j == 2 ? fa[cur][1].z : fa[cur][1].w;
-                const float b0 = j == 0 ? fb[cur][0].x : j == 1 ? fb[cur][0].y : j == 2 ? fb[cur][0].z : fb[cur][0].w;
-                const float b1 = j == 0 ? fb[cur][1].x : j == 1 ? fb[cur][1].y : j == 2 ? fb[cur][1].z : fb[cur][1].w;
-                acc[0][0] = __builtin_amdgcn_mfma_f32_32x32x2f32(a0, b0, acc[0][0], 0, 0, 0);
-                acc[0][1] = __builtin_amdgcn_mfma_f32_32x32x2f32(a0, b1, acc[0][1], 0, 0, 0);
-                acc[1][0] = __builtin_amdgcn_mfma_f32_32x32x2f32(a1, b0, acc[1][0], 0, 0, 0);
-                acc[1][1] = __builtin_amdgcn_mfma_f32_32x32x2f32(a1, b1, acc[1][1], 0, 0, 0);
-            }
-            // next group's LDS reads go out ahead of this group's MFMAs
-            __builtin_amdgcn_sched_group_barrier(0x100, 8, 0);   // DS reads
-            __builtin_amdgcn_sched_group_barrier(0x008, 16, 0);  // MFMA
+        for (int q = 0; q < kQuads; ++q) {
+            gload_a(knext, q);
+            gload_b(knext, q);
         }
-        if (kt + 1 < nk) sstore(buf ^ 1);
+        mfma_group(0);
+        __builtin_amdgcn_sched_group_barrier(0x100, 8, 0);      // DS reads first
+#pragma unroll
+        for (int q = 0; q < 2 * kQuads; ++q) {
+            __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);  // one global load
+            __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);  // two MFMAs
+        }
+        __builtin_amdgcn_sched_barrier(0);
+        // groups 1, 2
+        frag(As, Bs, 2, 0);
+        mfma_group(1);
+        __builtin_amdgcn_sched_barrier(0);
+        frag(As, Bs, 3, 1);
+        mfma_group(0);
+        __builtin_amdgcn_sched_barrier(0);
+        // group 3: the next K step goes into the other buffer (read by no
+        // one since the barrier ending the previous step)
+#pragma unroll
+        for (int q = 0; q < kQuads; ++q) sstore(buf ^ 1, q);
+        mfma_group(1);
+#pragma unroll
+        for (int q = 0; q < 2 * kQuads; ++q) {
+            __builtin_amdgcn_sched_group_barrier(0x200, 1, 0);  // one LDS store
+            __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);  // two MFMAs
+        }
+        __builtin_amdgcn_sched_barrier(0);
         __syncthreads();
+        if (kt + 1 < nk) frag(smem[buf ^ 1][0], smem[buf ^ 1][1], 0, 0);
     }
 
     // Epilogue. Accumulator element r of lane l is C[i][j] of the 32x32
