@@ -287,18 +287,17 @@ __global__ __launch_bounds__(kThreads, 2) void gemm_kernel(GemmBatch batch) {
             __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);  // two MFMAs
         }
         __builtin_amdgcn_sched_barrier(0);
-        // groups 1, 2
+        // group 1
         frag(As, Bs, 2, 0);
         mfma_group(1);
         __builtin_amdgcn_sched_barrier(0);
+        // group 2: the next K step goes into the other buffer, whose last
+        // reader (the previous step) finished before the previous barrier
         frag(As, Bs, 3, 1);
-        mfma_group(0);
-        __builtin_amdgcn_sched_barrier(0);
-        // group 3: the next K step goes into the other buffer (read by no
-        // one since the barrier ending the previous step)
 #pragma unroll
         for (int q = 0; q < kQuads; ++q) sstore(buf ^ 1, q);
-        mfma_group(1);
+        mfma_group(0);
+        __builtin_amdgcn_sched_group_barrier(0x100, 8, 0);      // DS reads first
 #pragma unroll
         for (int q = 0; q < 2 * kQuads; ++q) {
             __builtin_amdgcn_sched_group_barrier(0x200, 1, 0);  // one LDS store
@@ -306,7 +305,11 @@ __global__ __launch_bounds__(kThreads, 2) void gemm_kernel(GemmBatch batch) {
         }
         __builtin_amdgcn_sched_barrier(0);
         __syncthreads();
+        // group 3: its fragments are already in registers, so the next
+        // step's first LDS reads are hidden behind these MFMAs
         if (kt + 1 < nk) frag(smem[buf ^ 1][0], smem[buf ^ 1][1], 0, 0);
+        mfma_group(1);
+        __builtin_amdgcn_sched_barrier(0);
     }
 
     // Epilogue. Accumulator element r of lane l is C[i][j] of the 32x32
