@@ -245,6 +245,8 @@ int gcn_classifier_fwd(int32_t n, int32_t K, int32_t C, const float* H,
  *                dz   = (sigmoid(z) - y) / (n C);        labels uint8[n*C]
  *   logits, dlogits [n x C] (ld ldz, ldd; may be the same buffer);
  *   loss_out device float[1]. Deterministic (fixed summation order).
+ *   C <= 512 (GCN_E_UNSUPPORTED above; the same limit holds for the
+ *   training step).
  * Errors: labels are not range-checked on the device; class ids outside
  * [0, C) give an undefined loss but no out-of-bounds access. */
 int gcn_loss(int32_t n, int32_t C, int32_t kind, const float* logits,

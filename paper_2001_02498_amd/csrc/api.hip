@@ -172,10 +172,18 @@ int do_layer_fwd(const char* fn, const gcn_dgraph* g, int32_t F, int32_t h,
     return GCN_OK;
 }
 
+// Logits as split-K slices (or in place when not split): slices j at
+// part + j*stride, leading dimension ldp; bias not yet added when split.
+struct Logits {
+    const float* part;
+    int64_t stride, ldp;
+    int32_t splits;
+};
+
 int do_classifier_fwd(const char* fn, int32_t n, int32_t K, int32_t C,
                       const float* H, int64_t ldh, const float* Wc,
                       const float* bc, float* Z, int64_t ldz, const ScratchPlan& sp,
-                      void* ws, hipStream_t s) {
+                      void* ws, hipStream_t s, bool finish, Logits* out) {
     GemmBatch b;
     std::memset(&b, 0, sizeof(b));
     b.nprob = 1;
@@ -189,7 +197,8 @@ int do_classifier_fwd(const char* fn, int32_t n, int32_t K, int32_t C,
     p.B0 = p.B1 = Wc;
     p.ldb0 = p.ldb1 = C;
     p.ksplitB = K;
-    // A few output tiles cannot fill the GPU: split K, then sum the slices.
+    // A few output tiles cannot fill the GPU: split K, then sum the slices
+    // (with the bias) either here or inside the loss kernel.
     const int64_t tiles = (int64_t)((n + 127) / 128) * ((C + 127) / 128);
     int32_t splits = 1, kchunk = 0;
     if (tiles < 192) gemm_split_plan(n, C, K, 1, &splits, &kchunk);
@@ -201,7 +210,10 @@ int do_classifier_fwd(const char* fn, int32_t n, int32_t K, int32_t C,
         p.part_stride = (int64_t)n * p.ldc;
         b.p[0] = p;
         GCN_HIP(launch_gemm(b, A_MK, B_KN, EPI_PARTIAL, s), fn);
-        GCN_HIP(launch_splitk_finish(p.C, p.part_stride, p.ldc, splits, n, C, bc, Z, ldz, s), fn);
+        if (out) *out = Logits{p.C, p.part_stride, p.ldc, splits};
+        if (finish)
+            GCN_HIP(launch_splitk_finish(p.C, p.part_stride, p.ldc, splits, n, C, bc, Z, ldz, s),
+                    fn);
         return GCN_OK;
     }
     p.C = Z;
@@ -209,6 +221,7 @@ int do_classifier_fwd(const char* fn, int32_t n, int32_t K, int32_t C,
     p.bias = bc;
     b.p[0] = p;
     GCN_HIP(launch_gemm(b, A_MK, B_KN, EPI_BIAS, s), fn);
+    if (out) *out = Logits{Z, 0, ldz, 1};
     return GCN_OK;
 }
 
@@ -383,6 +396,10 @@ int check_desc(const char* fn, const gcn_model_desc* d) {
     GCN_CHECK_ARG(d->f_in >= 1, "%s: f_in < 1", fn);
     GCN_CHECK_ARG(d->h >= 4 && d->h % 4 == 0, "%s: h=%d must be a positive multiple of 4", fn, d->h);
     GCN_CHECK_ARG(d->C >= 1, "%s: C < 1", fn);
+    if (d->C > 64 * kMaxLossVPL) {
+        set_error("%s: C=%d above the %d classes of the loss kernel", fn, d->C, 64 * kMaxLossVPL);
+        return GCN_E_UNSUPPORTED;
+    }
     GCN_CHECK_ARG(d->loss == GCN_LOSS_SOFTMAX_CE || d->loss == GCN_LOSS_SIGMOID_BCE,
                   "%s: unknown loss %d", fn, d->loss);
     GCN_CHECK_ARG(d->ld_x >= d->f_in && d->ld_x % 4 == 0,
@@ -471,7 +488,7 @@ int gcn_classifier_fwd(int32_t n, int32_t K, int32_t C, const float* H, int64_t 
     const ScratchPlan sp = plan_scratch(n, 0, 0, std::max(K, C));
     GCN_TRY(check_ws(fn, ws, ws_bytes, sp.total));
     return do_classifier_fwd(fn, n, K, C, H, ldh, W_cls, b_cls, logits, ldz, sp, ws,
-                             (hipStream_t)stream);
+                             (hipStream_t)stream, true, nullptr);
 }
 
 int gcn_loss(int32_t n, int32_t C, int32_t kind, const float* logits, int64_t ldz,
@@ -481,6 +498,10 @@ int gcn_loss(int32_t n, int32_t C, int32_t kind, const float* logits, int64_t ld
     GCN_CHECK_ARG(n >= 0 && C >= 1, "%s: bad sizes", fn);
     GCN_CHECK_ARG(kind == GCN_LOSS_SOFTMAX_CE || kind == GCN_LOSS_SIGMOID_BCE,
                   "%s: unknown loss %d", fn, kind);
+    if (C > 64 * kMaxLossVPL) {
+        set_error("%s: C=%d above the %d classes of the loss kernel", fn, C, 64 * kMaxLossVPL);
+        return GCN_E_UNSUPPORTED;
+    }
     GCN_TRY(check_mat(fn, "logits", logits, n, C, ldz));
     GCN_TRY(check_mat(fn, "dlogits", dlogits, n, C, ldd));
     GCN_CHECK_ARG(n == 0 || labels != nullptr, "%s: labels is NULL", fn);
@@ -625,10 +646,14 @@ int gcn_train_step(const gcn_dgraph* g, const gcn_model_desc* d, const gcn_param
     // classifier + loss
     float* Z = act(sl.pub.logits);
     float* dZ = act(sl.pub.dlogits);
-    GCN_TRY(do_classifier_fwd(fn, (int32_t)n, 2 * h, C, Hprev, ldH, P->W_cls,
-                              d->has_bias ? P->b_cls : nullptr, Z, ldC, sp, scratch, s));
-    GCN_HIP(launch_loss((int32_t)n, C, d->loss, Z, ldC, labels, dZ, ldC,
-                        fptr(scratch, sp.rowloss), loss_out, s),
+    Logits lg;
+    const float* bcls = d->has_bias ? P->b_cls : nullptr;
+    GCN_TRY(do_classifier_fwd(fn, (int32_t)n, 2 * h, C, Hprev, ldH, P->W_cls, bcls, Z, ldC,
+                              sp, scratch, s, false, &lg));
+    // split logits are summed (with the bias) inside the loss kernel
+    GCN_HIP(launch_loss_parts((int32_t)n, C, d->loss, lg.part, lg.stride, lg.splits, lg.ldp,
+                              lg.splits > 1 ? bcls : nullptr, Z, ldC, labels, dZ, ldC,
+                              fptr(scratch, sp.rowloss), loss_out, s),
             fn);
     // backward (classifier, then Eq. 2a-2c layer by layer)
     float* Gcur = act(sl.pub.G[L - 1]);

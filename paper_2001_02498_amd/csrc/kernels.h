@@ -110,9 +110,16 @@ hipError_t launch_sgd_reduce(const SgdProblem* p, int nprob, float lr,
                              hipStream_t s);
 
 // ---------------------------------------------------------------- loss
+constexpr int kMaxLossVPL = 8;   // classes per lane: C <= 512
 hipError_t launch_loss(int32_t n, int32_t C, int32_t kind, const float* z,
                        int64_t ldz, const void* labels, float* dz,
                        int64_t ldd, float* rowloss, float* loss_out,
                        hipStream_t s);
+// The same with logits = sum of `splits` slices (stride apart, ld ldp) plus
+// bias, written to z_out.
+hipError_t launch_loss_parts(int32_t n, int32_t C, int32_t kind, const float* part,
+                             int64_t stride, int32_t splits, int64_t ldp, const float* bias,
+                             float* z_out, int64_t ldz, const void* labels, float* dz,
+                             int64_t ldd, float* rowloss, float* loss_out, hipStream_t s);
 
 }  // namespace gcn

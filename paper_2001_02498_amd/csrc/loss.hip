@@ -1,8 +1,10 @@
 // Classifier loss and its gradient w.r.t. the logits (Section 2.1: softmax
 // with cross-entropy, whose gradient is a subtraction; the multi-label
 // workloads use a sigmoid with binary cross-entropy). One wavefront per
-// vertex row; per-row losses are then summed by a single workgroup in a
-// fixed order, so the scalar loss is bitwise reproducible.
+// vertex row, the row's logits in registers (summed from the classifier's
+// split-K slices when it was split, which also writes the logits); per-row
+// losses are then summed by a single workgroup in a fixed order, so the
+// scalar loss is bitwise reproducible.
 #include "kernels.h"
 #include "prof.h"
 
@@ -21,62 +23,104 @@ __device__ __forceinline__ float wave_sum(float v) {
     return v;
 }
 
-__global__ __launch_bounds__(256) void softmax_ce_kernel(
-    int n, int C, const float* __restrict__ z, int64_t ldz,
-    const int32_t* __restrict__ labels, float* __restrict__ dz, int64_t ldd,
-    float* __restrict__ rowloss) {
-    const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
-    const int lane = threadIdx.x & 63;
-    if (row >= n) return;
-    const float* zr = z + (int64_t)row * ldz;
-    float m = -INFINITY;
-    for (int c = lane; c < C; c += 64) m = fmaxf(m, zr[c]);
-    m = wave_max(m);
-    float s = 0.f;
-    for (int c = lane; c < C; c += 64) s += expf(zr[c] - m);
-    s = wave_sum(s);
-    const int y = labels[row];
-    const bool y_ok = y >= 0 && y < C;
-    const float zy = y_ok ? zr[y] : 0.f;
-    const float inv_s = 1.0f / s;
-    const float inv_n = 1.0f / (float)n;
-    float* dr = dz + (int64_t)row * ldd;
-    for (int c = lane; c < C; c += 64) {
-        const float p = expf(zr[c] - m) * inv_s;
-        dr[c] = (p - (c == y ? 1.0f : 0.0f)) * inv_n;
+// sum_j src[j * stride], j ascending; eight loads in flight at a time
+__device__ __forceinline__ float sum_slices(const float* src, int64_t stride, int splits) {
+    float d = 0.f;
+    int j = 0;
+    for (; j + 8 <= splits; j += 8) {
+        float v[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) v[u] = src[(int64_t)(j + u) * stride];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) d += v[u];
     }
-    if (lane == 0) rowloss[row] = (m + logf(s)) - zy;
+    for (; j < splits; ++j) d += src[(int64_t)j * stride];
+    return d;
 }
 
-__global__ __launch_bounds__(256) void sigmoid_bce_kernel(
-    int n, int C, const float* __restrict__ z, int64_t ldz,
-    const uint8_t* __restrict__ labels, float* __restrict__ dz, int64_t ldd,
-    float* __restrict__ rowloss) {
+// One wavefront per row; lane l holds logits l, l+64, ... (VPL per lane).
+// The logits are the sum of `splits` split-K slices (one slice: the logits
+// themselves) plus the optional bias; they are written to z_out (if it
+// differs from the slices) and kept in registers for the loss.
+template <int VPL, bool BCE>
+__global__ __launch_bounds__(256) void loss_kernel(
+    int n, int C, const float* __restrict__ part, int64_t stride, int splits, int64_t ldp,
+    const float* __restrict__ bias, float* z_out, int64_t ldz, const void* __restrict__ labels,
+    float* __restrict__ dz, int64_t ldd, float* __restrict__ rowloss) {
     const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
     const int lane = threadIdx.x & 63;
     if (row >= n) return;
-    const float* zr = z + (int64_t)row * ldz;
-    const uint8_t* yr = labels + (int64_t)row * C;
-    float* dr = dz + (int64_t)row * ldd;
-    const float scale = 1.0f / ((float)n * (float)C);
-    float acc = 0.f;
-    for (int c = lane; c < C; c += 64) {
-        const float v = zr[c];
-        const float y = yr[c] ? 1.0f : 0.0f;
-        acc += fmaxf(v, 0.f) - v * y + log1pf(expf(-fabsf(v)));
-        const float sig = 1.0f / (1.0f + expf(-v));
-        dr[c] = (sig - y) * scale;
+    const bool write_z = z_out != part;
+    float v[VPL];
+#pragma unroll
+    for (int i = 0; i < VPL; ++i) {
+        const int c = lane + 64 * i;
+        v[i] = 0.f;
+        if (c < C) {
+            v[i] = sum_slices(part + (int64_t)row * ldp + c, stride, splits);
+            if (bias) v[i] += bias[c];
+            if (write_z) z_out[(int64_t)row * ldz + c] = v[i];
+        }
     }
-    acc = wave_sum(acc);
-    if (lane == 0) rowloss[row] = acc;
+    float* dr = dz + (int64_t)row * ldd;
+    if constexpr (!BCE) {
+        const int y = static_cast<const int32_t*>(labels)[row];
+        float m = -INFINITY;
+#pragma unroll
+        for (int i = 0; i < VPL; ++i)
+            if (lane + 64 * i < C) m = fmaxf(m, v[i]);
+        m = wave_max(m);
+        float ssum = 0.f;
+#pragma unroll
+        for (int i = 0; i < VPL; ++i)
+            if (lane + 64 * i < C) ssum += expf(v[i] - m);
+        ssum = wave_sum(ssum);
+        float zy = 0.f;
+#pragma unroll
+        for (int i = 0; i < VPL; ++i)
+            if (lane + 64 * i == y) zy = v[i];
+        zy = wave_sum(zy);   // exactly one lane holds z_y (none: label out of range)
+        const float inv_s = 1.0f / ssum, inv_n = 1.0f / (float)n;
+#pragma unroll
+        for (int i = 0; i < VPL; ++i) {
+            const int c = lane + 64 * i;
+            if (c < C) dr[c] = (expf(v[i] - m) * inv_s - (c == y ? 1.0f : 0.0f)) * inv_n;
+        }
+        if (lane == 0) rowloss[row] = (m + logf(ssum)) - zy;
+    } else {
+        const uint8_t* yr = static_cast<const uint8_t*>(labels) + (int64_t)row * C;
+        const float scale = 1.0f / ((float)n * (float)C);
+        float acc = 0.f;
+#pragma unroll
+        for (int i = 0; i < VPL; ++i) {
+            const int c = lane + 64 * i;
+            if (c < C) {
+                const float z = v[i];
+                const float y = yr[c] ? 1.0f : 0.0f;
+                acc += fmaxf(z, 0.f) - z * y + log1pf(expf(-fabsf(z)));
+                dr[c] = (1.0f / (1.0f + expf(-z)) - y) * scale;
+            }
+        }
+        acc = wave_sum(acc);
+        if (lane == 0) rowloss[row] = acc;
+    }
 }
 
 // Fixed-order reduction: thread t sums rows t, t+256, ...; then a tree.
 __global__ __launch_bounds__(256) void mean_kernel(int n, const float* __restrict__ rowloss,
                                                    float denom, float* __restrict__ out) {
     __shared__ float part[256];
+    // thread t sums rows t, t+256, ... in order, eight loads in flight
     float s = 0.f;
-    for (int i = threadIdx.x; i < n; i += 256) s += rowloss[i];
+    int i = threadIdx.x;
+    for (; i + 7 * 256 < n; i += 8 * 256) {
+        float v[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) v[u] = rowloss[i + u * 256];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) s += v[u];
+    }
+    for (; i < n; i += 256) s += rowloss[i];
     part[threadIdx.x] = s;
     __syncthreads();
     for (int w = 128; w >= 1; w >>= 1) {
@@ -88,18 +132,29 @@ __global__ __launch_bounds__(256) void mean_kernel(int n, const float* __restric
 
 }  // namespace
 
-hipError_t launch_loss(int32_t n, int32_t C, int32_t kind, const float* z,
-                       int64_t ldz, const void* labels, float* dz, int64_t ldd,
-                       float* rowloss, float* loss_out, hipStream_t s) {
+hipError_t launch_loss_parts(int32_t n, int32_t C, int32_t kind, const float* part,
+                             int64_t stride, int32_t splits, int64_t ldp, const float* bias,
+                             float* z_out, int64_t ldz, const void* labels, float* dz,
+                             int64_t ldd, float* rowloss, float* loss_out, hipStream_t s) {
+    if (C > 64 * kMaxLossVPL) return hipErrorInvalidValue;
     if (n > 0) {
         const dim3 grid((n + 3) / 4), block(256);
-        ProfScope prof(s, K_LOSS_ROWS, 8.0 * n * C, 8.0 * n * C + 4.0 * n);
-        if (kind == GCN_LOSS_SOFTMAX_CE)
-            softmax_ce_kernel<<<grid, block, 0, s>>>(
-                n, C, z, ldz, static_cast<const int32_t*>(labels), dz, ldd, rowloss);
-        else
-            sigmoid_bce_kernel<<<grid, block, 0, s>>>(
-                n, C, z, ldz, static_cast<const uint8_t*>(labels), dz, ldd, rowloss);
+        ProfScope prof(s, K_LOSS_ROWS, (double)n * C * (8.0 + splits),
+                       4.0 * (double)n * C * (splits + 2.0) + 4.0 * n);
+        const int vpl = (C + 63) / 64;
+#define GCN_LOSS_CASE(V_)                                                                 \
+        if (vpl <= V_) {                                                                  \
+            if (kind == GCN_LOSS_SOFTMAX_CE)                                              \
+                loss_kernel<V_, false><<<grid, block, 0, s>>>(n, C, part, stride, splits, \
+                    ldp, bias, z_out, ldz, labels, dz, ldd, rowloss);                     \
+            else                                                                          \
+                loss_kernel<V_, true><<<grid, block, 0, s>>>(n, C, part, stride, splits,  \
+                    ldp, bias, z_out, ldz, labels, dz, ldd, rowloss);                     \
+        } else
+        GCN_LOSS_CASE(1) GCN_LOSS_CASE(2) GCN_LOSS_CASE(4) GCN_LOSS_CASE(8) {
+            return hipErrorInvalidValue;
+        }
+#undef GCN_LOSS_CASE
         hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
     }
@@ -107,6 +162,13 @@ hipError_t launch_loss(int32_t n, int32_t C, int32_t kind, const float* z,
     ProfScope prof(s, K_LOSS_MEAN, (double)n, 4.0 * n);
     mean_kernel<<<dim3(1), dim3(256), 0, s>>>(n, rowloss, denom > 0 ? denom : 1.0f, loss_out);
     return hipGetLastError();
+}
+
+hipError_t launch_loss(int32_t n, int32_t C, int32_t kind, const float* z, int64_t ldz,
+                       const void* labels, float* dz, int64_t ldd, float* rowloss,
+                       float* loss_out, hipStream_t s) {
+    return launch_loss_parts(n, C, kind, z, 0, 1, ldz, nullptr, const_cast<float*>(z), ldz,
+                             labels, dz, ldd, rowloss, loss_out, s);
 }
 
 }  // namespace gcn
