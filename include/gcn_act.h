@@ -186,6 +186,46 @@ int gcn_graph_upload(const void* host_image, size_t bytes, void* dev_buf,
 int gcn_graph_describe(const void* host_image, size_t bytes,
                        const void* dev_buf, gcn_dgraph* out);
 
+/* ---------------------------------------- host preparation pipeline (a13)
+ * Section 4.4: subgraphs are independent, so while the device trains on one
+ * minibatch the host prepares the next ones, several at once. A pipeline
+ * owns `workers` host threads; each submitted subgraph is built
+ * (gcn_subgraph_build), reduced (gcn_redundancy_reduce with `params`) and
+ * packed (gcn_graph_pack) into a host buffer (page-locked when pinned != 0,
+ * so uploads are asynchronous DMA). Results come back in submission order.
+ * gcn_pipeline_submit - copies the edge arrays (the caller may free them on
+ *   return) and queues the job; *job_id receives its number (0, 1, ...).
+ * gcn_pipeline_next - waits for the oldest job not yet taken and returns its
+ *   image (valid until gcn_pipeline_release) and timings. A failed job
+ *   returns its error code (the pipeline keeps going). At most `depth` jobs
+ *   are prepared ahead or held by the caller: release taken jobs to let the
+ *   workers continue; taking a job while holding `depth` others returns
+ *   GCN_E_INVALID_ARG instead of waiting forever.
+ * gcn_pipeline_release - returns a taken job's buffer to the pool (after any
+ *   asynchronous copy from it has completed).
+ * gcn_pipeline_destroy - stops the workers (after their current job) and
+ *   frees every buffer.
+ */
+typedef struct gcn_pipeline* gcn_pipeline_t;
+typedef struct {
+    int32_t n, naux, rounds, reserved;
+    int64_t nnz;          /* list entries of G_s^#     */
+    int64_t nnz_direct;   /* list entries of G_s       */
+    double build_ms, reduce_ms, pack_ms;   /* host time of this job */
+} gcn_pipeline_info;
+
+int gcn_pipeline_create(const gcn_rr_params* params, int32_t seg_len,
+                        int32_t workers, int32_t depth, int32_t pinned,
+                        gcn_pipeline_t* out);
+int gcn_pipeline_submit(gcn_pipeline_t p, int64_t n_full, const int64_t* src,
+                        const int64_t* dst, int64_t n_edges,
+                        const int64_t* vertices, int64_t n_vertices,
+                        int64_t* job_id);
+int gcn_pipeline_next(gcn_pipeline_t p, int64_t* job_id, const void** image,
+                      size_t* bytes, gcn_pipeline_info* info);
+int gcn_pipeline_release(gcn_pipeline_t p, int64_t job_id);
+void gcn_pipeline_destroy(gcn_pipeline_t p);
+
 /* ------------------------------------------------------- scratch size
  * Bytes of `ws` needed by gcn_aggregate / gcn_layer_fwd / gcn_layer_bwd /
  * gcn_classifier_* / gcn_loss for widths up to max_width and row count of

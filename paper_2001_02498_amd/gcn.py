@@ -143,6 +143,21 @@ _prof_enable = _proto("gcn_profile_enable", [_i32])
 _prof_disable = _proto("gcn_profile_disable", [])
 _prof_read = _proto("gcn_profile_read", [C.POINTER(ProfileEntry), _i32, _pi32, _i32])
 
+class PipelineInfo(C.Structure):
+    _fields_ = [("n", _i32), ("naux", _i32), ("rounds", _i32), ("reserved", _i32),
+                ("nnz", _i64), ("nnz_direct", _i64), ("build_ms", C.c_double),
+                ("reduce_ms", C.c_double), ("pack_ms", C.c_double)]
+
+
+_pipe_create = _proto("gcn_pipeline_create", [C.POINTER(RrParams), _i32, _i32, _i32, _i32,
+                                              C.POINTER(_vp)])
+_pipe_submit = _proto("gcn_pipeline_submit", [_vp, _i64, _vp, _vp, _i64, _vp, _i64,
+                                              C.POINTER(_i64)])
+_pipe_next = _proto("gcn_pipeline_next", [_vp, C.POINTER(_i64), C.POINTER(_vp), C.POINTER(_sz),
+                                          C.POINTER(PipelineInfo)])
+_pipe_release = _proto("gcn_pipeline_release", [_vp, _i64])
+_pipe_destroy = _proto("gcn_pipeline_destroy", [_vp], None)
+
 EXPORTS = [
     "gcn_last_error", "gcn_abi_version", "gcn_subgraph_build", "gcn_graph_info",
     "gcn_graph_free", "gcn_redundancy_reduce", "gcn_reduced_info", "gcn_reduced_free",
@@ -150,7 +165,8 @@ EXPORTS = [
     "gcn_scratch_bytes", "gcn_aggregate", "gcn_layer_fwd", "gcn_classifier_fwd",
     "gcn_loss", "gcn_classifier_bwd", "gcn_layer_bwd", "gcn_workspace_layout",
     "gcn_workspace_bytes", "gcn_train_step", "gcn_profile_enable", "gcn_profile_disable",
-    "gcn_profile_read",
+    "gcn_profile_read", "gcn_pipeline_create", "gcn_pipeline_submit", "gcn_pipeline_next",
+    "gcn_pipeline_release", "gcn_pipeline_destroy",
 ]
 
 
@@ -432,3 +448,52 @@ def profile_read(reset=True):
                                        min_ms=buf[i].min_ms, max_ms=buf[i].max_ms,
                                        flops=buf[i].flops, bytes=buf[i].bytes)
             for i in range(min(cnt.value, 32))}
+
+
+# ------------------------------------------------------ preparation pipeline
+
+class Pipeline:
+    """Host worker pool preparing graph images in submission order."""
+
+    def __init__(self, theta=2, max_rounds=5, max_aux=-1, seg_len=0, workers=4, depth=8,
+                 pinned=True, num_threads=1):
+        p = RrParams(int(theta), int(max_rounds), int(max_aux), int(num_threads), 0)
+        self._h = _vp()
+        _check(_pipe_create(C.byref(p), int(seg_len), int(workers), int(depth),
+                            1 if pinned else 0, C.byref(self._h)))
+
+    def submit(self, n_full, src, dst, vertices=None):
+        src = np.ascontiguousarray(src, dtype=np.int64)
+        dst = np.ascontiguousarray(dst, dtype=np.int64)
+        v = None if vertices is None else np.ascontiguousarray(vertices, dtype=np.int64)
+        jid = _i64()
+        _check(_pipe_submit(self._h, int(n_full), _np_ptr(src), _np_ptr(dst), src.size,
+                            _np_ptr(v) if v is not None else None, 0 if v is None else v.size,
+                            C.byref(jid)))
+        return jid.value
+
+    def next(self):
+        """(job_id, host_ptr, nbytes, info) of the oldest job not yet taken."""
+        jid, ptr, nb, info = _i64(), _vp(), _sz(), PipelineInfo()
+        rc = _pipe_next(self._h, C.byref(jid), C.byref(ptr), C.byref(nb), C.byref(info))
+        if rc != OK:
+            raise GcnError(rc, last_error())
+        return jid.value, ptr.value, nb.value, info
+
+    def release(self, job_id):
+        _check(_pipe_release(self._h, int(job_id)))
+
+    def close(self):
+        if getattr(self, "_h", None) and self._h.value:
+            _pipe_destroy(self._h)
+            self._h = _vp()
+
+    def __del__(self):
+        self.close()
+
+
+def upload_image(host_ptr, nbytes, dev_view, stream=None) -> DGraph:
+    """Copy a packed image into a 256-byte-aligned device uint8 view."""
+    d = DGraph()
+    _check(_upload(_vp(host_ptr), nbytes, _vp(dev_view.data_ptr()), C.byref(d), _stream(stream)))
+    return d

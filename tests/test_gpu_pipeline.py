@@ -1,0 +1,95 @@
+"""GPU: the overlapped schedule (host workers preparing, copy-stream uploads
+into two device slots, compute stream waiting on copy events) trains to the
+same weights, bit for bit, as preparing and uploading each subgraph first."""
+import collections
+
+import numpy as np
+import pytest
+
+from paper_2001_02498_amd import synth
+from tests.gpu_helpers import dev, need_gpu, say, torch
+
+pytestmark = pytest.mark.gpu
+
+
+class _D:
+    def __init__(self, d):
+        self.desc = d
+
+
+def _model(gcn, wl, inp):
+    Ws = [dev(w, wl.h) for w in inp.W_self]
+    Wn = [dev(w, wl.h) for w in inp.W_neigh]
+    Wc = torch.from_numpy(inp.W_cls.copy()).cuda()
+    return Ws, Wn, Wc
+
+
+def test_pipelined_stream_matches_sequential():
+    need_gpu()
+    from paper_2001_02498_amd import gcn
+    import dataclasses
+    K = 6
+    wls = [dataclasses.replace(synth.stream_workload(i), n=1500, f_in=40, h=32, C=10)
+           for i in range(K)]
+    wl = wls[0]
+    inps = [synth.make_inputs(w) for w in wls]
+    Xs = [dev(inp.X) for inp in inps]
+    Ys = [torch.from_numpy(inp.labels).cuda() for inp in inps]
+    desc = gcn.model_desc(wl.L, wl.f_in, wl.h, wl.C, wl.loss, Xs[0].stride(0))
+    loss = torch.zeros(1, device="cuda")
+
+    # sequential reference
+    Ws, Wn, Wc = _model(gcn, wl, inps[0])
+    P = gcn.make_params(Ws, Wn, Wc)
+    dgs = []
+    for inp in inps:
+        red = gcn.redundancy_reduce(gcn.subgraph_build(wl.n, inp.src, inp.dst), theta=wl.theta,
+                                    max_rounds=wl.rounds, max_aux=wl.max_aux)
+        dgs.append(gcn.DeviceGraph(red))
+    ws = gcn.alloc_ws(max(gcn.workspace_bytes(d, desc) for d in dgs))
+    for i in range(K):
+        gcn.train_step(dgs[i], desc, P, Xs[i], Ys[i], wl.lr, loss, ws)
+    torch.cuda.synchronize()
+    ref = [w.clone() for w in Ws + Wn + [Wc]]
+    say("sequential loss", loss.item())
+
+    # overlapped schedule
+    Ws, Wn, Wc = _model(gcn, wl, inps[0])
+    P = gcn.make_params(Ws, Wn, Wc)
+    slots = [gcn.alloc_ws(max(d.nbytes for d in dgs)) for _ in range(2)]
+    copy = torch.cuda.Stream()
+    comp = torch.cuda.current_stream()
+    slot_free = [None, None]
+    held = collections.deque()
+    pipe = gcn.Pipeline(theta=wl.theta, max_rounds=wl.rounds, max_aux=wl.max_aux, workers=3,
+                        depth=4, pinned=True)
+    try:
+        for inp in inps:
+            pipe.submit(wl.n, inp.src, inp.dst)
+        for i in range(K):
+            jid, ptr, nb, info = pipe.next()
+            assert jid == i and nb == dgs[i].nbytes
+            slot = i % 2
+            with torch.cuda.stream(copy):
+                if slot_free[slot] is not None:
+                    copy.wait_event(slot_free[slot])
+                d = gcn.upload_image(ptr, nb, slots[slot], stream=copy)
+                copied = torch.cuda.Event()
+                copied.record(copy)
+            comp.wait_event(copied)
+            gcn.train_step(_D(d), desc, P, Xs[i], Ys[i], wl.lr, loss, ws)
+            done = torch.cuda.Event()
+            done.record(comp)
+            slot_free[slot] = done
+            held.append((jid, copied))
+            while len(held) > 1:
+                j, e = held.popleft()
+                e.synchronize()
+                pipe.release(j)
+        torch.cuda.synchronize()
+        for j, _ in held:
+            pipe.release(j)
+    finally:
+        pipe.close()
+    for a, b in zip(ref, Ws + Wn + [Wc]):
+        assert torch.equal(a, b)
