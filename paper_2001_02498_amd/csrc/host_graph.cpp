@@ -107,35 +107,49 @@ std::vector<Candidate> count_pairs(const Lists& L, int theta, int threads) {
         work += d * (d - 1) / 2;
     }
     int nt = pick_threads(threads, work);
-    std::vector<std::vector<Candidate>> out(nt);
-    std::atomic<int32_t> next{0};
+    // Candidates come out per chunk of 32 consecutive x, each x's pairs
+    // sorted by y, so concatenating the chunks gives (x, y) order.
     const int32_t chunk = 32;
-    parallel_run(nt, [&](int t) {
+    const int32_t nchunks = (ncols + chunk - 1) / chunk;
+    std::vector<std::vector<Candidate>> out(nchunks);
+    std::atomic<int32_t> next{0};
+    const int32_t nwords = (ncols + 63) / 64;
+    parallel_run(nt, [&](int) {
         std::vector<int32_t> cnt(ncols, 0);
-        std::vector<int32_t> touched;
-        touched.reserve(1024);
-        auto& mine = out[t];
+        std::vector<uint64_t> seen(nwords, 0);   // ids touched for the current x
+        std::vector<Candidate> mine;
         for (;;) {
-            int32_t x0 = next.fetch_add(chunk);
-            if (x0 >= ncols) break;
-            int32_t x1 = std::min(ncols, x0 + chunk);
+            const int32_t c = next.fetch_add(1);
+            if (c >= nchunks) break;
+            const int32_t x0 = c * chunk, x1 = std::min(ncols, x0 + chunk);
+            mine.clear();
             for (int32_t x = x0; x < x1; ++x) {
+                if (tptr[x + 1] - tptr[x] < 2) continue;   // in < 2 lists: no pair
                 for (int64_t k = tptr[x]; k < tptr[x + 1]; ++k) {
                     int32_t w = tlist[k];
                     const int32_t* row = L.col.data() + L.ptr[w];
                     int32_t d = (int32_t)(L.ptr[w + 1] - L.ptr[w]);
                     for (int32_t p = tpos[k] + 1; p < d; ++p) {
                         int32_t y = row[p];
-                        if (cnt[y]++ == 0) touched.push_back(y);
+                        cnt[y]++;
+                        seen[y >> 6] |= uint64_t(1) << (y & 63);
                     }
                 }
-                for (int32_t y : touched) {
-                    // weight-1 pairs are not edges of G_a (Alg. 1 drops them)
-                    if (cnt[y] > theta && cnt[y] >= 2) mine.push_back({cnt[y], x, y});
-                    cnt[y] = 0;
+                // touched ids in ascending order (all exceed x)
+                for (int32_t wd = (x + 1) >> 6; wd < nwords; ++wd) {
+                    uint64_t bits = seen[wd];
+                    if (!bits) continue;
+                    seen[wd] = 0;
+                    while (bits) {
+                        const int32_t y = (wd << 6) + __builtin_ctzll(bits);
+                        bits &= bits - 1;
+                        // weight-1 pairs are not edges of G_a (Alg. 1 drops them)
+                        if (cnt[y] > theta && cnt[y] >= 2) mine.push_back({cnt[y], x, y});
+                        cnt[y] = 0;
+                    }
                 }
-                touched.clear();
             }
+            out[c] = mine;
         }
     });
     std::vector<Candidate> all;
@@ -144,6 +158,19 @@ std::vector<Candidate> count_pairs(const Lists& L, int theta, int threads) {
     all.reserve(total);
     for (auto& v : out) all.insert(all.end(), v.begin(), v.end());
     return all;
+}
+
+// Orders candidates by decreasing weight, keeping the (x, y) order among
+// equal weights: a stable counting sort on the (small, integer) weights.
+std::vector<Candidate> order_by_weight(const std::vector<Candidate>& c) {
+    int64_t wmax = 0;
+    for (const Candidate& e : c) wmax = std::max(wmax, e.w);
+    std::vector<int64_t> start(wmax + 2, 0);
+    for (const Candidate& e : c) start[wmax - e.w + 1]++;
+    for (int64_t i = 0; i <= wmax; ++i) start[i + 1] += start[i];
+    std::vector<Candidate> out(c.size());
+    for (const Candidate& e : c) out[start[wmax - e.w]++] = e;
+    return out;
 }
 
 // Algorithm 3 for one round: rewrite every list, replacing each matched pair
@@ -345,13 +372,9 @@ int gcn_redundancy_reduce(gcn_graph_t g, const gcn_rr_params* params,
                 return GCN_E_INVALID_ARG;
             }
             // Algorithm 1 (candidates above theta only)
-            std::vector<Candidate> cand = count_pairs(L, params->theta, params->num_threads);
-            // Algorithm 2: decreasing weight, then (x, y) ascending
-            std::sort(cand.begin(), cand.end(), [](const Candidate& a, const Candidate& b) {
-                if (a.w != b.w) return a.w > b.w;
-                if (a.x != b.x) return a.x < b.x;
-                return a.y < b.y;
-            });
+            // Algorithm 2 scans by decreasing weight, then (x, y) ascending
+            const std::vector<Candidate> cand =
+                order_by_weight(count_pairs(L, params->theta, params->num_threads));
             std::vector<char> used(L.ncols, 0);
             std::vector<int32_t> partner(L.ncols, -1), newid(L.ncols, -1);
             int64_t taken = 0, wsum = 0;
