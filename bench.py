@@ -50,7 +50,212 @@ def parse():
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="also run one plain device copy of this size (HBM counter "
                          "calibration under rocprofv3 --pmc)")
+    ap.add_argument("--no-direct", action="store_true",
+                    help="skip the direct-aggregation comparison run (counter runs)")
+    ap.add_argument("--trace-summary", metavar="KERNEL_STATS_CSV",
+                    help="no GPU: turn a rocprofv3 --kernel-trace --stats kernel_stats.csv "
+                         "of this script into the per-class table under profiles/")
+    ap.add_argument("--traced-args", default="--no-cpu-baseline",
+                    help="with --trace-summary: the arguments the traced run was given")
+    ap.add_argument("--bench-line", help="with --trace-summary: the JSON line the traced run "
+                                         "printed (event timings shown beside the trace)")
+    ap.add_argument("--pmc-summary", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
+                    help="no GPU: turn two rocprofv3 --pmc counter files (FETCH_SIZE, "
+                         "WRITE_SIZE) of a --calib-copy-mib run into the per-launch "
+                         "HBM traffic table under profiles/")
     return ap.parse_args()
+
+
+# ---------------------------------------------------------------- HBM traffic
+#
+# Per-launch HBM bytes come from two rocprofv3 --pmc runs of this script
+# (FETCH_SIZE, then WRITE_SIZE, KiB per dispatch), each scaled by what the
+# same counter reads for one plain device copy of known size in the same run.
+# The table lives in profiles/<workload>_hbm_traffic.md together with a hash
+# of the sources each kernel class is built and launched from; when the
+# sources change the stored figure no longer describes the kernel and the
+# roofline reports traffic as null.
+
+CSRC = os.path.join(ROOT, "paper_2001_02498_amd", "csrc")
+_CLASS_SOURCES = {
+    "gemm": ["gemm.hip", "kernels.h", "api.hip"],
+    "agg": ["agg.hip", "kernels.h", "api.hip", "host_graph.cpp"],
+    "loss": ["loss.hip", "kernels.h", "api.hip"],
+    "sgd": ["gemm.hip", "kernels.h", "api.hip"],
+}
+_ROLE_CLASS = ["gemm_fwd", "gemm_cls", "gemm_dx", "gemm_cls_dx", "gemm_dw", "gemm_cls_dw"]
+
+
+def _family(cls):
+    if cls.startswith("gemm") or cls == "splitk_finish":
+        return "gemm"
+    if cls in ("pair_sums", "list_sums", "list_fixup"):
+        return "agg"
+    if cls.startswith("loss"):
+        return "loss"
+    return "sgd"
+
+
+def source_hash(cls):
+    import hashlib
+    h = hashlib.sha256()
+    for f in _CLASS_SOURCES[_family(cls)] + ["../synth.py"]:
+        with open(os.path.join(CSRC, f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def kernel_class(name):
+    """Timing class of a demangled kernel name (the classes gcn_profile_read
+    reports), or None for kernels that are not the library's."""
+    import re
+    if "gemm_kernel<" in name:
+        m = re.search(r"\(gcn::GemmRole\)(\d+)", name)
+        return _ROLE_CLASS[int(m.group(1))] if m else None
+    if "list_sums_kernel<" in name:
+        head = name[name.index("list_sums_kernel<"):]
+        return "pair_sums" if head.split(">")[0].rstrip().endswith("true") else "list_sums"
+    for key, cls in (("fixup_kernel<", "list_fixup"), ("sgd_reduce_kernel", "sgd_reduce"),
+                     ("splitk_finish_kernel", "splitk_finish"), ("loss_kernel<", "loss_rows"),
+                     ("mean_kernel", "loss_mean")):
+        if key in name:
+            return cls
+    return None
+
+
+def _counter_rows(path):
+    import csv
+    with open(path) as fh:
+        return [(r["Kernel_Name"], float(r["Counter_Value"])) for r in csv.DictReader(fh)]
+
+
+def pmc_summary(fetch_csv, write_csv, workload, cmd_args):
+    """Writes profiles/<workload>_hbm_traffic.md from two counter files."""
+    import collections
+    per = {}
+    scale = {}
+    for counter, path in (("FETCH_SIZE", fetch_csv), ("WRITE_SIZE", write_csv)):
+        rows = _counter_rows(path)
+        copy = [v for k, v in rows if "copyBuffer" in k]
+        if len(copy) != 1:
+            sys.exit(f"bench.py: expected one calibration copy in {path}, found {len(copy)}")
+        if cmd_args["calib_copy_mib"] <= 0:
+            sys.exit("bench.py: --pmc-summary needs the run's --calib-copy-mib")
+        scale[counter] = cmd_args["calib_copy_mib"] * 1024.0 / copy[0]   # true per counted
+        acc = collections.defaultdict(list)
+        for k, v in rows:
+            c = kernel_class(k)
+            if c:
+                acc[c].append(v)
+        per[counter] = acc
+    classes = sorted(per["FETCH_SIZE"], key=lambda c: -sum(per["FETCH_SIZE"][c]))
+    table = {}
+    for c in classes:
+        f = per["FETCH_SIZE"][c]
+        w = per["WRITE_SIZE"].get(c, [])
+        if not w or len(w) != len(f):
+            continue
+        fk, wk = sum(f) / len(f), sum(w) / len(w)
+        table[c] = dict(dispatches=len(f), fetch_kib=round(fk, 1), write_kib=round(wk, 1),
+                        bytes_per_launch=round(1024.0 * (fk * scale["FETCH_SIZE"]
+                                                         + wk * scale["WRITE_SIZE"])),
+                        source_hash=source_hash(c))
+    bargs = (f"--workload {workload} --steps {cmd_args['steps']} --warmup {cmd_args['warmup']} "
+             f"--profile-steps {cmd_args['profile_steps']} --no-cpu-baseline --no-direct "
+             f"--calib-copy-mib {cmd_args['calib_copy_mib']}")
+    lines = [
+        f"# HBM traffic per launch, {workload} training step",
+        "",
+        "Counters from two rocprofv3 passes over the same bench run (run from /tmp with",
+        "TMPDIR=/tmp; `$R` is the repository root):",
+        "",
+        "```",
+        f"rocprofv3 --pmc FETCH_SIZE --output-format csv -d OUT -o fetch -- python3 $R/bench.py {bargs}",
+        f"rocprofv3 --pmc WRITE_SIZE --output-format csv -d OUT -o write -- python3 $R/bench.py {bargs}",
+        f"python3 bench.py {bargs} --pmc-summary OUT/fetch_counter_collection.csv "
+        "OUT/write_counter_collection.csv",
+        "```",
+        "",
+        f"Calibration: one plain device copy of {cmd_args['calib_copy_mib']} MiB in the same "
+        f"run; its true bytes over the counted ones give the factors FETCH_SIZE "
+        f"x{scale['FETCH_SIZE']:.4f} and WRITE_SIZE x{scale['WRITE_SIZE']:.4f}, which multiply "
+        "every kernel's counters below.",
+        "",
+        "| kernel class | dispatches | FETCH_SIZE KiB/disp | WRITE_SIZE KiB/disp | HBM bytes/launch (scaled) |",
+        "|---|---:|---:|---:|---:|",
+    ]
+    for c, t in table.items():
+        lines.append(f"| {c} | {t['dispatches']} | {t['fetch_kib']} | {t['write_kib']} | "
+                     f"{t['bytes_per_launch']:,} |")
+    lines += ["", "```json",
+              json.dumps(dict(workload=workload, scale=scale, classes=table), indent=1),
+              "```", ""]
+    out = os.path.join(ROOT, "profiles", f"{workload}_hbm_traffic.md")
+    with open(out, "w") as fh:
+        fh.write("\n".join(lines))
+    print(out)
+
+
+def trace_summary(stats_csv, workload, cmd_args, bench_line=None):
+    """Writes profiles/<workload>_train_step_kernel_stats.md from a rocprofv3
+    kernel_stats.csv: per kernel and per timing class, calls and mean
+    duration."""
+    import collections
+    import csv
+    with open(stats_csv) as fh:
+        rows = list(csv.DictReader(fh))
+    by_cls = collections.defaultdict(lambda: [0, 0.0])
+    lines_k = []
+    for r in rows:
+        c = kernel_class(r["Name"])
+        calls, tot = int(r["Calls"]), float(r["TotalDurationNs"])
+        if c:
+            by_cls[c][0] += calls
+            by_cls[c][1] += tot
+        name = r["Name"].replace("gcn::(anonymous namespace)::", "")
+        name = name.split("(", 1)[0] if name.startswith("void ") else name[:90]
+        lines_k.append(f"| {c or '-'} | `{name[:110]}` | {calls} | "
+                       f"{float(r['AverageNs']) / 1e3:.2f} | {tot / 1e6:.3f} |")
+    bargs = f"--workload {workload} {cmd_args}"
+    out = [f"# Kernel durations, {workload} training step (rocprofv3 kernel trace)", "",
+           "```", "cd /tmp && export TMPDIR=/tmp",
+           f"rocprofv3 --kernel-trace --stats --output-format csv -d OUT -o run -- "
+           f"python3 $R/bench.py {bargs}",
+           f"python3 bench.py --workload {workload} --traced-args '{cmd_args}' "
+           "--trace-summary OUT/run_kernel_stats.csv --bench-line OUT/line.json", "```",
+           "", "The run covers the reduced-graph setup and the direct-aggregation comparison "
+           "(warm-up, timed and profiled steps of both); GEMM classes have the same shapes "
+           "in both.", "",
+           "## Per timing class (the classes bench.py times with HIP events)", "",
+           "| class | calls | mean us | total ms |", "|---|---:|---:|---:|"]
+    for c, (n, tot) in sorted(by_cls.items(), key=lambda kv: -kv[1][1]):
+        out.append(f"| {c} | {n} | {tot / n / 1e3:.2f} | {tot / 1e6:.3f} |")
+    if bench_line:
+        out += ["", "Event timing in the same process (bench.py `kernels`, mean us per launch):", "",
+                "| class | mean us (events) |", "|---|---:|"]
+        for c, k in bench_line["kernels"].items():
+            out.append(f"| {c} | {k['avg_us']} |")
+    out += ["", "## Per kernel", "", "| class | kernel | calls | mean us | total ms |",
+            "|---|---|---:|---:|---:|"] + lines_k + [""]
+    path = os.path.join(ROOT, "profiles", f"{workload}_train_step_kernel_stats.md")
+    with open(path, "w") as fh:
+        fh.write("\n".join(out))
+    print(path)
+
+
+def stored_traffic(workload, cls):
+    """Scaled HBM bytes per launch of `cls` from the committed counter table,
+    or None when there is none or the kernel's sources have changed since."""
+    path = os.path.join(ROOT, "profiles", f"{workload}_hbm_traffic.md")
+    if not os.path.exists(path):
+        return None
+    txt = open(path).read()
+    try:
+        blob = json.loads(txt.split("```json", 1)[1].split("```", 1)[0])
+        t = blob["classes"][cls]
+    except (IndexError, KeyError, ValueError):
+        return None
+    return t["bytes_per_launch"] if t["source_hash"] == source_hash(cls) else None
 
 
 class Setup:
@@ -148,16 +353,23 @@ def kernel_table(prof, steps):
     return out
 
 
-def roofline(name, k):
-    gemm = name.startswith("gemm")
-    if gemm:
+def roofline(name, k, workload):
+    """Roofline position of one kernel class: algorithmic flops (GEMM) or
+    bytes (everything else) per launch over the mean event-timed launch.
+    `traffic` is the counter-measured HBM bytes per launch (None when not
+    measured for the current sources); `algorithmic_bytes` sits beside it
+    for comparison."""
+    traffic = stored_traffic(workload, name)
+    extra = dict(traffic=traffic, traffic_unit="bytes/launch",
+                 algorithmic_bytes=round(k["bytes_per_launch"]))
+    if name.startswith("gemm"):
         achieved = k["flops_per_launch"] / (k["avg_us"] * 1e-6) / 1e12
         return dict(kernel=name, bound="mfma", achieved=round(achieved, 2),
                     peak=PEAK_FP32_MFMA_TFLOPS, unit="TFLOP/s",
-                    frac=round(achieved / PEAK_FP32_MFMA_TFLOPS, 4), traffic=None)
+                    frac=round(achieved / PEAK_FP32_MFMA_TFLOPS, 4), **extra)
     achieved = k["bytes_per_launch"] / (k["avg_us"] * 1e-6) / 1e9
     return dict(kernel=name, bound="hbm", achieved=round(achieved, 1), peak=PEAK_HBM_GBS,
-                unit="GB/s", frac=round(achieved / PEAK_HBM_GBS, 4), traffic=None)
+                unit="GB/s", frac=round(achieved / PEAK_HBM_GBS, 4), **extra)
 
 
 def cpu_baseline(wl, inp, budget_s):
@@ -305,7 +517,7 @@ def run_stream(args):
           file=sys.stderr, flush=True)
     ktab = kernel_table(prof, min(args.profile_steps, K))
     dominant = max(ktab, key=lambda k: ktab[k]["ms_per_step"])
-    roof = roofline(dominant, ktab[dominant])
+    roof = roofline(dominant, ktab[dominant], "stream8k")
     cpu = None
     if not args.no_cpu_baseline:
         cpu = cpu_baseline(wl, inps[0], args.cpu_seconds)
@@ -345,6 +557,17 @@ def run_stream(args):
 
 def main():
     args = parse()
+    if args.trace_summary:
+        line = None
+        if args.bench_line:
+            with open(args.bench_line) as fh:
+                line = json.loads(fh.read().strip().splitlines()[-1])
+        trace_summary(args.trace_summary, args.workload, args.traced_args, line)
+        return
+    if args.pmc_summary:
+        # the counted run's arguments are given again on this command line
+        pmc_summary(*args.pmc_summary, args.workload, vars(args))
+        return
     if args.gpus != 1:
         print(f"bench.py: this build runs on one GPU only (asked for --gpus {args.gpus}); "
               "the path shards by subgraph across GPUs but no multi-GPU run exists",
@@ -371,7 +594,7 @@ def main():
     ms = 1e3 * red.timed(args.steps, args.warmup, args.graph)
     print(f"[bench] timed {args.steps} steps: {ms:.3f} ms/step", file=sys.stderr, flush=True)
     direct = None
-    if wl.reduce:
+    if wl.reduce and not args.no_direct:
         d = Setup(dataclasses.replace(wl, reduce=False), False, inp, args.seg_len)
         direct = 1e3 * d.timed(args.steps, args.warmup, args.graph)
         print(f"[bench] direct aggregation: {direct:.3f} ms/step", file=sys.stderr, flush=True)
@@ -379,8 +602,8 @@ def main():
     prof = red.profile(args.profile_steps)
     ktab = kernel_table(prof, args.profile_steps)
     dominant = max(ktab, key=lambda k: ktab[k]["ms_per_step"])
-    roof = roofline(dominant, ktab[dominant])
-    agg = roofline("list_sums", ktab["list_sums"]) if "list_sums" in ktab else None
+    roof = roofline(dominant, ktab[dominant], wl.name)
+    agg = roofline("list_sums", ktab["list_sums"], wl.name) if "list_sums" in ktab else None
     print(f"[bench] profiled {args.profile_steps} steps; dominant {dominant}",
           file=sys.stderr, flush=True)
 

@@ -97,8 +97,10 @@ __device__ __forceinline__ Slice slice_of(int nsl, int slice_f4, int nf4) {
     return {b, min(nf4, b + slice_f4)};
 }
 
-// One group per segment (row, begin, end, slot) of the work list.
-template <int GL, int NCH, bool PRE, bool POST>
+// One group per segment (row, begin, end, slot) of the work list. PAIRS
+// marks the pair-sum launches (same code; a kernel name of their own so
+// per-kernel profiles and counters separate the two passes).
+template <int GL, int NCH, bool PRE, bool POST, bool PAIRS>
 __global__ __launch_bounds__(kBlock) void list_sums_kernel(
     const int4* __restrict__ seg, int nseg, const int32_t* __restrict__ col,
     RowSource src, const float* __restrict__ inv_deg, float* __restrict__ Y,
@@ -271,11 +273,11 @@ hipError_t launch_pair_sums(const gcn_dgraph* g, RowSource src, bool prescale,
 #define GCN_LAUNCH_PAIR(GL_, NCH_)                                                    \
     if (sh.gl == GL_ && sh.nch == NCH_) {                                             \
         if (prescale)                                                                 \
-            list_sums_kernel<GL_, NCH_, true, false><<<grid, block, 0, s>>>(          \
+            list_sums_kernel<GL_, NCH_, true, false, true><<<grid, block, 0, s>>>(          \
                 seg, g->naux, g->exp_col, src, g->inv_deg, aux, ldaux, nullptr, 0, F, \
                 sh.nsl, sh.slice_f4);                                                 \
         else                                                                          \
-            list_sums_kernel<GL_, NCH_, false, false><<<grid, block, 0, s>>>(         \
+            list_sums_kernel<GL_, NCH_, false, false, true><<<grid, block, 0, s>>>(         \
                 seg, g->naux, g->exp_col, src, g->inv_deg, aux, ldaux, nullptr, 0, F, \
                 sh.nsl, sh.slice_f4);                                                 \
         return hipGetLastError();                                                     \
@@ -305,11 +307,11 @@ hipError_t launch_list_sums(const gcn_dgraph* g, RowSource src, bool prescale,
 #define GCN_LAUNCH_LIST(GL_, NCH_)                                                    \
         if (sh.gl == GL_ && sh.nch == NCH_) {                                         \
             if (prescale)                                                             \
-                list_sums_kernel<GL_, NCH_, true, false><<<grid, block, 0, s>>>(      \
+                list_sums_kernel<GL_, NCH_, true, false, false><<<grid, block, 0, s>>>(      \
                     seg, g->nseg, g->col, src, g->inv_deg, Y, ldy, partial, ldp, F,   \
                     sh.nsl, sh.slice_f4);                                             \
             else                                                                      \
-                list_sums_kernel<GL_, NCH_, false, true><<<grid, block, 0, s>>>(      \
+                list_sums_kernel<GL_, NCH_, false, true, false><<<grid, block, 0, s>>>(      \
                     seg, g->nseg, g->col, src, g->inv_deg, Y, ldy, partial, ldp, F,   \
                     sh.nsl, sh.slice_f4);                                             \
         } else

@@ -168,7 +168,7 @@ int do_layer_fwd(const char* fn, const gcn_dgraph* g, int32_t F, int32_t h,
         p.bias = bias ? bias + (i == 0 ? 0 : h) : nullptr;
         b.p[i] = p;
     }
-    GCN_HIP(launch_gemm(b, A_MK, B_KN, EPI_BIAS_RELU, s), fn);
+    GCN_HIP(launch_gemm(b, A_MK, B_KN, EPI_BIAS_RELU, ROLE_FWD, s), fn);
     return GCN_OK;
 }
 
@@ -209,7 +209,7 @@ int do_classifier_fwd(const char* fn, int32_t n, int32_t K, int32_t C,
         p.ldc = r4(C);
         p.part_stride = (int64_t)n * p.ldc;
         b.p[0] = p;
-        GCN_HIP(launch_gemm(b, A_MK, B_KN, EPI_PARTIAL, s), fn);
+        GCN_HIP(launch_gemm(b, A_MK, B_KN, EPI_PARTIAL, ROLE_CLS_FWD, s), fn);
         if (out) *out = Logits{p.C, p.part_stride, p.ldc, splits};
         if (finish)
             GCN_HIP(launch_splitk_finish(p.C, p.part_stride, p.ldc, splits, n, C, bc, Z, ldz, s),
@@ -220,7 +220,7 @@ int do_classifier_fwd(const char* fn, int32_t n, int32_t K, int32_t C,
     p.ldc = ldz;
     p.bias = bc;
     b.p[0] = p;
-    GCN_HIP(launch_gemm(b, A_MK, B_KN, EPI_BIAS, s), fn);
+    GCN_HIP(launch_gemm(b, A_MK, B_KN, EPI_BIAS, ROLE_CLS_FWD, s), fn);
     if (out) *out = Logits{Z, 0, ldz, 1};
     return GCN_OK;
 }
@@ -285,13 +285,13 @@ int do_classifier_bwd(const char* fn, int32_t n, int32_t K, int32_t C,
         p.C = G_out;
         p.ldc = ldg;
         b.p[0] = p;
-        GCN_HIP(launch_gemm(b, A_MK, B_NK, EPI_MASK, s), fn);
+        GCN_HIP(launch_gemm(b, A_MK, B_NK, EPI_MASK, ROLE_CLS_DX, s), fn);
     }
     GemmBatch b;
     std::memset(&b, 0, sizeof(b));
     b.nprob = 1;
     b.p[0] = dw_problem(n, K, bc != nullptr, C, H, ldh, dZ, ldd, fptr(ws, sp.gemm_part), 1);
-    GCN_HIP(launch_gemm(b, A_KM, B_KN, EPI_PARTIAL, s), fn);
+    GCN_HIP(launch_gemm(b, A_KM, B_KN, EPI_PARTIAL, ROLE_CLS_DW, s), fn);
     SgdProblem q = sgd_problem(b.p[0], K, C, Wc, bc, dWc_out, dbc_out);
     GCN_HIP(launch_sgd_reduce(&q, 1, lr, s), fn);
     return GCN_OK;
@@ -331,7 +331,7 @@ int do_layer_bwd(const char* fn, const gcn_dgraph* g, int32_t F, int32_t h,
         p.C = G_in;
         p.ldc = ldgi;
         b.p[0] = p;
-        GCN_HIP(launch_gemm(b, A_MK, B_NK, EPI_MASK, s), fn);
+        GCN_HIP(launch_gemm(b, A_MK, B_NK, EPI_MASK, ROLE_DX, s), fn);
     }
     GemmBatch b;
     std::memset(&b, 0, sizeof(b));
@@ -341,7 +341,7 @@ int do_layer_bwd(const char* fn, const gcn_dgraph* g, int32_t F, int32_t h,
     const bool ones = bias != nullptr;
     b.p[0] = dw_problem(n, F, ones, h, H_in, ld_in, G, ldg, part0, 2);
     b.p[1] = dw_problem(n, F, ones, h, AH, ld_ah, G + h, ldg, part1, 2);
-    GCN_HIP(launch_gemm(b, A_KM, B_KN, EPI_PARTIAL, s), fn);
+    GCN_HIP(launch_gemm(b, A_KM, B_KN, EPI_PARTIAL, ROLE_DW, s), fn);
     SgdProblem q[2] = {
         sgd_problem(b.p[0], F, h, Ws, bias, dWs_out, db_out),
         sgd_problem(b.p[1], F, h, Wn, bias ? bias + h : nullptr, dWn_out,

@@ -99,7 +99,7 @@ struct ColQuad {      // K-major operand: columns c..c+3 of K row kofs + k0
 
 // A rows are always 16-byte aligned (checked on the host); BVEC selects
 // float4 or element loads for B (the classifier weight has any width C).
-template <ALayout AL, BLayout BL, Epilogue EP, bool BVEC>
+template <ALayout AL, BLayout BL, Epilogue EP, bool BVEC, GemmRole ROLE>
 __global__ __launch_bounds__(kThreads, 2) void gemm_kernel(GemmBatch batch) {
     // [buffer][A | B] operand tiles
     __shared__ __attribute__((aligned(16))) float smem[2][2][kOperandFloats];
@@ -439,7 +439,7 @@ void gemm_split_plan(int32_t M, int32_t N, int32_t K, int32_t nprob, int32_t* sp
     *splits = K > 0 ? (int32_t)((K + chunk - 1) / chunk) : 1;
 }
 
-hipError_t launch_gemm(GemmBatch& b, ALayout al, BLayout bl, Epilogue ep,
+hipError_t launch_gemm(GemmBatch& b, ALayout al, BLayout bl, Epilogue ep, GemmRole role,
                        hipStream_t s) {
     int total = 0;
     for (int i = 0; i < b.nprob; ++i) {
@@ -470,29 +470,30 @@ hipError_t launch_gemm(GemmBatch& b, ALayout al, BLayout bl, Epilogue ep,
         flops += 2.0 * M * N * K;
         bytes += 4.0 * (M * K + K * N + M * N) + (ep == EPI_MASK ? 4.0 * M * N : 0.0);
     }
-    const int kind = ep == EPI_BIAS_RELU            ? K_GEMM_FWD
-                   : ep == EPI_MASK                 ? K_GEMM_DX
-                   : ep == EPI_PARTIAL && al == A_KM ? K_GEMM_DW
-                                                    : K_GEMM_CLS;
+    static const int kKinds[] = {K_GEMM_FWD, K_GEMM_CLS, K_GEMM_DX,
+                                 K_GEMM_CLS_DX, K_GEMM_DW, K_GEMM_CLS_DW};
+    const int kind = kKinds[role];
     ProfScope prof(s, kind, flops, bytes);
     bool bvec = true;
     for (int i = 0; i < b.nprob; ++i) {
         if (!b.p[i].a_vec) return hipErrorInvalidValue;   // A rows must be aligned
         bvec = bvec && b.p[i].b_vec;
     }
-#define GCN_GEMM_CASE(AL_, BL_, EP_)                                        \
-    if (al == AL_ && bl == BL_ && ep == EP_) {                               \
-        if (bvec)                                                           \
-            gemm_kernel<AL_, BL_, EP_, true><<<grid, block, 0, s>>>(b);      \
-        else                                                                \
-            gemm_kernel<AL_, BL_, EP_, false><<<grid, block, 0, s>>>(b);     \
-        return hipGetLastError();                                           \
+#define GCN_GEMM_CASE(AL_, BL_, EP_, ROLE_)                                          \
+    if (al == AL_ && bl == BL_ && ep == EP_ && role == ROLE_) {                       \
+        if (bvec)                                                                    \
+            gemm_kernel<AL_, BL_, EP_, true, ROLE_><<<grid, block, 0, s>>>(b);        \
+        else                                                                         \
+            gemm_kernel<AL_, BL_, EP_, false, ROLE_><<<grid, block, 0, s>>>(b);       \
+        return hipGetLastError();                                                    \
     }
-    GCN_GEMM_CASE(A_MK, B_KN, EPI_BIAS_RELU)
-    GCN_GEMM_CASE(A_MK, B_KN, EPI_BIAS)
-    GCN_GEMM_CASE(A_MK, B_NK, EPI_MASK)
-    GCN_GEMM_CASE(A_KM, B_KN, EPI_PARTIAL)
-    GCN_GEMM_CASE(A_MK, B_KN, EPI_PARTIAL)
+    GCN_GEMM_CASE(A_MK, B_KN, EPI_BIAS_RELU, ROLE_FWD)
+    GCN_GEMM_CASE(A_MK, B_KN, EPI_BIAS, ROLE_CLS_FWD)
+    GCN_GEMM_CASE(A_MK, B_KN, EPI_PARTIAL, ROLE_CLS_FWD)
+    GCN_GEMM_CASE(A_MK, B_NK, EPI_MASK, ROLE_DX)
+    GCN_GEMM_CASE(A_MK, B_NK, EPI_MASK, ROLE_CLS_DX)
+    GCN_GEMM_CASE(A_KM, B_KN, EPI_PARTIAL, ROLE_DW)
+    GCN_GEMM_CASE(A_KM, B_KN, EPI_PARTIAL, ROLE_CLS_DW)
 #undef GCN_GEMM_CASE
     return hipErrorInvalidValue;
 }

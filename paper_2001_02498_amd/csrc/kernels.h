@@ -83,8 +83,19 @@ struct GemmBatch {
 void gemm_split_plan(int32_t M, int32_t N, int32_t K, int32_t nprob, int32_t* splits,
                      int32_t* kchunk);
 
+// Which product of the step a launch computes (its own kernel name and
+// timing class; the code depends only on layouts and epilogue).
+enum GemmRole : int {
+    ROLE_FWD = 0,     // layer transforms            [H W_self | AH W_neigh]
+    ROLE_CLS_FWD,     // classifier logits            H W_cls
+    ROLE_DX,          // layer input gradient         [G_s | T][W_s; W_n]^T
+    ROLE_CLS_DX,      // classifier input gradient    dZ W_cls^T
+    ROLE_DW,          // layer weight gradients       H^T G_s, AH^T G_n
+    ROLE_CLS_DW,      // classifier weight gradient   H^T dZ
+};
+
 // Launch C = A B for 1-2 problems of identical layouts / epilogue.
-hipError_t launch_gemm(GemmBatch& b, ALayout al, BLayout bl, Epilogue ep,
+hipError_t launch_gemm(GemmBatch& b, ALayout al, BLayout bl, Epilogue ep, GemmRole role,
                        hipStream_t s);
 
 // Sum of split-K slices in slice order plus an optional bias:

@@ -14,7 +14,9 @@ enum Kind : int {
     K_GEMM_FWD,
     K_GEMM_CLS,
     K_GEMM_DX,
+    K_GEMM_CLS_DX,
     K_GEMM_DW,
+    K_GEMM_CLS_DW,
     K_SGD,
     K_LOSS_ROWS,
     K_LOSS_MEAN,

@@ -35,7 +35,9 @@ const char* kind_name(int k) {
         case K_GEMM_FWD: return "gemm_fwd";
         case K_GEMM_CLS: return "gemm_cls";
         case K_GEMM_DX: return "gemm_dx";
+        case K_GEMM_CLS_DX: return "gemm_cls_dx";
         case K_GEMM_DW: return "gemm_dw";
+        case K_GEMM_CLS_DW: return "gemm_cls_dw";
         case K_SGD: return "sgd_reduce";
         case K_LOSS_ROWS: return "loss_rows";
         case K_LOSS_MEAN: return "loss_mean";
