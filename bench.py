@@ -27,6 +27,7 @@ sys.path.insert(0, ROOT)
 
 METRIC = "subgraph GCN fwd+bwd steps/s; SpMM GB/s and GEMM TFLOPS as % of MI355X peak"
 PEAK_FP32_MFMA_TFLOPS = 157.3    # MI355X dense fp32 matrix
+PEAK_BF16_MFMA_TFLOPS = 2500.0   # MI355X dense bf16 matrix
 PEAK_HBM_GBS = 8000.0            # MI355X HBM3E
 
 
@@ -39,6 +40,8 @@ def parse():
     ap.add_argument("--profile-steps", type=int, default=10)
     ap.add_argument("--seg-len", type=int, default=0,
                     help="list segment length of the device work list (0: library default)")
+    ap.add_argument("--precision", choices=("fp32", "bf16"), default="fp32",
+                    help="dense products in fp32 or with bf16 operands (fp32 accumulation)")
     ap.add_argument("--graph", action="store_true",
                     help="replay the step from a captured HIP graph")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -109,9 +112,10 @@ def kernel_class(name):
     """Timing class of a demangled kernel name (the classes gcn_profile_read
     reports), or None for kernels that are not the library's."""
     import re
-    if "gemm_kernel<" in name:
-        m = re.search(r"\(gcn::GemmRole\)(\d+)", name)
-        return _ROLE_CLASS[int(m.group(1))] if m else None
+    for key, suffix in (("gemm_kernel<", ""), ("gemm_bf16_kernel<", "_bf16")):
+        if key in name:
+            m = re.search(r"\(gcn::GemmRole\)(\d+)", name)
+            return _ROLE_CLASS[int(m.group(1))] + suffix if m else None
     if "list_sums_kernel<" in name:
         head = name[name.index("list_sums_kernel<"):]
         return "pair_sums" if head.split(">")[0].rstrip().endswith("true") else "list_sums"
@@ -261,7 +265,7 @@ def stored_traffic(workload, cls):
 class Setup:
     """Inputs of one workload on the device, ready for timed steps."""
 
-    def __init__(self, wl, reduce, inp, seg_len=0):
+    def __init__(self, wl, reduce, inp, seg_len=0, precision=0):
         import torch
         from paper_2001_02498_amd import gcn
         self.gcn, self.wl = gcn, wl
@@ -289,7 +293,8 @@ class Setup:
         self.Wc = torch.from_numpy(inp.W_cls.copy()).cuda()
         self.labels = torch.from_numpy(inp.labels).cuda()
         self.P = gcn.make_params(self.Ws, self.Wn, self.Wc)
-        self.desc = gcn.model_desc(wl.L, wl.f_in, wl.h, wl.C, wl.loss, self.X.stride(0))
+        self.desc = gcn.model_desc(wl.L, wl.f_in, wl.h, wl.C, wl.loss, self.X.stride(0),
+                                   precision=precision)
         self.ws = gcn.alloc_ws(gcn.workspace_bytes(self.dg, self.desc))
         self.loss = torch.zeros(1, device="cuda")
         torch.cuda.synchronize()
@@ -363,10 +368,10 @@ def roofline(name, k, workload):
     extra = dict(traffic=traffic, traffic_unit="bytes/launch",
                  algorithmic_bytes=round(k["bytes_per_launch"]))
     if name.startswith("gemm"):
+        peak = PEAK_BF16_MFMA_TFLOPS if name.endswith("_bf16") else PEAK_FP32_MFMA_TFLOPS
         achieved = k["flops_per_launch"] / (k["avg_us"] * 1e-6) / 1e12
-        return dict(kernel=name, bound="mfma", achieved=round(achieved, 2),
-                    peak=PEAK_FP32_MFMA_TFLOPS, unit="TFLOP/s",
-                    frac=round(achieved / PEAK_FP32_MFMA_TFLOPS, 4), **extra)
+        return dict(kernel=name, bound="mfma", achieved=round(achieved, 2), peak=peak,
+                    unit="TFLOP/s", frac=round(achieved / peak, 4), **extra)
     achieved = k["bytes_per_launch"] / (k["avg_us"] * 1e-6) / 1e9
     return dict(kernel=name, bound="hbm", achieved=round(achieved, 1), peak=PEAK_HBM_GBS,
                 unit="GB/s", frac=round(achieved / PEAK_HBM_GBS, 4), **extra)
@@ -590,12 +595,14 @@ def main():
     inp = synth.make_inputs(wl)
     print(f"[bench] workload {wl.name}: inputs ready", file=sys.stderr, flush=True)
 
-    red = Setup(wl, wl.reduce, inp, args.seg_len)
+    from paper_2001_02498_amd import gcn
+    prec = gcn.PREC_BF16 if args.precision == "bf16" else gcn.PREC_FP32
+    red = Setup(wl, wl.reduce, inp, args.seg_len, prec)
     ms = 1e3 * red.timed(args.steps, args.warmup, args.graph)
     print(f"[bench] timed {args.steps} steps: {ms:.3f} ms/step", file=sys.stderr, flush=True)
     direct = None
     if wl.reduce and not args.no_direct:
-        d = Setup(dataclasses.replace(wl, reduce=False), False, inp, args.seg_len)
+        d = Setup(dataclasses.replace(wl, reduce=False), False, inp, args.seg_len, prec)
         direct = 1e3 * d.timed(args.steps, args.warmup, args.graph)
         print(f"[bench] direct aggregation: {direct:.3f} ms/step", file=sys.stderr, flush=True)
         del d
@@ -633,7 +640,7 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "f32",
+        "dtype": "f32" if args.precision == "fp32" else "bf16 (dense products; fp32 accumulate)",
         "launch": "hip-graph replay" if args.graph else "eager stream launches",
         "data": "synthetic",
         "config": {

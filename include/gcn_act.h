@@ -255,7 +255,8 @@ int gcn_aggregate(const gcn_dgraph* g, int32_t mode, int32_t F,
  *   H_out = ReLU( H_in W_self | AH W_neigh  (+ bias) )
  *   H_in  [n x F] ld ld_in;  W_self, W_neigh [F x h];  bias [2h] or NULL
  *   AH    [n x F] ld ld_ah;  H_out [n x 2h] ld ld_out (self half first)
- *   precision GCN_PREC_FP32 (GCN_PREC_BF16: GCN_E_UNSUPPORTED until built)
+ *   precision GCN_PREC_FP32, or GCN_PREC_BF16: operands of every dense product
+ *   rounded to bfloat16 (nearest, ties to even), float32 accumulation
  */
 int gcn_layer_fwd(const gcn_dgraph* g, int32_t F, int32_t h,
                   const float* H_in, int64_t ld_in, const float* W_self,

@@ -12,6 +12,8 @@ Plain, slow, float64 NumPy/SciPy code written from the paper:
   * gcn.py        - aggregation (Eq. 1, Section 4.2), layer forward (Eq. 1),
                     classifier, loss, backward (Eq. 2a-2c) and the
                     gradient-descent update (Section 2.1)
+  * precision.py  - bfloat16 operand rounding of the bf16 variant of the
+                    dense products
 
 Pins (tests/test_oracle_*.py): the worked examples of Fig. 1 and Fig. 2,
 Theorem 1's exact accounting, brute force on tiny graphs, an independent

@@ -104,10 +104,6 @@ int check_ws(const char* fn, const void* ws, size_t ws_bytes, int64_t need) {
 int check_precision(const char* fn, int32_t precision) {
     GCN_CHECK_ARG(precision == GCN_PREC_FP32 || precision == GCN_PREC_BF16,
                   "%s: unknown precision %d", fn, precision);
-    if (precision != GCN_PREC_FP32) {
-        set_error("%s: bf16 MFMA path not built", fn);
-        return GCN_E_UNSUPPORTED;
-    }
     return GCN_OK;
 }
 
@@ -146,7 +142,7 @@ GemmProblem gp_zero() {
 int do_layer_fwd(const char* fn, const gcn_dgraph* g, int32_t F, int32_t h,
                  const float* H_in, int64_t ld_in, const float* Ws,
                  const float* Wn, const float* bias, float* AH, int64_t ld_ah,
-                 float* H_out, int64_t ld_out, const ScratchPlan& sp, void* ws,
+                 float* H_out, int64_t ld_out, bool bf16, const ScratchPlan& sp, void* ws,
                  hipStream_t s) {
     GCN_TRY(do_aggregate(fn, g, false, F, H_in, ld_in, AH, ld_ah, sp, ws, s));
     GemmBatch b;
@@ -168,7 +164,7 @@ int do_layer_fwd(const char* fn, const gcn_dgraph* g, int32_t F, int32_t h,
         p.bias = bias ? bias + (i == 0 ? 0 : h) : nullptr;
         b.p[i] = p;
     }
-    GCN_HIP(launch_gemm(b, A_MK, B_KN, EPI_BIAS_RELU, ROLE_FWD, s), fn);
+    GCN_HIP(launch_gemm(b, A_MK, B_KN, EPI_BIAS_RELU, ROLE_FWD, bf16, s), fn);
     return GCN_OK;
 }
 
@@ -182,7 +178,7 @@ struct Logits {
 
 int do_classifier_fwd(const char* fn, int32_t n, int32_t K, int32_t C,
                       const float* H, int64_t ldh, const float* Wc,
-                      const float* bc, float* Z, int64_t ldz, const ScratchPlan& sp,
+                      const float* bc, float* Z, int64_t ldz, bool bf16, const ScratchPlan& sp,
                       void* ws, hipStream_t s, bool finish, Logits* out) {
     GemmBatch b;
     std::memset(&b, 0, sizeof(b));
@@ -209,7 +205,7 @@ int do_classifier_fwd(const char* fn, int32_t n, int32_t K, int32_t C,
         p.ldc = r4(C);
         p.part_stride = (int64_t)n * p.ldc;
         b.p[0] = p;
-        GCN_HIP(launch_gemm(b, A_MK, B_KN, EPI_PARTIAL, ROLE_CLS_FWD, s), fn);
+        GCN_HIP(launch_gemm(b, A_MK, B_KN, EPI_PARTIAL, ROLE_CLS_FWD, bf16, s), fn);
         if (out) *out = Logits{p.C, p.part_stride, p.ldc, splits};
         if (finish)
             GCN_HIP(launch_splitk_finish(p.C, p.part_stride, p.ldc, splits, n, C, bc, Z, ldz, s),
@@ -220,7 +216,7 @@ int do_classifier_fwd(const char* fn, int32_t n, int32_t K, int32_t C,
     p.ldc = ldz;
     p.bias = bc;
     b.p[0] = p;
-    GCN_HIP(launch_gemm(b, A_MK, B_KN, EPI_BIAS, ROLE_CLS_FWD, s), fn);
+    GCN_HIP(launch_gemm(b, A_MK, B_KN, EPI_BIAS, ROLE_CLS_FWD, bf16, s), fn);
     if (out) *out = Logits{Z, 0, ldz, 1};
     return GCN_OK;
 }
@@ -264,7 +260,7 @@ SgdProblem sgd_problem(const GemmProblem& gpb, int32_t Mw, int32_t N, float* W,
 int do_classifier_bwd(const char* fn, int32_t n, int32_t K, int32_t C,
                       const float* dZ, int64_t ldd, const float* H, int64_t ldh,
                       float* Wc, float* bc, float lr, float* G_out, int64_t ldg,
-                      float* dWc_out, float* dbc_out, const ScratchPlan& sp,
+                      float* dWc_out, float* dbc_out, bool bf16, const ScratchPlan& sp,
                       void* ws, hipStream_t s) {
     if (G_out) {
         GemmBatch b;
@@ -285,13 +281,13 @@ int do_classifier_bwd(const char* fn, int32_t n, int32_t K, int32_t C,
         p.C = G_out;
         p.ldc = ldg;
         b.p[0] = p;
-        GCN_HIP(launch_gemm(b, A_MK, B_NK, EPI_MASK, ROLE_CLS_DX, s), fn);
+        GCN_HIP(launch_gemm(b, A_MK, B_NK, EPI_MASK, ROLE_CLS_DX, bf16, s), fn);
     }
     GemmBatch b;
     std::memset(&b, 0, sizeof(b));
     b.nprob = 1;
     b.p[0] = dw_problem(n, K, bc != nullptr, C, H, ldh, dZ, ldd, fptr(ws, sp.gemm_part), 1);
-    GCN_HIP(launch_gemm(b, A_KM, B_KN, EPI_PARTIAL, ROLE_CLS_DW, s), fn);
+    GCN_HIP(launch_gemm(b, A_KM, B_KN, EPI_PARTIAL, ROLE_CLS_DW, bf16, s), fn);
     SgdProblem q = sgd_problem(b.p[0], K, C, Wc, bc, dWc_out, dbc_out);
     GCN_HIP(launch_sgd_reduce(&q, 1, lr, s), fn);
     return GCN_OK;
@@ -301,7 +297,7 @@ int do_layer_bwd(const char* fn, const gcn_dgraph* g, int32_t F, int32_t h,
                  const float* G, int64_t ldg, const float* H_in, int64_t ld_in,
                  const float* AH, int64_t ld_ah, float* Ws, float* Wn,
                  float* bias, float lr, float* G_in, int64_t ldgi,
-                 float* dWs_out, float* dWn_out, float* db_out,
+                 float* dWs_out, float* dWn_out, float* db_out, bool bf16,
                  const ScratchPlan& sp, void* ws, hipStream_t s) {
     const int32_t n = g->n;
     if (G_in) {
@@ -331,7 +327,7 @@ int do_layer_bwd(const char* fn, const gcn_dgraph* g, int32_t F, int32_t h,
         p.C = G_in;
         p.ldc = ldgi;
         b.p[0] = p;
-        GCN_HIP(launch_gemm(b, A_MK, B_NK, EPI_MASK, ROLE_DX, s), fn);
+        GCN_HIP(launch_gemm(b, A_MK, B_NK, EPI_MASK, ROLE_DX, bf16, s), fn);
     }
     GemmBatch b;
     std::memset(&b, 0, sizeof(b));
@@ -341,7 +337,7 @@ int do_layer_bwd(const char* fn, const gcn_dgraph* g, int32_t F, int32_t h,
     const bool ones = bias != nullptr;
     b.p[0] = dw_problem(n, F, ones, h, H_in, ld_in, G, ldg, part0, 2);
     b.p[1] = dw_problem(n, F, ones, h, AH, ld_ah, G + h, ldg, part1, 2);
-    GCN_HIP(launch_gemm(b, A_KM, B_KN, EPI_PARTIAL, ROLE_DW, s), fn);
+    GCN_HIP(launch_gemm(b, A_KM, B_KN, EPI_PARTIAL, ROLE_DW, bf16, s), fn);
     SgdProblem q[2] = {
         sgd_problem(b.p[0], F, h, Ws, bias, dWs_out, db_out),
         sgd_problem(b.p[1], F, h, Wn, bias ? bias + h : nullptr, dWn_out,
@@ -471,7 +467,8 @@ int gcn_layer_fwd(const gcn_dgraph* g, int32_t F, int32_t h, const float* H_in,
     const ScratchPlan sp = plan_scratch(n, g->naux, g->nslots, std::max(F, 2 * h));
     GCN_TRY(check_ws(fn, ws, ws_bytes, sp.total));
     return do_layer_fwd(fn, g, F, h, H_in, ld_in, W_self, W_neigh, bias, AH, ld_ah,
-                        H_out, ld_out, sp, ws, (hipStream_t)stream);
+                        H_out, ld_out, precision == GCN_PREC_BF16, sp, ws,
+                        (hipStream_t)stream);
 }
 
 int gcn_classifier_fwd(int32_t n, int32_t K, int32_t C, const float* H, int64_t ldh,
@@ -487,8 +484,9 @@ int gcn_classifier_fwd(int32_t n, int32_t K, int32_t C, const float* H, int64_t 
     GCN_TRY(check_mat(fn, "logits", logits, n, C, ldz));
     const ScratchPlan sp = plan_scratch(n, 0, 0, std::max(K, C));
     GCN_TRY(check_ws(fn, ws, ws_bytes, sp.total));
-    return do_classifier_fwd(fn, n, K, C, H, ldh, W_cls, b_cls, logits, ldz, sp, ws,
-                             (hipStream_t)stream, true, nullptr);
+    return do_classifier_fwd(fn, n, K, C, H, ldh, W_cls, b_cls, logits, ldz,
+                             precision == GCN_PREC_BF16, sp, ws, (hipStream_t)stream, true,
+                             nullptr);
 }
 
 int gcn_loss(int32_t n, int32_t C, int32_t kind, const float* logits, int64_t ldz,
@@ -534,7 +532,8 @@ int gcn_classifier_bwd(int32_t n, int32_t K, int32_t C, const float* dZ, int64_t
     const ScratchPlan sp = plan_scratch(n, 0, 0, std::max(K, C));
     GCN_TRY(check_ws(fn, ws, ws_bytes, sp.total));
     return do_classifier_bwd(fn, n, K, C, dZ, ldd, H, ldh, W_cls, b_cls, lr, G_out, ldg,
-                             dW_cls_out, db_cls_out, sp, ws, (hipStream_t)stream);
+                             dW_cls_out, db_cls_out, precision == GCN_PREC_BF16, sp, ws,
+                             (hipStream_t)stream);
 }
 
 int gcn_layer_bwd(const gcn_dgraph* g, int32_t F, int32_t h, const float* G, int64_t ldg,
@@ -562,8 +561,8 @@ int gcn_layer_bwd(const gcn_dgraph* g, int32_t F, int32_t h, const float* G, int
     const ScratchPlan sp = plan_scratch(n, g->naux, g->nslots, std::max(F, 2 * h));
     GCN_TRY(check_ws(fn, ws, ws_bytes, sp.total));
     return do_layer_bwd(fn, g, F, h, G, ldg, H_in, ld_in, AH, ld_ah, W_self, W_neigh, bias,
-                        lr, G_in, ldgi, dW_self_out, dW_neigh_out, db_out, sp, ws,
-                        (hipStream_t)stream);
+                        lr, G_in, ldgi, dW_self_out, dW_neigh_out, db_out,
+                        precision == GCN_PREC_BF16, sp, ws, (hipStream_t)stream);
 }
 
 int gcn_workspace_layout(const gcn_dgraph* g, const gcn_model_desc* desc,
@@ -627,6 +626,7 @@ int gcn_train_step(const gcn_dgraph* g, const gcn_model_desc* d, const gcn_param
     GCN_TRY(check_ws(fn, ws, ws_bytes, sl.pub.total_bytes));
 
     hipStream_t s = (hipStream_t)stream;
+    const bool bf16 = d->precision == GCN_PREC_BF16;
     void* scratch = static_cast<char*>(ws) + sl.pub.scratch;
     const ScratchPlan& sp = sl.sp;
     const int64_t ldH = sl.pub.ld_H, ldC = sl.pub.ld_C;
@@ -639,7 +639,7 @@ int gcn_train_step(const gcn_dgraph* g, const gcn_model_desc* d, const gcn_param
         const int32_t F = l == 0 ? d->f_in : 2 * h;
         GCN_TRY(do_layer_fwd(fn, g, F, h, Hprev, ldprev, P->W_self[l], P->W_neigh[l],
                              d->has_bias ? P->b[l] : nullptr, act(sl.pub.AH[l]),
-                             sl.pub.ld_AH[l], act(sl.pub.H[l]), ldH, sp, scratch, s));
+                             sl.pub.ld_AH[l], act(sl.pub.H[l]), ldH, bf16, sp, scratch, s));
         Hprev = act(sl.pub.H[l]);
         ldprev = ldH;
     }
@@ -649,7 +649,7 @@ int gcn_train_step(const gcn_dgraph* g, const gcn_model_desc* d, const gcn_param
     Logits lg;
     const float* bcls = d->has_bias ? P->b_cls : nullptr;
     GCN_TRY(do_classifier_fwd(fn, (int32_t)n, 2 * h, C, Hprev, ldH, P->W_cls, bcls, Z, ldC,
-                              sp, scratch, s, false, &lg));
+                              bf16, sp, scratch, s, false, &lg));
     // split logits are summed (with the bias) inside the loss kernel
     GCN_HIP(launch_loss_parts((int32_t)n, C, d->loss, lg.part, lg.stride, lg.splits, lg.ldp,
                               lg.splits > 1 ? bcls : nullptr, Z, ldC, labels, dZ, ldC,
@@ -660,7 +660,7 @@ int gcn_train_step(const gcn_dgraph* g, const gcn_model_desc* d, const gcn_param
     GCN_TRY(do_classifier_bwd(fn, (int32_t)n, 2 * h, C, dZ, ldC, Hprev, ldH, P->W_cls,
                               d->has_bias ? P->b_cls : nullptr, lr, Gcur, ldH,
                               grads ? grads->W_cls : nullptr,
-                              grads ? grads->b_cls : nullptr, sp, scratch, s));
+                              grads ? grads->b_cls : nullptr, bf16, sp, scratch, s));
     for (int l = L - 1; l >= 0; --l) {
         const int32_t F = l == 0 ? d->f_in : 2 * h;
         const float* Hin = l == 0 ? X : act(sl.pub.H[l - 1]);
@@ -671,7 +671,7 @@ int gcn_train_step(const gcn_dgraph* g, const gcn_model_desc* d, const gcn_param
                              d->has_bias ? P->b[l] : nullptr, lr, Gnext, ldH,
                              grads ? grads->W_self[l] : nullptr,
                              grads ? grads->W_neigh[l] : nullptr,
-                             grads ? grads->b[l] : nullptr, sp, scratch, s));
+                             grads ? grads->b[l] : nullptr, bf16, sp, scratch, s));
         Gcur = Gnext;
     }
     return GCN_OK;

@@ -97,6 +97,70 @@ struct ColQuad {      // K-major operand: columns c..c+3 of K row kofs + k0
     int c;
 };
 
+// Output tile of a workgroup. XCD-aware renumbering: workgroup b runs on
+// XCD b % 8, and each XCD gets a contiguous range of logical tiles.
+struct TileInfo {
+    int pi, split, m0, n0, kbeg, kend, nk;
+};
+
+__device__ __forceinline__ TileInfo decode_tile(const GemmBatch& batch) {
+    const int T = batch.total_tiles;
+    const int bid = blockIdx.x;
+    const int xcd = bid % kXcds, slot = bid / kXcds;
+    const int per = T / kXcds, rem = T % kXcds;
+    const int tile = xcd * per + min(xcd, rem) + slot;
+    TileInfo ti;
+    ti.pi = (batch.nprob > 1 && tile >= batch.p[1].tile_begin) ? 1 : 0;
+    const GemmProblem& P = batch.p[ti.pi];
+    int local = tile - P.tile_begin;
+    const int per_split = P.tiles_m * P.tiles_n;
+    ti.split = local / per_split;
+    local -= ti.split * per_split;
+    ti.m0 = (local / P.tiles_n) * BM;
+    ti.n0 = (local % P.tiles_n) * BN;
+    ti.kbeg = ti.split * P.kchunk;
+    ti.kend = min(P.K, ti.kbeg + P.kchunk);
+    ti.nk = ti.kend > ti.kbeg ? (ti.kend - ti.kbeg + BK - 1) / BK : 0;
+    return ti;
+}
+
+// Epilogue of a wavefront's 64 x 64 block (2 x 2 accumulators of 32 x 32).
+// Accumulator element r of lane l is C[i][j] of its 32 x 32 block with
+// j = l % 32, i = (r % 4) + 8 (r / 4) + 4 (l / 32).
+template <Epilogue EP>
+__device__ __forceinline__ void store_tile(const GemmProblem& P, int split, int mw, int nw,
+                                           int half, int l32, const floatx16 (&acc)[2][2]) {
+    float* C = P.C;
+    if constexpr (EP == EPI_PARTIAL) C += (int64_t)split * P.part_stride;
+#pragma unroll
+    for (int bi = 0; bi < 2; ++bi) {
+#pragma unroll
+        for (int bj = 0; bj < 2; ++bj) {
+            const int n = nw + bj * 32 + l32;
+            if (n >= P.N) continue;
+            float bv = 0.f;
+            if constexpr (EP == EPI_BIAS_RELU || EP == EPI_BIAS) {
+                if (P.bias) bv = P.bias[n];
+            }
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+                const int m = mw + bi * 32 + (r & 3) + 8 * (r >> 2) + 4 * half;
+                if (m >= P.M) continue;
+                float v = acc[bi][bj][r];
+                if constexpr (EP == EPI_BIAS_RELU) {
+                    v += bv;
+                    v = v > 0.f ? v : 0.f;
+                } else if constexpr (EP == EPI_BIAS) {
+                    v += bv;
+                } else if constexpr (EP == EPI_MASK) {
+                    v = P.mask[(int64_t)m * P.ldmask + n] > 0.f ? v : 0.f;
+                }
+                C[(int64_t)m * P.ldc + n] = v;
+            }
+        }
+    }
+}
+
 // A rows are always 16-byte aligned (checked on the host); BVEC selects
 // float4 or element loads for B (the classifier weight has any width C).
 template <ALayout AL, BLayout BL, Epilogue EP, bool BVEC, GemmRole ROLE>
@@ -104,25 +168,10 @@ __global__ __launch_bounds__(kThreads, 2) void gemm_kernel(GemmBatch batch) {
     // [buffer][A | B] operand tiles
     __shared__ __attribute__((aligned(16))) float smem[2][2][kOperandFloats];
 
-    // XCD-aware renumbering: workgroup b runs on XCD b % 8; give each XCD a
-    // contiguous range of logical tiles.
-    const int T = batch.total_tiles;
-    const int bid = blockIdx.x;
-    const int xcd = bid % kXcds, slot = bid / kXcds;
-    const int per = T / kXcds, rem = T % kXcds;
-    const int tile = xcd * per + min(xcd, rem) + slot;
-
-    const int pi = (batch.nprob > 1 && tile >= batch.p[1].tile_begin) ? 1 : 0;
-    const GemmProblem& P = batch.p[pi];
-    int local = tile - P.tile_begin;
-    const int per_split = P.tiles_m * P.tiles_n;
-    const int split = local / per_split;
-    local -= split * per_split;
-    const int m0 = (local / P.tiles_n) * BM;
-    const int n0 = (local % P.tiles_n) * BN;
-    const int kbeg = split * P.kchunk;
-    const int kend = min(P.K, kbeg + P.kchunk);
-    const int nk = kend > kbeg ? (kend - kbeg + BK - 1) / BK : 0;
+    const TileInfo ti = decode_tile(batch);
+    const GemmProblem& P = batch.p[ti.pi];
+    const int split = ti.split, m0 = ti.m0, n0 = ti.n0;
+    const int kbeg = ti.kbeg, kend = ti.kend, nk = ti.nk;
 
     const int t = threadIdx.x;
     const int lane = t & 63, wave = t >> 6;
@@ -312,37 +361,195 @@ __global__ __launch_bounds__(kThreads, 2) void gemm_kernel(GemmBatch batch) {
         __builtin_amdgcn_sched_barrier(0);
     }
 
-    // Epilogue. Accumulator element r of lane l is C[i][j] of the 32x32
-    // block with j = l % 32, i = (r % 4) + 8 (r / 4) + 4 (l / 32).
-    float* C = P.C;
-    if constexpr (EP == EPI_PARTIAL) C += (int64_t)split * P.part_stride;
+    store_tile<EP>(P, split, m0 + wm * 64, n0 + wn * 64, half, l32, acc);
+}
+
+// ------------------------------------------------------------ bf16 variant
+// The same products with bf16 operands and fp32 accumulation
+// (v_mfma_f32_32x32x16_bf16). Operands stay fp32 in HBM; they are rounded
+// to bf16 (round to nearest even, v_cvt_pk_bf16_f32) when written to LDS,
+// which then always holds [row][k] with K contiguous, so every fragment is
+// one 128-bit LDS read of 8 consecutive K values for one row. A K-major
+// operand is transposed on the way: a thread loads four consecutive K rows
+// of the same four columns and writes four 4-element K runs. Tiling and
+// epilogues are those of the fp32 kernel; an MFMA step covers 16 K values,
+// so a K step of 32 is two MFMA steps. Global loads run two K steps ahead
+// (two register sets) to cover memory latency behind the shorter MFMA work.
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+
+constexpr int kHStride = BK + 8;   // bf16 per LDS row: 80 bytes, conflict-free 128-bit reads
+
+__device__ __forceinline__ bf16x4 to_bf16(float a, float b, float c, float d) {
+    bf16x4 r;
+    r[0] = (__bf16)a;
+    r[1] = (__bf16)b;
+    r[2] = (__bf16)c;
+    r[3] = (__bf16)d;
+    return r;
+}
+
+template <ALayout AL, BLayout BL, Epilogue EP, bool BVEC, GemmRole ROLE>
+__global__ __launch_bounds__(kThreads, 2) void gemm_bf16_kernel(GemmBatch batch) {
+    // [buffer][A | B] operand tiles, [row][k]
+    __shared__ __attribute__((aligned(16))) __bf16 hs[2][2][BM * kHStride];
+
+    const TileInfo ti = decode_tile(batch);
+    const GemmProblem& P = batch.p[ti.pi];
+    const int split = ti.split, m0 = ti.m0, n0 = ti.n0;
+    const int kbeg = ti.kbeg, kend = ti.kend, nk = ti.nk;
+
+    const int t = threadIdx.x;
+    const int lane = t & 63, wave = t >> 6;
+    const int wm = wave >> 1, wn = wave & 1;
+    const int half = lane >> 5, l32 = lane & 31;
+
+    const float* const A0 = P.A0;
+    const float* const B0 = P.B0;
+    const int M = P.M, N = P.N;
+    const int Areal = M - P.ones_row;
+    const bool ones = P.ones_row != 0;
+    const int ksplitA = P.ksplitA, ksplitB = P.ksplitB;
+    const int64_t lda0 = P.lda0, ldb0 = P.ldb0;
+
+    // Thread t moves kQuads float4 per operand and K step:
+    //   row-contiguous: row t / 8 + 32 q, K offset 4 (t % 8)
+    //   K-major:        K row 4 (t / 32) + q, columns 4 (t % 32) .. + 3
+    constexpr int kPerRow = BK / 4, kRowStep = kThreads / kPerRow;
+    static_assert(kQuads == 4 && kThreads / 32 * 4 == BK, "K-major quads cover 4 K rows");
+    const int rk = 4 * (t % kPerRow);
+    const int kq = 4 * (t >> 5);
+    const int ac = m0 + 4 * (t & 31), bc = n0 + 4 * (t & 31);
+    RowQuad arow[kQuads], brow[kQuads];
 #pragma unroll
-    for (int bi = 0; bi < 2; ++bi) {
-#pragma unroll
-        for (int bj = 0; bj < 2; ++bj) {
-            const int n = n0 + wn * 64 + bj * 32 + l32;
-            if (n >= P.N) continue;
-            float bv = 0.f;
-            if constexpr (EP == EPI_BIAS_RELU || EP == EPI_BIAS) {
-                if (P.bias) bv = P.bias[n];
-            }
-#pragma unroll
-            for (int r = 0; r < 16; ++r) {
-                const int m = m0 + wm * 64 + bi * 32 + (r & 3) + 8 * (r >> 2) + 4 * half;
-                if (m >= P.M) continue;
-                float v = acc[bi][bj][r];
-                if constexpr (EP == EPI_BIAS_RELU) {
-                    v += bv;
-                    v = v > 0.f ? v : 0.f;
-                } else if constexpr (EP == EPI_BIAS) {
-                    v += bv;
-                } else if constexpr (EP == EPI_MASK) {
-                    v = P.mask[(int64_t)m * P.ldmask + n] > 0.f ? v : 0.f;
-                }
-                C[(int64_t)m * P.ldc + n] = v;
-            }
+    for (int q = 0; q < kQuads; ++q) {
+        if constexpr (AL == A_MK) {
+            const int r = m0 + t / kPerRow + kRowStep * q;
+            arow[q].live = r < M;
+            const int rr = arow[q].live ? r : 0;
+            arow[q].p0 = A0 + (int64_t)rr * lda0;
+            arow[q].p1 = P.A1 + (int64_t)rr * P.lda1;
+        }
+        if constexpr (BL == B_NK) {
+            const int r = n0 + t / kPerRow + kRowStep * q;
+            brow[q].live = r < N;
+            const int rr = brow[q].live ? r : 0;
+            brow[q].p0 = B0 + (int64_t)rr * ldb0;
+            brow[q].p1 = P.B1 + (int64_t)rr * P.ldb1;
         }
     }
+
+    Quad ra[2][kQuads], rb[2][kQuads];
+    auto gload = [&](int set, int k0) {
+#pragma unroll
+        for (int q = 0; q < kQuads; ++q) {
+            Quad& a = ra[set][q];
+            if constexpr (AL == A_MK) {
+                const int k = k0 + rk;
+                const float* p = k < ksplitA ? arow[q].p0 + k : arow[q].p1 + (k - ksplitA);
+                a.one = -1;
+                issue<true>(a, p, A0, (arow[q].live && k < kend) ? kend - k : 0);
+            } else {
+                const int k = k0 + kq + q;
+                const bool krow = k < kend;
+                a.one = (ones && krow && Areal - ac >= 0 && Areal - ac < 4) ? Areal - ac : -1;
+                issue<true>(a, A0 + (int64_t)k * lda0 + ac, A0, (krow && ac < Areal) ? Areal - ac : 0);
+            }
+            Quad& b = rb[set][q];
+            if constexpr (BL == B_NK) {
+                const int k = k0 + rk;
+                const float* p = k < ksplitB ? brow[q].p0 + k : brow[q].p1 + (k - ksplitB);
+                b.one = -1;
+                issue<BVEC>(b, p, B0, (brow[q].live && k < kend) ? kend - k : 0);
+            } else {
+                const int k = k0 + kq + q;
+                b.one = -1;
+                issue<BVEC>(b, B0 + (int64_t)k * ldb0 + bc, B0, (k < kend && bc < N) ? N - bc : 0);
+            }
+        }
+    };
+    // one operand's quads of register set `set` into LDS tile S ([row][k])
+    auto sstore_op = [&](__bf16* S, const Quad (&r)[kQuads], bool kmajor) {
+        if (!kmajor) {
+#pragma unroll
+            for (int q = 0; q < kQuads; ++q) {
+                const float4 v = finish(r[q]);
+                *reinterpret_cast<bf16x4*>(&S[(t / kPerRow + kRowStep * q) * kHStride + rk]) =
+                    to_bf16(v.x, v.y, v.z, v.w);
+            }
+        } else {
+            const float4 v0 = finish(r[0]), v1 = finish(r[1]), v2 = finish(r[2]),
+                         v3 = finish(r[3]);
+            const int c = 4 * (t & 31);
+            *reinterpret_cast<bf16x4*>(&S[(c + 0) * kHStride + kq]) = to_bf16(v0.x, v1.x, v2.x, v3.x);
+            *reinterpret_cast<bf16x4*>(&S[(c + 1) * kHStride + kq]) = to_bf16(v0.y, v1.y, v2.y, v3.y);
+            *reinterpret_cast<bf16x4*>(&S[(c + 2) * kHStride + kq]) = to_bf16(v0.z, v1.z, v2.z, v3.z);
+            *reinterpret_cast<bf16x4*>(&S[(c + 3) * kHStride + kq]) = to_bf16(v0.w, v1.w, v2.w, v3.w);
+        }
+    };
+    auto sstore = [&](int buf, int set) {
+        sstore_op(hs[buf][0], ra[set], AL == A_KM);
+        sstore_op(hs[buf][1], rb[set], BL == B_KN);
+    };
+
+    floatx16 acc[2][2];
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+
+    // fragments of MFMA step ks (K values 16 ks .. 16 ks + 15 of the K step):
+    // lane half g holds K values 8 g .. 8 g + 7 of its row
+    bf16x8 fa[2][2], fb[2][2];
+    auto frag = [&](int buf, int ks, int fslot) {
+        const __bf16* As = hs[buf][0];
+        const __bf16* Bs = hs[buf][1];
+        const int kb = 16 * ks + 8 * half;
+#pragma unroll
+        for (int i = 0; i < 2; ++i) {
+            fa[fslot][i] = *reinterpret_cast<const bf16x8*>(&As[(wm * 64 + i * 32 + l32) * kHStride + kb]);
+            fb[fslot][i] = *reinterpret_cast<const bf16x8*>(&Bs[(wn * 64 + i * 32 + l32) * kHStride + kb]);
+        }
+    };
+    auto mfma = [&](int fslot) {
+#pragma unroll
+        for (int i = 0; i < 2; ++i)
+#pragma unroll
+            for (int j = 0; j < 2; ++j)
+                acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[fslot][i], fb[fslot][j],
+                                                                    acc[i][j], 0, 0, 0);
+    };
+
+    // LDS buffer kt % 2 holds K step kt; register set (kt + 1) % 2 holds
+    // step kt + 1, and step kt + 2 is loaded into set kt % 2 meanwhile.
+    auto kstep = [&](int kt, int set) {
+        const int buf = kt & 1;
+        gload(set, kbeg + (kt + 2) * BK);   // past kend: empty quads
+        frag(buf, 1, 1);
+        mfma(0);
+        mfma(1);
+        __builtin_amdgcn_sched_barrier(0);
+        if (kt + 1 < nk) sstore(buf ^ 1, set ^ 1);
+        __syncthreads();
+        if (kt + 1 < nk) frag(buf ^ 1, 0, 0);
+    };
+    if (nk > 0) {
+        gload(0, kbeg);
+        gload(1, kbeg + BK);
+        sstore(0, 0);
+        __syncthreads();
+        frag(0, 0, 0);
+    }
+    int kt = 0;
+    for (; kt + 1 < nk; kt += 2) {
+        kstep(kt, 0);
+        kstep(kt + 1, 1);
+    }
+    if (kt < nk) kstep(kt, 0);
+
+    store_tile<EP>(P, split, m0 + wm * 64, n0 + wn * 64, half, l32, acc);
 }
 
 // sum_j src[j * stride], j ascending; eight loads in flight at a time
@@ -440,7 +647,7 @@ void gemm_split_plan(int32_t M, int32_t N, int32_t K, int32_t nprob, int32_t* sp
 }
 
 hipError_t launch_gemm(GemmBatch& b, ALayout al, BLayout bl, Epilogue ep, GemmRole role,
-                       hipStream_t s) {
+                       bool bf16, hipStream_t s) {
     int total = 0;
     for (int i = 0; i < b.nprob; ++i) {
         GemmProblem& p = b.p[i];
@@ -472,7 +679,7 @@ hipError_t launch_gemm(GemmBatch& b, ALayout al, BLayout bl, Epilogue ep, GemmRo
     }
     static const int kKinds[] = {K_GEMM_FWD, K_GEMM_CLS, K_GEMM_DX,
                                  K_GEMM_CLS_DX, K_GEMM_DW, K_GEMM_CLS_DW};
-    const int kind = kKinds[role];
+    const int kind = kKinds[role] + (bf16 ? K_GEMM_BF16_OFFSET : 0);
     ProfScope prof(s, kind, flops, bytes);
     bool bvec = true;
     for (int i = 0; i < b.nprob; ++i) {
@@ -481,7 +688,11 @@ hipError_t launch_gemm(GemmBatch& b, ALayout al, BLayout bl, Epilogue ep, GemmRo
     }
 #define GCN_GEMM_CASE(AL_, BL_, EP_, ROLE_)                                          \
     if (al == AL_ && bl == BL_ && ep == EP_ && role == ROLE_) {                       \
-        if (bvec)                                                                    \
+        if (bf16 && bvec)                                                            \
+            gemm_bf16_kernel<AL_, BL_, EP_, true, ROLE_><<<grid, block, 0, s>>>(b);   \
+        else if (bf16)                                                               \
+            gemm_bf16_kernel<AL_, BL_, EP_, false, ROLE_><<<grid, block, 0, s>>>(b);  \
+        else if (bvec)                                                               \
             gemm_kernel<AL_, BL_, EP_, true, ROLE_><<<grid, block, 0, s>>>(b);        \
         else                                                                         \
             gemm_kernel<AL_, BL_, EP_, false, ROLE_><<<grid, block, 0, s>>>(b);       \

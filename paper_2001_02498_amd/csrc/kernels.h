@@ -94,9 +94,10 @@ enum GemmRole : int {
     ROLE_CLS_DW,      // classifier weight gradient   H^T dZ
 };
 
-// Launch C = A B for 1-2 problems of identical layouts / epilogue.
+// Launch C = A B for 1-2 problems of identical layouts / epilogue; bf16:
+// operands rounded to bf16 for the matrix cores, fp32 accumulation.
 hipError_t launch_gemm(GemmBatch& b, ALayout al, BLayout bl, Epilogue ep, GemmRole role,
-                       hipStream_t s);
+                       bool bf16, hipStream_t s);
 
 // Sum of split-K slices in slice order plus an optional bias:
 //   C[m][n] = sum_j part[j*stride + m*ldp + n] (+ bias[n]).

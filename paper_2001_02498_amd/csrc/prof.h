@@ -21,8 +21,16 @@ enum Kind : int {
     K_LOSS_ROWS,
     K_LOSS_MEAN,
     K_SPLITK_FINISH,
+    // the GEMM roles again, bf16 operands (same order as K_GEMM_FWD ..)
+    K_GEMM_FWD_BF16,
+    K_GEMM_CLS_BF16,
+    K_GEMM_DX_BF16,
+    K_GEMM_CLS_DX_BF16,
+    K_GEMM_DW_BF16,
+    K_GEMM_CLS_DW_BF16,
     K_COUNT
 };
+constexpr int K_GEMM_BF16_OFFSET = K_GEMM_FWD_BF16 - K_GEMM_FWD;
 
 const char* kind_name(int k);
 

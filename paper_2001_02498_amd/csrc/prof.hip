@@ -42,6 +42,12 @@ const char* kind_name(int k) {
         case K_LOSS_ROWS: return "loss_rows";
         case K_LOSS_MEAN: return "loss_mean";
         case K_SPLITK_FINISH: return "splitk_finish";
+        case K_GEMM_FWD_BF16: return "gemm_fwd_bf16";
+        case K_GEMM_CLS_BF16: return "gemm_cls_bf16";
+        case K_GEMM_DX_BF16: return "gemm_dx_bf16";
+        case K_GEMM_CLS_DX_BF16: return "gemm_cls_dx_bf16";
+        case K_GEMM_DW_BF16: return "gemm_dw_bf16";
+        case K_GEMM_CLS_DW_BF16: return "gemm_cls_dw_bf16";
         default: return "other";
     }
 }

@@ -8,6 +8,9 @@ fp32 GEMMs accumulate K <= ~10^4 products with a per-step rounding of
 give (~sqrt(K) * 2^-24 ~ 6e-6), so 1e-4 leaves an order of magnitude of
 margin while catching any dropped term, sign or index (errors of order 1).
 Aggregations sum at most a few thousand rows: 1e-5.
+The bf16 variant of the dense products rounds every operand to 8 significant
+bits (relative error up to 2^-9 each): 2e-2 against the float64 oracle, and
+the fp32 bound against the oracle with the same operands rounded.
 """
 import sys
 
@@ -21,6 +24,7 @@ torch = pytest.importorskip("torch")
 
 FP32_TOL = 1e-4
 AGG_TOL = 1e-5
+BF16_TOL = 2e-2
 
 
 def need_gpu():

@@ -1,0 +1,153 @@
+"""GPU parity of the bf16 variant of the dense products (operands rounded to
+bfloat16, float32 accumulation) through the C ABI.
+
+Two bars: against the float64 oracle with exact operands, 2e-2; and, where
+every operand of a product is a test input, against the oracle with those
+operands rounded to bfloat16 (oracle.precision), the float32 bound 1e-4 --
+which also shows that the rounding happens (exact operands differ from
+rounded ones by ~2^-9)."""
+import numpy as np
+import pytest
+
+from oracle import gcn as og
+from oracle.precision import round_bf16 as bf
+from paper_2001_02498_amd import synth
+from tests.gpu_helpers import (BF16_TOL, FP32_TOL, GraphCase, dev, empty, need_gpu, padding_of,
+                               rel, say, torch)
+from tests.test_gpu_step import StepRun, check_step
+
+pytestmark = pytest.mark.gpu
+
+
+def _graph(n, seed, seg_len=0):
+    wl = synth.small_workload(n, 14, 2, 4, 4, 2, synth.SOFTMAX_CE, (seed,))
+    inp = synth.make_inputs(wl)
+    return GraphCase(n, inp.src, inp.dst, rounds=5, seg_len=seg_len)
+
+
+def _ws(case, W):
+    return case.gcn.alloc_ws(case.gcn.scratch_bytes(case.dg, W))
+
+
+@pytest.mark.parametrize("n,K,C,bias", [(1000, 256, 121, True), (129, 1024, 41, False),
+                                        (8000, 1024, 100, False)])
+def test_classifier_bf16(n, K, C, bias):
+    need_gpu()
+    say("classifier bf16", n, K, C, bias)
+    from paper_2001_02498_amd import gcn
+    rng = np.random.default_rng(n + K + C + 1)
+    H = np.maximum(rng.standard_normal((n, K)), 0).astype(np.float32)
+    Wc = synth.glorot(rng, K, C)
+    bc = (rng.standard_normal(C) * 0.1).astype(np.float32) if bias else None
+    Hd, Wd = dev(H), torch.from_numpy(Wc.copy()).cuda()
+    bd = torch.from_numpy(bc.copy()).cuda() if bias else None
+    ws = gcn.alloc_ws(gcn.scratch_bytes(None, max(K, C), n=n))
+    Z = empty(n, C)
+    gcn.classifier_fwd(Hd, K, Wd, bd, Z, ws, precision=gcn.PREC_BF16)
+    torch.cuda.synchronize()
+    b0 = bc if bias else 0
+    exact = H.astype(float) @ Wc + b0
+    rounded = bf(H) @ bf(Wc) + b0
+    assert rel(Z, rounded) < FP32_TOL
+    assert 10 * FP32_TOL < rel(Z, exact) < BF16_TOL
+    assert torch.isnan(padding_of(Z)).all()
+    # backward with a given dZ
+    dZ = (rng.standard_normal((n, C)) / n).astype(np.float32)
+    W2 = Wd.clone()
+    b2 = bd.clone() if bias else None
+    G = empty(n, K)
+    dW = torch.zeros_like(Wd)
+    db = torch.zeros(C, device="cuda") if bias else None
+    lr = 0.5
+    gcn.classifier_bwd(dev(dZ), C, Hd, K, W2, b2, lr, G, dW, db, ws, precision=gcn.PREC_BF16)
+    torch.cuda.synchronize()
+    G_round = (bf(dZ) @ bf(Wc).T) * (H > 0)
+    dW_round = bf(H).T @ bf(dZ)
+    assert rel(G, G_round) < FP32_TOL
+    assert rel(dW, dW_round) < FP32_TOL
+    assert rel(G, (dZ.astype(float) @ Wc.T) * (H > 0)) < BF16_TOL
+    assert rel(dW, H.T.astype(float) @ dZ) < BF16_TOL
+    assert rel(W2.cpu().double().numpy() - Wc, -lr * dW_round) < FP32_TOL
+    if bias:   # the bias gradient is the product with a row of ones: dZ rounded too
+        assert rel(db, bf(dZ).sum(0)) < FP32_TOL
+        assert rel(db, dZ.astype(float).sum(0)) < BF16_TOL
+
+
+@pytest.mark.parametrize("n,F,h,bias", [(777, 50, 36, False), (1024, 300, 128, True),
+                                        (513, 1024, 132, False)])
+def test_layer_fwd_bf16(n, F, h, bias):
+    need_gpu()
+    say("layer_fwd bf16", n, F, h, bias)
+    case = _graph(n, F)
+    gcn = case.gcn
+    rng = np.random.default_rng(F + h + 1)
+    X = rng.standard_normal((n, F)).astype(np.float32)
+    Ws, Wn = synth.glorot(rng, F, h), synth.glorot(rng, F, h)
+    b = (rng.standard_normal(2 * h) * 0.1).astype(np.float32) if bias else np.zeros(2 * h)
+    AH = empty(n, F)
+    H = empty(n, 2 * h)
+    gcn.layer_fwd(case.dg, dev(X), dev(Ws, h), dev(Wn, h), dev(b) if bias else None, AH, H,
+                  _ws(case, max(F, 2 * h)), precision=gcn.PREC_BF16)
+    torch.cuda.synchronize()
+    AH_ref = og.aggregate(case.rp, case.cl, X)
+    assert rel(AH, AH_ref) < 1e-5          # the aggregation stays float32
+    exact = np.maximum(np.concatenate([X.astype(float) @ Ws, AH_ref @ Wn], 1) + b, 0)
+    assert rel(H, exact) < BF16_TOL
+    # the self half has only test inputs as operands
+    self_round = np.maximum(bf(X) @ bf(Ws) + b[:h], 0)
+    assert rel(H[:, :h], self_round) < FP32_TOL
+    assert torch.isnan(padding_of(H)).all()
+
+
+@pytest.mark.parametrize("n,F,h,bias,first", [(777, 50, 36, False, True),
+                                              (1500, 1024, 132, True, False),
+                                              (300, 602, 20, False, False)])
+def test_layer_bwd_bf16(n, F, h, bias, first):
+    need_gpu()
+    say("layer_bwd bf16", n, F, h, bias, first)
+    case = _graph(n, F + 1, seg_len=16)
+    gcn = case.gcn
+    rng = np.random.default_rng(F * 3 + h + 1)
+    H_in = rng.standard_normal((n, F)).astype(np.float32)
+    if not first:
+        H_in = np.maximum(H_in, 0)
+    AH = og.aggregate(case.rp, case.cl, H_in).astype(np.float32)
+    G = (rng.standard_normal((n, 2 * h)) * (rng.random((n, 2 * h)) < 0.6)).astype(np.float32)
+    Ws, Wn = synth.glorot(rng, F, h), synth.glorot(rng, F, h)
+    b = (rng.standard_normal(2 * h) * 0.1).astype(np.float32) if bias else None
+    Wsd, Wnd = dev(Ws, h), dev(Wn, h)
+    bd = dev(b) if bias else None
+    G_in = None if first else empty(n, F)
+    dWs, dWn = torch.zeros_like(Wsd), torch.zeros_like(Wnd)
+    db = torch.zeros(2 * h, device="cuda") if bias else None
+    lr = 0.25
+    gcn.layer_bwd(case.dg, dev(G), dev(H_in), dev(AH), Wsd, Wnd, bd, lr, G_in, dWs, dWn, db,
+                  _ws(case, max(F, 2 * h)), precision=gcn.PREC_BF16)
+    torch.cuda.synchronize()
+    Gs, Gn = G[:, :h], G[:, h:]
+    dWs_round = bf(H_in).T @ bf(Gs)
+    dWn_round = bf(AH).T @ bf(Gn)
+    assert rel(dWs, dWs_round) < FP32_TOL
+    assert rel(dWn, dWn_round) < FP32_TOL
+    assert rel(dWs, H_in.T.astype(float) @ Gs) < BF16_TOL
+    assert rel(dWn, AH.T.astype(float) @ Gn) < BF16_TOL
+    assert rel(Wsd.cpu().double().numpy() - Ws, -lr * dWs_round) < FP32_TOL
+    assert rel(Wnd.cpu().double().numpy() - Wn, -lr * dWn_round) < FP32_TOL
+    if bias:
+        assert rel(db, bf(G).sum(0)) < FP32_TOL
+        assert rel(db, G.astype(float).sum(0)) < BF16_TOL
+    if not first:
+        T = og.aggregate_transposed(case.rp, case.cl, Gn.astype(float))
+        exact = (Gs.astype(float) @ Ws.T + T @ Wn.T) * (H_in > 0)
+        assert rel(G_in, exact) < BF16_TOL
+        assert torch.isnan(padding_of(G_in)).all()
+
+
+@pytest.mark.parametrize("name", ["tiny", "ppi8k", "yelp10k"])
+def test_step_bf16(name):
+    need_gpu()
+    from paper_2001_02498_amd import gcn
+    run = StepRun(synth.WORKLOADS[name], precision=gcn.PREC_BF16).run()
+    errs = check_step(run, tol=BF16_TOL)
+    # rounding really happened: the dense results are not float32-exact
+    assert max(errs[k] for k in errs if k.startswith("H")) > 10 * FP32_TOL

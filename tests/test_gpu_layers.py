@@ -160,6 +160,6 @@ def test_layer_errors_before_launch():
         gcn.layer_fwd(case.dg, X, W6, W6, None, AH, empty(100, 12), _ws(case, 16))
     assert ei.value.code == gcn.E_INVALID_ARG
     with pytest.raises(gcn.GcnError) as ei:
-        gcn.layer_fwd(case.dg, X, W, W, None, AH, H, _ws(case, 16), precision=gcn.PREC_BF16)
-    assert ei.value.code == gcn.E_UNSUPPORTED
+        gcn.layer_fwd(case.dg, X, W, W, None, AH, H, _ws(case, 16), precision=7)
+    assert ei.value.code == gcn.E_INVALID_ARG
     assert torch.isnan(H).all()     # outputs untouched on error

@@ -21,9 +21,10 @@ pytestmark = pytest.mark.gpu
 class StepRun:
     """Runs one gcn_train_step on a workload and keeps every tensor."""
 
-    def __init__(self, wl, inp=None, bias=False, seg_len=0):
+    def __init__(self, wl, inp=None, bias=False, seg_len=0, precision=0):
         from paper_2001_02498_amd import gcn
         self.gcn, self.wl = gcn, wl
+        self.precision = precision
         self.inp = inp or synth.make_inputs(wl)
         rounds = wl.rounds if wl.reduce else 0
         self.case = GraphCase(wl.n, self.inp.src, self.inp.dst, theta=wl.theta,
@@ -58,14 +59,15 @@ class StepRun:
         self.grads_dev = (gWs, gWn, gWc, gb, gbc)
         Gp = gcn.make_params(gWs, gWn, gWc, gb, gbc)
         desc = gcn.model_desc(wl.L, wl.f_in, wl.h, wl.C, wl.loss, X.stride(0),
-                              has_bias=self.bias)
+                              has_bias=self.bias, precision=self.precision)
         self.layout = gcn.workspace_layout(self.case.dg, desc)
         ws = gcn.alloc_ws(gcn.workspace_bytes(self.case.dg, desc))
         self.ws = ws
         labels = torch.from_numpy(inp.labels).cuda()
         loss = torch.zeros(1, device="cuda")
         say("train_step", wl.name, "n", wl.n, "L", wl.L, "f_in", wl.f_in, "h", wl.h,
-            "C", wl.C, "naux", self.case.info["naux"], "bias", self.bias)
+            "C", wl.C, "naux", self.case.info["naux"], "bias", self.bias,
+            "precision", self.precision)
         gcn.train_step(self.case.dg, desc, P, X, labels, wl.lr, loss, ws, grads=Gp)
         torch.cuda.synchronize()
         self.loss = loss.item()
