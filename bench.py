@@ -377,6 +377,36 @@ def roofline(name, k, workload):
                 unit="GB/s", frac=round(achieved / PEAK_HBM_GBS, 4), **extra)
 
 
+def achievable_bandwidth(mib=1024, reps=10):
+    """Device-copy bandwidth (read + write bytes per second) of a buffer far
+    larger than the caches, timed with events: the HBM rate a streaming
+    kernel can reach on this GPU."""
+    import torch
+    a = torch.ones((mib << 20) // 4, dtype=torch.float32, device="cuda")
+    b = torch.empty_like(a)
+    b.copy_(a)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        b.copy_(a)
+    e1.record()
+    torch.cuda.synchronize()
+    gbs = 2.0 * a.numel() * 4 * reps / (e0.elapsed_time(e1) * 1e-3) / 1e9
+    del a, b
+    return round(gbs, 1)
+
+
+def aggregation_compulsory(wl, info):
+    """Compulsory bytes of one step's list-sum launches: every extended row
+    (n + naux of them) read once, every output row written once, the lists
+    and row pointers read once -- the floor under the algorithmic count,
+    which charges every neighbour-row gather."""
+    n, naux, nnz = wl.n, info["naux"], int(info["nnz"])
+    widths = [wl.f_in] + [2 * wl.h] * (wl.L - 1) + [wl.h] * (wl.L - 1)
+    per = [4.0 * F * (n + naux) + 4.0 * F * n + 4.0 * (n + 1 + nnz) for F in widths]
+    return sum(per) / len(per)
+
+
 def cpu_baseline(wl, inp, budget_s):
     import threadpoolctl
     from oracle import gcn as og
@@ -611,6 +641,14 @@ def main():
     dominant = max(ktab, key=lambda k: ktab[k]["ms_per_step"])
     roof = roofline(dominant, ktab[dominant], wl.name)
     agg = roofline("list_sums", ktab["list_sums"], wl.name) if "list_sums" in ktab else None
+    hbm = achievable_bandwidth()
+    if agg:
+        comp = aggregation_compulsory(wl, red.info)
+        k = ktab["list_sums"]
+        agg["achievable_GBs"] = hbm
+        agg["frac_of_achievable"] = round(agg["achieved"] / hbm, 4)
+        agg["compulsory_bytes"] = round(comp)
+        agg["compulsory_GBs"] = round(comp / (k["avg_us"] * 1e-6) / 1e9, 1)
     print(f"[bench] profiled {args.profile_steps} steps; dominant {dominant}",
           file=sys.stderr, flush=True)
 
