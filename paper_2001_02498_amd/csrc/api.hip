@@ -18,6 +18,7 @@ inline int64_t r4(int64_t x) { return round_up(x, 4); }
 struct ScratchPlan {
     int64_t aux, part_list, T, gemm_part, rowloss, total;
     int64_t gemm_part_floats;   // per problem
+    int64_t ld_max;             // widest row (floats) of the aux / T regions
 };
 
 int64_t gemm_part_bound(int64_t W) {
@@ -35,6 +36,7 @@ ScratchPlan plan_scratch(int64_t n, int64_t naux, int64_t nslots, int64_t W) {
         off = round_up(off + std::max<int64_t>(bytes, 1), kAlign);
         return o;
     };
+    p.ld_max = ldW;
     p.aux = take(4 * naux * ldW);
     p.part_list = take(4 * nslots * ldW);
     p.T = take(4 * n * ldW);
@@ -301,9 +303,12 @@ int do_layer_bwd(const char* fn, const gcn_dgraph* g, int32_t F, int32_t h,
                  const ScratchPlan& sp, void* ws, hipStream_t s) {
     const int32_t n = g->n;
     if (G_in) {
-        // T = A D^-1 G[:, h:]  (Eq. 2c), then G_in = [G_self | T] [W_self; W_neigh]^T
+        // T = A D^-1 G[:, h:]  (Eq. 2c), then G_in = [G_self | T] [W_self; W_neigh]^T;
+        // T takes G's leading dimension when the scratch rows are that wide
+        // (equal strides across the K concatenation keep the GEMM's loads
+        // on its fast path)
         float* T = fptr(ws, sp.T);
-        const int64_t ldt = r4(h);
+        const int64_t ldt = ldg <= sp.ld_max ? ldg : r4(h);
         GCN_TRY(do_aggregate(fn, g, true, h, G + h, ldg, T, ldt, sp, ws, s));
         GemmBatch b;
         std::memset(&b, 0, sizeof(b));

@@ -20,6 +20,7 @@
 // order). Tiles are renumbered so consecutive tiles (sharing A rows or a K
 // range) land on the same XCD, whose L2 then serves their common operand.
 #include <algorithm>
+#include <type_traits>
 
 #include "kernels.h"
 #include "prof.h"
@@ -439,8 +440,66 @@ __global__ __launch_bounds__(kThreads, 2) void gemm_bf16_kernel(GemmBatch batch)
         }
     }
 
+    // Fast steps. Outside the operand, a row (or a K-major column quad)
+    // only feeds outputs that the epilogue drops, so its loads are clamped
+    // to row 0 (column 0) instead of masked. In a tile with vector loads, no
+    // appended row of ones, and the K concatenation point on a K-step
+    // boundary between parts of equal leading dimension, every whole K step
+    // then needs no per-element work besides the bf16 conversion; the last
+    // (partial) steps and every other tile take the masked path.
+    const bool fast_tile = BVEC && !(ones && Areal >= m0 && Areal < m0 + BM) &&
+                           (AL == A_KM || (ksplitA % BK == 0 && P.lda1 == lda0)) &&
+                           (BL == B_KN || (ksplitB % BK == 0 && P.ldb1 == ldb0));
+    const int nfull = (kend - kbeg) / BK;   // whole K steps of this split
+    // Fast loads address element (row, k) of an operand as a base pointer
+    // that depends only on the K step (uniform: scalar registers) plus a
+    // per-thread offset fixed for the whole loop. Both parts of a
+    // K-concatenated operand then share the offsets, which needs equal
+    // leading dimensions (part of the fast-tile condition).
+    int64_t oa[kQuads], ob[kQuads];
+#pragma unroll
+    for (int q = 0; q < kQuads; ++q) {
+        if constexpr (AL == A_MK) {
+            const int r = m0 + t / kPerRow + kRowStep * q;
+            oa[q] = (int64_t)(r < M ? r : 0) * lda0 + rk;
+        } else {
+            oa[q] = (int64_t)(kq + q) * lda0 + (ac < Areal ? ac : 0);
+        }
+        if constexpr (BL == B_NK) {
+            const int r = n0 + t / kPerRow + kRowStep * q;
+            ob[q] = (int64_t)(r < N ? r : 0) * ldb0 + rk;
+        } else {
+            ob[q] = (int64_t)(kq + q) * ldb0 + (bc < N ? bc : 0);
+        }
+    }
+
     Quad ra[2][kQuads], rb[2][kQuads];
-    auto gload = [&](int set, int k0) {
+    auto gload_full = [&](int set, int k0) {
+        const float* sa;
+        const float* sb;
+        if constexpr (AL == A_MK)
+            sa = k0 >= ksplitA ? P.A1 + (k0 - ksplitA) : A0 + k0;
+        else
+            sa = A0 + (int64_t)k0 * lda0;
+        if constexpr (BL == B_NK)
+            sb = k0 >= ksplitB ? P.B1 + (k0 - ksplitB) : B0 + k0;
+        else
+            sb = B0 + (int64_t)k0 * ldb0;
+#pragma unroll
+        for (int q = 0; q < kQuads; ++q) {
+            ra[set][q].v = ld4(sa + oa[q]);
+            rb[set][q].v = ld4(sb + ob[q]);
+        }
+    };
+    // quads loaded whole, to be stored by the masked path
+    auto mark_full = [&](int set) {
+#pragma unroll
+        for (int q = 0; q < kQuads; ++q) {
+            ra[set][q].valid = rb[set][q].valid = 4;
+            ra[set][q].one = rb[set][q].one = -1;
+        }
+    };
+    auto gload_masked = [&](int set, int k0) {
 #pragma unroll
         for (int q = 0; q < kQuads; ++q) {
             Quad& a = ra[set][q];
@@ -468,28 +527,27 @@ __global__ __launch_bounds__(kThreads, 2) void gemm_bf16_kernel(GemmBatch batch)
             }
         }
     };
-    // one operand's quads of register set `set` into LDS tile S ([row][k])
-    auto sstore_op = [&](__bf16* S, const Quad (&r)[kQuads], bool kmajor) {
+    // one operand's quads into LDS tile S ([row][k]); `full`: no masking
+    auto sstore_op = [&](__bf16* S, const Quad (&r)[kQuads], bool kmajor, bool full) {
+        float4 v[kQuads];
+#pragma unroll
+        for (int q = 0; q < kQuads; ++q) v[q] = full ? r[q].v : finish(r[q]);
         if (!kmajor) {
 #pragma unroll
-            for (int q = 0; q < kQuads; ++q) {
-                const float4 v = finish(r[q]);
+            for (int q = 0; q < kQuads; ++q)
                 *reinterpret_cast<bf16x4*>(&S[(t / kPerRow + kRowStep * q) * kHStride + rk]) =
-                    to_bf16(v.x, v.y, v.z, v.w);
-            }
+                    to_bf16(v[q].x, v[q].y, v[q].z, v[q].w);
         } else {
-            const float4 v0 = finish(r[0]), v1 = finish(r[1]), v2 = finish(r[2]),
-                         v3 = finish(r[3]);
             const int c = 4 * (t & 31);
-            *reinterpret_cast<bf16x4*>(&S[(c + 0) * kHStride + kq]) = to_bf16(v0.x, v1.x, v2.x, v3.x);
-            *reinterpret_cast<bf16x4*>(&S[(c + 1) * kHStride + kq]) = to_bf16(v0.y, v1.y, v2.y, v3.y);
-            *reinterpret_cast<bf16x4*>(&S[(c + 2) * kHStride + kq]) = to_bf16(v0.z, v1.z, v2.z, v3.z);
-            *reinterpret_cast<bf16x4*>(&S[(c + 3) * kHStride + kq]) = to_bf16(v0.w, v1.w, v2.w, v3.w);
+            *reinterpret_cast<bf16x4*>(&S[(c + 0) * kHStride + kq]) = to_bf16(v[0].x, v[1].x, v[2].x, v[3].x);
+            *reinterpret_cast<bf16x4*>(&S[(c + 1) * kHStride + kq]) = to_bf16(v[0].y, v[1].y, v[2].y, v[3].y);
+            *reinterpret_cast<bf16x4*>(&S[(c + 2) * kHStride + kq]) = to_bf16(v[0].z, v[1].z, v[2].z, v[3].z);
+            *reinterpret_cast<bf16x4*>(&S[(c + 3) * kHStride + kq]) = to_bf16(v[0].w, v[1].w, v[2].w, v[3].w);
         }
     };
-    auto sstore = [&](int buf, int set) {
-        sstore_op(hs[buf][0], ra[set], AL == A_KM);
-        sstore_op(hs[buf][1], rb[set], BL == B_KN);
+    auto sstore = [&](int buf, int set, bool full) {
+        sstore_op(hs[buf][0], ra[set], AL == A_KM, full);
+        sstore_op(hs[buf][1], rb[set], BL == B_KN, full);
     };
 
     floatx16 acc[2][2];
@@ -524,30 +582,57 @@ __global__ __launch_bounds__(kThreads, 2) void gemm_bf16_kernel(GemmBatch batch)
 
     // LDS buffer kt % 2 holds K step kt; register set (kt + 1) % 2 holds
     // step kt + 1, and step kt + 2 is loaded into set kt % 2 meanwhile.
-    auto kstep = [&](int kt, int set) {
+    // FULL: steps kt + 1 and kt + 2 are whole steps of a fast tile.
+    auto kstep = [&](int kt, int set, auto FULL) {
         const int buf = kt & 1;
-        gload(set, kbeg + (kt + 2) * BK);   // past kend: empty quads
+        if constexpr (FULL)
+            gload_full(set, kbeg + (kt + 2) * BK);
+        else
+            gload_masked(set, kbeg + (kt + 2) * BK);   // past kend: empty quads
         frag(buf, 1, 1);
         mfma(0);
         mfma(1);
         __builtin_amdgcn_sched_barrier(0);
-        if (kt + 1 < nk) sstore(buf ^ 1, set ^ 1);
-        __syncthreads();
-        if (kt + 1 < nk) frag(buf ^ 1, 0, 0);
+        if constexpr (FULL) {
+            sstore(buf ^ 1, set ^ 1, true);
+            __syncthreads();
+            frag(buf ^ 1, 0, 0);
+        } else {
+            if (kt + 1 < nk) sstore(buf ^ 1, set ^ 1, false);
+            __syncthreads();
+            if (kt + 1 < nk) frag(buf ^ 1, 0, 0);
+        }
     };
+    using Full = std::true_type;
+    using Masked = std::false_type;
+    const bool fast_start = fast_tile && nfull >= 2;
+    if (fast_start) {
+        gload_full(0, kbeg);
+        gload_full(1, kbeg + BK);
+        sstore(0, 0, true);
+    } else if (nk > 0) {
+        gload_masked(0, kbeg);
+        gload_masked(1, kbeg + BK);
+        sstore(0, 0, false);
+    }
     if (nk > 0) {
-        gload(0, kbeg);
-        gload(1, kbeg + BK);
-        sstore(0, 0);
         __syncthreads();
         frag(0, 0, 0);
     }
     int kt = 0;
-    for (; kt + 1 < nk; kt += 2) {
-        kstep(kt, 0);
-        kstep(kt + 1, 1);
+    if (fast_start) {
+        for (; kt + 3 < nfull; kt += 2) {
+            kstep(kt, 0, Full{});
+            kstep(kt + 1, 1, Full{});
+        }
+        mark_full(0);
+        mark_full(1);
     }
-    if (kt < nk) kstep(kt, 0);
+    for (; kt + 1 < nk; kt += 2) {
+        kstep(kt, 0, Masked{});
+        kstep(kt + 1, 1, Masked{});
+    }
+    if (kt < nk) kstep(kt, 0, Masked{});
 
     store_tile<EP>(P, split, m0 + wm * 64, n0 + wn * 64, half, l32, acc);
 }

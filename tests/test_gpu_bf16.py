@@ -74,7 +74,7 @@ def test_classifier_bf16(n, K, C, bias):
 
 
 @pytest.mark.parametrize("n,F,h,bias", [(777, 50, 36, False), (1024, 300, 128, True),
-                                        (513, 1024, 132, False)])
+                                        (513, 1024, 132, False), (1000, 256, 128, False)])
 def test_layer_fwd_bf16(n, F, h, bias):
     need_gpu()
     say("layer_fwd bf16", n, F, h, bias)
@@ -101,7 +101,9 @@ def test_layer_fwd_bf16(n, F, h, bias):
 
 @pytest.mark.parametrize("n,F,h,bias,first", [(777, 50, 36, False, True),
                                               (1500, 1024, 132, True, False),
-                                              (300, 602, 20, False, False)])
+                                              (300, 602, 20, False, False),
+                                              (1500, 256, 128, False, False),
+                                              (1111, 512, 64, True, False)])
 def test_layer_bwd_bf16(n, F, h, bias, first):
     need_gpu()
     say("layer_bwd bf16", n, F, h, bias, first)
