@@ -306,6 +306,62 @@ __global__ __launch_bounds__(kThreads, 2) void gemm_kernel(GemmBatch batch) {
         }
     };
 
+    // Fast steps (as in the bf16 kernel below): operand rows / K-major
+    // column quads outside the operand are clamped into it, since they only
+    // feed outputs the epilogue drops; in a tile with vector loads, no
+    // appended row of ones and the K concatenation point on a K-step
+    // boundary between parts of equal leading dimension, a whole K step
+    // loads from a uniform per-step base plus fixed per-thread offsets and
+    // stores without masking.
+    const bool fast_tile = BVEC && !(ones && Areal >= m0 && Areal < m0 + BM) &&
+                           (AL == A_KM || (ksplitA % BK == 0 && P.lda1 == lda0)) &&
+                           (BL == B_KN || (ksplitB % BK == 0 && P.ldb1 == ldb0));
+    const int nfull = (kend - kbeg) / BK;
+    int64_t oa[kQuads], ob[kQuads];
+#pragma unroll
+    for (int q = 0; q < kQuads; ++q) {
+        if constexpr (AL == A_MK) {
+            const int r = m0 + t / kPerRow + kRowStep * q;
+            oa[q] = (int64_t)(r < M ? r : 0) * lda0 + rk;
+        } else {
+            oa[q] = (int64_t)(kr + 8 * q) * lda0 + (acol.c < Areal ? acol.c : 0);
+        }
+        if constexpr (BL == B_NK) {
+            const int r = n0 + t / kPerRow + kRowStep * q;
+            ob[q] = (int64_t)(r < N ? r : 0) * ldb0 + rk;
+        } else {
+            ob[q] = (int64_t)(kr + 8 * q) * ldb0 + (bcol.c < N ? bcol.c : 0);
+        }
+    }
+    auto gload_full = [&](int k0, int q) {
+        const float* sa;
+        const float* sb;
+        if constexpr (AL == A_MK)
+            sa = k0 >= ksplitA ? P.A1 + (k0 - ksplitA) : A0 + k0;
+        else
+            sa = A0 + (int64_t)k0 * lda0;
+        if constexpr (BL == B_NK)
+            sb = k0 >= ksplitB ? P.B1 + (k0 - ksplitB) : B0 + k0;
+        else
+            sb = B0 + (int64_t)k0 * ldb0;
+        ra[q].v = ld4(sa + oa[q]);
+        rb[q].v = ld4(sb + ob[q]);
+    };
+    auto sstore_full = [&](int buf, int q) {
+        float* As = smem[buf][0];
+        float* Bs = smem[buf][1];
+        if constexpr (AL == A_MK) {
+            *reinterpret_cast<float4*>(&As[(t / kPerRow + kRowStep * q) * kRowStride + rk]) = ra[q].v;
+        } else {
+            *reinterpret_cast<float4*>(&As[(kr + 8 * q) * kColStride + 4 * (t & 31)]) = ra[q].v;
+        }
+        if constexpr (BL == B_NK) {
+            *reinterpret_cast<float4*>(&Bs[(t / kPerRow + kRowStep * q) * kRowStride + rk]) = rb[q].v;
+        } else {
+            *reinterpret_cast<float4*>(&Bs[(kr + 8 * q) * kColStride + 4 * (t & 31)]) = rb[q].v;
+        }
+    };
+
     static_assert(BK / 8 == 4, "the K step is laid out as four groups of 8");
     if (nk > 0) {
 #pragma unroll
@@ -317,7 +373,9 @@ __global__ __launch_bounds__(kThreads, 2) void gemm_kernel(GemmBatch batch) {
         __syncthreads();
         frag(smem[0][0], smem[0][1], 0, 0);
     }
-    for (int kt = 0; kt < nk; ++kt) {
+    // One K step. FULL: the next step, loaded here, is a whole step of a
+    // fast tile (and a next step exists).
+    auto kstep = [&](int kt, auto FULL) {
         const int buf = kt & 1;
         const float* As = smem[buf][0];
         const float* Bs = smem[buf][1];
@@ -326,8 +384,12 @@ __global__ __launch_bounds__(kThreads, 2) void gemm_kernel(GemmBatch batch) {
         frag(As, Bs, 1, 1);
 #pragma unroll
         for (int q = 0; q < kQuads; ++q) {
-            gload_a(knext, q);
-            gload_b(knext, q);
+            if constexpr (FULL) {
+                gload_full(knext, q);
+            } else {
+                gload_a(knext, q);
+                gload_b(knext, q);
+            }
         }
         mfma_group(0);
         __builtin_amdgcn_sched_group_barrier(0x100, 8, 0);      // DS reads first
@@ -345,7 +407,12 @@ __global__ __launch_bounds__(kThreads, 2) void gemm_kernel(GemmBatch batch) {
         // reader (the previous step) finished before the previous barrier
         frag(As, Bs, 3, 1);
 #pragma unroll
-        for (int q = 0; q < kQuads; ++q) sstore(buf ^ 1, q);
+        for (int q = 0; q < kQuads; ++q) {
+            if constexpr (FULL)
+                sstore_full(buf ^ 1, q);
+            else
+                sstore(buf ^ 1, q);
+        }
         mfma_group(0);
         __builtin_amdgcn_sched_group_barrier(0x100, 8, 0);      // DS reads first
 #pragma unroll
@@ -357,10 +424,14 @@ __global__ __launch_bounds__(kThreads, 2) void gemm_kernel(GemmBatch batch) {
         __syncthreads();
         // group 3: its fragments are already in registers, so the next
         // step's first LDS reads are hidden behind these MFMAs
-        if (kt + 1 < nk) frag(smem[buf ^ 1][0], smem[buf ^ 1][1], 0, 0);
+        if (FULL || kt + 1 < nk) frag(smem[buf ^ 1][0], smem[buf ^ 1][1], 0, 0);
         mfma_group(1);
         __builtin_amdgcn_sched_barrier(0);
-    }
+    };
+    int kt = 0;
+    if (fast_tile)
+        for (; kt + 1 < nfull; ++kt) kstep(kt, std::true_type{});
+    for (; kt < nk; ++kt) kstep(kt, std::false_type{});
 
     store_tile<EP>(P, split, m0 + wm * 64, n0 + wn * 64, half, l32, acc);
 }
