@@ -225,7 +225,7 @@ def trace_summary(stats_csv, workload, cmd_args, bench_line=None):
            "```", "cd /tmp && export TMPDIR=/tmp",
            f"rocprofv3 --kernel-trace --stats --output-format csv -d OUT -o run -- "
            f"python3 $R/bench.py {bargs}",
-           f"python3 bench.py --workload {workload} --traced-args '{cmd_args}' "
+           f"python3 bench.py --workload {workload} --traced-args='{cmd_args}' "
            "--trace-summary OUT/run_kernel_stats.csv --bench-line OUT/line.json", "```",
            "", "The run covers the reduced-graph setup and the direct-aggregation comparison "
            "(warm-up, timed and profiled steps of both); GEMM classes have the same shapes "
@@ -368,10 +368,15 @@ def roofline(name, k, workload):
     extra = dict(traffic=traffic, traffic_unit="bytes/launch",
                  algorithmic_bytes=round(k["bytes_per_launch"]))
     if name.startswith("gemm"):
+        # a GEMM is bound by whichever of its flops (at the matrix peak of its
+        # operand type) and its compulsory bytes (at HBM peak) takes longer
         peak = PEAK_BF16_MFMA_TFLOPS if name.endswith("_bf16") else PEAK_FP32_MFMA_TFLOPS
-        achieved = k["flops_per_launch"] / (k["avg_us"] * 1e-6) / 1e12
-        return dict(kernel=name, bound="mfma", achieved=round(achieved, 2), peak=peak,
-                    unit="TFLOP/s", frac=round(achieved / peak, 4), **extra)
+        t_flops = k["flops_per_launch"] / (peak * 1e12)
+        t_bytes = k["bytes_per_launch"] / (PEAK_HBM_GBS * 1e9)
+        if t_flops >= t_bytes:
+            achieved = k["flops_per_launch"] / (k["avg_us"] * 1e-6) / 1e12
+            return dict(kernel=name, bound="mfma", achieved=round(achieved, 2), peak=peak,
+                        unit="TFLOP/s", frac=round(achieved / peak, 4), **extra)
     achieved = k["bytes_per_launch"] / (k["avg_us"] * 1e-6) / 1e9
     return dict(kernel=name, bound="hbm", achieved=round(achieved, 1), peak=PEAK_HBM_GBS,
                 unit="GB/s", frac=round(achieved / PEAK_HBM_GBS, 4), **extra)
@@ -641,8 +646,9 @@ def main():
     dominant = max(ktab, key=lambda k: ktab[k]["ms_per_step"])
     roof = roofline(dominant, ktab[dominant], wl.name)
     agg = roofline("list_sums", ktab["list_sums"], wl.name) if "list_sums" in ktab else None
-    hbm = achievable_bandwidth()
-    if agg:
+    # (skipped in counter runs, whose only plain copy is the calibration one)
+    hbm = None if args.calib_copy_mib else achievable_bandwidth()
+    if agg and hbm:
         comp = aggregation_compulsory(wl, red.info)
         k = ktab["list_sums"]
         agg["achievable_GBs"] = hbm
