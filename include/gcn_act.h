@@ -142,6 +142,32 @@ int gcn_reduced_info(gcn_reduced_t r, int32_t* n, int32_t* naux,
                      const gcn_rr_round** per_round, const int32_t** deg);
 void gcn_reduced_free(gcn_reduced_t r);
 
+/* ----------------------------- redundancy reduction on the device (a2)
+ * gcn_redundancy_reduce_device - the same rounds of Algorithms 1-3
+ * (Section 3.2) run on the GPU; the result object is identical, field by
+ * field, to what gcn_redundancy_reduce returns for the same graph and
+ * parameters (the same pairs, ids, lists and per-round counts). Per round:
+ * the pair counts of Algorithm 1 per vertex in LDS counters; the pairs
+ * above theta sorted by (count descending, smaller id, larger id); the
+ * greedy scan of Algorithm 2 under the max_aux cap; the list rewrite of
+ * Algorithm 3, one wavefront per list. Synchronous: uploads the lists,
+ * runs on `stream` (synchronising it twice per round to size the next
+ * launches), downloads the result, and returns.
+ *   ws, ws_bytes  device workspace, 256-byte aligned, of at least
+ *                 gcn_redundancy_reduce_device_bytes(g, params) bytes;
+ *                 caller-owned, reusable once the call returned
+ *   num_threads   ignored
+ * Limits: fewer than 65536 vertex ids (original plus pair sums) in any
+ * round (GCN_E_UNSUPPORTED beyond).
+ * Errors: GCN_E_INVALID_ARG (as gcn_redundancy_reduce, or a NULL /
+ * misaligned workspace); GCN_E_WORKSPACE; GCN_E_UNSUPPORTED; GCN_E_HIP;
+ * GCN_E_INTERNAL (a device-side capacity or range check failed); GCN_E_OOM.
+ */
+int gcn_redundancy_reduce_device_bytes(gcn_graph_t g, const gcn_rr_params* params,
+                                       size_t* bytes);
+int gcn_redundancy_reduce_device(gcn_graph_t g, const gcn_rr_params* params, void* ws,
+                                 size_t ws_bytes, gcn_stream_t stream, gcn_reduced_t* out);
+
 /* ------------------------------------------------ device graph image
  * The device form of G_s^# (what the accelerator receives in Section 4.1:
  * the lists, the pairs and D), plus a work list that splits long lists

@@ -12,6 +12,7 @@
 #include <vector>
 
 #include "common.h"
+#include "graph_types.h"
 
 namespace gcn {
 
@@ -32,17 +33,6 @@ void clear_error() { g_err.clear(); }
 
 using gcn::set_error;
 
-struct gcn_graph {
-    int32_t n = 0;
-    std::vector<int32_t> rowptr;  // n + 1
-    std::vector<int32_t> col;
-};
-
-struct gcn_reduced {
-    int32_t n = 0, naux = 0, rounds = 0;
-    std::vector<int32_t> rowptr, col, pairs, round_offsets, deg;
-    std::vector<gcn_rr_round> stats;
-};
 
 namespace {
 

@@ -1,0 +1,663 @@
+// Redundancy reduction on the GPU (Section 3.2: Algorithms 1-3 applied in
+// rounds), with results identical to the host version in host_graph.cpp.
+//
+// One round:
+//   Algorithm 1  transposed index of the lists (which lists hold each id and
+//                where), then one workgroup per id x counts, in 16-bit LDS
+//                counters, every larger id y that follows x in a list holding
+//                x; pairs above the threshold leave as 64-bit keys ordered
+//                by (weight descending, x, y).
+//   Algorithm 2  the keys are radix-sorted (rocPRIM); one workgroup scans
+//                them in blocks, drops pairs with a used endpoint in
+//                parallel and takes the rest in key order with one thread:
+//                the greedy matching under the budget, pair by pair as the
+//                host takes it.
+//   Algorithm 3  every list is rewritten by one wavefront: entries whose
+//                partner is in the same list are replaced by the pair's new
+//                id; kept entries keep their order and the new ids (all
+//                larger) follow in increasing order.
+// The host drives the rounds and reads a few counters back after the pair
+// counting and after the matching (the sort needs the candidate count).
+#include <rocprim/device/device_radix_sort.hpp>
+
+#include <algorithm>
+#include <cstring>
+#include <new>
+#include <vector>
+
+#include "common.h"
+#include "reduce_dev.h"
+
+namespace gcn {
+namespace {
+
+constexpr int kBlock = 256;
+constexpr int kScanThreads = 1024;
+constexpr int kGreedyThreads = 1024;
+constexpr int kGreedyPer = 4;                         // keys per thread per block
+constexpr int kGreedyBlock = kGreedyThreads * kGreedyPer;
+constexpr int kMaxIds = 65536;                        // 16-bit counters, 20-bit key fields
+
+// Device-side counters of one round (and the error flag).
+struct RoundCounters {
+    unsigned long long ncand;   // candidates emitted (may exceed capacity: overflow)
+    long long taken, wsum;
+    unsigned long long num_add;
+    int exhausted;
+    int error;                  // 1: candidate capacity, 2: id out of range
+};
+
+__device__ __forceinline__ uint64_t cand_key(uint32_t w, uint32_t x, uint32_t y) {
+    return ((uint64_t)(0xFFFFu - w) << 40) | ((uint64_t)x << 20) | (uint64_t)y;
+}
+
+// ------------------------------------------------------------------ scan
+// out[0] = 0, out[i + 1] = in[0] + .. + in[i]  (one workgroup)
+__global__ __launch_bounds__(kScanThreads) void scan_kernel(const int32_t* __restrict__ in,
+                                                            int32_t* __restrict__ out, int len) {
+    __shared__ int32_t part[kScanThreads];
+    const int t = threadIdx.x;
+    const int per = (len + kScanThreads - 1) / kScanThreads;
+    const int b = min(len, t * per), e = min(len, b + per);
+    int32_t s = 0;
+    for (int i = b; i < e; ++i) s += in[i];
+    part[t] = s;
+    __syncthreads();
+    for (int off = 1; off < kScanThreads; off <<= 1) {
+        const int32_t v = t >= off ? part[t - off] : 0;
+        __syncthreads();
+        part[t] += v;
+        __syncthreads();
+    }
+    int32_t run = part[t] - s;   // exclusive prefix of this chunk
+    if (t == 0) out[0] = 0;
+    for (int i = b; i < e; ++i) {
+        run += in[i];
+        out[i + 1] = run;
+    }
+}
+
+__global__ void fill_kernel(int32_t* __restrict__ p, int32_t v, int64_t len) {
+    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i < len) p[i] = v;
+}
+
+// ------------------------------------------------------------ Algorithm 1
+// one wavefront per list
+__global__ __launch_bounds__(kBlock) void tcount_kernel(int n, int ncols,
+                                                        const int32_t* __restrict__ rowptr,
+                                                        const int32_t* __restrict__ col,
+                                                        int32_t* __restrict__ tcnt,
+                                                        RoundCounters* rc) {
+    const int w = blockIdx.x * (kBlock / 64) + threadIdx.x / 64;
+    const int lane = threadIdx.x % 64;
+    if (w >= n) return;
+    for (int e = rowptr[w] + lane; e < rowptr[w + 1]; e += 64) {
+        const int c = col[e];
+        if (c < 0 || c >= ncols) {
+            rc->error = 2;
+            continue;
+        }
+        atomicAdd(&tcnt[c], 1);
+    }
+}
+
+// tlist[k] / tpos[k]: the list holding id c and c's position in it, for k in
+// [tptr[c], tptr[c + 1]) (any order inside: the counts do not depend on it)
+__global__ __launch_bounds__(kBlock) void tfill_kernel(int n, int ncols,
+                                                       const int32_t* __restrict__ rowptr,
+                                                       const int32_t* __restrict__ col,
+                                                       int32_t* __restrict__ tcur,
+                                                       int32_t* __restrict__ tlist,
+                                                       int32_t* __restrict__ tpos) {
+    const int w = blockIdx.x * (kBlock / 64) + threadIdx.x / 64;
+    const int lane = threadIdx.x % 64;
+    if (w >= n) return;
+    const int b = rowptr[w];
+    for (int e = b + lane; e < rowptr[w + 1]; e += 64) {
+        const int c = col[e];
+        if (c < 0 || c >= ncols) continue;
+        const int k = atomicAdd(&tcur[c], 1);
+        tlist[k] = w;
+        tpos[k] = e - b;
+    }
+}
+
+// One workgroup per id x (grid-stride): counts, for every y > x, the lists
+// holding both, in 16-bit counters packed two per LDS word (a count never
+// reaches 2^16: it is at most the number of lists); pairs whose count
+// exceeds theta (and 1: weight-1 pairs are no edges of G_a) are emitted.
+__global__ __launch_bounds__(kBlock) void count_pairs_kernel(
+    int ncols, int theta, const int32_t* __restrict__ rowptr, const int32_t* __restrict__ col,
+    const int32_t* __restrict__ tptr, const int32_t* __restrict__ tlist,
+    const int32_t* __restrict__ tpos, uint64_t* __restrict__ cand, int64_t cap,
+    RoundCounters* rc) {
+    extern __shared__ uint32_t cnt[];
+    const int nw = (ncols + 1) / 2;
+    const int t = threadIdx.x, lane = t % 64, wave = t / 64;
+    for (int i = t; i < nw; i += kBlock) cnt[i] = 0;
+    __syncthreads();
+    for (int x = blockIdx.x; x < ncols; x += gridDim.x) {
+        const int tb = tptr[x], te = tptr[x + 1];
+        if (te - tb < 2) continue;   // uniform: x in fewer than two lists
+        for (int k = tb + wave; k < te; k += kBlock / 64) {
+            const int w = tlist[k];
+            const int re = rowptr[w + 1];
+            for (int p = rowptr[w] + tpos[k] + 1 + lane; p < re; p += 64) {
+                const int y = col[p];
+                if (y < ncols) atomicAdd(&cnt[y >> 1], 1u << ((y & 1) * 16));
+            }
+        }
+        __syncthreads();
+        // emit and clear the counters of y > x (the word holding x + 1 on)
+        for (int wd0 = ((x + 1) >> 1); wd0 < nw; wd0 += kBlock) {
+            const int wd = wd0 + t;
+            uint32_t v = 0;
+            if (wd < nw) {
+                v = cnt[wd];
+                if (v) cnt[wd] = 0;
+            }
+            for (int h = 0; h < 2; ++h) {
+                const int y = 2 * wd + h;
+                const uint32_t c = (v >> (16 * h)) & 0xFFFFu;
+                const bool emit = wd < nw && y > x && (int)c > theta && c >= 2;
+                // wave-aggregated slot reservation
+                const uint64_t m = __ballot(emit);
+                if (m == 0) continue;
+                unsigned long long base = 0;
+                if (lane == 0) base = atomicAdd(&rc->ncand, (unsigned long long)__popcll(m));
+                base = __shfl(base, 0);
+                if (emit) {
+                    const int r = __popcll(m & ((1ull << lane) - 1));
+                    const unsigned long long slot = base + r;
+                    if ((int64_t)slot < cap)
+                        cand[slot] = cand_key(c, (uint32_t)x, (uint32_t)y);
+                    else
+                        rc->error = 1;
+                }
+            }
+        }
+        __syncthreads();
+    }
+}
+
+// ------------------------------------------------------------ Algorithm 2
+// The greedy matching over keys sorted ascending, i.e. weight descending,
+// then (x, y): a pair is taken when neither endpoint is used, while fewer
+// than `budget` pairs were taken this round. Blocks of keys are first
+// filtered in parallel against the used set; one thread then takes the
+// survivors in order. Taken pairs go to pairs[2 i], pairs[2 i + 1].
+__global__ __launch_bounds__(kGreedyThreads) void greedy_kernel(
+    const uint64_t* __restrict__ keys, int64_t nc, int ncols, int64_t budget,
+    int32_t* __restrict__ pairs, RoundCounters* rc) {
+    __shared__ uint32_t used[kMaxIds / 32];
+    __shared__ uint64_t surv[kGreedyBlock];
+    __shared__ int32_t wave_sum[kGreedyThreads / 64];
+    __shared__ int nsurv, stop;
+    __shared__ long long s_taken, s_wsum;
+    const int t = threadIdx.x, lane = t % 64, wave = t / 64;
+    for (int i = t; i < (ncols + 31) / 32; i += kGreedyThreads) used[i] = 0;
+    if (t == 0) {
+        stop = 0;
+        s_taken = 0;
+        s_wsum = 0;
+    }
+    __syncthreads();
+    auto is_used = [&](uint32_t v) { return (used[v >> 5] >> (v & 31)) & 1u; };
+    for (int64_t base = 0; base < nc; base += kGreedyBlock) {
+        uint64_t k[kGreedyPer];
+        int alive = 0;
+        bool live[kGreedyPer];
+#pragma unroll
+        for (int j = 0; j < kGreedyPer; ++j) {
+            const int64_t i = base + (int64_t)t * kGreedyPer + j;
+            k[j] = i < nc ? keys[i] : ~0ull;
+            const uint32_t x = (uint32_t)(k[j] >> 20) & 0xFFFFFu, y = (uint32_t)k[j] & 0xFFFFFu;
+            live[j] = i < nc && x < (uint32_t)ncols && y < (uint32_t)ncols && !is_used(x) && !is_used(y);
+            alive += live[j];
+        }
+        // survivors keep their order: exclusive prefix over threads
+        int incl = alive;
+        for (int off = 1; off < 64; off <<= 1) {
+            const int v = __shfl_up(incl, off);
+            if (lane >= off) incl += v;
+        }
+        if (lane == 63) wave_sum[wave] = incl;
+        __syncthreads();
+        if (t == 0) {
+            int run = 0;
+            for (int w = 0; w < kGreedyThreads / 64; ++w) {
+                const int v = wave_sum[w];
+                wave_sum[w] = run;
+                run += v;
+            }
+            nsurv = run;
+        }
+        __syncthreads();
+        int pos = wave_sum[wave] + incl - alive;
+#pragma unroll
+        for (int j = 0; j < kGreedyPer; ++j)
+            if (live[j]) surv[pos++] = k[j];
+        __syncthreads();
+        if (t == 0) {
+            long long taken = s_taken, wsum = s_wsum;
+            for (int s = 0; s < nsurv; ++s) {
+                const uint64_t key = surv[s];
+                const uint32_t x = (uint32_t)(key >> 20) & 0xFFFFFu, y = (uint32_t)key & 0xFFFFFu;
+                if (is_used(x) || is_used(y)) continue;
+                if (taken >= budget) {
+                    stop = 1;
+                    break;
+                }
+                used[x >> 5] |= 1u << (x & 31);
+                used[y >> 5] |= 1u << (y & 31);
+                pairs[2 * taken] = (int32_t)x;
+                pairs[2 * taken + 1] = (int32_t)y;
+                wsum += 0xFFFFu - (uint32_t)(key >> 40);
+                ++taken;
+            }
+            s_taken = taken;
+            s_wsum = wsum;
+            if (taken >= budget) stop = 1;
+        }
+        __syncthreads();
+        if (stop) break;
+    }
+    if (t == 0) {
+        rc->taken = s_taken;
+        rc->wsum = s_wsum;
+        rc->exhausted = s_taken >= budget ? 1 : 0;
+    }
+}
+
+// ------------------------------------------------------------ Algorithm 3
+__global__ void set_partner_kernel(const int32_t* __restrict__ pairs, int64_t taken,
+                                   int32_t id0, int32_t* __restrict__ partner,
+                                   int32_t* __restrict__ newid, int reset) {
+    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= taken) return;
+    const int32_t x = pairs[2 * i], y = pairs[2 * i + 1];
+    partner[x] = reset ? -1 : y;
+    partner[y] = reset ? -1 : x;
+    newid[x] = newid[y] = reset ? -1 : id0 + (int32_t)i;
+}
+
+__device__ __forceinline__ bool in_row(const int32_t* __restrict__ row, int d, int32_t v) {
+    int lo = 0, hi = d;
+    while (lo < hi) {
+        const int mid = (lo + hi) >> 1;
+        if (row[mid] < v)
+            lo = mid + 1;
+        else
+            hi = mid;
+    }
+    return lo < d && row[lo] == v;
+}
+
+// new length of every list (one wavefront per list) and the sum of
+// max(length - 1, 0), numAdd of Section 3.2
+__global__ __launch_bounds__(kBlock) void rewrite_count_kernel(
+    int n, const int32_t* __restrict__ rowptr, const int32_t* __restrict__ col,
+    const int32_t* __restrict__ partner, int32_t* __restrict__ rowlen, RoundCounters* rc) {
+    const int w = blockIdx.x * (kBlock / 64) + threadIdx.x / 64;
+    const int lane = threadIdx.x % 64;
+    if (w >= n) return;
+    const int b = rowptr[w], d = rowptr[w + 1] - b;
+    const int32_t* row = col + b;
+    int pairs_here = 0;
+    for (int i = lane; i < d; i += 64) {
+        const int32_t c = row[i], p = partner[c];
+        if (p >= 0 && c < p && in_row(row, d, p)) ++pairs_here;
+    }
+    for (int off = 32; off > 0; off >>= 1) pairs_here += __shfl_xor(pairs_here, off);
+    if (lane == 0) {
+        const int len = d - pairs_here;
+        rowlen[w] = len;
+        if (len > 1) atomicAdd(&rc->num_add, (unsigned long long)(len - 1));
+    }
+}
+
+// kept entries in order, then each new id written to a scratch copy at its
+// arrival position (its final place follows in rank_ids_kernel)
+__global__ __launch_bounds__(kBlock) void rewrite_fill_kernel(
+    int n, const int32_t* __restrict__ rowptr, const int32_t* __restrict__ col,
+    const int32_t* __restrict__ partner, const int32_t* __restrict__ newid,
+    const int32_t* __restrict__ rowptr_new, int32_t* __restrict__ col_new,
+    int32_t* __restrict__ scratch) {
+    const int w = blockIdx.x * (kBlock / 64) + threadIdx.x / 64;
+    const int lane = threadIdx.x % 64;
+    if (w >= n) return;
+    const int b = rowptr[w], d = rowptr[w + 1] - b;
+    const int out = rowptr_new[w], len = rowptr_new[w + 1] - out;
+    const int nadd = d - len, kept_total = len - nadd;
+    const int32_t* row = col + b;
+    int kept = 0, added = 0;
+    for (int i0 = 0; i0 < d; i0 += 64) {
+        const int i = i0 + lane;
+        int32_t c = -1;
+        bool pair_in = false;
+        if (i < d) {
+            c = row[i];
+            const int32_t p = partner[c];
+            pair_in = p >= 0 && in_row(row, d, p);
+        }
+        const bool keep = i < d && !pair_in;
+        const bool add = pair_in && c < partner[c];
+        const uint64_t km = __ballot(keep), am = __ballot(add);
+        const uint64_t below = (1ull << lane) - 1;
+        if (keep) col_new[out + kept + __popcll(km & below)] = c;
+        if (add) scratch[out + kept_total + added + __popcll(am & below)] = newid[c];
+        kept += __popcll(km);
+        added += __popcll(am);
+    }
+}
+
+__global__ __launch_bounds__(kBlock) void rank_ids_kernel(
+    int n, const int32_t* __restrict__ rowptr, const int32_t* __restrict__ rowptr_new,
+    const int32_t* __restrict__ scratch, int32_t* __restrict__ col_new) {
+    const int w = blockIdx.x * (kBlock / 64) + threadIdx.x / 64;
+    const int lane = threadIdx.x % 64;
+    if (w >= n) return;
+    const int d = rowptr[w + 1] - rowptr[w];
+    const int out = rowptr_new[w], len = rowptr_new[w + 1] - out;
+    const int nadd = d - len, first = out + len - nadd;
+    for (int j = lane; j < nadd; j += 64) {
+        const int32_t id = scratch[first + j];
+        int rank = 0;
+        for (int i = 0; i < nadd; ++i) rank += scratch[first + i] < id;
+        col_new[first + rank] = id;
+    }
+}
+
+}  // namespace
+
+// ------------------------------------------------------------ host driver
+
+namespace {
+
+struct DevPlan {
+    int64_t n, nnz, pairs_cap, ncols_cap, cand_cap;
+    size_t sort_tmp;
+    // byte offsets in the workspace
+    size_t rowptr[2], col[2], rowlen, scratch, tptr, tcur, tlist, tpos, partner, newid,
+        keys_in, keys_out, pairs, counters, sort, total;
+};
+
+int64_t visits_of(const int32_t* rowptr, int64_t n) {
+    int64_t s = 0;
+    for (int64_t w = 0; w < n; ++w) {
+        const int64_t d = rowptr[w + 1] - rowptr[w];
+        s += d * (d - 1) / 2;
+    }
+    return s;
+}
+
+int plan(const int32_t* rowptr, int64_t n, const gcn_rr_params* p, DevPlan* dp) {
+    std::memset(dp, 0, sizeof(*dp));
+    dp->n = n;
+    dp->nnz = rowptr[n];
+    dp->pairs_cap = dp->nnz / 2;   // every pair removes >= 2 list entries
+    if (p->max_aux >= 0) dp->pairs_cap = std::min<int64_t>(dp->pairs_cap, p->max_aux);
+    dp->ncols_cap = n + dp->pairs_cap;
+    // every candidate has weight >= max(theta + 1, 2), and the pair visits
+    // (sum of C(d, 2) over the lists) never grow from round to round
+    dp->cand_cap = std::max<int64_t>(1, visits_of(rowptr, n) / std::max(p->theta + 1, 2));
+    size_t tmp = 0;
+    if (rocprim::radix_sort_keys(nullptr, tmp, (uint64_t*)nullptr, (uint64_t*)nullptr,
+                                 (unsigned)std::min<int64_t>(dp->cand_cap, UINT32_MAX), 0, 56,
+                                 (hipStream_t)0) != hipSuccess)
+        return GCN_E_HIP;
+    dp->sort_tmp = tmp;
+    size_t off = 0;
+    auto take = [&](size_t bytes) {
+        size_t o = off;
+        off = (off + std::max<size_t>(bytes, 4) + 255) / 256 * 256;
+        return o;
+    };
+    for (int i = 0; i < 2; ++i) {
+        dp->rowptr[i] = take(4 * (size_t)(n + 1));
+        dp->col[i] = take(4 * (size_t)dp->nnz);
+    }
+    dp->rowlen = take(4 * (size_t)n);
+    dp->scratch = take(4 * (size_t)dp->nnz);
+    dp->tptr = take(4 * (size_t)(dp->ncols_cap + 1));
+    dp->tcur = take(4 * (size_t)dp->ncols_cap);
+    dp->tlist = take(4 * (size_t)dp->nnz);
+    dp->tpos = take(4 * (size_t)dp->nnz);
+    dp->partner = take(4 * (size_t)dp->ncols_cap);
+    dp->newid = take(4 * (size_t)dp->ncols_cap);
+    dp->keys_in = take(8 * (size_t)dp->cand_cap);
+    dp->keys_out = take(8 * (size_t)dp->cand_cap);
+    dp->pairs = take(8 * (size_t)std::max<int64_t>(dp->pairs_cap, 1));
+    dp->counters = take(sizeof(RoundCounters));
+    dp->sort = take(dp->sort_tmp);
+    dp->total = off;
+    return GCN_OK;
+}
+
+dim3 waves_grid(int64_t rows) { return dim3((unsigned)((rows + kBlock / 64 - 1) / (kBlock / 64))); }
+dim3 items_grid(int64_t items) { return dim3((unsigned)std::max<int64_t>(1, (items + kBlock - 1) / kBlock)); }
+
+}  // namespace
+
+int redundancy_reduce_device_bytes(const int32_t* rowptr, int64_t n, const gcn_rr_params* p,
+                                   size_t* bytes) {
+    DevPlan dp;
+    int rc = plan(rowptr, n, p, &dp);
+    if (rc) return rc;
+    *bytes = dp.total;
+    return GCN_OK;
+}
+
+int redundancy_reduce_device(const int32_t* rowptr_h, const int32_t* col_h, int64_t n,
+                             const gcn_rr_params* p, void* ws, size_t ws_bytes,
+                             hipStream_t s, DeviceReduceResult* out) {
+    DevPlan dp;
+    int rc = plan(rowptr_h, n, p, &dp);
+    if (rc) {
+        set_error("gcn_redundancy_reduce_device: rocPRIM sort planning failed");
+        return rc;
+    }
+    if (ws_bytes < dp.total) {
+        set_error("gcn_redundancy_reduce_device: workspace of %zu bytes, need %zu", ws_bytes,
+                  dp.total);
+        return GCN_E_WORKSPACE;
+    }
+    if (n >= kMaxIds) {
+        set_error("gcn_redundancy_reduce_device: %lld vertices; the device reduction "
+                  "handles fewer than %d",
+                  (long long)n, kMaxIds);
+        return GCN_E_UNSUPPORTED;
+    }
+    char* base = static_cast<char*>(ws);
+    auto I = [&](size_t off) { return reinterpret_cast<int32_t*>(base + off); };
+    int32_t* rowptr[2] = {I(dp.rowptr[0]), I(dp.rowptr[1])};
+    int32_t* col[2] = {I(dp.col[0]), I(dp.col[1])};
+    uint64_t* keys_in = reinterpret_cast<uint64_t*>(base + dp.keys_in);
+    uint64_t* keys_out = reinterpret_cast<uint64_t*>(base + dp.keys_out);
+    int32_t* pairs = I(dp.pairs);
+    RoundCounters* dctr = reinterpret_cast<RoundCounters*>(base + dp.counters);
+    auto fail = [&](hipError_t e, const char* what) {
+        set_error("gcn_redundancy_reduce_device: %s: HIP error %d (%s)", what, (int)e,
+                  hipGetErrorString(e));
+        return GCN_E_HIP;
+    };
+#define GCN_DR(call, what)                         \
+    do {                                           \
+        hipError_t e_ = (call);                    \
+        if (e_ != hipSuccess) return fail(e_, what); \
+    } while (0)
+
+    const int64_t nnz = dp.nnz;
+    out->round_offsets.assign(1, 0);
+    out->stats.clear();
+    if (n == 0 || nnz == 0 || p->max_rounds == 0) {   // no pairs: the lists as given
+        out->naux = 0;
+        out->rowptr.assign(rowptr_h, rowptr_h + n + 1);
+        out->col.assign(col_h, col_h + nnz);
+        out->pairs.clear();
+        return GCN_OK;
+    }
+    GCN_DR(hipMemcpyAsync(rowptr[0], rowptr_h, 4 * (size_t)(n + 1), hipMemcpyHostToDevice, s),
+           "upload");
+    if (nnz) GCN_DR(hipMemcpyAsync(col[0], col_h, 4 * (size_t)nnz, hipMemcpyHostToDevice, s), "upload");
+    fill_kernel<<<items_grid(dp.ncols_cap), kBlock, 0, s>>>(I(dp.partner), -1, dp.ncols_cap);
+    fill_kernel<<<items_grid(dp.ncols_cap), kBlock, 0, s>>>(I(dp.newid), -1, dp.ncols_cap);
+    GCN_DR(hipGetLastError(), "init");
+
+    int64_t naux = 0;
+    int32_t ncols = (int32_t)n;
+    int cur = 0;
+    int64_t cur_nnz = nnz;
+    RoundCounters hc;
+    for (int round = 0; round < p->max_rounds; ++round) {
+        const int64_t budget_left = p->max_aux < 0 ? INT64_MAX : p->max_aux - naux;
+        if (budget_left <= 0) break;
+        if ((int64_t)ncols >= kMaxIds) {
+            set_error("gcn_redundancy_reduce_device: %d vertex ids reached; the device "
+                      "reduction counts fewer than %d",
+                      ncols, kMaxIds);
+            return GCN_E_UNSUPPORTED;
+        }
+        std::memset(&hc, 0, sizeof(hc));
+        GCN_DR(hipMemcpyAsync(dctr, &hc, sizeof(hc), hipMemcpyHostToDevice, s), "counters");
+        // Algorithm 1: transposed index, then pair counts per id
+        fill_kernel<<<items_grid(ncols), kBlock, 0, s>>>(I(dp.tcur), 0, ncols);
+        tcount_kernel<<<waves_grid(n), kBlock, 0, s>>>((int)n, ncols, rowptr[cur], col[cur],
+                                                        I(dp.tcur), dctr);
+        scan_kernel<<<1, kScanThreads, 0, s>>>(I(dp.tcur), I(dp.tptr), ncols);
+        GCN_DR(hipMemcpyAsync(I(dp.tcur), I(dp.tptr), 4 * (size_t)ncols, hipMemcpyDeviceToDevice, s),
+               "cursor");
+        tfill_kernel<<<waves_grid(n), kBlock, 0, s>>>((int)n, ncols, rowptr[cur], col[cur],
+                                                       I(dp.tcur), I(dp.tlist), I(dp.tpos));
+        const size_t lds = 4 * (size_t)((ncols + 1) / 2);
+        if (lds > 65536)
+            GCN_DR(hipFuncSetAttribute((const void*)count_pairs_kernel,
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds),
+                   "pair counting LDS");
+        const unsigned grid = (unsigned)std::min<int64_t>(ncols, 4096);
+        count_pairs_kernel<<<grid, kBlock, lds, s>>>(ncols, p->theta, rowptr[cur], col[cur],
+                                                     I(dp.tptr), I(dp.tlist), I(dp.tpos),
+                                                     keys_in, dp.cand_cap, dctr);
+        GCN_DR(hipGetLastError(), "pair counting");
+        GCN_DR(hipMemcpyAsync(&hc, dctr, sizeof(hc), hipMemcpyDeviceToHost, s), "counters");
+        GCN_DR(hipStreamSynchronize(s), "pair counting");
+        if (hc.error) {
+            set_error("gcn_redundancy_reduce_device: %s in round %d",
+                      hc.error == 1 ? "candidate capacity exceeded" : "list id out of range",
+                      round + 1);
+            return GCN_E_INTERNAL;
+        }
+        const int64_t nc = (int64_t)hc.ncand;
+        if (nc == 0) break;
+        // Algorithm 2: sort by (weight descending, x, y), then the greedy scan
+        size_t tmp = dp.sort_tmp;
+        GCN_DR(rocprim::radix_sort_keys(base + dp.sort, tmp, keys_in, keys_out, (unsigned)nc, 0,
+                                        56, s),
+               "candidate sort");
+        const int64_t budget = std::min<int64_t>(budget_left, dp.pairs_cap - naux);
+        greedy_kernel<<<1, kGreedyThreads, 0, s>>>(keys_out, nc, ncols, budget,
+                                                   pairs + 2 * naux, dctr);
+        GCN_DR(hipGetLastError(), "matching");
+        GCN_DR(hipMemcpyAsync(&hc, dctr, sizeof(hc), hipMemcpyDeviceToHost, s), "counters");
+        GCN_DR(hipStreamSynchronize(s), "matching");
+        const int64_t taken = hc.taken;
+        if (taken == 0) break;
+        const bool exhausted = hc.exhausted && taken >= budget_left;
+        // Algorithm 3: rewrite every list
+        const int nxt = cur ^ 1;
+        set_partner_kernel<<<items_grid(taken), kBlock, 0, s>>>(pairs + 2 * naux, taken, ncols,
+                                                                I(dp.partner), I(dp.newid), 0);
+        rewrite_count_kernel<<<waves_grid(n), kBlock, 0, s>>>((int)n, rowptr[cur], col[cur],
+                                                               I(dp.partner), I(dp.rowlen), dctr);
+        scan_kernel<<<1, kScanThreads, 0, s>>>(I(dp.rowlen), rowptr[nxt], (int)n);
+        rewrite_fill_kernel<<<waves_grid(n), kBlock, 0, s>>>((int)n, rowptr[cur], col[cur],
+                                                              I(dp.partner), I(dp.newid),
+                                                              rowptr[nxt], col[nxt], I(dp.scratch));
+        rank_ids_kernel<<<waves_grid(n), kBlock, 0, s>>>((int)n, rowptr[cur], rowptr[nxt],
+                                                          I(dp.scratch), col[nxt]);
+        set_partner_kernel<<<items_grid(taken), kBlock, 0, s>>>(pairs + 2 * naux, taken, ncols,
+                                                                I(dp.partner), I(dp.newid), 1);
+        GCN_DR(hipGetLastError(), "rewrite");
+        int32_t new_nnz = 0;
+        GCN_DR(hipMemcpyAsync(&new_nnz, rowptr[nxt] + n, 4, hipMemcpyDeviceToHost, s), "nnz");
+        GCN_DR(hipMemcpyAsync(&hc, dctr, sizeof(hc), hipMemcpyDeviceToHost, s), "counters");
+        GCN_DR(hipStreamSynchronize(s), "rewrite");
+        naux += taken;
+        ncols += (int32_t)taken;
+        cur = nxt;
+        cur_nnz = new_nnz;
+        out->round_offsets.push_back((int32_t)naux);
+        out->stats.push_back({taken, hc.wsum, cur_nnz, (int64_t)hc.num_add});
+        if (exhausted) break;
+    }
+    out->naux = (int32_t)naux;
+    out->rowptr.resize(n + 1);
+    out->col.resize(cur_nnz);
+    out->pairs.resize(2 * naux);
+    GCN_DR(hipMemcpyAsync(out->rowptr.data(), rowptr[cur], 4 * (size_t)(n + 1),
+                          hipMemcpyDeviceToHost, s),
+           "download");
+    if (cur_nnz)
+        GCN_DR(hipMemcpyAsync(out->col.data(), col[cur], 4 * (size_t)cur_nnz, hipMemcpyDeviceToHost, s),
+               "download");
+    if (naux)
+        GCN_DR(hipMemcpyAsync(out->pairs.data(), pairs, 8 * (size_t)naux, hipMemcpyDeviceToHost, s),
+               "download");
+    GCN_DR(hipStreamSynchronize(s), "download");
+#undef GCN_DR
+    return GCN_OK;
+}
+
+}  // namespace gcn
+
+// ------------------------------------------------------------ C ABI
+using gcn::set_error;
+
+extern "C" {
+
+int gcn_redundancy_reduce_device_bytes(gcn_graph_t g, const gcn_rr_params* params,
+                                       size_t* bytes) {
+    GCN_CHECK_ARG(g && params && bytes, "gcn_redundancy_reduce_device_bytes: NULL argument");
+    GCN_CHECK_ARG(params->theta >= 0, "gcn_redundancy_reduce_device_bytes: theta < 0");
+    const int rc = gcn::redundancy_reduce_device_bytes(g->rowptr.data(), g->n, params, bytes);
+    if (rc) set_error("gcn_redundancy_reduce_device_bytes: sort planning failed");
+    return rc;
+}
+
+int gcn_redundancy_reduce_device(gcn_graph_t g, const gcn_rr_params* params, void* ws,
+                                 size_t ws_bytes, gcn_stream_t stream, gcn_reduced_t* out) {
+    GCN_CHECK_ARG(g && params && out, "gcn_redundancy_reduce_device: NULL argument");
+    GCN_CHECK_ARG(params->theta >= 0, "gcn_redundancy_reduce_device: theta < 0");
+    GCN_CHECK_ARG(params->max_rounds >= 0 && params->max_rounds <= GCN_MAX_ROUNDS,
+                  "gcn_redundancy_reduce_device: max_rounds %d outside [0, %d]",
+                  params->max_rounds, GCN_MAX_ROUNDS);
+    GCN_CHECK_ARG(ws != nullptr && ((uintptr_t)ws % 256) == 0,
+                  "gcn_redundancy_reduce_device: workspace NULL or not 256-byte aligned");
+    try {
+        gcn::DeviceReduceResult res;
+        const int rc = gcn::redundancy_reduce_device(g->rowptr.data(), g->col.data(), g->n,
+                                                     params, ws, ws_bytes,
+                                                     (hipStream_t)stream, &res);
+        if (rc) return rc;
+        auto* r = new gcn_reduced;
+        r->n = g->n;
+        r->naux = res.naux;
+        r->rounds = (int32_t)res.stats.size();
+        r->rowptr = std::move(res.rowptr);
+        r->col = std::move(res.col);
+        r->pairs = std::move(res.pairs);
+        r->round_offsets = std::move(res.round_offsets);
+        r->stats = std::move(res.stats);
+        r->deg.resize(g->n);
+        for (int32_t v = 0; v < g->n; ++v) r->deg[v] = g->rowptr[v + 1] - g->rowptr[v];
+        *out = r;
+        gcn::clear_error();
+        return GCN_OK;
+    } catch (const std::bad_alloc&) {
+        set_error("gcn_redundancy_reduce_device: out of host memory");
+        return GCN_E_OOM;
+    }
+}
+
+}  // extern "C"

@@ -102,6 +102,10 @@ _subgraph_build = _proto("gcn_subgraph_build", [_i64, _vp, _vp, _i64, _vp, _i64,
 _graph_info = _proto("gcn_graph_info", [_vp, _pi32, _pi64, C.POINTER(_pi32), C.POINTER(_pi32)])
 _graph_free = _proto("gcn_graph_free", [_vp], None)
 _reduce = _proto("gcn_redundancy_reduce", [_vp, C.POINTER(RrParams), C.POINTER(_vp)])
+_reduce_dev_bytes = _proto("gcn_redundancy_reduce_device_bytes",
+                           [_vp, C.POINTER(RrParams), C.POINTER(_sz)])
+_reduce_dev = _proto("gcn_redundancy_reduce_device",
+                     [_vp, C.POINTER(RrParams), _vp, _sz, _vp, C.POINTER(_vp)])
 _reduced_info = _proto("gcn_reduced_info", [_vp, _pi32, _pi32, _pi32, _pi64,
                                             C.POINTER(_pi32), C.POINTER(_pi32), C.POINTER(_pi32),
                                             C.POINTER(_pi32), C.POINTER(C.POINTER(RrRound)),
@@ -161,6 +165,7 @@ _pipe_destroy = _proto("gcn_pipeline_destroy", [_vp], None)
 EXPORTS = [
     "gcn_last_error", "gcn_abi_version", "gcn_subgraph_build", "gcn_graph_info",
     "gcn_graph_free", "gcn_redundancy_reduce", "gcn_reduced_info", "gcn_reduced_free",
+    "gcn_redundancy_reduce_device_bytes", "gcn_redundancy_reduce_device",
     "gcn_graph_image_bytes", "gcn_graph_pack", "gcn_graph_upload", "gcn_graph_describe",
     "gcn_scratch_bytes", "gcn_aggregate", "gcn_layer_fwd", "gcn_classifier_fwd",
     "gcn_loss", "gcn_classifier_bwd", "gcn_layer_bwd", "gcn_workspace_layout",
@@ -268,6 +273,23 @@ def redundancy_reduce(g: Graph, theta=2, max_rounds=5, max_aux=-1, num_threads=0
     p = RrParams(int(theta), int(max_rounds), int(max_aux), int(num_threads), 0)
     out = _vp()
     _check(_reduce(g._h, C.byref(p), C.byref(out)))
+    return Reduced(out.value)
+
+
+def redundancy_reduce_device_bytes(g: Graph, theta=2, max_rounds=5, max_aux=-1) -> int:
+    p = RrParams(int(theta), int(max_rounds), int(max_aux), 0, 0)
+    b = _sz()
+    _check(_reduce_dev_bytes(g._h, C.byref(p), C.byref(b)))
+    return b.value
+
+
+def redundancy_reduce_device(g: Graph, ws, theta=2, max_rounds=5, max_aux=-1,
+                             stream=None) -> Reduced:
+    """The rounds of Algorithms 1-3 on the GPU (synchronous); `ws` is a
+    device workspace of redundancy_reduce_device_bytes() bytes."""
+    p = RrParams(int(theta), int(max_rounds), int(max_aux), 0, 0)
+    out = _vp()
+    _check(_reduce_dev(g._h, C.byref(p), _ptr(ws), ws.numel(), _stream(stream), C.byref(out)))
     return Reduced(out.value)
 
 
