@@ -50,6 +50,8 @@ def parse():
     ap.add_argument("--workers", type=int, default=0,
                     help="host preparation threads of the stream workload (0: min(16, cores))")
     ap.add_argument("--stream-len", type=int, default=64)
+    ap.add_argument("--device-workers", type=int, default=4,
+                    help="stream workload: workers of the pipeline that reduces on the GPU")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="also run one plain device copy of this size (HBM counter "
                          "calibration under rocprofv3 --pmc)")
@@ -514,46 +516,55 @@ def run_stream(args):
     print(f"[bench] device only: {gpu_ms:.3f} ms/step", file=sys.stderr, flush=True)
 
     # Phase B: the overlapped schedule
-    workers = args.workers or min(16, os.cpu_count() or 1)
     slots = [gcn.alloc_ws(img_bytes) for _ in range(2)]
     copy = torch.cuda.Stream()
     comp = torch.cuda.current_stream()
-    slot_free = [None, None]
-    held = collections.deque()
-    infos = []
-    pipe = gcn.Pipeline(theta=wl.theta, max_rounds=wl.rounds, max_aux=wl.max_aux,
-                        seg_len=args.seg_len, workers=workers, depth=2 * workers + 2,
-                        pinned=True, num_threads=1)
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for inp in inps:
-        pipe.submit(wl.n, inp.src, inp.dst)
-    for i in range(K):
-        jid, ptr, nb, info = pipe.next()
-        infos.append(info)
-        slot = i % 2
-        with torch.cuda.stream(copy):
-            if slot_free[slot] is not None:
-                copy.wait_event(slot_free[slot])
-            d = gcn.upload_image(ptr, nb, slots[slot], stream=copy)
-            copied = torch.cuda.Event()
-            copied.record(copy)
-        comp.wait_event(copied)
-        step(_Desc(d), i)
-        done = torch.cuda.Event()
-        done.record(comp)
-        slot_free[slot] = done
-        held.append((jid, copied))
-        while len(held) > 1:
-            j, e = held.popleft()
-            e.synchronize()
+
+    def overlapped(workers, device_reduce):
+        slot_free = [None, None]
+        held = collections.deque()
+        infos = []
+        pipe = gcn.Pipeline(theta=wl.theta, max_rounds=wl.rounds, max_aux=wl.max_aux,
+                            seg_len=args.seg_len, workers=workers, depth=2 * workers + 2,
+                            pinned=True, num_threads=1, device_reduce=device_reduce)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for inp in inps:
+            pipe.submit(wl.n, inp.src, inp.dst)
+        for i in range(K):
+            jid, ptr, nb, info = pipe.next()
+            infos.append(info)
+            slot = i % 2
+            with torch.cuda.stream(copy):
+                if slot_free[slot] is not None:
+                    copy.wait_event(slot_free[slot])
+                d = gcn.upload_image(ptr, nb, slots[slot], stream=copy)
+                copied = torch.cuda.Event()
+                copied.record(copy)
+            comp.wait_event(copied)
+            step(_Desc(d), i)
+            done = torch.cuda.Event()
+            done.record(comp)
+            slot_free[slot] = done
+            held.append((jid, copied))
+            while len(held) > 1:
+                j, e = held.popleft()
+                e.synchronize()
+                pipe.release(j)
+        torch.cuda.synchronize()
+        ms = 1e3 * (time.perf_counter() - t0) / K
+        for j, _ in held:
             pipe.release(j)
-    torch.cuda.synchronize()
-    pipe_ms = 1e3 * (time.perf_counter() - t0) / K
-    for j, _ in held:
-        pipe.release(j)
-    pipe.close()
+        pipe.close()
+        return ms, infos
+
+    workers = args.workers or min(16, os.cpu_count() or 1)
+    pipe_ms, infos = overlapped(workers, False)
     print(f"[bench] pipelined with {workers} workers: {pipe_ms:.3f} ms/step",
+          file=sys.stderr, flush=True)
+    dworkers = args.device_workers
+    dev_ms, dinfos = overlapped(dworkers, True)
+    print(f"[bench] pipelined with {dworkers} workers reducing on the GPU: {dev_ms:.3f} ms/step",
           file=sys.stderr, flush=True)
     ktab = kernel_table(prof, min(args.profile_steps, K))
     dominant = max(ktab, key=lambda k: ktab[k]["ms_per_step"])
@@ -589,6 +600,12 @@ def run_stream(args):
         "host_prepare_ms_per_subgraph": {
             "one_thread_mean": round(sum(prep_ms) / K, 2),
             "in_pipeline_reduce_mean": round(sum(reduce_ms) / K, 2)},
+        "device_reduction_pipeline": {
+            "ms_per_step": round(dev_ms, 4), "steps_per_s": round(1e3 / dev_ms, 3),
+            "workers": dworkers,
+            "reduce_ms_mean": round(sum(i.reduce_ms for i in dinfos) / K, 3),
+            "note": "the same schedule with each worker running Algorithms 1-3 on the GPU "
+                    "(gcn_redundancy_reduce_device, identical result) on a stream of its own"},
         "kernels": {k: {kk: vv for kk, vv in v.items()
                         if kk not in ("flops_per_launch", "bytes_per_launch")}
                     for k, v in ktab.items()},

@@ -217,8 +217,15 @@ int gcn_graph_describe(const void* host_image, size_t bytes,
  * minibatch the host prepares the next ones, several at once. A pipeline
  * owns `workers` host threads; each submitted subgraph is built
  * (gcn_subgraph_build), reduced (gcn_redundancy_reduce with `params`) and
- * packed (gcn_graph_pack) into a host buffer (page-locked when pinned != 0,
- * so uploads are asynchronous DMA). Results come back in submission order.
+ * packed (gcn_graph_pack) into a host buffer (page-locked with
+ * GCN_PIPE_PINNED, so uploads are asynchronous DMA). Results come back in
+ * submission order.
+ *   flags  GCN_PIPE_PINNED: page-locked image buffers.
+ *          GCN_PIPE_DEVICE_REDUCE: each worker reduces on the GPU that is
+ *          current when the pipeline is created
+ *          (gcn_redundancy_reduce_device, same result), on a stream of its
+ *          own (default priority), with a device workspace that the worker
+ *          allocates, grows on demand and frees at destroy.
  * gcn_pipeline_submit - copies the edge arrays (the caller may free them on
  *   return) and queues the job; *job_id receives its number (0, 1, ...).
  * gcn_pipeline_next - waits for the oldest job not yet taken and returns its
@@ -237,11 +244,13 @@ typedef struct {
     int32_t n, naux, rounds, reserved;
     int64_t nnz;          /* list entries of G_s^#     */
     int64_t nnz_direct;   /* list entries of G_s       */
-    double build_ms, reduce_ms, pack_ms;   /* host time of this job */
+    double build_ms, reduce_ms, pack_ms;   /* wall time of this job's steps */
 } gcn_pipeline_info;
 
+#define GCN_PIPE_PINNED 1
+#define GCN_PIPE_DEVICE_REDUCE 2
 int gcn_pipeline_create(const gcn_rr_params* params, int32_t seg_len,
-                        int32_t workers, int32_t depth, int32_t pinned,
+                        int32_t workers, int32_t depth, int32_t flags,
                         gcn_pipeline_t* out);
 int gcn_pipeline_submit(gcn_pipeline_t p, int64_t n_full, const int64_t* src,
                         const int64_t* dst, int64_t n_edges,

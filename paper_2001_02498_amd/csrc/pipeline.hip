@@ -1,8 +1,9 @@
 // Host side of the per-minibatch schedule (Section 4.4): while the device
 // trains on one subgraph, host threads prepare the next ones — subgraph
-// construction, redundancy reduction (Algorithms 1-3 in rounds) and packing
-// of the device image into (optionally pinned) host memory — each worker on
-// its own subgraph, since minibatches are independent. The consumer takes
+// construction, redundancy reduction (Algorithms 1-3 in rounds, on the host
+// or driven on the GPU from the worker's own stream) and packing of the
+// device image into (optionally pinned) host memory — each worker on its
+// own subgraph, since minibatches are independent. The consumer takes
 // prepared images in submission order and uploads them itself.
 #include <hip/hip_runtime.h>
 
@@ -49,6 +50,8 @@ struct gcn_pipeline {
     int32_t seg_len = 0;
     int32_t depth = 1;
     bool pinned = false;
+    bool device_reduce = false;
+    int device = 0;
     std::mutex mu;
     std::condition_variable cv_work, cv_done;
     std::deque<std::shared_ptr<Job>> todo;
@@ -80,7 +83,50 @@ struct gcn_pipeline {
         b.cap = 0;
     }
 
+    // per-worker device state of the device reduction
+    struct DevState {
+        hipStream_t stream = nullptr;
+        void* ws = nullptr;
+        size_t cap = 0;
+    };
+
     void run() {
+        DevState ds;
+        if (device_reduce) {
+            (void)hipSetDevice(device);
+            if (hipStreamCreate(&ds.stream) != hipSuccess) ds.stream = nullptr;
+        }
+        run_jobs(ds);
+        if (ds.ws) (void)hipFree(ds.ws);
+        if (ds.stream) (void)hipStreamDestroy(ds.stream);
+    }
+
+    // device reduction with a workspace grown to fit (256-byte aligned by
+    // hipMalloc)
+    int reduce_on_device(gcn_graph_t g, DevState& ds, gcn_reduced_t* r) {
+        if (!ds.stream) {
+            set_error("gcn_pipeline: worker stream not created");
+            return GCN_E_HIP;
+        }
+        size_t need = 0;
+        int rc = gcn_redundancy_reduce_device_bytes(g, &rr, &need);
+        if (rc) return rc;
+        if (need > ds.cap) {
+            if (ds.ws) (void)hipFree(ds.ws);
+            ds.ws = nullptr;
+            ds.cap = 0;
+            const size_t bytes = need + need / 2;
+            if (hipMalloc(&ds.ws, bytes) != hipSuccess) {
+                ds.ws = nullptr;
+                set_error("gcn_pipeline: device workspace of %zu bytes not allocated", bytes);
+                return GCN_E_OOM;
+            }
+            ds.cap = bytes;
+        }
+        return gcn_redundancy_reduce_device(g, &rr, ds.ws, ds.cap, ds.stream, r);
+    }
+
+    void run_jobs(DevState& ds) {
         for (;;) {
             std::shared_ptr<Job> job;
             Buffer buf;
@@ -98,7 +144,7 @@ struct gcn_pipeline {
                     free_bufs.pop_back();
                 }
             }
-            prepare(*job, buf);
+            prepare(*job, buf, ds);
             {
                 std::lock_guard<std::mutex> lk(mu);
                 job->done = true;
@@ -107,7 +153,7 @@ struct gcn_pipeline {
         }
     }
 
-    void prepare(Job& job, Buffer& buf) {
+    void prepare(Job& job, Buffer& buf, DevState& ds) {
         using clock = std::chrono::steady_clock;
         const auto t0 = clock::now();
         gcn_graph_t g = nullptr;
@@ -117,7 +163,8 @@ struct gcn_pipeline {
                                     job.has_verts ? job.verts.data() : nullptr,
                                     (int64_t)job.verts.size(), &g);
         const auto t1 = clock::now();
-        if (rc == GCN_OK) rc = gcn_redundancy_reduce(g, &rr, &r);
+        if (rc == GCN_OK)
+            rc = device_reduce ? reduce_on_device(g, ds, &r) : gcn_redundancy_reduce(g, &rr, &r);
         const auto t2 = clock::now();
         size_t bytes = 0;
         if (rc == GCN_OK) rc = gcn_graph_image_bytes(r, seg_len, &bytes);
@@ -166,7 +213,7 @@ struct gcn_pipeline {
 extern "C" {
 
 int gcn_pipeline_create(const gcn_rr_params* params, int32_t seg_len, int32_t workers,
-                        int32_t depth, int32_t pinned, gcn_pipeline_t* out) {
+                        int32_t depth, int32_t flags, gcn_pipeline_t* out) {
     GCN_CHECK_ARG(params && out, "gcn_pipeline_create: NULL argument");
     GCN_CHECK_ARG(workers >= 1 && workers <= 256, "gcn_pipeline_create: workers outside [1, 256]");
     GCN_CHECK_ARG(depth >= 1 && depth <= 4096, "gcn_pipeline_create: depth outside [1, 4096]");
@@ -175,12 +222,20 @@ int gcn_pipeline_create(const gcn_rr_params* params, int32_t seg_len, int32_t wo
                   "gcn_pipeline_create: bad reduction parameters");
     GCN_CHECK_ARG(seg_len == 0 || (seg_len >= 1 && seg_len <= 65536),
                   "gcn_pipeline_create: seg_len outside [1, 65536]");
+    GCN_CHECK_ARG((flags & ~(GCN_PIPE_PINNED | GCN_PIPE_DEVICE_REDUCE)) == 0,
+                  "gcn_pipeline_create: unknown flags 0x%x", flags);
     try {
         auto* p = new gcn_pipeline;
         p->rr = *params;
         p->seg_len = seg_len;
         p->depth = depth;
-        p->pinned = pinned != 0;
+        p->pinned = (flags & GCN_PIPE_PINNED) != 0;
+        p->device_reduce = (flags & GCN_PIPE_DEVICE_REDUCE) != 0;
+        if (p->device_reduce && hipGetDevice(&p->device) != hipSuccess) {
+            delete p;
+            set_error("gcn_pipeline_create: no current GPU for the device reduction");
+            return GCN_E_HIP;
+        }
         for (int32_t i = 0; i < workers; ++i) p->workers.emplace_back([p] { p->run(); });
         *out = p;
         return GCN_OK;

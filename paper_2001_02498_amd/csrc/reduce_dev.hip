@@ -12,10 +12,11 @@
 //                parallel and takes the rest in key order with one thread:
 //                the greedy matching under the budget, pair by pair as the
 //                host takes it.
-//   Algorithm 3  every list is rewritten by one wavefront: entries whose
-//                partner is in the same list are replaced by the pair's new
-//                id; kept entries keep their order and the new ids (all
-//                larger) follow in increasing order.
+//   Algorithm 3  every list is rewritten by one workgroup (its ids marked
+//                in an LDS bitmap): entries whose partner is in the same
+//                list are replaced by the pair's new id; kept entries keep
+//                their order and the new ids (all larger) follow in
+//                increasing order.
 // The host drives the rounds and reads a few counters back after the pair
 // counting and after the matching (the sort needs the candidate count).
 #include <rocprim/device/device_radix_sort.hpp>
@@ -127,54 +128,121 @@ __global__ __launch_bounds__(kBlock) void tfill_kernel(int n, int ncols,
 // holding both, in 16-bit counters packed two per LDS word (a count never
 // reaches 2^16: it is at most the number of lists); pairs whose count
 // exceeds theta (and 1: weight-1 pairs are no edges of G_a) are emitted.
-__global__ __launch_bounds__(kBlock) void count_pairs_kernel(
+// The parts of the lists after x are staged (start, prefix of lengths) in
+// LDS, kCountStage lists at a time, and all threads sweep their
+// concatenation, so a hub with thousands of lists keeps every lane busy.
+constexpr int kCountThreads = 512;
+constexpr int kCountStage = 1024;
+
+__global__ __launch_bounds__(kCountThreads) void count_pairs_kernel(
     int ncols, int theta, const int32_t* __restrict__ rowptr, const int32_t* __restrict__ col,
     const int32_t* __restrict__ tptr, const int32_t* __restrict__ tlist,
     const int32_t* __restrict__ tpos, uint64_t* __restrict__ cand, int64_t cap,
     RoundCounters* rc) {
     extern __shared__ uint32_t cnt[];
+    __shared__ int32_t s_start[kCountStage];
+    __shared__ int32_t s_off[kCountStage + 1];
+    __shared__ int32_t s_wave[kCountThreads / 64];
     const int nw = (ncols + 1) / 2;
     const int t = threadIdx.x, lane = t % 64, wave = t / 64;
-    for (int i = t; i < nw; i += kBlock) cnt[i] = 0;
+    for (int i = t; i < nw; i += kCountThreads) cnt[i] = 0;
     __syncthreads();
     for (int x = blockIdx.x; x < ncols; x += gridDim.x) {
         const int tb = tptr[x], te = tptr[x + 1];
         if (te - tb < 2) continue;   // uniform: x in fewer than two lists
-        for (int k = tb + wave; k < te; k += kBlock / 64) {
-            const int w = tlist[k];
-            const int re = rowptr[w + 1];
-            for (int p = rowptr[w] + tpos[k] + 1 + lane; p < re; p += 64) {
-                const int y = col[p];
+        for (int kb = tb; kb < te; kb += kCountStage) {
+            const int m = min(kCountStage, te - kb);
+            // thread t stages lists 2t, 2t + 1 of this pass
+            int len[2], sum = 0;
+            for (int j = 0; j < 2; ++j) {
+                const int i = 2 * t + j;
+                len[j] = 0;
+                if (i < m) {
+                    const int k = kb + i, w = tlist[k];
+                    const int st = rowptr[w] + tpos[k] + 1;
+                    s_start[i] = st;
+                    len[j] = rowptr[w + 1] - st;
+                }
+                sum += len[j];
+            }
+            int incl = sum;
+            for (int off = 1; off < 64; off <<= 1) {
+                const int v = __shfl_up(incl, off);
+                if (lane >= off) incl += v;
+            }
+            if (lane == 63) s_wave[wave] = incl;
+            __syncthreads();
+            int before = 0;
+            for (int v = 0; v < wave; ++v) before += s_wave[v];
+            int run = before + incl - sum;
+            for (int j = 0; j < 2; ++j) {
+                const int i = 2 * t + j;
+                if (i < m) s_off[i] = run;
+                run += len[j];
+            }
+            if (t == kCountThreads - 1) s_off[m] = run;   // total (run after the last thread)
+            __syncthreads();
+            const int total = s_off[m];
+            int k = 0;
+            for (int v = t; v < total; v += kCountThreads) {
+                // the staged list holding visit v: the last k with s_off[k] <= v
+                int lo = k, hi = m - 1;
+                while (lo < hi) {
+                    const int mid = (lo + hi + 1) >> 1;
+                    if (s_off[mid] <= v)
+                        lo = mid;
+                    else
+                        hi = mid - 1;
+                }
+                k = lo;
+                const int y = col[s_start[k] + (v - s_off[k])];
                 if (y < ncols) atomicAdd(&cnt[y >> 1], 1u << ((y & 1) * 16));
             }
+            __syncthreads();
+        }
+        // Emit the pairs of x (counters of y > x, from the word holding
+        // x + 1): count them, reserve one range of slots for the workgroup,
+        // then write each thread's pairs at its prefix and clear.
+        const int w0 = (x + 1) >> 1;
+        auto emits = [&](uint32_t v, int wd, int h) {
+            const int y = 2 * wd + h;
+            const uint32_t c = (v >> (16 * h)) & 0xFFFFu;
+            return y > x && (int)c > theta && c >= 2;
+        };
+        int mine = 0;
+        for (int wd = w0 + t; wd < nw; wd += kCountThreads) {
+            const uint32_t v = cnt[wd];
+            if (v) mine += emits(v, wd, 0) + emits(v, wd, 1);
+        }
+        int incl = mine;
+        for (int off = 1; off < 64; off <<= 1) {
+            const int v = __shfl_up(incl, off);
+            if (lane >= off) incl += v;
+        }
+        if (lane == 63) s_wave[wave] = incl;
+        __syncthreads();
+        __shared__ unsigned long long s_base;
+        if (t == 0) {
+            int tot = 0;
+            for (int v = 0; v < kCountThreads / 64; ++v) tot += s_wave[v];
+            s_base = tot ? atomicAdd(&rc->ncand, (unsigned long long)tot) : 0ull;
         }
         __syncthreads();
-        // emit and clear the counters of y > x (the word holding x + 1 on)
-        for (int wd0 = ((x + 1) >> 1); wd0 < nw; wd0 += kBlock) {
-            const int wd = wd0 + t;
-            uint32_t v = 0;
-            if (wd < nw) {
-                v = cnt[wd];
-                if (v) cnt[wd] = 0;
-            }
+        int before = 0;
+        for (int v = 0; v < wave; ++v) before += s_wave[v];
+        unsigned long long slot = s_base + (unsigned long long)(before + incl - mine);
+        for (int wd = w0 + t; wd < nw; wd += kCountThreads) {
+            const uint32_t v = cnt[wd];
+            if (!v) continue;
+            cnt[wd] = 0;
             for (int h = 0; h < 2; ++h) {
-                const int y = 2 * wd + h;
-                const uint32_t c = (v >> (16 * h)) & 0xFFFFu;
-                const bool emit = wd < nw && y > x && (int)c > theta && c >= 2;
-                // wave-aggregated slot reservation
-                const uint64_t m = __ballot(emit);
-                if (m == 0) continue;
-                unsigned long long base = 0;
-                if (lane == 0) base = atomicAdd(&rc->ncand, (unsigned long long)__popcll(m));
-                base = __shfl(base, 0);
-                if (emit) {
-                    const int r = __popcll(m & ((1ull << lane) - 1));
-                    const unsigned long long slot = base + r;
-                    if ((int64_t)slot < cap)
-                        cand[slot] = cand_key(c, (uint32_t)x, (uint32_t)y);
-                    else
-                        rc->error = 1;
-                }
+                if (!emits(v, wd, h)) continue;
+                if ((int64_t)slot < cap)
+                    cand[slot] = cand_key((v >> (16 * h)) & 0xFFFFu, (uint32_t)x,
+                                          (uint32_t)(2 * wd + h));
+                else
+                    rc->error = 1;
+                ++slot;
             }
         }
         __syncthreads();
@@ -204,14 +272,26 @@ __global__ __launch_bounds__(kGreedyThreads) void greedy_kernel(
     }
     __syncthreads();
     auto is_used = [&](uint32_t v) { return (used[v >> 5] >> (v & 31)) & 1u; };
+    // keys of the next block are loaded while this one is filtered and taken
+    uint64_t k_next[kGreedyPer];
+#pragma unroll
+    for (int j = 0; j < kGreedyPer; ++j) {
+        const int64_t i = (int64_t)t * kGreedyPer + j;
+        k_next[j] = i < nc ? keys[i] : ~0ull;
+    }
     for (int64_t base = 0; base < nc; base += kGreedyBlock) {
         uint64_t k[kGreedyPer];
         int alive = 0;
         bool live[kGreedyPer];
 #pragma unroll
         for (int j = 0; j < kGreedyPer; ++j) {
+            k[j] = k_next[j];
+            const int64_t i2 = base + kGreedyBlock + (int64_t)t * kGreedyPer + j;
+            k_next[j] = i2 < nc ? keys[i2] : ~0ull;
+        }
+#pragma unroll
+        for (int j = 0; j < kGreedyPer; ++j) {
             const int64_t i = base + (int64_t)t * kGreedyPer + j;
-            k[j] = i < nc ? keys[i] : ~0ull;
             const uint32_t x = (uint32_t)(k[j] >> 20) & 0xFFFFFu, y = (uint32_t)k[j] & 0xFFFFFu;
             live[j] = i < nc && x < (uint32_t)ncols && y < (uint32_t)ncols && !is_used(x) && !is_used(y);
             alive += live[j];
@@ -239,26 +319,42 @@ __global__ __launch_bounds__(kGreedyThreads) void greedy_kernel(
         for (int j = 0; j < kGreedyPer; ++j)
             if (live[j]) surv[pos++] = k[j];
         __syncthreads();
-        if (t == 0) {
+        // wave 0 takes the survivors in order, 64 at a time: the first
+        // live one is taken, the others drop if they touch its endpoints
+        if (wave == 0) {
             long long taken = s_taken, wsum = s_wsum;
-            for (int s = 0; s < nsurv; ++s) {
-                const uint64_t key = surv[s];
+            bool halt = false;
+            for (int c0 = 0; c0 < nsurv && !halt; c0 += 64) {
+                const int si = c0 + lane;
+                const uint64_t key = si < nsurv ? surv[si] : ~0ull;
                 const uint32_t x = (uint32_t)(key >> 20) & 0xFFFFFu, y = (uint32_t)key & 0xFFFFFu;
-                if (is_used(x) || is_used(y)) continue;
-                if (taken >= budget) {
-                    stop = 1;
-                    break;
+                bool live = si < nsurv && !is_used(x) && !is_used(y);
+                uint64_t m = __ballot(live);
+                while (m) {
+                    if (taken >= budget) {
+                        halt = true;
+                        break;
+                    }
+                    const int j = __ffsll((long long)m) - 1;
+                    const uint64_t kj = __shfl(key, j);
+                    const uint32_t xj = (uint32_t)(kj >> 20) & 0xFFFFFu, yj = (uint32_t)kj & 0xFFFFFu;
+                    if (lane == 0) {
+                        used[xj >> 5] |= 1u << (xj & 31);
+                        used[yj >> 5] |= 1u << (yj & 31);
+                        pairs[2 * taken] = (int32_t)xj;
+                        pairs[2 * taken + 1] = (int32_t)yj;
+                    }
+                    wsum += 0xFFFFu - (uint32_t)(kj >> 40);
+                    ++taken;
+                    live = live && lane > j && x != xj && x != yj && y != xj && y != yj;
+                    m = __ballot(live);
                 }
-                used[x >> 5] |= 1u << (x & 31);
-                used[y >> 5] |= 1u << (y & 31);
-                pairs[2 * taken] = (int32_t)x;
-                pairs[2 * taken + 1] = (int32_t)y;
-                wsum += 0xFFFFu - (uint32_t)(key >> 40);
-                ++taken;
             }
-            s_taken = taken;
-            s_wsum = wsum;
-            if (taken >= budget) stop = 1;
+            if (lane == 0) {
+                s_taken = taken;
+                s_wsum = wsum;
+                if (halt || taken >= budget) stop = 1;
+            }
         }
         __syncthreads();
         if (stop) break;
@@ -282,90 +378,117 @@ __global__ void set_partner_kernel(const int32_t* __restrict__ pairs, int64_t ta
     newid[x] = newid[y] = reset ? -1 : id0 + (int32_t)i;
 }
 
-__device__ __forceinline__ bool in_row(const int32_t* __restrict__ row, int d, int32_t v) {
-    int lo = 0, hi = d;
-    while (lo < hi) {
-        const int mid = (lo + hi) >> 1;
-        if (row[mid] < v)
-            lo = mid + 1;
-        else
-            hi = mid;
+// One workgroup per list; the list's ids are marked in an LDS bitmap
+// (ncols bits, cleared first: LDS starts with whatever the previous
+// workgroup left) so that "is my partner in this list" is one LDS read.
+constexpr int kRowThreads = 256;
+constexpr int kRowIds = 4096;   // new ids of one list ranked in LDS (beyond: scratch)
+
+__device__ __forceinline__ void mark_row(uint32_t* bits, int nwords,
+                                         const int32_t* __restrict__ row, int d) {
+    for (int i = threadIdx.x; i < nwords; i += kRowThreads) bits[i] = 0;
+    __syncthreads();
+    for (int i = threadIdx.x; i < d; i += kRowThreads) {
+        const int32_t c = row[i];
+        atomicOr(&bits[c >> 5], 1u << (c & 31));
     }
-    return lo < d && row[lo] == v;
 }
 
-// new length of every list (one wavefront per list) and the sum of
-// max(length - 1, 0), numAdd of Section 3.2
-__global__ __launch_bounds__(kBlock) void rewrite_count_kernel(
-    int n, const int32_t* __restrict__ rowptr, const int32_t* __restrict__ col,
+__device__ __forceinline__ bool has(const uint32_t* bits, int32_t v) {
+    return (bits[v >> 5] >> (v & 31)) & 1u;
+}
+
+// block-wide exclusive prefix of a 0/1 flag (order = thread order); returns
+// the prefix and writes the block total
+__device__ __forceinline__ int block_prefix(bool f, int32_t* s_wave, int* total) {
+    const int lane = threadIdx.x % 64, wave = threadIdx.x / 64;
+    const uint64_t m = __ballot(f);
+    if (lane == 0) s_wave[wave] = __popcll(m);
+    __syncthreads();
+    int before = 0, all = 0;
+    for (int w = 0; w < kRowThreads / 64; ++w) {
+        const int v = s_wave[w];
+        if (w < wave) before += v;
+        all += v;
+    }
+    __syncthreads();
+    *total = all;
+    return before + __popcll(m & ((1ull << lane) - 1));
+}
+
+// new length of every list and the sum of max(length - 1, 0), numAdd of
+// Section 3.2
+__global__ __launch_bounds__(kRowThreads) void rewrite_count_kernel(
+    int n, int ncols, const int32_t* __restrict__ rowptr, const int32_t* __restrict__ col,
     const int32_t* __restrict__ partner, int32_t* __restrict__ rowlen, RoundCounters* rc) {
-    const int w = blockIdx.x * (kBlock / 64) + threadIdx.x / 64;
-    const int lane = threadIdx.x % 64;
-    if (w >= n) return;
+    extern __shared__ uint32_t bits[];
+    __shared__ int32_t s_wave[kRowThreads / 64];
+    const int w = blockIdx.x;
     const int b = rowptr[w], d = rowptr[w + 1] - b;
     const int32_t* row = col + b;
+    mark_row(bits, (ncols + 31) / 32, row, d);
+    __syncthreads();
     int pairs_here = 0;
-    for (int i = lane; i < d; i += 64) {
+    for (int i = threadIdx.x; i < d; i += kRowThreads) {
         const int32_t c = row[i], p = partner[c];
-        if (p >= 0 && c < p && in_row(row, d, p)) ++pairs_here;
+        if (p >= 0 && c < p && has(bits, p)) ++pairs_here;
     }
     for (int off = 32; off > 0; off >>= 1) pairs_here += __shfl_xor(pairs_here, off);
-    if (lane == 0) {
-        const int len = d - pairs_here;
+    if (threadIdx.x % 64 == 0) s_wave[threadIdx.x / 64] = pairs_here;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        int tot = 0;
+        for (int v = 0; v < kRowThreads / 64; ++v) tot += s_wave[v];
+        const int len = d - tot;
         rowlen[w] = len;
         if (len > 1) atomicAdd(&rc->num_add, (unsigned long long)(len - 1));
     }
 }
 
-// kept entries in order, then each new id written to a scratch copy at its
-// arrival position (its final place follows in rank_ids_kernel)
-__global__ __launch_bounds__(kBlock) void rewrite_fill_kernel(
-    int n, const int32_t* __restrict__ rowptr, const int32_t* __restrict__ col,
+// kept entries in order, then the new ids in increasing order (each placed
+// by its rank among the list's new ids)
+__global__ __launch_bounds__(kRowThreads) void rewrite_fill_kernel(
+    int n, int ncols, const int32_t* __restrict__ rowptr, const int32_t* __restrict__ col,
     const int32_t* __restrict__ partner, const int32_t* __restrict__ newid,
     const int32_t* __restrict__ rowptr_new, int32_t* __restrict__ col_new,
     int32_t* __restrict__ scratch) {
-    const int w = blockIdx.x * (kBlock / 64) + threadIdx.x / 64;
-    const int lane = threadIdx.x % 64;
-    if (w >= n) return;
+    extern __shared__ uint32_t bits[];
+    __shared__ int32_t s_wave[kRowThreads / 64];
+    __shared__ int32_t ids[kRowIds];
+    const int w = blockIdx.x;
     const int b = rowptr[w], d = rowptr[w + 1] - b;
     const int out = rowptr_new[w], len = rowptr_new[w + 1] - out;
     const int nadd = d - len, kept_total = len - nadd;
     const int32_t* row = col + b;
+    // new ids wait in LDS, or in the list's own stretch of scratch when many
+    int32_t* idbuf = nadd <= kRowIds ? ids : scratch + out + kept_total;
+    mark_row(bits, (ncols + 31) / 32, row, d);
+    __syncthreads();
     int kept = 0, added = 0;
-    for (int i0 = 0; i0 < d; i0 += 64) {
-        const int i = i0 + lane;
-        int32_t c = -1;
-        bool pair_in = false;
+    for (int i0 = 0; i0 < d; i0 += kRowThreads) {
+        const int i = i0 + threadIdx.x;
+        int32_t c = -1, p = -1;
         if (i < d) {
             c = row[i];
-            const int32_t p = partner[c];
-            pair_in = p >= 0 && in_row(row, d, p);
+            p = partner[c];
         }
+        const bool pair_in = p >= 0 && has(bits, p);
         const bool keep = i < d && !pair_in;
-        const bool add = pair_in && c < partner[c];
-        const uint64_t km = __ballot(keep), am = __ballot(add);
-        const uint64_t below = (1ull << lane) - 1;
-        if (keep) col_new[out + kept + __popcll(km & below)] = c;
-        if (add) scratch[out + kept_total + added + __popcll(am & below)] = newid[c];
-        kept += __popcll(km);
-        added += __popcll(am);
+        const bool add = pair_in && c < p;
+        int nk, na;
+        const int pk = block_prefix(keep, s_wave, &nk);
+        const int pa = block_prefix(add, s_wave, &na);
+        if (keep) col_new[out + kept + pk] = c;
+        if (add) idbuf[added + pa] = newid[c];
+        kept += nk;
+        added += na;
     }
-}
-
-__global__ __launch_bounds__(kBlock) void rank_ids_kernel(
-    int n, const int32_t* __restrict__ rowptr, const int32_t* __restrict__ rowptr_new,
-    const int32_t* __restrict__ scratch, int32_t* __restrict__ col_new) {
-    const int w = blockIdx.x * (kBlock / 64) + threadIdx.x / 64;
-    const int lane = threadIdx.x % 64;
-    if (w >= n) return;
-    const int d = rowptr[w + 1] - rowptr[w];
-    const int out = rowptr_new[w], len = rowptr_new[w + 1] - out;
-    const int nadd = d - len, first = out + len - nadd;
-    for (int j = lane; j < nadd; j += 64) {
-        const int32_t id = scratch[first + j];
+    __syncthreads();   // (also orders the scratch writes before the reads below)
+    for (int j = threadIdx.x; j < nadd; j += kRowThreads) {
+        const int32_t id = idbuf[j];
         int rank = 0;
-        for (int i = 0; i < nadd; ++i) rank += scratch[first + i] < id;
-        col_new[first + rank] = id;
+        for (int i = 0; i < nadd; ++i) rank += idbuf[i] < id;
+        col_new[out + kept_total + rank] = id;
     }
 }
 
@@ -531,12 +654,12 @@ int redundancy_reduce_device(const int32_t* rowptr_h, const int32_t* col_h, int6
         tfill_kernel<<<waves_grid(n), kBlock, 0, s>>>((int)n, ncols, rowptr[cur], col[cur],
                                                        I(dp.tcur), I(dp.tlist), I(dp.tpos));
         const size_t lds = 4 * (size_t)((ncols + 1) / 2);
-        if (lds > 65536)
+        if (lds > 48 * 1024)
             GCN_DR(hipFuncSetAttribute((const void*)count_pairs_kernel,
                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds),
                    "pair counting LDS");
         const unsigned grid = (unsigned)std::min<int64_t>(ncols, 4096);
-        count_pairs_kernel<<<grid, kBlock, lds, s>>>(ncols, p->theta, rowptr[cur], col[cur],
+        count_pairs_kernel<<<grid, kCountThreads, lds, s>>>(ncols, p->theta, rowptr[cur], col[cur],
                                                      I(dp.tptr), I(dp.tlist), I(dp.tpos),
                                                      keys_in, dp.cand_cap, dctr);
         GCN_DR(hipGetLastError(), "pair counting");
@@ -568,14 +691,13 @@ int redundancy_reduce_device(const int32_t* rowptr_h, const int32_t* col_h, int6
         const int nxt = cur ^ 1;
         set_partner_kernel<<<items_grid(taken), kBlock, 0, s>>>(pairs + 2 * naux, taken, ncols,
                                                                 I(dp.partner), I(dp.newid), 0);
-        rewrite_count_kernel<<<waves_grid(n), kBlock, 0, s>>>((int)n, rowptr[cur], col[cur],
-                                                               I(dp.partner), I(dp.rowlen), dctr);
+        const size_t bits = 4 * (size_t)((ncols + 31) / 32);
+        rewrite_count_kernel<<<(unsigned)n, kRowThreads, bits, s>>>(
+            (int)n, ncols, rowptr[cur], col[cur], I(dp.partner), I(dp.rowlen), dctr);
         scan_kernel<<<1, kScanThreads, 0, s>>>(I(dp.rowlen), rowptr[nxt], (int)n);
-        rewrite_fill_kernel<<<waves_grid(n), kBlock, 0, s>>>((int)n, rowptr[cur], col[cur],
-                                                              I(dp.partner), I(dp.newid),
-                                                              rowptr[nxt], col[nxt], I(dp.scratch));
-        rank_ids_kernel<<<waves_grid(n), kBlock, 0, s>>>((int)n, rowptr[cur], rowptr[nxt],
-                                                          I(dp.scratch), col[nxt]);
+        rewrite_fill_kernel<<<(unsigned)n, kRowThreads, bits, s>>>(
+            (int)n, ncols, rowptr[cur], col[cur], I(dp.partner), I(dp.newid), rowptr[nxt],
+            col[nxt], I(dp.scratch));
         set_partner_kernel<<<items_grid(taken), kBlock, 0, s>>>(pairs + 2 * naux, taken, ncols,
                                                                 I(dp.partner), I(dp.newid), 1);
         GCN_DR(hipGetLastError(), "rewrite");

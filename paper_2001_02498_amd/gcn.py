@@ -34,6 +34,8 @@ LOSS_SOFTMAX_CE = 0
 LOSS_SIGMOID_BCE = 1
 PREC_FP32 = 0
 PREC_BF16 = 1
+PIPE_PINNED = 1
+PIPE_DEVICE_REDUCE = 2
 AGG_MEAN = 0
 AGG_TRANSPOSED = 1
 ABI_VERSION = 2
@@ -478,11 +480,12 @@ class Pipeline:
     """Host worker pool preparing graph images in submission order."""
 
     def __init__(self, theta=2, max_rounds=5, max_aux=-1, seg_len=0, workers=4, depth=8,
-                 pinned=True, num_threads=1):
+                 pinned=True, num_threads=1, device_reduce=False):
         p = RrParams(int(theta), int(max_rounds), int(max_aux), int(num_threads), 0)
         self._h = _vp()
-        _check(_pipe_create(C.byref(p), int(seg_len), int(workers), int(depth),
-                            1 if pinned else 0, C.byref(self._h)))
+        flags = (PIPE_PINNED if pinned else 0) | (PIPE_DEVICE_REDUCE if device_reduce else 0)
+        _check(_pipe_create(C.byref(p), int(seg_len), int(workers), int(depth), flags,
+                            C.byref(self._h)))
 
     def submit(self, n_full, src, dst, vertices=None):
         src = np.ascontiguousarray(src, dtype=np.int64)

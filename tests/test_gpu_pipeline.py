@@ -1,6 +1,8 @@
-"""GPU: the overlapped schedule (host workers preparing, copy-stream uploads
-into two device slots, compute stream waiting on copy events) trains to the
-same weights, bit for bit, as preparing and uploading each subgraph first."""
+"""GPU: the overlapped schedule (host workers preparing -- reducing on the
+host or driving the device reduction on streams of their own -- copy-stream
+uploads into two device slots, compute stream waiting on copy events) trains
+to the same weights, bit for bit, as preparing and uploading each subgraph
+first."""
 import collections
 
 import numpy as np
@@ -24,7 +26,8 @@ def _model(gcn, wl, inp):
     return Ws, Wn, Wc
 
 
-def test_pipelined_stream_matches_sequential():
+@pytest.mark.parametrize("device_reduce", [False, True])
+def test_pipelined_stream_matches_sequential(device_reduce):
     need_gpu()
     from paper_2001_02498_amd import gcn
     import dataclasses
@@ -62,7 +65,7 @@ def test_pipelined_stream_matches_sequential():
     slot_free = [None, None]
     held = collections.deque()
     pipe = gcn.Pipeline(theta=wl.theta, max_rounds=wl.rounds, max_aux=wl.max_aux, workers=3,
-                        depth=4, pinned=True)
+                        depth=4, pinned=True, device_reduce=device_reduce)
     try:
         for inp in inps:
             pipe.submit(wl.n, inp.src, inp.dst)
