@@ -35,7 +35,7 @@ namespace {
 constexpr int kBlock = 256;
 constexpr int kScanThreads = 1024;
 constexpr int kGreedyThreads = 1024;
-constexpr int kGreedyPer = 4;                         // keys per thread per block
+constexpr int kGreedyPer = 8;                         // keys per thread per block
 constexpr int kGreedyBlock = kGreedyThreads * kGreedyPer;
 constexpr int kMaxIds = 65536;                        // 16-bit counters, 20-bit key fields
 
@@ -53,17 +53,34 @@ __device__ __forceinline__ uint64_t cand_key(uint32_t w, uint32_t x, uint32_t y)
 }
 
 // ------------------------------------------------------------------ scan
-// out[0] = 0, out[i + 1] = in[0] + .. + in[i]  (one workgroup)
+// out[0] = 0, out[i + 1] = in[0] + .. + in[i]  (one workgroup); with
+// num_add, also the sum of max(in[i] - 1, 0) (numAdd of Section 3.2 when
+// in holds list lengths)
 __global__ __launch_bounds__(kScanThreads) void scan_kernel(const int32_t* __restrict__ in,
-                                                            int32_t* __restrict__ out, int len) {
+                                                            int32_t* __restrict__ out, int len,
+                                                            unsigned long long* num_add) {
     __shared__ int32_t part[kScanThreads];
+    __shared__ unsigned long long adds[kScanThreads / 64];
     const int t = threadIdx.x;
     const int per = (len + kScanThreads - 1) / kScanThreads;
     const int b = min(len, t * per), e = min(len, b + per);
     int32_t s = 0;
-    for (int i = b; i < e; ++i) s += in[i];
+    unsigned long long a = 0;
+    for (int i = b; i < e; ++i) {
+        s += in[i];
+        a += in[i] > 1 ? (unsigned long long)(in[i] - 1) : 0ull;
+    }
+    if (num_add) {
+        for (int off = 32; off > 0; off >>= 1) a += __shfl_xor(a, off);
+        if (t % 64 == 0) adds[t / 64] = a;
+    }
     part[t] = s;
     __syncthreads();
+    if (num_add && t == 0) {
+        unsigned long long tot = 0;
+        for (int w = 0; w < kScanThreads / 64; ++w) tot += adds[w];
+        *num_add = tot;
+    }
     for (int off = 1; off < kScanThreads; off <<= 1) {
         const int32_t v = t >= off ? part[t - off] : 0;
         __syncthreads();
@@ -416,11 +433,10 @@ __device__ __forceinline__ int block_prefix(bool f, int32_t* s_wave, int* total)
     return before + __popcll(m & ((1ull << lane) - 1));
 }
 
-// new length of every list and the sum of max(length - 1, 0), numAdd of
-// Section 3.2
+// new length of every list
 __global__ __launch_bounds__(kRowThreads) void rewrite_count_kernel(
     int n, int ncols, const int32_t* __restrict__ rowptr, const int32_t* __restrict__ col,
-    const int32_t* __restrict__ partner, int32_t* __restrict__ rowlen, RoundCounters* rc) {
+    const int32_t* __restrict__ partner, int32_t* __restrict__ rowlen) {
     extern __shared__ uint32_t bits[];
     __shared__ int32_t s_wave[kRowThreads / 64];
     const int w = blockIdx.x;
@@ -439,9 +455,7 @@ __global__ __launch_bounds__(kRowThreads) void rewrite_count_kernel(
     if (threadIdx.x == 0) {
         int tot = 0;
         for (int v = 0; v < kRowThreads / 64; ++v) tot += s_wave[v];
-        const int len = d - tot;
-        rowlen[w] = len;
-        if (len > 1) atomicAdd(&rc->num_add, (unsigned long long)(len - 1));
+        rowlen[w] = d - tot;
     }
 }
 
@@ -648,7 +662,7 @@ int redundancy_reduce_device(const int32_t* rowptr_h, const int32_t* col_h, int6
         fill_kernel<<<items_grid(ncols), kBlock, 0, s>>>(I(dp.tcur), 0, ncols);
         tcount_kernel<<<waves_grid(n), kBlock, 0, s>>>((int)n, ncols, rowptr[cur], col[cur],
                                                         I(dp.tcur), dctr);
-        scan_kernel<<<1, kScanThreads, 0, s>>>(I(dp.tcur), I(dp.tptr), ncols);
+        scan_kernel<<<1, kScanThreads, 0, s>>>(I(dp.tcur), I(dp.tptr), ncols, nullptr);
         GCN_DR(hipMemcpyAsync(I(dp.tcur), I(dp.tptr), 4 * (size_t)ncols, hipMemcpyDeviceToDevice, s),
                "cursor");
         tfill_kernel<<<waves_grid(n), kBlock, 0, s>>>((int)n, ncols, rowptr[cur], col[cur],
@@ -693,8 +707,8 @@ int redundancy_reduce_device(const int32_t* rowptr_h, const int32_t* col_h, int6
                                                                 I(dp.partner), I(dp.newid), 0);
         const size_t bits = 4 * (size_t)((ncols + 31) / 32);
         rewrite_count_kernel<<<(unsigned)n, kRowThreads, bits, s>>>(
-            (int)n, ncols, rowptr[cur], col[cur], I(dp.partner), I(dp.rowlen), dctr);
-        scan_kernel<<<1, kScanThreads, 0, s>>>(I(dp.rowlen), rowptr[nxt], (int)n);
+            (int)n, ncols, rowptr[cur], col[cur], I(dp.partner), I(dp.rowlen));
+        scan_kernel<<<1, kScanThreads, 0, s>>>(I(dp.rowlen), rowptr[nxt], (int)n, &dctr->num_add);
         rewrite_fill_kernel<<<(unsigned)n, kRowThreads, bits, s>>>(
             (int)n, ncols, rowptr[cur], col[cur], I(dp.partner), I(dp.newid), rowptr[nxt],
             col[nxt], I(dp.scratch));
