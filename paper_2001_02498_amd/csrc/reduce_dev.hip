@@ -35,7 +35,8 @@ namespace {
 constexpr int kBlock = 256;
 constexpr int kScanThreads = 1024;
 constexpr int kGreedyThreads = 1024;
-constexpr int kGreedyPer = 8;                         // keys per thread per block
+constexpr int kGreedyPer = 4;                         // keys per thread per block
+constexpr int kGreedyBurst = 256;                     // survivors taken between refilters
 constexpr int kGreedyBlock = kGreedyThreads * kGreedyPer;
 constexpr int kMaxIds = 65536;                        // 16-bit counters, 20-bit key fields
 
@@ -276,7 +277,7 @@ __global__ __launch_bounds__(kGreedyThreads) void greedy_kernel(
     const uint64_t* __restrict__ keys, int64_t nc, int ncols, int64_t budget,
     int32_t* __restrict__ pairs, RoundCounters* rc) {
     __shared__ uint32_t used[kMaxIds / 32];
-    __shared__ uint64_t surv[kGreedyBlock];
+    __shared__ uint64_t surv[2][kGreedyBlock];
     __shared__ int32_t wave_sum[kGreedyThreads / 64];
     __shared__ int nsurv, stop;
     __shared__ long long s_taken, s_wsum;
@@ -289,13 +290,21 @@ __global__ __launch_bounds__(kGreedyThreads) void greedy_kernel(
     }
     __syncthreads();
     auto is_used = [&](uint32_t v) { return (used[v >> 5] >> (v & 31)) & 1u; };
-    // keys of the next block are loaded while this one is filtered and taken
+    // both endpoints free (no short-circuit: no branch, both reads in flight)
+    auto free_pair = [&](uint64_t key) {
+        const uint32_t x = (uint32_t)(key >> 20) & 0xFFFFu, y = (uint32_t)key & 0xFFFFu;
+        return (is_used(x) | is_used(y)) == 0u;
+    };
+    // Keys of the next block are loaded while this one is filtered and
+    // taken. Loads are unconditional (clamped index, the key replaced
+    // afterwards) so no branch makes the compiler wait for them early.
+    auto load_key = [&](int64_t i) {
+        const uint64_t v = keys[i < nc ? i : nc - 1];
+        return i < nc ? v : ~0ull;
+    };
     uint64_t k_next[kGreedyPer];
 #pragma unroll
-    for (int j = 0; j < kGreedyPer; ++j) {
-        const int64_t i = (int64_t)t * kGreedyPer + j;
-        k_next[j] = i < nc ? keys[i] : ~0ull;
-    }
+    for (int j = 0; j < kGreedyPer; ++j) k_next[j] = load_key((int64_t)t * kGreedyPer + j);
     for (int64_t base = 0; base < nc; base += kGreedyBlock) {
         uint64_t k[kGreedyPer];
         int alive = 0;
@@ -303,14 +312,13 @@ __global__ __launch_bounds__(kGreedyThreads) void greedy_kernel(
 #pragma unroll
         for (int j = 0; j < kGreedyPer; ++j) {
             k[j] = k_next[j];
-            const int64_t i2 = base + kGreedyBlock + (int64_t)t * kGreedyPer + j;
-            k_next[j] = i2 < nc ? keys[i2] : ~0ull;
+            k_next[j] = load_key(base + kGreedyBlock + (int64_t)t * kGreedyPer + j);
         }
 #pragma unroll
         for (int j = 0; j < kGreedyPer; ++j) {
-            const int64_t i = base + (int64_t)t * kGreedyPer + j;
+            // keys past nc are all ones: their ids exceed ncols
             const uint32_t x = (uint32_t)(k[j] >> 20) & 0xFFFFFu, y = (uint32_t)k[j] & 0xFFFFFu;
-            live[j] = i < nc && x < (uint32_t)ncols && y < (uint32_t)ncols && !is_used(x) && !is_used(y);
+            live[j] = (x < (uint32_t)ncols) & (y < (uint32_t)ncols) & free_pair(k[j]);
             alive += live[j];
         }
         // survivors keep their order: exclusive prefix over threads
@@ -331,46 +339,98 @@ __global__ __launch_bounds__(kGreedyThreads) void greedy_kernel(
             nsurv = run;
         }
         __syncthreads();
-        int pos = wave_sum[wave] + incl - alive;
+        int wpos = wave_sum[wave] + incl - alive;
 #pragma unroll
         for (int j = 0; j < kGreedyPer; ++j)
-            if (live[j]) surv[pos++] = k[j];
+            if (live[j]) surv[0][wpos++] = k[j];
         __syncthreads();
-        // wave 0 takes the survivors in order, 64 at a time: the first
-        // live one is taken, the others drop if they touch its endpoints
-        if (wave == 0) {
-            long long taken = s_taken, wsum = s_wsum;
-            bool halt = false;
-            for (int c0 = 0; c0 < nsurv && !halt; c0 += 64) {
-                const int si = c0 + lane;
-                const uint64_t key = si < nsurv ? surv[si] : ~0ull;
-                const uint32_t x = (uint32_t)(key >> 20) & 0xFFFFFu, y = (uint32_t)key & 0xFFFFFu;
-                bool live = si < nsurv && !is_used(x) && !is_used(y);
-                uint64_t m = __ballot(live);
-                while (m) {
-                    if (taken >= budget) {
-                        halt = true;
-                        break;
+        // Wave 0 takes the survivors in order, 64 at a time (the first live
+        // one is taken, the others drop if they touch its endpoints), a
+        // burst of kGreedyBurst at a time; between bursts all threads drop
+        // the remaining survivors that now have a used endpoint, so wave 0
+        // only walks pairs that are still possible.
+        int buf = 0, pos = 0, cnt = nsurv;
+        while (pos < cnt) {
+            const uint64_t* S = surv[buf];
+            const int end = min(cnt, pos + kGreedyBurst);
+            if (wave == 0) {
+                long long taken = s_taken, wsum = s_wsum;
+                bool halt = false;
+                for (int c0 = pos; c0 < end && !halt; c0 += 64) {
+                    const int si = c0 + lane;
+                    const uint64_t kv = S[si < end ? si : end - 1];
+                    const uint64_t key = si < end ? kv : ~0ull;
+                    const uint32_t x = (uint32_t)(key >> 20) & 0xFFFFFu, y = (uint32_t)key & 0xFFFFFu;
+                    bool live = (si < end) & free_pair(kv);
+                    uint64_t m = __ballot(live);
+                    while (m) {
+                        if (taken >= budget) {
+                            halt = true;
+                            break;
+                        }
+                        const int j = __ffsll((long long)m) - 1;
+                        const uint64_t kj = __shfl(key, j);
+                        const uint32_t xj = (uint32_t)(kj >> 20) & 0xFFFFFu, yj = (uint32_t)kj & 0xFFFFFu;
+                        if (lane == 0) {
+                            used[xj >> 5] |= 1u << (xj & 31);
+                            used[yj >> 5] |= 1u << (yj & 31);
+                            pairs[2 * taken] = (int32_t)xj;
+                            pairs[2 * taken + 1] = (int32_t)yj;
+                        }
+                        wsum += 0xFFFFu - (uint32_t)(kj >> 40);
+                        ++taken;
+                        live = live && lane > j && x != xj && x != yj && y != xj && y != yj;
+                        m = __ballot(live);
                     }
-                    const int j = __ffsll((long long)m) - 1;
-                    const uint64_t kj = __shfl(key, j);
-                    const uint32_t xj = (uint32_t)(kj >> 20) & 0xFFFFFu, yj = (uint32_t)kj & 0xFFFFFu;
-                    if (lane == 0) {
-                        used[xj >> 5] |= 1u << (xj & 31);
-                        used[yj >> 5] |= 1u << (yj & 31);
-                        pairs[2 * taken] = (int32_t)xj;
-                        pairs[2 * taken + 1] = (int32_t)yj;
-                    }
-                    wsum += 0xFFFFu - (uint32_t)(kj >> 40);
-                    ++taken;
-                    live = live && lane > j && x != xj && x != yj && y != xj && y != yj;
-                    m = __ballot(live);
+                }
+                if (lane == 0) {
+                    s_taken = taken;
+                    s_wsum = wsum;
+                    if (halt || taken >= budget) stop = 1;
                 }
             }
-            if (lane == 0) {
-                s_taken = taken;
-                s_wsum = wsum;
-                if (halt || taken >= budget) stop = 1;
+            __syncthreads();
+            if (stop) break;
+            pos = end;
+            if (cnt - pos > kGreedyBurst) {
+                // order-preserving filter of S[pos, cnt) into the other buffer
+                const int rem = cnt - pos;
+                const int per = (rem + kGreedyThreads - 1) / kGreedyThreads;
+                uint64_t kk[kGreedyPer];
+                bool lv[kGreedyPer];
+                int a = 0;
+#pragma unroll
+                for (int j = 0; j < kGreedyPer; ++j) {
+                    const int i = pos + t * per + j;
+                    lv[j] = false;
+                    kk[j] = 0;
+                    if (j < per && i < cnt) {
+                        kk[j] = S[i];
+                        lv[j] = free_pair(kk[j]);
+                    }
+                    a += lv[j];
+                }
+                int inc = a;
+                for (int off = 1; off < 64; off <<= 1) {
+                    const int v = __shfl_up(inc, off);
+                    if (lane >= off) inc += v;
+                }
+                if (lane == 63) wave_sum[wave] = inc;
+                __syncthreads();
+                int before = 0, total = 0;
+                for (int w = 0; w < kGreedyThreads / 64; ++w) {
+                    if (w < wave) before += wave_sum[w];
+                    total += wave_sum[w];
+                }
+                int o = before + inc - a;
+                uint64_t* D = surv[buf ^ 1];
+#pragma unroll
+                for (int j = 0; j < kGreedyPer; ++j)
+                    if (lv[j]) D[o++] = kk[j];
+                __syncthreads();
+                buf ^= 1;
+                pos = 0;
+                cnt = total;
             }
         }
         __syncthreads();
