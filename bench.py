@@ -55,12 +55,17 @@ def parse():
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="also run one plain device copy of this size (HBM counter "
                          "calibration under rocprofv3 --pmc)")
+    ap.add_argument("--order", choices=("paper", "narrow"), default="paper",
+                    help="paper: aggregate H then transform (Eq. 1); narrow: transform "
+                         "first where the input is wider than h")
+    ap.add_argument("--no-narrow", action="store_true",
+                    help="skip the extra timing of the narrow-side order")
     ap.add_argument("--no-direct", action="store_true",
                     help="skip the direct-aggregation comparison run (counter runs)")
     ap.add_argument("--trace-summary", metavar="KERNEL_STATS_CSV",
                     help="no GPU: turn a rocprofv3 --kernel-trace --stats kernel_stats.csv "
                          "of this script into the per-class table under profiles/")
-    ap.add_argument("--traced-args", default="--no-cpu-baseline",
+    ap.add_argument("--traced-args", default="--no-cpu-baseline --no-direct --no-narrow",
                     help="with --trace-summary: the arguments the traced run was given")
     ap.add_argument("--bench-line", help="with --trace-summary: the JSON line the traced run "
                                          "printed (event timings shown beside the trace)")
@@ -168,6 +173,7 @@ def pmc_summary(fetch_csv, write_csv, workload, cmd_args):
                         source_hash=source_hash(c))
     bargs = (f"--workload {workload} --steps {cmd_args['steps']} --warmup {cmd_args['warmup']} "
              f"--profile-steps {cmd_args['profile_steps']} --no-cpu-baseline --no-direct "
+             f"--no-narrow "
              f"--calib-copy-mib {cmd_args['calib_copy_mib']}")
     lines = [
         f"# HBM traffic per launch, {workload} training step",
@@ -267,7 +273,7 @@ def stored_traffic(workload, cls):
 class Setup:
     """Inputs of one workload on the device, ready for timed steps."""
 
-    def __init__(self, wl, reduce, inp, seg_len=0, precision=0):
+    def __init__(self, wl, reduce, inp, seg_len=0, precision=0, order=0):
         import torch
         from paper_2001_02498_amd import gcn
         self.gcn, self.wl = gcn, wl
@@ -296,7 +302,7 @@ class Setup:
         self.labels = torch.from_numpy(inp.labels).cuda()
         self.P = gcn.make_params(self.Ws, self.Wn, self.Wc)
         self.desc = gcn.model_desc(wl.L, wl.f_in, wl.h, wl.C, wl.loss, self.X.stride(0),
-                                   precision=precision)
+                                   precision=precision, order=order)
         self.ws = gcn.alloc_ws(gcn.workspace_bytes(self.dg, self.desc))
         self.loss = torch.zeros(1, device="cuda")
         torch.cuda.synchronize()
@@ -649,7 +655,8 @@ def main():
 
     from paper_2001_02498_amd import gcn
     prec = gcn.PREC_BF16 if args.precision == "bf16" else gcn.PREC_FP32
-    red = Setup(wl, wl.reduce, inp, args.seg_len, prec)
+    order = gcn.ORDER_NARROW if args.order == "narrow" else gcn.ORDER_PAPER
+    red = Setup(wl, wl.reduce, inp, args.seg_len, prec, order)
     ms = 1e3 * red.timed(args.steps, args.warmup, args.graph)
     print(f"[bench] timed {args.steps} steps: {ms:.3f} ms/step", file=sys.stderr, flush=True)
     direct = None
@@ -657,6 +664,12 @@ def main():
         d = Setup(dataclasses.replace(wl, reduce=False), False, inp, args.seg_len, prec)
         direct = 1e3 * d.timed(args.steps, args.warmup, args.graph)
         print(f"[bench] direct aggregation: {direct:.3f} ms/step", file=sys.stderr, flush=True)
+        del d
+    narrow = None
+    if order == gcn.ORDER_PAPER and not args.no_narrow:
+        d = Setup(wl, wl.reduce, inp, args.seg_len, prec, gcn.ORDER_NARROW)
+        narrow = 1e3 * d.timed(args.steps, args.warmup, args.graph)
+        print(f"[bench] narrow-side order: {narrow:.3f} ms/step", file=sys.stderr, flush=True)
         del d
     prof = red.profile(args.profile_steps)
     ktab = kernel_table(prof, args.profile_steps)
@@ -703,6 +716,7 @@ def main():
         "vs_baseline": None,
         "dtype": "f32" if args.precision == "fp32" else "bf16 (dense products; fp32 accumulate)",
         "launch": "hip-graph replay" if args.graph else "eager stream launches",
+        "order": args.order,
         "data": "synthetic",
         "config": {
             "workload": (f"{wl.name}: {wl.L}-layer GCN step on a {wl.n}-vertex Chung-Lu "
@@ -719,6 +733,7 @@ def main():
         "roofline": {k: v for k, v in roof.items() if k != "kernel"} | {"kernel": dominant},
         "cpu_baseline": cpu,
         "direct_aggregation_ms_per_step": None if direct is None else round(direct, 4),
+        "narrow_order_ms_per_step": None if narrow is None else round(narrow, 4),
         "host_preprocess_ms": {k: round(v, 2) for k, v in red.host_ms.items()},
         "aggregation_roofline": agg,
         "kernels": {k: {kk: vv for kk, vv in v.items()

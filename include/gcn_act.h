@@ -375,13 +375,24 @@ int gcn_layer_bwd(const gcn_dgraph* g, int32_t F, int32_t h, const float* G,
  *           individual NULL members, to skip)
  *   ws      >= gcn_workspace_bytes(); activations live at the offsets
  *           reported by gcn_workspace_layout (valid after the step).
+ * order GCN_ORDER_PAPER: every layer aggregates first, D^-1 A (H W_neigh)
+ *   as D^-1 A H then times W_neigh (Eq. 1), and keeps AH for Eq. 2b.
+ * order GCN_ORDER_NARROW: a layer whose input is wider than h (F > h)
+ *   transforms first and aggregates the h-wide product, D^-1 A (H W_neigh),
+ *   with the bias and ReLU applied after the aggregation; its neighbour
+ *   weight gradient becomes H^T (A D^-1 G_neigh) = (D^-1 A H)^T G_neigh,
+ *   the same product reassociated, and its AH region holds H W_neigh
+ *   instead. Equal results up to rounding, with every aggregation at width
+ *   h. Not with has_bias (GCN_E_UNSUPPORTED).
  */
+#define GCN_ORDER_PAPER 0
+#define GCN_ORDER_NARROW 1
 typedef struct {
     int32_t L, f_in, h, C;
     int32_t loss;         /* GCN_LOSS_*  */
     int32_t precision;    /* GCN_PREC_*  */
     int32_t has_bias;     /* biases on every layer and the classifier */
-    int32_t reserved;
+    int32_t order;        /* GCN_ORDER_* */
     int64_t ld_x;
 } gcn_model_desc;
 
@@ -394,7 +405,8 @@ typedef struct {          /* device pointers, row-major, ld == width */
 } gcn_params;
 
 typedef struct {          /* byte offsets into ws, -1 when absent */
-    int64_t AH[GCN_MAX_LAYERS];       /* [n x F_l], ld ld_AH[l]      */
+    int64_t AH[GCN_MAX_LAYERS];       /* [n x F_l], ld ld_AH[l] (narrow
+                                         layers: H W_neigh [n x h])  */
     int64_t H[GCN_MAX_LAYERS];        /* layer outputs [n x 2h]      */
     int64_t ld_AH[GCN_MAX_LAYERS];
     int64_t ld_H;

@@ -97,14 +97,39 @@ __device__ __forceinline__ Slice slice_of(int nsl, int slice_f4, int nf4) {
     return {b, min(nf4, b + slice_f4)};
 }
 
+// What a finished list sum becomes (AggEpi): the sum itself, its mean
+// over the original degree, or max(mean + bias, 0) (the neighbour branch
+// of Eq. 1 when the transform runs before the aggregation).
+template <int EPI>
+__device__ __forceinline__ float4 finish_row(float4 v, int row, int c4,
+                                             const float* __restrict__ inv_deg,
+                                             const float* __restrict__ bias, int F) {
+    if constexpr (EPI != AGG_SUM) {
+        const float sc = inv_deg[row];
+        v = make_float4(v.x * sc, v.y * sc, v.z * sc, v.w * sc);
+    }
+    if constexpr (EPI == AGG_MEAN_BIAS_RELU) {
+        if (bias) {
+            const int c = 4 * c4;
+            v.x += bias[c];
+            if (c + 1 < F) v.y += bias[c + 1];
+            if (c + 2 < F) v.z += bias[c + 2];
+            if (c + 3 < F) v.w += bias[c + 3];
+        }
+        v = make_float4(fmaxf(v.x, 0.f), fmaxf(v.y, 0.f), fmaxf(v.z, 0.f), fmaxf(v.w, 0.f));
+    }
+    return v;
+}
+
 // One group per segment (row, begin, end, slot) of the work list. PAIRS
 // marks the pair-sum launches (same code; a kernel name of their own so
 // per-kernel profiles and counters separate the two passes).
-template <int GL, int NCH, bool PRE, bool POST, bool PAIRS>
+template <int GL, int NCH, bool PRE, int EPI, bool PAIRS>
 __global__ __launch_bounds__(kBlock) void list_sums_kernel(
     const int4* __restrict__ seg, int nseg, const int32_t* __restrict__ col,
-    RowSource src, const float* __restrict__ inv_deg, float* __restrict__ Y,
-    int64_t ldy, float* __restrict__ partial, int64_t ldp, int F, int nsl, int slice_f4) {
+    RowSource src, const float* __restrict__ inv_deg, const float* __restrict__ bias,
+    float* __restrict__ Y, int64_t ldy, float* __restrict__ partial, int64_t ldp, int F, int nsl,
+    int slice_f4) {
     const int lane = (int)threadIdx.x % GL;
     const int sidx = group_index<GL>(nsl);
     if (sidx >= nseg) return;
@@ -164,16 +189,11 @@ __global__ __launch_bounds__(kBlock) void list_sums_kernel(
             }
         }
         if (slot < 0) {
-            const float sc = POST ? inv_deg[row] : 1.0f;
             float* out = Y + (int64_t)row * ldy;
 #pragma unroll
             for (int j = 0; j < NCH; ++j) {
                 const int c4 = base + lane + j * GL;
-                if (c4 < nf4) {
-                    float4 v = acc[j];
-                    if (POST) v = make_float4(v.x * sc, v.y * sc, v.z * sc, v.w * sc);
-                    st4_masked(out + 4 * c4, v, F - 4 * c4);
-                }
+                if (c4 < nf4) st4_masked(out + 4 * c4, finish_row<EPI>(acc[j], row, c4, inv_deg, bias, F), F - 4 * c4);
             }
         } else {
             float* out = partial + (int64_t)slot * ldp;
@@ -186,13 +206,13 @@ __global__ __launch_bounds__(kBlock) void list_sums_kernel(
     }
 }
 
-// One group per split list: add its slots in order, scale, store.
-template <int GL, int NCH, bool POST>
+// One group per split list: add its slots in order, finish, store.
+template <int GL, int NCH, int EPI>
 __global__ __launch_bounds__(kBlock) void fixup_kernel(
     const int4* __restrict__ longrows, int nlong,
     const float* __restrict__ partial, int64_t ldp,
-    const float* __restrict__ inv_deg, float* __restrict__ Y, int64_t ldy,
-    int F, int nsl, int slice_f4) {
+    const float* __restrict__ inv_deg, const float* __restrict__ bias, float* __restrict__ Y,
+    int64_t ldy, int F, int nsl, int slice_f4) {
     const int lane = (int)threadIdx.x % GL;
     const int li = group_index<GL>(nsl);
     if (li >= nlong) return;
@@ -200,7 +220,6 @@ __global__ __launch_bounds__(kBlock) void fixup_kernel(
     const int row = lr.x, first = lr.y, ns = lr.z;
     const Slice sl = slice_of(nsl, slice_f4, (F + 3) >> 2);
     const int nf4 = sl.c4_end;
-    const float sc = POST ? inv_deg[row] : 1.0f;
     float* out = Y + (int64_t)row * ldy;
     for (int base = sl.c4_begin; base < nf4; base += GL * NCH) {
 #pragma unroll
@@ -219,8 +238,7 @@ __global__ __launch_bounds__(kBlock) void fixup_kernel(
                     for (int u = 0; u < 8; ++u) add4(acc, v[u]);
                 }
                 for (; sI < ns; ++sI) add4(acc, ld4(src + (int64_t)sI * ldp));
-                if (POST) acc = make_float4(acc.x * sc, acc.y * sc, acc.z * sc, acc.w * sc);
-                st4_masked(out + 4 * c4, acc, F - 4 * c4);
+                st4_masked(out + 4 * c4, finish_row<EPI>(acc, row, c4, inv_deg, bias, F), F - 4 * c4);
             }
         }
     }
@@ -270,29 +288,28 @@ hipError_t launch_pair_sums(const gcn_dgraph* g, RowSource src, bool prescale,
     const double e = (double)g->exp_nnz, k = (double)g->naux;
     // one gather per expansion entry, its id, one write per pair sum
     ProfScope prof(s, K_PAIR_SUMS, e * F * (prescale ? 2.0 : 1.0), 4.0 * F * e + 4.0 * e + 4.0 * F * k);
-#define GCN_LAUNCH_PAIR(GL_, NCH_)                                                    \
-    if (sh.gl == GL_ && sh.nch == NCH_) {                                             \
-        if (prescale)                                                                 \
-            list_sums_kernel<GL_, NCH_, true, false, true><<<grid, block, 0, s>>>(          \
-                seg, g->naux, g->exp_col, src, g->inv_deg, aux, ldaux, nullptr, 0, F, \
-                sh.nsl, sh.slice_f4);                                                 \
-        else                                                                          \
-            list_sums_kernel<GL_, NCH_, false, false, true><<<grid, block, 0, s>>>(         \
-                seg, g->naux, g->exp_col, src, g->inv_deg, aux, ldaux, nullptr, 0, F, \
-                sh.nsl, sh.slice_f4);                                                 \
-        return hipGetLastError();                                                     \
+#define GCN_LAUNCH_PAIR(GL_, NCH_)                                                          \
+    if (sh.gl == GL_ && sh.nch == NCH_) {                                                   \
+        if (prescale)                                                                       \
+            list_sums_kernel<GL_, NCH_, true, AGG_SUM, true><<<grid, block, 0, s>>>(        \
+                seg, g->naux, g->exp_col, src, g->inv_deg, nullptr, aux, ldaux, nullptr, 0, \
+                F, sh.nsl, sh.slice_f4);                                                    \
+        else                                                                                \
+            list_sums_kernel<GL_, NCH_, false, AGG_SUM, true><<<grid, block, 0, s>>>(       \
+                seg, g->naux, g->exp_col, src, g->inv_deg, nullptr, aux, ldaux, nullptr, 0, \
+                F, sh.nsl, sh.slice_f4);                                                    \
+        return hipGetLastError();                                                           \
     }
     GCN_SHAPES(GCN_LAUNCH_PAIR)
 #undef GCN_LAUNCH_PAIR
     return hipErrorInvalidValue;
 }
 
-hipError_t launch_list_sums(const gcn_dgraph* g, RowSource src, bool prescale,
-                            bool postscale, float* Y, int64_t ldy,
-                            float* partial, int64_t ldp, int32_t F,
-                            hipStream_t s) {
+hipError_t launch_list_sums(const gcn_dgraph* g, RowSource src, bool prescale, AggEpi epi,
+                            const float* bias, float* Y, int64_t ldy, float* partial,
+                            int64_t ldp, int32_t F, hipStream_t s) {
     if (g->n <= 0 || F <= 0) return hipSuccess;
-    if (prescale == postscale) return hipErrorInvalidValue;
+    if (prescale && epi != AGG_SUM) return hipErrorInvalidValue;
     const Shape sh = pick_shape(F);
     const int4* seg = reinterpret_cast<const int4*>(g->seg);
     const int4* lr = reinterpret_cast<const int4*>(g->longrows);
@@ -302,18 +319,23 @@ hipError_t launch_list_sums(const gcn_dgraph* g, RowSource src, bool prescale,
     const double nnz = (double)g->nnz, n = (double)g->n;
     {
         // algorithmic: one gather per list entry, its id, one write per row
-        ProfScope prof(s, K_LIST_SUMS, nnz * F * (prescale ? 2.0 : 1.0) + (postscale ? n * F : 0.0),
+        ProfScope prof(s, K_LIST_SUMS,
+                       nnz * F * (prescale ? 2.0 : 1.0) + (epi != AGG_SUM ? n * F : 0.0),
                        4.0 * F * nnz + 4.0 * nnz + 4.0 * F * n);
-#define GCN_LAUNCH_LIST(GL_, NCH_)                                                    \
-        if (sh.gl == GL_ && sh.nch == NCH_) {                                         \
-            if (prescale)                                                             \
-                list_sums_kernel<GL_, NCH_, true, false, false><<<grid, block, 0, s>>>(      \
-                    seg, g->nseg, g->col, src, g->inv_deg, Y, ldy, partial, ldp, F,   \
-                    sh.nsl, sh.slice_f4);                                             \
-            else                                                                      \
-                list_sums_kernel<GL_, NCH_, false, true, false><<<grid, block, 0, s>>>(      \
-                    seg, g->nseg, g->col, src, g->inv_deg, Y, ldy, partial, ldp, F,   \
-                    sh.nsl, sh.slice_f4);                                             \
+#define GCN_LAUNCH_LIST(GL_, NCH_)                                                           \
+        if (sh.gl == GL_ && sh.nch == NCH_) {                                                \
+            if (prescale)                                                                    \
+                list_sums_kernel<GL_, NCH_, true, AGG_SUM, false><<<grid, block, 0, s>>>(    \
+                    seg, g->nseg, g->col, src, g->inv_deg, nullptr, Y, ldy, partial, ldp, F, \
+                    sh.nsl, sh.slice_f4);                                                    \
+            else if (epi == AGG_MEAN)                                                        \
+                list_sums_kernel<GL_, NCH_, false, AGG_MEAN, false><<<grid, block, 0, s>>>(  \
+                    seg, g->nseg, g->col, src, g->inv_deg, nullptr, Y, ldy, partial, ldp, F, \
+                    sh.nsl, sh.slice_f4);                                                    \
+            else                                                                             \
+                list_sums_kernel<GL_, NCH_, false, AGG_MEAN_BIAS_RELU, false>                \
+                    <<<grid, block, 0, s>>>(seg, g->nseg, g->col, src, g->inv_deg, bias, Y,  \
+                                            ldy, partial, ldp, F, sh.nsl, sh.slice_f4);      \
         } else
         GCN_SHAPES(GCN_LAUNCH_LIST) { return hipErrorInvalidValue; }
 #undef GCN_LAUNCH_LIST
@@ -323,14 +345,17 @@ hipError_t launch_list_sums(const gcn_dgraph* g, RowSource src, bool prescale,
     if (g->nlong == 0) return hipSuccess;
     ProfScope prof(s, K_LIST_FIXUP, (double)g->nslots * F,
                    4.0 * F * ((double)g->nslots + g->nlong));
-#define GCN_LAUNCH_FIX(GL_, NCH_)                                                     \
-    if (sh.gl == GL_ && sh.nch == NCH_) {                                             \
-        if (postscale)                                                                \
-            fixup_kernel<GL_, NCH_, true><<<gfix, block, 0, s>>>(                     \
-                lr, g->nlong, partial, ldp, g->inv_deg, Y, ldy, F, sh.nsl, sh.slice_f4); \
-        else                                                                          \
-            fixup_kernel<GL_, NCH_, false><<<gfix, block, 0, s>>>(                    \
-                lr, g->nlong, partial, ldp, g->inv_deg, Y, ldy, F, sh.nsl, sh.slice_f4); \
+#define GCN_LAUNCH_FIX(GL_, NCH_)                                                             \
+    if (sh.gl == GL_ && sh.nch == NCH_) {                                                     \
+        if (epi == AGG_SUM)                                                                   \
+            fixup_kernel<GL_, NCH_, AGG_SUM><<<gfix, block, 0, s>>>(                          \
+                lr, g->nlong, partial, ldp, g->inv_deg, nullptr, Y, ldy, F, sh.nsl, sh.slice_f4); \
+        else if (epi == AGG_MEAN)                                                             \
+            fixup_kernel<GL_, NCH_, AGG_MEAN><<<gfix, block, 0, s>>>(                         \
+                lr, g->nlong, partial, ldp, g->inv_deg, nullptr, Y, ldy, F, sh.nsl, sh.slice_f4); \
+        else                                                                                  \
+            fixup_kernel<GL_, NCH_, AGG_MEAN_BIAS_RELU><<<gfix, block, 0, s>>>(               \
+                lr, g->nlong, partial, ldp, g->inv_deg, bias, Y, ldy, F, sh.nsl, sh.slice_f4);    \
     } else
     GCN_SHAPES(GCN_LAUNCH_FIX) { return hipErrorInvalidValue; }
 #undef GCN_LAUNCH_FIX

@@ -122,15 +122,19 @@ float* fptr(void* ws, int64_t off) {
 // ------------------------------------------------------------ internals
 // (arguments already validated)
 
+// transposed: Y = A D^-1 X (Eq. 2c); else Y = epi(D^-1 A X) (Eq. 1), with
+// epi AGG_MEAN or AGG_MEAN_BIAS_RELU
 int do_aggregate(const char* fn, const gcn_dgraph* g, bool transposed, int32_t F,
                  const float* X, int64_t ldx, float* Y, int64_t ldy,
-                 const ScratchPlan& sp, void* ws, hipStream_t s) {
+                 const ScratchPlan& sp, void* ws, hipStream_t s,
+                 AggEpi epi = AGG_MEAN, const float* bias = nullptr) {
+    if (transposed) epi = AGG_SUM;
     const int64_t ldaux = r4(F);
     float* aux = fptr(ws, sp.aux);
     float* part = fptr(ws, sp.part_list);
     RowSource src{X, ldx, aux, ldaux, g->n};
     GCN_HIP(launch_pair_sums(g, src, transposed, aux, ldaux, F, s), fn);
-    GCN_HIP(launch_list_sums(g, src, transposed, !transposed, Y, ldy, part, ldaux, F, s), fn);
+    GCN_HIP(launch_list_sums(g, src, transposed, epi, bias, Y, ldy, part, ldaux, F, s), fn);
     return GCN_OK;
 }
 
@@ -351,6 +355,91 @@ int do_layer_bwd(const char* fn, const gcn_dgraph* g, int32_t F, int32_t h,
     return GCN_OK;
 }
 
+// Narrow-side order (GCN_ORDER_NARROW) for a layer with F > h: the
+// grouped GEMM writes ReLU(H W_self) and Z = H W_neigh, then the h-wide
+// aggregation finishes the neighbour half as ReLU(D^-1 A^# Z).
+int do_layer_fwd_narrow(const char* fn, const gcn_dgraph* g, int32_t F, int32_t h,
+                        const float* H_in, int64_t ld_in, const float* Ws, const float* Wn,
+                        float* Z, int64_t ldz, float* H_out, int64_t ld_out, bool bf16,
+                        const ScratchPlan& sp, void* ws, hipStream_t s) {
+    GemmBatch b;
+    std::memset(&b, 0, sizeof(b));
+    b.nprob = 2;
+    for (int i = 0; i < 2; ++i) {
+        GemmProblem p = gp_zero();
+        p.M = g->n;
+        p.N = h;
+        p.K = F;
+        p.A0 = p.A1 = H_in;
+        p.lda0 = p.lda1 = ld_in;
+        p.ksplitA = F;
+        p.B0 = p.B1 = i == 0 ? Ws : Wn;
+        p.ldb0 = p.ldb1 = h;
+        p.ksplitB = F;
+        p.C = i == 0 ? H_out : Z;
+        p.ldc = i == 0 ? ld_out : ldz;
+        p.no_relu = i == 1;
+        b.p[i] = p;
+    }
+    GCN_HIP(launch_gemm(b, A_MK, B_KN, EPI_BIAS_RELU, ROLE_FWD, bf16, s), fn);
+    return do_aggregate(fn, g, false, h, Z, ldz, H_out + h, ld_out, sp, ws, s,
+                        AGG_MEAN_BIAS_RELU, nullptr);
+}
+
+// Backward of a narrow layer: T = A D^-1 G_neigh (also for the first
+// layer), G_in as in the paper order, and dW_neigh = H_in^T T.
+int do_layer_bwd_narrow(const char* fn, const gcn_dgraph* g, int32_t F, int32_t h,
+                        const float* G, int64_t ldg, const float* H_in, int64_t ld_in,
+                        float* Ws, float* Wn, float lr, float* G_in, int64_t ldgi,
+                        float* dWs_out, float* dWn_out, bool bf16, const ScratchPlan& sp,
+                        void* ws, hipStream_t s) {
+    const int32_t n = g->n;
+    float* T = fptr(ws, sp.T);
+    const int64_t ldt = ldg <= sp.ld_max ? ldg : r4(h);
+    GCN_TRY(do_aggregate(fn, g, true, h, G + h, ldg, T, ldt, sp, ws, s));
+    if (G_in) {
+        GemmBatch b;
+        std::memset(&b, 0, sizeof(b));
+        b.nprob = 1;
+        GemmProblem p = gp_zero();
+        p.M = n;
+        p.N = F;
+        p.K = 2 * h;
+        p.A0 = G;
+        p.lda0 = ldg;
+        p.A1 = T;
+        p.lda1 = ldt;
+        p.ksplitA = h;
+        p.B0 = Ws;
+        p.ldb0 = h;
+        p.B1 = Wn;
+        p.ldb1 = h;
+        p.ksplitB = h;
+        p.mask = H_in;
+        p.ldmask = ld_in;
+        p.C = G_in;
+        p.ldc = ldgi;
+        b.p[0] = p;
+        GCN_HIP(launch_gemm(b, A_MK, B_NK, EPI_MASK, ROLE_DX, bf16, s), fn);
+    }
+    GemmBatch b;
+    std::memset(&b, 0, sizeof(b));
+    b.nprob = 2;
+    float* part0 = fptr(ws, sp.gemm_part);
+    float* part1 = part0 + sp.gemm_part_floats;
+    b.p[0] = dw_problem(n, F, false, h, H_in, ld_in, G, ldg, part0, 2);
+    b.p[1] = dw_problem(n, F, false, h, H_in, ld_in, T, ldt, part1, 2);
+    GCN_HIP(launch_gemm(b, A_KM, B_KN, EPI_PARTIAL, ROLE_DW, bf16, s), fn);
+    SgdProblem q[2] = {sgd_problem(b.p[0], F, h, Ws, nullptr, dWs_out, nullptr),
+                       sgd_problem(b.p[1], F, h, Wn, nullptr, dWn_out, nullptr)};
+    GCN_HIP(launch_sgd_reduce(q, 2, lr, s), fn);
+    return GCN_OK;
+}
+
+bool narrow_layer(const gcn_model_desc* d, int32_t F) {
+    return d->order == GCN_ORDER_NARROW && F > d->h;
+}
+
 struct StepLayout {
     gcn_ws_layout pub;
     ScratchPlan sp;
@@ -405,6 +494,12 @@ int check_desc(const char* fn, const gcn_model_desc* d) {
                   "%s: unknown loss %d", fn, d->loss);
     GCN_CHECK_ARG(d->ld_x >= d->f_in && d->ld_x % 4 == 0,
                   "%s: ld_x=%lld must be >= f_in and a multiple of 4", fn, (long long)d->ld_x);
+    GCN_CHECK_ARG(d->order == GCN_ORDER_PAPER || d->order == GCN_ORDER_NARROW,
+                  "%s: unknown order %d", fn, d->order);
+    if (d->order == GCN_ORDER_NARROW && d->has_bias) {
+        set_error("%s: the narrow-side order is built without biases", fn);
+        return GCN_E_UNSUPPORTED;
+    }
     return check_precision(fn, d->precision);
 }
 
@@ -642,9 +737,14 @@ int gcn_train_step(const gcn_dgraph* g, const gcn_model_desc* d, const gcn_param
     int64_t ldprev = d->ld_x;
     for (int l = 0; l < L; ++l) {
         const int32_t F = l == 0 ? d->f_in : 2 * h;
-        GCN_TRY(do_layer_fwd(fn, g, F, h, Hprev, ldprev, P->W_self[l], P->W_neigh[l],
-                             d->has_bias ? P->b[l] : nullptr, act(sl.pub.AH[l]),
-                             sl.pub.ld_AH[l], act(sl.pub.H[l]), ldH, bf16, sp, scratch, s));
+        if (narrow_layer(d, F))
+            GCN_TRY(do_layer_fwd_narrow(fn, g, F, h, Hprev, ldprev, P->W_self[l], P->W_neigh[l],
+                                        act(sl.pub.AH[l]), sl.pub.ld_AH[l], act(sl.pub.H[l]),
+                                        ldH, bf16, sp, scratch, s));
+        else
+            GCN_TRY(do_layer_fwd(fn, g, F, h, Hprev, ldprev, P->W_self[l], P->W_neigh[l],
+                                 d->has_bias ? P->b[l] : nullptr, act(sl.pub.AH[l]),
+                                 sl.pub.ld_AH[l], act(sl.pub.H[l]), ldH, bf16, sp, scratch, s));
         Hprev = act(sl.pub.H[l]);
         ldprev = ldH;
     }
@@ -671,6 +771,15 @@ int gcn_train_step(const gcn_dgraph* g, const gcn_model_desc* d, const gcn_param
         const float* Hin = l == 0 ? X : act(sl.pub.H[l - 1]);
         const int64_t ldin = l == 0 ? d->ld_x : ldH;
         float* Gnext = l > 0 ? act(sl.pub.G[l - 1]) : nullptr;
+        if (narrow_layer(d, F)) {
+            GCN_TRY(do_layer_bwd_narrow(fn, g, F, h, Gcur, ldH, Hin, ldin, P->W_self[l],
+                                        P->W_neigh[l], lr, Gnext, ldH,
+                                        grads ? grads->W_self[l] : nullptr,
+                                        grads ? grads->W_neigh[l] : nullptr, bf16, sp, scratch,
+                                        s));
+            Gcur = Gnext;
+            continue;
+        }
         GCN_TRY(do_layer_bwd(fn, g, F, h, Gcur, ldH, Hin, ldin, act(sl.pub.AH[l]),
                              sl.pub.ld_AH[l], P->W_self[l], P->W_neigh[l],
                              d->has_bias ? P->b[l] : nullptr, lr, Gnext, ldH,

@@ -150,7 +150,7 @@ __device__ __forceinline__ void store_tile(const GemmProblem& P, int split, int 
                 float v = acc[bi][bj][r];
                 if constexpr (EP == EPI_BIAS_RELU) {
                     v += bv;
-                    v = v > 0.f ? v : 0.f;
+                    if (!P.no_relu) v = v > 0.f ? v : 0.f;
                 } else if constexpr (EP == EPI_BIAS) {
                     v += bv;
                 } else if constexpr (EP == EPI_MASK) {

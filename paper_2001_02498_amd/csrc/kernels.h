@@ -25,20 +25,26 @@ struct RowSource {
 hipError_t launch_pair_sums(const gcn_dgraph* g, RowSource src, bool prescale,
                             float* aux, int64_t ldaux, int32_t F, hipStream_t s);
 
+// What a finished list sum becomes.
+enum AggEpi : int {
+    AGG_SUM = 0,             // Y_w = sum
+    AGG_MEAN = 1,            // Y_w = (1/d_w) sum
+    AGG_MEAN_BIAS_RELU = 2,  // Y_w = max((1/d_w) sum + bias, 0)  (bias may be NULL)
+};
+
 // Segment sums of G_s^# lists (see the work list of gcn_graph_pack), then the
-// fix-up of split lists. postscale: Y_w = (1/d_w) * sum; prescale: gathered
-// original rows are multiplied by their 1/d.
-hipError_t launch_list_sums(const gcn_dgraph* g, RowSource src, bool prescale,
-                            bool postscale, float* Y, int64_t ldy,
-                            float* partial, int64_t ldp, int32_t F,
-                            hipStream_t s);
+// fix-up of split lists, finished as `epi` says; prescale (with AGG_SUM
+// only): gathered original rows are multiplied by their 1/d.
+hipError_t launch_list_sums(const gcn_dgraph* g, RowSource src, bool prescale, AggEpi epi,
+                            const float* bias, float* Y, int64_t ldy, float* partial,
+                            int64_t ldp, int32_t F, hipStream_t s);
 
 // ---------------------------------------------------------------- GEMM
 enum ALayout : int { A_MK = 0, A_KM = 1 };   // A(m,k) = A[m*lda+k] | A[k*lda+m]
 enum BLayout : int { B_KN = 0, B_NK = 1 };   // B(k,n) = B[k*ldb+n] | B[n*ldb+k]
 enum Epilogue : int {
     EPI_STORE = 0,      // C = acc
-    EPI_BIAS_RELU = 1,  // C = max(acc + bias[n], 0)   (bias may be NULL)
+    EPI_BIAS_RELU = 1,  // C = max(acc + bias[n], 0)   (bias may be NULL; no_relu: no max)
     EPI_BIAS = 2,       // C = acc + bias[n]            (bias may be NULL)
     EPI_MASK = 3,       // C = acc * [mask[m,n] > 0]
     EPI_PARTIAL = 4,    // C + split*part_stride = acc over the split's K range
@@ -67,6 +73,7 @@ struct GemmProblem {
     int32_t kchunk;       // K per split (EPI_PARTIAL: from gemm_split_plan)
     int32_t tiles_m, tiles_n, tile_begin;
     int32_t a_vec, b_vec; // operand rows 16-byte aligned: float4 loads
+    int32_t no_relu;      // EPI_BIAS_RELU: this problem stores acc + bias only
 };
 
 constexpr int kMaxProblems = 2;

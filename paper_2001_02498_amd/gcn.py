@@ -36,6 +36,8 @@ PREC_FP32 = 0
 PREC_BF16 = 1
 PIPE_PINNED = 1
 PIPE_DEVICE_REDUCE = 2
+ORDER_PAPER = 0
+ORDER_NARROW = 1
 AGG_MEAN = 0
 AGG_TRANSPOSED = 1
 ABI_VERSION = 2
@@ -75,7 +77,7 @@ class DGraph(C.Structure):
 class ModelDesc(C.Structure):
     _fields_ = [("L", _i32), ("f_in", _i32), ("h", _i32), ("C", _i32),
                 ("loss", _i32), ("precision", _i32), ("has_bias", _i32),
-                ("reserved", _i32), ("ld_x", _i64)]
+                ("order", _i32), ("ld_x", _i64)]
 
 
 class Params(C.Structure):
@@ -418,8 +420,9 @@ def layer_bwd(dg, G, H_in, AH, W_self, W_neigh, bias, lr, G_in, dW_self, dW_neig
                       _ptr(db), precision, _ptr(ws), ws.numel(), _stream(stream)))
 
 
-def model_desc(L, f_in, h, C_, loss_kind, ld_x, precision=PREC_FP32, has_bias=False):
-    return ModelDesc(L, f_in, h, C_, loss_kind, precision, 1 if has_bias else 0, 0, ld_x)
+def model_desc(L, f_in, h, C_, loss_kind, ld_x, precision=PREC_FP32, has_bias=False,
+               order=ORDER_PAPER):
+    return ModelDesc(L, f_in, h, C_, loss_kind, precision, 1 if has_bias else 0, order, ld_x)
 
 
 def make_params(W_self, W_neigh, W_cls, b=None, b_cls=None):

@@ -21,10 +21,11 @@ pytestmark = pytest.mark.gpu
 class StepRun:
     """Runs one gcn_train_step on a workload and keeps every tensor."""
 
-    def __init__(self, wl, inp=None, bias=False, seg_len=0, precision=0):
+    def __init__(self, wl, inp=None, bias=False, seg_len=0, precision=0, order=0):
         from paper_2001_02498_amd import gcn
         self.gcn, self.wl = gcn, wl
         self.precision = precision
+        self.order = order
         self.inp = inp or synth.make_inputs(wl)
         rounds = wl.rounds if wl.reduce else 0
         self.case = GraphCase(wl.n, self.inp.src, self.inp.dst, theta=wl.theta,
@@ -59,7 +60,8 @@ class StepRun:
         self.grads_dev = (gWs, gWn, gWc, gb, gbc)
         Gp = gcn.make_params(gWs, gWn, gWc, gb, gbc)
         desc = gcn.model_desc(wl.L, wl.f_in, wl.h, wl.C, wl.loss, X.stride(0),
-                              has_bias=self.bias, precision=self.precision)
+                              has_bias=self.bias, precision=self.precision,
+                              order=self.order)
         self.layout = gcn.workspace_layout(self.case.dg, desc)
         ws = gcn.alloc_ws(gcn.workspace_bytes(self.case.dg, desc))
         self.ws = ws
@@ -67,11 +69,16 @@ class StepRun:
         loss = torch.zeros(1, device="cuda")
         say("train_step", wl.name, "n", wl.n, "L", wl.L, "f_in", wl.f_in, "h", wl.h,
             "C", wl.C, "naux", self.case.info["naux"], "bias", self.bias,
-            "precision", self.precision)
+            "precision", self.precision, "order", self.order)
         gcn.train_step(self.case.dg, desc, P, X, labels, wl.lr, loss, ws, grads=Gp)
         torch.cuda.synchronize()
         self.loss = loss.item()
         return self
+
+    def narrow(self, l):
+        """Layer l transforms before it aggregates (narrow-side order)."""
+        F = self.wl.f_in if l == 0 else 2 * self.wl.h
+        return self.order == 1 and F > self.wl.h
 
     def act(self, off, rows, cols, ld):
         t = self.ws[off:off + 4 * rows * ld].view(torch.float32).view(rows, ld)
@@ -105,7 +112,12 @@ def check_step(run, tol=FP32_TOL):
     errs = {}
     for l in range(wl.L):
         F = wl.f_in if l == 0 else 2 * wl.h
-        errs[f"AH{l}"] = rel(run.act(lay.AH[l], wl.n, F, lay.ld_AH[l]), ref["fw"]["AH"][l])
+        if run.narrow(l):
+            # the region holds H W_neigh, the product the layer aggregates
+            Z = ref["fw"]["H"][l] @ run.inp.W_neigh[l].astype(np.float64)
+            errs[f"Z{l}"] = rel(run.act(lay.AH[l], wl.n, wl.h, lay.ld_AH[l]), Z)
+        else:
+            errs[f"AH{l}"] = rel(run.act(lay.AH[l], wl.n, F, lay.ld_AH[l]), ref["fw"]["AH"][l])
         errs[f"H{l}"] = rel(run.act(lay.H[l], wl.n, 2 * wl.h, lay.ld_H), ref["fw"]["H"][l + 1])
     errs["logits"] = rel(run.act(lay.logits, wl.n, wl.C, lay.ld_C), ref["fw"]["logits"])
     errs["dlogits"] = rel(run.act(lay.dlogits, wl.n, wl.C, lay.ld_C), ref["dlogits"])
@@ -180,3 +192,37 @@ def test_step_deterministic():
     for x, y in zip(a.grads_dev[0] + a.grads_dev[1] + [a.grads_dev[2]],
                     b.grads_dev[0] + b.grads_dev[1] + [b.grads_dev[2]]):
         assert torch.equal(x, y)
+
+
+@pytest.mark.parametrize("name", ["tiny", "ppi8k", "reddit8k", "yelp10k"])
+def test_step_narrow_order(name):
+    """Aggregating H W_neigh instead of H (the product reassociated) gives
+    the paper-order step's results within tolerance."""
+    need_gpu()
+    check_step(StepRun(synth.WORKLOADS[name], order=1).run())
+
+
+@pytest.mark.parametrize("L,f_in,h", [(1, 37, 28), (2, 20, 28), (3, 61, 16)])
+def test_step_narrow_ragged(L, f_in, h):
+    need_gpu()
+    wl = synth.small_workload(437, 9, L, f_in, h, 7, synth.SOFTMAX_CE, (L, f_in, h, 5))
+    check_step(StepRun(wl, seg_len=4, order=1).run())
+
+
+def test_step_narrow_bf16():
+    need_gpu()
+    from tests.gpu_helpers import BF16_TOL
+    run = StepRun(synth.WORKLOADS["ppi8k"], order=1, precision=1).run()
+    check_step(run, tol=BF16_TOL)
+
+
+def test_step_narrow_rejects_bias():
+    need_gpu()
+    from paper_2001_02498_amd import gcn
+    wl = synth.WORKLOADS["tiny"]
+    run = StepRun(wl, bias=True, order=1)
+    desc = gcn.model_desc(wl.L, wl.f_in, wl.h, wl.C, wl.loss, wl.f_in, has_bias=True,
+                          order=1)
+    with pytest.raises(gcn.GcnError) as e:
+        gcn.workspace_bytes(run.case.dg, desc)
+    assert e.value.code == gcn.E_UNSUPPORTED
