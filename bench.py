@@ -235,9 +235,10 @@ def trace_summary(stats_csv, workload, cmd_args, bench_line=None):
            f"python3 $R/bench.py {bargs}",
            f"python3 bench.py --workload {workload} --traced-args='{cmd_args}' "
            "--trace-summary OUT/run_kernel_stats.csv --bench-line OUT/line.json", "```",
-           "", "The run covers the reduced-graph setup and the direct-aggregation comparison "
-           "(warm-up, timed and profiled steps of both); GEMM classes have the same shapes "
-           "in both.", "",
+           "", ("The run covers the warm-up, timed and profiled steps of the reduced-graph "
+                "step alone." if "--no-direct" in cmd_args and "--no-narrow" in cmd_args else
+                "The run also covers the comparison runs bench.py times beside the step "
+                "(their kernels are counted in the same classes)."), "",
            "## Per timing class (the classes bench.py times with HIP events)", "",
            "| class | calls | mean us | total ms |", "|---|---:|---:|---:|"]
     for c, (n, tot) in sorted(by_cls.items(), key=lambda kv: -kv[1][1]):
