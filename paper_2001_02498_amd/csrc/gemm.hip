@@ -126,37 +126,67 @@ __device__ __forceinline__ TileInfo decode_tile(const GemmBatch& batch) {
 }
 
 // Epilogue of a wavefront's 64 x 64 block (2 x 2 accumulators of 32 x 32).
-// Accumulator element r of lane l is C[i][j] of its 32 x 32 block with
-// j = l % 32, i = (r % 4) + 8 (r / 4) + 4 (l / 32).
+// The MFMAs take the B fragment as their first operand, so they produce the
+// transposed block: accumulator element r of lane l is C[i][j] of its
+// 32 x 32 block with i = l % 32 and j = (r % 4) + 8 (r / 4) + 4 (l / 32).
+// Every lane thus holds four runs of four consecutive columns of one row,
+// stored (and masked) with 16-byte accesses where the row is aligned.
 template <Epilogue EP>
 __device__ __forceinline__ void store_tile(const GemmProblem& P, int split, int mw, int nw,
                                            int half, int l32, const floatx16 (&acc)[2][2]) {
     float* C = P.C;
     if constexpr (EP == EPI_PARTIAL) C += (int64_t)split * P.part_stride;
+    const bool cvec = ((reinterpret_cast<uintptr_t>(C) | (uintptr_t)(P.ldc * 4)) & 15) == 0;
+    bool mvec = false;
+    if constexpr (EP == EPI_MASK)
+        mvec = ((reinterpret_cast<uintptr_t>(P.mask) | (uintptr_t)(P.ldmask * 4)) & 15) == 0;
 #pragma unroll
     for (int bi = 0; bi < 2; ++bi) {
+        const int m = mw + bi * 32 + l32;
+        if (m >= P.M) continue;
+        float* crow = C + (int64_t)m * P.ldc;
 #pragma unroll
         for (int bj = 0; bj < 2; ++bj) {
-            const int n = nw + bj * 32 + l32;
-            if (n >= P.N) continue;
-            float bv = 0.f;
-            if constexpr (EP == EPI_BIAS_RELU || EP == EPI_BIAS) {
-                if (P.bias) bv = P.bias[n];
-            }
 #pragma unroll
-            for (int r = 0; r < 16; ++r) {
-                const int m = mw + bi * 32 + (r & 3) + 8 * (r >> 2) + 4 * half;
-                if (m >= P.M) continue;
-                float v = acc[bi][bj][r];
-                if constexpr (EP == EPI_BIAS_RELU) {
-                    v += bv;
-                    if (!P.no_relu) v = v > 0.f ? v : 0.f;
-                } else if constexpr (EP == EPI_BIAS) {
-                    v += bv;
+            for (int g = 0; g < 4; ++g) {
+                const int n = nw + bj * 32 + 8 * g + 4 * half;
+                if (n >= P.N) continue;
+                const bool whole = n + 4 <= P.N;
+                float v[4];
+#pragma unroll
+                for (int t = 0; t < 4; ++t) v[t] = acc[bi][bj][4 * g + t];
+                if constexpr (EP == EPI_BIAS_RELU || EP == EPI_BIAS) {
+                    if (P.bias) {
+#pragma unroll
+                        for (int t = 0; t < 4; ++t)
+                            if (n + t < P.N) v[t] += P.bias[n + t];
+                    }
+                    if constexpr (EP == EPI_BIAS_RELU) {
+                        if (!P.no_relu) {
+#pragma unroll
+                            for (int t = 0; t < 4; ++t) v[t] = v[t] > 0.f ? v[t] : 0.f;
+                        }
+                    }
                 } else if constexpr (EP == EPI_MASK) {
-                    v = P.mask[(int64_t)m * P.ldmask + n] > 0.f ? v : 0.f;
+                    const float* mp = P.mask + (int64_t)m * P.ldmask + n;
+                    float h[4];
+                    if (whole && mvec) {
+                        const float4 q = ld4(mp);
+                        h[0] = q.x, h[1] = q.y, h[2] = q.z, h[3] = q.w;
+                    } else {
+#pragma unroll
+                        for (int t = 0; t < 4; ++t) h[t] = n + t < P.N ? mp[t] : 0.f;
+                    }
+#pragma unroll
+                    for (int t = 0; t < 4; ++t) v[t] = h[t] > 0.f ? v[t] : 0.f;
                 }
-                C[(int64_t)m * P.ldc + n] = v;
+                if (whole && cvec) {
+                    *reinterpret_cast<float4*>(crow + n) = make_float4(v[0], v[1], v[2], v[3]);
+                } else {
+#pragma unroll
+                    for (int t = 0; t < 4; ++t)
+                        if (n + t < P.N) crow[n + t] = v[t];
+                }
             }
         }
     }
@@ -299,10 +329,11 @@ __global__ __launch_bounds__(kThreads, 2) void gemm_kernel(GemmBatch batch) {
             const float a1 = j == 0 ? fa[fslot][1].x : j == 1 ? fa[fslot][1].y : j == 2 ? fa[fslot][1].z : fa[fslot][1].w;
             const float b0 = j == 0 ? fb[fslot][0].x : j == 1 ? fb[fslot][0].y : j == 2 ? fb[fslot][0].z : fb[fslot][0].w;
             const float b1 = j == 0 ? fb[fslot][1].x : j == 1 ? fb[fslot][1].y : j == 2 ? fb[fslot][1].z : fb[fslot][1].w;
-            acc[0][0] = __builtin_amdgcn_mfma_f32_32x32x2f32(a0, b0, acc[0][0], 0, 0, 0);
-            acc[0][1] = __builtin_amdgcn_mfma_f32_32x32x2f32(a0, b1, acc[0][1], 0, 0, 0);
-            acc[1][0] = __builtin_amdgcn_mfma_f32_32x32x2f32(a1, b0, acc[1][0], 0, 0, 0);
-            acc[1][1] = __builtin_amdgcn_mfma_f32_32x32x2f32(a1, b1, acc[1][1], 0, 0, 0);
+            // B first: the accumulators hold the transposed blocks (store_tile)
+            acc[0][0] = __builtin_amdgcn_mfma_f32_32x32x2f32(b0, a0, acc[0][0], 0, 0, 0);
+            acc[0][1] = __builtin_amdgcn_mfma_f32_32x32x2f32(b1, a0, acc[0][1], 0, 0, 0);
+            acc[1][0] = __builtin_amdgcn_mfma_f32_32x32x2f32(b0, a1, acc[1][0], 0, 0, 0);
+            acc[1][1] = __builtin_amdgcn_mfma_f32_32x32x2f32(b1, a1, acc[1][1], 0, 0, 0);
         }
     };
 
@@ -333,17 +364,23 @@ __global__ __launch_bounds__(kThreads, 2) void gemm_kernel(GemmBatch batch) {
             ob[q] = (int64_t)(kr + 8 * q) * ldb0 + (bcol.c < N ? bcol.c : 0);
         }
     }
-    auto gload_full = [&](int k0, int q) {
-        const float* sa;
-        const float* sb;
+    // per-step operand bases, uniform across the workgroup (computed once
+    // per K step, outside the per-quad loads)
+    const float* const A1 = P.A1;
+    const float* const B1 = P.B1;
+    auto step_base_a = [&](int k0) -> const float* {
         if constexpr (AL == A_MK)
-            sa = k0 >= ksplitA ? P.A1 + (k0 - ksplitA) : A0 + k0;
+            return k0 >= ksplitA ? A1 + (k0 - ksplitA) : A0 + k0;
         else
-            sa = A0 + (int64_t)k0 * lda0;
+            return A0 + (int64_t)k0 * lda0;
+    };
+    auto step_base_b = [&](int k0) -> const float* {
         if constexpr (BL == B_NK)
-            sb = k0 >= ksplitB ? P.B1 + (k0 - ksplitB) : B0 + k0;
+            return k0 >= ksplitB ? B1 + (k0 - ksplitB) : B0 + k0;
         else
-            sb = B0 + (int64_t)k0 * ldb0;
+            return B0 + (int64_t)k0 * ldb0;
+    };
+    auto gload_full = [&](const float* sa, const float* sb, int q) {
         ra[q].v = ld4(sa + oa[q]);
         rb[q].v = ld4(sb + ob[q]);
     };
@@ -382,10 +419,12 @@ __global__ __launch_bounds__(kThreads, 2) void gemm_kernel(GemmBatch batch) {
         const int knext = kbeg + (kt + 1) * BK;   // past kend on the last step: empty quads
         // group 0: next group's fragments, the next K step's global loads
         frag(As, Bs, 1, 1);
+        const float* const sa = step_base_a(knext);
+        const float* const sb = step_base_b(knext);
 #pragma unroll
         for (int q = 0; q < kQuads; ++q) {
             if constexpr (FULL) {
-                gload_full(knext, q);
+                gload_full(sa, sb, q);
             } else {
                 gload_a(knext, q);
                 gload_b(knext, q);
@@ -647,7 +686,7 @@ __global__ __launch_bounds__(kThreads, 2) void gemm_bf16_kernel(GemmBatch batch)
         for (int i = 0; i < 2; ++i)
 #pragma unroll
             for (int j = 0; j < 2; ++j)
-                acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[fslot][i], fb[fslot][j],
+                acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fb[fslot][j], fa[fslot][i],
                                                                     acc[i][j], 0, 0, 0);
     };
 
