@@ -246,50 +246,50 @@ __global__ __launch_bounds__(kThreads, 2) void gemm_kernel(GemmBatch batch) {
         }
     }
 
-    Quad ra[kQuads], rb[kQuads];
-    auto gload_a = [&](int k0, int q) {
+    // two register sets: set s holds the K steps kt with kt % 2 == s
+    Quad ra[2][kQuads], rb[2][kQuads];
+    auto gload_a = [&](int set, int k0, int q) {
+        Quad& r = ra[set][q];
         if constexpr (AL == A_MK) {
             const int k = k0 + rk;
             const float* p = k < ksplitA ? arow[q].p0 + k : arow[q].p1 + (k - ksplitA);
-            ra[q].one = -1;
-            issue<true>(ra[q], p, A0, (arow[q].live && k < kend) ? kend - k : 0);
+            r.one = -1;
+            issue<true>(r, p, A0, (arow[q].live && k < kend) ? kend - k : 0);
         } else {
             const int k = k0 + kr + 8 * q;
             const int c = acol.c;
             const bool krow = k < kend;
-            ra[q].one = (ones && krow && Areal - c >= 0 && Areal - c < 4) ? Areal - c : -1;
-            issue<true>(ra[q], A0 + (int64_t)k * lda0 + c, A0, (krow && c < Areal) ? Areal - c : 0);
+            r.one = (ones && krow && Areal - c >= 0 && Areal - c < 4) ? Areal - c : -1;
+            issue<true>(r, A0 + (int64_t)k * lda0 + c, A0, (krow && c < Areal) ? Areal - c : 0);
         }
     };
-    auto gload_b = [&](int k0, int q) {
+    auto gload_b = [&](int set, int k0, int q) {
+        Quad& r = rb[set][q];
         if constexpr (BL == B_NK) {
             const int k = k0 + rk;
             const float* p = k < ksplitB ? brow[q].p0 + k : brow[q].p1 + (k - ksplitB);
-            rb[q].one = -1;
-            issue<BVEC>(rb[q], p, B0, (brow[q].live && k < kend) ? kend - k : 0);
+            r.one = -1;
+            issue<BVEC>(r, p, B0, (brow[q].live && k < kend) ? kend - k : 0);
         } else {
             const int k = k0 + kr + 8 * q;
             const int c = bcol.c;
             const bool krow = k < kend;
-            rb[q].one = -1;
-            issue<BVEC>(rb[q], B0 + (int64_t)k * ldb0 + c, B0, (krow && c < N) ? N - c : 0);
+            r.one = -1;
+            issue<BVEC>(r, B0 + (int64_t)k * ldb0 + c, B0, (krow && c < N) ? N - c : 0);
         }
     };
-    auto sstore = [&](int buf, int q) {
-        float* As = smem[buf][0];
-        float* Bs = smem[buf][1];
-        const float4 a = finish(ra[q]);
-        const float4 b = finish(rb[q]);
-        if constexpr (AL == A_MK) {
-            *reinterpret_cast<float4*>(&As[(t / kPerRow + kRowStep * q) * kRowStride + rk]) = a;
-        } else {
-            *reinterpret_cast<float4*>(&As[(kr + 8 * q) * kColStride + 4 * (t & 31)]) = a;
-        }
-        if constexpr (BL == B_NK) {
-            *reinterpret_cast<float4*>(&Bs[(t / kPerRow + kRowStep * q) * kRowStride + rk]) = b;
-        } else {
-            *reinterpret_cast<float4*>(&Bs[(kr + 8 * q) * kColStride + 4 * (t & 31)]) = b;
-        }
+    // LDS placement of quad q (row-contiguous: [row][k]; K-major: [k][col])
+    auto a_slot = [&](int q) {
+        return AL == A_MK ? (t / kPerRow + kRowStep * q) * kRowStride + rk
+                          : (kr + 8 * q) * kColStride + 4 * (t & 31);
+    };
+    auto b_slot = [&](int q) {
+        return BL == B_NK ? (t / kPerRow + kRowStep * q) * kRowStride + rk
+                          : (kr + 8 * q) * kColStride + 4 * (t & 31);
+    };
+    auto sstore = [&](int buf, int set, int q) {
+        *reinterpret_cast<float4*>(&smem[buf][0][a_slot(q)]) = finish(ra[set][q]);
+        *reinterpret_cast<float4*>(&smem[buf][1][b_slot(q)]) = finish(rb[set][q]);
     };
 
     floatx16 acc[2][2];
@@ -380,54 +380,44 @@ __global__ __launch_bounds__(kThreads, 2) void gemm_kernel(GemmBatch batch) {
         else
             return B0 + (int64_t)k0 * ldb0;
     };
-    auto gload_full = [&](const float* sa, const float* sb, int q) {
-        ra[q].v = ld4(sa + oa[q]);
-        rb[q].v = ld4(sb + ob[q]);
+    auto gload_full = [&](int set, const float* sa, const float* sb, int q) {
+        ra[set][q].v = ld4(sa + oa[q]);
+        rb[set][q].v = ld4(sb + ob[q]);
     };
-    auto sstore_full = [&](int buf, int q) {
-        float* As = smem[buf][0];
-        float* Bs = smem[buf][1];
-        if constexpr (AL == A_MK) {
-            *reinterpret_cast<float4*>(&As[(t / kPerRow + kRowStep * q) * kRowStride + rk]) = ra[q].v;
-        } else {
-            *reinterpret_cast<float4*>(&As[(kr + 8 * q) * kColStride + 4 * (t & 31)]) = ra[q].v;
-        }
-        if constexpr (BL == B_NK) {
-            *reinterpret_cast<float4*>(&Bs[(t / kPerRow + kRowStep * q) * kRowStride + rk]) = rb[q].v;
-        } else {
-            *reinterpret_cast<float4*>(&Bs[(kr + 8 * q) * kColStride + 4 * (t & 31)]) = rb[q].v;
+    auto sstore_full = [&](int buf, int set, int q) {
+        *reinterpret_cast<float4*>(&smem[buf][0][a_slot(q)]) = ra[set][q].v;
+        *reinterpret_cast<float4*>(&smem[buf][1][b_slot(q)]) = rb[set][q].v;
+    };
+    // quads of a set filled by whole-step loads, for a masked store
+    auto mark_full = [&](int set) {
+#pragma unroll
+        for (int q = 0; q < kQuads; ++q) {
+            ra[set][q].valid = rb[set][q].valid = 4;
+            ra[set][q].one = rb[set][q].one = -1;
         }
     };
 
     static_assert(BK / 8 == 4, "the K step is laid out as four groups of 8");
-    if (nk > 0) {
-#pragma unroll
-        for (int q = 0; q < kQuads; ++q) {
-            gload_a(kbeg, q);
-            gload_b(kbeg, q);
-            sstore(0, q);
-        }
-        __syncthreads();
-        frag(smem[0][0], smem[0][1], 0, 0);
-    }
-    // One K step. FULL: the next step, loaded here, is a whole step of a
-    // fast tile (and a next step exists).
-    auto kstep = [&](int kt, auto FULL) {
+    // One K step. LDS buffer kt % 2 holds step kt; register set (kt + 1) % 2
+    // holds step kt + 1 and step kt + 2 is loaded into set kt % 2 meanwhile,
+    // so every global load has two K steps of MFMA work to arrive. FULL:
+    // steps kt + 1 and kt + 2 are whole steps of a fast tile.
+    auto kstep = [&](int kt, int set, auto FULL) {
         const int buf = kt & 1;
         const float* As = smem[buf][0];
         const float* Bs = smem[buf][1];
-        const int knext = kbeg + (kt + 1) * BK;   // past kend on the last step: empty quads
-        // group 0: next group's fragments, the next K step's global loads
+        const int kload = kbeg + (kt + 2) * BK;   // past kend near the end: empty quads
+        // group 0: next group's fragments, the global loads of step kt + 2
         frag(As, Bs, 1, 1);
-        const float* const sa = step_base_a(knext);
-        const float* const sb = step_base_b(knext);
+        const float* const sa = step_base_a(kload);
+        const float* const sb = step_base_b(kload);
 #pragma unroll
         for (int q = 0; q < kQuads; ++q) {
             if constexpr (FULL) {
-                gload_full(sa, sb, q);
+                gload_full(set, sa, sb, q);
             } else {
-                gload_a(knext, q);
-                gload_b(knext, q);
+                gload_a(set, kload, q);
+                gload_b(set, kload, q);
             }
         }
         mfma_group(0);
@@ -442,15 +432,19 @@ __global__ __launch_bounds__(kThreads, 2) void gemm_kernel(GemmBatch batch) {
         frag(As, Bs, 2, 0);
         mfma_group(1);
         __builtin_amdgcn_sched_barrier(0);
-        // group 2: the next K step goes into the other buffer, whose last
-        // reader (the previous step) finished before the previous barrier
+        // group 2: step kt + 1 goes from its register set into the other
+        // buffer, whose last reader (step kt - 1) finished before the
+        // previous barrier
         frag(As, Bs, 3, 1);
+        const bool more = FULL || kt + 1 < nk;
+        if (more) {
 #pragma unroll
-        for (int q = 0; q < kQuads; ++q) {
-            if constexpr (FULL)
-                sstore_full(buf ^ 1, q);
-            else
-                sstore(buf ^ 1, q);
+            for (int q = 0; q < kQuads; ++q) {
+                if constexpr (FULL)
+                    sstore_full(buf ^ 1, set ^ 1, q);
+                else
+                    sstore(buf ^ 1, set ^ 1, q);
+            }
         }
         mfma_group(0);
         __builtin_amdgcn_sched_group_barrier(0x100, 8, 0);      // DS reads first
@@ -463,14 +457,50 @@ __global__ __launch_bounds__(kThreads, 2) void gemm_kernel(GemmBatch batch) {
         __syncthreads();
         // group 3: its fragments are already in registers, so the next
         // step's first LDS reads are hidden behind these MFMAs
-        if (FULL || kt + 1 < nk) frag(smem[buf ^ 1][0], smem[buf ^ 1][1], 0, 0);
+        if (more) frag(smem[buf ^ 1][0], smem[buf ^ 1][1], 0, 0);
         mfma_group(1);
         __builtin_amdgcn_sched_barrier(0);
     };
+    using Full = std::true_type;
+    using Masked = std::false_type;
+    const bool fast_start = fast_tile && nfull >= 2;
+    if (fast_start) {
+#pragma unroll
+        for (int q = 0; q < kQuads; ++q) {
+            gload_full(0, step_base_a(kbeg), step_base_b(kbeg), q);
+            gload_full(1, step_base_a(kbeg + BK), step_base_b(kbeg + BK), q);
+        }
+#pragma unroll
+        for (int q = 0; q < kQuads; ++q) sstore_full(0, 0, q);
+    } else if (nk > 0) {
+#pragma unroll
+        for (int q = 0; q < kQuads; ++q) {
+            gload_a(0, kbeg, q);
+            gload_b(0, kbeg, q);
+            gload_a(1, kbeg + BK, q);
+            gload_b(1, kbeg + BK, q);
+        }
+#pragma unroll
+        for (int q = 0; q < kQuads; ++q) sstore(0, 0, q);
+    }
+    if (nk > 0) {
+        __syncthreads();
+        frag(smem[0][0], smem[0][1], 0, 0);
+    }
     int kt = 0;
-    if (fast_tile)
-        for (; kt + 1 < nfull; ++kt) kstep(kt, std::true_type{});
-    for (; kt < nk; ++kt) kstep(kt, std::false_type{});
+    if (fast_start) {
+        for (; kt + 3 < nfull; kt += 2) {
+            kstep(kt, 0, Full{});
+            kstep(kt + 1, 1, Full{});
+        }
+        mark_full(0);
+        mark_full(1);
+    }
+    for (; kt + 1 < nk; kt += 2) {
+        kstep(kt, 0, Masked{});
+        kstep(kt + 1, 1, Masked{});
+    }
+    if (kt < nk) kstep(kt, 0, Masked{});
 
     store_tile<EP>(P, split, m0 + wm * 64, n0 + wn * 64, half, l32, acc);
 }
