@@ -14,12 +14,15 @@ Plain, slow, float64 NumPy/SciPy code written from the paper:
                     gradient-descent update (Section 2.1)
   * precision.py  - bfloat16 operand rounding of the bf16 variant of the
                     dense products
+  * optim.py      - the momentum and Adam weight updates (Section 4.1 names
+                    their state; the rules are the cited methods')
 
 Pins (tests/test_oracle_*.py): the worked examples of Fig. 1 and Fig. 2,
 Theorem 1's exact accounting, brute force on tiny graphs, an independent
 sparse-matrix form of Algorithm 1, the greedy matching's 1/2-approximation
 against an exact maximum-weight matching, constant-feature and closed-form
-loss cases, and central finite differences of the loss.
+loss cases, central finite differences of the loss, and closed forms of the
+optimisers under a constant gradient.
 
 Parity unpinned (no printed value or closed form fixes it): the greedy
 matching's order among equal weights. The paper leaves it open; the oracle

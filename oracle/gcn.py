@@ -12,7 +12,8 @@ Backward (Eq. 2a-2c), G = mask(dL/dH_l) with mask = ReLU' (0 at 0):
                    dW_neigh = (D^-1 A H_{l-1})^T G[:, h:]
                    dH_{l-1} = G[:, :h] W_self^T + A D^-1 G[:, h:] W_neigh^T
 Update:            W <- W - lr dW (plain gradient descent, Section 4.1 notes
-                   vanilla gradient descent keeps no optimiser state).
+                   vanilla gradient descent keeps no optimiser state); momentum
+                   and Adam in optim.py.
 
 Optional biases (not in Eq. 1; kept off by default): b_l in R^{2h} added
 before the ReLU, b_cls in R^C added to the logits.
@@ -23,6 +24,7 @@ import numpy as np
 import scipy.sparse as sp
 
 from . import graph as _graph
+from . import optim as _optim
 
 SOFTMAX_CE = 0
 SIGMOID_BCE = 1
@@ -209,13 +211,19 @@ def sgd(params, grads, lr):
     return new
 
 
-def train_step(rowptr, col, X, params, labels, loss_kind, lr, masks=None):
-    """One forward + loss + backward + gradient-descent step."""
+def train_step(rowptr, col, X, params, labels, loss_kind, lr, masks=None, opt=None,
+               state1=None, state2=None):
+    """One forward + loss + backward + update step: plain gradient descent
+    with step lr, or the optimiser `opt` (optim.Optim) with its states."""
     fw = forward(rowptr, col, X, params)
     loss, dlogits = loss_and_grad(loss_kind, fw["logits"], labels)
     grads = backward(rowptr, col, params, fw, dlogits, masks)
-    new = sgd(params, grads, lr)
-    return dict(fw=fw, loss=loss, dlogits=dlogits, grads=grads, params=new)
+    if opt is None:
+        return dict(fw=fw, loss=loss, dlogits=dlogits, grads=grads,
+                    params=sgd(params, grads, lr))
+    new, s1, s2 = _optim.apply(opt, params, grads, state1, state2)
+    return dict(fw=fw, loss=loss, dlogits=dlogits, grads=grads, params=new, state1=s1,
+                state2=s2)
 
 
 def loss_only(rowptr, col, X, params, labels, loss_kind):
