@@ -60,12 +60,14 @@ def parse():
                          "first where the input is wider than h")
     ap.add_argument("--no-narrow", action="store_true",
                     help="skip the extra timing of the narrow-side order")
+    ap.add_argument("--no-adam", action="store_true",
+                    help="skip the extra timing of the step with the Adam update")
     ap.add_argument("--no-direct", action="store_true",
                     help="skip the direct-aggregation comparison run (counter runs)")
     ap.add_argument("--trace-summary", metavar="KERNEL_STATS_CSV",
                     help="no GPU: turn a rocprofv3 --kernel-trace --stats kernel_stats.csv "
                          "of this script into the per-class table under profiles/")
-    ap.add_argument("--traced-args", default="--no-cpu-baseline --no-direct --no-narrow",
+    ap.add_argument("--traced-args", default="--no-cpu-baseline --no-direct --no-narrow --no-adam",
                     help="with --trace-summary: the arguments the traced run was given")
     ap.add_argument("--bench-line", help="with --trace-summary: the JSON line the traced run "
                                          "printed (event timings shown beside the trace)")
@@ -173,7 +175,7 @@ def pmc_summary(fetch_csv, write_csv, workload, cmd_args):
                         source_hash=source_hash(c))
     bargs = (f"--workload {workload} --steps {cmd_args['steps']} --warmup {cmd_args['warmup']} "
              f"--profile-steps {cmd_args['profile_steps']} --no-cpu-baseline --no-direct "
-             f"--no-narrow "
+             f"--no-narrow --no-adam "
              f"--calib-copy-mib {cmd_args['calib_copy_mib']}")
     lines = [
         f"# HBM traffic per launch, {workload} training step",
@@ -236,7 +238,7 @@ def trace_summary(stats_csv, workload, cmd_args, bench_line=None):
            f"python3 bench.py --workload {workload} --traced-args='{cmd_args}' "
            "--trace-summary OUT/run_kernel_stats.csv --bench-line OUT/line.json", "```",
            "", ("The run covers the warm-up, timed and profiled steps of the reduced-graph "
-                "step alone." if "--no-direct" in cmd_args and "--no-narrow" in cmd_args else
+                "step alone." if all(f in cmd_args for f in ("--no-direct", "--no-narrow", "--no-adam")) else
                 "The run also covers the comparison runs bench.py times beside the step "
                 "(their kernels are counted in the same classes)."), "",
            "## Per timing class (the classes bench.py times with HIP events)", "",
@@ -274,7 +276,7 @@ def stored_traffic(workload, cls):
 class Setup:
     """Inputs of one workload on the device, ready for timed steps."""
 
-    def __init__(self, wl, reduce, inp, seg_len=0, precision=0, order=0):
+    def __init__(self, wl, reduce, inp, seg_len=0, precision=0, order=0, optim=None):
         import torch
         from paper_2001_02498_amd import gcn
         self.gcn, self.wl = gcn, wl
@@ -306,9 +308,23 @@ class Setup:
                                    precision=precision, order=order)
         self.ws = gcn.alloc_ws(gcn.workspace_bytes(self.dg, self.desc))
         self.loss = torch.zeros(1, device="cuda")
+        # optimiser states (zero, shaped like the weights) when not plain descent
+        self.opt, self.S = None, [None, None]
+        if optim is not None:
+            self.opt = gcn.optim(optim, wl.lr)
+            self.states = []
+            for _ in range(2 if optim == gcn.OPT_ADAM else 1):
+                t = ([torch.zeros_like(w) for w in self.Ws], [torch.zeros_like(w) for w in self.Wn],
+                     torch.zeros_like(self.Wc))
+                self.states.append(t)
+                self.S[len(self.states) - 1] = gcn.make_params(*t)
         torch.cuda.synchronize()
 
     def step(self):
+        if self.opt is not None:
+            self.gcn.train_step_optim(self.dg, self.desc, self.P, self.X, self.labels, self.opt,
+                                      self.loss, self.ws, state1=self.S[0], state2=self.S[1])
+            return
         self.gcn.train_step(self.dg, self.desc, self.P, self.X, self.labels, self.wl.lr,
                             self.loss, self.ws)
 
@@ -672,6 +688,12 @@ def main():
         narrow = 1e3 * d.timed(args.steps, args.warmup, args.graph)
         print(f"[bench] narrow-side order: {narrow:.3f} ms/step", file=sys.stderr, flush=True)
         del d
+    adam = None
+    if not args.no_adam:
+        d = Setup(wl, wl.reduce, inp, args.seg_len, prec, order, optim=gcn.OPT_ADAM)
+        adam = 1e3 * d.timed(args.steps, args.warmup, args.graph)
+        print(f"[bench] Adam update: {adam:.3f} ms/step", file=sys.stderr, flush=True)
+        del d
     prof = red.profile(args.profile_steps)
     ktab = kernel_table(prof, args.profile_steps)
     dominant = max(ktab, key=lambda k: ktab[k]["ms_per_step"])
@@ -735,6 +757,7 @@ def main():
         "cpu_baseline": cpu,
         "direct_aggregation_ms_per_step": None if direct is None else round(direct, 4),
         "narrow_order_ms_per_step": None if narrow is None else round(narrow, 4),
+        "adam_ms_per_step": None if adam is None else round(adam, 4),
         "host_preprocess_ms": {k: round(v, 2) for k, v in red.host_ms.items()},
         "aggregation_roofline": agg,
         "kernels": {k: {kk: vv for kk, vv in v.items()

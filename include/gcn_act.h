@@ -427,6 +427,49 @@ int gcn_train_step(const gcn_dgraph* g, const gcn_model_desc* desc,
                    const gcn_params* grads, void* ws, size_t ws_bytes,
                    gcn_stream_t stream);
 
+/* ------------------------------------------------------ optimisers
+ * gcn_train_step_optim - gcn_train_step with every weight (and bias)
+ * updated by the optimiser `opt` instead of plain gradient descent.
+ * Section 4.1 names the state each optimiser keeps beside the weights:
+ * none for gradient descent, the earlier steps' weight gradients for
+ * gradient descent with momentum, first and second moment estimates for
+ * Adam; the update rules are those of the cited methods, with g the
+ * weight's gradient of this step and t = opt->step:
+ *   GCN_OPT_SGD       W <- W - lr g                       (gcn_train_step)
+ *   GCN_OPT_MOMENTUM  u <- mu u + g;  W <- W - lr u
+ *   GCN_OPT_ADAM      m <- b1 m + (1 - b1) g;  v <- b2 v + (1 - b2) g^2;
+ *                     W <- W - lr (m / (1 - b1^t)) / (sqrt(v / (1 - b2^t)) + eps)
+ * The update runs where the weight-gradient slices are summed, so each
+ * weight and each state word is read and written once per step.
+ *   opt     host struct; step counts updates from 1 (Adam's bias
+ *           correction); momentum in [0, 1); beta1, beta2 in [0, 1);
+ *           eps > 0; lr finite
+ *   state1  momentum: u, Adam: m; state2: Adam's v (NULL otherwise).
+ *           Device buffers shaped like `params` (every member the model
+ *           uses non-NULL), zero before the first step, updated in place;
+ *           owned by the caller. SGD reads neither.
+ * Errors: GCN_E_INVALID_ARG for an unknown kind, a value out of range or a
+ * missing state buffer (nothing launched); otherwise as gcn_train_step.
+ */
+#define GCN_OPT_SGD 0
+#define GCN_OPT_MOMENTUM 1
+#define GCN_OPT_ADAM 2
+typedef struct {
+    int32_t kind;         /* GCN_OPT_* */
+    int32_t step;         /* Adam: 1 for the first update */
+    float lr;
+    float momentum;       /* GCN_OPT_MOMENTUM: mu */
+    float beta1, beta2, eps;   /* GCN_OPT_ADAM */
+    float reserved;
+} gcn_optim;
+
+int gcn_train_step_optim(const gcn_dgraph* g, const gcn_model_desc* desc,
+                         const gcn_params* params, const float* X,
+                         const void* labels, const gcn_optim* opt,
+                         const gcn_params* state1, const gcn_params* state2,
+                         float* loss_out, const gcn_params* grads, void* ws,
+                         size_t ws_bytes, gcn_stream_t stream);
+
 /* ---------------------------------------------------- launch timing
  * Tracing for measurement: when enabled, every kernel launch made by the
  * entry points above is bracketed by two HIP events on its own stream and

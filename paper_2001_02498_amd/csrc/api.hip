@@ -2,6 +2,7 @@
 // and the composition of aggregation, GEMMs, loss and update into layer and
 // training-step calls. Every check runs before the first launch.
 #include <algorithm>
+#include <cmath>
 #include <cstring>
 
 #include "kernels.h"
@@ -260,14 +261,39 @@ SgdProblem sgd_problem(const GemmProblem& gpb, int32_t Mw, int32_t N, float* W,
     q.b = b;
     q.dW_out = dW_out;
     q.db_out = db_out;
+    q.s1 = q.s2 = q.s1b = q.s2b = nullptr;
     return q;
+}
+
+// Optimiser state of one weight and of the bias it shares a reduction with
+// (NULL members: plain gradient descent keeps none).
+struct OptState {
+    float* s1 = nullptr;
+    float* s2 = nullptr;
+    float* s1b = nullptr;
+    float* s2b = nullptr;
+};
+
+SgdProblem with_state(SgdProblem q, const OptState& st) {
+    q.s1 = st.s1;
+    q.s2 = st.s2;
+    q.s1b = st.s1b;
+    q.s2b = st.s2b;
+    return q;
+}
+
+OptimArgs sgd_args(float lr) {
+    OptimArgs o{};
+    o.kind = OPT_SGD;
+    o.lr = lr;
+    return o;
 }
 
 int do_classifier_bwd(const char* fn, int32_t n, int32_t K, int32_t C,
                       const float* dZ, int64_t ldd, const float* H, int64_t ldh,
-                      float* Wc, float* bc, float lr, float* G_out, int64_t ldg,
-                      float* dWc_out, float* dbc_out, bool bf16, const ScratchPlan& sp,
-                      void* ws, hipStream_t s) {
+                      float* Wc, float* bc, const OptimArgs& oa, const OptState& st,
+                      float* G_out, int64_t ldg, float* dWc_out, float* dbc_out, bool bf16,
+                      const ScratchPlan& sp, void* ws, hipStream_t s) {
     if (G_out) {
         GemmBatch b;
         std::memset(&b, 0, sizeof(b));
@@ -294,15 +320,16 @@ int do_classifier_bwd(const char* fn, int32_t n, int32_t K, int32_t C,
     b.nprob = 1;
     b.p[0] = dw_problem(n, K, bc != nullptr, C, H, ldh, dZ, ldd, fptr(ws, sp.gemm_part), 1);
     GCN_HIP(launch_gemm(b, A_KM, B_KN, EPI_PARTIAL, ROLE_CLS_DW, bf16, s), fn);
-    SgdProblem q = sgd_problem(b.p[0], K, C, Wc, bc, dWc_out, dbc_out);
-    GCN_HIP(launch_sgd_reduce(&q, 1, lr, s), fn);
+    SgdProblem q = with_state(sgd_problem(b.p[0], K, C, Wc, bc, dWc_out, dbc_out), st);
+    GCN_HIP(launch_sgd_reduce(&q, 1, oa, s), fn);
     return GCN_OK;
 }
 
 int do_layer_bwd(const char* fn, const gcn_dgraph* g, int32_t F, int32_t h,
                  const float* G, int64_t ldg, const float* H_in, int64_t ld_in,
                  const float* AH, int64_t ld_ah, float* Ws, float* Wn,
-                 float* bias, float lr, float* G_in, int64_t ldgi,
+                 float* bias, const OptimArgs& oa, const OptState& st_self,
+                 const OptState& st_neigh, float* G_in, int64_t ldgi,
                  float* dWs_out, float* dWn_out, float* db_out, bool bf16,
                  const ScratchPlan& sp, void* ws, hipStream_t s) {
     const int32_t n = g->n;
@@ -348,10 +375,11 @@ int do_layer_bwd(const char* fn, const gcn_dgraph* g, int32_t F, int32_t h,
     b.p[1] = dw_problem(n, F, ones, h, AH, ld_ah, G + h, ldg, part1, 2);
     GCN_HIP(launch_gemm(b, A_KM, B_KN, EPI_PARTIAL, ROLE_DW, bf16, s), fn);
     SgdProblem q[2] = {
-        sgd_problem(b.p[0], F, h, Ws, bias, dWs_out, db_out),
-        sgd_problem(b.p[1], F, h, Wn, bias ? bias + h : nullptr, dWn_out,
-                    db_out ? db_out + h : nullptr)};
-    GCN_HIP(launch_sgd_reduce(q, 2, lr, s), fn);
+        with_state(sgd_problem(b.p[0], F, h, Ws, bias, dWs_out, db_out), st_self),
+        with_state(sgd_problem(b.p[1], F, h, Wn, bias ? bias + h : nullptr, dWn_out,
+                               db_out ? db_out + h : nullptr),
+                   st_neigh)};
+    GCN_HIP(launch_sgd_reduce(q, 2, oa, s), fn);
     return GCN_OK;
 }
 
@@ -390,7 +418,8 @@ int do_layer_fwd_narrow(const char* fn, const gcn_dgraph* g, int32_t F, int32_t 
 // layer), G_in as in the paper order, and dW_neigh = H_in^T T.
 int do_layer_bwd_narrow(const char* fn, const gcn_dgraph* g, int32_t F, int32_t h,
                         const float* G, int64_t ldg, const float* H_in, int64_t ld_in,
-                        float* Ws, float* Wn, float lr, float* G_in, int64_t ldgi,
+                        float* Ws, float* Wn, const OptimArgs& oa, const OptState& st_self,
+                        const OptState& st_neigh, float* G_in, int64_t ldgi,
                         float* dWs_out, float* dWn_out, bool bf16, const ScratchPlan& sp,
                         void* ws, hipStream_t s) {
     const int32_t n = g->n;
@@ -430,9 +459,10 @@ int do_layer_bwd_narrow(const char* fn, const gcn_dgraph* g, int32_t F, int32_t 
     b.p[0] = dw_problem(n, F, false, h, H_in, ld_in, G, ldg, part0, 2);
     b.p[1] = dw_problem(n, F, false, h, H_in, ld_in, T, ldt, part1, 2);
     GCN_HIP(launch_gemm(b, A_KM, B_KN, EPI_PARTIAL, ROLE_DW, bf16, s), fn);
-    SgdProblem q[2] = {sgd_problem(b.p[0], F, h, Ws, nullptr, dWs_out, nullptr),
-                       sgd_problem(b.p[1], F, h, Wn, nullptr, dWn_out, nullptr)};
-    GCN_HIP(launch_sgd_reduce(q, 2, lr, s), fn);
+    SgdProblem q[2] = {
+        with_state(sgd_problem(b.p[0], F, h, Ws, nullptr, dWs_out, nullptr), st_self),
+        with_state(sgd_problem(b.p[1], F, h, Wn, nullptr, dWn_out, nullptr), st_neigh)};
+    GCN_HIP(launch_sgd_reduce(q, 2, oa, s), fn);
     return GCN_OK;
 }
 
@@ -631,9 +661,9 @@ int gcn_classifier_bwd(int32_t n, int32_t K, int32_t C, const float* dZ, int64_t
     if (db_cls_out) GCN_TRY(check_vec(fn, "db_cls_out", db_cls_out, C));
     const ScratchPlan sp = plan_scratch(n, 0, 0, std::max(K, C));
     GCN_TRY(check_ws(fn, ws, ws_bytes, sp.total));
-    return do_classifier_bwd(fn, n, K, C, dZ, ldd, H, ldh, W_cls, b_cls, lr, G_out, ldg,
-                             dW_cls_out, db_cls_out, precision == GCN_PREC_BF16, sp, ws,
-                             (hipStream_t)stream);
+    return do_classifier_bwd(fn, n, K, C, dZ, ldd, H, ldh, W_cls, b_cls, sgd_args(lr),
+                             OptState{}, G_out, ldg, dW_cls_out, db_cls_out,
+                             precision == GCN_PREC_BF16, sp, ws, (hipStream_t)stream);
 }
 
 int gcn_layer_bwd(const gcn_dgraph* g, int32_t F, int32_t h, const float* G, int64_t ldg,
@@ -661,8 +691,9 @@ int gcn_layer_bwd(const gcn_dgraph* g, int32_t F, int32_t h, const float* G, int
     const ScratchPlan sp = plan_scratch(n, g->naux, g->nslots, std::max(F, 2 * h));
     GCN_TRY(check_ws(fn, ws, ws_bytes, sp.total));
     return do_layer_bwd(fn, g, F, h, G, ldg, H_in, ld_in, AH, ld_ah, W_self, W_neigh, bias,
-                        lr, G_in, ldgi, dW_self_out, dW_neigh_out, db_out,
-                        precision == GCN_PREC_BF16, sp, ws, (hipStream_t)stream);
+                        sgd_args(lr), OptState{}, OptState{}, G_in, ldgi, dW_self_out,
+                        dW_neigh_out, db_out, precision == GCN_PREC_BF16, sp, ws,
+                        (hipStream_t)stream);
 }
 
 int gcn_workspace_layout(const gcn_dgraph* g, const gcn_model_desc* desc,
@@ -685,11 +716,49 @@ int gcn_workspace_bytes(const gcn_dgraph* g, const gcn_model_desc* desc, size_t*
     return GCN_OK;
 }
 
-int gcn_train_step(const gcn_dgraph* g, const gcn_model_desc* d, const gcn_params* P,
-                   const float* X, const void* labels, float lr, float* loss_out,
-                   const gcn_params* grads, void* ws, size_t ws_bytes,
-                   gcn_stream_t stream) {
-    const char* fn = "gcn_train_step";
+}  // extern "C"
+
+namespace {
+
+// The state buffers an optimiser needs for every weight (and bias) of the
+// model: shaped like the weights, non-NULL.
+int check_state(const char* fn, const char* what, const gcn_model_desc* d,
+                const gcn_params* st) {
+    GCN_CHECK_ARG(st != nullptr, "%s: %s is NULL", fn, what);
+    const int32_t h = d->h, C = d->C;
+    for (int l = 0; l < d->L; ++l) {
+        const int64_t F = l == 0 ? d->f_in : 2 * (int64_t)h;
+        GCN_TRY(check_vec(fn, what, st->W_self[l], F * h));
+        GCN_TRY(check_vec(fn, what, st->W_neigh[l], F * h));
+        if (d->has_bias) GCN_TRY(check_vec(fn, what, st->b[l], 2 * (int64_t)h));
+    }
+    GCN_TRY(check_vec(fn, what, st->W_cls, 2 * (int64_t)h * C));
+    if (d->has_bias) GCN_TRY(check_vec(fn, what, st->b_cls, C));
+    return GCN_OK;
+}
+
+// Optimiser state of layer l's self (half 0) or neighbour (half 1) weight,
+// with the matching half of its bias.
+OptState layer_state(const gcn_model_desc* d, const gcn_params* s1, const gcn_params* s2,
+                     int l, int half) {
+    OptState st;
+    const int64_t boff = half ? d->h : 0;
+    if (s1) {
+        st.s1 = half ? s1->W_neigh[l] : s1->W_self[l];
+        st.s1b = d->has_bias ? s1->b[l] + boff : nullptr;
+    }
+    if (s2) {
+        st.s2 = half ? s2->W_neigh[l] : s2->W_self[l];
+        st.s2b = d->has_bias ? s2->b[l] + boff : nullptr;
+    }
+    return st;
+}
+
+int train_step_impl(const char* fn, const gcn_dgraph* g, const gcn_model_desc* d,
+                    const gcn_params* P, const float* X, const void* labels,
+                    const OptimArgs& oa, const gcn_params* st1, const gcn_params* st2,
+                    float* loss_out, const gcn_params* grads, void* ws, size_t ws_bytes,
+                    gcn_stream_t stream) {
     GCN_TRY(check_graph(fn, g));
     GCN_TRY(check_desc(fn, d));
     GCN_CHECK_ARG(P != nullptr, "%s: params is NULL", fn);
@@ -762,8 +831,17 @@ int gcn_train_step(const gcn_dgraph* g, const gcn_model_desc* d, const gcn_param
             fn);
     // backward (classifier, then Eq. 2a-2c layer by layer)
     float* Gcur = act(sl.pub.G[L - 1]);
+    OptState cst;
+    if (st1) {
+        cst.s1 = st1->W_cls;
+        cst.s1b = d->has_bias ? st1->b_cls : nullptr;
+    }
+    if (st2) {
+        cst.s2 = st2->W_cls;
+        cst.s2b = d->has_bias ? st2->b_cls : nullptr;
+    }
     GCN_TRY(do_classifier_bwd(fn, (int32_t)n, 2 * h, C, dZ, ldC, Hprev, ldH, P->W_cls,
-                              d->has_bias ? P->b_cls : nullptr, lr, Gcur, ldH,
+                              d->has_bias ? P->b_cls : nullptr, oa, cst, Gcur, ldH,
                               grads ? grads->W_cls : nullptr,
                               grads ? grads->b_cls : nullptr, bf16, sp, scratch, s));
     for (int l = L - 1; l >= 0; --l) {
@@ -773,7 +851,8 @@ int gcn_train_step(const gcn_dgraph* g, const gcn_model_desc* d, const gcn_param
         float* Gnext = l > 0 ? act(sl.pub.G[l - 1]) : nullptr;
         if (narrow_layer(d, F)) {
             GCN_TRY(do_layer_bwd_narrow(fn, g, F, h, Gcur, ldH, Hin, ldin, P->W_self[l],
-                                        P->W_neigh[l], lr, Gnext, ldH,
+                                        P->W_neigh[l], oa, layer_state(d, st1, st2, l, 0),
+                                        layer_state(d, st1, st2, l, 1), Gnext, ldH,
                                         grads ? grads->W_self[l] : nullptr,
                                         grads ? grads->W_neigh[l] : nullptr, bf16, sp, scratch,
                                         s));
@@ -782,13 +861,77 @@ int gcn_train_step(const gcn_dgraph* g, const gcn_model_desc* d, const gcn_param
         }
         GCN_TRY(do_layer_bwd(fn, g, F, h, Gcur, ldH, Hin, ldin, act(sl.pub.AH[l]),
                              sl.pub.ld_AH[l], P->W_self[l], P->W_neigh[l],
-                             d->has_bias ? P->b[l] : nullptr, lr, Gnext, ldH,
-                             grads ? grads->W_self[l] : nullptr,
+                             d->has_bias ? P->b[l] : nullptr, oa,
+                             layer_state(d, st1, st2, l, 0), layer_state(d, st1, st2, l, 1),
+                             Gnext, ldH, grads ? grads->W_self[l] : nullptr,
                              grads ? grads->W_neigh[l] : nullptr,
                              grads ? grads->b[l] : nullptr, bf16, sp, scratch, s));
         Gcur = Gnext;
     }
     return GCN_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int gcn_train_step(const gcn_dgraph* g, const gcn_model_desc* d, const gcn_params* P,
+                   const float* X, const void* labels, float lr, float* loss_out,
+                   const gcn_params* grads, void* ws, size_t ws_bytes,
+                   gcn_stream_t stream) {
+    return train_step_impl("gcn_train_step", g, d, P, X, labels, sgd_args(lr), nullptr,
+                           nullptr, loss_out, grads, ws, ws_bytes, stream);
+}
+
+int gcn_train_step_optim(const gcn_dgraph* g, const gcn_model_desc* d, const gcn_params* P,
+                         const float* X, const void* labels, const gcn_optim* opt,
+                         const gcn_params* state1, const gcn_params* state2,
+                         float* loss_out, const gcn_params* grads, void* ws,
+                         size_t ws_bytes, gcn_stream_t stream) {
+    const char* fn = "gcn_train_step_optim";
+    GCN_CHECK_ARG(opt != nullptr, "%s: opt is NULL", fn);
+    GCN_TRY(check_desc(fn, d));
+    GCN_CHECK_ARG(std::isfinite(opt->lr), "%s: lr is not finite", fn);
+    OptimArgs oa = sgd_args(opt->lr);
+    const gcn_params* s1 = nullptr;
+    const gcn_params* s2 = nullptr;
+    switch (opt->kind) {
+        case GCN_OPT_SGD:
+            break;
+        case GCN_OPT_MOMENTUM:
+            GCN_CHECK_ARG(opt->momentum >= 0.f && opt->momentum < 1.f,
+                          "%s: momentum %g outside [0, 1)", fn, (double)opt->momentum);
+            GCN_TRY(check_state(fn, "state1", d, state1));
+            oa.kind = OPT_MOMENTUM;
+            oa.mu = opt->momentum;
+            s1 = state1;
+            break;
+        case GCN_OPT_ADAM: {
+            GCN_CHECK_ARG(opt->beta1 >= 0.f && opt->beta1 < 1.f && opt->beta2 >= 0.f &&
+                              opt->beta2 < 1.f,
+                          "%s: beta1 %g / beta2 %g outside [0, 1)", fn, (double)opt->beta1,
+                          (double)opt->beta2);
+            GCN_CHECK_ARG(opt->eps > 0.f && std::isfinite(opt->eps), "%s: eps must be > 0",
+                          fn);
+            GCN_CHECK_ARG(opt->step >= 1, "%s: step %d < 1", fn, opt->step);
+            GCN_TRY(check_state(fn, "state1", d, state1));
+            GCN_TRY(check_state(fn, "state2", d, state2));
+            oa.kind = OPT_ADAM;
+            oa.b1 = opt->beta1;
+            oa.b2 = opt->beta2;
+            oa.eps = opt->eps;
+            oa.c1 = (float)(1.0 / (1.0 - std::pow((double)opt->beta1, (double)opt->step)));
+            oa.c2 = (float)(1.0 / (1.0 - std::pow((double)opt->beta2, (double)opt->step)));
+            s1 = state1;
+            s2 = state2;
+            break;
+        }
+        default:
+            set_error("%s: unknown optimiser kind %d", fn, opt->kind);
+            return GCN_E_INVALID_ARG;
+    }
+    return train_step_impl(fn, g, d, P, X, labels, oa, s1, s2, loss_out, grads, ws, ws_bytes,
+                           stream);
 }
 
 }  // extern "C"

@@ -792,11 +792,29 @@ __device__ __forceinline__ float sum_slices(const float* src, int64_t stride, in
     return d;
 }
 
-__global__ __launch_bounds__(256) void sgd_reduce_kernel(SgdProblem p0,
-                                                         SgdProblem p1,
-                                                         int64_t total0,
-                                                         int64_t total,
-                                                         float lr) {
+// One weight's update from its summed gradient d (and its state slot i).
+template <int KIND>
+__device__ __forceinline__ float opt_update(float w, float d, float* s1, float* s2, int64_t i,
+                                            const OptimArgs& o) {
+    if constexpr (KIND == OPT_SGD) {
+        return fmaf(-o.lr, d, w);
+    } else if constexpr (KIND == OPT_MOMENTUM) {
+        const float u = fmaf(o.mu, s1[i], d);
+        s1[i] = u;
+        return fmaf(-o.lr, u, w);
+    } else {
+        const float m = o.b1 * s1[i] + (1.0f - o.b1) * d;
+        const float v = o.b2 * s2[i] + (1.0f - o.b2) * (d * d);
+        s1[i] = m;
+        s2[i] = v;
+        return w - o.lr * (m * o.c1) / (sqrtf(v * o.c2) + o.eps);
+    }
+}
+
+template <int KIND>
+__global__ __launch_bounds__(256) void sgd_reduce_kernel(SgdProblem p0, SgdProblem p1,
+                                                         int64_t total0, int64_t total,
+                                                         OptimArgs o) {
     const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (idx >= total) return;
     const bool second = idx >= total0;
@@ -807,10 +825,10 @@ __global__ __launch_bounds__(256) void sgd_reduce_kernel(SgdProblem p0,
     const float d = sum_slices(src, p.part_stride, p.splits);
     if (m < p.Mw) {
         const int64_t w = (int64_t)m * p.N + nn;
-        p.W[w] = fmaf(-lr, d, p.W[w]);
+        p.W[w] = opt_update<KIND>(p.W[w], d, p.s1, p.s2, w, o);
         if (p.dW_out) p.dW_out[w] = d;
     } else {
-        p.b[nn] = fmaf(-lr, d, p.b[nn]);
+        p.b[nn] = opt_update<KIND>(p.b[nn], d, p.s1b, p.s2b, nn, o);
         if (p.db_out) p.db_out[nn] = d;
     }
 }
@@ -934,7 +952,7 @@ hipError_t launch_gemm(GemmBatch& b, ALayout al, BLayout bl, Epilogue ep, GemmRo
     return hipErrorInvalidValue;
 }
 
-hipError_t launch_sgd_reduce(const SgdProblem* p, int nprob, float lr,
+hipError_t launch_sgd_reduce(const SgdProblem* p, int nprob, const OptimArgs& o,
                              hipStream_t s) {
     if (nprob <= 0) return hipSuccess;
     auto count = [](const SgdProblem& q) {
@@ -946,13 +964,21 @@ hipError_t launch_sgd_reduce(const SgdProblem* p, int nprob, float lr,
     const SgdProblem second = nprob > 1 ? p[1] : p[0];
     const int64_t blocks = (total + 255) / 256;
     double flops = 0, bytes = 0;
+    // state words read and written per weight: momentum 1, Adam 2
+    const double state = o.kind == OPT_ADAM ? 2.0 : o.kind == OPT_MOMENTUM ? 1.0 : 0.0;
     for (int i = 0; i < nprob; ++i) {
         const double cells = (double)(p[i].Mw + (p[i].b ? 1 : 0)) * p[i].N;
-        flops += cells * (p[i].splits + 1.0);
-        bytes += 4.0 * cells * (p[i].splits + 2.0);
+        flops += cells * (p[i].splits + 1.0 + 4.0 * state);
+        bytes += 4.0 * cells * (p[i].splits + 2.0 + 2.0 * state);
     }
     ProfScope prof(s, K_SGD, flops, bytes);
-    sgd_reduce_kernel<<<dim3((unsigned)blocks), dim3(256), 0, s>>>(p[0], second, t0, total, lr);
+    const dim3 grid((unsigned)blocks), block(256);
+    if (o.kind == OPT_ADAM)
+        sgd_reduce_kernel<OPT_ADAM><<<grid, block, 0, s>>>(p[0], second, t0, total, o);
+    else if (o.kind == OPT_MOMENTUM)
+        sgd_reduce_kernel<OPT_MOMENTUM><<<grid, block, 0, s>>>(p[0], second, t0, total, o);
+    else
+        sgd_reduce_kernel<OPT_SGD><<<grid, block, 0, s>>>(p[0], second, t0, total, o);
     return hipGetLastError();
 }
 

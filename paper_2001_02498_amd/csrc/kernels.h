@@ -124,8 +124,21 @@ struct SgdProblem {
     float* b;
     float* dW_out;
     float* db_out;
+    // optimiser state of W and of the bias row (momentum: s1 = velocity;
+    // Adam: s1 = first, s2 = second moment); NULL for plain descent
+    float* s1;
+    float* s2;
+    float* s1b;
+    float* s2b;
 };
-hipError_t launch_sgd_reduce(const SgdProblem* p, int nprob, float lr,
+// Weight update applied where the gradient slices are summed.
+enum OptKind : int32_t { OPT_SGD = 0, OPT_MOMENTUM = 1, OPT_ADAM = 2 };
+struct OptimArgs {
+    int32_t kind;
+    float lr, mu, b1, b2, eps;
+    float c1, c2;   // Adam bias corrections 1 / (1 - b1^t), 1 / (1 - b2^t)
+};
+hipError_t launch_sgd_reduce(const SgdProblem* p, int nprob, const OptimArgs& o,
                              hipStream_t s);
 
 // ---------------------------------------------------------------- loss

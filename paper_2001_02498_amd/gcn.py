@@ -38,6 +38,9 @@ PIPE_PINNED = 1
 PIPE_DEVICE_REDUCE = 2
 ORDER_PAPER = 0
 ORDER_NARROW = 1
+OPT_SGD = 0
+OPT_MOMENTUM = 1
+OPT_ADAM = 2
 AGG_MEAN = 0
 AGG_TRANSPOSED = 1
 ABI_VERSION = 2
@@ -141,6 +144,17 @@ _train_step = _proto("gcn_train_step", [C.POINTER(DGraph), C.POINTER(ModelDesc),
                                         C.POINTER(Params), _vp, _vp, _f32, _vp,
                                         C.POINTER(Params), _vp, _sz, _vp])
 
+
+class Optim(C.Structure):
+    _fields_ = [("kind", _i32), ("step", _i32), ("lr", _f32), ("momentum", _f32),
+                ("beta1", _f32), ("beta2", _f32), ("eps", _f32), ("reserved", _f32)]
+
+
+_train_step_optim = _proto("gcn_train_step_optim",
+                           [C.POINTER(DGraph), C.POINTER(ModelDesc), C.POINTER(Params), _vp,
+                            _vp, C.POINTER(Optim), C.POINTER(Params), C.POINTER(Params), _vp,
+                            C.POINTER(Params), _vp, _sz, _vp])
+
 class ProfileEntry(C.Structure):
     _fields_ = [("kind", _i32), ("launches", _i32), ("name", C.c_char_p),
                 ("total_ms", C.c_double), ("min_ms", C.c_double), ("max_ms", C.c_double),
@@ -173,7 +187,8 @@ EXPORTS = [
     "gcn_graph_image_bytes", "gcn_graph_pack", "gcn_graph_upload", "gcn_graph_describe",
     "gcn_scratch_bytes", "gcn_aggregate", "gcn_layer_fwd", "gcn_classifier_fwd",
     "gcn_loss", "gcn_classifier_bwd", "gcn_layer_bwd", "gcn_workspace_layout",
-    "gcn_workspace_bytes", "gcn_train_step", "gcn_profile_enable", "gcn_profile_disable",
+    "gcn_workspace_bytes", "gcn_train_step", "gcn_train_step_optim", "gcn_profile_enable",
+    "gcn_profile_disable",
     "gcn_profile_read", "gcn_pipeline_create", "gcn_pipeline_submit", "gcn_pipeline_next",
     "gcn_pipeline_release", "gcn_pipeline_destroy",
 ]
@@ -454,6 +469,20 @@ def train_step(dg, desc, params, X, labels, lr, loss_out, ws, grads=None, stream
                        _ptr(labels), float(lr), _ptr(loss_out),
                        C.byref(grads) if grads is not None else None, _ptr(ws), ws.numel(),
                        _stream(stream)))
+
+
+def optim(kind, lr, step=1, momentum=0.9, beta1=0.9, beta2=0.999, eps=1e-8) -> Optim:
+    return Optim(kind, step, lr, momentum, beta1, beta2, eps, 0.0)
+
+
+def train_step_optim(dg, desc, params, X, labels, opt, loss_out, ws, state1=None, state2=None,
+                     grads=None, stream=None):
+    _check(_train_step_optim(C.byref(dg.desc), C.byref(desc), C.byref(params), _ptr(X),
+                             _ptr(labels), C.byref(opt),
+                             C.byref(state1) if state1 is not None else None,
+                             C.byref(state2) if state2 is not None else None, _ptr(loss_out),
+                             C.byref(grads) if grads is not None else None, _ptr(ws),
+                             ws.numel(), _stream(stream)))
 
 
 # ------------------------------------------------------------ launch timing
