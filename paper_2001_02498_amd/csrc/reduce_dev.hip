@@ -268,18 +268,34 @@ __global__ __launch_bounds__(kCountThreads) void count_pairs_kernel(
 }
 
 // ------------------------------------------------------------ Algorithm 2
+// Workgroup barrier for LDS traffic only: waits for this wave's LDS
+// operations but leaves its global loads and stores in flight (the key
+// prefetch and the pair stores of the greedy scan), which __syncthreads
+// would drain at every barrier.
+__device__ __forceinline__ void lds_barrier() {
+    asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+}
+
+// set bits of m in the lanes below this one
+__device__ __forceinline__ int lanes_below(uint64_t m) {
+    return (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32),
+                                          __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
+}
+
 // The greedy matching over keys sorted ascending, i.e. weight descending,
 // then (x, y): a pair is taken when neither endpoint is used, while fewer
 // than `budget` pairs were taken this round. Blocks of keys are first
-// filtered in parallel against the used set; one thread then takes the
-// survivors in order. Taken pairs go to pairs[2 i], pairs[2 i + 1].
+// filtered in parallel against the used set; one wavefront then takes the
+// survivors in order, 64 at a time. Taken pairs go to pairs[2 i],
+// pairs[2 i + 1].
+
 __global__ __launch_bounds__(kGreedyThreads) void greedy_kernel(
     const uint64_t* __restrict__ keys, int64_t nc, int ncols, int64_t budget,
     int32_t* __restrict__ pairs, RoundCounters* rc) {
     __shared__ uint32_t used[kMaxIds / 32];
     __shared__ uint64_t surv[2][kGreedyBlock];
     __shared__ int32_t wave_sum[kGreedyThreads / 64];
-    __shared__ int nsurv, stop;
+    __shared__ int stop;
     __shared__ long long s_taken, s_wsum;
     const int t = threadIdx.x, lane = t % 64, wave = t / 64;
     for (int i = t; i < (ncols + 31) / 32; i += kGreedyThreads) used[i] = 0;
@@ -288,7 +304,7 @@ __global__ __launch_bounds__(kGreedyThreads) void greedy_kernel(
         s_taken = 0;
         s_wsum = 0;
     }
-    __syncthreads();
+    lds_barrier();
     auto is_used = [&](uint32_t v) { return (used[v >> 5] >> (v & 31)) & 1u; };
     // both endpoints free (no short-circuit: no branch, both reads in flight)
     auto free_pair = [&](uint64_t key) {
@@ -296,59 +312,51 @@ __global__ __launch_bounds__(kGreedyThreads) void greedy_kernel(
         return (is_used(x) | is_used(y)) == 0u;
     };
     // Keys of the next block are loaded while this one is filtered and
-    // taken. Loads are unconditional (clamped index, the key replaced
-    // afterwards) so no branch makes the compiler wait for them early.
-    auto load_key = [&](int64_t i) {
-        const uint64_t v = keys[i < nc ? i : nc - 1];
-        return i < nc ? v : ~0ull;
-    };
-    uint64_t k_next[kGreedyPer];
+    // taken. Loads are unconditional (clamped index); a key past nc is
+    // replaced by all ones only when its block is used, so nothing waits
+    // for a load before then.
+    auto load_raw = [&](int64_t i) { return keys[i < nc ? i : nc - 1]; };
+    uint64_t k_raw[kGreedyPer];
 #pragma unroll
-    for (int j = 0; j < kGreedyPer; ++j) k_next[j] = load_key((int64_t)t * kGreedyPer + j);
+    for (int j = 0; j < kGreedyPer; ++j) k_raw[j] = load_raw((int64_t)t * kGreedyPer + j);
     for (int64_t base = 0; base < nc; base += kGreedyBlock) {
         uint64_t k[kGreedyPer];
-        int alive = 0;
         bool live[kGreedyPer];
 #pragma unroll
         for (int j = 0; j < kGreedyPer; ++j) {
-            k[j] = k_next[j];
-            k_next[j] = load_key(base + kGreedyBlock + (int64_t)t * kGreedyPer + j);
+            const int64_t i = base + (int64_t)t * kGreedyPer + j;
+            k[j] = i < nc ? k_raw[j] : ~0ull;
+            k_raw[j] = load_raw(i + kGreedyBlock);
         }
 #pragma unroll
         for (int j = 0; j < kGreedyPer; ++j) {
             // keys past nc are all ones: their ids exceed ncols
             const uint32_t x = (uint32_t)(k[j] >> 20) & 0xFFFFFu, y = (uint32_t)k[j] & 0xFFFFFu;
             live[j] = (x < (uint32_t)ncols) & (y < (uint32_t)ncols) & free_pair(k[j]);
-            alive += live[j];
         }
-        // survivors keep their order: exclusive prefix over threads
-        int incl = alive;
-        for (int off = 1; off < 64; off <<= 1) {
-            const int v = __shfl_up(incl, off);
-            if (lane >= off) incl += v;
+        // survivors keep their order (thread-major, then j): the prefix
+        // inside a wave from one ballot per key slot, across waves from the
+        // per-wave totals
+        int excl = 0, wtot = 0;
+#pragma unroll
+        for (int j = 0; j < kGreedyPer; ++j) {
+            const uint64_t mj = __ballot(live[j]);
+            excl += lanes_below(mj);
+            wtot += __popcll(mj);
         }
-        if (lane == 63) wave_sum[wave] = incl;
-        __syncthreads();
-        if (t == 0) {
-            int run = 0;
-            for (int w = 0; w < kGreedyThreads / 64; ++w) {
-                const int v = wave_sum[w];
-                wave_sum[w] = run;
-                run += v;
-            }
-            nsurv = run;
+        if (lane == 0) wave_sum[wave] = wtot;
+        lds_barrier();
+        int before = 0, nsurv = 0;
+        for (int w = 0; w < kGreedyThreads / 64; ++w) {
+            const int v = wave_sum[w];
+            before += w < wave ? v : 0;
+            nsurv += v;
         }
-        __syncthreads();
-        int wpos = wave_sum[wave] + incl - alive;
+        int wpos = before + excl;
 #pragma unroll
         for (int j = 0; j < kGreedyPer; ++j)
             if (live[j]) surv[0][wpos++] = k[j];
-        __syncthreads();
-        // Wave 0 takes the survivors in order, 64 at a time (the first live
-        // one is taken, the others drop if they touch its endpoints), a
-        // burst of kGreedyBurst at a time; between bursts all threads drop
-        // the remaining survivors that now have a used endpoint, so wave 0
-        // only walks pairs that are still possible.
+        lds_barrier();
         int buf = 0, pos = 0, cnt = nsurv;
         while (pos < cnt) {
             const uint64_t* S = surv[buf];
@@ -361,7 +369,13 @@ __global__ __launch_bounds__(kGreedyThreads) void greedy_kernel(
                     const uint64_t kv = S[si < end ? si : end - 1];
                     const uint64_t key = si < end ? kv : ~0ull;
                     const uint32_t x = (uint32_t)(key >> 20) & 0xFFFFFu, y = (uint32_t)key & 0xFFFFFu;
+                    const uint32_t w = 0xFFFFu - (uint32_t)(key >> 40);
                     bool live = (si < end) & free_pair(kv);
+                    bool took = false;
+                    const long long first = taken;
+                    // the first live pair is taken; later ones sharing an
+                    // endpoint with it drop (register compares only: the
+                    // used set and the output follow after the chunk)
                     uint64_t m = __ballot(live);
                     while (m) {
                         if (taken >= budget) {
@@ -369,18 +383,21 @@ __global__ __launch_bounds__(kGreedyThreads) void greedy_kernel(
                             break;
                         }
                         const int j = __ffsll((long long)m) - 1;
-                        const uint64_t kj = __shfl(key, j);
-                        const uint32_t xj = (uint32_t)(kj >> 20) & 0xFFFFFu, yj = (uint32_t)kj & 0xFFFFFu;
-                        if (lane == 0) {
-                            used[xj >> 5] |= 1u << (xj & 31);
-                            used[yj >> 5] |= 1u << (yj & 31);
-                            pairs[2 * taken] = (int32_t)xj;
-                            pairs[2 * taken + 1] = (int32_t)yj;
-                        }
-                        wsum += 0xFFFFu - (uint32_t)(kj >> 40);
+                        const uint32_t xj = __builtin_amdgcn_readlane(x, j);
+                        const uint32_t yj = __builtin_amdgcn_readlane(y, j);
+                        wsum += __builtin_amdgcn_readlane(w, j);
+                        took |= lane == j;
                         ++taken;
                         live = live && lane > j && x != xj && x != yj && y != xj && y != yj;
                         m = __ballot(live);
+                    }
+                    const uint64_t tm = __ballot(took);
+                    if (took) {
+                        const long long r = first + lanes_below(tm);
+                        atomicOr(&used[x >> 5], 1u << (x & 31));
+                        atomicOr(&used[y >> 5], 1u << (y & 31));
+                        pairs[2 * r] = (int32_t)x;
+                        pairs[2 * r + 1] = (int32_t)y;
                     }
                 }
                 if (lane == 0) {
@@ -389,7 +406,7 @@ __global__ __launch_bounds__(kGreedyThreads) void greedy_kernel(
                     if (halt || taken >= budget) stop = 1;
                 }
             }
-            __syncthreads();
+            lds_barrier();
             if (stop) break;
             pos = end;
             if (cnt - pos > kGreedyBurst) {
@@ -416,7 +433,7 @@ __global__ __launch_bounds__(kGreedyThreads) void greedy_kernel(
                     if (lane >= off) inc += v;
                 }
                 if (lane == 63) wave_sum[wave] = inc;
-                __syncthreads();
+                lds_barrier();
                 int before = 0, total = 0;
                 for (int w = 0; w < kGreedyThreads / 64; ++w) {
                     if (w < wave) before += wave_sum[w];
@@ -427,13 +444,13 @@ __global__ __launch_bounds__(kGreedyThreads) void greedy_kernel(
 #pragma unroll
                 for (int j = 0; j < kGreedyPer; ++j)
                     if (lv[j]) D[o++] = kk[j];
-                __syncthreads();
+                lds_barrier();
                 buf ^= 1;
                 pos = 0;
                 cnt = total;
             }
         }
-        __syncthreads();
+        lds_barrier();
         if (stop) break;
     }
     if (t == 0) {
