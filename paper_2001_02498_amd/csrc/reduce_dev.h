@@ -23,8 +23,8 @@ struct DeviceReduceResult {
 int redundancy_reduce_device_bytes(const int32_t* rowptr, int64_t n, const gcn_rr_params* p,
                                    size_t* bytes);
 
-// Runs the rounds on stream s (synchronising it after the pair counting
-// and the matching of every round) and downloads the reduced lists.
+// Runs the rounds on stream s (synchronising it once per round, after the
+// pair counting) and downloads the reduced lists.
 int redundancy_reduce_device(const int32_t* rowptr, const int32_t* col, int64_t n,
                              const gcn_rr_params* p, void* ws, size_t ws_bytes, hipStream_t s,
                              DeviceReduceResult* out);

@@ -17,11 +17,13 @@
 //                list are replaced by the pair's new id; kept entries keep
 //                their order and the new ids (all larger) follow in
 //                increasing order.
-// The host drives the rounds and reads a few counters back after the pair
-// counting and after the matching (the sort needs the candidate count).
+// The host enqueues the rounds back to back; the kernels read the ids and
+// the budget left from a small device-side state, so the host waits once
+// per round, after the pair counting (the sort needs the candidate count).
 #include <rocprim/device/device_radix_sort.hpp>
 
 #include <algorithm>
+#include <climits>
 #include <cstring>
 #include <new>
 #include <vector>
@@ -45,8 +47,18 @@ struct RoundCounters {
     unsigned long long ncand;   // candidates emitted (may exceed capacity: overflow)
     long long taken, wsum;
     unsigned long long num_add;
-    int exhausted;
-    int error;                  // 1: candidate capacity, 2: id out of range
+    long long nnz;              // list entries after the round's rewrite
+};
+
+// Device-side state of a reduction: the rounds run back to back on the
+// stream, each reading the ids issued so far from here, so the host waits
+// only once per round (for the candidate count the sort needs).
+struct DevState {
+    long long naux;             // pairs taken in all rounds so far
+    int done;                   // a round took no pair, or the budget is spent
+    int error;                  // 1: candidate capacity, 2: id out of range,
+                                // 3: ids reach the 16-bit counter range
+    RoundCounters round[GCN_MAX_ROUNDS];
 };
 
 __device__ __forceinline__ uint64_t cand_key(uint32_t w, uint32_t x, uint32_t y) {
@@ -59,7 +71,8 @@ __device__ __forceinline__ uint64_t cand_key(uint32_t w, uint32_t x, uint32_t y)
 // in holds list lengths)
 __global__ __launch_bounds__(kScanThreads) void scan_kernel(const int32_t* __restrict__ in,
                                                             int32_t* __restrict__ out, int len,
-                                                            unsigned long long* num_add) {
+                                                            unsigned long long* num_add,
+                                                            long long* total) {
     __shared__ int32_t part[kScanThreads];
     __shared__ unsigned long long adds[kScanThreads / 64];
     const int t = threadIdx.x;
@@ -94,6 +107,7 @@ __global__ __launch_bounds__(kScanThreads) void scan_kernel(const int32_t* __res
         run += in[i];
         out[i + 1] = run;
     }
+    if (total && t == kScanThreads - 1) *total = part[t];
 }
 
 __global__ void fill_kernel(int32_t* __restrict__ p, int32_t v, int64_t len) {
@@ -103,18 +117,18 @@ __global__ void fill_kernel(int32_t* __restrict__ p, int32_t v, int64_t len) {
 
 // ------------------------------------------------------------ Algorithm 1
 // one wavefront per list
-__global__ __launch_bounds__(kBlock) void tcount_kernel(int n, int ncols,
-                                                        const int32_t* __restrict__ rowptr,
+__global__ __launch_bounds__(kBlock) void tcount_kernel(int n, const int32_t* __restrict__ rowptr,
                                                         const int32_t* __restrict__ col,
                                                         int32_t* __restrict__ tcnt,
-                                                        RoundCounters* rc) {
+                                                        DevState* st) {
     const int w = blockIdx.x * (kBlock / 64) + threadIdx.x / 64;
     const int lane = threadIdx.x % 64;
-    if (w >= n) return;
+    if (w >= n || st->done) return;
+    const int ncols = n + (int)st->naux;
     for (int e = rowptr[w] + lane; e < rowptr[w + 1]; e += 64) {
         const int c = col[e];
         if (c < 0 || c >= ncols) {
-            rc->error = 2;
+            st->error = 2;
             continue;
         }
         atomicAdd(&tcnt[c], 1);
@@ -123,15 +137,16 @@ __global__ __launch_bounds__(kBlock) void tcount_kernel(int n, int ncols,
 
 // tlist[k] / tpos[k]: the list holding id c and c's position in it, for k in
 // [tptr[c], tptr[c + 1]) (any order inside: the counts do not depend on it)
-__global__ __launch_bounds__(kBlock) void tfill_kernel(int n, int ncols,
-                                                       const int32_t* __restrict__ rowptr,
+__global__ __launch_bounds__(kBlock) void tfill_kernel(int n, const int32_t* __restrict__ rowptr,
                                                        const int32_t* __restrict__ col,
                                                        int32_t* __restrict__ tcur,
                                                        int32_t* __restrict__ tlist,
-                                                       int32_t* __restrict__ tpos) {
+                                                       int32_t* __restrict__ tpos,
+                                                       const DevState* st) {
     const int w = blockIdx.x * (kBlock / 64) + threadIdx.x / 64;
     const int lane = threadIdx.x % 64;
-    if (w >= n) return;
+    if (w >= n || st->done) return;
+    const int ncols = n + (int)st->naux;
     const int b = rowptr[w];
     for (int e = b + lane; e < rowptr[w + 1]; e += 64) {
         const int c = col[e];
@@ -153,14 +168,21 @@ constexpr int kCountThreads = 512;
 constexpr int kCountStage = 1024;
 
 __global__ __launch_bounds__(kCountThreads) void count_pairs_kernel(
-    int ncols, int theta, const int32_t* __restrict__ rowptr, const int32_t* __restrict__ col,
+    int n, int theta, const int32_t* __restrict__ rowptr, const int32_t* __restrict__ col,
     const int32_t* __restrict__ tptr, const int32_t* __restrict__ tlist,
     const int32_t* __restrict__ tpos, uint64_t* __restrict__ cand, int64_t cap,
-    RoundCounters* rc) {
+    DevState* st, int round) {
     extern __shared__ uint32_t cnt[];
     __shared__ int32_t s_start[kCountStage];
     __shared__ int32_t s_off[kCountStage + 1];
     __shared__ int32_t s_wave[kCountThreads / 64];
+    if (st->done) return;
+    const int ncols = n + (int)st->naux;
+    if (ncols >= kMaxIds) {   // pair keys hold 16-bit ids
+        if (threadIdx.x == 0 && blockIdx.x == 0) st->error = 3;
+        return;
+    }
+    RoundCounters* rc = &st->round[round];
     const int nw = (ncols + 1) / 2;
     const int t = threadIdx.x, lane = t % 64, wave = t / 64;
     for (int i = t; i < nw; i += kCountThreads) cnt[i] = 0;
@@ -259,7 +281,7 @@ __global__ __launch_bounds__(kCountThreads) void count_pairs_kernel(
                     cand[slot] = cand_key((v >> (16 * h)) & 0xFFFFu, (uint32_t)x,
                                           (uint32_t)(2 * wd + h));
                 else
-                    rc->error = 1;
+                    st->error = 1;
                 ++slot;
             }
         }
@@ -290,17 +312,24 @@ __device__ __forceinline__ int lanes_below(uint64_t m) {
 // pairs[2 i + 1].
 
 __global__ __launch_bounds__(kGreedyThreads) void greedy_kernel(
-    const uint64_t* __restrict__ keys, int64_t nc, int ncols, int64_t budget,
-    int32_t* __restrict__ pairs, RoundCounters* rc) {
+    const uint64_t* __restrict__ keys, int64_t nc, int n, int64_t max_aux, int64_t pairs_cap,
+    int32_t* __restrict__ all_pairs, DevState* st, int round) {
     __shared__ uint32_t used[kMaxIds / 32];
     __shared__ uint64_t surv[2][kGreedyBlock];
     __shared__ int32_t wave_sum[kGreedyThreads / 64];
     __shared__ int stop;
     __shared__ long long s_taken, s_wsum;
     const int t = threadIdx.x, lane = t % 64, wave = t / 64;
+    // this round's ids and budget follow from the pairs of earlier rounds
+    const long long naux0 = st->naux;
+    const int ncols = n + (int)naux0;
+    const long long budget_left = max_aux < 0 ? LLONG_MAX : max_aux - naux0;
+    const long long budget = min(budget_left, (long long)pairs_cap - naux0);
+    int32_t* __restrict__ pairs = all_pairs + 2 * naux0;
+    RoundCounters* rc = &st->round[round];
     for (int i = t; i < (ncols + 31) / 32; i += kGreedyThreads) used[i] = 0;
     if (t == 0) {
-        stop = 0;
+        stop = budget <= 0;
         s_taken = 0;
         s_wsum = 0;
     }
@@ -319,7 +348,7 @@ __global__ __launch_bounds__(kGreedyThreads) void greedy_kernel(
     uint64_t k_raw[kGreedyPer];
 #pragma unroll
     for (int j = 0; j < kGreedyPer; ++j) k_raw[j] = load_raw((int64_t)t * kGreedyPer + j);
-    for (int64_t base = 0; base < nc; base += kGreedyBlock) {
+    for (int64_t base = 0; base < nc && !stop; base += kGreedyBlock) {
         uint64_t k[kGreedyPer];
         bool live[kGreedyPer];
 #pragma unroll
@@ -456,20 +485,26 @@ __global__ __launch_bounds__(kGreedyThreads) void greedy_kernel(
     if (t == 0) {
         rc->taken = s_taken;
         rc->wsum = s_wsum;
-        rc->exhausted = s_taken >= budget ? 1 : 0;
+        st->naux = naux0 + s_taken;
+        // no pair taken, or the budget spent: the later rounds do nothing
+        st->done = s_taken == 0 || s_taken >= budget_left;
     }
 }
 
 // ------------------------------------------------------------ Algorithm 3
-__global__ void set_partner_kernel(const int32_t* __restrict__ pairs, int64_t taken,
-                                   int32_t id0, int32_t* __restrict__ partner,
-                                   int32_t* __restrict__ newid, int reset) {
+// the pairs of round `round` (the last `taken` of all pairs so far)
+__global__ void set_partner_kernel(const int32_t* __restrict__ all_pairs, int n,
+                                   const DevState* st, int round,
+                                   int32_t* __restrict__ partner, int32_t* __restrict__ newid,
+                                   int reset) {
     const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    const long long taken = st->round[round].taken, naux0 = st->naux - taken;
     if (i >= taken) return;
+    const int32_t* pairs = all_pairs + 2 * naux0;
     const int32_t x = pairs[2 * i], y = pairs[2 * i + 1];
     partner[x] = reset ? -1 : y;
     partner[y] = reset ? -1 : x;
-    newid[x] = newid[y] = reset ? -1 : id0 + (int32_t)i;
+    newid[x] = newid[y] = reset ? -1 : n + (int32_t)(naux0 + i);
 }
 
 // One workgroup per list; the list's ids are marked in an LDS bitmap
@@ -512,10 +547,12 @@ __device__ __forceinline__ int block_prefix(bool f, int32_t* s_wave, int* total)
 
 // new length of every list
 __global__ __launch_bounds__(kRowThreads) void rewrite_count_kernel(
-    int n, int ncols, const int32_t* __restrict__ rowptr, const int32_t* __restrict__ col,
-    const int32_t* __restrict__ partner, int32_t* __restrict__ rowlen) {
+    int n, const DevState* st, int round, const int32_t* __restrict__ rowptr,
+    const int32_t* __restrict__ col, const int32_t* __restrict__ partner,
+    int32_t* __restrict__ rowlen) {
     extern __shared__ uint32_t bits[];
     __shared__ int32_t s_wave[kRowThreads / 64];
+    const int ncols = n + (int)(st->naux - st->round[round].taken);   // ids before the round
     const int w = blockIdx.x;
     const int b = rowptr[w], d = rowptr[w + 1] - b;
     const int32_t* row = col + b;
@@ -539,13 +576,14 @@ __global__ __launch_bounds__(kRowThreads) void rewrite_count_kernel(
 // kept entries in order, then the new ids in increasing order (each placed
 // by its rank among the list's new ids)
 __global__ __launch_bounds__(kRowThreads) void rewrite_fill_kernel(
-    int n, int ncols, const int32_t* __restrict__ rowptr, const int32_t* __restrict__ col,
-    const int32_t* __restrict__ partner, const int32_t* __restrict__ newid,
-    const int32_t* __restrict__ rowptr_new, int32_t* __restrict__ col_new,
-    int32_t* __restrict__ scratch) {
+    int n, const DevState* st, int round, const int32_t* __restrict__ rowptr,
+    const int32_t* __restrict__ col, const int32_t* __restrict__ partner,
+    const int32_t* __restrict__ newid, const int32_t* __restrict__ rowptr_new,
+    int32_t* __restrict__ col_new, int32_t* __restrict__ scratch) {
     extern __shared__ uint32_t bits[];
     __shared__ int32_t s_wave[kRowThreads / 64];
     __shared__ int32_t ids[kRowIds];
+    const int ncols = n + (int)(st->naux - st->round[round].taken);   // ids before the round
     const int w = blockIdx.x;
     const int b = rowptr[w], d = rowptr[w + 1] - b;
     const int out = rowptr_new[w], len = rowptr_new[w + 1] - out;
@@ -643,7 +681,7 @@ int plan(const int32_t* rowptr, int64_t n, const gcn_rr_params* p, DevPlan* dp) 
     dp->keys_in = take(8 * (size_t)dp->cand_cap);
     dp->keys_out = take(8 * (size_t)dp->cand_cap);
     dp->pairs = take(8 * (size_t)std::max<int64_t>(dp->pairs_cap, 1));
-    dp->counters = take(sizeof(RoundCounters));
+    dp->counters = take(sizeof(DevState));
     dp->sort = take(dp->sort_tmp);
     dp->total = off;
     return GCN_OK;
@@ -690,7 +728,7 @@ int redundancy_reduce_device(const int32_t* rowptr_h, const int32_t* col_h, int6
     uint64_t* keys_in = reinterpret_cast<uint64_t*>(base + dp.keys_in);
     uint64_t* keys_out = reinterpret_cast<uint64_t*>(base + dp.keys_out);
     int32_t* pairs = I(dp.pairs);
-    RoundCounters* dctr = reinterpret_cast<RoundCounters*>(base + dp.counters);
+    DevState* dst = reinterpret_cast<DevState*>(base + dp.counters);
     auto fail = [&](hipError_t e, const char* what) {
         set_error("gcn_redundancy_reduce_device: %s: HIP error %d (%s)", what, (int)e,
                   hipGetErrorString(e));
@@ -705,7 +743,7 @@ int redundancy_reduce_device(const int32_t* rowptr_h, const int32_t* col_h, int6
     const int64_t nnz = dp.nnz;
     out->round_offsets.assign(1, 0);
     out->stats.clear();
-    if (n == 0 || nnz == 0 || p->max_rounds == 0) {   // no pairs: the lists as given
+    if (n == 0 || nnz == 0 || p->max_rounds == 0 || p->max_aux == 0) {   // no pairs: the lists as given
         out->naux = 0;
         out->rowptr.assign(rowptr_h, rowptr_h + n + 1);
         out->col.assign(col_h, col_h + nnz);
@@ -714,95 +752,103 @@ int redundancy_reduce_device(const int32_t* rowptr_h, const int32_t* col_h, int6
     }
     GCN_DR(hipMemcpyAsync(rowptr[0], rowptr_h, 4 * (size_t)(n + 1), hipMemcpyHostToDevice, s),
            "upload");
-    if (nnz) GCN_DR(hipMemcpyAsync(col[0], col_h, 4 * (size_t)nnz, hipMemcpyHostToDevice, s), "upload");
+    GCN_DR(hipMemcpyAsync(col[0], col_h, 4 * (size_t)nnz, hipMemcpyHostToDevice, s), "upload");
+    GCN_DR(hipMemsetAsync(dst, 0, sizeof(DevState), s), "state");
     fill_kernel<<<items_grid(dp.ncols_cap), kBlock, 0, s>>>(I(dp.partner), -1, dp.ncols_cap);
     fill_kernel<<<items_grid(dp.ncols_cap), kBlock, 0, s>>>(I(dp.newid), -1, dp.ncols_cap);
     GCN_DR(hipGetLastError(), "init");
 
-    int64_t naux = 0;
-    int32_t ncols = (int32_t)n;
-    int cur = 0;
-    int64_t cur_nnz = nnz;
-    RoundCounters hc;
+    // The host knows the ids exactly at each round's wait (after the pair
+    // counting); the round after may add at most its budget of new ids.
+    int64_t naux_known = 0;
+    int64_t ncols_ub = n;   // bound on the ids the next round sees
+    int cur = 0, rounds = 0;
+    DevState hs;
     for (int round = 0; round < p->max_rounds; ++round) {
-        const int64_t budget_left = p->max_aux < 0 ? INT64_MAX : p->max_aux - naux;
-        if (budget_left <= 0) break;
-        if ((int64_t)ncols >= kMaxIds) {
-            set_error("gcn_redundancy_reduce_device: %d vertex ids reached; the device "
-                      "reduction counts fewer than %d",
-                      ncols, kMaxIds);
-            return GCN_E_UNSUPPORTED;
-        }
-        std::memset(&hc, 0, sizeof(hc));
-        GCN_DR(hipMemcpyAsync(dctr, &hc, sizeof(hc), hipMemcpyHostToDevice, s), "counters");
+        const int32_t nc_ub = (int32_t)std::min<int64_t>(ncols_ub, dp.ncols_cap);
         // Algorithm 1: transposed index, then pair counts per id
-        fill_kernel<<<items_grid(ncols), kBlock, 0, s>>>(I(dp.tcur), 0, ncols);
-        tcount_kernel<<<waves_grid(n), kBlock, 0, s>>>((int)n, ncols, rowptr[cur], col[cur],
-                                                        I(dp.tcur), dctr);
-        scan_kernel<<<1, kScanThreads, 0, s>>>(I(dp.tcur), I(dp.tptr), ncols, nullptr);
-        GCN_DR(hipMemcpyAsync(I(dp.tcur), I(dp.tptr), 4 * (size_t)ncols, hipMemcpyDeviceToDevice, s),
+        fill_kernel<<<items_grid(nc_ub), kBlock, 0, s>>>(I(dp.tcur), 0, nc_ub);
+        tcount_kernel<<<waves_grid(n), kBlock, 0, s>>>((int)n, rowptr[cur], col[cur], I(dp.tcur),
+                                                        dst);
+        scan_kernel<<<1, kScanThreads, 0, s>>>(I(dp.tcur), I(dp.tptr), nc_ub, nullptr, nullptr);
+        GCN_DR(hipMemcpyAsync(I(dp.tcur), I(dp.tptr), 4 * (size_t)nc_ub, hipMemcpyDeviceToDevice, s),
                "cursor");
-        tfill_kernel<<<waves_grid(n), kBlock, 0, s>>>((int)n, ncols, rowptr[cur], col[cur],
-                                                       I(dp.tcur), I(dp.tlist), I(dp.tpos));
-        const size_t lds = 4 * (size_t)((ncols + 1) / 2);
+        tfill_kernel<<<waves_grid(n), kBlock, 0, s>>>((int)n, rowptr[cur], col[cur], I(dp.tcur),
+                                                       I(dp.tlist), I(dp.tpos), dst);
+        const size_t lds = 4 * (size_t)((std::min<int64_t>(nc_ub, kMaxIds) + 1) / 2);
         if (lds > 48 * 1024)
             GCN_DR(hipFuncSetAttribute((const void*)count_pairs_kernel,
                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds),
                    "pair counting LDS");
-        const unsigned grid = (unsigned)std::min<int64_t>(ncols, 4096);
-        count_pairs_kernel<<<grid, kCountThreads, lds, s>>>(ncols, p->theta, rowptr[cur], col[cur],
-                                                     I(dp.tptr), I(dp.tlist), I(dp.tpos),
-                                                     keys_in, dp.cand_cap, dctr);
+        const unsigned grid = (unsigned)std::min<int64_t>(nc_ub, 4096);
+        count_pairs_kernel<<<grid, kCountThreads, lds, s>>>((int)n, p->theta, rowptr[cur],
+                                                            col[cur], I(dp.tptr), I(dp.tlist),
+                                                            I(dp.tpos), keys_in, dp.cand_cap,
+                                                            dst, round);
         GCN_DR(hipGetLastError(), "pair counting");
-        GCN_DR(hipMemcpyAsync(&hc, dctr, sizeof(hc), hipMemcpyDeviceToHost, s), "counters");
+        // the one wait of the round: the sort needs the candidate count
+        GCN_DR(hipMemcpyAsync(&hs, dst, sizeof(hs), hipMemcpyDeviceToHost, s), "state");
         GCN_DR(hipStreamSynchronize(s), "pair counting");
-        if (hc.error) {
+        if (hs.error) {
             set_error("gcn_redundancy_reduce_device: %s in round %d",
-                      hc.error == 1 ? "candidate capacity exceeded" : "list id out of range",
+                      hs.error == 1   ? "candidate capacity exceeded"
+                      : hs.error == 2 ? "list id out of range"
+                                      : "ids reach the device reduction's 16-bit range",
                       round + 1);
-            return GCN_E_INTERNAL;
+            return hs.error == 3 ? GCN_E_UNSUPPORTED : GCN_E_INTERNAL;
         }
-        const int64_t nc = (int64_t)hc.ncand;
+        if (hs.done) break;   // the previous round ended the reduction
+        naux_known = hs.naux;
+        const int64_t nc = (int64_t)hs.round[round].ncand;
         if (nc == 0) break;
         // Algorithm 2: sort by (weight descending, x, y), then the greedy scan
         size_t tmp = dp.sort_tmp;
         GCN_DR(rocprim::radix_sort_keys(base + dp.sort, tmp, keys_in, keys_out, (unsigned)nc, 0,
                                         56, s),
                "candidate sort");
-        const int64_t budget = std::min<int64_t>(budget_left, dp.pairs_cap - naux);
-        greedy_kernel<<<1, kGreedyThreads, 0, s>>>(keys_out, nc, ncols, budget,
-                                                   pairs + 2 * naux, dctr);
+        greedy_kernel<<<1, kGreedyThreads, 0, s>>>(keys_out, nc, (int)n, p->max_aux,
+                                                   dp.pairs_cap, pairs, dst, round);
         GCN_DR(hipGetLastError(), "matching");
-        GCN_DR(hipMemcpyAsync(&hc, dctr, sizeof(hc), hipMemcpyDeviceToHost, s), "counters");
-        GCN_DR(hipStreamSynchronize(s), "matching");
-        const int64_t taken = hc.taken;
-        if (taken == 0) break;
-        const bool exhausted = hc.exhausted && taken >= budget_left;
-        // Algorithm 3: rewrite every list
+        // Algorithm 3: rewrite every list (a round that took no pair
+        // copies the lists unchanged)
+        const int64_t budget_ub =
+            std::min<int64_t>(p->max_aux < 0 ? INT64_MAX : p->max_aux - naux_known,
+                              dp.pairs_cap - naux_known);
         const int nxt = cur ^ 1;
-        set_partner_kernel<<<items_grid(taken), kBlock, 0, s>>>(pairs + 2 * naux, taken, ncols,
-                                                                I(dp.partner), I(dp.newid), 0);
-        const size_t bits = 4 * (size_t)((ncols + 31) / 32);
+        const size_t bits = 4 * (size_t)((std::min<int64_t>(n + naux_known, kMaxIds) + 31) / 32);
+        set_partner_kernel<<<items_grid(budget_ub), kBlock, 0, s>>>(pairs, (int)n, dst, round,
+                                                                    I(dp.partner), I(dp.newid), 0);
         rewrite_count_kernel<<<(unsigned)n, kRowThreads, bits, s>>>(
-            (int)n, ncols, rowptr[cur], col[cur], I(dp.partner), I(dp.rowlen));
-        scan_kernel<<<1, kScanThreads, 0, s>>>(I(dp.rowlen), rowptr[nxt], (int)n, &dctr->num_add);
+            (int)n, dst, round, rowptr[cur], col[cur], I(dp.partner), I(dp.rowlen));
+        scan_kernel<<<1, kScanThreads, 0, s>>>(I(dp.rowlen), rowptr[nxt], (int)n,
+                                               &dst->round[round].num_add,
+                                               &dst->round[round].nnz);
         rewrite_fill_kernel<<<(unsigned)n, kRowThreads, bits, s>>>(
-            (int)n, ncols, rowptr[cur], col[cur], I(dp.partner), I(dp.newid), rowptr[nxt],
+            (int)n, dst, round, rowptr[cur], col[cur], I(dp.partner), I(dp.newid), rowptr[nxt],
             col[nxt], I(dp.scratch));
-        set_partner_kernel<<<items_grid(taken), kBlock, 0, s>>>(pairs + 2 * naux, taken, ncols,
-                                                                I(dp.partner), I(dp.newid), 1);
+        set_partner_kernel<<<items_grid(budget_ub), kBlock, 0, s>>>(pairs, (int)n, dst, round,
+                                                                    I(dp.partner), I(dp.newid), 1);
         GCN_DR(hipGetLastError(), "rewrite");
-        int32_t new_nnz = 0;
-        GCN_DR(hipMemcpyAsync(&new_nnz, rowptr[nxt] + n, 4, hipMemcpyDeviceToHost, s), "nnz");
-        GCN_DR(hipMemcpyAsync(&hc, dctr, sizeof(hc), hipMemcpyDeviceToHost, s), "counters");
-        GCN_DR(hipStreamSynchronize(s), "rewrite");
-        naux += taken;
-        ncols += (int32_t)taken;
         cur = nxt;
-        cur_nnz = new_nnz;
+        rounds = round + 1;
+        ncols_ub = n + naux_known + budget_ub;
+    }
+    // the rounds' results (a round that took nothing ends the list)
+    GCN_DR(hipMemcpyAsync(&hs, dst, sizeof(hs), hipMemcpyDeviceToHost, s), "state");
+    GCN_DR(hipStreamSynchronize(s), "rounds");
+    int64_t naux = 0, cur_nnz = nnz;
+    for (int r = 0; r < rounds; ++r) {
+        const RoundCounters& rc = hs.round[r];
+        if (rc.taken == 0) break;
+        naux += rc.taken;
+        cur_nnz = rc.nnz;
         out->round_offsets.push_back((int32_t)naux);
-        out->stats.push_back({taken, hc.wsum, cur_nnz, (int64_t)hc.num_add});
-        if (exhausted) break;
+        out->stats.push_back({rc.taken, rc.wsum, rc.nnz, (int64_t)rc.num_add});
+    }
+    if (naux != hs.naux) {
+        set_error("gcn_redundancy_reduce_device: pair count mismatch (%lld vs %lld)",
+                  (long long)naux, (long long)hs.naux);
+        return GCN_E_INTERNAL;
     }
     out->naux = (int32_t)naux;
     out->rowptr.resize(n + 1);
