@@ -71,6 +71,9 @@ def parse():
                     help="with --trace-summary: the arguments the traced run was given")
     ap.add_argument("--bench-line", help="with --trace-summary: the JSON line the traced run "
                                          "printed (event timings shown beside the trace)")
+    ap.add_argument("--l2-summary", metavar="COUNTER_CSV",
+                    help="no GPU: turn a rocprofv3 TCC_HIT_sum / TCC_MISS_sum counter file of "
+                         "this script into the L2 hit-rate table under profiles/")
     ap.add_argument("--pmc-summary", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
                     help="no GPU: turn two rocprofv3 --pmc counter files (FETCH_SIZE, "
                          "WRITE_SIZE) of a --calib-copy-mib run into the per-launch "
@@ -205,6 +208,47 @@ def pmc_summary(fetch_csv, write_csv, workload, cmd_args):
               json.dumps(dict(workload=workload, scale=scale, classes=table), indent=1),
               "```", ""]
     out = os.path.join(ROOT, "profiles", f"{workload}_hbm_traffic.md")
+    with open(out, "w") as fh:
+        fh.write("\n".join(lines))
+    print(out)
+
+
+def l2_summary(counter_csv, workload, cmd_args):
+    """Writes profiles/<workload>_l2_hit_rate.md: per kernel class, the L2
+    (TCC) hits and misses per launch from one rocprofv3 pass; misses go on
+    to the Infinity Cache or HBM."""
+    import collections
+    import csv
+    acc = collections.defaultdict(lambda: collections.defaultdict(list))
+    with open(counter_csv) as fh:
+        for r in csv.DictReader(fh):
+            c = kernel_class(r["Kernel_Name"])
+            if c:
+                acc[c][r["Counter_Name"]].append(float(r["Counter_Value"]))
+    bargs = (f"--workload {workload} --steps {cmd_args['steps']} --warmup {cmd_args['warmup']} "
+             f"--profile-steps {cmd_args['profile_steps']} --no-cpu-baseline --no-direct "
+             f"--no-narrow --no-adam")
+    lines = [f"# L2 hit rate per kernel class, {workload} training step", "",
+             "One rocprofv3 counter pass over a bench run (run from /tmp with TMPDIR=/tmp; "
+             "`$R` is the repository root):", "", "```",
+             f"rocprofv3 --pmc TCC_HIT_sum TCC_MISS_sum --output-format csv -d OUT -o l2 -- "
+             f"python3 $R/bench.py {bargs}",
+             f"python3 bench.py {bargs} --l2-summary OUT/l2_counter_collection.csv", "```", "",
+             "Hits and misses are L2 (TCC) requests summed over the eight XCDs; a miss is "
+             "served by the Infinity Cache or HBM.", "",
+             "| kernel class | dispatches | L2 hits / launch | L2 misses / launch | hit rate |",
+             "|---|---:|---:|---:|---:|"]
+    rows = []
+    for c, d in acc.items():
+        h, m = d.get("TCC_HIT_sum", []), d.get("TCC_MISS_sum", [])
+        if not h or len(h) != len(m):
+            continue
+        hk, mk = sum(h) / len(h), sum(m) / len(m)
+        rows.append((c, len(h), hk, mk, hk / max(hk + mk, 1.0)))
+    for c, n, hk, mk, rate in sorted(rows, key=lambda r: -(r[2] + r[3])):
+        lines.append(f"| {c} | {n} | {hk:,.0f} | {mk:,.0f} | {rate:.3f} |")
+    lines.append("")
+    out = os.path.join(ROOT, "profiles", f"{workload}_l2_hit_rate.md")
     with open(out, "w") as fh:
         fh.write("\n".join(lines))
     print(out)
@@ -643,6 +687,9 @@ def main():
             with open(args.bench_line) as fh:
                 line = json.loads(fh.read().strip().splitlines()[-1])
         trace_summary(args.trace_summary, args.workload, args.traced_args, line)
+        return
+    if args.l2_summary:
+        l2_summary(args.l2_summary, args.workload, vars(args))
         return
     if args.pmc_summary:
         # the counted run's arguments are given again on this command line
