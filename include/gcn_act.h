@@ -65,7 +65,7 @@ const char* gcn_last_error(void);
 
 /* ABI version of this header (bumped on incompatible change). */
 int gcn_abi_version(void);
-#define GCN_ABI_VERSION 2
+#define GCN_ABI_VERSION 3
 
 /* ------------------------------------------------ subgraph (host, a1)
  * gcn_subgraph_build - undirected simple subgraph in CSR form.
@@ -384,6 +384,15 @@ int gcn_layer_bwd(const gcn_dgraph* g, int32_t F, int32_t h, const float* G,
  *   the same product reassociated, and its AH region holds H W_neigh
  *   instead. Equal results up to rounding, with every aggregation at width
  *   h. Not with has_bias (GCN_E_UNSUPPORTED).
+ * precision GCN_PREC_BF16 with order GCN_ORDER_PAPER and h a multiple of 8:
+ *   the step keeps a bf16 copy (rounded to nearest even) of every operand
+ *   of a dense product, written by the kernel that produces the operand
+ *   (X and the weights are rounded once at the start of the step), and the
+ *   products read those copies: the same rounded operands as the per-layer
+ *   entry points' bf16 products, at half the operand bytes. AH, read only
+ *   by products, is then stored in bf16 only (layout field ah_bytes = 2).
+ *   Otherwise (narrow order, h % 8 != 0) the products round fp32 operands
+ *   on the way, as in the per-layer entry points.
  */
 #define GCN_ORDER_PAPER 0
 #define GCN_ORDER_NARROW 1
@@ -415,6 +424,8 @@ typedef struct {          /* byte offsets into ws, -1 when absent */
                                          ping-pong, so only the last
                                          two written stay valid      */
     int64_t scratch, scratch_bytes, total_bytes;
+    int64_t ah_bytes;                 /* bytes per AH element: 4 (float),
+                                         2 (bf16, see gcn_train_step) */
 } gcn_ws_layout;
 
 int gcn_workspace_layout(const gcn_dgraph* g, const gcn_model_desc* desc,

@@ -49,6 +49,33 @@ __device__ __forceinline__ void st4_masked(float* p, float4 v, int valid) {
     if (valid > 2) p[2] = v.z;
 }
 
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+
+// bf16 (nearest even) of the first `valid` elements of v (valid >= 1)
+__device__ __forceinline__ void st4h_masked(__bf16* p, float4 v, int valid) {
+    if (valid >= 4) {
+        bf16x4 h;
+        h[0] = (__bf16)v.x;
+        h[1] = (__bf16)v.y;
+        h[2] = (__bf16)v.z;
+        h[3] = (__bf16)v.w;
+        *reinterpret_cast<bf16x4*>(p) = h;
+        return;
+    }
+    p[0] = (__bf16)v.x;
+    if (valid > 1) p[1] = (__bf16)v.y;
+    if (valid > 2) p[2] = (__bf16)v.z;
+}
+
+// A finished row chunk goes to Yh as bf16 when Yh is set, else to Y.
+__device__ __forceinline__ void put_row(float* Y, int64_t ldy, __bf16* Yh, int64_t ldyh, int row,
+                                        int c, float4 v, int valid) {
+    if (Yh)
+        st4h_masked(Yh + (int64_t)row * ldyh + c, v, valid);
+    else
+        st4_masked(Y + (int64_t)row * ldy + c, v, valid);
+}
+
 __device__ __forceinline__ void fma4(float4& acc, float s, float4 v) {
     acc.x = fmaf(s, v.x, acc.x);
     acc.y = fmaf(s, v.y, acc.y);
@@ -129,7 +156,7 @@ __global__ __launch_bounds__(kBlock) void list_sums_kernel(
     const int4* __restrict__ seg, int nseg, const int32_t* __restrict__ col,
     RowSource src, const float* __restrict__ inv_deg, const float* __restrict__ bias,
     float* __restrict__ Y, int64_t ldy, float* __restrict__ partial, int64_t ldp, int F, int nsl,
-    int slice_f4) {
+    int slice_f4, __bf16* __restrict__ Yh, int64_t ldyh) {
     const int lane = (int)threadIdx.x % GL;
     const int sidx = group_index<GL>(nsl);
     if (sidx >= nseg) return;
@@ -189,11 +216,12 @@ __global__ __launch_bounds__(kBlock) void list_sums_kernel(
             }
         }
         if (slot < 0) {
-            float* out = Y + (int64_t)row * ldy;
 #pragma unroll
             for (int j = 0; j < NCH; ++j) {
                 const int c4 = base + lane + j * GL;
-                if (c4 < nf4) st4_masked(out + 4 * c4, finish_row<EPI>(acc[j], row, c4, inv_deg, bias, F), F - 4 * c4);
+                if (c4 < nf4)
+                    put_row(Y, ldy, Yh, ldyh, row, 4 * c4,
+                            finish_row<EPI>(acc[j], row, c4, inv_deg, bias, F), F - 4 * c4);
             }
         } else {
             float* out = partial + (int64_t)slot * ldp;
@@ -212,7 +240,7 @@ __global__ __launch_bounds__(kBlock) void fixup_kernel(
     const int4* __restrict__ longrows, int nlong,
     const float* __restrict__ partial, int64_t ldp,
     const float* __restrict__ inv_deg, const float* __restrict__ bias, float* __restrict__ Y,
-    int64_t ldy, int F, int nsl, int slice_f4) {
+    int64_t ldy, int F, int nsl, int slice_f4, __bf16* __restrict__ Yh, int64_t ldyh) {
     const int lane = (int)threadIdx.x % GL;
     const int li = group_index<GL>(nsl);
     if (li >= nlong) return;
@@ -220,7 +248,6 @@ __global__ __launch_bounds__(kBlock) void fixup_kernel(
     const int row = lr.x, first = lr.y, ns = lr.z;
     const Slice sl = slice_of(nsl, slice_f4, (F + 3) >> 2);
     const int nf4 = sl.c4_end;
-    float* out = Y + (int64_t)row * ldy;
     for (int base = sl.c4_begin; base < nf4; base += GL * NCH) {
 #pragma unroll
         for (int j = 0; j < NCH; ++j) {
@@ -238,7 +265,8 @@ __global__ __launch_bounds__(kBlock) void fixup_kernel(
                     for (int u = 0; u < 8; ++u) add4(acc, v[u]);
                 }
                 for (; sI < ns; ++sI) add4(acc, ld4(src + (int64_t)sI * ldp));
-                st4_masked(out + 4 * c4, finish_row<EPI>(acc, row, c4, inv_deg, bias, F), F - 4 * c4);
+                put_row(Y, ldy, Yh, ldyh, row, 4 * c4,
+                        finish_row<EPI>(acc, row, c4, inv_deg, bias, F), F - 4 * c4);
             }
         }
     }
@@ -293,11 +321,11 @@ hipError_t launch_pair_sums(const gcn_dgraph* g, RowSource src, bool prescale,
         if (prescale)                                                                       \
             list_sums_kernel<GL_, NCH_, true, AGG_SUM, true><<<grid, block, 0, s>>>(        \
                 seg, g->naux, g->exp_col, src, g->inv_deg, nullptr, aux, ldaux, nullptr, 0, \
-                F, sh.nsl, sh.slice_f4);                                                    \
+                F, sh.nsl, sh.slice_f4, nullptr, 0);                                        \
         else                                                                                \
             list_sums_kernel<GL_, NCH_, false, AGG_SUM, true><<<grid, block, 0, s>>>(       \
                 seg, g->naux, g->exp_col, src, g->inv_deg, nullptr, aux, ldaux, nullptr, 0, \
-                F, sh.nsl, sh.slice_f4);                                                    \
+                F, sh.nsl, sh.slice_f4, nullptr, 0);                                        \
         return hipGetLastError();                                                           \
     }
     GCN_SHAPES(GCN_LAUNCH_PAIR)
@@ -307,7 +335,7 @@ hipError_t launch_pair_sums(const gcn_dgraph* g, RowSource src, bool prescale,
 
 hipError_t launch_list_sums(const gcn_dgraph* g, RowSource src, bool prescale, AggEpi epi,
                             const float* bias, float* Y, int64_t ldy, float* partial,
-                            int64_t ldp, int32_t F, hipStream_t s) {
+                            int64_t ldp, int32_t F, hipStream_t s, __bf16* Yh, int64_t ldyh) {
     if (g->n <= 0 || F <= 0) return hipSuccess;
     if (prescale && epi != AGG_SUM) return hipErrorInvalidValue;
     const Shape sh = pick_shape(F);
@@ -321,21 +349,22 @@ hipError_t launch_list_sums(const gcn_dgraph* g, RowSource src, bool prescale, A
         // algorithmic: one gather per list entry, its id, one write per row
         ProfScope prof(s, K_LIST_SUMS,
                        nnz * F * (prescale ? 2.0 : 1.0) + (epi != AGG_SUM ? n * F : 0.0),
-                       4.0 * F * nnz + 4.0 * nnz + 4.0 * F * n);
+                       4.0 * F * nnz + 4.0 * nnz + (Yh ? 2.0 : 4.0) * F * n);
 #define GCN_LAUNCH_LIST(GL_, NCH_)                                                           \
         if (sh.gl == GL_ && sh.nch == NCH_) {                                                \
             if (prescale)                                                                    \
                 list_sums_kernel<GL_, NCH_, true, AGG_SUM, false><<<grid, block, 0, s>>>(    \
                     seg, g->nseg, g->col, src, g->inv_deg, nullptr, Y, ldy, partial, ldp, F, \
-                    sh.nsl, sh.slice_f4);                                                    \
+                    sh.nsl, sh.slice_f4, Yh, ldyh);                                          \
             else if (epi == AGG_MEAN)                                                        \
                 list_sums_kernel<GL_, NCH_, false, AGG_MEAN, false><<<grid, block, 0, s>>>(  \
                     seg, g->nseg, g->col, src, g->inv_deg, nullptr, Y, ldy, partial, ldp, F, \
-                    sh.nsl, sh.slice_f4);                                                    \
+                    sh.nsl, sh.slice_f4, Yh, ldyh);                                          \
             else                                                                             \
                 list_sums_kernel<GL_, NCH_, false, AGG_MEAN_BIAS_RELU, false>                \
                     <<<grid, block, 0, s>>>(seg, g->nseg, g->col, src, g->inv_deg, bias, Y,  \
-                                            ldy, partial, ldp, F, sh.nsl, sh.slice_f4);      \
+                                            ldy, partial, ldp, F, sh.nsl, sh.slice_f4, Yh,   \
+                                            ldyh);                                           \
         } else
         GCN_SHAPES(GCN_LAUNCH_LIST) { return hipErrorInvalidValue; }
 #undef GCN_LAUNCH_LIST
@@ -344,18 +373,21 @@ hipError_t launch_list_sums(const gcn_dgraph* g, RowSource src, bool prescale, A
     }
     if (g->nlong == 0) return hipSuccess;
     ProfScope prof(s, K_LIST_FIXUP, (double)g->nslots * F,
-                   4.0 * F * ((double)g->nslots + g->nlong));
+                   4.0 * F * g->nslots + (Yh ? 2.0 : 4.0) * F * g->nlong);
 #define GCN_LAUNCH_FIX(GL_, NCH_)                                                             \
     if (sh.gl == GL_ && sh.nch == NCH_) {                                                     \
         if (epi == AGG_SUM)                                                                   \
             fixup_kernel<GL_, NCH_, AGG_SUM><<<gfix, block, 0, s>>>(                          \
-                lr, g->nlong, partial, ldp, g->inv_deg, nullptr, Y, ldy, F, sh.nsl, sh.slice_f4); \
+                lr, g->nlong, partial, ldp, g->inv_deg, nullptr, Y, ldy, F, sh.nsl, sh.slice_f4, \
+                Yh, ldyh);                                                                    \
         else if (epi == AGG_MEAN)                                                             \
             fixup_kernel<GL_, NCH_, AGG_MEAN><<<gfix, block, 0, s>>>(                         \
-                lr, g->nlong, partial, ldp, g->inv_deg, nullptr, Y, ldy, F, sh.nsl, sh.slice_f4); \
+                lr, g->nlong, partial, ldp, g->inv_deg, nullptr, Y, ldy, F, sh.nsl, sh.slice_f4, \
+                Yh, ldyh);                                                                    \
         else                                                                                  \
             fixup_kernel<GL_, NCH_, AGG_MEAN_BIAS_RELU><<<gfix, block, 0, s>>>(               \
-                lr, g->nlong, partial, ldp, g->inv_deg, bias, Y, ldy, F, sh.nsl, sh.slice_f4);    \
+                lr, g->nlong, partial, ldp, g->inv_deg, bias, Y, ldy, F, sh.nsl, sh.slice_f4,    \
+                Yh, ldyh);                                                                    \
     } else
     GCN_SHAPES(GCN_LAUNCH_FIX) { return hipErrorInvalidValue; }
 #undef GCN_LAUNCH_FIX

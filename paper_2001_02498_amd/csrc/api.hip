@@ -14,6 +14,7 @@ namespace {
 constexpr int64_t kAlign = 256;
 
 inline int64_t r4(int64_t x) { return round_up(x, 4); }
+inline int64_t r8(int64_t x) { return round_up(x, 8); }
 
 // Scratch regions (bytes from the start of ws) for widths up to W.
 struct ScratchPlan {
@@ -116,6 +117,10 @@ int check_precision(const char* fn, int32_t precision) {
         if (rc_ != GCN_OK) return rc_; \
     } while (0)
 
+__bf16* hptr(void* ws, int64_t off) {
+    return reinterpret_cast<__bf16*>(static_cast<char*>(ws) + off);
+}
+
 float* fptr(void* ws, int64_t off) {
     return reinterpret_cast<float*>(static_cast<char*>(ws) + off);
 }
@@ -128,14 +133,16 @@ float* fptr(void* ws, int64_t off) {
 int do_aggregate(const char* fn, const gcn_dgraph* g, bool transposed, int32_t F,
                  const float* X, int64_t ldx, float* Y, int64_t ldy,
                  const ScratchPlan& sp, void* ws, hipStream_t s,
-                 AggEpi epi = AGG_MEAN, const float* bias = nullptr) {
+                 AggEpi epi = AGG_MEAN, const float* bias = nullptr, __bf16* Yh = nullptr,
+                 int64_t ldyh = 0) {
     if (transposed) epi = AGG_SUM;
     const int64_t ldaux = r4(F);
     float* aux = fptr(ws, sp.aux);
     float* part = fptr(ws, sp.part_list);
     RowSource src{X, ldx, aux, ldaux, g->n};
     GCN_HIP(launch_pair_sums(g, src, transposed, aux, ldaux, F, s), fn);
-    GCN_HIP(launch_list_sums(g, src, transposed, epi, bias, Y, ldy, part, ldaux, F, s), fn);
+    GCN_HIP(launch_list_sums(g, src, transposed, epi, bias, Y, ldy, part, ldaux, F, s, Yh, ldyh),
+            fn);
     return GCN_OK;
 }
 
@@ -146,12 +153,33 @@ GemmProblem gp_zero() {
     return p;
 }
 
+// bf16 copies of a layer's product operands (the step's bf16 variant):
+// the inputs are read by the products, the outputs written beside (or, for
+// AH and T, instead of) their fp32 versions. Leading dimensions in elements.
+struct LayerCopies {
+    const __bf16* Hin;   // layer input                      [n x F]
+    int64_t ld_hin;
+    __bf16* AH;          // its aggregation, bf16 only        [n x F]
+    int64_t ld_ah;
+    const __bf16* Ws;    // weights                           [F x h], ld h
+    const __bf16* Wn;
+    __bf16* Hout;        // layer output (forward)            [n x 2h]
+    int64_t ld_hout;
+    const __bf16* G;     // output gradient (backward)        [n x 2h]
+    int64_t ldg;
+    __bf16* T;           // aggregated neighbour gradient, bf16 only
+    int64_t ldt;
+    __bf16* Gin;         // input gradient (backward)         [n x F]
+    int64_t ldgi;
+};
+
 int do_layer_fwd(const char* fn, const gcn_dgraph* g, int32_t F, int32_t h,
                  const float* H_in, int64_t ld_in, const float* Ws,
                  const float* Wn, const float* bias, float* AH, int64_t ld_ah,
                  float* H_out, int64_t ld_out, bool bf16, const ScratchPlan& sp, void* ws,
-                 hipStream_t s) {
-    GCN_TRY(do_aggregate(fn, g, false, F, H_in, ld_in, AH, ld_ah, sp, ws, s));
+                 hipStream_t s, const LayerCopies* c = nullptr) {
+    GCN_TRY(do_aggregate(fn, g, false, F, H_in, ld_in, AH, ld_ah, sp, ws, s, AGG_MEAN, nullptr,
+                         c ? c->AH : nullptr, c ? c->ld_ah : 0));
     GemmBatch b;
     std::memset(&b, 0, sizeof(b));
     b.nprob = 2;
@@ -169,6 +197,14 @@ int do_layer_fwd(const char* fn, const gcn_dgraph* g, int32_t F, int32_t h,
         p.C = H_out + (i == 0 ? 0 : h);
         p.ldc = ld_out;
         p.bias = bias ? bias + (i == 0 ? 0 : h) : nullptr;
+        if (c) {
+            p.hA0 = p.hA1 = i == 0 ? c->Hin : c->AH;
+            p.hlda0 = p.hlda1 = i == 0 ? c->ld_hin : c->ld_ah;
+            p.hB0 = p.hB1 = i == 0 ? c->Ws : c->Wn;
+            p.hldb0 = p.hldb1 = h;
+            p.hC = c->Hout + (i == 0 ? 0 : h);
+            p.ldhc = c->ld_hout;
+        }
         b.p[i] = p;
     }
     GCN_HIP(launch_gemm(b, A_MK, B_KN, EPI_BIAS_RELU, ROLE_FWD, bf16, s), fn);
@@ -186,7 +222,9 @@ struct Logits {
 int do_classifier_fwd(const char* fn, int32_t n, int32_t K, int32_t C,
                       const float* H, int64_t ldh, const float* Wc,
                       const float* bc, float* Z, int64_t ldz, bool bf16, const ScratchPlan& sp,
-                      void* ws, hipStream_t s, bool finish, Logits* out) {
+                      void* ws, hipStream_t s, bool finish, Logits* out,
+                      const __bf16* Hb = nullptr, int64_t ldhb = 0, const __bf16* Wb = nullptr,
+                      int64_t ldwb = 0) {
     GemmBatch b;
     std::memset(&b, 0, sizeof(b));
     b.nprob = 1;
@@ -200,6 +238,12 @@ int do_classifier_fwd(const char* fn, int32_t n, int32_t K, int32_t C,
     p.B0 = p.B1 = Wc;
     p.ldb0 = p.ldb1 = C;
     p.ksplitB = K;
+    if (Hb) {
+        p.hA0 = p.hA1 = Hb;
+        p.hlda0 = p.hlda1 = ldhb;
+        p.hB0 = p.hB1 = Wb;
+        p.hldb0 = p.hldb1 = ldwb;
+    }
     // A few output tiles cannot fill the GPU: split K, then sum the slices
     // (with the bias) either here or inside the loss kernel.
     const int64_t tiles = (int64_t)((n + 127) / 128) * ((C + 127) / 128);
@@ -289,11 +333,24 @@ OptimArgs sgd_args(float lr) {
     return o;
 }
 
+// bf16 copies of the classifier's operands (the step's bf16 variant).
+struct ClsCopies {
+    const __bf16* H;    // classifier input          [n x K]
+    int64_t ldh;
+    const __bf16* W;    // W_cls                     [K x C]
+    int64_t ldw;
+    const __bf16* dZ;   // logit gradient            [n x C]
+    int64_t lddz;
+    __bf16* G;          // input gradient, written    [n x K]
+    int64_t ldg;
+};
+
 int do_classifier_bwd(const char* fn, int32_t n, int32_t K, int32_t C,
                       const float* dZ, int64_t ldd, const float* H, int64_t ldh,
                       float* Wc, float* bc, const OptimArgs& oa, const OptState& st,
                       float* G_out, int64_t ldg, float* dWc_out, float* dbc_out, bool bf16,
-                      const ScratchPlan& sp, void* ws, hipStream_t s) {
+                      const ScratchPlan& sp, void* ws, hipStream_t s,
+                      const ClsCopies* c = nullptr) {
     if (G_out) {
         GemmBatch b;
         std::memset(&b, 0, sizeof(b));
@@ -312,6 +369,14 @@ int do_classifier_bwd(const char* fn, int32_t n, int32_t K, int32_t C,
         p.ldmask = ldh;
         p.C = G_out;
         p.ldc = ldg;
+        if (c) {
+            p.hA0 = p.hA1 = c->dZ;
+            p.hlda0 = p.hlda1 = c->lddz;
+            p.hB0 = p.hB1 = c->W;
+            p.hldb0 = p.hldb1 = c->ldw;
+            p.hC = c->G;
+            p.ldhc = c->ldg;
+        }
         b.p[0] = p;
         GCN_HIP(launch_gemm(b, A_MK, B_NK, EPI_MASK, ROLE_CLS_DX, bf16, s), fn);
     }
@@ -319,6 +384,12 @@ int do_classifier_bwd(const char* fn, int32_t n, int32_t K, int32_t C,
     std::memset(&b, 0, sizeof(b));
     b.nprob = 1;
     b.p[0] = dw_problem(n, K, bc != nullptr, C, H, ldh, dZ, ldd, fptr(ws, sp.gemm_part), 1);
+    if (c) {
+        b.p[0].hA0 = b.p[0].hA1 = c->H;
+        b.p[0].hlda0 = b.p[0].hlda1 = c->ldh;
+        b.p[0].hB0 = b.p[0].hB1 = c->dZ;
+        b.p[0].hldb0 = b.p[0].hldb1 = c->lddz;
+    }
     GCN_HIP(launch_gemm(b, A_KM, B_KN, EPI_PARTIAL, ROLE_CLS_DW, bf16, s), fn);
     SgdProblem q = with_state(sgd_problem(b.p[0], K, C, Wc, bc, dWc_out, dbc_out), st);
     GCN_HIP(launch_sgd_reduce(&q, 1, oa, s), fn);
@@ -331,7 +402,8 @@ int do_layer_bwd(const char* fn, const gcn_dgraph* g, int32_t F, int32_t h,
                  float* bias, const OptimArgs& oa, const OptState& st_self,
                  const OptState& st_neigh, float* G_in, int64_t ldgi,
                  float* dWs_out, float* dWn_out, float* db_out, bool bf16,
-                 const ScratchPlan& sp, void* ws, hipStream_t s) {
+                 const ScratchPlan& sp, void* ws, hipStream_t s,
+                 const LayerCopies* c = nullptr) {
     const int32_t n = g->n;
     if (G_in) {
         // T = A D^-1 G[:, h:]  (Eq. 2c), then G_in = [G_self | T] [W_self; W_neigh]^T;
@@ -340,7 +412,8 @@ int do_layer_bwd(const char* fn, const gcn_dgraph* g, int32_t F, int32_t h,
         // on its fast path)
         float* T = fptr(ws, sp.T);
         const int64_t ldt = ldg <= sp.ld_max ? ldg : r4(h);
-        GCN_TRY(do_aggregate(fn, g, true, h, G + h, ldg, T, ldt, sp, ws, s));
+        GCN_TRY(do_aggregate(fn, g, true, h, G + h, ldg, T, ldt, sp, ws, s, AGG_SUM, nullptr,
+                             c ? c->T : nullptr, c ? c->ldt : 0));
         GemmBatch b;
         std::memset(&b, 0, sizeof(b));
         b.nprob = 1;
@@ -362,6 +435,17 @@ int do_layer_bwd(const char* fn, const gcn_dgraph* g, int32_t F, int32_t h,
         p.ldmask = ld_in;
         p.C = G_in;
         p.ldc = ldgi;
+        if (c) {
+            p.hA0 = c->G;
+            p.hlda0 = c->ldg;
+            p.hA1 = c->T;
+            p.hlda1 = c->ldt;
+            p.hB0 = c->Ws;
+            p.hB1 = c->Wn;
+            p.hldb0 = p.hldb1 = h;
+            p.hC = c->Gin;
+            p.ldhc = c->ldgi;
+        }
         b.p[0] = p;
         GCN_HIP(launch_gemm(b, A_MK, B_NK, EPI_MASK, ROLE_DX, bf16, s), fn);
     }
@@ -373,6 +457,14 @@ int do_layer_bwd(const char* fn, const gcn_dgraph* g, int32_t F, int32_t h,
     const bool ones = bias != nullptr;
     b.p[0] = dw_problem(n, F, ones, h, H_in, ld_in, G, ldg, part0, 2);
     b.p[1] = dw_problem(n, F, ones, h, AH, ld_ah, G + h, ldg, part1, 2);
+    if (c) {
+        for (int i = 0; i < 2; ++i) {
+            b.p[i].hA0 = b.p[i].hA1 = i == 0 ? c->Hin : c->AH;
+            b.p[i].hlda0 = b.p[i].hlda1 = i == 0 ? c->ld_hin : c->ld_ah;
+            b.p[i].hB0 = b.p[i].hB1 = c->G + (i == 0 ? 0 : h);
+            b.p[i].hldb0 = b.p[i].hldb1 = c->ldg;
+        }
+    }
     GCN_HIP(launch_gemm(b, A_KM, B_KN, EPI_PARTIAL, ROLE_DW, bf16, s), fn);
     SgdProblem q[2] = {
         with_state(sgd_problem(b.p[0], F, h, Ws, bias, dWs_out, db_out), st_self),
@@ -470,9 +562,28 @@ bool narrow_layer(const gcn_model_desc* d, int32_t F) {
     return d->order == GCN_ORDER_NARROW && F > d->h;
 }
 
+// bf16 copies of the step's product operands (precision GCN_PREC_BF16,
+// paper order, h a multiple of 8): byte offsets into the workspace, ld in
+// elements. AH itself is then kept in bf16 only (pub.AH, pub.ld_AH).
+struct CopyLayout {
+    bool on;
+    int64_t X, ld_x;                                  // [n x f_in]
+    int64_t Ws[GCN_MAX_LAYERS], Wn[GCN_MAX_LAYERS];   // [F_l x h], ld h
+    int64_t Wc, ld_wc;                                // [2h x C]
+    int64_t H[GCN_MAX_LAYERS];                        // [n x 2h], ld ld_H
+    int64_t G[GCN_MAX_LAYERS];                        // ping-pong like the fp32 G
+    int64_t T;                                        // [n x h], ld ld_H
+    int64_t dZ, ld_dz;                                // [n x C]
+};
+
+bool step_copies(const gcn_model_desc* d) {
+    return d->precision == GCN_PREC_BF16 && d->order == GCN_ORDER_PAPER && d->h % 8 == 0;
+}
+
 struct StepLayout {
     gcn_ws_layout pub;
     ScratchPlan sp;
+    CopyLayout cp;
 };
 
 int plan_step(const gcn_dgraph* g, const gcn_model_desc* d, StepLayout* out) {
@@ -488,10 +599,15 @@ int plan_step(const gcn_dgraph* g, const gcn_model_desc* d, StepLayout* out) {
     };
     const int64_t ldH = r4(2 * (int64_t)d->h);
     const int64_t ldC = r4(d->C);
+    const bool copies = step_copies(d);
+    CopyLayout& cp = out->cp;
+    std::memset(&cp, 0, sizeof(cp));
+    cp.on = copies;
+    out->pub.ah_bytes = copies ? 2 : 4;
     for (int l = 0; l < d->L; ++l) {
         const int64_t F = l == 0 ? d->f_in : 2 * (int64_t)d->h;
-        out->pub.ld_AH[l] = r4(F);
-        out->pub.AH[l] = take(4 * n * r4(F));
+        out->pub.ld_AH[l] = copies ? r8(F) : r4(F);
+        out->pub.AH[l] = take(out->pub.ah_bytes * n * out->pub.ld_AH[l]);
         out->pub.H[l] = take(4 * n * ldH);
     }
     out->pub.ld_H = ldH;
@@ -501,6 +617,24 @@ int plan_step(const gcn_dgraph* g, const gcn_model_desc* d, StepLayout* out) {
     const int64_t g0 = take(4 * n * ldH), g1 = take(4 * n * ldH);
     // G[l] is the masked gradient of layer l's output; layers alternate
     for (int l = 0; l < d->L; ++l) out->pub.G[l] = ((d->L - 1 - l) % 2 == 0) ? g0 : g1;
+    if (copies) {
+        const int64_t h = d->h;
+        cp.ld_x = r8(d->f_in);
+        cp.X = take(2 * n * cp.ld_x);
+        for (int l = 0; l < d->L; ++l) {
+            const int64_t F = l == 0 ? d->f_in : 2 * h;
+            cp.Ws[l] = take(2 * F * h);
+            cp.Wn[l] = take(2 * F * h);
+        }
+        cp.ld_wc = r8(d->C);
+        cp.Wc = take(2 * 2 * h * cp.ld_wc);
+        for (int l = 0; l < d->L; ++l) cp.H[l] = take(2 * n * ldH);
+        const int64_t h0 = take(2 * n * ldH), h1 = take(2 * n * ldH);
+        for (int l = 0; l < d->L; ++l) cp.G[l] = ((d->L - 1 - l) % 2 == 0) ? h0 : h1;
+        cp.T = take(2 * n * ldH);
+        cp.ld_dz = r8(d->C);
+        cp.dZ = take(2 * n * cp.ld_dz);
+    }
     const int64_t W = std::max<int64_t>({(int64_t)d->f_in, 2 * (int64_t)d->h, (int64_t)d->C});
     out->sp = plan_scratch(n, g->naux, g->nslots, W);
     out->pub.scratch = off;
@@ -798,8 +932,42 @@ int train_step_impl(const char* fn, const gcn_dgraph* g, const gcn_model_desc* d
     const bool bf16 = d->precision == GCN_PREC_BF16;
     void* scratch = static_cast<char*>(ws) + sl.pub.scratch;
     const ScratchPlan& sp = sl.sp;
+    const CopyLayout& cp = sl.cp;
     const int64_t ldH = sl.pub.ld_H, ldC = sl.pub.ld_C;
     auto act = [&](int64_t off) { return fptr(ws, off); };
+    auto h16 = [&](int64_t off) { return hptr(ws, off); };
+    // With copies, the region of AH holds bf16 values that only the products
+    // read; the fp32 pointers handed along for it are never dereferenced.
+    if (cp.on) {
+        ConvJob jobs[kMaxConvJobs];
+        int nj = 0;
+        jobs[nj++] = ConvJob{X, d->ld_x, h16(cp.X), cp.ld_x, (int32_t)n, d->f_in};
+        for (int l = 0; l < L; ++l) {
+            const int32_t F = l == 0 ? d->f_in : 2 * h;
+            jobs[nj++] = ConvJob{P->W_self[l], h, h16(cp.Ws[l]), h, F, h};
+            jobs[nj++] = ConvJob{P->W_neigh[l], h, h16(cp.Wn[l]), h, F, h};
+        }
+        jobs[nj++] = ConvJob{P->W_cls, C, h16(cp.Wc), cp.ld_wc, 2 * h, C};
+        GCN_HIP(launch_to_bf16(jobs, nj, s), fn);
+    }
+    auto layer_copies = [&](int l) {
+        LayerCopies c{};
+        c.Hin = l == 0 ? h16(cp.X) : h16(cp.H[l - 1]);
+        c.ld_hin = l == 0 ? cp.ld_x : ldH;
+        c.AH = h16(sl.pub.AH[l]);
+        c.ld_ah = sl.pub.ld_AH[l];
+        c.Ws = h16(cp.Ws[l]);
+        c.Wn = h16(cp.Wn[l]);
+        c.Hout = h16(cp.H[l]);
+        c.ld_hout = ldH;
+        c.G = h16(cp.G[l]);
+        c.ldg = ldH;
+        c.T = h16(cp.T);
+        c.ldt = ldH;
+        c.Gin = l > 0 ? h16(cp.G[l - 1]) : nullptr;
+        c.ldgi = ldH;
+        return c;
+    };
 
     // forward (Eq. 1, every layer)
     const float* Hprev = X;
@@ -810,10 +978,13 @@ int train_step_impl(const char* fn, const gcn_dgraph* g, const gcn_model_desc* d
             GCN_TRY(do_layer_fwd_narrow(fn, g, F, h, Hprev, ldprev, P->W_self[l], P->W_neigh[l],
                                         act(sl.pub.AH[l]), sl.pub.ld_AH[l], act(sl.pub.H[l]),
                                         ldH, bf16, sp, scratch, s));
-        else
+        else {
+            const LayerCopies lc = layer_copies(l);
             GCN_TRY(do_layer_fwd(fn, g, F, h, Hprev, ldprev, P->W_self[l], P->W_neigh[l],
                                  d->has_bias ? P->b[l] : nullptr, act(sl.pub.AH[l]),
-                                 sl.pub.ld_AH[l], act(sl.pub.H[l]), ldH, bf16, sp, scratch, s));
+                                 sl.pub.ld_AH[l], act(sl.pub.H[l]), ldH, bf16, sp, scratch, s,
+                                 cp.on ? &lc : nullptr));
+        }
         Hprev = act(sl.pub.H[l]);
         ldprev = ldH;
     }
@@ -823,11 +994,14 @@ int train_step_impl(const char* fn, const gcn_dgraph* g, const gcn_model_desc* d
     Logits lg;
     const float* bcls = d->has_bias ? P->b_cls : nullptr;
     GCN_TRY(do_classifier_fwd(fn, (int32_t)n, 2 * h, C, Hprev, ldH, P->W_cls, bcls, Z, ldC,
-                              bf16, sp, scratch, s, false, &lg));
+                              bf16, sp, scratch, s, false, &lg,
+                              cp.on ? h16(cp.H[L - 1]) : nullptr, ldH,
+                              cp.on ? h16(cp.Wc) : nullptr, cp.ld_wc));
     // split logits are summed (with the bias) inside the loss kernel
     GCN_HIP(launch_loss_parts((int32_t)n, C, d->loss, lg.part, lg.stride, lg.splits, lg.ldp,
                               lg.splits > 1 ? bcls : nullptr, Z, ldC, labels, dZ, ldC,
-                              fptr(scratch, sp.rowloss), loss_out, s),
+                              fptr(scratch, sp.rowloss), loss_out, s,
+                              cp.on ? h16(cp.dZ) : nullptr, cp.ld_dz),
             fn);
     // backward (classifier, then Eq. 2a-2c layer by layer)
     float* Gcur = act(sl.pub.G[L - 1]);
@@ -840,10 +1014,15 @@ int train_step_impl(const char* fn, const gcn_dgraph* g, const gcn_model_desc* d
         cst.s2 = st2->W_cls;
         cst.s2b = d->has_bias ? st2->b_cls : nullptr;
     }
+    const ClsCopies cc{cp.on ? h16(cp.H[L - 1]) : nullptr, ldH,
+                       cp.on ? h16(cp.Wc) : nullptr, cp.ld_wc,
+                       cp.on ? h16(cp.dZ) : nullptr, cp.ld_dz,
+                       cp.on ? h16(cp.G[L - 1]) : nullptr, ldH};
     GCN_TRY(do_classifier_bwd(fn, (int32_t)n, 2 * h, C, dZ, ldC, Hprev, ldH, P->W_cls,
                               d->has_bias ? P->b_cls : nullptr, oa, cst, Gcur, ldH,
                               grads ? grads->W_cls : nullptr,
-                              grads ? grads->b_cls : nullptr, bf16, sp, scratch, s));
+                              grads ? grads->b_cls : nullptr, bf16, sp, scratch, s,
+                              cp.on ? &cc : nullptr));
     for (int l = L - 1; l >= 0; --l) {
         const int32_t F = l == 0 ? d->f_in : 2 * h;
         const float* Hin = l == 0 ? X : act(sl.pub.H[l - 1]);
@@ -859,13 +1038,15 @@ int train_step_impl(const char* fn, const gcn_dgraph* g, const gcn_model_desc* d
             Gcur = Gnext;
             continue;
         }
+        const LayerCopies lc = layer_copies(l);
         GCN_TRY(do_layer_bwd(fn, g, F, h, Gcur, ldH, Hin, ldin, act(sl.pub.AH[l]),
                              sl.pub.ld_AH[l], P->W_self[l], P->W_neigh[l],
                              d->has_bias ? P->b[l] : nullptr, oa,
                              layer_state(d, st1, st2, l, 0), layer_state(d, st1, st2, l, 1),
                              Gnext, ldH, grads ? grads->W_self[l] : nullptr,
                              grads ? grads->W_neigh[l] : nullptr,
-                             grads ? grads->b[l] : nullptr, bf16, sp, scratch, s));
+                             grads ? grads->b[l] : nullptr, bf16, sp, scratch, s,
+                             cp.on ? &lc : nullptr));
         Gcur = Gnext;
     }
     return GCN_OK;

@@ -20,6 +20,7 @@
 // order). Tiles are renumbered so consecutive tiles (sharing A rows or a K
 // range) land on the same XCD, whose L2 then serves their common operand.
 #include <algorithm>
+#include <cstring>
 #include <type_traits>
 
 #include "kernels.h"
@@ -29,6 +30,8 @@ namespace gcn {
 namespace {
 
 typedef float floatx16 __attribute__((ext_vector_type(16)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 
 constexpr int BM = 128, BN = 128, BK = 32;
 constexpr int kThreads = 256;
@@ -131,15 +134,67 @@ __device__ __forceinline__ TileInfo decode_tile(const GemmBatch& batch) {
 // 32 x 32 block with i = l % 32 and j = (r % 4) + 8 (r / 4) + 4 (l / 32).
 // Every lane thus holds four runs of four consecutive columns of one row,
 // stored (and masked) with 16-byte accesses where the row is aligned.
-template <Epilogue EP>
+__device__ __forceinline__ bf16x4 to_bf16(float a, float b, float c, float d) {
+    bf16x4 r;
+    r[0] = (__bf16)a;
+    r[1] = (__bf16)b;
+    r[2] = (__bf16)c;
+    r[3] = (__bf16)d;
+    return r;
+}
+
+// HC: also write the finished values, rounded to bf16, to P.hC when set.
+// PRE: everything the epilogue reads (mask, bias) is loaded before its
+// first store. The compiler must assume C may alias them, so loads placed
+// between stores each wait for the store before them; the bf16 kernels,
+// whose K loops are short, gain from the preload, while in the fp32 kernel
+// the other workgroup on the CU hides those waits and the preload's extra
+// registers cost more than it saves.
+template <Epilogue EP, bool HC = false, bool PRE = false>
 __device__ __forceinline__ void store_tile(const GemmProblem& P, int split, int mw, int nw,
                                            int half, int l32, const floatx16 (&acc)[2][2]) {
     float* C = P.C;
     if constexpr (EP == EPI_PARTIAL) C += (int64_t)split * P.part_stride;
     const bool cvec = ((reinterpret_cast<uintptr_t>(C) | (uintptr_t)(P.ldc * 4)) & 15) == 0;
-    bool mvec = false;
-    if constexpr (EP == EPI_MASK)
-        mvec = ((reinterpret_cast<uintptr_t>(P.mask) | (uintptr_t)(P.ldmask * 4)) & 15) == 0;
+    // mask values of this lane's outputs (EPI_MASK), bias of its columns (EPI_BIAS*)
+    float mk[2][2][4][4];
+    float bv[2][4][4];
+    const bool mvec =
+        EP == EPI_MASK &&
+        ((reinterpret_cast<uintptr_t>(P.mask) | (uintptr_t)(P.ldmask * 4)) & 15) == 0;
+    if constexpr (PRE && EP == EPI_MASK) {
+#pragma unroll
+        for (int bi = 0; bi < 2; ++bi) {
+            const int m = mw + bi * 32 + l32;
+#pragma unroll
+            for (int bj = 0; bj < 2; ++bj)
+#pragma unroll
+                for (int g = 0; g < 4; ++g) {
+                    const int n = nw + bj * 32 + 8 * g + 4 * half;
+                    const float* mp = P.mask + (int64_t)m * P.ldmask + n;
+                    if (m < P.M && n + 4 <= P.N && mvec) {
+                        const float4 q = ld4(mp);
+                        mk[bi][bj][g][0] = q.x, mk[bi][bj][g][1] = q.y;
+                        mk[bi][bj][g][2] = q.z, mk[bi][bj][g][3] = q.w;
+                    } else {
+#pragma unroll
+                        for (int t = 0; t < 4; ++t)
+                            mk[bi][bj][g][t] = (m < P.M && n + t < P.N) ? mp[t] : 0.f;
+                    }
+                }
+        }
+    }
+    if constexpr (PRE && (EP == EPI_BIAS_RELU || EP == EPI_BIAS)) {
+#pragma unroll
+        for (int bj = 0; bj < 2; ++bj)
+#pragma unroll
+            for (int g = 0; g < 4; ++g) {
+                const int n = nw + bj * 32 + 8 * g + 4 * half;
+#pragma unroll
+                for (int t = 0; t < 4; ++t)
+                    bv[bj][g][t] = (P.bias && n + t < P.N) ? P.bias[n + t] : 0.f;
+            }
+    }
 #pragma unroll
     for (int bi = 0; bi < 2; ++bi) {
         const int m = mw + bi * 32 + l32;
@@ -159,7 +214,10 @@ __device__ __forceinline__ void store_tile(const GemmProblem& P, int split, int 
                     if (P.bias) {
 #pragma unroll
                         for (int t = 0; t < 4; ++t)
-                            if (n + t < P.N) v[t] += P.bias[n + t];
+                            if constexpr (PRE)
+                                v[t] += bv[bj][g][t];
+                            else if (n + t < P.N)
+                                v[t] += P.bias[n + t];
                     }
                     if constexpr (EP == EPI_BIAS_RELU) {
                         if (!P.no_relu) {
@@ -168,17 +226,22 @@ __device__ __forceinline__ void store_tile(const GemmProblem& P, int split, int 
                         }
                     }
                 } else if constexpr (EP == EPI_MASK) {
-                    const float* mp = P.mask + (int64_t)m * P.ldmask + n;
-                    float h[4];
-                    if (whole && mvec) {
-                        const float4 q = ld4(mp);
-                        h[0] = q.x, h[1] = q.y, h[2] = q.z, h[3] = q.w;
-                    } else {
+                    float hm[4];
+                    if constexpr (PRE) {
 #pragma unroll
-                        for (int t = 0; t < 4; ++t) h[t] = n + t < P.N ? mp[t] : 0.f;
+                        for (int t = 0; t < 4; ++t) hm[t] = mk[bi][bj][g][t];
+                    } else {
+                        const float* mp = P.mask + (int64_t)m * P.ldmask + n;
+                        if (whole && mvec) {
+                            const float4 q = ld4(mp);
+                            hm[0] = q.x, hm[1] = q.y, hm[2] = q.z, hm[3] = q.w;
+                        } else {
+#pragma unroll
+                            for (int t = 0; t < 4; ++t) hm[t] = n + t < P.N ? mp[t] : 0.f;
+                        }
                     }
 #pragma unroll
-                    for (int t = 0; t < 4; ++t) v[t] = h[t] > 0.f ? v[t] : 0.f;
+                    for (int t = 0; t < 4; ++t) v[t] = hm[t] > 0.f ? v[t] : 0.f;
                 }
                 if (whole && cvec) {
                     *reinterpret_cast<float4*>(crow + n) = make_float4(v[0], v[1], v[2], v[3]);
@@ -186,6 +249,18 @@ __device__ __forceinline__ void store_tile(const GemmProblem& P, int split, int 
 #pragma unroll
                     for (int t = 0; t < 4; ++t)
                         if (n + t < P.N) crow[n + t] = v[t];
+                }
+                if constexpr (HC) {
+                    if (P.hC) {
+                        __bf16* hrow = P.hC + (int64_t)m * P.ldhc + n;
+                        if (whole) {
+                            *reinterpret_cast<bf16x4*>(hrow) = to_bf16(v[0], v[1], v[2], v[3]);
+                        } else {
+#pragma unroll
+                            for (int t = 0; t < 4; ++t)
+                                if (n + t < P.N) hrow[t] = (__bf16)v[t];
+                        }
+                    }
                 }
             }
         }
@@ -516,19 +591,7 @@ __global__ __launch_bounds__(kThreads, 2) void gemm_kernel(GemmBatch batch) {
 // epilogues are those of the fp32 kernel; an MFMA step covers 16 K values,
 // so a K step of 32 is two MFMA steps. Global loads run two K steps ahead
 // (two register sets) to cover memory latency behind the shorter MFMA work.
-typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
-typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
-
 constexpr int kHStride = BK + 8;   // bf16 per LDS row: 80 bytes, conflict-free 128-bit reads
-
-__device__ __forceinline__ bf16x4 to_bf16(float a, float b, float c, float d) {
-    bf16x4 r;
-    r[0] = (__bf16)a;
-    r[1] = (__bf16)b;
-    r[2] = (__bf16)c;
-    r[3] = (__bf16)d;
-    return r;
-}
 
 template <ALayout AL, BLayout BL, Epilogue EP, bool BVEC, GemmRole ROLE>
 __global__ __launch_bounds__(kThreads, 2) void gemm_bf16_kernel(GemmBatch batch) {
@@ -774,7 +837,322 @@ __global__ __launch_bounds__(kThreads, 2) void gemm_bf16_kernel(GemmBatch batch)
     }
     if (kt < nk) kstep(kt, 0, Masked{});
 
-    store_tile<EP>(P, split, m0 + wm * 64, n0 + wn * 64, half, l32, acc);
+    store_tile<EP, false, true>(P, split, m0 + wm * 64, n0 + wn * 64, half, l32, acc);
+}
+
+// ------------------------------------------------------------ bf16 copies
+// The bf16 products when every operand already has a bf16 copy in HBM
+// (written by the kernel that produced it): half the operand bytes of the
+// kernel above and no per-element work between the loads and LDS. LDS keeps
+// each operand in its HBM orientation. K-contiguous operands are [row][k]
+// (stride 40 bf16, 80 bytes), a fragment being one 128-bit read. K-major
+// operands are [k][col] (stride 144 bf16, 288 bytes) and their fragments
+// come from two transposing reads (ds_read_b64_tr_b16): each group of 16
+// lanes names a 4 x 16 block (lane j: k row j / 4, columns 4 (j % 4) ..
+// + 3) and lane i receives column i of it, four consecutive K values. Tile,
+// K step, tile order, split-K and epilogues are those of the kernels above,
+// and the MFMAs take the same K values in the same order, so every product
+// equals that of the fp32-operand bf16 kernel bit for bit.
+typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+typedef short s16x8 __attribute__((ext_vector_type(8)));
+
+constexpr int kRS16 = BK + 8;    // [row][k] stride, bf16
+constexpr int kKS16 = BM + 16;   // [k][col] stride, bf16
+constexpr int kOp16 = (BM * kRS16 > BK * kKS16) ? BM * kRS16 : BK * kKS16;
+constexpr int kQ16 = BK * BM / 8 / kThreads;   // 16-byte chunks per operand per thread
+
+// Eight bf16 of one operand row (or K-major row) and how many are real.
+struct HChunk {
+    u32x4 v;
+    int valid;   // elements [0, valid) are real; the rest become 0
+    int one;     // element that is an implicit 1.0, or -1
+};
+
+__device__ __forceinline__ u32x4 finish16(const HChunk& q) {
+    u32x4 v = q.v;
+    // word w holds elements 2w (low half) and 2w + 1 (high half)
+#pragma unroll
+    for (int w = 0; w < 4; ++w) {
+        const unsigned keep = q.valid >= 2 * w + 2 ? 0xffffffffu
+                              : q.valid == 2 * w + 1 ? 0x0000ffffu : 0u;
+        v[w] &= keep;
+        if (q.one >= 0 && (q.one >> 1) == w)
+            v[w] |= (q.one & 1) ? 0x3f800000u : 0x00003f80u;   // bf16 1.0
+    }
+    return v;
+}
+
+__device__ __forceinline__ u32x4 ld16(const __bf16* p) {
+    return *reinterpret_cast<const u32x4*>(p);
+}
+
+template <ALayout AL, BLayout BL, Epilogue EP, GemmRole ROLE>
+__global__ __launch_bounds__(kThreads, 2) void gemm_h16_kernel(GemmBatch batch) {
+    // [buffer][A | B] operand tiles
+    __shared__ __attribute__((aligned(16))) __bf16 hs[2][2][kOp16];
+
+    const TileInfo ti = decode_tile(batch);
+    const GemmProblem& P = batch.p[ti.pi];
+    const int split = ti.split, m0 = ti.m0, n0 = ti.n0;
+    const int kbeg = ti.kbeg, kend = ti.kend, nk = ti.nk;
+
+    const int t = threadIdx.x;
+    const int lane = t & 63, wave = t >> 6;
+    const int wm = wave >> 1, wn = wave & 1;
+    const int half = lane >> 5, l32 = lane & 31;
+    const int i16 = lane & 15, sub = (lane >> 4) & 1;
+
+    const __bf16* const A0 = P.hA0;
+    const __bf16* const B0 = P.hB0;
+    const int M = P.M, N = P.N;
+    const int Areal = M - P.ones_row;
+    const bool ones = P.ones_row != 0;
+    const int ksplitA = P.ksplitA, ksplitB = P.ksplitB;
+    const int64_t lda0 = P.hlda0, ldb0 = P.hldb0;
+
+    // Thread t moves kQ16 chunks of 8 bf16 per operand and K step:
+    //   K-contiguous: row t / 4 + 64 q, K offset 8 (t % 4)
+    //   K-major:      K row t / 16 + 16 q, columns 8 (t % 16) .. + 7
+    constexpr int kCPR = BK / 8, kRowStep = kThreads / kCPR;
+    constexpr int kCPK = BM / 8, kKStep = kThreads / kCPK;
+    static_assert(kQ16 * kRowStep == BM && kQ16 * kKStep == BK, "chunks cover the tile");
+    const int rk = 8 * (t % kCPR);
+    const int kq = t / kCPK;
+    const int ac = m0 + 8 * (t % kCPK), bc = n0 + 8 * (t % kCPK);
+    int sofs_a[kQ16], sofs_b[kQ16];   // LDS element offsets of the chunks
+#pragma unroll
+    for (int q = 0; q < kQ16; ++q) {
+        sofs_a[q] = AL == A_MK ? (t / kCPR + kRowStep * q) * kRS16 + rk
+                               : (kq + kKStep * q) * kKS16 + 8 * (t % kCPK);
+        sofs_b[q] = BL == B_NK ? (t / kCPR + kRowStep * q) * kRS16 + rk
+                               : (kq + kKStep * q) * kKS16 + 8 * (t % kCPK);
+    }
+
+    // Fast tiles: no appended row of ones here and the K concatenation
+    // point on a K-step boundary between parts of equal leading dimension;
+    // whole K steps then load from a per-step base plus fixed per-thread
+    // offsets (rows / columns outside the operand clamped into it: they
+    // only feed outputs the epilogue drops).
+    const bool fast_tile = !(ones && Areal >= m0 && Areal < m0 + BM) &&
+                           (AL == A_KM || (ksplitA % BK == 0 && P.hlda1 == lda0)) &&
+                           (BL == B_KN || (ksplitB % BK == 0 && P.hldb1 == ldb0));
+    const int nfull = (kend - kbeg) / BK;
+    int64_t oa[kQ16], ob[kQ16];
+#pragma unroll
+    for (int q = 0; q < kQ16; ++q) {
+        if constexpr (AL == A_MK) {
+            const int r = m0 + t / kCPR + kRowStep * q;
+            oa[q] = (int64_t)(r < M ? r : 0) * lda0 + rk;
+        } else {
+            oa[q] = (int64_t)(kq + kKStep * q) * lda0 + (ac < Areal ? ac : 0);
+        }
+        if constexpr (BL == B_NK) {
+            const int r = n0 + t / kCPR + kRowStep * q;
+            ob[q] = (int64_t)(r < N ? r : 0) * ldb0 + rk;
+        } else {
+            ob[q] = (int64_t)(kq + kKStep * q) * ldb0 + (bc < N ? bc : 0);
+        }
+    }
+
+    HChunk ra[2][kQ16], rb[2][kQ16];
+    auto gload_full = [&](int set, int k0) {
+        const __bf16* sa;
+        const __bf16* sb;
+        if constexpr (AL == A_MK)
+            sa = k0 >= ksplitA ? P.hA1 + (k0 - ksplitA) : A0 + k0;
+        else
+            sa = A0 + (int64_t)k0 * lda0;
+        if constexpr (BL == B_NK)
+            sb = k0 >= ksplitB ? P.hB1 + (k0 - ksplitB) : B0 + k0;
+        else
+            sb = B0 + (int64_t)k0 * ldb0;
+#pragma unroll
+        for (int q = 0; q < kQ16; ++q) {
+            ra[set][q].v = ld16(sa + oa[q]);
+            rb[set][q].v = ld16(sb + ob[q]);
+        }
+    };
+    auto mark_full = [&](int set) {
+#pragma unroll
+        for (int q = 0; q < kQ16; ++q) {
+            ra[set][q].valid = rb[set][q].valid = 8;
+            ra[set][q].one = rb[set][q].one = -1;
+        }
+    };
+    // a K-contiguous chunk (row r, K offset k) of a possibly concatenated operand
+    auto row_chunk = [&](HChunk& c, const __bf16* p0, const __bf16* p1, int64_t ld0, int64_t ld1,
+                         int ksplit, int r, int rows, int k) {
+        const bool live = r < rows && k < kend;
+        c.valid = live ? min(8, kend - k) : 0;
+        c.one = -1;
+        const __bf16* p = k < ksplit ? p0 + (int64_t)r * ld0 + k
+                                     : p1 + (int64_t)r * ld1 + (k - ksplit);
+        c.v = ld16(live ? p : p0);
+    };
+    auto gload_masked = [&](int set, int k0) {
+#pragma unroll
+        for (int q = 0; q < kQ16; ++q) {
+            HChunk& a = ra[set][q];
+            if constexpr (AL == A_MK) {
+                row_chunk(a, A0, P.hA1, lda0, P.hlda1, ksplitA, m0 + t / kCPR + kRowStep * q, M,
+                          k0 + rk);
+            } else {
+                const int k = k0 + kq + kKStep * q;
+                const bool krow = k < kend;
+                a.valid = (krow && ac < Areal) ? min(8, Areal - ac) : 0;
+                a.one = (ones && krow && Areal - ac >= 0 && Areal - ac < 8) ? Areal - ac : -1;
+                a.v = ld16(a.valid > 0 ? A0 + (int64_t)k * lda0 + ac : A0);
+            }
+            HChunk& b = rb[set][q];
+            if constexpr (BL == B_NK) {
+                row_chunk(b, B0, P.hB1, ldb0, P.hldb1, ksplitB, n0 + t / kCPR + kRowStep * q, N,
+                          k0 + rk);
+            } else {
+                const int k = k0 + kq + kKStep * q;
+                b.valid = (k < kend && bc < N) ? min(8, N - bc) : 0;
+                b.one = -1;
+                b.v = ld16(b.valid > 0 ? B0 + (int64_t)k * ldb0 + bc : B0);
+            }
+        }
+    };
+    auto sstore = [&](int buf, int set, bool full) {
+        __bf16* As = hs[buf][0];
+        __bf16* Bs = hs[buf][1];
+#pragma unroll
+        for (int q = 0; q < kQ16; ++q) {
+            *reinterpret_cast<u32x4*>(&As[sofs_a[q]]) = full ? ra[set][q].v : finish16(ra[set][q]);
+            *reinterpret_cast<u32x4*>(&Bs[sofs_b[q]]) = full ? rb[set][q].v : finish16(rb[set][q]);
+        }
+    };
+
+    floatx16 acc[2][2];
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+
+    // fragment of MFMA step ks for the 32 rows (columns) from `base`: lane
+    // half g holds K values 16 ks + 8 g .. + 7 of row (column) base + l32
+    auto frag_op = [&](const __bf16* S, bool kmajor, int base, int ks) -> bf16x8 {
+        if (!kmajor)
+            return *reinterpret_cast<const bf16x8*>(&S[(base + l32) * kRS16 + 16 * ks + 8 * half]);
+        typedef __attribute__((address_space(3))) s16x4* lds_s16x4;
+        const int k0 = 16 * ks + 8 * half + (i16 >> 2);
+        const int c = base + 16 * sub + 4 * (i16 & 3);
+        const s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4)(S + k0 * kKS16 + c));
+        const s16x4 hi =
+            __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4)(S + (k0 + 4) * kKS16 + c));
+        return __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+    };
+    bf16x8 fa[2][2], fb[2][2];
+    auto frag = [&](int buf, int ks, int fslot) {
+#pragma unroll
+        for (int i = 0; i < 2; ++i) {
+            fa[fslot][i] = frag_op(hs[buf][0], AL == A_KM, wm * 64 + i * 32, ks);
+            fb[fslot][i] = frag_op(hs[buf][1], BL == B_KN, wn * 64 + i * 32, ks);
+        }
+    };
+    auto mfma = [&](int fslot) {
+#pragma unroll
+        for (int i = 0; i < 2; ++i)
+#pragma unroll
+            for (int j = 0; j < 2; ++j)
+                acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fb[fslot][j], fa[fslot][i],
+                                                                    acc[i][j], 0, 0, 0);
+    };
+
+    // LDS buffer kt % 2 holds K step kt; register set (kt + 1) % 2 holds
+    // step kt + 1, and step kt + 2 is loaded into set kt % 2 meanwhile.
+    auto kstep = [&](int kt, int set, auto FULL) {
+        const int buf = kt & 1;
+        if constexpr (FULL)
+            gload_full(set, kbeg + (kt + 2) * BK);
+        else
+            gload_masked(set, kbeg + (kt + 2) * BK);   // past kend: empty chunks
+        frag(buf, 1, 1);
+        mfma(0);
+        mfma(1);
+        __builtin_amdgcn_sched_barrier(0);
+        if constexpr (FULL) {
+            sstore(buf ^ 1, set ^ 1, true);
+            __syncthreads();
+            frag(buf ^ 1, 0, 0);
+        } else {
+            if (kt + 1 < nk) sstore(buf ^ 1, set ^ 1, false);
+            __syncthreads();
+            if (kt + 1 < nk) frag(buf ^ 1, 0, 0);
+        }
+    };
+    using Full = std::true_type;
+    using Masked = std::false_type;
+    const bool fast_start = fast_tile && nfull >= 2;
+    if (fast_start) {
+        gload_full(0, kbeg);
+        gload_full(1, kbeg + BK);
+        sstore(0, 0, true);
+    } else if (nk > 0) {
+        gload_masked(0, kbeg);
+        gload_masked(1, kbeg + BK);
+        sstore(0, 0, false);
+    }
+    if (nk > 0) {
+        __syncthreads();
+        frag(0, 0, 0);
+    }
+    int kt = 0;
+    if (fast_start) {
+        for (; kt + 3 < nfull; kt += 2) {
+            kstep(kt, 0, Full{});
+            kstep(kt + 1, 1, Full{});
+        }
+        mark_full(0);
+        mark_full(1);
+    }
+    for (; kt + 1 < nk; kt += 2) {
+        kstep(kt, 0, Masked{});
+        kstep(kt + 1, 1, Masked{});
+    }
+    if (kt < nk) kstep(kt, 0, Masked{});
+
+    store_tile<EP, EP == EPI_BIAS_RELU || EP == EPI_MASK, true>(P, split, m0 + wm * 64,
+                                                               n0 + wn * 64, half, l32, acc);
+}
+
+// Rounding of fp32 matrices to bf16 copies: one thread per 8 output
+// elements of one row, jobs laid end to end (fewer than 2^31 chunks).
+struct ConvBatch {
+    ConvJob job[kMaxConvJobs];
+    int32_t first[kMaxConvJobs + 1];   // first chunk of each job
+    int32_t njobs;
+};
+
+__global__ __launch_bounds__(256) void to_bf16_kernel(ConvBatch b) {
+    const int idx = (int)(blockIdx.x * 256 + threadIdx.x);
+    if (idx >= b.first[b.njobs]) return;
+    int j = 0;
+    while (idx >= b.first[j + 1]) ++j;
+    const ConvJob& J = b.job[j];
+    const int per_row = (int)(J.ldd >> 3);
+    const int local = idx - b.first[j];
+    const int r = local / per_row;
+    const int c0 = (local - r * per_row) * 8;
+    const float* src = J.src + (int64_t)r * J.lds + c0;
+    float f[8];
+    if (c0 + 8 <= J.cols && (reinterpret_cast<uintptr_t>(src) & 15) == 0) {
+        const float4 x = ld4(src), y = ld4(src + 4);
+        f[0] = x.x, f[1] = x.y, f[2] = x.z, f[3] = x.w;
+        f[4] = y.x, f[5] = y.y, f[6] = y.z, f[7] = y.w;
+    } else {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) f[e] = c0 + e < J.cols ? src[e] : 0.f;
+    }
+    bf16x8 out;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) out[e] = (__bf16)f[e];
+    *reinterpret_cast<bf16x8*>(J.dst + (int64_t)r * J.ldd + c0) = out;
 }
 
 // sum_j src[j * stride], j ascending; eight loads in flight at a time
@@ -922,16 +1300,44 @@ hipError_t launch_gemm(GemmBatch& b, ALayout al, BLayout bl, Epilogue ep, GemmRo
     }
     static const int kKinds[] = {K_GEMM_FWD, K_GEMM_CLS, K_GEMM_DX,
                                  K_GEMM_CLS_DX, K_GEMM_DW, K_GEMM_CLS_DW};
+    // bf16 with operand copies in every problem: the copies kernel
+    bool copies = bf16;
+    for (int i = 0; i < b.nprob; ++i) copies = copies && b.p[i].hA0 && b.p[i].hB0;
+    if (copies) {
+        auto ok16 = [](const __bf16* q, int64_t ld) {
+            return q == nullptr || (((uintptr_t)q & 15) == 0 && (ld & 7) == 0);
+        };
+        for (int i = 0; i < b.nprob; ++i) {
+            const GemmProblem& p = b.p[i];
+            const bool catA = al == A_MK && p.ksplitA < p.K;
+            const bool catB = bl == B_NK && p.ksplitB < p.K;
+            if (!ok16(p.hA0, p.hlda0) || !ok16(p.hB0, p.hldb0) ||
+                (catA && (!p.hA1 || !ok16(p.hA1, p.hlda1) || p.ksplitA % 8)) ||
+                (catB && (!p.hB1 || !ok16(p.hB1, p.hldb1) || p.ksplitB % 8)) ||
+                (p.hC && (((uintptr_t)p.hC & 7) || (p.ldhc & 3))))
+                return hipErrorInvalidValue;
+        }
+        // operands are read as bf16
+        bytes = 0;
+        for (int i = 0; i < b.nprob; ++i) {
+            const GemmProblem& p = b.p[i];
+            const double M = p.M, N = p.N, K = p.K;
+            bytes += 2.0 * (M * K + K * N) + 4.0 * M * N + (ep == EPI_MASK ? 4.0 * M * N : 0.0) +
+                     (p.hC ? 2.0 * M * N : 0.0);
+        }
+    }
     const int kind = kKinds[role] + (bf16 ? K_GEMM_BF16_OFFSET : 0);
     ProfScope prof(s, kind, flops, bytes);
     bool bvec = true;
     for (int i = 0; i < b.nprob; ++i) {
-        if (!b.p[i].a_vec) return hipErrorInvalidValue;   // A rows must be aligned
+        if (!copies && !b.p[i].a_vec) return hipErrorInvalidValue;   // A rows must be aligned
         bvec = bvec && b.p[i].b_vec;
     }
 #define GCN_GEMM_CASE(AL_, BL_, EP_, ROLE_)                                          \
     if (al == AL_ && bl == BL_ && ep == EP_ && role == ROLE_) {                       \
-        if (bf16 && bvec)                                                            \
+        if (copies)                                                                  \
+            gemm_h16_kernel<AL_, BL_, EP_, ROLE_><<<grid, block, 0, s>>>(b);          \
+        else if (bf16 && bvec)                                                       \
             gemm_bf16_kernel<AL_, BL_, EP_, true, ROLE_><<<grid, block, 0, s>>>(b);   \
         else if (bf16)                                                               \
             gemm_bf16_kernel<AL_, BL_, EP_, false, ROLE_><<<grid, block, 0, s>>>(b);  \
@@ -950,6 +1356,31 @@ hipError_t launch_gemm(GemmBatch& b, ALayout al, BLayout bl, Epilogue ep, GemmRo
     GCN_GEMM_CASE(A_KM, B_KN, EPI_PARTIAL, ROLE_CLS_DW)
 #undef GCN_GEMM_CASE
     return hipErrorInvalidValue;
+}
+
+hipError_t launch_to_bf16(const ConvJob* jobs, int njobs, hipStream_t s) {
+    if (njobs < 0 || njobs > kMaxConvJobs) return hipErrorInvalidValue;
+    ConvBatch b;
+    std::memset(&b, 0, sizeof(b));
+    b.njobs = njobs;
+    b.first[0] = 0;
+    double elems = 0;
+    for (int j = 0; j < njobs; ++j) {
+        const ConvJob& J = jobs[j];
+        if (J.rows < 0 || J.cols < 0 || J.ldd < 8 || (J.ldd & 7) || J.ldd < J.cols ||
+            ((uintptr_t)J.dst & 15) || (J.rows > 0 && (!J.src || !J.dst || J.lds < J.cols)))
+            return hipErrorInvalidValue;
+        b.job[j] = J;
+        const int64_t next = (int64_t)b.first[j] + (int64_t)J.rows * (J.ldd / 8);
+        if (next >= (int64_t)1 << 31) return hipErrorInvalidValue;
+        b.first[j + 1] = (int32_t)next;
+        elems += (double)J.rows * J.cols;
+    }
+    const int64_t total = b.first[njobs];
+    if (total == 0) return hipSuccess;
+    ProfScope prof(s, K_TO_BF16, elems, 6.0 * elems);
+    to_bf16_kernel<<<dim3((unsigned)((total + 255) / 256)), dim3(256), 0, s>>>(b);
+    return hipGetLastError();
 }
 
 hipError_t launch_sgd_reduce(const SgdProblem* p, int nprob, const OptimArgs& o,

@@ -35,9 +35,12 @@ enum AggEpi : int {
 // Segment sums of G_s^# lists (see the work list of gcn_graph_pack), then the
 // fix-up of split lists, finished as `epi` says; prescale (with AGG_SUM
 // only): gathered original rows are multiplied by their 1/d.
+// Yh != NULL: the finished rows go to Yh as bf16 (rounded to nearest even;
+// leading dimension ldyh) instead of to Y.
 hipError_t launch_list_sums(const gcn_dgraph* g, RowSource src, bool prescale, AggEpi epi,
                             const float* bias, float* Y, int64_t ldy, float* partial,
-                            int64_t ldp, int32_t F, hipStream_t s);
+                            int64_t ldp, int32_t F, hipStream_t s, __bf16* Yh = nullptr,
+                            int64_t ldyh = 0);
 
 // ---------------------------------------------------------------- GEMM
 enum ALayout : int { A_MK = 0, A_KM = 1 };   // A(m,k) = A[m*lda+k] | A[k*lda+m]
@@ -74,6 +77,20 @@ struct GemmProblem {
     int32_t tiles_m, tiles_n, tile_begin;
     int32_t a_vec, b_vec; // operand rows 16-byte aligned: float4 loads
     int32_t no_relu;      // EPI_BIAS_RELU: this problem stores acc + bias only
+    // bf16 copies of the operands (launch_gemm with bf16 and hA0 != NULL):
+    // the same elements as A0/A1/B0/B1, rounded to bf16, with their own
+    // leading dimensions (multiples of 8, rows 16-byte aligned; a K
+    // concatenation point must then be a multiple of 8)
+    const __bf16* hA0;
+    const __bf16* hA1;
+    int64_t hlda0, hlda1;
+    const __bf16* hB0;
+    const __bf16* hB1;
+    int64_t hldb0, hldb1;
+    // optional bf16 copy of the finished output (EPI_BIAS_RELU, EPI_MASK),
+    // leading dimension a multiple of 4
+    __bf16* hC;
+    int64_t ldhc;
 };
 
 constexpr int kMaxProblems = 2;
@@ -102,7 +119,9 @@ enum GemmRole : int {
 };
 
 // Launch C = A B for 1-2 problems of identical layouts / epilogue; bf16:
-// operands rounded to bf16 for the matrix cores, fp32 accumulation.
+// operands rounded to bf16 for the matrix cores, fp32 accumulation. With
+// bf16 and operand copies (hA0 set in every problem) the products read the
+// copies; otherwise they read the fp32 operands and round them on the way.
 hipError_t launch_gemm(GemmBatch& b, ALayout al, BLayout bl, Epilogue ep, GemmRole role,
                        bool bf16, hipStream_t s);
 
@@ -141,6 +160,19 @@ struct OptimArgs {
 hipError_t launch_sgd_reduce(const SgdProblem* p, int nprob, const OptimArgs& o,
                              hipStream_t s);
 
+// Rounding of fp32 matrices to bf16 copies (nearest even), up to
+// kMaxConvJobs matrices in one launch: dst[r][c] = bf16(src[r][c]) for
+// c < cols, 0 for cols <= c < ldd (ldd a multiple of 8).
+constexpr int kMaxConvJobs = 2 * GCN_MAX_LAYERS + 2;
+struct ConvJob {
+    const float* src;
+    int64_t lds;
+    __bf16* dst;
+    int64_t ldd;
+    int32_t rows, cols;
+};
+hipError_t launch_to_bf16(const ConvJob* jobs, int njobs, hipStream_t s);
+
 // ---------------------------------------------------------------- loss
 constexpr int kMaxLossVPL = 8;   // classes per lane: C <= 512
 hipError_t launch_loss(int32_t n, int32_t C, int32_t kind, const float* z,
@@ -149,9 +181,11 @@ hipError_t launch_loss(int32_t n, int32_t C, int32_t kind, const float* z,
                        hipStream_t s);
 // The same with logits = sum of `splits` slices (stride apart, ld ldp) plus
 // bias, written to z_out.
+// dzh != NULL: also a bf16 copy of dz (leading dimension lddh).
 hipError_t launch_loss_parts(int32_t n, int32_t C, int32_t kind, const float* part,
                              int64_t stride, int32_t splits, int64_t ldp, const float* bias,
                              float* z_out, int64_t ldz, const void* labels, float* dz,
-                             int64_t ldd, float* rowloss, float* loss_out, hipStream_t s);
+                             int64_t ldd, float* rowloss, float* loss_out, hipStream_t s,
+                             __bf16* dzh = nullptr, int64_t lddh = 0);
 
 }  // namespace gcn

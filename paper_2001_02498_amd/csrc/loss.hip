@@ -46,7 +46,8 @@ template <int VPL, bool BCE>
 __global__ __launch_bounds__(256) void loss_kernel(
     int n, int C, const float* __restrict__ part, int64_t stride, int splits, int64_t ldp,
     const float* __restrict__ bias, float* z_out, int64_t ldz, const void* __restrict__ labels,
-    float* __restrict__ dz, int64_t ldd, float* __restrict__ rowloss) {
+    float* __restrict__ dz, int64_t ldd, float* __restrict__ rowloss, __bf16* __restrict__ dzh,
+    int64_t lddh) {
     const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
     const int lane = threadIdx.x & 63;
     if (row >= n) return;
@@ -63,6 +64,7 @@ __global__ __launch_bounds__(256) void loss_kernel(
         }
     }
     float* dr = dz + (int64_t)row * ldd;
+    __bf16* drh = dzh ? dzh + (int64_t)row * lddh : nullptr;
     if constexpr (!BCE) {
         const int y = static_cast<const int32_t*>(labels)[row];
         float m = -INFINITY;
@@ -84,7 +86,11 @@ __global__ __launch_bounds__(256) void loss_kernel(
 #pragma unroll
         for (int i = 0; i < VPL; ++i) {
             const int c = lane + 64 * i;
-            if (c < C) dr[c] = (expf(v[i] - m) * inv_s - (c == y ? 1.0f : 0.0f)) * inv_n;
+            if (c < C) {
+                const float d = (expf(v[i] - m) * inv_s - (c == y ? 1.0f : 0.0f)) * inv_n;
+                dr[c] = d;
+                if (drh) drh[c] = (__bf16)d;
+            }
         }
         if (lane == 0) rowloss[row] = (m + logf(ssum)) - zy;
     } else {
@@ -98,7 +104,9 @@ __global__ __launch_bounds__(256) void loss_kernel(
                 const float z = v[i];
                 const float y = yr[c] ? 1.0f : 0.0f;
                 acc += fmaxf(z, 0.f) - z * y + log1pf(expf(-fabsf(z)));
-                dr[c] = (1.0f / (1.0f + expf(-z)) - y) * scale;
+                const float d = (1.0f / (1.0f + expf(-z)) - y) * scale;
+                dr[c] = d;
+                if (drh) drh[c] = (__bf16)d;
             }
         }
         acc = wave_sum(acc);
@@ -135,21 +143,23 @@ __global__ __launch_bounds__(256) void mean_kernel(int n, const float* __restric
 hipError_t launch_loss_parts(int32_t n, int32_t C, int32_t kind, const float* part,
                              int64_t stride, int32_t splits, int64_t ldp, const float* bias,
                              float* z_out, int64_t ldz, const void* labels, float* dz,
-                             int64_t ldd, float* rowloss, float* loss_out, hipStream_t s) {
+                             int64_t ldd, float* rowloss, float* loss_out, hipStream_t s,
+                             __bf16* dzh, int64_t lddh) {
     if (C > 64 * kMaxLossVPL) return hipErrorInvalidValue;
     if (n > 0) {
         const dim3 grid((n + 3) / 4), block(256);
         ProfScope prof(s, K_LOSS_ROWS, (double)n * C * (8.0 + splits),
-                       4.0 * (double)n * C * (splits + 2.0) + 4.0 * n);
+                       4.0 * (double)n * C * (splits + 2.0) + (dzh ? 2.0 : 0.0) * n * C +
+                           4.0 * n);
         const int vpl = (C + 63) / 64;
 #define GCN_LOSS_CASE(V_)                                                                 \
         if (vpl <= V_) {                                                                  \
             if (kind == GCN_LOSS_SOFTMAX_CE)                                              \
                 loss_kernel<V_, false><<<grid, block, 0, s>>>(n, C, part, stride, splits, \
-                    ldp, bias, z_out, ldz, labels, dz, ldd, rowloss);                     \
+                    ldp, bias, z_out, ldz, labels, dz, ldd, rowloss, dzh, lddh);         \
             else                                                                          \
                 loss_kernel<V_, true><<<grid, block, 0, s>>>(n, C, part, stride, splits,  \
-                    ldp, bias, z_out, ldz, labels, dz, ldd, rowloss);                     \
+                    ldp, bias, z_out, ldz, labels, dz, ldd, rowloss, dzh, lddh);         \
         } else
         GCN_LOSS_CASE(1) GCN_LOSS_CASE(2) GCN_LOSS_CASE(4) GCN_LOSS_CASE(8) {
             return hipErrorInvalidValue;

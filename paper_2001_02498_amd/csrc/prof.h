@@ -28,6 +28,7 @@ enum Kind : int {
     K_GEMM_CLS_DX_BF16,
     K_GEMM_DW_BF16,
     K_GEMM_CLS_DW_BF16,
+    K_TO_BF16,
     K_COUNT
 };
 constexpr int K_GEMM_BF16_OFFSET = K_GEMM_FWD_BF16 - K_GEMM_FWD;

@@ -48,6 +48,7 @@ const char* kind_name(int k) {
         case K_GEMM_CLS_DX_BF16: return "gemm_cls_dx_bf16";
         case K_GEMM_DW_BF16: return "gemm_dw_bf16";
         case K_GEMM_CLS_DW_BF16: return "gemm_cls_dw_bf16";
+        case K_TO_BF16: return "to_bf16";
         default: return "other";
     }
 }

@@ -153,3 +153,63 @@ def test_step_bf16(name):
     errs = check_step(run, tol=BF16_TOL)
     # rounding really happened: the dense results are not float32-exact
     assert max(errs[k] for k in errs if k.startswith("H")) > 10 * FP32_TOL
+
+
+@pytest.mark.parametrize("L,loss,bias", [(2, synth.SIGMOID_BCE, True),
+                                         (3, synth.SOFTMAX_CE, False),
+                                         (1, synth.SOFTMAX_CE, True)])
+def test_step_bf16_copies_ragged(L, loss, bias):
+    """The bf16 step on operand copies (h a multiple of 8) at ragged sizes:
+    n, f_in and C off every tile and every 8-element chunk, the K
+    concatenation point h = 40 off the K step, biases through the appended
+    row of ones, split lists."""
+    need_gpu()
+    from paper_2001_02498_amd import gcn
+    wl = synth.small_workload(437, 9, L, 29, 40, 7, loss, (L, loss, int(bias), 16))
+    run = StepRun(wl, bias=bias, seg_len=4, precision=gcn.PREC_BF16).run()
+    assert run.layout.ah_bytes == 2
+    check_step(run, tol=BF16_TOL)
+
+
+def test_step_bf16_without_copies():
+    """h not a multiple of 8: the step's products round fp32 operands."""
+    need_gpu()
+    from paper_2001_02498_amd import gcn
+    wl = synth.small_workload(437, 9, 2, 29, 36, 7, synth.SOFTMAX_CE, (17,))
+    run = StepRun(wl, bias=True, precision=gcn.PREC_BF16).run()
+    assert run.layout.ah_bytes == 4
+    check_step(run, tol=BF16_TOL)
+
+
+@pytest.mark.parametrize("name", ["tiny", "ppi8k"])
+def test_step_bf16_copies_match_entry_points(name):
+    """The step's forward products on bf16 copies equal, bit for bit, those
+    of the per-layer entry points, whose products round float32 operands on
+    the way: the same rounded operands, summed in the same K order. Each
+    layer is fed the step's own input to it."""
+    need_gpu()
+    from paper_2001_02498_amd import gcn
+    wl = synth.WORKLOADS[name]
+    run = StepRun(wl, precision=gcn.PREC_BF16).run()
+    lay = run.layout
+    assert lay.ah_bytes == 2
+    Ws0, Wn0, Wc0, _, _ = run.params_dev()   # the weights before the update
+    Hin = run.X
+    for l in range(wl.L):
+        F = wl.f_in if l == 0 else 2 * wl.h
+        AH, H = empty(wl.n, F), empty(wl.n, 2 * wl.h)
+        say("layer_fwd vs step", name, "layer", l)
+        gcn.layer_fwd(run.case.dg, Hin, Ws0[l], Wn0[l], None, AH, H,
+                      _ws(run.case, max(F, 2 * wl.h)), precision=gcn.PREC_BF16)
+        torch.cuda.synchronize()
+        H_step = run.act(lay.H[l], wl.n, 2 * wl.h, lay.ld_H)
+        assert torch.equal(H, H_step), l
+        AH_step = run.ws[lay.AH[l]:lay.AH[l] + 2 * wl.n * lay.ld_AH[l]].view(
+            torch.bfloat16).view(wl.n, lay.ld_AH[l])[:, :F]
+        assert torch.equal(AH.to(torch.bfloat16), AH_step), l
+        Hin = H_step
+    Z = empty(wl.n, wl.C)
+    gcn.classifier_fwd(Hin, 2 * wl.h, Wc0, None, Z, _ws(run.case, max(2 * wl.h, wl.C)),
+                       precision=gcn.PREC_BF16)
+    torch.cuda.synchronize()
+    assert torch.equal(Z, run.act(lay.logits, wl.n, wl.C, lay.ld_C))

@@ -84,6 +84,15 @@ class StepRun:
         t = self.ws[off:off + 4 * rows * ld].view(torch.float32).view(rows, ld)
         return t[:, :cols]
 
+    def ah(self, l, rows, cols):
+        """Layer l's AH region as float32 (the bf16 step keeps it in bf16)."""
+        lay = self.layout
+        off, ld = lay.AH[l], lay.ld_AH[l]
+        if lay.ah_bytes == 4:
+            return self.act(off, rows, cols, ld)
+        t = self.ws[off:off + 2 * rows * ld].view(torch.bfloat16).view(rows, ld)
+        return t[:, :cols].float()
+
     def oracle(self):
         wl, inp = self.wl, self.inp
         lay = self.layout
@@ -115,9 +124,9 @@ def check_step(run, tol=FP32_TOL):
         if run.narrow(l):
             # the region holds H W_neigh, the product the layer aggregates
             Z = ref["fw"]["H"][l] @ run.inp.W_neigh[l].astype(np.float64)
-            errs[f"Z{l}"] = rel(run.act(lay.AH[l], wl.n, wl.h, lay.ld_AH[l]), Z)
+            errs[f"Z{l}"] = rel(run.ah(l, wl.n, wl.h), Z)
         else:
-            errs[f"AH{l}"] = rel(run.act(lay.AH[l], wl.n, F, lay.ld_AH[l]), ref["fw"]["AH"][l])
+            errs[f"AH{l}"] = rel(run.ah(l, wl.n, F), ref["fw"]["AH"][l])
         errs[f"H{l}"] = rel(run.act(lay.H[l], wl.n, 2 * wl.h, lay.ld_H), ref["fw"]["H"][l + 1])
     errs["logits"] = rel(run.act(lay.logits, wl.n, wl.C, lay.ld_C), ref["fw"]["logits"])
     errs["dlogits"] = rel(run.act(lay.dlogits, wl.n, wl.C, lay.ld_C), ref["dlogits"])
