@@ -124,7 +124,8 @@ def kernel_class(name):
     """Timing class of a demangled kernel name (the classes gcn_profile_read
     reports), or None for kernels that are not the library's."""
     import re
-    for key, suffix in (("gemm_kernel<", ""), ("gemm_bf16_kernel<", "_bf16")):
+    for key, suffix in (("gemm_kernel<", ""), ("gemm_bf16_kernel<", "_bf16"),
+                        ("gemm_h16_kernel<", "_bf16")):
         if key in name:
             m = re.search(r"\(gcn::GemmRole\)(\d+)", name)
             return _ROLE_CLASS[int(m.group(1))] + suffix if m else None
@@ -133,7 +134,7 @@ def kernel_class(name):
         return "pair_sums" if head.split(">")[0].rstrip().endswith("true") else "list_sums"
     for key, cls in (("fixup_kernel<", "list_fixup"), ("sgd_reduce_kernel", "sgd_reduce"),
                      ("splitk_finish_kernel", "splitk_finish"), ("loss_kernel<", "loss_rows"),
-                     ("mean_kernel", "loss_mean")):
+                     ("mean_kernel", "loss_mean"), ("to_bf16_kernel", "to_bf16")):
         if key in name:
             return cls
     return None

@@ -13,6 +13,8 @@ import bench
 GEMM = ("void gcn::(anonymous namespace)::gemm_kernel<(gcn::ALayout)1, (gcn::BLayout)0, "
         "(gcn::Epilogue)4, true, (gcn::GemmRole){}>(gcn::GemmBatch)")
 GEMM16 = GEMM.replace("gemm_kernel<", "gemm_bf16_kernel<")
+H16 = ("void gcn::(anonymous namespace)::gemm_h16_kernel<(gcn::ALayout)1, (gcn::BLayout)0, "
+       "(gcn::Epilogue)4, (gcn::GemmRole){}>(gcn::GemmBatch)")
 LIST = ("void gcn::(anonymous namespace)::list_sums_kernel<32, 1, false, 1, {}>(int4 const*, "
         "int, int const*, gcn::RowSource, float const*, float const*, float*, long, float*, "
         "long, int, int, int)")
@@ -22,6 +24,7 @@ LIST = ("void gcn::(anonymous namespace)::list_sums_kernel<32, 1, false, 1, {}>(
 def test_gemm_roles_map_to_classes(role, cls):
     assert bench.kernel_class(GEMM.format(role)) == cls
     assert bench.kernel_class(GEMM16.format(role)) == cls + "_bf16"
+    assert bench.kernel_class(H16.format(role)) == cls + "_bf16"
 
 
 def test_other_kernels_map_to_classes():
@@ -32,6 +35,8 @@ def test_other_kernels_map_to_classes():
         "void gcn::(anonymous namespace)::sgd_reduce_kernel<2>(gcn::SgdProblem)": "sgd_reduce",
         "void gcn::(anonymous namespace)::loss_kernel<2, true>(int, int)": "loss_rows",
         "gcn::(anonymous namespace)::mean_kernel(int, float const*, float, float*)": "loss_mean",
+        "gcn::(anonymous namespace)::to_bf16_kernel(gcn::(anonymous namespace)::ConvBatch)":
+            "to_bf16",
         "__amd_rocclr_copyBuffer": None,
         "void at::native::vectorized_elementwise_kernel<4>(int)": None,
     }
