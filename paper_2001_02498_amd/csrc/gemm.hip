@@ -887,6 +887,108 @@ __device__ __forceinline__ u32x4 ld16(const __bf16* p) {
     return *reinterpret_cast<const u32x4*>(p);
 }
 
+// Epilogue through LDS: the wavefront's 64 x 64 block goes to `stage` (its
+// own 2176 floats of the freed operand buffers) 32 rows at a time, and is
+// read back so that each load and store instruction covers four whole
+// 256-byte row runs (16 lanes per row) instead of 32 rows x 32 bytes.
+// HC: also the bf16 copy. The caller has synchronised the workgroup.
+template <Epilogue EP, bool HC>
+__device__ __forceinline__ void store_tile_lds(const GemmProblem& P, int split, int mw, int nw,
+                                               int half, int l32, int lane, float* stage,
+                                               const floatx16 (&acc)[2][2]) {
+    constexpr int kSS = 64 + 4;   // staged row stride, floats
+    float* C = P.C;
+    if constexpr (EP == EPI_PARTIAL) C += (int64_t)split * P.part_stride;
+    const bool cvec = ((reinterpret_cast<uintptr_t>(C) | (uintptr_t)(P.ldc * 4)) & 15) == 0;
+    const bool mvec =
+        EP == EPI_MASK &&
+        ((reinterpret_cast<uintptr_t>(P.mask) | (uintptr_t)(P.ldmask * 4)) & 15) == 0;
+    const int c = 4 * (lane & 15);   // this lane's four columns of the block
+    const int n = nw + c;
+    const bool whole = n + 4 <= P.N;
+    float bv[4] = {0.f, 0.f, 0.f, 0.f};
+    if constexpr (EP == EPI_BIAS_RELU || EP == EPI_BIAS) {
+        if (P.bias) {
+#pragma unroll
+            for (int t = 0; t < 4; ++t) bv[t] = n + t < P.N ? P.bias[n + t] : 0.f;
+        }
+    }
+#pragma unroll
+    for (int bi = 0; bi < 2; ++bi) {
+        // lane (l32, half): row l32, columns 32 bj + 8 g + 4 half .. + 3
+#pragma unroll
+        for (int bj = 0; bj < 2; ++bj)
+#pragma unroll
+            for (int g = 0; g < 4; ++g)
+                *reinterpret_cast<float4*>(&stage[l32 * kSS + 32 * bj + 8 * g + 4 * half]) =
+                    make_float4(acc[bi][bj][4 * g], acc[bi][bj][4 * g + 1],
+                                acc[bi][bj][4 * g + 2], acc[bi][bj][4 * g + 3]);
+        __syncthreads();
+        // lane l: rows l / 16 + 4 k of the 32, columns c .. c + 3
+        float v[8][4];
+        float mk[8][4];
+#pragma unroll
+        for (int k = 0; k < 8; ++k) {
+            const int r = (lane >> 4) + 4 * k;
+            const float4 q = *reinterpret_cast<const float4*>(&stage[r * kSS + c]);
+            v[k][0] = q.x, v[k][1] = q.y, v[k][2] = q.z, v[k][3] = q.w;
+            if constexpr (EP == EPI_MASK) {
+                const int m = mw + 32 * bi + r;
+                const float* mp = P.mask + (int64_t)m * P.ldmask + n;
+                if (m < P.M && whole && mvec) {
+                    const float4 h = ld4(mp);
+                    mk[k][0] = h.x, mk[k][1] = h.y, mk[k][2] = h.z, mk[k][3] = h.w;
+                } else {
+#pragma unroll
+                    for (int t = 0; t < 4; ++t) mk[k][t] = (m < P.M && n + t < P.N) ? mp[t] : 0.f;
+                }
+            }
+        }
+        __syncthreads();   // the stage is rewritten by the next pass
+#pragma unroll
+        for (int k = 0; k < 8; ++k) {
+            const int m = mw + 32 * bi + (lane >> 4) + 4 * k;
+            if (m >= P.M || n >= P.N) continue;
+            float* w = v[k];
+            if constexpr (EP == EPI_BIAS_RELU || EP == EPI_BIAS) {
+                if (P.bias) {
+#pragma unroll
+                    for (int t = 0; t < 4; ++t) w[t] += bv[t];
+                }
+                if constexpr (EP == EPI_BIAS_RELU) {
+                    if (!P.no_relu) {
+#pragma unroll
+                        for (int t = 0; t < 4; ++t) w[t] = w[t] > 0.f ? w[t] : 0.f;
+                    }
+                }
+            } else if constexpr (EP == EPI_MASK) {
+#pragma unroll
+                for (int t = 0; t < 4; ++t) w[t] = mk[k][t] > 0.f ? w[t] : 0.f;
+            }
+            float* crow = C + (int64_t)m * P.ldc;
+            if (whole && cvec) {
+                *reinterpret_cast<float4*>(crow + n) = make_float4(w[0], w[1], w[2], w[3]);
+            } else {
+#pragma unroll
+                for (int t = 0; t < 4; ++t)
+                    if (n + t < P.N) crow[n + t] = w[t];
+            }
+            if constexpr (HC) {
+                if (P.hC) {
+                    __bf16* hrow = P.hC + (int64_t)m * P.ldhc + n;
+                    if (whole) {
+                        *reinterpret_cast<bf16x4*>(hrow) = to_bf16(w[0], w[1], w[2], w[3]);
+                    } else {
+#pragma unroll
+                        for (int t = 0; t < 4; ++t)
+                            if (n + t < P.N) hrow[t] = (__bf16)w[t];
+                    }
+                }
+            }
+        }
+    }
+}
+
 template <ALayout AL, BLayout BL, Epilogue EP, GemmRole ROLE>
 __global__ __launch_bounds__(kThreads, 2) void gemm_h16_kernel(GemmBatch batch) {
     // [buffer][A | B] operand tiles
@@ -1117,8 +1219,13 @@ __global__ __launch_bounds__(kThreads, 2) void gemm_h16_kernel(GemmBatch batch) 
     }
     if (kt < nk) kstep(kt, 0, Masked{});
 
-    store_tile<EP, EP == EPI_BIAS_RELU || EP == EPI_MASK, true>(P, split, m0 + wm * 64,
-                                                               n0 + wn * 64, half, l32, acc);
+    __syncthreads();   // every fragment read done: the operand buffers become the stage
+    constexpr int kStage = 2 * 2 * kOp16 / 2 / 4;   // floats per wavefront
+    static_assert(kStage >= 32 * (64 + 4), "a 32 x 64 block fits each wavefront's share");
+    float* stage = reinterpret_cast<float*>(&hs[0][0][0]) + wave * kStage;
+    store_tile_lds<EP, EP == EPI_BIAS_RELU || EP == EPI_MASK>(P, split, m0 + wm * 64,
+                                                              n0 + wn * 64, half, l32, lane,
+                                                              stage, acc);
 }
 
 // Rounding of fp32 matrices to bf16 copies: one thread per 8 output
