@@ -128,12 +128,6 @@ __device__ __forceinline__ TileInfo decode_tile(const GemmBatch& batch) {
     return ti;
 }
 
-// Epilogue of a wavefront's 64 x 64 block (2 x 2 accumulators of 32 x 32).
-// The MFMAs take the B fragment as their first operand, so they produce the
-// transposed block: accumulator element r of lane l is C[i][j] of its
-// 32 x 32 block with i = l % 32 and j = (r % 4) + 8 (r / 4) + 4 (l / 32).
-// Every lane thus holds four runs of four consecutive columns of one row,
-// stored (and masked) with 16-byte accesses where the row is aligned.
 __device__ __forceinline__ bf16x4 to_bf16(float a, float b, float c, float d) {
     bf16x4 r;
     r[0] = (__bf16)a;
@@ -143,58 +137,21 @@ __device__ __forceinline__ bf16x4 to_bf16(float a, float b, float c, float d) {
     return r;
 }
 
-// HC: also write the finished values, rounded to bf16, to P.hC when set.
-// PRE: everything the epilogue reads (mask, bias) is loaded before its
-// first store. The compiler must assume C may alias them, so loads placed
-// between stores each wait for the store before them; the bf16 kernels,
-// whose K loops are short, gain from the preload, while in the fp32 kernel
-// the other workgroup on the CU hides those waits and the preload's extra
-// registers cost more than it saves.
-template <Epilogue EP, bool HC = false, bool PRE = false>
+// Epilogue of a wavefront's 64 x 64 block (2 x 2 accumulators of 32 x 32).
+// The MFMAs take the B fragment as their first operand, so they produce the
+// transposed block: accumulator element r of lane l is C[i][j] of its
+// 32 x 32 block with i = l % 32 and j = (r % 4) + 8 (r / 4) + 4 (l / 32).
+// Every lane thus holds four runs of four consecutive columns of one row,
+// stored (and masked) with 16-byte accesses where the row is aligned.
+template <Epilogue EP>
 __device__ __forceinline__ void store_tile(const GemmProblem& P, int split, int mw, int nw,
                                            int half, int l32, const floatx16 (&acc)[2][2]) {
     float* C = P.C;
     if constexpr (EP == EPI_PARTIAL) C += (int64_t)split * P.part_stride;
     const bool cvec = ((reinterpret_cast<uintptr_t>(C) | (uintptr_t)(P.ldc * 4)) & 15) == 0;
-    // mask values of this lane's outputs (EPI_MASK), bias of its columns (EPI_BIAS*)
-    float mk[2][2][4][4];
-    float bv[2][4][4];
-    const bool mvec =
-        EP == EPI_MASK &&
-        ((reinterpret_cast<uintptr_t>(P.mask) | (uintptr_t)(P.ldmask * 4)) & 15) == 0;
-    if constexpr (PRE && EP == EPI_MASK) {
-#pragma unroll
-        for (int bi = 0; bi < 2; ++bi) {
-            const int m = mw + bi * 32 + l32;
-#pragma unroll
-            for (int bj = 0; bj < 2; ++bj)
-#pragma unroll
-                for (int g = 0; g < 4; ++g) {
-                    const int n = nw + bj * 32 + 8 * g + 4 * half;
-                    const float* mp = P.mask + (int64_t)m * P.ldmask + n;
-                    if (m < P.M && n + 4 <= P.N && mvec) {
-                        const float4 q = ld4(mp);
-                        mk[bi][bj][g][0] = q.x, mk[bi][bj][g][1] = q.y;
-                        mk[bi][bj][g][2] = q.z, mk[bi][bj][g][3] = q.w;
-                    } else {
-#pragma unroll
-                        for (int t = 0; t < 4; ++t)
-                            mk[bi][bj][g][t] = (m < P.M && n + t < P.N) ? mp[t] : 0.f;
-                    }
-                }
-        }
-    }
-    if constexpr (PRE && (EP == EPI_BIAS_RELU || EP == EPI_BIAS)) {
-#pragma unroll
-        for (int bj = 0; bj < 2; ++bj)
-#pragma unroll
-            for (int g = 0; g < 4; ++g) {
-                const int n = nw + bj * 32 + 8 * g + 4 * half;
-#pragma unroll
-                for (int t = 0; t < 4; ++t)
-                    bv[bj][g][t] = (P.bias && n + t < P.N) ? P.bias[n + t] : 0.f;
-            }
-    }
+    bool mvec = false;
+    if constexpr (EP == EPI_MASK)
+        mvec = ((reinterpret_cast<uintptr_t>(P.mask) | (uintptr_t)(P.ldmask * 4)) & 15) == 0;
 #pragma unroll
     for (int bi = 0; bi < 2; ++bi) {
         const int m = mw + bi * 32 + l32;
@@ -214,10 +171,7 @@ __device__ __forceinline__ void store_tile(const GemmProblem& P, int split, int 
                     if (P.bias) {
 #pragma unroll
                         for (int t = 0; t < 4; ++t)
-                            if constexpr (PRE)
-                                v[t] += bv[bj][g][t];
-                            else if (n + t < P.N)
-                                v[t] += P.bias[n + t];
+                            if (n + t < P.N) v[t] += P.bias[n + t];
                     }
                     if constexpr (EP == EPI_BIAS_RELU) {
                         if (!P.no_relu) {
@@ -226,22 +180,17 @@ __device__ __forceinline__ void store_tile(const GemmProblem& P, int split, int 
                         }
                     }
                 } else if constexpr (EP == EPI_MASK) {
-                    float hm[4];
-                    if constexpr (PRE) {
-#pragma unroll
-                        for (int t = 0; t < 4; ++t) hm[t] = mk[bi][bj][g][t];
+                    const float* mp = P.mask + (int64_t)m * P.ldmask + n;
+                    float h[4];
+                    if (whole && mvec) {
+                        const float4 q = ld4(mp);
+                        h[0] = q.x, h[1] = q.y, h[2] = q.z, h[3] = q.w;
                     } else {
-                        const float* mp = P.mask + (int64_t)m * P.ldmask + n;
-                        if (whole && mvec) {
-                            const float4 q = ld4(mp);
-                            hm[0] = q.x, hm[1] = q.y, hm[2] = q.z, hm[3] = q.w;
-                        } else {
 #pragma unroll
-                            for (int t = 0; t < 4; ++t) hm[t] = n + t < P.N ? mp[t] : 0.f;
-                        }
+                        for (int t = 0; t < 4; ++t) h[t] = n + t < P.N ? mp[t] : 0.f;
                     }
 #pragma unroll
-                    for (int t = 0; t < 4; ++t) v[t] = hm[t] > 0.f ? v[t] : 0.f;
+                    for (int t = 0; t < 4; ++t) v[t] = h[t] > 0.f ? v[t] : 0.f;
                 }
                 if (whole && cvec) {
                     *reinterpret_cast<float4*>(crow + n) = make_float4(v[0], v[1], v[2], v[3]);
@@ -250,16 +199,106 @@ __device__ __forceinline__ void store_tile(const GemmProblem& P, int split, int 
                     for (int t = 0; t < 4; ++t)
                         if (n + t < P.N) crow[n + t] = v[t];
                 }
-                if constexpr (HC) {
-                    if (P.hC) {
-                        __bf16* hrow = P.hC + (int64_t)m * P.ldhc + n;
-                        if (whole) {
-                            *reinterpret_cast<bf16x4*>(hrow) = to_bf16(v[0], v[1], v[2], v[3]);
-                        } else {
+            }
+        }
+    }
+}
+
+// Epilogue through LDS: the wavefront's 64 x 64 block goes to `stage` (its
+// own 2176 floats of the freed operand buffers) 32 rows at a time, and is
+// read back so that each load and store instruction covers four whole
+// 256-byte row runs (16 lanes per row) instead of 32 rows x 32 bytes.
+// HC: also the bf16 copy. The caller has synchronised the workgroup.
+template <Epilogue EP, bool HC>
+__device__ __forceinline__ void store_tile_lds(const GemmProblem& P, int split, int mw, int nw,
+                                               int half, int l32, int lane, float* stage,
+                                               const floatx16 (&acc)[2][2]) {
+    constexpr int kSS = 64 + 4;   // staged row stride, floats
+    float* C = P.C;
+    if constexpr (EP == EPI_PARTIAL) C += (int64_t)split * P.part_stride;
+    const bool cvec = ((reinterpret_cast<uintptr_t>(C) | (uintptr_t)(P.ldc * 4)) & 15) == 0;
+    const bool mvec =
+        EP == EPI_MASK &&
+        ((reinterpret_cast<uintptr_t>(P.mask) | (uintptr_t)(P.ldmask * 4)) & 15) == 0;
+    const int c = 4 * (lane & 15);   // this lane's four columns of the block
+    const int n = nw + c;
+    const bool whole = n + 4 <= P.N;
+    float bv[4] = {0.f, 0.f, 0.f, 0.f};
+    if constexpr (EP == EPI_BIAS_RELU || EP == EPI_BIAS) {
+        if (P.bias) {
 #pragma unroll
-                            for (int t = 0; t < 4; ++t)
-                                if (n + t < P.N) hrow[t] = (__bf16)v[t];
-                        }
+            for (int t = 0; t < 4; ++t) bv[t] = n + t < P.N ? P.bias[n + t] : 0.f;
+        }
+    }
+#pragma unroll
+    for (int bi = 0; bi < 2; ++bi) {
+        // lane (l32, half): row l32, columns 32 bj + 8 g + 4 half .. + 3
+#pragma unroll
+        for (int bj = 0; bj < 2; ++bj)
+#pragma unroll
+            for (int g = 0; g < 4; ++g)
+                *reinterpret_cast<float4*>(&stage[l32 * kSS + 32 * bj + 8 * g + 4 * half]) =
+                    make_float4(acc[bi][bj][4 * g], acc[bi][bj][4 * g + 1],
+                                acc[bi][bj][4 * g + 2], acc[bi][bj][4 * g + 3]);
+        __syncthreads();
+        // lane l: rows l / 16 + 4 k of the 32, columns c .. c + 3
+        float v[8][4];
+        float mk[8][4];
+#pragma unroll
+        for (int k = 0; k < 8; ++k) {
+            const int r = (lane >> 4) + 4 * k;
+            const float4 q = *reinterpret_cast<const float4*>(&stage[r * kSS + c]);
+            v[k][0] = q.x, v[k][1] = q.y, v[k][2] = q.z, v[k][3] = q.w;
+            if constexpr (EP == EPI_MASK) {
+                const int m = mw + 32 * bi + r;
+                const float* mp = P.mask + (int64_t)m * P.ldmask + n;
+                if (m < P.M && whole && mvec) {
+                    const float4 h = ld4(mp);
+                    mk[k][0] = h.x, mk[k][1] = h.y, mk[k][2] = h.z, mk[k][3] = h.w;
+                } else {
+#pragma unroll
+                    for (int t = 0; t < 4; ++t) mk[k][t] = (m < P.M && n + t < P.N) ? mp[t] : 0.f;
+                }
+            }
+        }
+        __syncthreads();   // the stage is rewritten by the next pass
+#pragma unroll
+        for (int k = 0; k < 8; ++k) {
+            const int m = mw + 32 * bi + (lane >> 4) + 4 * k;
+            if (m >= P.M || n >= P.N) continue;
+            float* w = v[k];
+            if constexpr (EP == EPI_BIAS_RELU || EP == EPI_BIAS) {
+                if (P.bias) {
+#pragma unroll
+                    for (int t = 0; t < 4; ++t) w[t] += bv[t];
+                }
+                if constexpr (EP == EPI_BIAS_RELU) {
+                    if (!P.no_relu) {
+#pragma unroll
+                        for (int t = 0; t < 4; ++t) w[t] = w[t] > 0.f ? w[t] : 0.f;
+                    }
+                }
+            } else if constexpr (EP == EPI_MASK) {
+#pragma unroll
+                for (int t = 0; t < 4; ++t) w[t] = mk[k][t] > 0.f ? w[t] : 0.f;
+            }
+            float* crow = C + (int64_t)m * P.ldc;
+            if (whole && cvec) {
+                *reinterpret_cast<float4*>(crow + n) = make_float4(w[0], w[1], w[2], w[3]);
+            } else {
+#pragma unroll
+                for (int t = 0; t < 4; ++t)
+                    if (n + t < P.N) crow[n + t] = w[t];
+            }
+            if constexpr (HC) {
+                if (P.hC) {
+                    __bf16* hrow = P.hC + (int64_t)m * P.ldhc + n;
+                    if (whole) {
+                        *reinterpret_cast<bf16x4*>(hrow) = to_bf16(w[0], w[1], w[2], w[3]);
+                    } else {
+#pragma unroll
+                        for (int t = 0; t < 4; ++t)
+                            if (n + t < P.N) hrow[t] = (__bf16)w[t];
                     }
                 }
             }
@@ -837,7 +876,7 @@ __global__ __launch_bounds__(kThreads, 2) void gemm_bf16_kernel(GemmBatch batch)
     }
     if (kt < nk) kstep(kt, 0, Masked{});
 
-    store_tile<EP, false, true>(P, split, m0 + wm * 64, n0 + wn * 64, half, l32, acc);
+    store_tile<EP>(P, split, m0 + wm * 64, n0 + wn * 64, half, l32, acc);
 }
 
 // ------------------------------------------------------------ bf16 copies
@@ -885,108 +924,6 @@ __device__ __forceinline__ u32x4 finish16(const HChunk& q) {
 
 __device__ __forceinline__ u32x4 ld16(const __bf16* p) {
     return *reinterpret_cast<const u32x4*>(p);
-}
-
-// Epilogue through LDS: the wavefront's 64 x 64 block goes to `stage` (its
-// own 2176 floats of the freed operand buffers) 32 rows at a time, and is
-// read back so that each load and store instruction covers four whole
-// 256-byte row runs (16 lanes per row) instead of 32 rows x 32 bytes.
-// HC: also the bf16 copy. The caller has synchronised the workgroup.
-template <Epilogue EP, bool HC>
-__device__ __forceinline__ void store_tile_lds(const GemmProblem& P, int split, int mw, int nw,
-                                               int half, int l32, int lane, float* stage,
-                                               const floatx16 (&acc)[2][2]) {
-    constexpr int kSS = 64 + 4;   // staged row stride, floats
-    float* C = P.C;
-    if constexpr (EP == EPI_PARTIAL) C += (int64_t)split * P.part_stride;
-    const bool cvec = ((reinterpret_cast<uintptr_t>(C) | (uintptr_t)(P.ldc * 4)) & 15) == 0;
-    const bool mvec =
-        EP == EPI_MASK &&
-        ((reinterpret_cast<uintptr_t>(P.mask) | (uintptr_t)(P.ldmask * 4)) & 15) == 0;
-    const int c = 4 * (lane & 15);   // this lane's four columns of the block
-    const int n = nw + c;
-    const bool whole = n + 4 <= P.N;
-    float bv[4] = {0.f, 0.f, 0.f, 0.f};
-    if constexpr (EP == EPI_BIAS_RELU || EP == EPI_BIAS) {
-        if (P.bias) {
-#pragma unroll
-            for (int t = 0; t < 4; ++t) bv[t] = n + t < P.N ? P.bias[n + t] : 0.f;
-        }
-    }
-#pragma unroll
-    for (int bi = 0; bi < 2; ++bi) {
-        // lane (l32, half): row l32, columns 32 bj + 8 g + 4 half .. + 3
-#pragma unroll
-        for (int bj = 0; bj < 2; ++bj)
-#pragma unroll
-            for (int g = 0; g < 4; ++g)
-                *reinterpret_cast<float4*>(&stage[l32 * kSS + 32 * bj + 8 * g + 4 * half]) =
-                    make_float4(acc[bi][bj][4 * g], acc[bi][bj][4 * g + 1],
-                                acc[bi][bj][4 * g + 2], acc[bi][bj][4 * g + 3]);
-        __syncthreads();
-        // lane l: rows l / 16 + 4 k of the 32, columns c .. c + 3
-        float v[8][4];
-        float mk[8][4];
-#pragma unroll
-        for (int k = 0; k < 8; ++k) {
-            const int r = (lane >> 4) + 4 * k;
-            const float4 q = *reinterpret_cast<const float4*>(&stage[r * kSS + c]);
-            v[k][0] = q.x, v[k][1] = q.y, v[k][2] = q.z, v[k][3] = q.w;
-            if constexpr (EP == EPI_MASK) {
-                const int m = mw + 32 * bi + r;
-                const float* mp = P.mask + (int64_t)m * P.ldmask + n;
-                if (m < P.M && whole && mvec) {
-                    const float4 h = ld4(mp);
-                    mk[k][0] = h.x, mk[k][1] = h.y, mk[k][2] = h.z, mk[k][3] = h.w;
-                } else {
-#pragma unroll
-                    for (int t = 0; t < 4; ++t) mk[k][t] = (m < P.M && n + t < P.N) ? mp[t] : 0.f;
-                }
-            }
-        }
-        __syncthreads();   // the stage is rewritten by the next pass
-#pragma unroll
-        for (int k = 0; k < 8; ++k) {
-            const int m = mw + 32 * bi + (lane >> 4) + 4 * k;
-            if (m >= P.M || n >= P.N) continue;
-            float* w = v[k];
-            if constexpr (EP == EPI_BIAS_RELU || EP == EPI_BIAS) {
-                if (P.bias) {
-#pragma unroll
-                    for (int t = 0; t < 4; ++t) w[t] += bv[t];
-                }
-                if constexpr (EP == EPI_BIAS_RELU) {
-                    if (!P.no_relu) {
-#pragma unroll
-                        for (int t = 0; t < 4; ++t) w[t] = w[t] > 0.f ? w[t] : 0.f;
-                    }
-                }
-            } else if constexpr (EP == EPI_MASK) {
-#pragma unroll
-                for (int t = 0; t < 4; ++t) w[t] = mk[k][t] > 0.f ? w[t] : 0.f;
-            }
-            float* crow = C + (int64_t)m * P.ldc;
-            if (whole && cvec) {
-                *reinterpret_cast<float4*>(crow + n) = make_float4(w[0], w[1], w[2], w[3]);
-            } else {
-#pragma unroll
-                for (int t = 0; t < 4; ++t)
-                    if (n + t < P.N) crow[n + t] = w[t];
-            }
-            if constexpr (HC) {
-                if (P.hC) {
-                    __bf16* hrow = P.hC + (int64_t)m * P.ldhc + n;
-                    if (whole) {
-                        *reinterpret_cast<bf16x4*>(hrow) = to_bf16(w[0], w[1], w[2], w[3]);
-                    } else {
-#pragma unroll
-                        for (int t = 0; t < 4; ++t)
-                            if (n + t < P.N) hrow[t] = (__bf16)w[t];
-                    }
-                }
-            }
-        }
-    }
 }
 
 template <ALayout AL, BLayout BL, Epilogue EP, GemmRole ROLE>
