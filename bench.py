@@ -276,7 +276,10 @@ def trace_summary(stats_csv, workload, cmd_args, bench_line=None):
         lines_k.append(f"| {c or '-'} | `{name[:110]}` | {calls} | "
                        f"{float(r['AverageNs']) / 1e3:.2f} | {tot / 1e6:.3f} |")
     bargs = f"--workload {workload} {cmd_args}"
-    out = [f"# Kernel durations, {workload} training step (rocprofv3 kernel trace)", "",
+    bf16 = "--precision bf16" in cmd_args
+    tag = f"{workload}_bf16" if bf16 else workload
+    out = [f"# Kernel durations, {workload} {'bf16 ' if bf16 else ''}training step "
+           "(rocprofv3 kernel trace)", "",
            "```", "cd /tmp && export TMPDIR=/tmp",
            f"rocprofv3 --kernel-trace --stats --output-format csv -d OUT -o run -- "
            f"python3 $R/bench.py {bargs}",
@@ -297,7 +300,7 @@ def trace_summary(stats_csv, workload, cmd_args, bench_line=None):
             out.append(f"| {c} | {k['avg_us']} |")
     out += ["", "## Per kernel", "", "| class | kernel | calls | mean us | total ms |",
             "|---|---|---:|---:|---:|"] + lines_k + [""]
-    path = os.path.join(ROOT, "profiles", f"{workload}_train_step_kernel_stats.md")
+    path = os.path.join(ROOT, "profiles", f"{tag}_train_step_kernel_stats.md")
     with open(path, "w") as fh:
         fh.write("\n".join(out))
     print(path)

@@ -124,3 +124,15 @@ def test_trace_summary_totals_per_class(scratch_root):
     cells = [c.strip() for c in row.strip("|").split("|")]
     assert cells == ["gemm_dw", "5", "120.00", "0.600"]   # 5 calls, 600 us in all
     assert "step alone" in txt
+
+
+def test_trace_summary_names_the_bf16_variant(scratch_root):
+    path = scratch_root / "stats.csv"
+    with open(path, "w", newline="") as fh:
+        w = csv.DictWriter(fh, fieldnames=["Name", "Calls", "TotalDurationNs", "AverageNs"])
+        w.writeheader()
+        w.writerow(dict(Name=H16.format(0), Calls=2, TotalDurationNs=100000, AverageNs=50000))
+    bench.trace_summary(str(path), "wl", "--precision bf16 --no-cpu-baseline")
+    txt = (scratch_root / "profiles" / "wl_bf16_train_step_kernel_stats.md").read_text()
+    assert "bf16 training step" in txt
+    assert "| gemm_fwd_bf16 | 2 | 50.00 | 0.100 |" in txt
