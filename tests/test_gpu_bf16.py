@@ -213,3 +213,18 @@ def test_step_bf16_copies_match_entry_points(name):
                        precision=gcn.PREC_BF16)
     torch.cuda.synchronize()
     assert torch.equal(Z, run.act(lay.logits, wl.n, wl.C, lay.ld_C))
+
+
+@pytest.mark.parametrize("n,dbar,f_in,C,bias,loss", [(5, 1, 1, 1, True, synth.SIGMOID_BCE),
+                                                     (70, 2, 3, 2, False, synth.SOFTMAX_CE),
+                                                     (130, 4, 8, 9, True, synth.SIGMOID_BCE)])
+def test_step_bf16_copies_tiny_shapes(n, dbar, f_in, C, bias, loss):
+    """The bf16-copies step at the smallest shapes: a single input feature
+    or class (8-element chunks nearly all padding), h = 8, isolated
+    vertices, M just past a tile, the row of ones alone in its tile."""
+    need_gpu()
+    from paper_2001_02498_amd import gcn
+    wl = synth.small_workload(n, dbar, 2, f_in, 8, C, loss, (n, f_in, C))
+    run = StepRun(wl, bias=bias, seg_len=3, precision=gcn.PREC_BF16).run()
+    assert run.layout.ah_bytes == 2
+    check_step(run, tol=BF16_TOL)

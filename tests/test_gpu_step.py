@@ -130,7 +130,7 @@ def check_step(run, tol=FP32_TOL):
         errs[f"H{l}"] = rel(run.act(lay.H[l], wl.n, 2 * wl.h, lay.ld_H), ref["fw"]["H"][l + 1])
     errs["logits"] = rel(run.act(lay.logits, wl.n, wl.C, lay.ld_C), ref["fw"]["logits"])
     errs["dlogits"] = rel(run.act(lay.dlogits, wl.n, wl.C, lay.ld_C), ref["dlogits"])
-    errs["loss"] = abs(run.loss - ref["loss"]) / abs(ref["loss"])
+    errs["loss"] = abs(run.loss - ref["loss"]) / max(abs(ref["loss"]), 1e-30)
     # masked gradients still resident: the last two written (layers 0 and 1)
     for l in range(min(2, wl.L)):
         errs[f"G{l}"] = rel(run.act(lay.G[l], wl.n, 2 * wl.h, lay.ld_H), ref["grads"]["G"][l])
