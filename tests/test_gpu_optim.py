@@ -12,7 +12,7 @@ import pytest
 from oracle import gcn as og
 from oracle import optim as oo
 from paper_2001_02498_amd import synth
-from tests.gpu_helpers import FP32_TOL, dev, need_gpu, rel, say, torch
+from tests.gpu_helpers import BF16_TOL, FP32_TOL, dev, need_gpu, rel, say, torch
 from tests.test_gpu_step import StepRun, _update_err
 
 pytestmark = pytest.mark.gpu
@@ -98,7 +98,7 @@ class OptRun(StepRun):
         self.state_dev = [to_dev(s) for s in self.state_np]
         S = [p for _, p in self.state_dev] + [None, None]
         desc = gcn.model_desc(wl.L, wl.f_in, wl.h, wl.C, wl.loss, X.stride(0),
-                              has_bias=self.bias)
+                              has_bias=self.bias, precision=self.precision)
         self.layout = gcn.workspace_layout(self.case.dg, desc)
         ws = gcn.alloc_ws(gcn.workspace_bytes(self.case.dg, desc))
         self.ws = ws
@@ -134,7 +134,7 @@ def _dev_tensor(run, key, l):
             "W_cls": lambda: Wc, "b_cls": lambda: bc}[key]()
 
 
-def check_opt(run, first_step_bound=False):
+def check_opt(run, first_step_bound=False, tol=FP32_TOL):
     ref = run.oracle()
     errs = {}
     for key, l in _named(run):
@@ -163,7 +163,7 @@ def check_opt(run, first_step_bound=False):
         say(tag, "firm", int(firm.sum()), "of", firm.size)
     worst = max(errs, key=errs.get)
     say("max error", worst, errs[worst])
-    bad = {k: v for k, v in errs.items() if not v < FP32_TOL}
+    bad = {k: v for k, v in errs.items() if not v < tol}
     assert not bad, bad
     return errs
 
@@ -236,3 +236,22 @@ def test_optim_errors_before_launch():
     torch.cuda.synchronize()
     for w0, w in zip(before, Ws):
         assert torch.equal(w0, w)
+
+
+@pytest.mark.parametrize("name,kind", [("ppi8k", oo.ADAM), ("tiny", oo.MOMENTUM)])
+def test_optim_bf16_step(name, kind):
+    """Optimisers in the bf16 step on operand copies: the weights' copies are
+    taken before their in-place update."""
+    need_gpu()
+    from paper_2001_02498_amd import gcn
+    run = OptRun(synth.WORKLOADS[name], kind, step=5, precision=gcn.PREC_BF16).run()
+    assert run.layout.ah_bytes == 2
+    check_opt(run, tol=BF16_TOL)
+
+
+def test_optim_bf16_ragged_with_bias():
+    need_gpu()
+    from paper_2001_02498_amd import gcn
+    wl = synth.small_workload(437, 9, 2, 29, 40, 7, synth.SIGMOID_BCE, (2, 9, 16))
+    run = OptRun(wl, oo.ADAM, step=3, bias=True, seg_len=4, precision=gcn.PREC_BF16).run()
+    check_opt(run, tol=BF16_TOL)
