@@ -65,7 +65,7 @@ const char* gcn_last_error(void);
 
 /* ABI version of this header (bumped on incompatible change). */
 int gcn_abi_version(void);
-#define GCN_ABI_VERSION 3
+#define GCN_ABI_VERSION 4
 
 /* ------------------------------------------------ subgraph (host, a1)
  * gcn_subgraph_build - undirected simple subgraph in CSR form.
@@ -390,7 +390,9 @@ int gcn_layer_bwd(const gcn_dgraph* g, int32_t F, int32_t h, const float* G,
  *   (X and the weights are rounded once at the start of the step), and the
  *   products read those copies: the same rounded operands as the per-layer
  *   entry points' bf16 products, at half the operand bytes. AH, read only
- *   by products, is then stored in bf16 only (layout field ah_bytes = 2).
+ *   by products, is then stored in bf16 only (layout field ah_bytes = 2),
+ *   and the fp32 G[l] only where the fp32 aggregation reads it: columns
+ *   [h, 2h) for l >= 1, none for l = 0 (the full gradients are G16).
  *   Otherwise (narrow order, h % 8 != 0) the products round fp32 operands
  *   on the way, as in the per-layer entry points.
  */
@@ -426,6 +428,11 @@ typedef struct {          /* byte offsets into ws, -1 when absent */
     int64_t scratch, scratch_bytes, total_bytes;
     int64_t ah_bytes;                 /* bytes per AH element: 4 (float),
                                          2 (bf16, see gcn_train_step) */
+    int64_t H16[GCN_MAX_LAYERS];      /* bf16 step with operand copies
+                                         (ah_bytes = 2): bf16 copies of
+                                         H[l] and of G[l], ld ld_H (G16
+                                         ping-pongs like G); -1 else */
+    int64_t G16[GCN_MAX_LAYERS];
 } gcn_ws_layout;
 
 int gcn_workspace_layout(const gcn_dgraph* g, const gcn_model_desc* desc,

@@ -171,6 +171,7 @@ struct LayerCopies {
     int64_t ldt;
     __bf16* Gin;         // input gradient (backward)         [n x F]
     int64_t ldgi;
+    int32_t gin_fp32_from;   // first column of Gin also kept in fp32
 };
 
 int do_layer_fwd(const char* fn, const gcn_dgraph* g, int32_t F, int32_t h,
@@ -343,6 +344,7 @@ struct ClsCopies {
     int64_t lddz;
     __bf16* G;          // input gradient, written    [n x K]
     int64_t ldg;
+    int32_t g_fp32_from;   // first column of G also kept in fp32
 };
 
 int do_classifier_bwd(const char* fn, int32_t n, int32_t K, int32_t C,
@@ -376,6 +378,7 @@ int do_classifier_bwd(const char* fn, int32_t n, int32_t K, int32_t C,
             p.hldb0 = p.hldb1 = c->ldw;
             p.hC = c->G;
             p.ldhc = c->ldg;
+            p.c_from = c->g_fp32_from;
         }
         b.p[0] = p;
         GCN_HIP(launch_gemm(b, A_MK, B_NK, EPI_MASK, ROLE_CLS_DX, bf16, s), fn);
@@ -445,6 +448,7 @@ int do_layer_bwd(const char* fn, const gcn_dgraph* g, int32_t F, int32_t h,
             p.hldb0 = p.hldb1 = h;
             p.hC = c->Gin;
             p.ldhc = c->ldgi;
+            p.c_from = c->gin_fp32_from;
         }
         b.p[0] = p;
         GCN_HIP(launch_gemm(b, A_MK, B_NK, EPI_MASK, ROLE_DX, bf16, s), fn);
@@ -604,6 +608,7 @@ int plan_step(const gcn_dgraph* g, const gcn_model_desc* d, StepLayout* out) {
     std::memset(&cp, 0, sizeof(cp));
     cp.on = copies;
     out->pub.ah_bytes = copies ? 2 : 4;
+    for (int i = 0; i < GCN_MAX_LAYERS; ++i) out->pub.H16[i] = out->pub.G16[i] = -1;
     for (int l = 0; l < d->L; ++l) {
         const int64_t F = l == 0 ? d->f_in : 2 * (int64_t)d->h;
         out->pub.ld_AH[l] = copies ? r8(F) : r4(F);
@@ -631,6 +636,10 @@ int plan_step(const gcn_dgraph* g, const gcn_model_desc* d, StepLayout* out) {
         for (int l = 0; l < d->L; ++l) cp.H[l] = take(2 * n * ldH);
         const int64_t h0 = take(2 * n * ldH), h1 = take(2 * n * ldH);
         for (int l = 0; l < d->L; ++l) cp.G[l] = ((d->L - 1 - l) % 2 == 0) ? h0 : h1;
+        for (int l = 0; l < d->L; ++l) {
+            out->pub.H16[l] = cp.H[l];
+            out->pub.G16[l] = cp.G[l];
+        }
         cp.T = take(2 * n * ldH);
         cp.ld_dz = r8(d->C);
         cp.dZ = take(2 * n * cp.ld_dz);
@@ -966,6 +975,9 @@ int train_step_impl(const char* fn, const gcn_dgraph* g, const gcn_model_desc* d
         c.ldt = ldH;
         c.Gin = l > 0 ? h16(cp.G[l - 1]) : nullptr;
         c.ldgi = ldH;
+        // the fp32 aggregation of the layer below reads only the neighbour
+        // half of its gradient; the first layer aggregates none
+        c.gin_fp32_from = l > 1 ? h : 2 * h;
         return c;
     };
 
@@ -1017,7 +1029,8 @@ int train_step_impl(const char* fn, const gcn_dgraph* g, const gcn_model_desc* d
     const ClsCopies cc{cp.on ? h16(cp.H[L - 1]) : nullptr, ldH,
                        cp.on ? h16(cp.Wc) : nullptr, cp.ld_wc,
                        cp.on ? h16(cp.dZ) : nullptr, cp.ld_dz,
-                       cp.on ? h16(cp.G[L - 1]) : nullptr, ldH};
+                       cp.on ? h16(cp.G[L - 1]) : nullptr, ldH,
+                       L > 1 ? h : 2 * h};
     GCN_TRY(do_classifier_bwd(fn, (int32_t)n, 2 * h, C, dZ, ldC, Hprev, ldH, P->W_cls,
                               d->has_bias ? P->b_cls : nullptr, oa, cst, Gcur, ldH,
                               grads ? grads->W_cls : nullptr,

@@ -282,13 +282,15 @@ __device__ __forceinline__ void store_tile_lds(const GemmProblem& P, int split, 
 #pragma unroll
                 for (int t = 0; t < 4; ++t) w[t] = mk[k][t] > 0.f ? w[t] : 0.f;
             }
-            float* crow = C + (int64_t)m * P.ldc;
-            if (whole && cvec) {
-                *reinterpret_cast<float4*>(crow + n) = make_float4(w[0], w[1], w[2], w[3]);
-            } else {
+            if (!HC || !P.hC || n >= P.c_from) {
+                float* crow = C + (int64_t)m * P.ldc;
+                if (whole && cvec) {
+                    *reinterpret_cast<float4*>(crow + n) = make_float4(w[0], w[1], w[2], w[3]);
+                } else {
 #pragma unroll
-                for (int t = 0; t < 4; ++t)
-                    if (n + t < P.N) crow[n + t] = w[t];
+                    for (int t = 0; t < 4; ++t)
+                        if (n + t < P.N) crow[n + t] = w[t];
+                }
             }
             if constexpr (HC) {
                 if (P.hC) {
@@ -1355,7 +1357,8 @@ hipError_t launch_gemm(GemmBatch& b, ALayout al, BLayout bl, Epilogue ep, GemmRo
             const GemmProblem& p = b.p[i];
             const bool catA = al == A_MK && p.ksplitA < p.K;
             const bool catB = bl == B_NK && p.ksplitB < p.K;
-            if (!ok16(p.hA0, p.hlda0) || !ok16(p.hB0, p.hldb0) ||
+            if ((p.hC && p.c_from % 4) || (!p.C && !(p.hC && p.c_from >= p.N)) ||
+                !ok16(p.hA0, p.hlda0) || !ok16(p.hB0, p.hldb0) ||
                 (catA && (!p.hA1 || !ok16(p.hA1, p.hlda1) || p.ksplitA % 8)) ||
                 (catB && (!p.hB1 || !ok16(p.hB1, p.hldb1) || p.ksplitB % 8)) ||
                 (p.hC && (((uintptr_t)p.hC & 7) || (p.ldhc & 3))))
@@ -1366,8 +1369,9 @@ hipError_t launch_gemm(GemmBatch& b, ALayout al, BLayout bl, Epilogue ep, GemmRo
         for (int i = 0; i < b.nprob; ++i) {
             const GemmProblem& p = b.p[i];
             const double M = p.M, N = p.N, K = p.K;
-            bytes += 2.0 * (M * K + K * N) + 4.0 * M * N + (ep == EPI_MASK ? 4.0 * M * N : 0.0) +
-                     (p.hC ? 2.0 * M * N : 0.0);
+            const double n32 = p.hC ? std::max(0.0, N - p.c_from) : N;   // fp32 columns
+            bytes += 2.0 * (M * K + K * N) + 4.0 * M * n32 +
+                     (ep == EPI_MASK ? 4.0 * M * N : 0.0) + (p.hC ? 2.0 * M * N : 0.0);
         }
     }
     const int kind = kKinds[role] + (bf16 ? K_GEMM_BF16_OFFSET : 0);

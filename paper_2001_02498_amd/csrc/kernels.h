@@ -91,6 +91,9 @@ struct GemmProblem {
     // leading dimension a multiple of 4
     __bf16* hC;
     int64_t ldhc;
+    // with hC: the fp32 output C is written only for columns >= c_from (a
+    // multiple of 4; N or more: not at all, C may then be NULL)
+    int32_t c_from;
 };
 
 constexpr int kMaxProblems = 2;

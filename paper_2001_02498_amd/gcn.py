@@ -43,7 +43,7 @@ OPT_MOMENTUM = 1
 OPT_ADAM = 2
 AGG_MEAN = 0
 AGG_TRANSPOSED = 1
-ABI_VERSION = 3
+ABI_VERSION = 4
 
 _i32, _i64, _f32 = C.c_int32, C.c_int64, C.c_float
 _vp, _sz = C.c_void_p, C.c_size_t
@@ -94,7 +94,7 @@ class WsLayout(C.Structure):
                 ("logits", _i64), ("dlogits", _i64), ("ld_C", _i64),
                 ("G", _i64 * MAX_LAYERS),
                 ("scratch", _i64), ("scratch_bytes", _i64), ("total_bytes", _i64),
-                ("ah_bytes", _i64)]
+                ("ah_bytes", _i64), ("H16", _i64 * MAX_LAYERS), ("G16", _i64 * MAX_LAYERS)]
 
 
 def _proto(name, args, res=C.c_int):

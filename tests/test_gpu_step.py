@@ -84,14 +84,18 @@ class StepRun:
         t = self.ws[off:off + 4 * rows * ld].view(torch.float32).view(rows, ld)
         return t[:, :cols]
 
+    def act16(self, off, rows, cols, ld):
+        """A bf16 region of the workspace, as bf16."""
+        t = self.ws[off:off + 2 * rows * ld].view(torch.bfloat16).view(rows, ld)
+        return t[:, :cols]
+
     def ah(self, l, rows, cols):
         """Layer l's AH region as float32 (the bf16 step keeps it in bf16)."""
         lay = self.layout
         off, ld = lay.AH[l], lay.ld_AH[l]
         if lay.ah_bytes == 4:
             return self.act(off, rows, cols, ld)
-        t = self.ws[off:off + 2 * rows * ld].view(torch.bfloat16).view(rows, ld)
-        return t[:, :cols].float()
+        return self.act16(off, rows, cols, ld).float()
 
     def oracle(self):
         wl, inp = self.wl, self.inp
@@ -132,8 +136,22 @@ def check_step(run, tol=FP32_TOL):
     errs["dlogits"] = rel(run.act(lay.dlogits, wl.n, wl.C, lay.ld_C), ref["dlogits"])
     errs["loss"] = abs(run.loss - ref["loss"]) / max(abs(ref["loss"]), 1e-30)
     # masked gradients still resident: the last two written (layers 0 and 1)
+    h = wl.h
     for l in range(min(2, wl.L)):
-        errs[f"G{l}"] = rel(run.act(lay.G[l], wl.n, 2 * wl.h, lay.ld_H), ref["grads"]["G"][l])
+        G_ref = ref["grads"]["G"][l]
+        if lay.ah_bytes == 4:
+            errs[f"G{l}"] = rel(run.act(lay.G[l], wl.n, 2 * h, lay.ld_H), G_ref)
+            continue
+        # bf16 step on operand copies: the full gradient in bf16, the fp32
+        # one only where the fp32 aggregation reads it
+        errs[f"G16_{l}"] = rel(run.act16(lay.G16[l], wl.n, 2 * h, lay.ld_H).float(), G_ref)
+        if l >= 1:
+            errs[f"G{l}n"] = rel(run.act(lay.G[l], wl.n, 2 * h, lay.ld_H)[:, h:], G_ref[:, h:])
+    if lay.ah_bytes == 2:
+        for l in range(wl.L):
+            H = run.act(lay.H[l], wl.n, 2 * h, lay.ld_H)
+            assert torch.equal(run.act16(lay.H16[l], wl.n, 2 * h, lay.ld_H),
+                               H.to(torch.bfloat16)), l
     gWs, gWn, gWc, gb, gbc = run.grads_dev
     Ws, Wn, Wc, b, bc = run.dev_params
     g = ref["grads"]
