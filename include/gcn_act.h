@@ -392,7 +392,10 @@ int gcn_layer_bwd(const gcn_dgraph* g, int32_t F, int32_t h, const float* G,
  *   entry points' bf16 products, at half the operand bytes. AH, read only
  *   by products, is then stored in bf16 only (layout field ah_bytes = 2),
  *   and the fp32 G[l] only where the fp32 aggregation reads it: columns
- *   [h, 2h) for l >= 1, none for l = 0 (the full gradients are G16).
+ *   [h, 2h) for l >= 1, none for l = 0 (the full gradients are G16); the
+ *   last layer's fp32 H is not written either (H16 holds it), and the
+ *   backward's ReLU masks are read from H16, which has the fp32 sign
+ *   except for activations in (0, 2^-134].
  *   Otherwise (narrow order, h % 8 != 0) the products round fp32 operands
  *   on the way, as in the per-layer entry points.
  */

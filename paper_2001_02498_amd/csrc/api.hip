@@ -165,6 +165,7 @@ struct LayerCopies {
     const __bf16* Wn;
     __bf16* Hout;        // layer output (forward)            [n x 2h]
     int64_t ld_hout;
+    bool hout_fp32;      // the fp32 output is read later (by an aggregation)
     const __bf16* G;     // output gradient (backward)        [n x 2h]
     int64_t ldg;
     __bf16* T;           // aggregated neighbour gradient, bf16 only
@@ -205,6 +206,7 @@ int do_layer_fwd(const char* fn, const gcn_dgraph* g, int32_t F, int32_t h,
             p.hldb0 = p.hldb1 = h;
             p.hC = c->Hout + (i == 0 ? 0 : h);
             p.ldhc = c->ld_hout;
+            p.c_from = c->hout_fp32 ? 0 : h;
         }
         b.p[i] = p;
     }
@@ -379,6 +381,8 @@ int do_classifier_bwd(const char* fn, int32_t n, int32_t K, int32_t C,
             p.hC = c->G;
             p.ldhc = c->ldg;
             p.c_from = c->g_fp32_from;
+            p.hmask = c->H;   // the ReLU mask of H from its bf16 copy
+            p.ldhmask = c->ldh;
         }
         b.p[0] = p;
         GCN_HIP(launch_gemm(b, A_MK, B_NK, EPI_MASK, ROLE_CLS_DX, bf16, s), fn);
@@ -449,6 +453,8 @@ int do_layer_bwd(const char* fn, const gcn_dgraph* g, int32_t F, int32_t h,
             p.hC = c->Gin;
             p.ldhc = c->ldgi;
             p.c_from = c->gin_fp32_from;
+            p.hmask = c->Hin;   // the ReLU mask of H_in from its bf16 copy
+            p.ldhmask = c->ld_hin;
         }
         b.p[0] = p;
         GCN_HIP(launch_gemm(b, A_MK, B_NK, EPI_MASK, ROLE_DX, bf16, s), fn);
@@ -969,6 +975,7 @@ int train_step_impl(const char* fn, const gcn_dgraph* g, const gcn_model_desc* d
         c.Wn = h16(cp.Wn[l]);
         c.Hout = h16(cp.H[l]);
         c.ld_hout = ldH;
+        c.hout_fp32 = l < L - 1;   // the next layer aggregates it
         c.G = h16(cp.G[l]);
         c.ldg = ldH;
         c.T = h16(cp.T);

@@ -249,6 +249,24 @@ __device__ __forceinline__ void store_tile_lds(const GemmProblem& P, int split, 
             const int r = (lane >> 4) + 4 * k;
             const float4 q = *reinterpret_cast<const float4*>(&stage[r * kSS + c]);
             v[k][0] = q.x, v[k][1] = q.y, v[k][2] = q.z, v[k][3] = q.w;
+            if constexpr (EP == EPI_MASK && HC) {
+                if (P.hmask) {
+                    // only the sign is used: for the non-negative activations
+                    // a mask reads, bf16(x) > 0 exactly when x > 2^-134
+                    const int m = mw + 32 * bi + r;
+                    const __bf16* mp = P.hmask + (int64_t)m * P.ldhmask + n;
+                    if (m < P.M && whole) {
+                        const bf16x4 h = *reinterpret_cast<const bf16x4*>(mp);
+#pragma unroll
+                        for (int t = 0; t < 4; ++t) mk[k][t] = (float)h[t];
+                    } else {
+#pragma unroll
+                        for (int t = 0; t < 4; ++t)
+                            mk[k][t] = (m < P.M && n + t < P.N) ? (float)mp[t] : 0.f;
+                    }
+                    continue;
+                }
+            }
             if constexpr (EP == EPI_MASK) {
                 const int m = mw + 32 * bi + r;
                 const float* mp = P.mask + (int64_t)m * P.ldmask + n;
@@ -1358,6 +1376,7 @@ hipError_t launch_gemm(GemmBatch& b, ALayout al, BLayout bl, Epilogue ep, GemmRo
             const bool catA = al == A_MK && p.ksplitA < p.K;
             const bool catB = bl == B_NK && p.ksplitB < p.K;
             if ((p.hC && p.c_from % 4) || (!p.C && !(p.hC && p.c_from >= p.N)) ||
+                (p.hmask && (((uintptr_t)p.hmask & 7) || (p.ldhmask & 3))) ||
                 !ok16(p.hA0, p.hlda0) || !ok16(p.hB0, p.hldb0) ||
                 (catA && (!p.hA1 || !ok16(p.hA1, p.hlda1) || p.ksplitA % 8)) ||
                 (catB && (!p.hB1 || !ok16(p.hB1, p.hldb1) || p.ksplitB % 8)) ||
@@ -1371,7 +1390,8 @@ hipError_t launch_gemm(GemmBatch& b, ALayout al, BLayout bl, Epilogue ep, GemmRo
             const double M = p.M, N = p.N, K = p.K;
             const double n32 = p.hC ? std::max(0.0, N - p.c_from) : N;   // fp32 columns
             bytes += 2.0 * (M * K + K * N) + 4.0 * M * n32 +
-                     (ep == EPI_MASK ? 4.0 * M * N : 0.0) + (p.hC ? 2.0 * M * N : 0.0);
+                     (ep == EPI_MASK ? (p.hmask ? 2.0 : 4.0) * M * N : 0.0) +
+                     (p.hC ? 2.0 * M * N : 0.0);
         }
     }
     const int kind = kKinds[role] + (bf16 ? K_GEMM_BF16_OFFSET : 0);

@@ -94,6 +94,10 @@ struct GemmProblem {
     // with hC: the fp32 output C is written only for columns >= c_from (a
     // multiple of 4; N or more: not at all, C may then be NULL)
     int32_t c_from;
+    // EPI_MASK in the copies kernel: the mask read from this bf16 matrix
+    // (leading dimension a multiple of 4) instead of `mask`, when set
+    const __bf16* hmask;
+    int64_t ldhmask;
 };
 
 constexpr int kMaxProblems = 2;

@@ -115,9 +115,8 @@ class OptRun(StepRun):
         return self
 
     def oracle(self):
-        wl, lay = self.wl, self.layout
-        masks = [self.act(lay.H[l], wl.n, 2 * wl.h, lay.ld_H).cpu().numpy() > 0
-                 for l in range(wl.L)]
+        wl = self.wl
+        masks = self.masks()
         opt = oo.Optim(self.kind, lr=self.hp["lr"], step=self.step,
                        momentum=self.hp["momentum"], beta1=self.hp["beta1"],
                        beta2=self.hp["beta2"], eps=self.hp["eps"])

@@ -97,11 +97,28 @@ class StepRun:
             return self.act(off, rows, cols, ld)
         return self.act16(off, rows, cols, ld).float()
 
+    def H(self, l):
+        """Layer l's output as float32: the fp32 activations, or in the bf16
+        step on operand copies their bf16 copy where no fp32 one is kept
+        (the last layer)."""
+        wl, lay = self.wl, self.layout
+        if lay.ah_bytes == 2 and l == wl.L - 1:
+            return self.act16(lay.H16[l], wl.n, 2 * wl.h, lay.ld_H).float()
+        return self.act(lay.H[l], wl.n, 2 * wl.h, lay.ld_H)
+
+    def masks(self):
+        """The ReLU decisions the kernels took: from the fp32 activations, or
+        in the bf16 step on operand copies from their bf16 copies."""
+        wl, lay = self.wl, self.layout
+        if lay.ah_bytes == 2:
+            return [self.act16(lay.H16[l], wl.n, 2 * wl.h, lay.ld_H).float().cpu().numpy() > 0
+                    for l in range(wl.L)]
+        return [self.act(lay.H[l], wl.n, 2 * wl.h, lay.ld_H).cpu().numpy() > 0
+                for l in range(wl.L)]
+
     def oracle(self):
         wl, inp = self.wl, self.inp
-        lay = self.layout
-        masks = [self.act(lay.H[l], wl.n, 2 * wl.h, lay.ld_H).cpu().numpy() > 0
-                 for l in range(wl.L)]
+        masks = self.masks()
         params = dict(W_self=inp.W_self, W_neigh=inp.W_neigh,
                       b=self.b if self.bias else [None] * wl.L, W_cls=inp.W_cls,
                       b_cls=self.bc)
@@ -131,7 +148,7 @@ def check_step(run, tol=FP32_TOL):
             errs[f"Z{l}"] = rel(run.ah(l, wl.n, wl.h), Z)
         else:
             errs[f"AH{l}"] = rel(run.ah(l, wl.n, F), ref["fw"]["AH"][l])
-        errs[f"H{l}"] = rel(run.act(lay.H[l], wl.n, 2 * wl.h, lay.ld_H), ref["fw"]["H"][l + 1])
+        errs[f"H{l}"] = rel(run.H(l), ref["fw"]["H"][l + 1])
     errs["logits"] = rel(run.act(lay.logits, wl.n, wl.C, lay.ld_C), ref["fw"]["logits"])
     errs["dlogits"] = rel(run.act(lay.dlogits, wl.n, wl.C, lay.ld_C), ref["dlogits"])
     errs["loss"] = abs(run.loss - ref["loss"]) / max(abs(ref["loss"]), 1e-30)
@@ -148,7 +165,7 @@ def check_step(run, tol=FP32_TOL):
         if l >= 1:
             errs[f"G{l}n"] = rel(run.act(lay.G[l], wl.n, 2 * h, lay.ld_H)[:, h:], G_ref[:, h:])
     if lay.ah_bytes == 2:
-        for l in range(wl.L):
+        for l in range(wl.L - 1):   # the last layer keeps no fp32 copy
             H = run.act(lay.H[l], wl.n, 2 * h, lay.ld_H)
             assert torch.equal(run.act16(lay.H16[l], wl.n, 2 * h, lay.ld_H),
                                H.to(torch.bfloat16)), l
