@@ -384,20 +384,21 @@ int gcn_layer_bwd(const gcn_dgraph* g, int32_t F, int32_t h, const float* G,
  *   the same product reassociated, and its AH region holds H W_neigh
  *   instead. Equal results up to rounding, with every aggregation at width
  *   h. Not with has_bias (GCN_E_UNSUPPORTED).
- * precision GCN_PREC_BF16 with order GCN_ORDER_PAPER and h a multiple of 8:
+ * precision GCN_PREC_BF16 with h a multiple of 8 (either order):
  *   the step keeps a bf16 copy (rounded to nearest even) of every operand
  *   of a dense product, written by the kernel that produces the operand
  *   (X and the weights are rounded once at the start of the step), and the
  *   products read those copies: the same rounded operands as the per-layer
- *   entry points' bf16 products, at half the operand bytes. AH, read only
- *   by products, is then stored in bf16 only (layout field ah_bytes = 2),
- *   and the fp32 G[l] only where the fp32 aggregation reads it: columns
- *   [h, 2h) for l >= 1, none for l = 0 (the full gradients are G16); the
- *   last layer's fp32 H is not written either (H16 holds it), and the
- *   backward's ReLU masks are read from H16, which has the fp32 sign
- *   except for activations in (0, 2^-134].
- *   Otherwise (narrow order, h % 8 != 0) the products round fp32 operands
- *   on the way, as in the per-layer entry points.
+ *   entry points' bf16 products, at half the operand bytes. A paper-order
+ *   layer's AH, read only by products, is then stored in bf16 only (layout
+ *   field ah_bytes = 2). Only what an fp32 aggregation reads is kept in
+ *   fp32: a layer output only when the next layer aggregates it first
+ *   (layout H[l] is -1 otherwise; H16 holds every output), a gradient only
+ *   in its neighbour half [h, 2h) and only when its layer aggregates it
+ *   (G16 holds the full gradients). The backward's ReLU masks are read
+ *   from H16, which has the fp32 sign except for activations in
+ *   (0, 2^-134]. With h % 8 != 0 the products round fp32 operands on the
+ *   way, as in the per-layer entry points.
  */
 #define GCN_ORDER_PAPER 0
 #define GCN_ORDER_NARROW 1
@@ -429,8 +430,11 @@ typedef struct {          /* byte offsets into ws, -1 when absent */
                                          ping-pong, so only the last
                                          two written stay valid      */
     int64_t scratch, scratch_bytes, total_bytes;
-    int64_t ah_bytes;                 /* bytes per AH element: 4 (float),
-                                         2 (bf16, see gcn_train_step) */
+    int64_t ah_bytes;                 /* bytes per AH element of the
+                                         layers that aggregate first: 4
+                                         (float), 2 (bf16, see
+                                         gcn_train_step); a narrow
+                                         layer's region is float */
     int64_t H16[GCN_MAX_LAYERS];      /* bf16 step with operand copies
                                          (ah_bytes = 2): bf16 copies of
                                          H[l] and of G[l], ld ld_H (G16

@@ -491,7 +491,8 @@ int do_layer_bwd(const char* fn, const gcn_dgraph* g, int32_t F, int32_t h,
 int do_layer_fwd_narrow(const char* fn, const gcn_dgraph* g, int32_t F, int32_t h,
                         const float* H_in, int64_t ld_in, const float* Ws, const float* Wn,
                         float* Z, int64_t ldz, float* H_out, int64_t ld_out, bool bf16,
-                        const ScratchPlan& sp, void* ws, hipStream_t s) {
+                        const ScratchPlan& sp, void* ws, hipStream_t s,
+                        const LayerCopies* c = nullptr) {
     GemmBatch b;
     std::memset(&b, 0, sizeof(b));
     b.nprob = 2;
@@ -509,11 +510,32 @@ int do_layer_fwd_narrow(const char* fn, const gcn_dgraph* g, int32_t F, int32_t 
         p.C = i == 0 ? H_out : Z;
         p.ldc = i == 0 ? ld_out : ldz;
         p.no_relu = i == 1;
+        if (c) {
+            // Z stays fp32 for the aggregation; the self half is kept in
+            // bf16 (and in fp32 only when an aggregation reads it)
+            p.hA0 = p.hA1 = c->Hin;
+            p.hlda0 = p.hlda1 = c->ld_hin;
+            p.hB0 = p.hB1 = i == 0 ? c->Ws : c->Wn;
+            p.hldb0 = p.hldb1 = h;
+            if (i == 0) {
+                p.hC = c->Hout;
+                p.ldhc = c->ld_hout;
+                p.c_from = c->hout_fp32 ? 0 : h;
+            }
+        }
         b.p[i] = p;
     }
     GCN_HIP(launch_gemm(b, A_MK, B_KN, EPI_BIAS_RELU, ROLE_FWD, bf16, s), fn);
+    // with copies the neighbour half goes to the bf16 copy only (no
+    // aggregation reads a narrow layer's output: the next layer transforms
+    // before it aggregates)
+    if (c && c->hout_fp32) {
+        set_error("%s: a narrow layer's fp32 output is not kept with bf16 copies", fn);
+        return GCN_E_INTERNAL;
+    }
     return do_aggregate(fn, g, false, h, Z, ldz, H_out + h, ld_out, sp, ws, s,
-                        AGG_MEAN_BIAS_RELU, nullptr);
+                        AGG_MEAN_BIAS_RELU, nullptr, c ? c->Hout + h : nullptr,
+                        c ? c->ld_hout : 0);
 }
 
 // Backward of a narrow layer: T = A D^-1 G_neigh (also for the first
@@ -523,11 +545,12 @@ int do_layer_bwd_narrow(const char* fn, const gcn_dgraph* g, int32_t F, int32_t 
                         float* Ws, float* Wn, const OptimArgs& oa, const OptState& st_self,
                         const OptState& st_neigh, float* G_in, int64_t ldgi,
                         float* dWs_out, float* dWn_out, bool bf16, const ScratchPlan& sp,
-                        void* ws, hipStream_t s) {
+                        void* ws, hipStream_t s, const LayerCopies* c = nullptr) {
     const int32_t n = g->n;
     float* T = fptr(ws, sp.T);
     const int64_t ldt = ldg <= sp.ld_max ? ldg : r4(h);
-    GCN_TRY(do_aggregate(fn, g, true, h, G + h, ldg, T, ldt, sp, ws, s));
+    GCN_TRY(do_aggregate(fn, g, true, h, G + h, ldg, T, ldt, sp, ws, s, AGG_SUM, nullptr,
+                         c ? c->T : nullptr, c ? c->ldt : 0));
     if (G_in) {
         GemmBatch b;
         std::memset(&b, 0, sizeof(b));
@@ -550,6 +573,20 @@ int do_layer_bwd_narrow(const char* fn, const gcn_dgraph* g, int32_t F, int32_t 
         p.ldmask = ld_in;
         p.C = G_in;
         p.ldc = ldgi;
+        if (c) {
+            p.hA0 = c->G;
+            p.hlda0 = c->ldg;
+            p.hA1 = c->T;
+            p.hlda1 = c->ldt;
+            p.hB0 = c->Ws;
+            p.hB1 = c->Wn;
+            p.hldb0 = p.hldb1 = h;
+            p.hC = c->Gin;
+            p.ldhc = c->ldgi;
+            p.c_from = c->gin_fp32_from;
+            p.hmask = c->Hin;
+            p.ldhmask = c->ld_hin;
+        }
         b.p[0] = p;
         GCN_HIP(launch_gemm(b, A_MK, B_NK, EPI_MASK, ROLE_DX, bf16, s), fn);
     }
@@ -560,6 +597,14 @@ int do_layer_bwd_narrow(const char* fn, const gcn_dgraph* g, int32_t F, int32_t 
     float* part1 = part0 + sp.gemm_part_floats;
     b.p[0] = dw_problem(n, F, false, h, H_in, ld_in, G, ldg, part0, 2);
     b.p[1] = dw_problem(n, F, false, h, H_in, ld_in, T, ldt, part1, 2);
+    if (c) {
+        for (int i = 0; i < 2; ++i) {
+            b.p[i].hA0 = b.p[i].hA1 = c->Hin;
+            b.p[i].hlda0 = b.p[i].hlda1 = c->ld_hin;
+            b.p[i].hB0 = b.p[i].hB1 = i == 0 ? c->G : c->T;
+            b.p[i].hldb0 = b.p[i].hldb1 = i == 0 ? c->ldg : c->ldt;
+        }
+    }
     GCN_HIP(launch_gemm(b, A_KM, B_KN, EPI_PARTIAL, ROLE_DW, bf16, s), fn);
     SgdProblem q[2] = {
         with_state(sgd_problem(b.p[0], F, h, Ws, nullptr, dWs_out, nullptr), st_self),
@@ -572,9 +617,10 @@ bool narrow_layer(const gcn_model_desc* d, int32_t F) {
     return d->order == GCN_ORDER_NARROW && F > d->h;
 }
 
-// bf16 copies of the step's product operands (precision GCN_PREC_BF16,
-// paper order, h a multiple of 8): byte offsets into the workspace, ld in
-// elements. AH itself is then kept in bf16 only (pub.AH, pub.ld_AH).
+// bf16 copies of the step's product operands (precision GCN_PREC_BF16, h a
+// multiple of 8): byte offsets into the workspace, ld in elements. A
+// paper-order layer's AH is then kept in bf16 only (pub.AH, pub.ld_AH); a
+// narrow layer's region keeps holding the fp32 H W_neigh it aggregates.
 struct CopyLayout {
     bool on;
     int64_t X, ld_x;                                  // [n x f_in]
@@ -587,13 +633,28 @@ struct CopyLayout {
 };
 
 bool step_copies(const gcn_model_desc* d) {
-    return d->precision == GCN_PREC_BF16 && d->order == GCN_ORDER_PAPER && d->h % 8 == 0;
+    return d->precision == GCN_PREC_BF16 && d->h % 8 == 0;
+}
+
+// Whether layer l's fp32 output is read by an aggregation: the next layer's,
+// when that layer aggregates before it transforms. With bf16 copies nothing
+// else reads it (products and ReLU masks read the bf16 copy).
+bool output_aggregated(const gcn_model_desc* d, int l) {
+    return l + 1 < d->L && !narrow_layer(d, 2 * d->h);
+}
+
+// Whether the fp32 gradient of layer l's output is aggregated (its
+// neighbour half): by layer l's backward when it computes T, i.e. above the
+// first layer, or at any layer that transforms first.
+bool gradient_aggregated(const gcn_model_desc* d, int l) {
+    return l > 0 || narrow_layer(d, d->f_in);
 }
 
 struct StepLayout {
     gcn_ws_layout pub;
     ScratchPlan sp;
     CopyLayout cp;
+    int64_t H32[GCN_MAX_LAYERS];   // the fp32 H regions (pub.H reports -1 where unwritten)
 };
 
 int plan_step(const gcn_dgraph* g, const gcn_model_desc* d, StepLayout* out) {
@@ -617,9 +678,11 @@ int plan_step(const gcn_dgraph* g, const gcn_model_desc* d, StepLayout* out) {
     for (int i = 0; i < GCN_MAX_LAYERS; ++i) out->pub.H16[i] = out->pub.G16[i] = -1;
     for (int l = 0; l < d->L; ++l) {
         const int64_t F = l == 0 ? d->f_in : 2 * (int64_t)d->h;
-        out->pub.ld_AH[l] = copies ? r8(F) : r4(F);
-        out->pub.AH[l] = take(out->pub.ah_bytes * n * out->pub.ld_AH[l]);
-        out->pub.H[l] = take(4 * n * ldH);
+        const bool h16 = copies && !narrow_layer(d, (int32_t)F);   // AH in bf16
+        out->pub.ld_AH[l] = h16 ? r8(F) : r4(F);
+        out->pub.AH[l] = take((h16 ? 2 : 4) * n * out->pub.ld_AH[l]);
+        out->H32[l] = take(4 * n * ldH);
+        out->pub.H[l] = (copies && !output_aggregated(d, l)) ? -1 : out->H32[l];
     }
     out->pub.ld_H = ldH;
     out->pub.logits = take(4 * n * ldC);
@@ -975,7 +1038,7 @@ int train_step_impl(const char* fn, const gcn_dgraph* g, const gcn_model_desc* d
         c.Wn = h16(cp.Wn[l]);
         c.Hout = h16(cp.H[l]);
         c.ld_hout = ldH;
-        c.hout_fp32 = l < L - 1;   // the next layer aggregates it
+        c.hout_fp32 = output_aggregated(d, l);
         c.G = h16(cp.G[l]);
         c.ldg = ldH;
         c.T = h16(cp.T);
@@ -983,8 +1046,8 @@ int train_step_impl(const char* fn, const gcn_dgraph* g, const gcn_model_desc* d
         c.Gin = l > 0 ? h16(cp.G[l - 1]) : nullptr;
         c.ldgi = ldH;
         // the fp32 aggregation of the layer below reads only the neighbour
-        // half of its gradient; the first layer aggregates none
-        c.gin_fp32_from = l > 1 ? h : 2 * h;
+        // half of its gradient, and only where that layer aggregates it
+        c.gin_fp32_from = l > 0 && gradient_aggregated(d, l - 1) ? h : 2 * h;
         return c;
     };
 
@@ -993,18 +1056,18 @@ int train_step_impl(const char* fn, const gcn_dgraph* g, const gcn_model_desc* d
     int64_t ldprev = d->ld_x;
     for (int l = 0; l < L; ++l) {
         const int32_t F = l == 0 ? d->f_in : 2 * h;
-        if (narrow_layer(d, F))
+        const LayerCopies lc = layer_copies(l);
+        if (narrow_layer(d, F)) {
             GCN_TRY(do_layer_fwd_narrow(fn, g, F, h, Hprev, ldprev, P->W_self[l], P->W_neigh[l],
-                                        act(sl.pub.AH[l]), sl.pub.ld_AH[l], act(sl.pub.H[l]),
-                                        ldH, bf16, sp, scratch, s));
-        else {
-            const LayerCopies lc = layer_copies(l);
+                                        act(sl.pub.AH[l]), sl.pub.ld_AH[l], act(sl.H32[l]),
+                                        ldH, bf16, sp, scratch, s, cp.on ? &lc : nullptr));
+        } else {
             GCN_TRY(do_layer_fwd(fn, g, F, h, Hprev, ldprev, P->W_self[l], P->W_neigh[l],
                                  d->has_bias ? P->b[l] : nullptr, act(sl.pub.AH[l]),
-                                 sl.pub.ld_AH[l], act(sl.pub.H[l]), ldH, bf16, sp, scratch, s,
+                                 sl.pub.ld_AH[l], act(sl.H32[l]), ldH, bf16, sp, scratch, s,
                                  cp.on ? &lc : nullptr));
         }
-        Hprev = act(sl.pub.H[l]);
+        Hprev = act(sl.H32[l]);
         ldprev = ldH;
     }
     // classifier + loss
@@ -1037,7 +1100,7 @@ int train_step_impl(const char* fn, const gcn_dgraph* g, const gcn_model_desc* d
                        cp.on ? h16(cp.Wc) : nullptr, cp.ld_wc,
                        cp.on ? h16(cp.dZ) : nullptr, cp.ld_dz,
                        cp.on ? h16(cp.G[L - 1]) : nullptr, ldH,
-                       L > 1 ? h : 2 * h};
+                       gradient_aggregated(d, L - 1) ? h : 2 * h};
     GCN_TRY(do_classifier_bwd(fn, (int32_t)n, 2 * h, C, dZ, ldC, Hprev, ldH, P->W_cls,
                               d->has_bias ? P->b_cls : nullptr, oa, cst, Gcur, ldH,
                               grads ? grads->W_cls : nullptr,
@@ -1045,20 +1108,20 @@ int train_step_impl(const char* fn, const gcn_dgraph* g, const gcn_model_desc* d
                               cp.on ? &cc : nullptr));
     for (int l = L - 1; l >= 0; --l) {
         const int32_t F = l == 0 ? d->f_in : 2 * h;
-        const float* Hin = l == 0 ? X : act(sl.pub.H[l - 1]);
+        const float* Hin = l == 0 ? X : act(sl.H32[l - 1]);
         const int64_t ldin = l == 0 ? d->ld_x : ldH;
         float* Gnext = l > 0 ? act(sl.pub.G[l - 1]) : nullptr;
+        const LayerCopies lc = layer_copies(l);
         if (narrow_layer(d, F)) {
             GCN_TRY(do_layer_bwd_narrow(fn, g, F, h, Gcur, ldH, Hin, ldin, P->W_self[l],
                                         P->W_neigh[l], oa, layer_state(d, st1, st2, l, 0),
                                         layer_state(d, st1, st2, l, 1), Gnext, ldH,
                                         grads ? grads->W_self[l] : nullptr,
                                         grads ? grads->W_neigh[l] : nullptr, bf16, sp, scratch,
-                                        s));
+                                        s, cp.on ? &lc : nullptr));
             Gcur = Gnext;
             continue;
         }
-        const LayerCopies lc = layer_copies(l);
         GCN_TRY(do_layer_bwd(fn, g, F, h, Gcur, ldH, Hin, ldin, act(sl.pub.AH[l]),
                              sl.pub.ld_AH[l], P->W_self[l], P->W_neigh[l],
                              d->has_bias ? P->b[l] : nullptr, oa,

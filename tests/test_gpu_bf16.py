@@ -203,7 +203,7 @@ def test_step_bf16_copies_match_entry_points(name):
                       _ws(run.case, max(F, 2 * wl.h)), precision=gcn.PREC_BF16)
         torch.cuda.synchronize()
         # the step keeps the last layer's output in bf16 only
-        if l < wl.L - 1:
+        if lay.H[l] >= 0:
             assert torch.equal(H, run.act(lay.H[l], wl.n, 2 * wl.h, lay.ld_H)), l
         assert torch.equal(H.to(torch.bfloat16),
                            run.act16(lay.H16[l], wl.n, 2 * wl.h, lay.ld_H)), l
@@ -228,4 +228,18 @@ def test_step_bf16_copies_tiny_shapes(n, dbar, f_in, C, bias, loss):
     wl = synth.small_workload(n, dbar, 2, f_in, 8, C, loss, (n, f_in, C))
     run = StepRun(wl, bias=bias, seg_len=3, precision=gcn.PREC_BF16).run()
     assert run.layout.ah_bytes == 2
+    check_step(run, tol=BF16_TOL)
+
+
+@pytest.mark.parametrize("L,f_in", [(2, 29), (3, 60), (1, 60)])
+def test_step_bf16_copies_narrow(L, f_in):
+    """The narrow-side order on operand copies: a first layer that
+    aggregates first (f_in <= h) or transforms first (f_in > h), ragged
+    sizes, no fp32 layer outputs kept."""
+    need_gpu()
+    from paper_2001_02498_amd import gcn
+    wl = synth.small_workload(437, 9, L, f_in, 40, 7, synth.SOFTMAX_CE, (L, f_in, 23))
+    run = StepRun(wl, seg_len=4, precision=gcn.PREC_BF16, order=1).run()
+    assert run.layout.ah_bytes == 2
+    assert all(run.layout.H[l] < 0 for l in range(L))
     check_step(run, tol=BF16_TOL)

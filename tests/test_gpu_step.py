@@ -100,9 +100,9 @@ class StepRun:
     def H(self, l):
         """Layer l's output as float32: the fp32 activations, or in the bf16
         step on operand copies their bf16 copy where no fp32 one is kept
-        (the last layer)."""
+        (the layout reports -1: outputs no aggregation reads)."""
         wl, lay = self.wl, self.layout
-        if lay.ah_bytes == 2 and l == wl.L - 1:
+        if lay.H[l] < 0:
             return self.act16(lay.H16[l], wl.n, 2 * wl.h, lay.ld_H).float()
         return self.act(lay.H[l], wl.n, 2 * wl.h, lay.ld_H)
 
@@ -145,7 +145,7 @@ def check_step(run, tol=FP32_TOL):
         if run.narrow(l):
             # the region holds H W_neigh, the product the layer aggregates
             Z = ref["fw"]["H"][l] @ run.inp.W_neigh[l].astype(np.float64)
-            errs[f"Z{l}"] = rel(run.ah(l, wl.n, wl.h), Z)
+            errs[f"Z{l}"] = rel(run.act(lay.AH[l], wl.n, wl.h, lay.ld_AH[l]), Z)
         else:
             errs[f"AH{l}"] = rel(run.ah(l, wl.n, F), ref["fw"]["AH"][l])
         errs[f"H{l}"] = rel(run.H(l), ref["fw"]["H"][l + 1])
@@ -165,7 +165,7 @@ def check_step(run, tol=FP32_TOL):
         if l >= 1:
             errs[f"G{l}n"] = rel(run.act(lay.G[l], wl.n, 2 * h, lay.ld_H)[:, h:], G_ref[:, h:])
     if lay.ah_bytes == 2:
-        for l in range(wl.L - 1):   # the last layer keeps no fp32 copy
+        for l in [l for l in range(wl.L) if lay.H[l] >= 0]:
             H = run.act(lay.H[l], wl.n, 2 * h, lay.ld_H)
             assert torch.equal(run.act16(lay.H16[l], wl.n, 2 * h, lay.ld_H),
                                H.to(torch.bfloat16)), l
