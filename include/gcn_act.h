@@ -452,6 +452,25 @@ int gcn_train_step(const gcn_dgraph* g, const gcn_model_desc* desc,
                    const gcn_params* grads, void* ws, size_t ws_bytes,
                    gcn_stream_t stream);
 
+/* ------------------------------------------------------- inference
+ * gcn_infer - the forward pass of gcn_train_step alone, finished into
+ * logits: Eq. 1 through the L layers and the classifier (logits plus b_cls),
+ * no loss and no update. The paper's conclusion names inference on large,
+ * un-sampled graphs as the method's extension, with the redundancy
+ * reduction applied to the whole graph: `g` is then the reduced (or direct)
+ * image of that graph, built exactly as for a training subgraph. Same
+ * descriptor, parameters (read only), precision and order as the step, and
+ * the same workspace (gcn_workspace_bytes); the activations it leaves at
+ * the gcn_workspace_layout offsets are those of the step's forward pass.
+ *   X       device [n x f_in] ld desc->ld_x
+ *   logits  device [n x C] ld ld_logits (>= C, a multiple of 4, 16-byte
+ *           aligned)
+ * Errors: as gcn_train_step (GCN_E_INVALID_ARG before any launch).
+ */
+int gcn_infer(const gcn_dgraph* g, const gcn_model_desc* desc,
+              const gcn_params* params, const float* X, float* logits,
+              int64_t ld_logits, void* ws, size_t ws_bytes, gcn_stream_t stream);
+
 /* ------------------------------------------------------ optimisers
  * gcn_train_step_optim - gcn_train_step with every weight (and bias)
  * updated by the optimiser `opt` instead of plain gradient descent.

@@ -966,19 +966,27 @@ OptState layer_state(const gcn_model_desc* d, const gcn_params* s1, const gcn_pa
     return st;
 }
 
+// The training step; or, with infer_logits set, its forward pass alone
+// finished into the caller's logits (inference: no loss, no update).
 int train_step_impl(const char* fn, const gcn_dgraph* g, const gcn_model_desc* d,
                     const gcn_params* P, const float* X, const void* labels,
                     const OptimArgs& oa, const gcn_params* st1, const gcn_params* st2,
                     float* loss_out, const gcn_params* grads, void* ws, size_t ws_bytes,
-                    gcn_stream_t stream) {
+                    gcn_stream_t stream, float* infer_logits = nullptr,
+                    int64_t ld_infer = 0) {
     GCN_TRY(check_graph(fn, g));
     GCN_TRY(check_desc(fn, d));
     GCN_CHECK_ARG(P != nullptr, "%s: params is NULL", fn);
     const int64_t n = g->n;
     const int32_t h = d->h, C = d->C, L = d->L;
+    const bool infer = infer_logits != nullptr || ld_infer != 0;
     GCN_TRY(check_mat(fn, "X", X, n, d->f_in, d->ld_x));
-    GCN_CHECK_ARG(n == 0 || labels != nullptr, "%s: labels is NULL", fn);
-    GCN_TRY(check_vec(fn, "loss_out", loss_out, 1));
+    if (infer) {
+        GCN_TRY(check_mat(fn, "logits", infer_logits, n, C, ld_infer));
+    } else {
+        GCN_CHECK_ARG(n == 0 || labels != nullptr, "%s: labels is NULL", fn);
+        GCN_TRY(check_vec(fn, "loss_out", loss_out, 1));
+    }
     for (int l = 0; l < L; ++l) {
         const int64_t F = l == 0 ? d->f_in : 2 * (int64_t)h;
         GCN_TRY(check_mat(fn, "W_self[l]", P->W_self[l], F, h, h));
@@ -1070,11 +1078,20 @@ int train_step_impl(const char* fn, const gcn_dgraph* g, const gcn_model_desc* d
         Hprev = act(sl.H32[l]);
         ldprev = ldH;
     }
+    const float* bcls = d->has_bias ? P->b_cls : nullptr;
+    if (infer) {
+        // inference ends with the logits, slices summed with the bias here
+        if (n > 0)
+            GCN_TRY(do_classifier_fwd(fn, (int32_t)n, 2 * h, C, Hprev, ldH, P->W_cls, bcls,
+                                      infer_logits, ld_infer, bf16, sp, scratch, s, true, nullptr,
+                                      cp.on ? h16(cp.H[L - 1]) : nullptr, ldH,
+                                      cp.on ? h16(cp.Wc) : nullptr, cp.ld_wc));
+        return GCN_OK;
+    }
     // classifier + loss
     float* Z = act(sl.pub.logits);
     float* dZ = act(sl.pub.dlogits);
     Logits lg;
-    const float* bcls = d->has_bias ? P->b_cls : nullptr;
     GCN_TRY(do_classifier_fwd(fn, (int32_t)n, 2 * h, C, Hprev, ldH, P->W_cls, bcls, Z, ldC,
                               bf16, sp, scratch, s, false, &lg,
                               cp.on ? h16(cp.H[L - 1]) : nullptr, ldH,
@@ -1145,6 +1162,14 @@ int gcn_train_step(const gcn_dgraph* g, const gcn_model_desc* d, const gcn_param
                    gcn_stream_t stream) {
     return train_step_impl("gcn_train_step", g, d, P, X, labels, sgd_args(lr), nullptr,
                            nullptr, loss_out, grads, ws, ws_bytes, stream);
+}
+
+int gcn_infer(const gcn_dgraph* g, const gcn_model_desc* d, const gcn_params* P,
+              const float* X, float* logits, int64_t ld_logits, void* ws, size_t ws_bytes,
+              gcn_stream_t stream) {
+    GCN_CHECK_ARG(ld_logits > 0, "gcn_infer: ld_logits must be positive");
+    return train_step_impl("gcn_infer", g, d, P, X, nullptr, sgd_args(0.f), nullptr, nullptr,
+                           nullptr, nullptr, ws, ws_bytes, stream, logits, ld_logits);
 }
 
 int gcn_train_step_optim(const gcn_dgraph* g, const gcn_model_desc* d, const gcn_params* P,

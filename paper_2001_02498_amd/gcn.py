@@ -151,6 +151,8 @@ class Optim(C.Structure):
                 ("beta1", _f32), ("beta2", _f32), ("eps", _f32), ("reserved", _f32)]
 
 
+_infer = _proto("gcn_infer", [C.POINTER(DGraph), C.POINTER(ModelDesc), C.POINTER(Params), _vp,
+                              _vp, _i64, _vp, _sz, _vp])
 _train_step_optim = _proto("gcn_train_step_optim",
                            [C.POINTER(DGraph), C.POINTER(ModelDesc), C.POINTER(Params), _vp,
                             _vp, C.POINTER(Optim), C.POINTER(Params), C.POINTER(Params), _vp,
@@ -188,7 +190,7 @@ EXPORTS = [
     "gcn_graph_image_bytes", "gcn_graph_pack", "gcn_graph_upload", "gcn_graph_describe",
     "gcn_scratch_bytes", "gcn_aggregate", "gcn_layer_fwd", "gcn_classifier_fwd",
     "gcn_loss", "gcn_classifier_bwd", "gcn_layer_bwd", "gcn_workspace_layout",
-    "gcn_workspace_bytes", "gcn_train_step", "gcn_train_step_optim", "gcn_profile_enable",
+    "gcn_workspace_bytes", "gcn_train_step", "gcn_train_step_optim", "gcn_infer", "gcn_profile_enable",
     "gcn_profile_disable",
     "gcn_profile_read", "gcn_pipeline_create", "gcn_pipeline_submit", "gcn_pipeline_next",
     "gcn_pipeline_release", "gcn_pipeline_destroy",
@@ -470,6 +472,12 @@ def train_step(dg, desc, params, X, labels, lr, loss_out, ws, grads=None, stream
                        _ptr(labels), float(lr), _ptr(loss_out),
                        C.byref(grads) if grads is not None else None, _ptr(ws), ws.numel(),
                        _stream(stream)))
+
+
+def infer(dg, desc, params, X, logits, ws, stream=None):
+    """Forward pass and classifier logits of the whole (reduced) graph."""
+    _check(_infer(C.byref(dg.desc), C.byref(desc), C.byref(params), _ptr(X), _ptr(logits),
+                  _ld(logits), _ptr(ws), ws.numel(), _stream(stream)))
 
 
 def optim(kind, lr, step=1, momentum=0.9, beta1=0.9, beta2=0.999, eps=1e-8) -> Optim:
