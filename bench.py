@@ -64,6 +64,11 @@ def parse():
                     help="skip the extra timing of the step with the Adam update")
     ap.add_argument("--no-direct", action="store_true",
                     help="skip the direct-aggregation comparison run (counter runs)")
+    ap.add_argument("--infer", action="store_true",
+                    help="time gcn_infer (forward pass into logits) on a whole synthetic "
+                         "graph instead of the training step")
+    ap.add_argument("--infer-n", type=int, default=60000,
+                    help="with --infer: vertices of the whole graph")
     ap.add_argument("--trace-summary", metavar="KERNEL_STATS_CSV",
                     help="no GPU: turn a rocprofv3 --kernel-trace --stats kernel_stats.csv "
                          "of this script into the per-class table under profiles/")
@@ -277,15 +282,19 @@ def trace_summary(stats_csv, workload, cmd_args, bench_line=None):
                        f"{float(r['AverageNs']) / 1e3:.2f} | {tot / 1e6:.3f} |")
     bargs = f"--workload {workload} {cmd_args}"
     bf16 = "--precision bf16" in cmd_args
-    tag = f"{workload}_bf16" if bf16 else workload
-    out = [f"# Kernel durations, {workload} {'bf16 ' if bf16 else ''}training step "
+    infer = "--infer" in cmd_args
+    what = "inference" if infer else "training step"
+    tag = (f"{workload}_bf16" if bf16 else workload) + ("_infer" if infer else "_train_step")
+    out = [f"# Kernel durations, {workload} {'bf16 ' if bf16 else ''}{what} "
            "(rocprofv3 kernel trace)", "",
            "```", "cd /tmp && export TMPDIR=/tmp",
            f"rocprofv3 --kernel-trace --stats --output-format csv -d OUT -o run -- "
            f"python3 $R/bench.py {bargs}",
            f"python3 bench.py --workload {workload} --traced-args='{cmd_args}' "
            "--trace-summary OUT/run_kernel_stats.csv --bench-line OUT/line.json", "```",
-           "", ("The run covers the warm-up, timed and profiled steps of the reduced-graph "
+           "", ("The run covers the warm-up, timed and profiled inference calls on the "
+                "reduced graph." if infer and "--no-direct" in cmd_args else
+                "The run covers the warm-up, timed and profiled steps of the reduced-graph "
                 "step alone." if all(f in cmd_args for f in ("--no-direct", "--no-narrow", "--no-adam")) else
                 "The run also covers the comparison runs bench.py times beside the step "
                 "(their kernels are counted in the same classes)."), "",
@@ -300,7 +309,7 @@ def trace_summary(stats_csv, workload, cmd_args, bench_line=None):
             out.append(f"| {c} | {k['avg_us']} |")
     out += ["", "## Per kernel", "", "| class | kernel | calls | mean us | total ms |",
             "|---|---|---:|---:|---:|"] + lines_k + [""]
-    path = os.path.join(ROOT, "profiles", f"{tag}_train_step_kernel_stats.md")
+    path = os.path.join(ROOT, "profiles", f"{tag}_kernel_stats.md")
     with open(path, "w") as fh:
         fh.write("\n".join(out))
     print(path)
@@ -683,6 +692,110 @@ def run_stream(args):
     }
 
 
+class InferSetup(Setup):
+    """A whole graph and the model on the device, ready for timed inference."""
+
+    def __init__(self, *a, **kw):
+        super().__init__(*a, **kw)
+        import torch
+        wl = self.wl
+        self.Z = torch.empty((wl.n, (wl.C + 3) // 4 * 4), device="cuda")[:, :wl.C]
+
+    def step(self):
+        self.gcn.infer(self.dg, self.desc, self.P, self.X, self.Z, self.ws)
+
+
+def infer_workload(n):
+    """The ppi8k model (2 layers, f_in 50, 512 per branch, 121 classes) on a
+    whole n-vertex graph of the same structure (Chung-Lu, exponent 2.5, mean
+    degree 15): the stand-in for inference on an un-sampled graph."""
+    from paper_2001_02498_amd import synth
+    import dataclasses
+    ppi = synth.WORKLOADS["ppi8k"]
+    wl = synth.small_workload(n, ppi.dbar, ppi.L, ppi.f_in, ppi.h, ppi.C, ppi.loss, (7, n),
+                              gamma=ppi.gamma, theta=ppi.theta, rounds=ppi.rounds,
+                              label_p=ppi.label_p, budget=ppi.budget)
+    return dataclasses.replace(wl, name=f"full{n // 1000}k")
+
+
+def cpu_forward_baseline(wl, inp, budget_s):
+    """The oracle's forward pass (aggregation as D^-1 A H) on the same graph."""
+    import threadpoolctl
+    from oracle import gcn as og
+    from oracle import graph as gr
+    rp, cl = gr.subgraph_build(wl.n, inp.src, inp.dst)
+    params = dict(W_self=inp.W_self, W_neigh=inp.W_neigh, b=[None] * wl.L, W_cls=inp.W_cls,
+                  b_cls=None)
+    reps, t0 = 0, time.perf_counter()
+    while True:
+        og.forward(rp, cl, inp.X, params)
+        reps += 1
+        el = time.perf_counter() - t0
+        if el >= budget_s or reps >= 20:
+            break
+    threads = max((p.get("num_threads", 1) for p in threadpoolctl.threadpool_info()
+                   if p.get("user_api") == "blas"), default=1)
+    return dict(value=round(reps * wl.n / el, 1), unit="vertices/s", cores=int(threads),
+                kind="oracle",
+                sample=f"{reps} float64 oracle forward passes of {wl.name} in {el:.1f} s; "
+                       f"BLAS threads {threads}, os.cpu_count {os.cpu_count()}")
+
+
+def run_infer(args):
+    import dataclasses
+
+    from paper_2001_02498_amd import gcn, synth
+    wl = infer_workload(args.infer_n)
+    inp = synth.make_inputs(wl)
+    print(f"[bench] whole graph {wl.name}: inputs ready", file=sys.stderr, flush=True)
+    prec = gcn.PREC_BF16 if args.precision == "bf16" else gcn.PREC_FP32
+    order = gcn.ORDER_NARROW if args.order == "narrow" else gcn.ORDER_PAPER
+    red = InferSetup(wl, True, inp, args.seg_len, prec, order)
+    ms = 1e3 * red.timed(args.steps, args.warmup)
+    print(f"[bench] timed {args.steps} inference calls: {ms:.3f} ms/call", file=sys.stderr,
+          flush=True)
+    direct = None
+    if not args.no_direct:
+        d = InferSetup(dataclasses.replace(wl, reduce=False), False, inp, args.seg_len, prec,
+                       order)
+        direct = 1e3 * d.timed(args.steps, args.warmup)
+        print(f"[bench] direct aggregation: {direct:.3f} ms/call", file=sys.stderr, flush=True)
+        del d
+    prof = red.profile(args.profile_steps)
+    ktab = kernel_table(prof, args.profile_steps)
+    dominant = max(ktab, key=lambda k: ktab[k]["ms_per_step"])
+    roof = roofline(dominant, ktab[dominant], wl.name)
+    cpu = None if args.no_cpu_baseline else cpu_forward_baseline(wl, inp, args.cpu_seconds)
+    i = red.info
+    return {
+        "metric": "whole-graph GCN inference (forward pass into logits) vertices/s",
+        "value": round(wl.n / (ms * 1e-3), 1),
+        "unit": "vertices/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_call": round(ms, 4),
+        "higher_is_better": True,
+        "dtype": "f32" if args.precision == "fp32" else "bf16 (dense products; fp32 accumulate)",
+        "order": args.order,
+        "data": "synthetic",
+        "config": {
+            "workload": (f"{wl.name}: the ppi8k model ({wl.L} layers, f_in {wl.f_in}, {wl.h} "
+                         f"per branch, {wl.C} classes) on a whole {wl.n}-vertex Chung-Lu graph "
+                         f"(exponent {wl.gamma}, mean degree {wl.dbar}), reduced on the host "
+                         f"({wl.rounds} rounds, threshold {wl.theta})"),
+            "n": wl.n, "nnz": int(red.dg.desc.nnz), "naux": i["naux"],
+        },
+        "roofline": {k: v for k, v in roof.items() if k != "kernel"} | {"kernel": dominant},
+        "cpu_baseline": cpu,
+        "direct_aggregation_ms_per_call": None if direct is None else round(direct, 4),
+        "host_preprocess_ms": {k: round(v, 2) for k, v in red.host_ms.items()},
+        "kernels": {k: {kk: vv for kk, vv in v.items()
+                        if kk not in ("flops_per_launch", "bytes_per_launch")}
+                    for k, v in ktab.items()},
+    }
+
+
 def main():
     args = parse()
     if args.trace_summary:
@@ -714,6 +827,9 @@ def main():
         print("bench.py: no GPU visible", file=sys.stderr)
         sys.exit(1)
     torch.cuda.set_device(0)
+    if args.infer:
+        print(json.dumps(run_infer(args)), flush=True)
+        return
     if args.workload == "stream8k":
         print(json.dumps(run_stream(args)), flush=True)
         return

@@ -136,3 +136,25 @@ def test_trace_summary_names_the_bf16_variant(scratch_root):
     txt = (scratch_root / "profiles" / "wl_bf16_train_step_kernel_stats.md").read_text()
     assert "bf16 training step" in txt
     assert "| gemm_fwd_bf16 | 2 | 50.00 | 0.100 |" in txt
+
+
+def test_infer_workload_is_the_ppi_model_on_a_whole_graph():
+    from paper_2001_02498_amd import synth
+    ppi = synth.WORKLOADS["ppi8k"]
+    wl = bench.infer_workload(20000)
+    assert (wl.n, wl.name) == (20000, "full20k")
+    assert (wl.L, wl.f_in, wl.h, wl.C, wl.loss) == (ppi.L, ppi.f_in, ppi.h, ppi.C, ppi.loss)
+    assert (wl.gamma, wl.dbar, wl.theta, wl.rounds, wl.budget) == (
+        ppi.gamma, ppi.dbar, ppi.theta, ppi.rounds, ppi.budget)
+    assert wl.reduce
+
+
+def test_trace_summary_names_inference(scratch_root):
+    path = scratch_root / "stats.csv"
+    with open(path, "w", newline="") as fh:
+        w = csv.DictWriter(fh, fieldnames=["Name", "Calls", "TotalDurationNs", "AverageNs"])
+        w.writeheader()
+        w.writerow(dict(Name=GEMM.format(0), Calls=2, TotalDurationNs=100000, AverageNs=50000))
+    bench.trace_summary(str(path), "full9k", "--infer --no-cpu-baseline --no-direct")
+    txt = (scratch_root / "profiles" / "full9k_infer_kernel_stats.md").read_text()
+    assert "full9k inference" in txt and "inference calls" in txt
