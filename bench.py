@@ -103,7 +103,8 @@ _CLASS_SOURCES = {
     "loss": ["loss.hip", "kernels.h", "api.hip"],
     "sgd": ["gemm.hip", "kernels.h", "api.hip"],
 }
-_ROLE_CLASS = ["gemm_fwd", "gemm_cls", "gemm_dx", "gemm_cls_dx", "gemm_dw", "gemm_cls_dw"]
+_ROLE_CLASS = ["gemm_fwd", "gemm_cls", "gemm_dx", "gemm_cls_dx", "gemm_dw", "gemm_cls_dw",
+               "gemm_fwd_in", "gemm_dw_in"]
 
 
 def _family(cls):

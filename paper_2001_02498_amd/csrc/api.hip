@@ -179,7 +179,7 @@ int do_layer_fwd(const char* fn, const gcn_dgraph* g, int32_t F, int32_t h,
                  const float* H_in, int64_t ld_in, const float* Ws,
                  const float* Wn, const float* bias, float* AH, int64_t ld_ah,
                  float* H_out, int64_t ld_out, bool bf16, const ScratchPlan& sp, void* ws,
-                 hipStream_t s, const LayerCopies* c = nullptr) {
+                 hipStream_t s, const LayerCopies* c = nullptr, bool first = false) {
     GCN_TRY(do_aggregate(fn, g, false, F, H_in, ld_in, AH, ld_ah, sp, ws, s, AGG_MEAN, nullptr,
                          c ? c->AH : nullptr, c ? c->ld_ah : 0));
     GemmBatch b;
@@ -210,7 +210,8 @@ int do_layer_fwd(const char* fn, const gcn_dgraph* g, int32_t F, int32_t h,
         }
         b.p[i] = p;
     }
-    GCN_HIP(launch_gemm(b, A_MK, B_KN, EPI_BIAS_RELU, ROLE_FWD, bf16, s), fn);
+    GCN_HIP(launch_gemm(b, A_MK, B_KN, EPI_BIAS_RELU, first ? ROLE_FWD_IN : ROLE_FWD, bf16, s),
+            fn);
     return GCN_OK;
 }
 
@@ -410,7 +411,7 @@ int do_layer_bwd(const char* fn, const gcn_dgraph* g, int32_t F, int32_t h,
                  const OptState& st_neigh, float* G_in, int64_t ldgi,
                  float* dWs_out, float* dWn_out, float* db_out, bool bf16,
                  const ScratchPlan& sp, void* ws, hipStream_t s,
-                 const LayerCopies* c = nullptr) {
+                 const LayerCopies* c = nullptr, bool first = false) {
     const int32_t n = g->n;
     if (G_in) {
         // T = A D^-1 G[:, h:]  (Eq. 2c), then G_in = [G_self | T] [W_self; W_neigh]^T;
@@ -475,7 +476,7 @@ int do_layer_bwd(const char* fn, const gcn_dgraph* g, int32_t F, int32_t h,
             b.p[i].hldb0 = b.p[i].hldb1 = c->ldg;
         }
     }
-    GCN_HIP(launch_gemm(b, A_KM, B_KN, EPI_PARTIAL, ROLE_DW, bf16, s), fn);
+    GCN_HIP(launch_gemm(b, A_KM, B_KN, EPI_PARTIAL, first ? ROLE_DW_IN : ROLE_DW, bf16, s), fn);
     SgdProblem q[2] = {
         with_state(sgd_problem(b.p[0], F, h, Ws, bias, dWs_out, db_out), st_self),
         with_state(sgd_problem(b.p[1], F, h, Wn, bias ? bias + h : nullptr, dWn_out,
@@ -492,7 +493,7 @@ int do_layer_fwd_narrow(const char* fn, const gcn_dgraph* g, int32_t F, int32_t 
                         const float* H_in, int64_t ld_in, const float* Ws, const float* Wn,
                         float* Z, int64_t ldz, float* H_out, int64_t ld_out, bool bf16,
                         const ScratchPlan& sp, void* ws, hipStream_t s,
-                        const LayerCopies* c = nullptr) {
+                        const LayerCopies* c = nullptr, bool first = false) {
     GemmBatch b;
     std::memset(&b, 0, sizeof(b));
     b.nprob = 2;
@@ -525,7 +526,8 @@ int do_layer_fwd_narrow(const char* fn, const gcn_dgraph* g, int32_t F, int32_t 
         }
         b.p[i] = p;
     }
-    GCN_HIP(launch_gemm(b, A_MK, B_KN, EPI_BIAS_RELU, ROLE_FWD, bf16, s), fn);
+    GCN_HIP(launch_gemm(b, A_MK, B_KN, EPI_BIAS_RELU, first ? ROLE_FWD_IN : ROLE_FWD, bf16, s),
+            fn);
     // with copies the neighbour half goes to the bf16 copy only (no
     // aggregation reads a narrow layer's output: the next layer transforms
     // before it aggregates)
@@ -545,7 +547,8 @@ int do_layer_bwd_narrow(const char* fn, const gcn_dgraph* g, int32_t F, int32_t 
                         float* Ws, float* Wn, const OptimArgs& oa, const OptState& st_self,
                         const OptState& st_neigh, float* G_in, int64_t ldgi,
                         float* dWs_out, float* dWn_out, bool bf16, const ScratchPlan& sp,
-                        void* ws, hipStream_t s, const LayerCopies* c = nullptr) {
+                        void* ws, hipStream_t s, const LayerCopies* c = nullptr,
+                        bool first = false) {
     const int32_t n = g->n;
     float* T = fptr(ws, sp.T);
     const int64_t ldt = ldg <= sp.ld_max ? ldg : r4(h);
@@ -605,7 +608,7 @@ int do_layer_bwd_narrow(const char* fn, const gcn_dgraph* g, int32_t F, int32_t 
             b.p[i].hldb0 = b.p[i].hldb1 = i == 0 ? c->ldg : c->ldt;
         }
     }
-    GCN_HIP(launch_gemm(b, A_KM, B_KN, EPI_PARTIAL, ROLE_DW, bf16, s), fn);
+    GCN_HIP(launch_gemm(b, A_KM, B_KN, EPI_PARTIAL, first ? ROLE_DW_IN : ROLE_DW, bf16, s), fn);
     SgdProblem q[2] = {
         with_state(sgd_problem(b.p[0], F, h, Ws, nullptr, dWs_out, nullptr), st_self),
         with_state(sgd_problem(b.p[1], F, h, Wn, nullptr, dWn_out, nullptr), st_neigh)};
@@ -1068,12 +1071,12 @@ int train_step_impl(const char* fn, const gcn_dgraph* g, const gcn_model_desc* d
         if (narrow_layer(d, F)) {
             GCN_TRY(do_layer_fwd_narrow(fn, g, F, h, Hprev, ldprev, P->W_self[l], P->W_neigh[l],
                                         act(sl.pub.AH[l]), sl.pub.ld_AH[l], act(sl.H32[l]),
-                                        ldH, bf16, sp, scratch, s, cp.on ? &lc : nullptr));
+                                        ldH, bf16, sp, scratch, s, cp.on ? &lc : nullptr, l == 0));
         } else {
             GCN_TRY(do_layer_fwd(fn, g, F, h, Hprev, ldprev, P->W_self[l], P->W_neigh[l],
                                  d->has_bias ? P->b[l] : nullptr, act(sl.pub.AH[l]),
                                  sl.pub.ld_AH[l], act(sl.H32[l]), ldH, bf16, sp, scratch, s,
-                                 cp.on ? &lc : nullptr));
+                                 cp.on ? &lc : nullptr, l == 0));
         }
         Hprev = act(sl.H32[l]);
         ldprev = ldH;
@@ -1135,7 +1138,7 @@ int train_step_impl(const char* fn, const gcn_dgraph* g, const gcn_model_desc* d
                                         layer_state(d, st1, st2, l, 1), Gnext, ldH,
                                         grads ? grads->W_self[l] : nullptr,
                                         grads ? grads->W_neigh[l] : nullptr, bf16, sp, scratch,
-                                        s, cp.on ? &lc : nullptr));
+                                        s, cp.on ? &lc : nullptr, l == 0));
             Gcur = Gnext;
             continue;
         }
@@ -1146,7 +1149,7 @@ int train_step_impl(const char* fn, const gcn_dgraph* g, const gcn_model_desc* d
                              Gnext, ldH, grads ? grads->W_self[l] : nullptr,
                              grads ? grads->W_neigh[l] : nullptr,
                              grads ? grads->b[l] : nullptr, bf16, sp, scratch, s,
-                             cp.on ? &lc : nullptr));
+                             cp.on ? &lc : nullptr, l == 0));
         Gcur = Gnext;
     }
     return GCN_OK;

@@ -1362,8 +1362,11 @@ hipError_t launch_gemm(GemmBatch& b, ALayout al, BLayout bl, Epilogue ep, GemmRo
         flops += 2.0 * M * N * K;
         bytes += 4.0 * (M * K + K * N + M * N) + (ep == EPI_MASK ? 4.0 * M * N : 0.0);
     }
-    static const int kKinds[] = {K_GEMM_FWD, K_GEMM_CLS, K_GEMM_DX,
-                                 K_GEMM_CLS_DX, K_GEMM_DW, K_GEMM_CLS_DW};
+    static const int kKinds[] = {K_GEMM_FWD, K_GEMM_CLS, K_GEMM_DX, K_GEMM_CLS_DX,
+                                 K_GEMM_DW, K_GEMM_CLS_DW, K_GEMM_FWD_IN, K_GEMM_DW_IN};
+    static const int kKinds16[] = {K_GEMM_FWD_BF16, K_GEMM_CLS_BF16, K_GEMM_DX_BF16,
+                                   K_GEMM_CLS_DX_BF16, K_GEMM_DW_BF16, K_GEMM_CLS_DW_BF16,
+                                   K_GEMM_FWD_IN_BF16, K_GEMM_DW_IN_BF16};
     // bf16 with operand copies in every problem: the copies kernel
     bool copies = bf16;
     for (int i = 0; i < b.nprob; ++i) copies = copies && b.p[i].hA0 && b.p[i].hB0;
@@ -1394,7 +1397,7 @@ hipError_t launch_gemm(GemmBatch& b, ALayout al, BLayout bl, Epilogue ep, GemmRo
                      (p.hC ? 2.0 * M * N : 0.0);
         }
     }
-    const int kind = kKinds[role] + (bf16 ? K_GEMM_BF16_OFFSET : 0);
+    const int kind = bf16 ? kKinds16[role] : kKinds[role];
     ProfScope prof(s, kind, flops, bytes);
     bool bvec = true;
     for (int i = 0; i < b.nprob; ++i) {
@@ -1416,11 +1419,13 @@ hipError_t launch_gemm(GemmBatch& b, ALayout al, BLayout bl, Epilogue ep, GemmRo
         return hipGetLastError();                                                    \
     }
     GCN_GEMM_CASE(A_MK, B_KN, EPI_BIAS_RELU, ROLE_FWD)
+    GCN_GEMM_CASE(A_MK, B_KN, EPI_BIAS_RELU, ROLE_FWD_IN)
     GCN_GEMM_CASE(A_MK, B_KN, EPI_BIAS, ROLE_CLS_FWD)
     GCN_GEMM_CASE(A_MK, B_KN, EPI_PARTIAL, ROLE_CLS_FWD)
     GCN_GEMM_CASE(A_MK, B_NK, EPI_MASK, ROLE_DX)
     GCN_GEMM_CASE(A_MK, B_NK, EPI_MASK, ROLE_CLS_DX)
     GCN_GEMM_CASE(A_KM, B_KN, EPI_PARTIAL, ROLE_DW)
+    GCN_GEMM_CASE(A_KM, B_KN, EPI_PARTIAL, ROLE_DW_IN)
     GCN_GEMM_CASE(A_KM, B_KN, EPI_PARTIAL, ROLE_CLS_DW)
 #undef GCN_GEMM_CASE
     return hipErrorInvalidValue;

@@ -123,6 +123,8 @@ enum GemmRole : int {
     ROLE_CLS_DX,      // classifier input gradient    dZ W_cls^T
     ROLE_DW,          // layer weight gradients       H^T G_s, AH^T G_n
     ROLE_CLS_DW,      // classifier weight gradient   H^T dZ
+    ROLE_FWD_IN,      // first layer's transforms     (K = f_in)
+    ROLE_DW_IN,       // first layer's weight grads   (M = f_in)
 };
 
 // Launch C = A B for 1-2 problems of identical layouts / epilogue; bf16:

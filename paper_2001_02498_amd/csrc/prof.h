@@ -21,7 +21,7 @@ enum Kind : int {
     K_LOSS_ROWS,
     K_LOSS_MEAN,
     K_SPLITK_FINISH,
-    // the GEMM roles again, bf16 operands (same order as K_GEMM_FWD ..)
+    // the GEMM roles again, bf16 operands
     K_GEMM_FWD_BF16,
     K_GEMM_CLS_BF16,
     K_GEMM_DX_BF16,
@@ -29,9 +29,13 @@ enum Kind : int {
     K_GEMM_DW_BF16,
     K_GEMM_CLS_DW_BF16,
     K_TO_BF16,
+    // the first layer's products (K or M = f_in), fp32 and bf16 operands
+    K_GEMM_FWD_IN,
+    K_GEMM_DW_IN,
+    K_GEMM_FWD_IN_BF16,
+    K_GEMM_DW_IN_BF16,
     K_COUNT
 };
-constexpr int K_GEMM_BF16_OFFSET = K_GEMM_FWD_BF16 - K_GEMM_FWD;
 
 const char* kind_name(int k);
 

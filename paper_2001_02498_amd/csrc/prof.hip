@@ -49,6 +49,10 @@ const char* kind_name(int k) {
         case K_GEMM_DW_BF16: return "gemm_dw_bf16";
         case K_GEMM_CLS_DW_BF16: return "gemm_cls_dw_bf16";
         case K_TO_BF16: return "to_bf16";
+        case K_GEMM_FWD_IN: return "gemm_fwd_in";
+        case K_GEMM_DW_IN: return "gemm_dw_in";
+        case K_GEMM_FWD_IN_BF16: return "gemm_fwd_in_bf16";
+        case K_GEMM_DW_IN_BF16: return "gemm_dw_in_bf16";
         default: return "other";
     }
 }
