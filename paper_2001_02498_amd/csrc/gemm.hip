@@ -328,7 +328,7 @@ __device__ __forceinline__ void store_tile_lds(const GemmProblem& P, int split, 
 
 // A rows are always 16-byte aligned (checked on the host); BVEC selects
 // float4 or element loads for B (the classifier weight has any width C).
-template <ALayout AL, BLayout BL, Epilogue EP, bool BVEC, GemmRole ROLE>
+template <ALayout AL, BLayout BL, Epilogue EP, bool BVEC, GemmRole ROLE, bool HALF = false>
 __global__ __launch_bounds__(kThreads, 2) void gemm_kernel(GemmBatch batch) {
     // [buffer][A | B] operand tiles
     __shared__ __attribute__((aligned(16))) float smem[2][2][kOperandFloats];
@@ -342,6 +342,10 @@ __global__ __launch_bounds__(kThreads, 2) void gemm_kernel(GemmBatch batch) {
     const int lane = t & 63, wave = t >> 6;
     const int wm = wave >> 1, wn = wave & 1;
     const int half = lane >> 5, l32 = lane & 31;
+    // HALF (every row of the product within the tile's first 64): both
+    // wavefront rows work on rows 0-63, each on two of the four K groups
+    // of every step; their sums are added before the epilogue
+    const int g0 = HALF ? 2 * wm : 0;   // this wavefront's first K group
 
     // operand descriptors, fixed for the whole K loop
     const float* const A0 = P.A0;
@@ -440,7 +444,7 @@ __global__ __launch_bounds__(kThreads, 2) void gemm_kernel(GemmBatch batch) {
         const int kb = 8 * sg + 4 * half;
 #pragma unroll
         for (int i = 0; i < 2; ++i) {
-            const int m = wm * 64 + i * 32 + l32;
+            const int m = (HALF ? 0 : wm * 64) + i * 32 + l32;
             if constexpr (AL == A_MK) {
                 fa[fslot][i] = *reinterpret_cast<const float4*>(&As[m * kRowStride + kb]);
             } else {
@@ -595,6 +599,59 @@ __global__ __launch_bounds__(kThreads, 2) void gemm_kernel(GemmBatch batch) {
         mfma_group(1);
         __builtin_amdgcn_sched_barrier(0);
     };
+    // HALF: the wavefront's two groups of the step; loads and stores are
+    // interleaved with them as above
+    auto kstep_half = [&](int kt, int set, auto FULL) __attribute__((always_inline)) {
+        const int buf = kt & 1;
+        const float* As = smem[buf][0];
+        const float* Bs = smem[buf][1];
+        const int kload = kbeg + (kt + 2) * BK;
+        frag(As, Bs, g0 + 1, 1);
+        const float* const sa = step_base_a(kload);
+        const float* const sb = step_base_b(kload);
+#pragma unroll
+        for (int q = 0; q < kQuads; ++q) {
+            if constexpr (FULL) {
+                gload_full(set, sa, sb, q);
+            } else {
+                gload_a(set, kload, q);
+                gload_b(set, kload, q);
+            }
+        }
+        mfma_group(0);
+        __builtin_amdgcn_sched_group_barrier(0x100, 8, 0);
+#pragma unroll
+        for (int q = 0; q < 2 * kQuads; ++q) {
+            __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
+            __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
+        }
+        __builtin_amdgcn_sched_barrier(0);
+        const bool more = FULL || kt + 1 < nk;
+        if (more) {
+#pragma unroll
+            for (int q = 0; q < kQuads; ++q) {
+                if constexpr (FULL)
+                    sstore_full(buf ^ 1, set ^ 1, q);
+                else
+                    sstore(buf ^ 1, set ^ 1, q);
+            }
+        }
+        mfma_group(1);
+#pragma unroll
+        for (int q = 0; q < 2 * kQuads; ++q) {
+            __builtin_amdgcn_sched_group_barrier(0x200, 1, 0);
+            __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
+        }
+        __builtin_amdgcn_sched_barrier(0);
+        __syncthreads();
+        if (more) frag(smem[buf ^ 1][0], smem[buf ^ 1][1], g0, 0);
+    };
+    auto step = [&](int kt, int set, auto FULL) __attribute__((always_inline)) {
+        if constexpr (HALF)
+            kstep_half(kt, set, FULL);
+        else
+            kstep(kt, set, FULL);
+    };
     using Full = std::true_type;
     using Masked = std::false_type;
     const bool fast_start = fast_tile && nfull >= 2;
@@ -619,23 +676,47 @@ __global__ __launch_bounds__(kThreads, 2) void gemm_kernel(GemmBatch batch) {
     }
     if (nk > 0) {
         __syncthreads();
-        frag(smem[0][0], smem[0][1], 0, 0);
+        frag(smem[0][0], smem[0][1], g0, 0);
     }
     int kt = 0;
     if (fast_start) {
         for (; kt + 3 < nfull; kt += 2) {
-            kstep(kt, 0, Full{});
-            kstep(kt + 1, 1, Full{});
+            step(kt, 0, Full{});
+            step(kt + 1, 1, Full{});
         }
         mark_full(0);
         mark_full(1);
     }
     for (; kt + 1 < nk; kt += 2) {
-        kstep(kt, 0, Masked{});
-        kstep(kt + 1, 1, Masked{});
+        step(kt, 0, Masked{});
+        step(kt + 1, 1, Masked{});
     }
-    if (kt < nk) kstep(kt, 0, Masked{});
+    if (kt < nk) step(kt, 0, Masked{});
 
+    if constexpr (HALF) {
+        // the second wavefront row's sums join the first's (fixed order);
+        // its own rows (64-127) lie outside the product and store nothing
+        __syncthreads();
+        float* red = &smem[0][0][0];
+        auto at = [&](int i, int j, int r) { return ((wn * 4 + i * 2 + j) * 16 + r) * 64 + lane; };
+        if (wm == 1) {
+#pragma unroll
+            for (int i = 0; i < 2; ++i)
+#pragma unroll
+                for (int j = 0; j < 2; ++j)
+#pragma unroll
+                    for (int r = 0; r < 16; ++r) red[at(i, j, r)] = acc[i][j][r];
+        }
+        __syncthreads();
+        if (wm == 0) {
+#pragma unroll
+            for (int i = 0; i < 2; ++i)
+#pragma unroll
+                for (int j = 0; j < 2; ++j)
+#pragma unroll
+                    for (int r = 0; r < 16; ++r) acc[i][j][r] += red[at(i, j, r)];
+        }
+    }
     store_tile<EP>(P, split, m0 + wm * 64, n0 + wn * 64, half, l32, acc);
 }
 
@@ -1404,6 +1485,8 @@ hipError_t launch_gemm(GemmBatch& b, ALayout al, BLayout bl, Epilogue ep, GemmRo
         if (!copies && !b.p[i].a_vec) return hipErrorInvalidValue;   // A rows must be aligned
         bvec = bvec && b.p[i].b_vec;
     }
+    bool half_m = true;   // every problem's rows fit the first half of a tile
+    for (int i = 0; i < b.nprob; ++i) half_m = half_m && b.p[i].M <= BM / 2;
 #define GCN_GEMM_CASE(AL_, BL_, EP_, ROLE_)                                          \
     if (al == AL_ && bl == BL_ && ep == EP_ && role == ROLE_) {                       \
         if (copies)                                                                  \
@@ -1412,6 +1495,8 @@ hipError_t launch_gemm(GemmBatch& b, ALayout al, BLayout bl, Epilogue ep, GemmRo
             gemm_bf16_kernel<AL_, BL_, EP_, true, ROLE_><<<grid, block, 0, s>>>(b);   \
         else if (bf16)                                                               \
             gemm_bf16_kernel<AL_, BL_, EP_, false, ROLE_><<<grid, block, 0, s>>>(b);  \
+        else if (bvec && half_m && EP_ == EPI_PARTIAL && AL_ == A_KM)                 \
+            gemm_kernel<AL_, BL_, EP_, true, ROLE_, true><<<grid, block, 0, s>>>(b);  \
         else if (bvec)                                                               \
             gemm_kernel<AL_, BL_, EP_, true, ROLE_><<<grid, block, 0, s>>>(b);        \
         else                                                                         \

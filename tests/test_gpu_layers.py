@@ -107,7 +107,14 @@ def test_classifier_fwd_loss_bwd(n, K, C, bias):
 @pytest.mark.parametrize("n,F,h,bias,first", [(777, 50, 36, False, True),
                                               (1024, 256, 128, True, False),
                                               (300, 602, 20, False, False),
-                                              (1500, 1024, 132, True, False)])
+                                              (1500, 1024, 132, True, False),
+                                              # weight gradients with at most 64
+                                              # rows (both wavefront rows split K)
+                                              # and just past that bound
+                                              (5000, 64, 128, True, True),
+                                              (5000, 63, 72, True, True),
+                                              (2000, 65, 40, False, True),
+                                              (4100, 8, 24, False, True)])
 def test_layer_bwd(n, F, h, bias, first):
     need_gpu()
     say("layer_bwd", n, F, h, bias, first)
