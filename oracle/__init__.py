@@ -16,13 +16,19 @@ Plain, slow, float64 NumPy/SciPy code written from the paper:
                     dense products
   * optim.py      - the momentum and Adam weight updates (Section 4.1 names
                     their state; the rules are the cited methods')
+  * sample.py     - frontier sampling of a minibatch's vertex set and the
+                    induced subgraph (Section 3.1 names the cited
+                    multi-dimensional random walk as its sampler)
 
 Pins (tests/test_oracle_*.py): the worked examples of Fig. 1 and Fig. 2,
 Theorem 1's exact accounting, brute force on tiny graphs, an independent
 sparse-matrix form of Algorithm 1, the greedy matching's 1/2-approximation
 against an exact maximum-weight matching, constant-feature and closed-form
 loss cases, central finite differences of the loss, and closed forms of the
-optimisers under a constant gradient.
+optimisers under a constant gradient, the sampler's published generator
+outputs, a closed-form step share between two regular components, its
+steady state (visits in proportion to degree) and a dense-matrix induced
+subgraph.
 
 Parity unpinned (no printed value or closed form fixes it): the greedy
 matching's order among equal weights. The paper leaves it open; the oracle
