@@ -65,7 +65,7 @@ const char* gcn_last_error(void);
 
 /* ABI version of this header (bumped on incompatible change). */
 int gcn_abi_version(void);
-#define GCN_ABI_VERSION 4
+#define GCN_ABI_VERSION 5
 
 /* ------------------------------------------------ subgraph (host, a1)
  * gcn_subgraph_build - undirected simple subgraph in CSR form.
@@ -91,6 +91,68 @@ int gcn_subgraph_build(int64_t n_full, const int64_t* src, const int64_t* dst,
 int gcn_graph_info(gcn_graph_t g, int32_t* n, int64_t* nnz,
                    const int32_t** rowptr, const int32_t** col);
 void gcn_graph_free(gcn_graph_t g);
+
+/* ------------------------------------------ minibatch sampling (host)
+ * gcn_sample_frontier - the vertex set of one minibatch, drawn from the full
+ * training graph by frontier sampling. Section 3.1 forms a minibatch as the
+ * subgraph induced on vertices that a graph sampler draws from the training
+ * graph, and names the multi-dimensional random walk of the cited work
+ * (Ribeiro and Towsley, IMC 2010) as such a sampler. As run here:
+ *   1. a frontier of m distinct vertices is drawn uniformly (a draw that
+ *      repeats a taken vertex is dropped and drawn again); they are sampled;
+ *   2. each step picks frontier slot s with probability deg(u_s) / (sum of
+ *      the frontier's degrees) - the first slot whose running degree sum
+ *      exceeds a uniform draw r in [0, sum) - moves along a uniformly chosen
+ *      edge (u_s, v), puts v in slot s and samples v;
+ *   3. it stops once `budget` distinct vertices are sampled, after
+ *      max_steps steps, or when every frontier vertex is isolated.
+ * Random numbers: SplitMix64 of `seed` (Steele, Lea and Flood, OOPSLA
+ * 2014) as a counter-based generator, output i = mix(seed + (i+1) *
+ * 0x9E3779B97F4A7C15); a draw in [0, b) is the high 64 bits of output * b;
+ * outputs are used in the order: the initial frontier's draws, then per step
+ * the slot draw and the edge draw.
+ *   full       graph from gcn_subgraph_build (vertices = NULL); read only,
+ *              so concurrent calls on one graph are safe
+ *   m, budget  1 <= m <= budget <= n of `full`
+ *   max_steps  >= 0
+ *   vertices   host int32[budget]: receives the sampled ids, ascending
+ *   n_out      receives their count (budget unless the walk stopped early)
+ *   steps_out  NULL, or receives the number of steps taken
+ * Errors: GCN_E_INVALID_ARG (NULL, sizes as above); GCN_E_OOM.
+ */
+int gcn_sample_frontier(gcn_graph_t full, int32_t m, int32_t budget, uint64_t seed,
+                        int64_t max_steps, int32_t* vertices, int32_t* n_out,
+                        int64_t* steps_out);
+
+/* gcn_subgraph_induce - the subgraph of `full` induced on a vertex subset
+ * (Section 3.1): vertex vertices[k] becomes k, an edge is kept when both
+ * ends are in the subset, lists sorted. The same graph as gcn_subgraph_build
+ * on the full graph's edges with this subset, in time proportional to the
+ * subset's degree sum.
+ *   vertices   host int32[n_vertices], distinct, each in [0, n of full)
+ *   out        receives a new graph; free with gcn_graph_free
+ * Errors: GCN_E_INVALID_ARG (NULL, out-of-range or repeated id); GCN_E_OOM.
+ */
+int gcn_subgraph_induce(gcn_graph_t full, const int32_t* vertices, int32_t n_vertices,
+                        gcn_graph_t* out);
+
+/* gcn_gather_rows - rows of the full graph's arrays for the minibatch's
+ * vertices (Section 4.1: the accelerator receives the input features of the
+ * minibatch's vertices; their labels likewise): dst row k = src row idx[k].
+ *   src       device, rows of row_bytes bytes at a stride of ld_src bytes,
+ *             n_src rows
+ *   idx       device int32[n]
+ *   dst       device, n rows at a stride of ld_dst bytes; bytes of a row
+ *             beyond row_bytes are never written
+ * Rows whose idx lies outside [0, n_src) are not written. 16-byte copies
+ * when both pointers, both strides and row_bytes are multiples of 16, else
+ * 4-byte copies when they are multiples of 4, else single bytes.
+ * Errors: GCN_E_INVALID_ARG (NULL with n > 0, negative sizes, row_bytes
+ * above a stride); GCN_E_HIP.
+ */
+int gcn_gather_rows(const void* src, int64_t ld_src, int64_t n_src, const int32_t* idx,
+                    int32_t n, int64_t row_bytes, void* dst, int64_t ld_dst,
+                    gcn_stream_t stream);
 
 /* ------------------------------------- redundancy reduction (host, a2)
  * gcn_redundancy_reduce - rounds of Algorithms 1-3 (Section 3.2).
@@ -178,7 +240,10 @@ int gcn_redundancy_reduce_device(gcn_graph_t g, const gcn_rr_params* params, voi
  * gcn_graph_image_bytes - size of the packed image (host and device).
  * gcn_graph_pack        - write the image into a caller host buffer (may
  *                         be pinned); the reduced object may then be freed.
- * gcn_graph_upload      - copy the image to a caller device buffer on
+ * gcn_graph_upload      - copy `bytes` bytes from host_image (the image
+ *                         and anything the caller placed after it, such as
+ *                         a sampled pipeline job's vertex ids) to a caller
+ *                         device buffer of at least `bytes` bytes on
  *                         `stream` (hipMemcpyAsync; the host buffer must
  *                         stay valid until the copy completes) and fill the
  *                         descriptor, whose pointers are into dev_buf.
@@ -228,6 +293,13 @@ int gcn_graph_describe(const void* host_image, size_t bytes,
  *          allocates, grows on demand and frees at destroy.
  * gcn_pipeline_submit - copies the edge arrays (the caller may free them on
  *   return) and queues the job; *job_id receives its number (0, 1, ...).
+ * gcn_pipeline_submit_sample - queues a job that samples its vertex set
+ *   from `full` (gcn_sample_frontier with these arguments) and induces the
+ *   subgraph on it (gcn_subgraph_induce) before the reduction and packing.
+ *   `full` is borrowed: keep it alive until the job has been taken. The
+ *   job's buffer holds the image and, at info.vertices_offset, the sampled
+ *   ids (the induced subgraph's vertex k is the k-th), and `bytes` from
+ *   gcn_pipeline_next covers both, so one copy uploads them together.
  * gcn_pipeline_next - waits for the oldest job not yet taken and returns its
  *   image (valid until gcn_pipeline_release) and timings. A failed job
  *   returns its error code (the pipeline keeps going). At most `depth` jobs
@@ -245,6 +317,12 @@ typedef struct {
     int64_t nnz;          /* list entries of G_s^#     */
     int64_t nnz_direct;   /* list entries of G_s       */
     double build_ms, reduce_ms, pack_ms;   /* wall time of this job's steps */
+    double sample_ms;     /* sampled jobs: the walk (0 otherwise)         */
+    int64_t image_bytes;  /* the graph image, at the buffer's start       */
+    int64_t vertices_offset;  /* sampled jobs: byte offset of the sampled
+                             ids, int32[n] ascending, in the buffer (a
+                             multiple of 256); -1 otherwise              */
+    int64_t steps;        /* sampled jobs: walk steps taken               */
 } gcn_pipeline_info;
 
 #define GCN_PIPE_PINNED 1
@@ -256,6 +334,9 @@ int gcn_pipeline_submit(gcn_pipeline_t p, int64_t n_full, const int64_t* src,
                         const int64_t* dst, int64_t n_edges,
                         const int64_t* vertices, int64_t n_vertices,
                         int64_t* job_id);
+int gcn_pipeline_submit_sample(gcn_pipeline_t p, gcn_graph_t full, int32_t m,
+                               int32_t budget, uint64_t seed, int64_t max_steps,
+                               int64_t* job_id);
 int gcn_pipeline_next(gcn_pipeline_t p, int64_t* job_id, const void** image,
                       size_t* bytes, gcn_pipeline_info* info);
 int gcn_pipeline_release(gcn_pipeline_t p, int64_t job_id);

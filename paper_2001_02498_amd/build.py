@@ -20,7 +20,7 @@ OUT_DIR = os.path.join(PKG, "_lib")
 LIB = os.path.join(OUT_DIR, "libgcnact.so")
 OBJ_DIR = os.path.join(ROOT, "_build", "obj")
 
-SOURCES = ["host_graph.cpp", "reduce_dev.hip", "agg.hip", "gemm.hip", "loss.hip", "prof.hip",
+SOURCES = ["host_graph.cpp", "sample.cpp", "gather.hip", "reduce_dev.hip", "agg.hip", "gemm.hip", "loss.hip", "prof.hip",
            "pipeline.hip",
            "api.hip"]
 ARCH = "gfx950"

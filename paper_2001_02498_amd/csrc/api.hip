@@ -759,7 +759,9 @@ int gcn_graph_upload(const void* host_image, size_t bytes, void* dev_buf,
     if (rc) return rc;
     ImageHeader h;
     std::memcpy(&h, host_image, sizeof(h));
-    GCN_HIP(hipMemcpyAsync(dev_buf, host_image, (size_t)h.total, hipMemcpyHostToDevice,
+    // all `bytes`: the image and what the caller placed after it (a sampled
+    // pipeline job's vertex ids)
+    GCN_HIP(hipMemcpyAsync(dev_buf, host_image, bytes, hipMemcpyHostToDevice,
                            (hipStream_t)stream),
             "gcn_graph_upload");
     *out = tmp;

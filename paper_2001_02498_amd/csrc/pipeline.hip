@@ -1,6 +1,7 @@
 // Host side of the per-minibatch schedule (Section 4.4): while the device
 // trains on one subgraph, host threads prepare the next ones — subgraph
-// construction, redundancy reduction (Algorithms 1-3 in rounds, on the host
+// construction (from an edge list, or by frontier sampling of a full graph
+// and the induced subgraph, Section 3.1), redundancy reduction (Algorithms 1-3 in rounds, on the host
 // or driven on the GPU from the worker's own stream) and packing of the
 // device image into (optionally pinned) host memory — each worker on its
 // own subgraph, since minibatches are independent. The consumer takes
@@ -34,6 +35,11 @@ struct Job {
     int64_t n_full = 0;
     std::vector<int64_t> src, dst, verts;
     bool has_verts = false;
+    // sampled jobs: frontier sampling on a full graph the caller keeps alive
+    gcn_graph_t full = nullptr;
+    int32_t m = 0, budget = 0;
+    uint64_t seed = 0;
+    int64_t max_steps = 0;
     // results
     bool done = false;
     int status = GCN_OK;
@@ -158,16 +164,42 @@ struct gcn_pipeline {
         const auto t0 = clock::now();
         gcn_graph_t g = nullptr;
         gcn_reduced_t r = nullptr;
-        int rc = gcn_subgraph_build(job.n_full, job.src.data(), job.dst.data(),
+        int rc = GCN_OK;
+        std::vector<int32_t> sampled;
+        auto ts = t0;
+        if (job.full) {
+            // the walk, then the subgraph induced on its vertices
+            int32_t count = 0;
+            int64_t steps = 0;
+            try {
+                sampled.resize((size_t)job.budget);
+            } catch (const std::bad_alloc&) {
+                set_error("gcn_pipeline: out of host memory");
+                rc = GCN_E_OOM;
+            }
+            if (rc == GCN_OK)
+                rc = gcn_sample_frontier(job.full, job.m, job.budget, job.seed, job.max_steps,
+                                         sampled.data(), &count, &steps);
+            sampled.resize(rc == GCN_OK ? (size_t)count : 0);
+            job.info.steps = steps;
+            ts = clock::now();
+            if (rc == GCN_OK) rc = gcn_subgraph_induce(job.full, sampled.data(), count, &g);
+        } else {
+            rc = gcn_subgraph_build(job.n_full, job.src.data(), job.dst.data(),
                                     (int64_t)job.src.size(),
                                     job.has_verts ? job.verts.data() : nullptr,
                                     (int64_t)job.verts.size(), &g);
+        }
         const auto t1 = clock::now();
         if (rc == GCN_OK)
             rc = device_reduce ? reduce_on_device(g, ds, &r) : gcn_redundancy_reduce(g, &rr, &r);
         const auto t2 = clock::now();
-        size_t bytes = 0;
-        if (rc == GCN_OK) rc = gcn_graph_image_bytes(r, seg_len, &bytes);
+        size_t img = 0, bytes = 0;
+        if (rc == GCN_OK) rc = gcn_graph_image_bytes(r, seg_len, &img);
+        // a sampled job's vertex ids follow the image (256-byte aligned), so
+        // one copy moves both
+        const size_t voff = job.full ? (size_t)gcn::round_up((int64_t)img, 256) : img;
+        bytes = voff + sizeof(int32_t) * sampled.size();
         if (rc == GCN_OK) {
             alloc(buf, bytes);
             if (!buf.ptr) {
@@ -175,7 +207,15 @@ struct gcn_pipeline {
                 rc = GCN_E_OOM;
             }
         }
-        if (rc == GCN_OK) rc = gcn_graph_pack(r, seg_len, buf.ptr, bytes);
+        if (rc == GCN_OK) rc = gcn_graph_pack(r, seg_len, buf.ptr, img);
+        if (rc == GCN_OK && job.full) {
+            std::memset(static_cast<char*>(buf.ptr) + img, 0, voff - img);
+            if (!sampled.empty())
+                std::memcpy(static_cast<char*>(buf.ptr) + voff, sampled.data(),
+                            sizeof(int32_t) * sampled.size());
+        }
+        job.info.image_bytes = (int64_t)img;
+        job.info.vertices_offset = job.full ? (int64_t)voff : -1;
         const auto t3 = clock::now();
         if (rc == GCN_OK) {
             int32_t n = 0, naux = 0, rounds = 0;
@@ -194,7 +234,8 @@ struct gcn_pipeline {
         auto ms = [](auto a, auto b) {
             return std::chrono::duration<double, std::milli>(b - a).count();
         };
-        job.info.build_ms = ms(t0, t1);
+        job.info.sample_ms = ms(t0, ts);
+        job.info.build_ms = ms(ts, t1);
         job.info.reduce_ms = ms(t1, t2);
         job.info.pack_ms = ms(t2, t3);
         job.status = rc;
@@ -272,6 +313,39 @@ int gcn_pipeline_submit(gcn_pipeline_t p, int64_t n_full, const int64_t* src,
         return GCN_OK;
     } catch (const std::bad_alloc&) {
         set_error("gcn_pipeline_submit: out of host memory");
+        return GCN_E_OOM;
+    }
+}
+
+int gcn_pipeline_submit_sample(gcn_pipeline_t p, gcn_graph_t full, int32_t m,
+                               int32_t budget, uint64_t seed, int64_t max_steps,
+                               int64_t* job_id) {
+    GCN_CHECK_ARG(p && full, "gcn_pipeline_submit_sample: NULL argument");
+    int32_t n = 0;
+    int64_t nnz = 0;
+    if (int rc = gcn_graph_info(full, &n, &nnz, nullptr, nullptr)) return rc;
+    GCN_CHECK_ARG(m >= 1 && m <= budget && budget <= n,
+                  "gcn_pipeline_submit_sample: need 1 <= m (%d) <= budget (%d) <= n (%d)", m,
+                  budget, n);
+    GCN_CHECK_ARG(max_steps >= 0, "gcn_pipeline_submit_sample: negative max_steps");
+    try {
+        auto job = std::make_shared<Job>();
+        job->full = full;
+        job->m = m;
+        job->budget = budget;
+        job->seed = seed;
+        job->max_steps = max_steps;
+        {
+            std::lock_guard<std::mutex> lk(p->mu);
+            job->id = p->next_id++;
+            p->jobs[job->id] = job;
+            p->todo.push_back(job);
+            if (job_id) *job_id = job->id;
+        }
+        p->cv_work.notify_one();
+        return GCN_OK;
+    } catch (const std::bad_alloc&) {
+        set_error("gcn_pipeline_submit_sample: out of host memory");
         return GCN_E_OOM;
     }
 }

@@ -34,6 +34,8 @@ enum Kind : int {
     K_GEMM_DW_IN,
     K_GEMM_FWD_IN_BF16,
     K_GEMM_DW_IN_BF16,
+    // rows of the full graph's features and labels for a sampled minibatch
+    K_GATHER,
     K_COUNT
 };
 

@@ -53,6 +53,7 @@ const char* kind_name(int k) {
         case K_GEMM_DW_IN: return "gemm_dw_in";
         case K_GEMM_FWD_IN_BF16: return "gemm_fwd_in_bf16";
         case K_GEMM_DW_IN_BF16: return "gemm_dw_in_bf16";
+        case K_GATHER: return "gather_rows";
         default: return "other";
     }
 }

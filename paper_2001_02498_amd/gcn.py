@@ -43,7 +43,7 @@ OPT_MOMENTUM = 1
 OPT_ADAM = 2
 AGG_MEAN = 0
 AGG_TRANSPOSED = 1
-ABI_VERSION = 4
+ABI_VERSION = 5
 
 _i32, _i64, _f32 = C.c_int32, C.c_int64, C.c_float
 _vp, _sz = C.c_void_p, C.c_size_t
@@ -109,6 +109,10 @@ _abi_version = _proto("gcn_abi_version", [])
 _subgraph_build = _proto("gcn_subgraph_build", [_i64, _vp, _vp, _i64, _vp, _i64, C.POINTER(_vp)])
 _graph_info = _proto("gcn_graph_info", [_vp, _pi32, _pi64, C.POINTER(_pi32), C.POINTER(_pi32)])
 _graph_free = _proto("gcn_graph_free", [_vp], None)
+_sample_frontier = _proto("gcn_sample_frontier", [_vp, _i32, _i32, C.c_uint64, _i64, _vp,
+                                                  _pi32, _pi64])
+_subgraph_induce = _proto("gcn_subgraph_induce", [_vp, _vp, _i32, C.POINTER(_vp)])
+_gather_rows = _proto("gcn_gather_rows", [_vp, _i64, _i64, _vp, _i32, _i64, _vp, _i64, _vp])
 _reduce = _proto("gcn_redundancy_reduce", [_vp, C.POINTER(RrParams), C.POINTER(_vp)])
 _reduce_dev_bytes = _proto("gcn_redundancy_reduce_device_bytes",
                            [_vp, C.POINTER(RrParams), C.POINTER(_sz)])
@@ -171,13 +175,17 @@ _prof_read = _proto("gcn_profile_read", [C.POINTER(ProfileEntry), _i32, _pi32, _
 class PipelineInfo(C.Structure):
     _fields_ = [("n", _i32), ("naux", _i32), ("rounds", _i32), ("reserved", _i32),
                 ("nnz", _i64), ("nnz_direct", _i64), ("build_ms", C.c_double),
-                ("reduce_ms", C.c_double), ("pack_ms", C.c_double)]
+                ("reduce_ms", C.c_double), ("pack_ms", C.c_double),
+                ("sample_ms", C.c_double), ("image_bytes", _i64),
+                ("vertices_offset", _i64), ("steps", _i64)]
 
 
 _pipe_create = _proto("gcn_pipeline_create", [C.POINTER(RrParams), _i32, _i32, _i32, _i32,
                                               C.POINTER(_vp)])
 _pipe_submit = _proto("gcn_pipeline_submit", [_vp, _i64, _vp, _vp, _i64, _vp, _i64,
                                               C.POINTER(_i64)])
+_pipe_submit_sample = _proto("gcn_pipeline_submit_sample", [_vp, _vp, _i32, _i32, C.c_uint64,
+                                                            _i64, C.POINTER(_i64)])
 _pipe_next = _proto("gcn_pipeline_next", [_vp, C.POINTER(_i64), C.POINTER(_vp), C.POINTER(_sz),
                                           C.POINTER(PipelineInfo)])
 _pipe_release = _proto("gcn_pipeline_release", [_vp, _i64])
@@ -185,7 +193,8 @@ _pipe_destroy = _proto("gcn_pipeline_destroy", [_vp], None)
 
 EXPORTS = [
     "gcn_last_error", "gcn_abi_version", "gcn_subgraph_build", "gcn_graph_info",
-    "gcn_graph_free", "gcn_redundancy_reduce", "gcn_reduced_info", "gcn_reduced_free",
+    "gcn_graph_free", "gcn_sample_frontier", "gcn_subgraph_induce", "gcn_gather_rows",
+    "gcn_redundancy_reduce", "gcn_reduced_info", "gcn_reduced_free",
     "gcn_redundancy_reduce_device_bytes", "gcn_redundancy_reduce_device",
     "gcn_graph_image_bytes", "gcn_graph_pack", "gcn_graph_upload", "gcn_graph_describe",
     "gcn_scratch_bytes", "gcn_aggregate", "gcn_layer_fwd", "gcn_classifier_fwd",
@@ -193,7 +202,7 @@ EXPORTS = [
     "gcn_workspace_bytes", "gcn_train_step", "gcn_train_step_optim", "gcn_infer", "gcn_profile_enable",
     "gcn_profile_disable",
     "gcn_profile_read", "gcn_pipeline_create", "gcn_pipeline_submit", "gcn_pipeline_next",
-    "gcn_pipeline_release", "gcn_pipeline_destroy",
+    "gcn_pipeline_release", "gcn_pipeline_destroy", "gcn_pipeline_submit_sample",
 ]
 
 
@@ -254,11 +263,48 @@ def subgraph_build(n_full, src, dst, vertices=None) -> Graph:
     if src.shape != dst.shape:
         raise ValueError("src and dst differ in length")
     v = None if vertices is None else np.ascontiguousarray(vertices, dtype=np.int64)
+    # an empty subset still passes a pointer (NULL means every vertex)
+    vp = None if v is None else (_np_ptr(v) if v.size else np.zeros(1, np.int64).ctypes.data_as(_vp))
     out = _vp()
-    _check(_subgraph_build(int(n_full), _np_ptr(src), _np_ptr(dst), src.size,
-                           _np_ptr(v) if v is not None else None,
+    _check(_subgraph_build(int(n_full), _np_ptr(src), _np_ptr(dst), src.size, vp,
                            0 if v is None else v.size, C.byref(out)))
     return Graph(out.value)
+
+
+def sample_frontier(full: Graph, m, budget, seed, max_steps):
+    """Frontier sampling of a minibatch's vertex set from `full`.
+    Returns (vertices int32 ascending, steps taken)."""
+    out = np.empty(max(int(budget), 0), dtype=np.int32)
+    cnt, steps = _i32(), _i64()
+    _check(_sample_frontier(full._h, int(m), int(budget), int(seed) & (2 ** 64 - 1),
+                            int(max_steps), _np_ptr(out), C.byref(cnt), C.byref(steps)))
+    return out[:cnt.value].copy(), steps.value
+
+
+def subgraph_induce(full: Graph, vertices) -> Graph:
+    """Subgraph of `full` induced on `vertices` (vertex vertices[k] becomes k)."""
+    v = np.ascontiguousarray(vertices, dtype=np.int32)
+    out = _vp()
+    _check(_subgraph_induce(full._h, _np_ptr(v), v.size, C.byref(out)))
+    return Graph(out.value)
+
+
+def gather_rows(src, idx, dst, n_src=None, stream=None):
+    """dst[k] = src[idx[k]] on the device for 2-D tensors (rows may be
+    strided views; row widths equal), or 1-D tensors of 4-byte elements."""
+    if src.dim() == 1:
+        src, dst = src.view(-1, 1), dst.view(-1, 1)
+    if src.dtype != dst.dtype or src.shape[1] != dst.shape[1]:
+        raise ValueError("src and dst rows differ")
+    if src.stride(1) != 1 or dst.stride(1) != 1 or idx.dtype.itemsize != 4:
+        raise ValueError("rows must be contiguous and idx int32")
+    es = src.element_size()
+    n = idx.numel()
+    if dst.shape[0] < n:
+        raise ValueError("dst has fewer rows than idx")
+    _check(_gather_rows(_ptr(src), src.stride(0) * es, src.shape[0] if n_src is None else n_src,
+                        _ptr(idx), n, src.shape[1] * es, _ptr(dst), dst.stride(0) * es,
+                        _stream(stream)))
 
 
 class Reduced:
@@ -536,6 +582,14 @@ class Pipeline:
         _check(_pipe_submit(self._h, int(n_full), _np_ptr(src), _np_ptr(dst), src.size,
                             _np_ptr(v) if v is not None else None, 0 if v is None else v.size,
                             C.byref(jid)))
+        return jid.value
+
+    def submit_sample(self, full: Graph, m, budget, seed, max_steps):
+        """Queue a job that samples its subgraph from `full` (kept alive by
+        the caller until the job is taken)."""
+        jid = _i64()
+        _check(_pipe_submit_sample(self._h, full._h, int(m), int(budget),
+                                   int(seed) & (2 ** 64 - 1), int(max_steps), C.byref(jid)))
         return jid.value
 
     def next(self):

@@ -179,6 +179,98 @@ def small_workload(n, dbar, L, f_in, h, C, loss, seed, gamma=2.5, reduce=True,
                     rounds=rounds, budget=budget, seed=(1000,) + tuple(seed))
 
 
+def chung_lu_edge_draws(n, gamma, dbar, rng):
+    """Chung-Lu graph for full training graphs too large for one draw per
+    pair: round(n dbar / 2) edges, each endpoint drawn independently with
+    probability r_i / sum(r) (the same raw weights as chung_lu_edges), then a
+    seeded relabelling. Self-loops and repeated edges stay in the list; the
+    graph builders drop them, so the realised mean degree is a little below
+    dbar."""
+    r = (np.arange(n, dtype=np.float64) + 1.0) ** (-1.0 / (gamma - 1.0))
+    cdf = np.cumsum(r)
+    cdf /= cdf[-1]
+    m = int(round(n * dbar / 2.0))
+    src = np.minimum(np.searchsorted(cdf, rng.random(m), side="right"), n - 1)
+    dst = np.minimum(np.searchsorted(cdf, rng.random(m), side="right"), n - 1)
+    perm = rng.permutation(n).astype(np.int64)
+    return perm[src.astype(np.int64)], perm[dst.astype(np.int64)]
+
+
+@dataclasses.dataclass(frozen=True)
+class SampledWorkload:
+    """Minibatches sampled from one full training graph (Section 3.1): the
+    full graph's shape, the frontier sampler's size and budget, and the model
+    trained on each induced subgraph."""
+    name: str
+    n_full: int
+    gamma: float
+    dbar: float
+    m: int             # frontier size
+    budget: int        # sampled vertices per minibatch
+    max_steps: int     # walk cap
+    L: int
+    f_in: int
+    h: int
+    C: int
+    loss: int
+    theta: int = 2
+    rounds: int = 5
+    aux_budget: float = 0.5
+    lr: float = 0.01
+    seed: tuple = ()
+
+    @property
+    def max_aux(self) -> int:
+        return int(math.ceil(self.aux_budget * self.budget)) - 1
+
+    def sample_seed(self, i: int) -> int:
+        """Seed of the i-th minibatch's walk (64-bit)."""
+        ss = np.random.SeedSequence(list(self.seed) + [int(i)])
+        return int(ss.generate_state(1, dtype=np.uint64)[0])
+
+
+# A Yelp-sized full graph (Table 2: 716,847 vertices, 6,977,410 edges) with
+# the epoch stream's model (3 layers, 256 inputs, 256 per branch, 64
+# classes); 8,000-vertex minibatches by frontier sampling with 1,000 walkers.
+SAMPLED = {
+    "yelpfull": SampledWorkload("yelpfull", 716847, 2.5, 2 * 6977410 / 716847, 1000, 8000,
+                                200000, 3, 256, 256, 64, SOFTMAX_CE, seed=(6,)),
+}
+
+
+@dataclasses.dataclass
+class FullInputs:
+    wl: SampledWorkload
+    src: np.ndarray
+    dst: np.ndarray
+    X: np.ndarray           # n_full x f_in float32
+    W_self: list
+    W_neigh: list
+    W_cls: np.ndarray
+    labels: np.ndarray      # int32[n_full] (softmax) or uint8[n_full, C]
+
+
+def make_full_inputs(wl: SampledWorkload, n_full=None) -> FullInputs:
+    """The full graph, its features and labels, and the model's initial
+    weights (streams: graph, features, weights, labels). `n_full` overrides
+    the vertex count (same recipe, for tests)."""
+    n = wl.n_full if n_full is None else int(n_full)
+    g_rng, x_rng, w_rng, y_rng = _streams(wl.seed)
+    src, dst = chung_lu_edge_draws(n, wl.gamma, wl.dbar, g_rng)
+    X = x_rng.standard_normal((n, wl.f_in), dtype=np.float32)
+    Ws, Wn = [], []
+    for layer in range(1, wl.L + 1):
+        fi = wl.f_in if layer == 1 else 2 * wl.h
+        Ws.append(glorot(w_rng, fi, wl.h))
+        Wn.append(glorot(w_rng, fi, wl.h))
+    Wc = glorot(w_rng, 2 * wl.h, wl.C)
+    if wl.loss == SOFTMAX_CE:
+        labels = y_rng.integers(0, wl.C, size=n).astype(np.int32)
+    else:
+        labels = (y_rng.random((n, wl.C)) < 0.1).astype(np.uint8)
+    return FullInputs(wl, src, dst, X, Ws, Wn, Wc, labels)
+
+
 def random_edges(n, m, rng, self_loops=True, duplicates=True):
     """Uniform random edge list (may hold self-loops and repeats) for tests of
     the subgraph builder's clean-up."""
