@@ -102,6 +102,7 @@ _CLASS_SOURCES = {
     "agg": ["agg.hip", "kernels.h", "api.hip", "host_graph.cpp"],
     "loss": ["loss.hip", "kernels.h", "api.hip"],
     "sgd": ["gemm.hip", "kernels.h", "api.hip"],
+    "gather": ["gather.hip"],
 }
 _ROLE_CLASS = ["gemm_fwd", "gemm_cls", "gemm_dx", "gemm_cls_dx", "gemm_dw", "gemm_cls_dw",
                "gemm_fwd_in", "gemm_dw_in"]
@@ -114,6 +115,8 @@ def _family(cls):
         return "agg"
     if cls.startswith("loss"):
         return "loss"
+    if cls == "gather_rows":
+        return "gather"
     return "sgd"
 
 
@@ -140,7 +143,8 @@ def kernel_class(name):
         return "pair_sums" if head.split(">")[0].rstrip().endswith("true") else "list_sums"
     for key, cls in (("fixup_kernel<", "list_fixup"), ("sgd_reduce_kernel", "sgd_reduce"),
                      ("splitk_finish_kernel", "splitk_finish"), ("loss_kernel<", "loss_rows"),
-                     ("mean_kernel", "loss_mean"), ("to_bf16_kernel", "to_bf16")):
+                     ("mean_kernel", "loss_mean"), ("to_bf16_kernel", "to_bf16"),
+                     ("gather_rows_kernel<", "gather_rows")):
         if key in name:
             return cls
     return None
@@ -693,6 +697,225 @@ def run_stream(args):
     }
 
 
+def cpu_baseline_sampled(wl, fi, budget_s):
+    """The oracle per sampled minibatch: its walk and induced subgraph on the
+    full graph (plain loops), then its training step; the full graph's CSR is
+    built once beforehand, as the library builds it once."""
+    import threadpoolctl
+    from oracle import gcn as og
+    from oracle import graph as gr
+    from oracle import sample as osample
+    rp, cl = gr.subgraph_build(wl.n_full, fi.src, fi.dst)
+    params = dict(W_self=fi.W_self, W_neigh=fi.W_neigh, b=[None] * wl.L, W_cls=fi.W_cls,
+                  b_cls=None)
+    reps, t0 = 0, time.perf_counter()
+    while True:
+        V = osample.frontier_sample(rp, cl, wl.m, wl.budget, wl.sample_seed(reps),
+                                    wl.max_steps)
+        srp, scl = osample.induce(rp, cl, V)
+        og.train_step(srp, scl, fi.X[V], params, fi.labels[V], wl.loss, wl.lr)
+        reps += 1
+        el = time.perf_counter() - t0
+        if el >= budget_s or reps >= 100:
+            break
+    threads = max((p.get("num_threads", 1) for p in threadpoolctl.threadpool_info()
+                   if p.get("user_api") == "blas"), default=1)
+    return dict(value=round(reps / el, 4), unit="steps/s", cores=int(threads), kind="oracle",
+                sample=f"{reps} sampled minibatches of {wl.name} (oracle walk and induced "
+                       f"subgraph, then a float64 oracle step) in {el:.1f} s; BLAS threads "
+                       f"{threads} (the walk and induction are single-threaded), "
+                       f"os.cpu_count {os.cpu_count()}")
+
+
+def run_sampled(args):
+    """Minibatches sampled from one full graph (Section 3.1), trained in turn.
+
+    The full graph's CSR lives on the host, its features and labels in device
+    memory. A minibatch = frontier sampling + induced subgraph + reduction +
+    packing (host workers, gcn_pipeline_submit_sample), one upload of the
+    image with the sampled ids, gathers of the minibatch's feature and label
+    rows on the device, and the training step. Phase A prepares every
+    minibatch first and times the device work alone (gathers + step); phase B
+    overlaps host preparation with device training (Section 4.4), with the
+    reduction on the host workers, then on the GPU."""
+    import collections
+
+    import numpy as np
+    import torch
+
+    from paper_2001_02498_amd import gcn, synth
+
+    wl = synth.SAMPLED[args.workload]
+    K = args.stream_len
+    t0 = time.perf_counter()
+    fi = synth.make_full_inputs(wl)
+    full = gcn.subgraph_build(wl.n_full, fi.src, fi.dst)
+    X_full = _mat(fi.X)
+    Y_full = torch.from_numpy(fi.labels).cuda()
+    frp, _ = full.csr()
+    fdeg = np.diff(frp)
+    print(f"[bench] full graph {wl.n_full} vertices, {full.nnz} list entries: inputs ready in "
+          f"{time.perf_counter() - t0:.1f} s", file=sys.stderr, flush=True)
+    Ws = [_mat(w, wl.h) for w in fi.W_self]
+    Wn = [_mat(w, wl.h) for w in fi.W_neigh]
+    Wc = torch.from_numpy(fi.W_cls.copy()).cuda()
+    P = gcn.make_params(Ws, Wn, Wc)
+    desc = gcn.model_desc(wl.L, wl.f_in, wl.h, wl.C, wl.loss, X_full.stride(0))
+    loss = torch.zeros(1, device="cuda")
+    Xb = torch.empty((wl.budget, X_full.stride(0)), dtype=torch.float32, device="cuda")
+    Yb = torch.empty(wl.budget, dtype=torch.int32, device="cuda")
+    seeds = [wl.sample_seed(i) for i in range(K)]
+    workers = args.workers or min(16, os.cpu_count() or 1)
+
+    def new_pipe(nw, device_reduce):
+        return gcn.Pipeline(theta=wl.theta, max_rounds=wl.rounds, max_aux=wl.max_aux,
+                            seg_len=args.seg_len, workers=nw, depth=2 * nw + 2, pinned=True,
+                            num_threads=1, device_reduce=device_reduce)
+
+    # Phase A: every minibatch prepared and resident, then device work alone
+    pipe = new_pipe(workers, False)
+    images, infos = [], []
+    for sd in seeds:
+        pipe.submit_sample(full, wl.m, wl.budget, sd, wl.max_steps)
+    for i in range(K):
+        jid, ptr, nb, info = pipe.next()
+        buf = gcn.alloc_ws(nb)
+        d = gcn.upload_image(ptr, nb, buf)
+        torch.cuda.synchronize()
+        pipe.release(jid)
+        images.append((buf, d, nb))
+        infos.append(info)
+    pipe.close()
+    dgs = [_Desc(d) for _, d, _ in images]
+    ws = gcn.alloc_ws(max(gcn.workspace_bytes(d, desc) for d in dgs))
+    img_bytes = max(nb for _, _, nb in images)
+
+    def step(i, dg, buf, info):
+        n = info.n
+        vidx = buf[info.vertices_offset:info.vertices_offset + 4 * n].view(torch.int32)
+        X = Xb[:n, :wl.f_in]
+        gcn.gather_rows(X_full, vidx, X)
+        gcn.gather_rows(Y_full, vidx, Yb[:n])
+        gcn.train_step(dg, desc, P, X, Yb[:n], wl.lr, loss, ws)
+
+    for i in range(min(args.warmup, K)):
+        step(i, dgs[i], images[i][0], infos[i])
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(K):
+        step(i, dgs[i], images[i][0], infos[i])
+    torch.cuda.synchronize()
+    gpu_ms = 1e3 * (time.perf_counter() - t0) / K
+    gcn.profile_enable(8192)
+    for i in range(min(args.profile_steps, K)):
+        step(i, dgs[i], images[i][0], infos[i])
+    torch.cuda.synchronize()
+    prof = gcn.profile_read(reset=True)
+    gcn.profile_disable()
+    print(f"[bench] device only: {gpu_ms:.3f} ms/step", file=sys.stderr, flush=True)
+
+    # Phase B: the overlapped schedule
+    slots = [gcn.alloc_ws(img_bytes) for _ in range(2)]
+    copy = torch.cuda.Stream()
+    comp = torch.cuda.current_stream()
+
+    def overlapped(nw, device_reduce):
+        slot_free = [None, None]
+        held = collections.deque()
+        got = []
+        p = new_pipe(nw, device_reduce)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for sd in seeds:
+            p.submit_sample(full, wl.m, wl.budget, sd, wl.max_steps)
+        for i in range(K):
+            jid, ptr, nb, info = p.next()
+            got.append(info)
+            slot = i % 2
+            with torch.cuda.stream(copy):
+                if slot_free[slot] is not None:
+                    copy.wait_event(slot_free[slot])
+                d = gcn.upload_image(ptr, nb, slots[slot], stream=copy)
+                copied = torch.cuda.Event()
+                copied.record(copy)
+            comp.wait_event(copied)
+            step(i, _Desc(d), slots[slot], info)
+            done = torch.cuda.Event()
+            done.record(comp)
+            slot_free[slot] = done
+            held.append((jid, copied))
+            while len(held) > 1:
+                j, e = held.popleft()
+                e.synchronize()
+                p.release(j)
+        torch.cuda.synchronize()
+        ms = 1e3 * (time.perf_counter() - t0) / K
+        for j, _ in held:
+            p.release(j)
+        p.close()
+        return ms, got
+
+    pipe_ms, pinfos = overlapped(workers, False)
+    print(f"[bench] pipelined with {workers} workers: {pipe_ms:.3f} ms/step", file=sys.stderr,
+          flush=True)
+    dworkers = args.device_workers
+    dev_ms, dinfos = overlapped(dworkers, True)
+    print(f"[bench] pipelined with {dworkers} workers reducing on the GPU: {dev_ms:.3f} ms/step",
+          file=sys.stderr, flush=True)
+    ktab = kernel_table(prof, min(args.profile_steps, K))
+    dominant = max(ktab, key=lambda k: ktab[k]["ms_per_step"])
+    roof = roofline(dominant, ktab[dominant], wl.name)
+    cpu = None
+    if not args.no_cpu_baseline:
+        cpu = cpu_baseline_sampled(wl, fi, args.cpu_seconds)
+
+    def mean(xs):
+        return round(float(np.mean(xs)), 3)
+    return {
+        "metric": METRIC,
+        "value": round(1e3 / pipe_ms, 3),
+        "unit": "steps/s",
+        "n_gpus": 1,
+        "steps": K,
+        "warmup": args.warmup,
+        "ms_per_step": round(pipe_ms, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {
+            "workload": (f"{wl.name}: {K} minibatches of {wl.budget} vertices sampled by "
+                         f"frontier sampling ({wl.m} walkers) from a {wl.n_full}-vertex "
+                         f"Chung-Lu graph (exponent {wl.gamma}, mean degree {wl.dbar:.2f}); "
+                         f"{wl.L}-layer GCN, f_in {wl.f_in}, {wl.h} per branch, {wl.C}-class "
+                         f"softmax CE, reduced graph ({wl.rounds} rounds, threshold "
+                         f"{wl.theta}, budget {wl.aux_budget} n); host preparation of later "
+                         f"minibatches overlapped with device training"),
+            "n_full": wl.n_full, "full_nnz": int(full.nnz), "full_max_degree": int(fdeg.max()),
+            "host_workers": workers, "parallelism": "single GPU",
+        },
+        "roofline": {k: v for k, v in roof.items() if k != "kernel"} | {"kernel": dominant},
+        "cpu_baseline": cpu,
+        "device_only_ms_per_step": round(gpu_ms, 4),
+        "minibatch": {"n_mean": mean([i.n for i in infos]),
+                      "nnz_mean": mean([i.nnz_direct for i in infos]),
+                      "nnz_reduced_mean": mean([i.nnz for i in infos]),
+                      "naux_mean": mean([i.naux for i in infos]),
+                      "walk_steps_mean": mean([i.steps for i in infos])},
+        "host_ms_per_minibatch": {"sample": mean([i.sample_ms for i in pinfos]),
+                                  "induce": mean([i.build_ms for i in pinfos]),
+                                  "reduce": mean([i.reduce_ms for i in pinfos]),
+                                  "pack": mean([i.pack_ms for i in pinfos])},
+        "device_reduction_pipeline": {
+            "ms_per_step": round(dev_ms, 4), "steps_per_s": round(1e3 / dev_ms, 3),
+            "workers": dworkers, "reduce_ms_mean": mean([i.reduce_ms for i in dinfos])},
+        "kernels": {k: {kk: vv for kk, vv in v.items()
+                        if kk not in ("flops_per_launch", "bytes_per_launch")}
+                    for k, v in ktab.items()},
+    }
+
+
 class InferSetup(Setup):
     """A whole graph and the model on the device, ready for timed inference."""
 
@@ -833,6 +1056,9 @@ def main():
         return
     if args.workload == "stream8k":
         print(json.dumps(run_stream(args)), flush=True)
+        return
+    if args.workload in synth.SAMPLED:
+        print(json.dumps(run_sampled(args)), flush=True)
         return
     wl = synth.WORKLOADS[args.workload]
     inp = synth.make_inputs(wl)
