@@ -104,6 +104,7 @@ _CLASS_SOURCES = {
     "sgd": ["gemm.hip", "kernels.h", "api.hip"],
     "gather": ["gather.hip"],
 }
+_SAMPLED_NAMES = ("yelpfull",)
 _ROLE_CLASS = ["gemm_fwd", "gemm_cls", "gemm_dx", "gemm_cls_dx", "gemm_dw", "gemm_cls_dw",
                "gemm_fwd_in", "gemm_dw_in"]
 
@@ -297,7 +298,11 @@ def trace_summary(stats_csv, workload, cmd_args, bench_line=None):
            f"python3 $R/bench.py {bargs}",
            f"python3 bench.py --workload {workload} --traced-args='{cmd_args}' "
            "--trace-summary OUT/run_kernel_stats.csv --bench-line OUT/line.json", "```",
-           "", ("The run covers the warm-up, timed and profiled inference calls on the "
+           "", ("The run covers the device-only pass over the sampled minibatches (gathers "
+                "and steps), then the host-pipelined and device-reduction-pipelined passes; "
+                "the device reduction's own kernels are listed per kernel below, outside "
+                "the timing classes." if workload in _SAMPLED_NAMES else
+                "The run covers the warm-up, timed and profiled inference calls on the "
                 "reduced graph." if infer and "--no-direct" in cmd_args else
                 "The run covers the warm-up, timed and profiled steps of the reduced-graph "
                 "step alone." if all(f in cmd_args for f in ("--no-direct", "--no-narrow", "--no-adam")) else
