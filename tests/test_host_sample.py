@@ -182,3 +182,25 @@ def test_pipeline_sampled_rejects():
             pipe.submit_sample(full, 1, 11, 0, 10)      # budget > n
     finally:
         pipe.close()
+
+
+def test_sample_full_size():
+    # the benchmarked shape: the 716,847-vertex full graph, 1,000 walkers,
+    # 8,000 vertices, the first two minibatch seeds; and the induced
+    # subgraph of the first against the oracle's
+    wl = synth.SAMPLED["yelpfull"]
+    fi = synth.make_full_inputs(wl)
+    full = gcn.subgraph_build(wl.n_full, fi.src, fi.dst)
+    rp, cl = ograph.subgraph_build(wl.n_full, fi.src, fi.dst)
+    grp, gcl = full.csr()
+    assert np.array_equal(grp, rp) and np.array_equal(gcl, cl)
+    rpl, cll = rp.tolist(), cl.tolist()
+    for i in range(2):
+        seed = wl.sample_seed(i)
+        want, want_steps = _oracle_sample(rpl, cll, wl.m, wl.budget, seed, wl.max_steps)
+        got, steps = gcn.sample_frontier(full, wl.m, wl.budget, seed, wl.max_steps)
+        assert steps == want_steps and np.array_equal(got, want) and got.size == wl.budget
+        if i == 0:
+            orp, ocl = osample.induce(rp, cl, want)
+            srp, scl = gcn.subgraph_induce(full, got).csr()
+            assert np.array_equal(srp, orp) and np.array_equal(scl, ocl)
