@@ -610,13 +610,15 @@ def run_stream(args):
     copy = torch.cuda.Stream()
     comp = torch.cuda.current_stream()
 
-    def overlapped(workers, device_reduce):
+    def overlapped(workers, device_reduce, device_workers=None):
         slot_free = [None, None]
         held = collections.deque()
         infos = []
+        nw = workers + (device_workers or 0)
         pipe = gcn.Pipeline(theta=wl.theta, max_rounds=wl.rounds, max_aux=wl.max_aux,
-                            seg_len=args.seg_len, workers=workers, depth=2 * workers + 2,
-                            pinned=True, num_threads=1, device_reduce=device_reduce)
+                            seg_len=args.seg_len, workers=workers, depth=2 * nw + 2,
+                            pinned=True, num_threads=1, device_reduce=device_reduce,
+                            device_workers=device_workers)
         torch.cuda.synchronize()
         t0 = time.perf_counter()
         for inp in inps:
@@ -656,6 +658,10 @@ def run_stream(args):
     dev_ms, dinfos = overlapped(dworkers, True)
     print(f"[bench] pipelined with {dworkers} workers reducing on the GPU: {dev_ms:.3f} ms/step",
           file=sys.stderr, flush=True)
+    hmix = max(1, workers - dworkers)
+    mix_ms, minfos = overlapped(hmix, False, dworkers)
+    print(f"[bench] pipelined with {hmix} host and {dworkers} GPU-reducing workers: "
+          f"{mix_ms:.3f} ms/step", file=sys.stderr, flush=True)
     ktab = kernel_table(prof, min(args.profile_steps, K))
     dominant = max(ktab, key=lambda k: ktab[k]["ms_per_step"])
     roof = roofline(dominant, ktab[dominant], "stream8k")
@@ -696,6 +702,11 @@ def run_stream(args):
             "reduce_ms_mean": round(sum(i.reduce_ms for i in dinfos) / K, 3),
             "note": "the same schedule with each worker running Algorithms 1-3 on the GPU "
                     "(gcn_redundancy_reduce_device, identical result) on a stream of its own"},
+        "mixed_reduction_pipeline": {
+            "ms_per_step": round(mix_ms, 4), "steps_per_s": round(1e3 / mix_ms, 3),
+            "host_workers": hmix, "device_workers": dworkers,
+            "note": "host and GPU-reducing workers taking jobs from one queue "
+                    "(gcn_pipeline_create_mixed)"},
         "kernels": {k: {kk: vv for kk, vv in v.items()
                         if kk not in ("flops_per_launch", "bytes_per_launch")}
                     for k, v in ktab.items()},
@@ -772,10 +783,12 @@ def run_sampled(args):
     seeds = [wl.sample_seed(i) for i in range(K)]
     workers = args.workers or min(16, os.cpu_count() or 1)
 
-    def new_pipe(nw, device_reduce):
+    def new_pipe(nw, device_reduce, device_workers=None):
+        tot = nw + (device_workers or 0)
         return gcn.Pipeline(theta=wl.theta, max_rounds=wl.rounds, max_aux=wl.max_aux,
-                            seg_len=args.seg_len, workers=nw, depth=2 * nw + 2, pinned=True,
-                            num_threads=1, device_reduce=device_reduce)
+                            seg_len=args.seg_len, workers=nw, depth=2 * tot + 2, pinned=True,
+                            num_threads=1, device_reduce=device_reduce,
+                            device_workers=device_workers)
 
     # Phase A: every minibatch prepared and resident, then device work alone
     pipe = new_pipe(workers, False)
@@ -824,11 +837,11 @@ def run_sampled(args):
     copy = torch.cuda.Stream()
     comp = torch.cuda.current_stream()
 
-    def overlapped(nw, device_reduce):
+    def overlapped(nw, device_reduce, device_workers=None):
         slot_free = [None, None]
         held = collections.deque()
         got = []
-        p = new_pipe(nw, device_reduce)
+        p = new_pipe(nw, device_reduce, device_workers)
         torch.cuda.synchronize()
         t0 = time.perf_counter()
         for sd in seeds:
@@ -867,6 +880,10 @@ def run_sampled(args):
     dev_ms, dinfos = overlapped(dworkers, True)
     print(f"[bench] pipelined with {dworkers} workers reducing on the GPU: {dev_ms:.3f} ms/step",
           file=sys.stderr, flush=True)
+    hmix = max(1, workers - dworkers)
+    mix_ms, _ = overlapped(hmix, False, dworkers)
+    print(f"[bench] pipelined with {hmix} host and {dworkers} GPU-reducing workers: "
+          f"{mix_ms:.3f} ms/step", file=sys.stderr, flush=True)
     ktab = kernel_table(prof, min(args.profile_steps, K))
     dominant = max(ktab, key=lambda k: ktab[k]["ms_per_step"])
     roof = roofline(dominant, ktab[dominant], wl.name)
@@ -915,6 +932,9 @@ def run_sampled(args):
         "device_reduction_pipeline": {
             "ms_per_step": round(dev_ms, 4), "steps_per_s": round(1e3 / dev_ms, 3),
             "workers": dworkers, "reduce_ms_mean": mean([i.reduce_ms for i in dinfos])},
+        "mixed_reduction_pipeline": {
+            "ms_per_step": round(mix_ms, 4), "steps_per_s": round(1e3 / mix_ms, 3),
+            "host_workers": hmix, "device_workers": dworkers},
         "kernels": {k: {kk: vv for kk, vv in v.items()
                         if kk not in ("flops_per_launch", "bytes_per_launch")}
                     for k, v in ktab.items()},

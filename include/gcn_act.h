@@ -330,6 +330,15 @@ typedef struct {
 int gcn_pipeline_create(const gcn_rr_params* params, int32_t seg_len,
                         int32_t workers, int32_t depth, int32_t flags,
                         gcn_pipeline_t* out);
+/* gcn_pipeline_create_mixed - the same pipeline with host_workers reducing
+ * on the host and device_workers on the GPU (as GCN_PIPE_DEVICE_REDUCE);
+ * every job goes to whichever worker is free, and since both reductions give
+ * the same result, so do the jobs. flags: GCN_PIPE_PINNED only.
+ * Errors: GCN_E_INVALID_ARG (no worker, more than 256, other flags); as
+ * gcn_pipeline_create otherwise. */
+int gcn_pipeline_create_mixed(const gcn_rr_params* params, int32_t seg_len,
+                              int32_t host_workers, int32_t device_workers, int32_t depth,
+                              int32_t flags, gcn_pipeline_t* out);
 int gcn_pipeline_submit(gcn_pipeline_t p, int64_t n_full, const int64_t* src,
                         const int64_t* dst, int64_t n_edges,
                         const int64_t* vertices, int64_t n_vertices,

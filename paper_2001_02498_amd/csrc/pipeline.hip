@@ -91,14 +91,16 @@ struct gcn_pipeline {
 
     // per-worker device state of the device reduction
     struct DevState {
+        bool device = false;   // this worker reduces on the GPU
         hipStream_t stream = nullptr;
         void* ws = nullptr;
         size_t cap = 0;
     };
 
-    void run() {
+    void run(bool device_worker) {
         DevState ds;
-        if (device_reduce) {
+        ds.device = device_worker;
+        if (device_worker) {
             (void)hipSetDevice(device);
             if (hipStreamCreate(&ds.stream) != hipSuccess) ds.stream = nullptr;
         }
@@ -192,7 +194,7 @@ struct gcn_pipeline {
         }
         const auto t1 = clock::now();
         if (rc == GCN_OK)
-            rc = device_reduce ? reduce_on_device(g, ds, &r) : gcn_redundancy_reduce(g, &rr, &r);
+            rc = ds.device ? reduce_on_device(g, ds, &r) : gcn_redundancy_reduce(g, &rr, &r);
         const auto t2 = clock::now();
         size_t img = 0, bytes = 0;
         if (rc == GCN_OK) rc = gcn_graph_image_bytes(r, seg_len, &img);
@@ -253,37 +255,51 @@ struct gcn_pipeline {
 
 extern "C" {
 
-int gcn_pipeline_create(const gcn_rr_params* params, int32_t seg_len, int32_t workers,
-                        int32_t depth, int32_t flags, gcn_pipeline_t* out) {
+int gcn_pipeline_create_mixed(const gcn_rr_params* params, int32_t seg_len,
+                              int32_t host_workers, int32_t device_workers, int32_t depth,
+                              int32_t flags, gcn_pipeline_t* out) {
     GCN_CHECK_ARG(params && out, "gcn_pipeline_create: NULL argument");
-    GCN_CHECK_ARG(workers >= 1 && workers <= 256, "gcn_pipeline_create: workers outside [1, 256]");
+    GCN_CHECK_ARG(host_workers >= 0 && device_workers >= 0 &&
+                      host_workers + device_workers >= 1 && host_workers + device_workers <= 256,
+                  "gcn_pipeline_create: workers outside [1, 256]");
     GCN_CHECK_ARG(depth >= 1 && depth <= 4096, "gcn_pipeline_create: depth outside [1, 4096]");
     GCN_CHECK_ARG(params->theta >= 0 && params->max_rounds >= 0 &&
                       params->max_rounds <= GCN_MAX_ROUNDS && params->num_threads >= 0,
                   "gcn_pipeline_create: bad reduction parameters");
     GCN_CHECK_ARG(seg_len == 0 || (seg_len >= 1 && seg_len <= 65536),
                   "gcn_pipeline_create: seg_len outside [1, 65536]");
-    GCN_CHECK_ARG((flags & ~(GCN_PIPE_PINNED | GCN_PIPE_DEVICE_REDUCE)) == 0,
-                  "gcn_pipeline_create: unknown flags 0x%x", flags);
+    GCN_CHECK_ARG((flags & ~GCN_PIPE_PINNED) == 0, "gcn_pipeline_create: unknown flags 0x%x",
+                  flags);
     try {
         auto* p = new gcn_pipeline;
         p->rr = *params;
         p->seg_len = seg_len;
         p->depth = depth;
         p->pinned = (flags & GCN_PIPE_PINNED) != 0;
-        p->device_reduce = (flags & GCN_PIPE_DEVICE_REDUCE) != 0;
+        p->device_reduce = device_workers > 0;
         if (p->device_reduce && hipGetDevice(&p->device) != hipSuccess) {
             delete p;
             set_error("gcn_pipeline_create: no current GPU for the device reduction");
             return GCN_E_HIP;
         }
-        for (int32_t i = 0; i < workers; ++i) p->workers.emplace_back([p] { p->run(); });
+        for (int32_t i = 0; i < device_workers; ++i) p->workers.emplace_back([p] { p->run(true); });
+        for (int32_t i = 0; i < host_workers; ++i) p->workers.emplace_back([p] { p->run(false); });
         *out = p;
         return GCN_OK;
     } catch (const std::exception& e) {
         set_error("gcn_pipeline_create: %s", e.what());
         return GCN_E_OOM;
     }
+}
+
+int gcn_pipeline_create(const gcn_rr_params* params, int32_t seg_len, int32_t workers,
+                        int32_t depth, int32_t flags, gcn_pipeline_t* out) {
+    GCN_CHECK_ARG((flags & ~(GCN_PIPE_PINNED | GCN_PIPE_DEVICE_REDUCE)) == 0,
+                  "gcn_pipeline_create: unknown flags 0x%x", flags);
+    GCN_CHECK_ARG(workers >= 1 && workers <= 256, "gcn_pipeline_create: workers outside [1, 256]");
+    const bool dev = (flags & GCN_PIPE_DEVICE_REDUCE) != 0;
+    return gcn_pipeline_create_mixed(params, seg_len, dev ? 0 : workers, dev ? workers : 0, depth,
+                                     flags & GCN_PIPE_PINNED, out);
 }
 
 int gcn_pipeline_submit(gcn_pipeline_t p, int64_t n_full, const int64_t* src,

@@ -182,6 +182,8 @@ class PipelineInfo(C.Structure):
 
 _pipe_create = _proto("gcn_pipeline_create", [C.POINTER(RrParams), _i32, _i32, _i32, _i32,
                                               C.POINTER(_vp)])
+_pipe_create_mixed = _proto("gcn_pipeline_create_mixed", [C.POINTER(RrParams), _i32, _i32, _i32,
+                                                          _i32, _i32, C.POINTER(_vp)])
 _pipe_submit = _proto("gcn_pipeline_submit", [_vp, _i64, _vp, _vp, _i64, _vp, _i64,
                                               C.POINTER(_i64)])
 _pipe_submit_sample = _proto("gcn_pipeline_submit_sample", [_vp, _vp, _i32, _i32, C.c_uint64,
@@ -203,6 +205,7 @@ EXPORTS = [
     "gcn_profile_disable",
     "gcn_profile_read", "gcn_pipeline_create", "gcn_pipeline_submit", "gcn_pipeline_next",
     "gcn_pipeline_release", "gcn_pipeline_destroy", "gcn_pipeline_submit_sample",
+    "gcn_pipeline_create_mixed",
 ]
 
 
@@ -567,9 +570,17 @@ class Pipeline:
     """Host worker pool preparing graph images in submission order."""
 
     def __init__(self, theta=2, max_rounds=5, max_aux=-1, seg_len=0, workers=4, depth=8,
-                 pinned=True, num_threads=1, device_reduce=False):
+                 pinned=True, num_threads=1, device_reduce=False, device_workers=None):
+        """`workers` threads reducing on the host (on the GPU with
+        device_reduce); device_workers > 0 adds that many GPU-reducing
+        workers beside `workers` host ones."""
         p = RrParams(int(theta), int(max_rounds), int(max_aux), int(num_threads), 0)
         self._h = _vp()
+        if device_workers is not None:
+            _check(_pipe_create_mixed(C.byref(p), int(seg_len), int(workers), int(device_workers),
+                                      int(depth), PIPE_PINNED if pinned else 0,
+                                      C.byref(self._h)))
+            return
         flags = (PIPE_PINNED if pinned else 0) | (PIPE_DEVICE_REDUCE if device_reduce else 0)
         _check(_pipe_create(C.byref(p), int(seg_len), int(workers), int(depth), flags,
                             C.byref(self._h)))

@@ -26,7 +26,7 @@ def _model(gcn, wl, inp):
     return Ws, Wn, Wc
 
 
-@pytest.mark.parametrize("device_reduce", [False, True])
+@pytest.mark.parametrize("device_reduce", [False, True, "mixed"])
 def test_pipelined_stream_matches_sequential(device_reduce):
     need_gpu()
     from paper_2001_02498_amd import gcn
@@ -64,8 +64,13 @@ def test_pipelined_stream_matches_sequential(device_reduce):
     comp = torch.cuda.current_stream()
     slot_free = [None, None]
     held = collections.deque()
-    pipe = gcn.Pipeline(theta=wl.theta, max_rounds=wl.rounds, max_aux=wl.max_aux, workers=3,
-                        depth=4, pinned=True, device_reduce=device_reduce)
+    if device_reduce == "mixed":
+        # two host and two GPU-reducing workers share the queue
+        pipe = gcn.Pipeline(theta=wl.theta, max_rounds=wl.rounds, max_aux=wl.max_aux,
+                            workers=2, device_workers=2, depth=4, pinned=True)
+    else:
+        pipe = gcn.Pipeline(theta=wl.theta, max_rounds=wl.rounds, max_aux=wl.max_aux,
+                            workers=3, depth=4, pinned=True, device_reduce=device_reduce)
     try:
         for inp in inps:
             pipe.submit(wl.n, inp.src, inp.dst)

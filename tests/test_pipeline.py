@@ -117,3 +117,28 @@ def test_pipeline_argument_errors():
         gcn.Pipeline(depth=0)
     with pytest.raises(gcn.GcnError):
         gcn.Pipeline(max_rounds=gcn.MAX_ROUNDS + 1)
+
+
+def test_mixed_pipeline_host_only_and_rejects():
+    # the mixed form with no GPU-reducing worker is the host pipeline
+    rng = np.random.default_rng(11)
+    graphs = []
+    for _ in range(5):
+        n = int(rng.integers(50, 200))
+        s, d = synth.random_edges(n, 6 * n, rng)
+        graphs.append((n, s, d))
+    pipe = gcn.Pipeline(theta=1, max_rounds=2, seg_len=5, workers=3, device_workers=0, depth=3,
+                        pinned=False)
+    try:
+        for n, s, d in graphs:
+            pipe.submit(n, s, d)
+        for i, (n, s, d) in enumerate(graphs):
+            jid, ptr, nb, info = pipe.next()
+            want, _ = _direct_image(n, s, d, 1, 2, 5)
+            assert jid == i and np.array_equal(_image_bytes(ptr, nb), want)
+            pipe.release(jid)
+    finally:
+        pipe.close()
+    for hw, dw in ((0, 0), (-1, 1), (200, 100)):
+        with pytest.raises(gcn.GcnError):
+            gcn.Pipeline(workers=hw, device_workers=dw, pinned=False)
