@@ -576,6 +576,7 @@ class Pipeline:
         workers beside `workers` host ones."""
         p = RrParams(int(theta), int(max_rounds), int(max_aux), int(num_threads), 0)
         self._h = _vp()
+        self._borrowed = {}   # job id -> full graph a sampled job reads
         if device_workers is not None:
             _check(_pipe_create_mixed(C.byref(p), int(seg_len), int(workers), int(device_workers),
                                       int(depth), PIPE_PINNED if pinned else 0,
@@ -601,12 +602,14 @@ class Pipeline:
         jid = _i64()
         _check(_pipe_submit_sample(self._h, full._h, int(m), int(budget),
                                    int(seed) & (2 ** 64 - 1), int(max_steps), C.byref(jid)))
+        self._borrowed[jid.value] = full   # freed only once the job is taken
         return jid.value
 
     def next(self):
         """(job_id, host_ptr, nbytes, info) of the oldest job not yet taken."""
         jid, ptr, nb, info = _i64(), _vp(), _sz(), PipelineInfo()
         rc = _pipe_next(self._h, C.byref(jid), C.byref(ptr), C.byref(nb), C.byref(info))
+        self._borrowed.pop(jid.value, None)
         if rc != OK:
             raise GcnError(rc, last_error())
         return jid.value, ptr.value, nb.value, info
@@ -616,8 +619,9 @@ class Pipeline:
 
     def close(self):
         if getattr(self, "_h", None) and self._h.value:
-            _pipe_destroy(self._h)
+            _pipe_destroy(self._h)   # joins the workers: no job reads a graph after this
             self._h = _vp()
+        self._borrowed = {}
 
     def __del__(self):
         self.close()

@@ -204,3 +204,32 @@ def test_sample_full_size():
             orp, ocl = osample.induce(rp, cl, want)
             srp, scl = gcn.subgraph_induce(full, got).csr()
             assert np.array_equal(srp, orp) and np.array_equal(scl, ocl)
+
+
+def test_pipeline_keeps_sampled_graph_alive():
+    # the caller may drop its handle right after submitting
+    import gc
+    n, s, d = _graphs(50, 500, 3000)
+    rp, cl = _oracle_csr(n, s, d)
+    pipe = gcn.Pipeline(theta=2, max_rounds=2, workers=2, depth=2, pinned=False)
+    try:
+        pipe.submit_sample(gcn.subgraph_build(n, s, d), 4, 100, 77, 10 ** 6)
+        gc.collect()
+        jid, ptr, nb, info = pipe.next()
+        want, _ = _oracle_sample(rp, cl, 4, 100, 77, 10 ** 6)
+        got = _image(ptr, nb)[info.vertices_offset:].view(np.int32)
+        assert np.array_equal(got, want)
+        pipe.release(jid)
+    finally:
+        pipe.close()
+
+
+def test_gather_rows_rejects_before_launch():
+    # argument checks run before any device call, so they hold without a GPU
+    f = gcn._gather_rows
+    fake = gcn._vp(4096)
+    assert f(None, 16, 10, fake, 5, 16, fake, 16, None) == gcn.E_INVALID_ARG    # NULL src
+    assert f(fake, 16, 10, fake, 5, 32, fake, 64, None) == gcn.E_INVALID_ARG    # row > ld_src
+    assert f(fake, 64, 10, fake, 5, 32, fake, 16, None) == gcn.E_INVALID_ARG    # row > ld_dst
+    assert f(fake, 16, 10, fake, -1, 16, fake, 16, None) == gcn.E_INVALID_ARG   # negative n
+    assert f(None, 16, 10, None, 0, 16, None, 16, None) == gcn.OK               # nothing to do
