@@ -7,6 +7,7 @@
 // latency; independent minibatches run on independent host threads.
 #include <algorithm>
 #include <cstring>
+#include <memory>
 #include <new>
 #include <vector>
 
@@ -203,7 +204,7 @@ int gcn_subgraph_induce(gcn_graph_t full, const int32_t* vertices, int32_t n_ver
             ascending = ascending && (k == 0 || vertices[k - 1] < vertices[k]);
         }
 
-        auto* g = new gcn_graph;
+        auto g = std::make_unique<gcn_graph>();
         g->n = n_vertices;
         g->rowptr.assign((size_t)n_vertices + 1, 0);
         const int32_t* rowptr = full->rowptr.data();
@@ -221,7 +222,7 @@ int gcn_subgraph_induce(gcn_graph_t full, const int32_t* vertices, int32_t n_ver
             if (!ascending) std::sort(g->col.begin() + first, g->col.end());
             g->rowptr[k + 1] = (int32_t)g->col.size();
         }
-        *out = g;
+        *out = g.release();
         return GCN_OK;
     } catch (const std::bad_alloc&) {
         set_error("gcn_subgraph_induce: out of host memory");
