@@ -270,3 +270,42 @@ def test_step_narrow_rejects_bias():
     with pytest.raises(gcn.GcnError) as e:
         gcn.workspace_bytes(run.case.dg, desc)
     assert e.value.code == gcn.E_UNSUPPORTED
+
+
+def _inputs_with_edges(wl, src, dst, seed):
+    """Seeded features, weights and labels of `wl` on a given edge list."""
+    rng = np.random.default_rng(seed)
+    F = [wl.f_in] + [2 * wl.h] * (wl.L - 1)
+    Ws = [synth.glorot(rng, f, wl.h) for f in F]
+    Wn = [synth.glorot(rng, f, wl.h) for f in F]
+    Wc = synth.glorot(rng, 2 * wl.h, wl.C)
+    X = rng.standard_normal((wl.n, wl.f_in), dtype=np.float32)
+    if wl.loss == synth.SOFTMAX_CE:
+        y = rng.integers(0, wl.C, wl.n).astype(np.int32)
+    else:
+        y = (rng.random((wl.n, wl.C)) < 0.3).astype(np.uint8)
+    return synth.Inputs(wl, np.asarray(src, np.int64), np.asarray(dst, np.int64), X, Ws, Wn,
+                        Wc, y)
+
+
+@pytest.mark.parametrize("shape", ["edgeless", "single", "bipartite"])
+def test_step_degenerate_graphs(shape):
+    # no edge at all (every aggregated row is zero); one vertex; K_{3,50},
+    # whose 50 identical lists give three pairs of weight 50 for the
+    # reduction (one is taken per round, the later rounds see new ids)
+    need_gpu()
+    if shape == "edgeless":
+        wl = synth.small_workload(37, 0, 2, 13, 12, 5, synth.SOFTMAX_CE, (91,))
+        src, dst = [], []
+    elif shape == "single":
+        wl = synth.small_workload(1, 0, 2, 6, 8, 3, synth.SIGMOID_BCE, (92,))
+        src, dst = [], []
+    else:
+        wl = synth.small_workload(53, 0, 3, 10, 16, 4, synth.SOFTMAX_CE, (93,))
+        src = [a for a in range(3) for _ in range(3, 53)]
+        dst = [b for _ in range(3) for b in range(3, 53)]
+    inp = _inputs_with_edges(wl, src, dst, 5)
+    run = StepRun(wl, inp=inp, bias=True, seg_len=8).run()
+    if shape == "bipartite":
+        assert run.case.red.info()["naux"] >= 1
+    check_step(run)
