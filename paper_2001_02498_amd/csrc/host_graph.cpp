@@ -6,6 +6,7 @@
 #include <atomic>
 #include <cstring>
 #include <exception>
+#include <emmintrin.h>
 #include <new>
 #include <numeric>
 #include <thread>
@@ -59,8 +60,38 @@ int pick_threads(int requested, int64_t work) {
     return (int)std::max<int64_t>(1, std::min<int64_t>(t, cap));
 }
 
+// Bit i set when blk[i] > floor, for i < len <= 64.
+inline uint64_t above(const int32_t* blk, int32_t len, int32_t floor) {
+    uint64_t bits = 0;
+    for (int32_t i = 0; i < len; ++i) bits |= (uint64_t)(blk[i] > floor) << i;
+    return bits;
+}
+
+// 16-bit counters: eight per SSE2 compare (blk[i] - floor saturates at zero
+// exactly when blk[i] <= floor); a whole block of 64 is eight compares.
+inline uint64_t above(const uint16_t* blk, int32_t len, uint16_t floor) {
+    if (len < 64) {
+        uint64_t bits = 0;
+        for (int32_t i = 0; i < len; ++i) bits |= (uint64_t)(blk[i] > floor) << i;
+        return bits;
+    }
+    const __m128i f = _mm_set1_epi16((short)floor);
+    const __m128i zero = _mm_setzero_si128();
+    uint64_t le_bits = 0;   // bit i: blk[i] <= floor
+    for (int q = 0; q < 4; ++q) {
+        const __m128i a = _mm_loadu_si128(reinterpret_cast<const __m128i*>(blk + 16 * q));
+        const __m128i b = _mm_loadu_si128(reinterpret_cast<const __m128i*>(blk + 16 * q + 8));
+        // all-ones lanes where the count does not exceed floor, packed to
+        // one byte per lane (saturation keeps -1 and 0), one bit per byte
+        const __m128i le = _mm_packs_epi16(_mm_cmpeq_epi16(_mm_subs_epu16(a, f), zero),
+                                           _mm_cmpeq_epi16(_mm_subs_epu16(b, f), zero));
+        le_bits |= (uint64_t)(uint32_t)_mm_movemask_epi8(le) << (16 * q);
+    }
+    return ~le_bits;
+}
+
 struct Candidate {
-    int64_t w;
+    int32_t w;   // lists holding both (at most the number of lists)
     int32_t x, y;
 };
 
@@ -75,7 +106,8 @@ struct Lists {
 // walk the lists that hold x and count every larger id y that follows x in
 // the same (sorted) list; the count of {x, y} is the number of lists holding
 // both. A dense counter per thread plays the hash table.
-std::vector<Candidate> count_pairs(const Lists& L, int theta, int threads) {
+template <class Count>
+std::vector<Candidate> count_pairs_t(const Lists& L, int theta, int threads) {
     const int32_t ncols = L.ncols;
     // transposed index: for each id, the (list, position) pairs holding it
     std::vector<int64_t> tptr(ncols + 1, 0);
@@ -105,7 +137,7 @@ std::vector<Candidate> count_pairs(const Lists& L, int theta, int threads) {
     std::atomic<int32_t> next{0};
     const int32_t nwords = (ncols + 63) / 64;
     parallel_run(nt, [&](int) {
-        std::vector<int32_t> cnt(ncols, 0);
+        std::vector<Count> cnt(ncols, 0);
         std::vector<uint64_t> seen(nwords, 0);   // ids touched for the current x
         std::vector<Candidate> mine;
         for (;;) {
@@ -115,27 +147,59 @@ std::vector<Candidate> count_pairs(const Lists& L, int theta, int threads) {
             mine.clear();
             for (int32_t x = x0; x < x1; ++x) {
                 if (tptr[x + 1] - tptr[x] < 2) continue;   // in < 2 lists: no pair
+                // visits of x: the tails after x in the lists holding it
+                int64_t visits = 0;
+                for (int64_t k = tptr[x]; k < tptr[x + 1]; ++k) {
+                    const int32_t w = tlist[k];
+                    visits += (L.ptr[w + 1] - L.ptr[w]) - tpos[k] - 1;
+                }
+                // Dense when the counters after x are few against the visits:
+                // count without marking, then sweep every counter after x in
+                // blocks of 64 (a vectorisable compare gives the block's
+                // candidate bits; the block is cleared with plain stores).
+                // Sparse otherwise: mark touched ids in the bitmap and visit
+                // only those. Both emit the same pairs in ascending y.
+                const bool dense = (int64_t)(ncols - x - 1) <= 8 * visits;
                 for (int64_t k = tptr[x]; k < tptr[x + 1]; ++k) {
                     int32_t w = tlist[k];
                     const int32_t* row = L.col.data() + L.ptr[w];
                     int32_t d = (int32_t)(L.ptr[w + 1] - L.ptr[w]);
-                    for (int32_t p = tpos[k] + 1; p < d; ++p) {
-                        int32_t y = row[p];
-                        cnt[y]++;
-                        seen[y >> 6] |= uint64_t(1) << (y & 63);
+                    if (dense) {
+                        for (int32_t p = tpos[k] + 1; p < d; ++p) cnt[row[p]]++;
+                    } else {
+                        for (int32_t p = tpos[k] + 1; p < d; ++p) {
+                            int32_t y = row[p];
+                            cnt[y]++;
+                            seen[y >> 6] |= uint64_t(1) << (y & 63);
+                        }
                     }
                 }
-                // touched ids in ascending order (all exceed x)
-                for (int32_t wd = (x + 1) >> 6; wd < nwords; ++wd) {
-                    uint64_t bits = seen[wd];
-                    if (!bits) continue;
-                    seen[wd] = 0;
-                    while (bits) {
-                        const int32_t y = (wd << 6) + __builtin_ctzll(bits);
-                        bits &= bits - 1;
-                        // weight-1 pairs are not edges of G_a (Alg. 1 drops them)
-                        if (cnt[y] > theta && cnt[y] >= 2) mine.push_back({cnt[y], x, y});
-                        cnt[y] = 0;
+                // weight-1 pairs are not edges of G_a (Alg. 1 drops them)
+                const Count floor = (Count)std::max(theta, 1);
+                if (dense) {
+                    for (int32_t y0 = x + 1; y0 < ncols; y0 += 64) {
+                        const int32_t len = std::min<int32_t>(64, ncols - y0);
+                        Count* blk = cnt.data() + y0;
+                        const uint64_t bits = above(blk, len, floor);
+                        for (uint64_t b = bits; b;) {
+                            const int32_t i = __builtin_ctzll(b);
+                            b &= b - 1;
+                            mine.push_back({(int32_t)blk[i], x, y0 + i});
+                        }
+                        std::memset(blk, 0, sizeof(Count) * len);
+                    }
+                } else {
+                    // touched ids in ascending order (all exceed x)
+                    for (int32_t wd = (x + 1) >> 6; wd < nwords; ++wd) {
+                        uint64_t bits = seen[wd];
+                        if (!bits) continue;
+                        seen[wd] = 0;
+                        while (bits) {
+                            const int32_t y = (wd << 6) + __builtin_ctzll(bits);
+                            bits &= bits - 1;
+                            if (cnt[y] > floor) mine.push_back({(int32_t)cnt[y], x, y});
+                            cnt[y] = 0;
+                        }
                     }
                 }
             }
@@ -150,11 +214,18 @@ std::vector<Candidate> count_pairs(const Lists& L, int theta, int threads) {
     return all;
 }
 
+// A pair's count is at most the number of lists: 16-bit counters when that
+// fits (half the bytes for the dense sweep).
+std::vector<Candidate> count_pairs(const Lists& L, int theta, int threads) {
+    if (L.n < 65536) return count_pairs_t<uint16_t>(L, theta, threads);
+    return count_pairs_t<int32_t>(L, theta, threads);
+}
+
 // Orders candidates by decreasing weight, keeping the (x, y) order among
 // equal weights: a stable counting sort on the (small, integer) weights.
 std::vector<Candidate> order_by_weight(const std::vector<Candidate>& c) {
     int64_t wmax = 0;
-    for (const Candidate& e : c) wmax = std::max(wmax, e.w);
+    for (const Candidate& e : c) wmax = std::max<int64_t>(wmax, e.w);
     std::vector<int64_t> start(wmax + 2, 0);
     for (const Candidate& e : c) start[wmax - e.w + 1]++;
     for (int64_t i = 0; i <= wmax; ++i) start[i + 1] += start[i];
