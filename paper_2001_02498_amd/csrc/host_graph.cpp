@@ -221,6 +221,86 @@ std::vector<Candidate> count_pairs(const Lists& L, int theta, int threads) {
     return count_pairs_t<int32_t>(L, theta, threads);
 }
 
+// Algorithm 1 after a round whose greedy scan ran to the end of its
+// candidates. Every pair counted above theta then had an endpoint taken
+// (the matching is maximal), and a pair with neither endpoint taken nor new
+// is held by the same lists as before, so its count is unchanged: no such
+// pair exceeds theta now. The candidates are therefore the pairs with an
+// endpoint in `touched` (the previous round's matched ids and new ids): for
+// each u in it, the whole lists holding u are counted and every counter is
+// swept; a pair of two touched ids is kept from its smaller one. Returned in
+// Algorithm 2's order (weight descending, then (x, y)).
+template <class Count>
+std::vector<Candidate> count_touched_t(const Lists& L, int theta, int threads,
+                                       const std::vector<int32_t>& touched) {
+    const int32_t ncols = L.ncols;
+    std::vector<char> in_t(ncols, 0);
+    for (int32_t u : touched) in_t[u] = 1;
+    std::vector<int64_t> tptr(ncols + 1, 0);
+    for (int64_t e = 0; e < L.ptr[L.n]; ++e) tptr[L.col[e] + 1]++;
+    for (int32_t c = 0; c < ncols; ++c) tptr[c + 1] += tptr[c];
+    std::vector<int32_t> tlist(L.ptr[L.n]);
+    {
+        std::vector<int64_t> fill(tptr.begin(), tptr.end() - 1);
+        for (int32_t w = 0; w < L.n; ++w)
+            for (int64_t e = L.ptr[w]; e < L.ptr[w + 1]; ++e) tlist[fill[L.col[e]]++] = w;
+    }
+    int64_t work = 0;
+    for (int32_t u : touched)
+        for (int64_t k = tptr[u]; k < tptr[u + 1]; ++k) work += L.ptr[tlist[k] + 1] - L.ptr[tlist[k]];
+    const int nt = pick_threads(threads, work);
+    const int32_t nu = (int32_t)touched.size(), chunk = 16;
+    const int32_t nchunks = (nu + chunk - 1) / chunk;
+    std::vector<std::vector<Candidate>> out(nchunks);
+    std::atomic<int32_t> next{0};
+    const Count floor = (Count)std::max(theta, 1);
+    parallel_run(nt, [&](int) {
+        std::vector<Count> cnt(ncols, 0);
+        for (;;) {
+            const int32_t c = next.fetch_add(1);
+            if (c >= nchunks) break;
+            std::vector<Candidate>& mine = out[c];
+            for (int32_t i = c * chunk; i < std::min(nu, (c + 1) * chunk); ++i) {
+                const int32_t u = touched[i];
+                if (tptr[u + 1] - tptr[u] < 2) continue;   // in < 2 lists: no pair
+                for (int64_t k = tptr[u]; k < tptr[u + 1]; ++k) {
+                    const int32_t w = tlist[k];
+                    for (int64_t e = L.ptr[w]; e < L.ptr[w + 1]; ++e) cnt[L.col[e]]++;
+                }
+                cnt[u] = 0;
+                for (int32_t y0 = 0; y0 < ncols; y0 += 64) {
+                    const int32_t len = std::min<int32_t>(64, ncols - y0);
+                    Count* blk = cnt.data() + y0;
+                    for (uint64_t b = above(blk, len, floor); b;) {
+                        const int32_t j = __builtin_ctzll(b);
+                        b &= b - 1;
+                        const int32_t y = y0 + j;
+                        if (in_t[y] && y < u) continue;
+                        mine.push_back({(int32_t)blk[j], std::min(u, y), std::max(u, y)});
+                    }
+                    std::memset(blk, 0, sizeof(Count) * len);
+                }
+            }
+        }
+    });
+    std::vector<Candidate> all;
+    size_t total = 0;
+    for (auto& v : out) total += v.size();
+    all.reserve(total);
+    for (auto& v : out) all.insert(all.end(), v.begin(), v.end());
+    std::sort(all.begin(), all.end(), [](const Candidate& a, const Candidate& b) {
+        if (a.w != b.w) return a.w > b.w;
+        return a.x != b.x ? a.x < b.x : a.y < b.y;
+    });
+    return all;
+}
+
+std::vector<Candidate> count_touched(const Lists& L, int theta, int threads,
+                                     const std::vector<int32_t>& touched) {
+    if (L.n < 65536) return count_touched_t<uint16_t>(L, theta, threads, touched);
+    return count_touched_t<int32_t>(L, theta, threads, touched);
+}
+
 // Orders candidates by decreasing weight, keeping the (x, y) order among
 // equal weights: a stable counting sort on the (small, integer) weights.
 std::vector<Candidate> order_by_weight(const std::vector<Candidate>& c) {
@@ -423,6 +503,7 @@ int gcn_redundancy_reduce(gcn_graph_t g, const gcn_rr_params* params,
         for (int32_t v = 0; v < n; ++v) r->deg[v] = g->rowptr[v + 1] - g->rowptr[v];
         r->round_offsets.push_back(0);
         const int64_t max_aux = params->max_aux;
+        std::vector<int32_t> touched;
         for (int round = 0; round < params->max_rounds; ++round) {
             int64_t naux = (int64_t)r->pairs.size() / 2;
             int64_t budget_left = max_aux < 0 ? INT64_MAX : max_aux - naux;
@@ -432,10 +513,14 @@ int gcn_redundancy_reduce(gcn_graph_t g, const gcn_rr_params* params,
                 set_error("gcn_redundancy_reduce: vertex ids would exceed 2^31-1");
                 return GCN_E_INVALID_ARG;
             }
-            // Algorithm 1 (candidates above theta only)
-            // Algorithm 2 scans by decreasing weight, then (x, y) ascending
+            // Algorithm 1 (candidates above theta only), from the ids the last
+            // round touched when they are few; Algorithm 2 scans by
+            // decreasing weight, then (x, y) ascending
+            const bool incremental =
+                round > 0 && (int64_t)touched.size() * 5 <= (int64_t)L.ncols;
             const std::vector<Candidate> cand =
-                order_by_weight(count_pairs(L, params->theta, params->num_threads));
+                incremental ? count_touched(L, params->theta, params->num_threads, touched)
+                            : order_by_weight(count_pairs(L, params->theta, params->num_threads));
             std::vector<char> used(L.ncols, 0);
             std::vector<int32_t> partner(L.ncols, -1), newid(L.ncols, -1);
             int64_t taken = 0, wsum = 0;
@@ -457,6 +542,11 @@ int gcn_redundancy_reduce(gcn_graph_t g, const gcn_rr_params* params,
                 ++taken;
             }
             if (taken == 0) break;
+            // the ids this round touched: its matched ids and its new ids
+            touched.clear();
+            for (int32_t v = 0; v < L.ncols; ++v)
+                if (used[v]) touched.push_back(v);
+            for (int32_t k = 0; k < (int32_t)taken; ++k) touched.push_back(L.ncols + k);
             // Algorithm 3
             L = rewrite(L, partner, newid, L.ncols + (int32_t)taken, params->num_threads);
             r->round_offsets.push_back((int32_t)(r->pairs.size() / 2));

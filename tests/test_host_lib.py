@@ -245,3 +245,21 @@ def test_device_image_work_list(seg_len):
     bad[:4] = 0
     with pytest.raises(gcn.GcnError):
         gcn.describe(bad.ctypes.data, nbytes, bad.ctypes.data)
+
+
+@pytest.mark.parametrize("threads", [1, 4])
+def test_reduction_many_rounds_bit_exact(threads):
+    # eight rounds on ppi8k: the later rounds count only the pairs touching
+    # the previous matching (their touched ids fall below a fifth of all ids),
+    # which must give the oracle's full recount exactly
+    wl = synth.WORKLOADS["ppi8k"]
+    inp = synth.make_inputs(wl)
+    g = gcn.subgraph_build(wl.n, inp.src, inp.dst)
+    got = gcn.redundancy_reduce(g, theta=2, max_rounds=8, max_aux=wl.max_aux,
+                                num_threads=threads).info()
+    rp, cl = gr.subgraph_build(wl.n, inp.src, inp.dst)
+    want = rd.reduce(rp, cl, theta=2, max_rounds=8, max_aux=wl.max_aux)
+    assert got["rounds"] == len(want["stats"]) == 8
+    for k in ("rowptr", "col", "pairs", "round_offsets"):
+        assert np.array_equal(got[k], want[k]), k
+    assert [tuple(s) for s in got["stats"]] == [tuple(s) for s in want["stats"]]
