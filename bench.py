@@ -299,9 +299,13 @@ def trace_summary(stats_csv, workload, cmd_args, bench_line=None):
            f"python3 bench.py --workload {workload} --traced-args='{cmd_args}' "
            "--trace-summary OUT/run_kernel_stats.csv --bench-line OUT/line.json", "```",
            "", ("The run covers the device-only pass over the sampled minibatches (gathers "
-                "and steps), then the host-pipelined and device-reduction-pipelined passes; "
-                "the device reduction's own kernels are listed per kernel below, outside "
-                "the timing classes." if workload in _SAMPLED_NAMES else
+                "and steps), then the host-pipelined, device-reduction-pipelined and mixed "
+                "passes; the device reduction's own kernels are listed per kernel below, "
+                "outside the timing classes." if workload in _SAMPLED_NAMES else
+                "The run covers the device-only pass over the 64 subgraphs, then the "
+                "host-pipelined, device-reduction-pipelined and mixed passes; the device "
+                "reduction's own kernels are listed per kernel below, outside the timing "
+                "classes." if workload == "stream8k" else
                 "The run covers the warm-up, timed and profiled inference calls on the "
                 "reduced graph." if infer and "--no-direct" in cmd_args else
                 "The run covers the warm-up, timed and profiled steps of the reduced-graph "
