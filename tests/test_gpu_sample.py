@@ -120,3 +120,39 @@ def test_sampled_minibatch_step():
     say(f"loss {loss.item():.6f} oracle {ref['loss']:.6f}; rel loss {e_loss:.2e} "
         f"dW_cls {e_dw:.2e} W {max(errs):.2e}")
     assert e_loss < FP32_TOL and e_dw < FP32_TOL and max(errs) < FP32_TOL
+
+
+@pytest.mark.parametrize("mode", ["device", "mixed"])
+def test_sampled_jobs_reduced_on_gpu_match_host(mode):
+    # sampled jobs whose reduction runs on the GPU (all workers, or one of
+    # two) give byte-identical buffers (image and ids) to host-reduced jobs
+    need_gpu()
+    import ctypes
+    from paper_2001_02498_amd import gcn
+    wl = synth.SAMPLED["yelpfull"]
+    fi = synth.make_full_inputs(wl, n_full=30000)
+    full = gcn.subgraph_build(30000, fi.src, fi.dst)
+    jobs = [(60, 2000, wl.sample_seed(i), wl.max_steps) for i in range(5)]
+
+    def buffers(**kw):
+        pipe = gcn.Pipeline(theta=wl.theta, max_rounds=wl.rounds, max_aux=wl.max_aux, depth=3,
+                            pinned=True, **kw)
+        out = []
+        try:
+            for j in jobs:
+                pipe.submit_sample(full, *j)
+            for _ in jobs:
+                jid, ptr, nb, info = pipe.next()
+                out.append(bytes((ctypes.c_uint8 * nb).from_address(ptr)))
+                pipe.release(jid)
+        finally:
+            pipe.close()
+        return out
+
+    host = buffers(workers=2)
+    if mode == "device":
+        dev_ = buffers(workers=2, device_reduce=True)
+    else:
+        dev_ = buffers(workers=1, device_workers=1)
+    say("sampled job buffers", [len(b) for b in host])
+    assert host == dev_
