@@ -263,3 +263,26 @@ def test_reduction_many_rounds_bit_exact(threads):
     for k in ("rowptr", "col", "pairs", "round_offsets"):
         assert np.array_equal(got[k], want[k]), k
     assert [tuple(s) for s in got["stats"]] == [tuple(s) for s in want["stats"]]
+
+
+@pytest.mark.parametrize("right", [33000, 66000])
+def test_reduction_counter_width_edges(right):
+    # K_{2,R}: the pair (0, 1) is held by all R lists of the right side, and
+    # every pair of right vertices by exactly two lists (those of 0 and 1),
+    # so with theta 2 round 1 takes (0, 1) alone, weight R, and round 2 finds
+    # nothing. R = 33,000 exceeds the signed 16-bit range on the 16-bit
+    # counter path; 66,002 lists take the 32-bit counter path. Theorem 1
+    # fixes the lists: 4R entries lose R, and the right lists become {n}.
+    # (The oracle's counting would enumerate ~R^2/2 pairs here.)
+    n = right + 2
+    src = [0] * right + [1] * right
+    dst = list(range(2, n)) * 2
+    g = gcn.subgraph_build(n, src, dst)
+    got = gcn.redundancy_reduce(g, theta=2, max_rounds=3).info()
+    assert got["naux"] == 1 and got["rounds"] == 1
+    assert [tuple(p) for p in got["pairs"]] == [(0, 1)]
+    assert list(got["round_offsets"]) == [0, 1]
+    assert tuple(got["stats"][0]) == (1, right, 3 * right, 2 * (right - 1))
+    rp, cl = got["rowptr"], got["col"]
+    assert list(cl[rp[0]:rp[1]]) == list(range(2, n)) == list(cl[rp[1]:rp[2]])
+    assert np.all(np.diff(rp)[2:] == 1) and np.all(cl[rp[2]:] == n)
