@@ -159,11 +159,11 @@ def forward(rowptr, col, X, params):
 def backward(rowptr, col, params, fw, dlogits, masks=None):
     """Eq. 2a-2c for every layer, plus the classifier's gradients.
 
-    masks: optional list of 0/1 arrays, one per layer, taking the ReLU
-    decision [Z_l > 0] from elsewhere. The paper computes in single
-    precision (Section 6); a comparison against a float32 implementation
-    passes the float32 decision here so both sides mask the same entries
-    (an entry with |Z| near 1e-7 may otherwise fall on different sides).
+    masks: optional list of 0/1 arrays, one per layer, to use as the ReLU
+    decision instead of [Z_l > 0]. By default the decision is this oracle's
+    own, from its float64 Z_l. A caller comparing with a lower-precision
+    computation may override entries whose |Z_l| lies within that
+    computation's rounding of zero (the caller states and checks the bound).
 
     Returns dict with dW_self, dW_neigh, db (lists, layer order), dW_cls,
     db_cls, G (masked gradients per layer) and dH (dL/dH_l for l = 1..L).
@@ -212,10 +212,12 @@ def sgd(params, grads, lr):
 
 
 def train_step(rowptr, col, X, params, labels, loss_kind, lr, masks=None, opt=None,
-               state1=None, state2=None):
+               state1=None, state2=None, fw=None):
     """One forward + loss + backward + update step: plain gradient descent
-    with step lr, or the optimiser `opt` (optim.Optim) with its states."""
-    fw = forward(rowptr, col, X, params)
+    with step lr, or the optimiser `opt` (optim.Optim) with its states.
+    fw: forward() of these same inputs, when already computed."""
+    if fw is None:
+        fw = forward(rowptr, col, X, params)
     loss, dlogits = loss_and_grad(loss_kind, fw["logits"], labels)
     grads = backward(rowptr, col, params, fw, dlogits, masks)
     if opt is None:

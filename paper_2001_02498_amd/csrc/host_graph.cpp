@@ -217,6 +217,9 @@ std::vector<Candidate> count_pairs_t(const Lists& L, int theta, int threads) {
 // A pair's count is at most the number of lists: 16-bit counters when that
 // fits (half the bytes for the dense sweep).
 std::vector<Candidate> count_pairs(const Lists& L, int theta, int threads) {
+    // a count is at most the number of lists, so theta >= L.n leaves no pair
+    // (and keeps every floor below within the counter type)
+    if ((int64_t)theta >= (int64_t)L.n) return {};
     if (L.n < 65536) return count_pairs_t<uint16_t>(L, theta, threads);
     return count_pairs_t<int32_t>(L, theta, threads);
 }
@@ -297,6 +300,7 @@ std::vector<Candidate> count_touched_t(const Lists& L, int theta, int threads,
 
 std::vector<Candidate> count_touched(const Lists& L, int theta, int threads,
                                      const std::vector<int32_t>& touched) {
+    if ((int64_t)theta >= (int64_t)L.n) return {};
     if (L.n < 65536) return count_touched_t<uint16_t>(L, theta, threads, touched);
     return count_touched_t<int32_t>(L, theta, threads, touched);
 }

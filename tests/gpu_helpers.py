@@ -88,3 +88,78 @@ class GraphCase:
         i = self.info
         return dict(rowptr=i["rowptr"], col=i["col"], pairs=i["pairs"],
                     round_offsets=i["round_offsets"], naux=i["naux"], n=i["n"])
+
+
+# ------------------------------------------------------------ ReLU decisions
+# The oracle takes its own ReLU decisions, [Z > 0] on its float64 Z. The
+# kernels decide from their float32 (or bfloat16) Z, which differs from Z by
+# rounding, so an entry within that rounding of zero may fall on the other
+# side. Every such disagreement is checked against a bound on
+# |Z_gpu - Z_ref| (Section 2.1, Eq. 1 and Eq. 2a-2c), and only those entries
+# take the kernel's decision.
+#
+# Z_gpu = fl(Hg W + b), Hg the kernel's own layer input (read back), so
+#   Z_gpu - Z_ref = (Hg - H_ref) W + e,
+# where e is the rounding of the product. The first term is bounded
+# rigorously by |Hg - H_ref| |W|. For e the bound is probabilistic (rounding
+# errors independent with mean zero, as in Higham and Mary's probabilistic
+# rounding-error analysis, SIAM J. Sci. Comput. 2019): to first order
+# e = sum_k delta_k S_k with |delta_k| <= u and S_k the partial sums, so by
+# Hoeffding's inequality |e| <= lam u sqrt(sum_k S_k^2) except with
+# probability 2 exp(-lam^2 / 2); terms h_k w_k of random sign (zero-mean
+# weights) make the partial sums a random walk, sum_k S_k^2 ~ K ||t||_2^2 with
+# ||t||_2^2 = sum_k (h_k w_k)^2 + b^2. With bfloat16 operands each term also
+# carries |delta_h + delta_w| <= 2 u16 + u16^2, independent over k:
+# lam (2 u16 + u16^2) ||t||_2 more. lam = 8 (exceedance 2.5e-14 per entry)
+# and a factor 2 for second-order terms:
+#   bound = |Hg - H_ref| |W| + 2 lam (sqrt(K + 2) u + [bf16] (2 u16 + u16^2)) ||t||_2.
+# A narrow-order neighbour half Z = fl(D^-1 A P_gpu), P_gpu = fl(Hg W): the
+# mean of d_w rows adds lam u sqrt(D^-1 A P^2) by the same argument:
+#   bound = D^-1 A |P_gpu - H_ref W| + 2 lam u sqrt(D^-1 A P_gpu^2).
+# For K = 1024, unit weights scale this is ~2e-5 of a typical |Z|, so a
+# kernel that zeroed small activations (which the normwise check of H would
+# let pass) shows up here as disagreements far outside it.
+U32 = 2.0 ** -24
+U16 = 2.0 ** -8
+LAM = 8.0
+
+
+def product_bound(Hg, H_ref, W, b=None, bf16=False):
+    Hg = np.asarray(Hg, np.float64)
+    W = np.asarray(W, np.float64)
+    K = Hg.shape[1]
+    t2 = (Hg * Hg) @ (W * W)
+    if b is not None:
+        t2 = t2 + np.square(np.asarray(b, np.float64))[None, :]
+    gam = np.sqrt(K + 2.0) * U32 + ((2 * U16 + U16 * U16) if bf16 else 0.0)
+    return np.abs(Hg - np.asarray(H_ref, np.float64)) @ np.abs(W) + 2 * LAM * gam * np.sqrt(t2)
+
+
+def narrow_bound(rp, cl, Pg, P_ref):
+    from oracle import gcn as og
+    Pg = np.asarray(Pg, np.float64)
+    err = og.aggregate(rp, cl, np.abs(Pg - P_ref))
+    return err + 2 * LAM * U32 * np.sqrt(og.aggregate(rp, cl, Pg * Pg))
+
+
+def checked_masks(Z_ref, gpu_masks, bounds, tag=""):
+    """Per layer: the oracle's [Z_ref > 0]; wherever the kernel decided
+    otherwise, assert |Z_ref| <= bound there and take the kernel's
+    decision at exactly those entries. Returns (masks, flip counts)."""
+    masks, flips = [], []
+    for l, (Z, mg, bd) in enumerate(zip(Z_ref, gpu_masks, bounds)):
+        mine = Z > 0.0
+        mg = np.asarray(mg, bool)
+        diff = mine != mg
+        nd = int(diff.sum())
+        if nd:
+            z, lim = np.abs(Z[diff]), bd[diff]
+            assert (z <= lim).all(), (
+                f"{tag} layer {l}: {int((z > lim).sum())} of {nd} ReLU decisions differ "
+                f"from the oracle's beyond rounding (worst |Z| {z.max():.3e}, "
+                f"bound there {lim[np.argmax(z)]:.3e})")
+        masks.append(np.where(diff, mg, mine))
+        flips.append(nd)
+    say(f"{tag} ReLU decisions differing from the oracle's, per layer "
+        f"(each within its rounding bound): {flips}")
+    return masks, flips

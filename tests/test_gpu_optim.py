@@ -114,17 +114,13 @@ class OptRun(StepRun):
         self.loss = loss.item()
         return self
 
-    def oracle(self):
-        wl = self.wl
-        masks = self.masks()
+    def oracle(self, unconditioned=False):
         opt = oo.Optim(self.kind, lr=self.hp["lr"], step=self.step,
                        momentum=self.hp["momentum"], beta1=self.hp["beta1"],
                        beta2=self.hp["beta2"], eps=self.hp["eps"])
         s1 = self.state_np[0]
         s2 = self.state_np[1] if len(self.state_np) > 1 else None
-        return og.train_step(self.case.rp, self.case.cl, self.inp.X, self.params_np(),
-                             self.inp.labels, wl.loss, wl.lr, masks=masks, opt=opt,
-                             state1=s1, state2=s2)
+        return super().oracle(unconditioned=unconditioned, opt=opt, state1=s1, state2=s2)
 
 
 def _dev_tensor(run, key, l):

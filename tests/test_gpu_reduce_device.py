@@ -1,8 +1,7 @@
 """The device redundancy reduction (gcn_redundancy_reduce_device) equals the
-host reduction field by field -- pairs, round offsets, rewritten lists and
-per-round counts -- and therefore the oracle (the host library is pinned
-to the oracle bit for bit in test_host_lib.py; the figures are checked here
-against the oracle directly)."""
+oracle's Algorithms 1-3 field by field -- pairs, round offsets, rewritten
+lists and per-round counts -- on every case here, and the host reduction as
+well."""
 import numpy as np
 import pytest
 
@@ -15,11 +14,23 @@ pytestmark = pytest.mark.gpu
 
 
 def _both(gcn, n, s, d, **kw):
+    """Device and host reductions, the device one also checked against the
+    oracle's reduction of the oracle's own subgraph."""
     g = gcn.subgraph_build(n, s, d)
     host = gcn.redundancy_reduce(g, **kw).info()
     ws = gcn.alloc_ws(max(gcn.redundancy_reduce_device_bytes(g, **kw), 256))
     dev = gcn.redundancy_reduce_device(g, ws, **kw).info()
+    rp, cl = gr.subgraph_build(n, s, d)
+    _same_as_oracle(dev, rd.reduce(rp, cl, **kw))
     return host, dev
+
+
+def _same_as_oracle(dev, ora):
+    assert dev["naux"] == ora["naux"]
+    assert np.array_equal(dev["pairs"], np.asarray(ora["pairs"], np.int32).reshape(-1, 2))
+    for k in ("round_offsets", "rowptr", "col"):
+        assert np.array_equal(dev[k], ora[k]), k
+    assert [tuple(x) for x in dev["stats"]] == [tuple(x) for x in ora["stats"]]
 
 
 def _same(host, dev):

@@ -13,7 +13,8 @@ from oracle import gcn as og
 from oracle import graph as ograph
 from oracle import sample as osample
 from paper_2001_02498_amd import synth
-from tests.gpu_helpers import FP32_TOL, dev, empty, need_gpu, rel, say, torch
+from tests.gpu_helpers import (FP32_TOL, checked_masks, dev, empty, need_gpu, product_bound,
+                               rel, say, torch)
 
 pytestmark = pytest.mark.gpu
 
@@ -106,12 +107,26 @@ def test_sampled_minibatch_step():
     assert torch.equal(X.cpu(), torch.from_numpy(fi.X[V]))
     assert np.array_equal(Y.cpu().numpy(), fi.labels[V])
     srp, scl = osample.induce(rp, cl, V)
-    H = [ws[lay.H[l]:lay.H[l] + 4 * n * lay.ld_H].view(torch.float32)
-         .view(n, lay.ld_H)[:, :2 * wl.h].cpu().numpy() for l in range(wl.L)]
+    def region(off, cols, ld):
+        return ws[off:off + 4 * n * ld].view(torch.float32).view(n, ld)[:, :cols].cpu().numpy()
+
+    H = [region(lay.H[l], 2 * wl.h, lay.ld_H) for l in range(wl.L)]
     params = dict(W_self=fi.W_self, W_neigh=fi.W_neigh, b=[None] * wl.L, W_cls=fi.W_cls,
                   b_cls=None)
+    # the oracle's own ReLU decisions; the kernel's may differ only within
+    # rounding of zero (checked), and only there does the oracle follow them
+    fw = og.forward(srp, scl, fi.X[V], params)
+    bounds = []
+    for l in range(wl.L):
+        F = wl.f_in if l == 0 else 2 * wl.h
+        Hg = fi.X[V] if l == 0 else H[l - 1]
+        AHg = region(lay.AH[l], F, lay.ld_AH[l])
+        bounds.append(np.concatenate(
+            [product_bound(Hg, fw["H"][l], fi.W_self[l]),
+             product_bound(AHg, fw["AH"][l], fi.W_neigh[l])], axis=1))
+    masks, _ = checked_masks(fw["Z"], [x > 0 for x in H], bounds, "sampled")
     ref = og.train_step(srp, scl, fi.X[V], params, fi.labels[V], wl.loss, wl.lr,
-                        masks=[h > 0 for h in H])
+                        masks=masks, fw=fw)
     e_loss = abs(loss.item() - ref["loss"]) / abs(ref["loss"])
     e_dw = rel(gWc, ref["grads"]["dW_cls"])
     errs = [rel(w, ref["params"]["W_self"][l]) for l, w in enumerate(Ws)]

@@ -138,6 +138,24 @@ def test_reduction_workloads_bit_exact(name):
     assert info["naux"] > 0
 
 
+@pytest.mark.parametrize("which", ["reddit8k", 1, 7, 63])
+def test_reduction_more_workloads_bit_exact(which):
+    # the heavy-tailed workload (theta 2, 5 rounds, B = 0.5) and three more
+    # subgraphs of the 64-subgraph stream, where the budget binds
+    if which == "reddit8k":
+        wl = synth.WORKLOADS[which]
+        rounds = 5
+    else:
+        wl = synth.stream_workload(which)
+        rounds = wl.rounds
+    inp = synth.make_inputs(wl)
+    rp, cl = gr.subgraph_build(wl.n, inp.src, inp.dst)
+    ora = rd.reduce(rp, cl, theta=wl.theta, max_rounds=rounds, max_aux=wl.max_aux)
+    red = gcn.redundancy_reduce(gcn.subgraph_build(wl.n, inp.src, inp.dst),
+                                theta=wl.theta, max_rounds=rounds, max_aux=wl.max_aux)
+    assert _compare_reduction(red, ora)["naux"] > 0
+
+
 @pytest.mark.slow
 def test_reduction_yelp_bit_exact():
     wl = synth.WORKLOADS["yelp10k"]
@@ -286,3 +304,17 @@ def test_reduction_counter_width_edges(right):
     rp, cl = got["rowptr"], got["col"]
     assert list(cl[rp[0]:rp[1]]) == list(range(2, n)) == list(cl[rp[1]:rp[2]])
     assert np.all(np.diff(rp)[2:] == 1) and np.all(cl[rp[2]:] == n)
+
+
+@pytest.mark.parametrize("theta", [49, 50, 51, 65535, 65536, 100000])
+def test_reduction_large_theta_matches_oracle(theta):
+    # K_{2,50}: (0, 1) is held by 50 lists, so it is taken for theta < 50 and
+    # no pair is taken for theta >= 50, including thresholds beyond the
+    # 16-bit counters' range
+    src = [0] * 50 + [1] * 50
+    dst = list(range(2, 52)) * 2
+    rp, cl = gr.subgraph_build(52, src, dst)
+    ora = rd.reduce(rp, cl, theta=theta, max_rounds=3)
+    red = gcn.redundancy_reduce(gcn.subgraph_build(52, src, dst), theta=theta, max_rounds=3)
+    info = _compare_reduction(red, ora)
+    assert info["naux"] == (1 if theta < 50 else 0)
