@@ -1,20 +1,24 @@
 #!/usr/bin/env python3
 """Benchmark of the subgraph GCN training step on one MI355X.
 
-    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload ppi8k]
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload yelp10k]
 
 A step is one gcn_train_step: forward through every layer (pair sums of the
 redundancy-reduced graph, aggregation, both weight transforms with fused
 ReLU / concatenation), classifier, loss, backward (masked input gradients,
 the transposed aggregation, weight gradients) and the gradient-descent
 update of every weight, on one seeded synthetic subgraph already resident in
-device memory. Default workload: 8,000-vertex Chung-Lu subgraph (power-law
-exponent 2.5, mean degree 15), f_in 50, 512 per branch, 121-way sigmoid BCE,
-aggregation on the graph reduced by 5 rounds of Algorithms 1-3 (threshold 2).
+device memory. Default workload: the largest single-subgraph one, a
+10,000-vertex Chung-Lu subgraph (power-law exponent 2.5, mean degree 20),
+3 layers, f_in 300, 512 per branch, 100-way sigmoid BCE (the Yelp-like
+widths of Table 2), fp32, aggregation on the graph reduced by 5 rounds of
+Algorithms 1-3 (threshold 2, at most n/2 pair sums).
 
 Prints ONE JSON line: steps/s (value), the dominant kernel's roofline
-position measured with HIP events on the launch stream, and the CPU oracle's
-throughput on a bounded sample of the same workload.
+position measured with HIP events on the launch stream, the aggregation's
+position against HBM (compulsory bytes, and the counter-measured bytes when
+recorded for the current sources) and against a read-only streaming probe,
+and the CPU oracle's throughput on a bounded sample of the same workload.
 """
 import argparse
 import json
@@ -36,7 +40,7 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--workload", default="ppi8k")
+    ap.add_argument("--workload", default="yelp10k")
     ap.add_argument("--profile-steps", type=int, default=10)
     ap.add_argument("--seg-len", type=int, default=0,
                     help="list segment length of the device work list (0: library default)")
@@ -62,6 +66,9 @@ def parse():
                     help="skip the extra timing of the narrow-side order")
     ap.add_argument("--no-adam", action="store_true",
                     help="skip the extra timing of the step with the Adam update")
+    ap.add_argument("--no-extra", action="store_true",
+                    help="skip the extra figures (bf16 step of the workload; ppi8k fp32 "
+                         "step, reduced and direct)")
     ap.add_argument("--no-direct", action="store_true",
                     help="skip the direct-aggregation comparison run (counter runs)")
     ap.add_argument("--infer", action="store_true",
@@ -72,7 +79,7 @@ def parse():
     ap.add_argument("--trace-summary", metavar="KERNEL_STATS_CSV",
                     help="no GPU: turn a rocprofv3 --kernel-trace --stats kernel_stats.csv "
                          "of this script into the per-class table under profiles/")
-    ap.add_argument("--traced-args", default="--no-cpu-baseline --no-direct --no-narrow --no-adam",
+    ap.add_argument("--traced-args", default="--no-cpu-baseline --no-direct --no-narrow --no-adam --no-extra",
                     help="with --trace-summary: the arguments the traced run was given")
     ap.add_argument("--bench-line", help="with --trace-summary: the JSON line the traced run "
                                          "printed (event timings shown beside the trace)")
@@ -83,6 +90,9 @@ def parse():
                     help="no GPU: turn two rocprofv3 --pmc counter files (FETCH_SIZE, "
                          "WRITE_SIZE) of a --calib-copy-mib run into the per-launch "
                          "HBM traffic table under profiles/")
+    ap.add_argument("--mfma-summary", metavar="COUNTER_CSV",
+                    help="no GPU: turn one rocprofv3 --pmc pass (MfmaUtil and MFMA, LDS "
+                         "and wait counters) into the per-class table under profiles/")
     return ap.parse_args()
 
 
@@ -190,7 +200,7 @@ def pmc_summary(fetch_csv, write_csv, workload, cmd_args):
                         source_hash=source_hash(c))
     bargs = (f"--workload {workload} --steps {cmd_args['steps']} --warmup {cmd_args['warmup']} "
              f"--profile-steps {cmd_args['profile_steps']} --no-cpu-baseline --no-direct "
-             f"--no-narrow --no-adam "
+             f"--no-narrow --no-adam --no-extra "
              f"--calib-copy-mib {cmd_args['calib_copy_mib']}")
     lines = [
         f"# HBM traffic per launch, {workload} training step",
@@ -239,7 +249,7 @@ def l2_summary(counter_csv, workload, cmd_args):
                 acc[c][r["Counter_Name"]].append(float(r["Counter_Value"]))
     bargs = (f"--workload {workload} --steps {cmd_args['steps']} --warmup {cmd_args['warmup']} "
              f"--profile-steps {cmd_args['profile_steps']} --no-cpu-baseline --no-direct "
-             f"--no-narrow --no-adam")
+             f"--no-narrow --no-adam --no-extra")
     lines = [f"# L2 hit rate per kernel class, {workload} training step", "",
              "One rocprofv3 counter pass over a bench run (run from /tmp with TMPDIR=/tmp; "
              "`$R` is the repository root):", "", "```",
@@ -261,6 +271,65 @@ def l2_summary(counter_csv, workload, cmd_args):
         lines.append(f"| {c} | {n} | {hk:,.0f} | {mk:,.0f} | {rate:.3f} |")
     lines.append("")
     out = os.path.join(ROOT, "profiles", f"{workload}_l2_hit_rate.md")
+    with open(out, "w") as fh:
+        fh.write("\n".join(lines))
+    print(out)
+
+
+MFMA_COUNTERS = ("MfmaUtil SQ_INSTS_VALU_MFMA_MOPS_F32 SQ_INSTS_VALU_MFMA_MOPS_BF16 "
+                 "LdsBankConflict SQ_WAIT_INST_ANY SQ_BUSY_CU_CYCLES")
+
+
+def mfma_summary(counter_csv, workload, cmd_args):
+    """Writes profiles/<workload>[_bf16]_mfma_util.md: per kernel class and
+    launch, the matrix-core utilisation (MfmaUtil: MFMA busy cycles over
+    active cycles of all 1,024 SIMDs, in %), the MFMA operations the
+    counters saw (x512 flops) against the algorithmic flops, LDS bank
+    conflicts and issue waits, from one rocprofv3 pass."""
+    import collections
+    import csv
+    acc = collections.defaultdict(lambda: collections.defaultdict(list))
+    with open(counter_csv) as fh:
+        for r in csv.DictReader(fh):
+            c = kernel_class(r["Kernel_Name"])
+            if c:
+                acc[c][r["Counter_Name"]].append(float(r["Counter_Value"]))
+    bf16 = cmd_args.get("precision") == "bf16"
+    bargs = (f"--workload {workload} --steps {cmd_args['steps']} --warmup {cmd_args['warmup']} "
+             f"--profile-steps {cmd_args['profile_steps']} --no-cpu-baseline --no-direct "
+             f"--no-narrow --no-adam --no-extra" + (" --precision bf16" if bf16 else ""))
+    tag = f"{workload}_bf16" if bf16 else workload
+    lines = [f"# Matrix-core utilisation per kernel class, {tag} training step", "",
+             "One rocprofv3 counter pass over a bench run (run from /tmp with TMPDIR=/tmp; "
+             "`$R` is the repository root):", "", "```",
+             f"rocprofv3 --pmc {MFMA_COUNTERS} --output-format csv -d OUT -o mfma -- "
+             f"python3 $R/bench.py {bargs}",
+             f"python3 bench.py {bargs} --mfma-summary OUT/mfma_counter_collection.csv", "```",
+             "",
+             "MfmaUtil is rocprofv3's derived metric: SQ_VALU_MFMA_BUSY_CYCLES summed over the "
+             "SIMDs over GRBM_GUI_ACTIVE times the 1,024 SIMDs, in %, averaged over the "
+             "class's dispatches. MFMA GFLOP = (MOPS_F32 + MOPS_BF16) x 512 per launch. "
+             "LdsBankConflict: % of active cycles the LDS stalled on bank conflicts. "
+             "SQ_WAIT_INST_ANY and SQ_BUSY_CU_CYCLES are per launch, summed over the "
+             "GPU.", "",
+             "| kernel class | dispatches | MfmaUtil % | MFMA GFLOP / launch | LdsBankConflict % "
+             "| SQ_WAIT_INST_ANY / launch | SQ_BUSY_CU_CYCLES / launch |",
+             "|---|---:|---:|---:|---:|---:|---:|"]
+
+    def mean(d, k):
+        v = d.get(k, [])
+        return sum(v) / len(v) if v else float("nan")
+    rows = []
+    for c, d in acc.items():
+        n = max(len(v) for v in d.values())
+        mops = mean(d, "SQ_INSTS_VALU_MFMA_MOPS_F32") + mean(d, "SQ_INSTS_VALU_MFMA_MOPS_BF16")
+        rows.append((c, n, mean(d, "MfmaUtil"), mops * 512 / 1e9, mean(d, "LdsBankConflict"),
+                     mean(d, "SQ_WAIT_INST_ANY"), mean(d, "SQ_BUSY_CU_CYCLES")))
+    for c, n, u, gf, lds, wait, busy in sorted(rows, key=lambda r: -r[3]):
+        lines.append(f"| {c} | {n} | {u:.1f} | {gf:.3f} | {lds:.2f} | {wait:,.0f} | "
+                     f"{busy:,.0f} |")
+    lines.append("")
+    out = os.path.join(ROOT, "profiles", f"{tag}_mfma_util.md")
     with open(out, "w") as fh:
         fh.write("\n".join(lines))
     print(out)
@@ -309,7 +378,7 @@ def trace_summary(stats_csv, workload, cmd_args, bench_line=None):
                 "The run covers the warm-up, timed and profiled inference calls on the "
                 "reduced graph." if infer and "--no-direct" in cmd_args else
                 "The run covers the warm-up, timed and profiled steps of the reduced-graph "
-                "step alone." if all(f in cmd_args for f in ("--no-direct", "--no-narrow", "--no-adam")) else
+                "step alone." if all(f in cmd_args for f in ("--no-direct", "--no-narrow", "--no-adam", "--no-extra")) else
                 "The run also covers the comparison runs bench.py times beside the step "
                 "(their kernels are counted in the same classes)."), "",
            "## Per timing class (the classes bench.py times with HIP events)", "",
@@ -480,8 +549,7 @@ def roofline(name, k, workload):
 
 def achievable_bandwidth(mib=1024, reps=10):
     """Device-copy bandwidth (read + write bytes per second) of a buffer far
-    larger than the caches, timed with events: the HBM rate a streaming
-    kernel can reach on this GPU."""
+    larger than the caches, timed with events."""
     import torch
     a = torch.ones((mib << 20) // 4, dtype=torch.float32, device="cuda")
     b = torch.empty_like(a)
@@ -497,6 +565,27 @@ def achievable_bandwidth(mib=1024, reps=10):
     return round(gbs, 1)
 
 
+def read_bandwidth(mib=2048, reps=10):
+    """HBM bandwidth of a read-only kernel (gcn_read_probe: every word of a
+    buffer 8x the Infinity Cache read once), timed with events on the stream
+    it is launched on: the denominator for kernels that mostly read."""
+    import torch
+    from paper_2001_02498_amd import gcn
+    a = torch.ones((mib << 20) // 4, dtype=torch.float32, device="cuda")
+    sink = torch.empty(gcn.READ_PROBE_SINK, dtype=torch.float32, device="cuda")
+    gcn.read_probe(a, sink)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        gcn.read_probe(a, sink)
+    e1.record()
+    torch.cuda.synchronize()
+    assert float(sink.sum().item()) == float(a.numel()), "read probe summed wrongly"
+    gbs = a.numel() * 4.0 * reps / (e0.elapsed_time(e1) * 1e-3) / 1e9
+    del a, sink
+    return round(gbs, 1)
+
+
 def aggregation_compulsory(wl, info):
     """Compulsory bytes of one step's list-sum launches: every extended row
     (n + naux of them) read once, every output row written once, the lists
@@ -506,6 +595,33 @@ def aggregation_compulsory(wl, info):
     widths = [wl.f_in] + [2 * wl.h] * (wl.L - 1) + [wl.h] * (wl.L - 1)
     per = [4.0 * F * (n + naux) + 4.0 * F * n + 4.0 * (n + 1 + nnz) for F in widths]
     return sum(per) / len(per)
+
+
+def aggregation_roofline(wl, info, ktab, read_gbs):
+    """The list sums against HBM. achieved = compulsory bytes per launch
+    (every extended row read once, every output written once, the lists
+    read once) over the mean event-timed launch; frac against the 8 TB/s
+    peak, frac_of_achievable against the read-only probe measured in the
+    same process. The algorithmic count, which charges every neighbour-row
+    gather (most served by L2 and the Infinity Cache), is reported beside it
+    as gather_GBs, and the counter-measured bytes (traffic) when recorded
+    for the current sources."""
+    k = ktab["list_sums"]
+    t = k["avg_us"] * 1e-6
+    comp = aggregation_compulsory(wl, info)
+    achieved = comp / t / 1e9
+    traffic = stored_traffic(wl.name, "list_sums")
+    out = dict(kernel="list_sums", bound="hbm", achieved=round(achieved, 1),
+               peak=PEAK_HBM_GBS, unit="GB/s", frac=round(achieved / PEAK_HBM_GBS, 4),
+               bytes="compulsory", compulsory_bytes=round(comp),
+               achievable_read_GBs=read_gbs,
+               frac_of_achievable=None if not read_gbs else round(achieved / read_gbs, 4),
+               traffic=traffic, traffic_unit="bytes/launch",
+               traffic_GBs=None if traffic is None else round(traffic / t / 1e9, 1),
+               gather_bytes=round(k["bytes_per_launch"]),
+               gather_GBs=round(k["bytes_per_launch"] / t / 1e9, 1),
+               avg_us=k["avg_us"])
+    return out
 
 
 def cpu_baseline(wl, inp, budget_s):
@@ -1014,6 +1130,23 @@ def run_infer(args):
         direct = 1e3 * d.timed(args.steps, args.warmup)
         print(f"[bench] direct aggregation: {direct:.3f} ms/call", file=sys.stderr, flush=True)
         del d
+    extra = {}
+    if not args.no_extra:
+        if prec == gcn.PREC_FP32:
+            d = Setup(wl, wl.reduce, inp, args.seg_len, gcn.PREC_BF16, order)
+            extra["bf16_ms_per_step"] = round(1e3 * d.timed(args.steps, args.warmup,
+                                                            args.graph), 4)
+            del d
+        if wl.name != "ppi8k":
+            pw = synth.WORKLOADS["ppi8k"]
+            pin = synth.make_inputs(pw)
+            for key, reduce in (("ppi8k_fp32_ms_per_step", True),
+                                ("ppi8k_fp32_direct_ms_per_step", False)):
+                d = Setup(dataclasses.replace(pw, reduce=reduce), reduce, pin, args.seg_len,
+                          gcn.PREC_FP32, order)
+                extra[key] = round(1e3 * d.timed(args.steps, args.warmup, args.graph), 4)
+                del d
+        print(f"[bench] extra figures: {extra}", file=sys.stderr, flush=True)
     prof = red.profile(args.profile_steps)
     ktab = kernel_table(prof, args.profile_steps)
     dominant = max(ktab, key=lambda k: ktab[k]["ms_per_step"])
@@ -1060,6 +1193,9 @@ def main():
         return
     if args.l2_summary:
         l2_summary(args.l2_summary, args.workload, vars(args))
+        return
+    if args.mfma_summary:
+        mfma_summary(args.mfma_summary, args.workload, vars(args))
         return
     if args.pmc_summary:
         # the counted run's arguments are given again on this command line
@@ -1117,20 +1253,31 @@ def main():
         adam = 1e3 * d.timed(args.steps, args.warmup, args.graph)
         print(f"[bench] Adam update: {adam:.3f} ms/step", file=sys.stderr, flush=True)
         del d
+    extra = {}
+    if not args.no_extra:
+        if prec == gcn.PREC_FP32:
+            d = Setup(wl, wl.reduce, inp, args.seg_len, gcn.PREC_BF16, order)
+            extra["bf16_ms_per_step"] = round(1e3 * d.timed(args.steps, args.warmup,
+                                                            args.graph), 4)
+            del d
+        if wl.name != "ppi8k":
+            pw = synth.WORKLOADS["ppi8k"]
+            pin = synth.make_inputs(pw)
+            for key, reduce in (("ppi8k_fp32_ms_per_step", True),
+                                ("ppi8k_fp32_direct_ms_per_step", False)):
+                d = Setup(dataclasses.replace(pw, reduce=reduce), reduce, pin, args.seg_len,
+                          gcn.PREC_FP32, order)
+                extra[key] = round(1e3 * d.timed(args.steps, args.warmup, args.graph), 4)
+                del d
+        print(f"[bench] extra figures: {extra}", file=sys.stderr, flush=True)
     prof = red.profile(args.profile_steps)
     ktab = kernel_table(prof, args.profile_steps)
     dominant = max(ktab, key=lambda k: ktab[k]["ms_per_step"])
     roof = roofline(dominant, ktab[dominant], wl.name)
-    agg = roofline("list_sums", ktab["list_sums"], wl.name) if "list_sums" in ktab else None
-    # (skipped in counter runs, whose only plain copy is the calibration one)
-    hbm = None if args.calib_copy_mib else achievable_bandwidth()
-    if agg and hbm:
-        comp = aggregation_compulsory(wl, red.info)
-        k = ktab["list_sums"]
-        agg["achievable_GBs"] = hbm
-        agg["frac_of_achievable"] = round(agg["achieved"] / hbm, 4)
-        agg["compulsory_bytes"] = round(comp)
-        agg["compulsory_GBs"] = round(comp / (k["avg_us"] * 1e-6) / 1e9, 1)
+    # (the bandwidth probes are skipped in counter runs, whose only plain
+    # copy is the calibration one)
+    rd_bw = None if args.calib_copy_mib else read_bandwidth()
+    agg = aggregation_roofline(wl, red.info, ktab, rd_bw) if "list_sums" in ktab else None
     print(f"[bench] profiled {args.profile_steps} steps; dominant {dominant}",
           file=sys.stderr, flush=True)
 
@@ -1183,6 +1330,7 @@ def main():
         "adam_ms_per_step": None if adam is None else round(adam, 4),
         "host_preprocess_ms": {k: round(v, 2) for k, v in red.host_ms.items()},
         "aggregation_roofline": agg,
+        "extra": extra,
         "kernels": {k: {kk: vv for kk, vv in v.items()
                         if kk not in ("flops_per_launch", "bytes_per_launch")}
                     for k, v in ktab.items()},

@@ -633,6 +633,20 @@ int gcn_profile_disable(void);
 int gcn_profile_read(gcn_profile_entry* out, int32_t max_entries,
                      int32_t* count, int32_t reset);
 
+/* ---------------------------------------------------- bandwidth probe
+ * gcn_read_probe - measurement helper, not part of the training step: one
+ *   launch on `stream` that reads every 16-byte word of `buf` (device
+ *   memory, 16-byte aligned, `bytes` a positive multiple of 16) once and
+ *   sums it, writing one float per wavefront to `sink` (device memory,
+ *   GCN_READ_PROBE_SINK floats, caller-owned). Timed over a buffer far
+ *   larger than the 256 MB Infinity Cache it gives the HBM bandwidth a
+ *   kernel that only reads can reach: the denominator for the aggregation's
+ *   compulsory bytes. Timed as class "read_probe". GCN_E_INVALID_ARG on bad
+ *   pointers or sizes (nothing launched), GCN_E_HIP if the launch fails.
+ */
+#define GCN_READ_PROBE_SINK 16384
+int gcn_read_probe(const void* buf, size_t bytes, float* sink, gcn_stream_t stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -36,6 +36,8 @@ enum Kind : int {
     K_GEMM_DW_IN_BF16,
     // rows of the full graph's features and labels for a sampled minibatch
     K_GATHER,
+    // streaming read of a buffer larger than the caches (measurement)
+    K_READ_PROBE,
     K_COUNT
 };
 

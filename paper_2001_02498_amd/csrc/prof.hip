@@ -54,6 +54,7 @@ const char* kind_name(int k) {
         case K_GEMM_FWD_IN_BF16: return "gemm_fwd_in_bf16";
         case K_GEMM_DW_IN_BF16: return "gemm_dw_in_bf16";
         case K_GATHER: return "gather_rows";
+        case K_READ_PROBE: return "read_probe";
         default: return "other";
     }
 }
@@ -77,6 +78,33 @@ ProfScope::~ProfScope() {
     if (idx_ < 0) return;
     std::lock_guard<std::mutex> lk(g_mu);
     if (idx_ < (int64_t)g_recs.size()) (void)hipEventRecord(g_recs[idx_].b, s_);
+}
+
+// Read-only streaming kernel: every 16-byte word of the buffer is loaded
+// once, four words in flight per thread, and summed; each wavefront's sum
+// (reduced across lanes, so no load is dead) goes to its own word of the
+// sink. The bandwidth it reaches on a buffer far beyond the 256 MB
+// Infinity Cache is what a kernel that only reads can get from HBM.
+constexpr int kProbeBlocks = 4096, kProbeThreads = 256;
+static_assert(GCN_READ_PROBE_SINK == kProbeBlocks * (kProbeThreads / 64), "sink size");
+
+__global__ __launch_bounds__(kProbeThreads) void read_probe_kernel(const float4* __restrict__ p,
+                                                                   int64_t n4,
+                                                                   float* __restrict__ sink) {
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    float s = 0.f;
+    for (; i + 3 * stride < n4; i += 4 * stride) {
+        const float4 a = p[i], b = p[i + stride], c = p[i + 2 * stride], d = p[i + 3 * stride];
+        s += ((a.x + a.y) + (a.z + a.w)) + ((b.x + b.y) + (b.z + b.w)) +
+             ((c.x + c.y) + (c.z + c.w)) + ((d.x + d.y) + (d.z + d.w));
+    }
+    for (; i < n4; i += stride) {
+        const float4 a = p[i];
+        s += (a.x + a.y) + (a.z + a.w);
+    }
+    for (int o = 32; o > 0; o >>= 1) s += __shfl_xor(s, o, 64);
+    if ((threadIdx.x & 63) == 0) sink[blockIdx.x * (kProbeThreads / 64) + (threadIdx.x >> 6)] = s;
 }
 
 }  // namespace gcn
@@ -163,6 +191,26 @@ int gcn_profile_read(gcn_profile_entry* out, int32_t max_entries, int32_t* count
     if (dropped) {
         set_error("gcn_profile_read: launches went untimed (capacity exhausted)");
         return GCN_E_INTERNAL;
+    }
+    return GCN_OK;
+}
+
+int gcn_read_probe(const void* buf, size_t bytes, float* sink, gcn_stream_t stream) {
+    GCN_CHECK_ARG(buf != nullptr && sink != nullptr, "gcn_read_probe: NULL pointer");
+    GCN_CHECK_ARG(((uintptr_t)buf & 15) == 0 && (bytes & 15) == 0 && bytes > 0,
+                  "gcn_read_probe: buffer must be 16-byte aligned, bytes a positive multiple "
+                  "of 16 (got %zu)", bytes);
+    GCN_CHECK_ARG(((uintptr_t)sink & 3) == 0, "gcn_read_probe: sink not 4-byte aligned");
+    hipStream_t s = (hipStream_t)stream;
+    {
+        ProfScope prof(s, K_READ_PROBE, (double)bytes / 4, (double)bytes);
+        read_probe_kernel<<<dim3(kProbeBlocks), dim3(kProbeThreads), 0, s>>>(
+            (const float4*)buf, (int64_t)(bytes / 16), sink);
+    }
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) {
+        set_error("gcn_read_probe: launch failed (%s)", hipGetErrorString(e));
+        return GCN_E_HIP;
     }
     return GCN_OK;
 }

@@ -171,6 +171,8 @@ class ProfileEntry(C.Structure):
 _prof_enable = _proto("gcn_profile_enable", [_i32])
 _prof_disable = _proto("gcn_profile_disable", [])
 _prof_read = _proto("gcn_profile_read", [C.POINTER(ProfileEntry), _i32, _pi32, _i32])
+_read_probe = _proto("gcn_read_probe", [_vp, _sz, _vp, _vp])
+READ_PROBE_SINK = 16384
 
 class PipelineInfo(C.Structure):
     _fields_ = [("n", _i32), ("naux", _i32), ("rounds", _i32), ("reserved", _i32),
@@ -205,7 +207,7 @@ EXPORTS = [
     "gcn_profile_disable",
     "gcn_profile_read", "gcn_pipeline_create", "gcn_pipeline_submit", "gcn_pipeline_next",
     "gcn_pipeline_release", "gcn_pipeline_destroy", "gcn_pipeline_submit_sample",
-    "gcn_pipeline_create_mixed",
+    "gcn_pipeline_create_mixed", "gcn_read_probe",
 ]
 
 
@@ -562,6 +564,18 @@ def profile_read(reset=True):
                                        min_ms=buf[i].min_ms, max_ms=buf[i].max_ms,
                                        flops=buf[i].flops, bytes=buf[i].bytes)
             for i in range(min(cnt.value, 32))}
+
+
+def read_probe(buf, sink, stream=None):
+    """One streaming read of every byte of the device tensor `buf`
+    (gcn_read_probe); `sink`: device float32 tensor of READ_PROBE_SINK."""
+    torch = _torch()
+    if not (buf.is_cuda and sink.is_cuda and sink.dtype == torch.float32
+            and sink.numel() >= READ_PROBE_SINK and buf.is_contiguous()):
+        raise ValueError("read_probe: contiguous device buffer and a float32 device sink "
+                         f"of {READ_PROBE_SINK} needed")
+    _check(_read_probe(_ptr(buf), buf.numel() * buf.element_size(), _ptr(sink),
+                       _stream(stream)))
 
 
 # ------------------------------------------------------ preparation pipeline
