@@ -118,7 +118,7 @@ def test_trace_summary_totals_per_class(scratch_root):
                         TotalDurationNs=200000, AverageNs=200000))
         w.writerow(dict(Name="__amd_rocclr_copyBuffer", Calls=9, TotalDurationNs=9000,
                         AverageNs=1000))
-    bench.trace_summary(str(path), "wl", "--no-cpu-baseline --no-direct --no-narrow --no-adam")
+    bench.trace_summary(str(path), "wl", "--no-cpu-baseline --no-direct --no-narrow --no-adam --no-extra")
     txt = (scratch_root / "profiles" / "wl_train_step_kernel_stats.md").read_text()
     row = [ln for ln in txt.splitlines() if ln.startswith("| gemm_dw |")][0]
     cells = [c.strip() for c in row.strip("|").split("|")]
