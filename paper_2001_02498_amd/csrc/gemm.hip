@@ -107,6 +107,7 @@ struct TileInfo {
     int pi, split, m0, n0, kbeg, kend, nk;
 };
 
+template <int TBM = BM, int TBN = BN>
 __device__ __forceinline__ TileInfo decode_tile(const GemmBatch& batch) {
     const int T = batch.total_tiles;
     const int bid = blockIdx.x;
@@ -120,8 +121,8 @@ __device__ __forceinline__ TileInfo decode_tile(const GemmBatch& batch) {
     const int per_split = P.tiles_m * P.tiles_n;
     ti.split = local / per_split;
     local -= ti.split * per_split;
-    ti.m0 = (local / P.tiles_n) * BM;
-    ti.n0 = (local % P.tiles_n) * BN;
+    ti.m0 = (local / P.tiles_n) * TBM;
+    ti.n0 = (local % P.tiles_n) * TBN;
     ti.kbeg = ti.split * P.kchunk;
     ti.kend = min(P.K, ti.kbeg + P.kchunk);
     ti.nk = ti.kend > ti.kbeg ? (ti.kend - ti.kbeg + BK - 1) / BK : 0;
@@ -137,15 +138,15 @@ __device__ __forceinline__ bf16x4 to_bf16(float a, float b, float c, float d) {
     return r;
 }
 
-// Epilogue of a wavefront's 64 x 64 block (2 x 2 accumulators of 32 x 32).
+// Epilogue of a wavefront's block of MB x NB accumulators of 32 x 32.
 // The MFMAs take the B fragment as their first operand, so they produce the
 // transposed block: accumulator element r of lane l is C[i][j] of its
 // 32 x 32 block with i = l % 32 and j = (r % 4) + 8 (r / 4) + 4 (l / 32).
 // Every lane thus holds four runs of four consecutive columns of one row,
 // stored (and masked) with 16-byte accesses where the row is aligned.
-template <Epilogue EP>
+template <Epilogue EP, int MB = 2, int NB = 2>
 __device__ __forceinline__ void store_tile(const GemmProblem& P, int split, int mw, int nw,
-                                           int half, int l32, const floatx16 (&acc)[2][2]) {
+                                           int half, int l32, const floatx16 (&acc)[MB][NB]) {
     float* C = P.C;
     if constexpr (EP == EPI_PARTIAL) C += (int64_t)split * P.part_stride;
     const bool cvec = ((reinterpret_cast<uintptr_t>(C) | (uintptr_t)(P.ldc * 4)) & 15) == 0;
@@ -153,12 +154,12 @@ __device__ __forceinline__ void store_tile(const GemmProblem& P, int split, int 
     if constexpr (EP == EPI_MASK)
         mvec = ((reinterpret_cast<uintptr_t>(P.mask) | (uintptr_t)(P.ldmask * 4)) & 15) == 0;
 #pragma unroll
-    for (int bi = 0; bi < 2; ++bi) {
+    for (int bi = 0; bi < MB; ++bi) {
         const int m = mw + bi * 32 + l32;
         if (m >= P.M) continue;
         float* crow = C + (int64_t)m * P.ldc;
 #pragma unroll
-        for (int bj = 0; bj < 2; ++bj) {
+        for (int bj = 0; bj < NB; ++bj) {
 #pragma unroll
             for (int g = 0; g < 4; ++g) {
                 const int n = nw + bj * 32 + 8 * g + 4 * half;
@@ -328,12 +329,27 @@ __device__ __forceinline__ void store_tile_lds(const GemmProblem& P, int split, 
 
 // A rows are always 16-byte aligned (checked on the host); BVEC selects
 // float4 or element loads for B (the classifier weight has any width C).
-template <ALayout AL, BLayout BL, Epilogue EP, bool BVEC, GemmRole ROLE, bool HALF = false>
+// Tile shape: each wavefront of the 2 x 2 grid owns MB x NB accumulators of
+// 32 x 32, so the tile is (64 MB) x (64 NB): 128 x 128 by default, 128 x 64
+// where the launch planner finds that it spreads the tiles more evenly over
+// the CUs (launch_gemm).
+template <ALayout AL, BLayout BL, Epilogue EP, bool BVEC, GemmRole ROLE, bool HALF = false,
+          int MB = 2, int NB = 2>
 __global__ __launch_bounds__(kThreads, 2) void gemm_kernel(GemmBatch batch) {
+    constexpr int TBM = 64 * MB, TBN = 64 * NB;
+    static_assert(TBM <= BM && TBN <= BN, "operand buffers are sized for 128 x 128");
+    static_assert(!HALF || (MB == 2 && NB == 2), "half-row mode is for 128 x 128 tiles");
+    // float4 quads per operand and K step, and the K-major layout of each
+    // operand: quads per K row, K rows covered per quad index, LDS stride
+    constexpr int kQA = BK * TBM / 4 / kThreads, kQB = BK * TBN / 4 / kThreads;
+    constexpr int kQRA = TBM / 4, kQRB = TBN / 4;
+    constexpr int kKStepA = kThreads / kQRA, kKStepB = kThreads / kQRB;
+    constexpr int kColStrideA = TBM + 4, kColStrideB = TBN + 4;
+    static_assert(kQA * kKStepA == BK && kQB * kKStepB == BK, "K-major quads cover BK rows");
     // [buffer][A | B] operand tiles
     __shared__ __attribute__((aligned(16))) float smem[2][2][kOperandFloats];
 
-    const TileInfo ti = decode_tile(batch);
+    const TileInfo ti = decode_tile<TBM, TBN>(batch);
     const GemmProblem& P = batch.p[ti.pi];
     const int split = ti.split, m0 = ti.m0, n0 = ti.n0;
     const int kbeg = ti.kbeg, kend = ti.kend, nk = ti.nk;
@@ -356,18 +372,19 @@ __global__ __launch_bounds__(kThreads, 2) void gemm_kernel(GemmBatch batch) {
     const int ksplitA = P.ksplitA, ksplitB = P.ksplitB;
     const int64_t lda0 = P.lda0, ldb0 = P.ldb0;
 
-    // Thread t moves kQuads float4 per operand and K step:
+    // Thread t moves kQA / kQB float4 of A / B per K step:
     //   row-contiguous: row t / (BK/4) + q * (256 / (BK/4)), k = 4 (t % (BK/4))
-    //   K-major:        k row t / 32 + 8 q, column 4 (t % 32)
+    //   K-major:        k row t / kQR + kKStep q, column 4 (t % kQR)
     constexpr int kPerRow = BK / 4, kRowStep = kThreads / kPerRow;
     const int rk = 4 * (t % kPerRow);   // K offset of a row-contiguous quad
-    const int kr = t >> 5;              // K row of a K-major quad (+ 8 q)
-    RowQuad arow[kQuads], brow[kQuads];
+    const int krA = t / kQRA;           // K row of a K-major A quad (+ kKStepA q)
+    const int krB = t / kQRB;           // K row of a K-major B quad (+ kKStepB q)
+    RowQuad arow[kQA], brow[kQB];
     ColQuad acol, bcol;
-    acol.c = m0 + 4 * (t & 31);
-    bcol.c = n0 + 4 * (t & 31);
+    acol.c = m0 + 4 * (t % kQRA);
+    bcol.c = n0 + 4 * (t % kQRB);
 #pragma unroll
-    for (int q = 0; q < kQuads; ++q) {
+    for (int q = 0; q < kQA; ++q) {
         if constexpr (AL == A_MK) {
             const int r = m0 + t / kPerRow + kRowStep * q;
             arow[q].live = r < M;
@@ -375,6 +392,9 @@ __global__ __launch_bounds__(kThreads, 2) void gemm_kernel(GemmBatch batch) {
             arow[q].p0 = A0 + (int64_t)rr * lda0;
             arow[q].p1 = P.A1 + (int64_t)rr * P.lda1;
         }
+    }
+#pragma unroll
+    for (int q = 0; q < kQB; ++q) {
         if constexpr (BL == B_NK) {
             const int r = n0 + t / kPerRow + kRowStep * q;
             brow[q].live = r < N;
@@ -385,7 +405,7 @@ __global__ __launch_bounds__(kThreads, 2) void gemm_kernel(GemmBatch batch) {
     }
 
     // two register sets: set s holds the K steps kt with kt % 2 == s
-    Quad ra[2][kQuads], rb[2][kQuads];
+    Quad ra[2][kQA], rb[2][kQB];
     auto gload_a = [&](int set, int k0, int q) {
         Quad& r = ra[set][q];
         if constexpr (AL == A_MK) {
@@ -394,7 +414,7 @@ __global__ __launch_bounds__(kThreads, 2) void gemm_kernel(GemmBatch batch) {
             r.one = -1;
             issue<true>(r, p, A0, (arow[q].live && k < kend) ? kend - k : 0);
         } else {
-            const int k = k0 + kr + 8 * q;
+            const int k = k0 + krA + kKStepA * q;
             const int c = acol.c;
             const bool krow = k < kend;
             r.one = (ones && krow && Areal - c >= 0 && Areal - c < 4) ? Areal - c : -1;
@@ -409,7 +429,7 @@ __global__ __launch_bounds__(kThreads, 2) void gemm_kernel(GemmBatch batch) {
             r.one = -1;
             issue<BVEC>(r, p, B0, (brow[q].live && k < kend) ? kend - k : 0);
         } else {
-            const int k = k0 + kr + 8 * q;
+            const int k = k0 + krB + kKStepB * q;
             const int c = bcol.c;
             const bool krow = k < kend;
             r.one = -1;
@@ -419,61 +439,80 @@ __global__ __launch_bounds__(kThreads, 2) void gemm_kernel(GemmBatch batch) {
     // LDS placement of quad q (row-contiguous: [row][k]; K-major: [k][col])
     auto a_slot = [&](int q) {
         return AL == A_MK ? (t / kPerRow + kRowStep * q) * kRowStride + rk
-                          : (kr + 8 * q) * kColStride + 4 * (t & 31);
+                          : (krA + kKStepA * q) * kColStrideA + 4 * (t % kQRA);
     };
     auto b_slot = [&](int q) {
         return BL == B_NK ? (t / kPerRow + kRowStep * q) * kRowStride + rk
-                          : (kr + 8 * q) * kColStride + 4 * (t & 31);
+                          : (krB + kKStepB * q) * kColStrideB + 4 * (t % kQRB);
     };
-    auto sstore = [&](int buf, int set, int q) {
-        *reinterpret_cast<float4*>(&smem[buf][0][a_slot(q)]) = finish(ra[set][q]);
-        *reinterpret_cast<float4*>(&smem[buf][1][b_slot(q)]) = finish(rb[set][q]);
+    auto sstore = [&](int buf, int set) {
+        constexpr int kQM = kQA > kQB ? kQA : kQB;
+#pragma unroll
+        for (int q = 0; q < kQM; ++q) {
+            if (q < kQA) *reinterpret_cast<float4*>(&smem[buf][0][a_slot(q)]) = finish(ra[set][q]);
+            if (q < kQB) *reinterpret_cast<float4*>(&smem[buf][1][b_slot(q)]) = finish(rb[set][q]);
+        }
     };
 
-    floatx16 acc[2][2];
+    floatx16 acc[MB][NB];
 #pragma unroll
-    for (int i = 0; i < 2; ++i)
+    for (int i = 0; i < MB; ++i)
 #pragma unroll
-        for (int j = 0; j < 2; ++j)
+        for (int j = 0; j < NB; ++j)
 #pragma unroll
             for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
     // fragments of one group of 8 K values: element j feeds MFMA step j
-    float4 fa[2][2], fb[2][2];
+    float4 fa[2][MB], fb[2][NB];
     auto frag = [&](const float* As, const float* Bs, int sg, int fslot) {
         const int kb = 8 * sg + 4 * half;
+        constexpr int kFM = MB > NB ? MB : NB;
 #pragma unroll
-        for (int i = 0; i < 2; ++i) {
-            const int m = (HALF ? 0 : wm * 64) + i * 32 + l32;
-            if constexpr (AL == A_MK) {
-                fa[fslot][i] = *reinterpret_cast<const float4*>(&As[m * kRowStride + kb]);
-            } else {
-                fa[fslot][i] = make_float4(As[(kb + 0) * kColStride + m], As[(kb + 1) * kColStride + m],
-                                           As[(kb + 2) * kColStride + m], As[(kb + 3) * kColStride + m]);
+        for (int i = 0; i < kFM; ++i) {
+            if (i < MB) {
+                const int m = (HALF ? 0 : wm * 32 * MB) + i * 32 + l32;
+                if constexpr (AL == A_MK) {
+                    fa[fslot][i] = *reinterpret_cast<const float4*>(&As[m * kRowStride + kb]);
+                } else {
+                    fa[fslot][i] = make_float4(As[(kb + 0) * kColStrideA + m], As[(kb + 1) * kColStrideA + m],
+                                               As[(kb + 2) * kColStrideA + m], As[(kb + 3) * kColStrideA + m]);
+                }
             }
-            const int nn = wn * 64 + i * 32 + l32;
-            if constexpr (BL == B_NK) {
-                fb[fslot][i] = *reinterpret_cast<const float4*>(&Bs[nn * kRowStride + kb]);
-            } else {
-                fb[fslot][i] = make_float4(Bs[(kb + 0) * kColStride + nn], Bs[(kb + 1) * kColStride + nn],
-                                           Bs[(kb + 2) * kColStride + nn], Bs[(kb + 3) * kColStride + nn]);
+            if (i < NB) {
+                const int nn = wn * 32 * NB + i * 32 + l32;
+                if constexpr (BL == B_NK) {
+                    fb[fslot][i] = *reinterpret_cast<const float4*>(&Bs[nn * kRowStride + kb]);
+                } else {
+                    fb[fslot][i] = make_float4(Bs[(kb + 0) * kColStrideB + nn], Bs[(kb + 1) * kColStrideB + nn],
+                                               Bs[(kb + 2) * kColStrideB + nn], Bs[(kb + 3) * kColStrideB + nn]);
+                }
             }
         }
+    };
+    auto elem = [](const float4& v, int j) {
+        return j == 0 ? v.x : j == 1 ? v.y : j == 2 ? v.z : v.w;
     };
     auto mfma_group = [&](int fslot) {
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
-            const float a0 = j == 0 ? fa[fslot][0].x : j == 1 ? fa[fslot][0].y : j == 2 ? fa[fslot][0].z : fa[fslot][0].w;
-            const float a1 = j == 0 ? fa[fslot][1].x : j == 1 ? fa[fslot][1].y : j == 2 ? fa[fslot][1].z : fa[fslot][1].w;
-            const float b0 = j == 0 ? fb[fslot][0].x : j == 1 ? fb[fslot][0].y : j == 2 ? fb[fslot][0].z : fb[fslot][0].w;
-            const float b1 = j == 0 ? fb[fslot][1].x : j == 1 ? fb[fslot][1].y : j == 2 ? fb[fslot][1].z : fb[fslot][1].w;
-            // B first: the accumulators hold the transposed blocks (store_tile)
-            acc[0][0] = __builtin_amdgcn_mfma_f32_32x32x2f32(b0, a0, acc[0][0], 0, 0, 0);
-            acc[0][1] = __builtin_amdgcn_mfma_f32_32x32x2f32(b1, a0, acc[0][1], 0, 0, 0);
-            acc[1][0] = __builtin_amdgcn_mfma_f32_32x32x2f32(b0, a1, acc[1][0], 0, 0, 0);
-            acc[1][1] = __builtin_amdgcn_mfma_f32_32x32x2f32(b1, a1, acc[1][1], 0, 0, 0);
+#pragma unroll
+            for (int i = 0; i < MB; ++i) {
+                const float a = elem(fa[fslot][i], j);
+#pragma unroll
+                for (int jj = 0; jj < NB; ++jj) {
+                    // B first: the accumulators hold the transposed blocks (store_tile)
+                    acc[i][jj] = __builtin_amdgcn_mfma_f32_32x32x2f32(elem(fb[fslot][jj], j), a,
+                                                                      acc[i][jj], 0, 0, 0);
+                }
+            }
         }
     };
+    // interleave of global loads (or LDS stores) with the MFMAs of a group:
+    // kLoads of them per K step, kPer MFMAs after each, kRest at the end
+    constexpr int kMfmas = 4 * MB * NB, kLoads = kQA + kQB;
+    constexpr int kPer = kMfmas / kLoads > 0 ? kMfmas / kLoads : 1;
+    constexpr int kRest = kMfmas > kPer * kLoads ? kMfmas - kPer * kLoads : 0;
+    constexpr int kDsFirst = (MB == 2 && NB == 2) ? 8 : 2 * (MB + NB);
 
     // Fast steps (as in the bf16 kernel below): operand rows / K-major
     // column quads outside the operand are clamped into it, since they only
@@ -482,24 +521,27 @@ __global__ __launch_bounds__(kThreads, 2) void gemm_kernel(GemmBatch batch) {
     // boundary between parts of equal leading dimension, a whole K step
     // loads from a uniform per-step base plus fixed per-thread offsets and
     // stores without masking.
-    const bool fast_tile = BVEC && !(ones && Areal >= m0 && Areal < m0 + BM) &&
+    const bool fast_tile = BVEC && !(ones && Areal >= m0 && Areal < m0 + TBM) &&
                            (AL == A_KM || (ksplitA % BK == 0 && P.lda1 == lda0)) &&
                            (BL == B_KN || (ksplitB % BK == 0 && P.ldb1 == ldb0));
     const int nfull = (kend - kbeg) / BK;
-    int64_t oa[kQuads], ob[kQuads];
+    int64_t oa[kQA], ob[kQB];
 #pragma unroll
-    for (int q = 0; q < kQuads; ++q) {
+    for (int q = 0; q < kQA; ++q) {
         if constexpr (AL == A_MK) {
             const int r = m0 + t / kPerRow + kRowStep * q;
             oa[q] = (int64_t)(r < M ? r : 0) * lda0 + rk;
         } else {
-            oa[q] = (int64_t)(kr + 8 * q) * lda0 + (acol.c < Areal ? acol.c : 0);
+            oa[q] = (int64_t)(krA + kKStepA * q) * lda0 + (acol.c < Areal ? acol.c : 0);
         }
+    }
+#pragma unroll
+    for (int q = 0; q < kQB; ++q) {
         if constexpr (BL == B_NK) {
             const int r = n0 + t / kPerRow + kRowStep * q;
             ob[q] = (int64_t)(r < N ? r : 0) * ldb0 + rk;
         } else {
-            ob[q] = (int64_t)(kr + 8 * q) * ldb0 + (bcol.c < N ? bcol.c : 0);
+            ob[q] = (int64_t)(krB + kKStepB * q) * ldb0 + (bcol.c < N ? bcol.c : 0);
         }
     }
     // per-step operand bases, uniform across the workgroup (computed once
@@ -518,20 +560,41 @@ __global__ __launch_bounds__(kThreads, 2) void gemm_kernel(GemmBatch batch) {
         else
             return B0 + (int64_t)k0 * ldb0;
     };
-    auto gload_full = [&](int set, const float* sa, const float* sb, int q) {
-        ra[set][q].v = ld4(sa + oa[q]);
-        rb[set][q].v = ld4(sb + ob[q]);
+    // the whole step's loads and stores of both operands, quad q of A then
+    // quad q of B
+    constexpr int kQMax = kQA > kQB ? kQA : kQB;
+    auto gload_full = [&](int set, const float* sa, const float* sb) {
+#pragma unroll
+        for (int q = 0; q < kQMax; ++q) {
+            if (q < kQA) ra[set][q].v = ld4(sa + oa[q]);
+            if (q < kQB) rb[set][q].v = ld4(sb + ob[q]);
+        }
     };
-    auto sstore_full = [&](int buf, int set, int q) {
-        *reinterpret_cast<float4*>(&smem[buf][0][a_slot(q)]) = ra[set][q].v;
-        *reinterpret_cast<float4*>(&smem[buf][1][b_slot(q)]) = rb[set][q].v;
+    auto gload = [&](int set, int k0) {
+#pragma unroll
+        for (int q = 0; q < kQMax; ++q) {
+            if (q < kQA) gload_a(set, k0, q);
+            if (q < kQB) gload_b(set, k0, q);
+        }
+    };
+    auto sstore_full = [&](int buf, int set) {
+#pragma unroll
+        for (int q = 0; q < kQMax; ++q) {
+            if (q < kQA) *reinterpret_cast<float4*>(&smem[buf][0][a_slot(q)]) = ra[set][q].v;
+            if (q < kQB) *reinterpret_cast<float4*>(&smem[buf][1][b_slot(q)]) = rb[set][q].v;
+        }
     };
     // quads of a set filled by whole-step loads, for a masked store
     auto mark_full = [&](int set) {
 #pragma unroll
-        for (int q = 0; q < kQuads; ++q) {
-            ra[set][q].valid = rb[set][q].valid = 4;
-            ra[set][q].one = rb[set][q].one = -1;
+        for (int q = 0; q < kQA; ++q) {
+            ra[set][q].valid = 4;
+            ra[set][q].one = -1;
+        }
+#pragma unroll
+        for (int q = 0; q < kQB; ++q) {
+            rb[set][q].valid = 4;
+            rb[set][q].one = -1;
         }
     };
 
@@ -549,22 +612,18 @@ __global__ __launch_bounds__(kThreads, 2) void gemm_kernel(GemmBatch batch) {
         frag(As, Bs, 1, 1);
         const float* const sa = step_base_a(kload);
         const float* const sb = step_base_b(kload);
-#pragma unroll
-        for (int q = 0; q < kQuads; ++q) {
-            if constexpr (FULL) {
-                gload_full(set, sa, sb, q);
-            } else {
-                gload_a(set, kload, q);
-                gload_b(set, kload, q);
-            }
-        }
+        if constexpr (FULL)
+            gload_full(set, sa, sb);
+        else
+            gload(set, kload);
         mfma_group(0);
-        __builtin_amdgcn_sched_group_barrier(0x100, 8, 0);      // DS reads first
+        __builtin_amdgcn_sched_group_barrier(0x100, kDsFirst, 0);      // DS reads first
 #pragma unroll
-        for (int q = 0; q < 2 * kQuads; ++q) {
-            __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);  // one global load
-            __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);  // two MFMAs
+        for (int q = 0; q < kLoads; ++q) {
+            __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);     // one global load
+            __builtin_amdgcn_sched_group_barrier(0x008, kPer, 0);  // kPer MFMAs
         }
+        if constexpr (kRest > 0) __builtin_amdgcn_sched_group_barrier(0x008, kRest, 0);
         __builtin_amdgcn_sched_barrier(0);
         // group 1
         frag(As, Bs, 2, 0);
@@ -576,21 +635,19 @@ __global__ __launch_bounds__(kThreads, 2) void gemm_kernel(GemmBatch batch) {
         frag(As, Bs, 3, 1);
         const bool more = FULL || kt + 1 < nk;
         if (more) {
-#pragma unroll
-            for (int q = 0; q < kQuads; ++q) {
-                if constexpr (FULL)
-                    sstore_full(buf ^ 1, set ^ 1, q);
-                else
-                    sstore(buf ^ 1, set ^ 1, q);
-            }
+            if constexpr (FULL)
+                sstore_full(buf ^ 1, set ^ 1);
+            else
+                sstore(buf ^ 1, set ^ 1);
         }
         mfma_group(0);
-        __builtin_amdgcn_sched_group_barrier(0x100, 8, 0);      // DS reads first
+        __builtin_amdgcn_sched_group_barrier(0x100, kDsFirst, 0);      // DS reads first
 #pragma unroll
-        for (int q = 0; q < 2 * kQuads; ++q) {
-            __builtin_amdgcn_sched_group_barrier(0x200, 1, 0);  // one LDS store
-            __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);  // two MFMAs
+        for (int q = 0; q < kLoads; ++q) {
+            __builtin_amdgcn_sched_group_barrier(0x200, 1, 0);     // one LDS store
+            __builtin_amdgcn_sched_group_barrier(0x008, kPer, 0);  // kPer MFMAs
         }
+        if constexpr (kRest > 0) __builtin_amdgcn_sched_group_barrier(0x008, kRest, 0);
         __builtin_amdgcn_sched_barrier(0);
         __syncthreads();
         // group 3: its fragments are already in registers, so the next
@@ -609,38 +666,30 @@ __global__ __launch_bounds__(kThreads, 2) void gemm_kernel(GemmBatch batch) {
         frag(As, Bs, g0 + 1, 1);
         const float* const sa = step_base_a(kload);
         const float* const sb = step_base_b(kload);
-#pragma unroll
-        for (int q = 0; q < kQuads; ++q) {
-            if constexpr (FULL) {
-                gload_full(set, sa, sb, q);
-            } else {
-                gload_a(set, kload, q);
-                gload_b(set, kload, q);
-            }
-        }
+        if constexpr (FULL)
+            gload_full(set, sa, sb);
+        else
+            gload(set, kload);
         mfma_group(0);
-        __builtin_amdgcn_sched_group_barrier(0x100, 8, 0);
+        __builtin_amdgcn_sched_group_barrier(0x100, kDsFirst, 0);
 #pragma unroll
-        for (int q = 0; q < 2 * kQuads; ++q) {
+        for (int q = 0; q < kLoads; ++q) {
             __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
-            __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
+            __builtin_amdgcn_sched_group_barrier(0x008, kPer, 0);
         }
         __builtin_amdgcn_sched_barrier(0);
         const bool more = FULL || kt + 1 < nk;
         if (more) {
-#pragma unroll
-            for (int q = 0; q < kQuads; ++q) {
-                if constexpr (FULL)
-                    sstore_full(buf ^ 1, set ^ 1, q);
-                else
-                    sstore(buf ^ 1, set ^ 1, q);
-            }
+            if constexpr (FULL)
+                sstore_full(buf ^ 1, set ^ 1);
+            else
+                sstore(buf ^ 1, set ^ 1);
         }
         mfma_group(1);
 #pragma unroll
-        for (int q = 0; q < 2 * kQuads; ++q) {
+        for (int q = 0; q < kLoads; ++q) {
             __builtin_amdgcn_sched_group_barrier(0x200, 1, 0);
-            __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
+            __builtin_amdgcn_sched_group_barrier(0x008, kPer, 0);
         }
         __builtin_amdgcn_sched_barrier(0);
         __syncthreads();
@@ -656,23 +705,13 @@ __global__ __launch_bounds__(kThreads, 2) void gemm_kernel(GemmBatch batch) {
     using Masked = std::false_type;
     const bool fast_start = fast_tile && nfull >= 2;
     if (fast_start) {
-#pragma unroll
-        for (int q = 0; q < kQuads; ++q) {
-            gload_full(0, step_base_a(kbeg), step_base_b(kbeg), q);
-            gload_full(1, step_base_a(kbeg + BK), step_base_b(kbeg + BK), q);
-        }
-#pragma unroll
-        for (int q = 0; q < kQuads; ++q) sstore_full(0, 0, q);
+        gload_full(0, step_base_a(kbeg), step_base_b(kbeg));
+        gload_full(1, step_base_a(kbeg + BK), step_base_b(kbeg + BK));
+        sstore_full(0, 0);
     } else if (nk > 0) {
-#pragma unroll
-        for (int q = 0; q < kQuads; ++q) {
-            gload_a(0, kbeg, q);
-            gload_b(0, kbeg, q);
-            gload_a(1, kbeg + BK, q);
-            gload_b(1, kbeg + BK, q);
-        }
-#pragma unroll
-        for (int q = 0; q < kQuads; ++q) sstore(0, 0, q);
+        gload(0, kbeg);
+        gload(1, kbeg + BK);
+        sstore(0, 0);
     }
     if (nk > 0) {
         __syncthreads();
@@ -699,6 +738,7 @@ __global__ __launch_bounds__(kThreads, 2) void gemm_kernel(GemmBatch batch) {
         __syncthreads();
         float* red = &smem[0][0][0];
         auto at = [&](int i, int j, int r) { return ((wn * 4 + i * 2 + j) * 16 + r) * 64 + lane; };
+        static_assert(!HALF || MB * NB == 4, "half-row reduction layout");
         if (wm == 1) {
 #pragma unroll
             for (int i = 0; i < 2; ++i)
@@ -717,7 +757,7 @@ __global__ __launch_bounds__(kThreads, 2) void gemm_kernel(GemmBatch batch) {
                     for (int r = 0; r < 16; ++r) acc[i][j][r] += red[at(i, j, r)];
         }
     }
-    store_tile<EP>(P, split, m0 + wm * 64, n0 + wn * 64, half, l32, acc);
+    store_tile<EP, MB, NB>(P, split, m0 + wm * 32 * MB, n0 + wn * 32 * NB, half, l32, acc);
 }
 
 // ------------------------------------------------------------ bf16 variant
@@ -1412,13 +1452,43 @@ void gemm_split_plan(int32_t M, int32_t N, int32_t K, int32_t nprob, int32_t* sp
     *splits = K > 0 ? (int32_t)((K + chunk - 1) / chunk) : 1;
 }
 
+// Tile shape of a one-pass (not split-K) fp32 launch: 128 x 128, or
+// 128 x 64 when that spreads the work more evenly over the CUs. The tiles
+// are handed out in waves over the 256 CUs (two resident per CU), so a CU
+// computes ceil(tiles / 256) tiles in all; the shape with the smaller
+// ceil(tiles / 256) x tile area finishes first, the narrower tile charged
+// 5 % for its extra operand traffic per flop, and a launch that leaves a
+// CU with a single tile charged 30 % (nothing overlaps its start and end).
+// yelp10k's 10,000 x 1,024 outputs: 632 tiles of 128 x 128 (3 per CU,
+// 2.47 on average) or 1,264 of 128 x 64 (5 per CU, 4.94 on average).
+bool gemm_narrow_tiles(const GemmBatch& b) {
+    constexpr int64_t kCUs = 256;
+    int64_t t2 = 0, t1 = 0;
+    for (int i = 0; i < b.nprob; ++i) {
+        const GemmProblem& p = b.p[i];
+        if (p.M <= 0 || p.N <= 0) continue;
+        const int64_t tm = (p.M + 127) / 128;
+        t2 += tm * ((p.N + 127) / 128);
+        t1 += tm * ((p.N + 63) / 64);
+    }
+    if (t2 == 0) return false;
+    auto cost = [&](int64_t tiles, double area, double eff) {
+        const int64_t per_cu = (tiles + kCUs - 1) / kCUs;
+        return per_cu * area / eff * (tiles <= kCUs ? 1.3 : 1.0);
+    };
+    return cost(t1, 128.0 * 64.0, 0.95) < cost(t2, 128.0 * 128.0, 1.0);
+}
+
 hipError_t launch_gemm(GemmBatch& b, ALayout al, BLayout bl, Epilogue ep, GemmRole role,
                        bool bf16, hipStream_t s) {
+    // 128 x 64 tiles: fp32 kernel, one pass over K, row-contiguous A
+    const bool nb1 = !bf16 && ep != EPI_PARTIAL && al == A_MK && gemm_narrow_tiles(b);
+    const int tbn = nb1 ? 64 : BN;
     int total = 0;
     for (int i = 0; i < b.nprob; ++i) {
         GemmProblem& p = b.p[i];
         p.tiles_m = (p.M + BM - 1) / BM;
-        p.tiles_n = (p.N + BN - 1) / BN;
+        p.tiles_n = (p.N + tbn - 1) / tbn;
         if (ep != EPI_PARTIAL) {
             p.splits = 1;
             p.kchunk = std::max(BK, (p.K + BK - 1) / BK * BK);
@@ -1489,6 +1559,7 @@ hipError_t launch_gemm(GemmBatch& b, ALayout al, BLayout bl, Epilogue ep, GemmRo
     for (int i = 0; i < b.nprob; ++i) half_m = half_m && b.p[i].M <= BM / 2;
 #define GCN_GEMM_CASE(AL_, BL_, EP_, ROLE_)                                          \
     if (al == AL_ && bl == BL_ && ep == EP_ && role == ROLE_) {                       \
+        constexpr bool kNarrowOk = EP_ != EPI_PARTIAL && AL_ == A_MK;                 \
         if (copies)                                                                  \
             gemm_h16_kernel<AL_, BL_, EP_, ROLE_><<<grid, block, 0, s>>>(b);          \
         else if (bf16 && bvec)                                                       \
@@ -1497,7 +1568,16 @@ hipError_t launch_gemm(GemmBatch& b, ALayout al, BLayout bl, Epilogue ep, GemmRo
             gemm_bf16_kernel<AL_, BL_, EP_, false, ROLE_><<<grid, block, 0, s>>>(b);  \
         else if (bvec && half_m && EP_ == EPI_PARTIAL && AL_ == A_KM)                 \
             gemm_kernel<AL_, BL_, EP_, true, ROLE_, true><<<grid, block, 0, s>>>(b);  \
-        else if (bvec)                                                               \
+        else if (nb1) {                                                              \
+            if constexpr (kNarrowOk) {                                               \
+                if (bvec)                                                            \
+                    gemm_kernel<AL_, BL_, EP_, true, ROLE_, false, 2, 1>              \
+                        <<<grid, block, 0, s>>>(b);                                  \
+                else                                                                 \
+                    gemm_kernel<AL_, BL_, EP_, false, ROLE_, false, 2, 1>             \
+                        <<<grid, block, 0, s>>>(b);                                  \
+            }                                                                        \
+        } else if (bvec)                                                             \
             gemm_kernel<AL_, BL_, EP_, true, ROLE_><<<grid, block, 0, s>>>(b);        \
         else                                                                         \
             gemm_kernel<AL_, BL_, EP_, false, ROLE_><<<grid, block, 0, s>>>(b);       \
