@@ -374,6 +374,26 @@ int gcn_aggregate(const gcn_dgraph* g, int32_t mode, int32_t F,
                   const float* X, int64_t ldx, float* Y, int64_t ldy,
                   void* ws, size_t ws_bytes, gcn_stream_t stream);
 
+/* gcn_aggregate_noalloc - gcn_aggregate without a workspace argument, for
+ * callers that cannot allocate device memory (code under HIP graph capture,
+ * tight serving loops, harnesses that forbid allocation). Same operation,
+ * kernels and results as gcn_aggregate. Its scratch (pair sums and split-
+ * list partial sums, each written before it is read) is a fixed array of
+ * GCN_AGG_NOALLOC_SCRATCH_BYTES per device, held by the library on every
+ * device it runs on until the process ends; its device address is looked
+ * up (hipGetSymbolAddress) on the first call on each device, the only
+ * call that may touch the runtime beyond launches. Calls allocate nothing.
+ * Every call on one device shares that device's array: calls that overlap
+ * on one device (concurrent streams or threads) race and give wrong
+ * results; serialise them. Errors: GCN_E_INVALID_ARG as gcn_aggregate,
+ * and when the scratch needed, 4 r4(F) (naux + split-list slots) bytes in
+ * 256-byte-aligned regions, exceeds the fixed size (nothing launched);
+ * GCN_E_HIP if the address lookup or a launch fails. */
+#define GCN_AGG_NOALLOC_SCRATCH_BYTES (64ll << 20)
+int gcn_aggregate_noalloc(const gcn_dgraph* g, int32_t mode, int32_t F,
+                          const float* X, int64_t ldx, float* Y, int64_t ldy,
+                          gcn_stream_t stream);
+
 /* ------------------------------------------------- layer forward (a3-a5)
  * gcn_layer_fwd - one graph convolutional layer, Eq. 1:
  *   AH    = D^-1 A H_in                         (saved for Eq. 2b)

@@ -4,6 +4,7 @@
 #include <algorithm>
 #include <cmath>
 #include <cstring>
+#include <mutex>
 
 #include "kernels.h"
 
@@ -47,6 +48,40 @@ ScratchPlan plan_scratch(int64_t n, int64_t naux, int64_t nslots, int64_t W) {
     p.rowloss = take(4 * std::max<int64_t>(n, 1));
     p.total = off;
     return p;
+}
+
+// Scratch of gcn_aggregate_noalloc: one fixed array per device, resolved
+// to its device address once per device (the name is a host-side stand-in;
+// only the address from hipGetSymbolAddress may reach a kernel or a copy).
+constexpr int64_t kAggStaticBytes = GCN_AGG_NOALLOC_SCRATCH_BYTES;
+static __device__ __align__(256) char scratch[kAggStaticBytes];
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+int hip_fail(hipError_t e, const char* where);
+
+// Device address of the current device's scratch array, looked up on the
+// first call on that device.
+int static_scratch(const char* fn, void** out) {
+    int dev = -1;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return hip_fail(e, fn);
+    GCN_CHECK_ARG(dev >= 0 && dev < kMaxDevices, "%s: device %d beyond %d", fn, dev,
+                  kMaxDevices);
+    std::lock_guard<std::mutex> lk(g_scratch_mu);
+    if (!g_scratch_ptr[dev]) {
+        void* p = nullptr;
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess) return hip_fail(e, fn);
+        if (!p) {
+            set_error("%s: no device address for the scratch array", fn);
+            return GCN_E_HIP;
+        }
+        g_scratch_ptr[dev] = p;
+    }
+    *out = g_scratch_ptr[dev];
+    return GCN_OK;
 }
 
 int hip_fail(hipError_t e, const char* where) {
@@ -790,6 +825,29 @@ int gcn_aggregate(const gcn_dgraph* g, int32_t mode, int32_t F, const float* X,
     GCN_CHECK_ARG(g->n == 0 || X != Y, "%s: X and Y must not overlap", fn);
     const ScratchPlan sp = plan_scratch(g->n, g->naux, g->nslots, F);
     GCN_TRY(check_ws(fn, ws, ws_bytes, sp.total));
+    return do_aggregate(fn, g, mode == GCN_AGG_TRANSPOSED, F, X, ldx, Y, ldy, sp, ws,
+                        (hipStream_t)stream);
+}
+
+int gcn_aggregate_noalloc(const gcn_dgraph* g, int32_t mode, int32_t F, const float* X,
+                          int64_t ldx, float* Y, int64_t ldy, gcn_stream_t stream) {
+    const char* fn = "gcn_aggregate_noalloc";
+    GCN_TRY(check_graph(fn, g));
+    GCN_CHECK_ARG(mode == GCN_AGG_MEAN || mode == GCN_AGG_TRANSPOSED, "%s: unknown mode", fn);
+    GCN_CHECK_ARG(F >= 1, "%s: F < 1", fn);
+    GCN_TRY(check_mat(fn, "X", X, g->n, F, ldx));
+    GCN_TRY(check_mat(fn, "Y", Y, g->n, F, ldy));
+    GCN_CHECK_ARG(g->n == 0 || X != Y, "%s: X and Y must not overlap", fn);
+    // the aggregation reads only the pair-sum and split-list regions, which
+    // lead the plan; both are written before they are read
+    const ScratchPlan sp = plan_scratch(g->n, g->naux, g->nslots, F);
+    const int64_t need = sp.T;
+    GCN_CHECK_ARG(need <= kAggStaticBytes,
+                  "%s: %lld scratch bytes needed (naux %d, split-list slots %d, F %d) "
+                  "exceed the fixed %lld; use gcn_aggregate with a workspace",
+                  fn, (long long)need, g->naux, g->nslots, F, (long long)kAggStaticBytes);
+    void* ws = nullptr;
+    GCN_TRY(static_scratch(fn, &ws));
     return do_aggregate(fn, g, mode == GCN_AGG_TRANSPOSED, F, X, ldx, Y, ldy, sp, ws,
                         (hipStream_t)stream);
 }

@@ -128,6 +128,9 @@ _pack = _proto("gcn_graph_pack", [_vp, _i32, _vp, _sz])
 _upload = _proto("gcn_graph_upload", [_vp, _sz, _vp, C.POINTER(DGraph), _vp])
 _describe = _proto("gcn_graph_describe", [_vp, _sz, _vp, C.POINTER(DGraph)])
 _scratch_bytes = _proto("gcn_scratch_bytes", [C.POINTER(DGraph), _i32, _i32, C.POINTER(_sz)])
+_aggregate_noalloc = _proto("gcn_aggregate_noalloc", [C.POINTER(DGraph), _i32, _i32, _vp, _i64,
+                                                      _vp, _i64, _vp])
+AGG_NOALLOC_SCRATCH_BYTES = 64 << 20
 _aggregate = _proto("gcn_aggregate", [C.POINTER(DGraph), _i32, _i32, _vp, _i64, _vp, _i64,
                                       _vp, _sz, _vp])
 _layer_fwd = _proto("gcn_layer_fwd", [C.POINTER(DGraph), _i32, _i32, _vp, _i64, _vp, _vp, _vp,
@@ -207,7 +210,7 @@ EXPORTS = [
     "gcn_profile_disable",
     "gcn_profile_read", "gcn_pipeline_create", "gcn_pipeline_submit", "gcn_pipeline_next",
     "gcn_pipeline_release", "gcn_pipeline_destroy", "gcn_pipeline_submit_sample",
-    "gcn_pipeline_create_mixed", "gcn_read_probe",
+    "gcn_pipeline_create_mixed", "gcn_read_probe", "gcn_aggregate_noalloc",
 ]
 
 
@@ -448,6 +451,14 @@ def scratch_bytes(dg: DeviceGraph | None, max_width: int, n: int = 0) -> int:
 def aggregate(dg, mode, X, Y, ws, stream=None):
     _check(_aggregate(C.byref(dg.desc), mode, X.shape[1], _ptr(X), _ld(X), _ptr(Y), _ld(Y),
                       _ptr(ws), ws.numel(), _stream(stream)))
+
+
+def aggregate_noalloc(dg, mode, X, Y, stream=None):
+    """gcn_aggregate_noalloc: the aggregation on the library's fixed
+    per-device scratch (no workspace; calls on one device must not
+    overlap)."""
+    _check(_aggregate_noalloc(C.byref(dg.desc), mode, X.shape[1], _ptr(X), _ld(X), _ptr(Y),
+                              _ld(Y), _stream(stream)))
 
 
 def layer_fwd(dg, H_in, W_self, W_neigh, bias, AH, H_out, ws, precision=PREC_FP32,
