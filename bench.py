@@ -725,7 +725,11 @@ def run_stream(args):
     gcn.profile_disable()
     print(f"[bench] device only: {gpu_ms:.3f} ms/step", file=sys.stderr, flush=True)
 
-    # Phase B: the overlapped schedule
+    # Phase B: the overlapped schedule (GPU-reducing workers get a device
+    # workspace share each, sized up front for the largest subgraph)
+    dev_share = gcn.device_reduce_bytes(
+        [gcn.subgraph_build(wl.n, inp.src, inp.dst) for inp in inps], 1, theta=wl.theta,
+        max_rounds=wl.rounds, max_aux=wl.max_aux)
     slots = [gcn.alloc_ws(img_bytes) for _ in range(2)]
     copy = torch.cuda.Stream()
     comp = torch.cuda.current_stream()
@@ -735,10 +739,12 @@ def run_stream(args):
         held = collections.deque()
         infos = []
         nw = workers + (device_workers or 0)
+        ndev = device_workers or (workers if device_reduce else 0)
+        dws = gcn.alloc_ws(ndev * dev_share) if ndev else None
         pipe = gcn.Pipeline(theta=wl.theta, max_rounds=wl.rounds, max_aux=wl.max_aux,
                             seg_len=args.seg_len, workers=workers, depth=2 * nw + 2,
                             pinned=True, num_threads=1, device_reduce=device_reduce,
-                            device_workers=device_workers)
+                            device_workers=device_workers, device_ws=dws)
         torch.cuda.synchronize()
         t0 = time.perf_counter()
         for inp in inps:
@@ -903,12 +909,23 @@ def run_sampled(args):
     seeds = [wl.sample_seed(i) for i in range(K)]
     workers = args.workers or min(16, os.cpu_count() or 1)
 
+    dev_share = []   # the GPU-reducing workers' workspace share, once known
+
     def new_pipe(nw, device_reduce, device_workers=None):
         tot = nw + (device_workers or 0)
+        ndev = device_workers or (nw if device_reduce else 0)
+        if ndev and not dev_share:
+            # sized up front from the minibatches' own walks, taken on the host
+            gs = [gcn.subgraph_induce(full, gcn.sample_frontier(full, wl.m, wl.budget, sd,
+                                                                 wl.max_steps)[0])
+                  for sd in seeds]
+            dev_share.append(gcn.device_reduce_bytes(gs, 1, theta=wl.theta,
+                                                     max_rounds=wl.rounds, max_aux=wl.max_aux))
+        dws = gcn.alloc_ws(ndev * dev_share[0]) if ndev else None
         return gcn.Pipeline(theta=wl.theta, max_rounds=wl.rounds, max_aux=wl.max_aux,
                             seg_len=args.seg_len, workers=nw, depth=2 * tot + 2, pinned=True,
                             num_threads=1, device_reduce=device_reduce,
-                            device_workers=device_workers)
+                            device_workers=device_workers, device_ws=dws)
 
     # Phase A: every minibatch prepared and resident, then device work alone
     pipe = new_pipe(workers, False)
@@ -952,7 +969,11 @@ def run_sampled(args):
     gcn.profile_disable()
     print(f"[bench] device only: {gpu_ms:.3f} ms/step", file=sys.stderr, flush=True)
 
-    # Phase B: the overlapped schedule
+    # Phase B: the overlapped schedule (GPU-reducing workers get a device
+    # workspace share each, sized up front for the largest subgraph)
+    dev_share = gcn.device_reduce_bytes(
+        [gcn.subgraph_build(wl.n, inp.src, inp.dst) for inp in inps], 1, theta=wl.theta,
+        max_rounds=wl.rounds, max_aux=wl.max_aux)
     slots = [gcn.alloc_ws(img_bytes) for _ in range(2)]
     copy = torch.cuda.Stream()
     comp = torch.cuda.current_stream()

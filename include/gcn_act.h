@@ -19,8 +19,10 @@
  *   - Device buffers are caller-owned. Dense matrices are row-major float32
  *     with an explicit leading dimension ld (in elements): ld >= width,
  *     ld % 4 == 0, base pointer 16-byte aligned. Weight matrices are dense
- *     with ld == width. The library never allocates device memory; scratch
- *     space is the caller's `ws` buffer (256-byte aligned) of `ws_bytes`.
+ *     with ld == width. The library never allocates device memory: scratch
+ *     space is the caller's `ws` buffer (256-byte aligned) of `ws_bytes`
+ *     (gcn_aggregate_noalloc alone uses a fixed array per device that the
+ *     loaded library holds).
  *   - Device entry points take a stream (a hipStream_t passed as void*; NULL
  *     is the null stream), only enqueue work on it, never synchronise, and
  *     return before the work completes.
@@ -45,6 +47,7 @@ extern "C" {
 #define GCN_E_UNSUPPORTED  (-4)  /* valid request this build cannot serve  */
 #define GCN_E_WORKSPACE    (-5)  /* ws_bytes below the required size       */
 #define GCN_E_INTERNAL     (-6)
+#define GCN_E_NONFINITE    (-7)  /* the loss of a call was inf or NaN      */
 
 #define GCN_MAX_ROUNDS 64
 #define GCN_MAX_LAYERS 8
@@ -65,7 +68,7 @@ const char* gcn_last_error(void);
 
 /* ABI version of this header (bumped on incompatible change). */
 int gcn_abi_version(void);
-#define GCN_ABI_VERSION 5
+#define GCN_ABI_VERSION 6
 
 /* ------------------------------------------------ subgraph (host, a1)
  * gcn_subgraph_build - undirected simple subgraph in CSR form.
@@ -289,8 +292,15 @@ int gcn_graph_describe(const void* host_image, size_t bytes,
  *          GCN_PIPE_DEVICE_REDUCE: each worker reduces on the GPU that is
  *          current when the pipeline is created
  *          (gcn_redundancy_reduce_device, same result), on a stream of its
- *          own (default priority), with a device workspace that the worker
- *          allocates, grows on demand and frees at destroy.
+ *          own (default priority), in its share of dev_ws.
+ *   dev_ws, dev_ws_bytes  device workspace of the GPU-reducing workers,
+ *          caller-owned, 256-byte aligned, kept alive until destroy: split
+ *          evenly between them (256-byte-aligned shares). Size it up front
+ *          from gcn_redundancy_reduce_device_bytes of the largest subgraph
+ *          to be submitted: a job needing more than a share fails with
+ *          GCN_E_WORKSPACE (from gcn_pipeline_next); nothing is allocated
+ *          or freed on the device while jobs run. NULL, 0 without
+ *          GPU-reducing workers.
  * gcn_pipeline_submit - copies the edge arrays (the caller may free them on
  *   return) and queues the job; *job_id receives its number (0, 1, ...).
  * gcn_pipeline_submit_sample - queues a job that samples its vertex set
@@ -329,7 +339,7 @@ typedef struct {
 #define GCN_PIPE_DEVICE_REDUCE 2
 int gcn_pipeline_create(const gcn_rr_params* params, int32_t seg_len,
                         int32_t workers, int32_t depth, int32_t flags,
-                        gcn_pipeline_t* out);
+                        void* dev_ws, size_t dev_ws_bytes, gcn_pipeline_t* out);
 /* gcn_pipeline_create_mixed - the same pipeline with host_workers reducing
  * on the host and device_workers on the GPU (as GCN_PIPE_DEVICE_REDUCE);
  * every job goes to whichever worker is free, and since both reductions give
@@ -338,7 +348,8 @@ int gcn_pipeline_create(const gcn_rr_params* params, int32_t seg_len,
  * gcn_pipeline_create otherwise. */
 int gcn_pipeline_create_mixed(const gcn_rr_params* params, int32_t seg_len,
                               int32_t host_workers, int32_t device_workers, int32_t depth,
-                              int32_t flags, gcn_pipeline_t* out);
+                              int32_t flags, void* dev_ws, size_t dev_ws_bytes,
+                              gcn_pipeline_t* out);
 int gcn_pipeline_submit(gcn_pipeline_t p, int64_t n_full, const int64_t* src,
                         const int64_t* dst, int64_t n_edges,
                         const int64_t* vertices, int64_t n_vertices,
@@ -433,8 +444,11 @@ int gcn_classifier_fwd(int32_t n, int32_t K, int32_t C, const float* H,
  *   loss_out device float[1]. Deterministic (fixed summation order).
  *   C <= 512 (GCN_E_UNSUPPORTED above; the same limit holds for the
  *   training step).
- * Errors: labels are not range-checked on the device; class ids outside
- * [0, C) give an undefined loss but no out-of-bounds access. */
+ * Status: the call writes a status word, the first int32 of ws, on the
+ * device (bit 0: a label is invalid -- a class outside [0, C), or a
+ * multi-label byte other than 0 or 1 -- which gives a wrong loss but no
+ * out-of-bounds access; bit 1: the loss is not finite). gcn_status_check
+ * reads it at the caller's next host sync. */
 int gcn_loss(int32_t n, int32_t C, int32_t kind, const float* logits,
              int64_t ldz, const void* labels, float* dlogits, int64_t ldd,
              float* loss_out, void* ws, size_t ws_bytes, gcn_stream_t stream);
@@ -550,6 +564,9 @@ typedef struct {          /* byte offsets into ws, -1 when absent */
                                          H[l] and of G[l], ld ld_H (G16
                                          ping-pongs like G); -1 else */
     int64_t G16[GCN_MAX_LAYERS];
+    int64_t status;                   /* the step's loss status word (int32;
+                                         see gcn_loss), for
+                                         gcn_status_check */
 } gcn_ws_layout;
 
 int gcn_workspace_layout(const gcn_dgraph* g, const gcn_model_desc* desc,
@@ -652,6 +669,15 @@ int gcn_profile_enable(int32_t capacity);
 int gcn_profile_disable(void);
 int gcn_profile_read(gcn_profile_entry* out, int32_t max_entries,
                      int32_t* count, int32_t reset);
+
+/* gcn_status_check - the host side of the loss status word that gcn_loss
+ * (the first int32 of its ws) and gcn_train_step / gcn_train_step_optim
+ * (at ws + layout.status) write on the device every call: waits for
+ * `stream`, reads the word and returns GCN_OK, GCN_E_INVALID_ARG if a label
+ * of the last call was invalid, or GCN_E_NONFINITE if its loss was inf or
+ * NaN (message in gcn_last_error). A device-side check, so the step itself
+ * never waits on the host. `status` is a device pointer. */
+int gcn_status_check(const void* status, gcn_stream_t stream);
 
 /* ---------------------------------------------------- bandwidth probe
  * gcn_read_probe - measurement helper, not part of the training step: one

@@ -143,7 +143,9 @@ __device__ __forceinline__ float4 finish_row(float4 v, int row, int c4,
             if (c + 2 < F) v.z += bias[c + 2];
             if (c + 3 < F) v.w += bias[c + 3];
         }
-        v = make_float4(fmaxf(v.x, 0.f), fmaxf(v.y, 0.f), fmaxf(v.z, 0.f), fmaxf(v.w, 0.f));
+        // max(x, 0) keeping a NaN, as the GEMM epilogues do
+        auto relu = [](float x) { return x <= 0.f ? 0.f : x; };
+        v = make_float4(relu(v.x), relu(v.y), relu(v.z), relu(v.w));
     }
     return v;
 }

@@ -17,9 +17,10 @@ constexpr int64_t kAlign = 256;
 inline int64_t r4(int64_t x) { return round_up(x, 4); }
 inline int64_t r8(int64_t x) { return round_up(x, 8); }
 
-// Scratch regions (bytes from the start of ws) for widths up to W.
+// Scratch regions (bytes from the start of ws) for widths up to W. The
+// loss status word (one int32) comes first, at offset 0.
 struct ScratchPlan {
-    int64_t aux, part_list, T, gemm_part, rowloss, total;
+    int64_t status, aux, part_list, T, gemm_part, rowloss, rowflag, total;
     int64_t gemm_part_floats;   // per problem
     int64_t ld_max;             // widest row (floats) of the aux / T regions
 };
@@ -40,12 +41,14 @@ ScratchPlan plan_scratch(int64_t n, int64_t naux, int64_t nslots, int64_t W) {
         return o;
     };
     p.ld_max = ldW;
+    p.status = take(4);
     p.aux = take(4 * naux * ldW);
     p.part_list = take(4 * nslots * ldW);
     p.T = take(4 * n * ldW);
     p.gemm_part_floats = gemm_part_bound(W);
     p.gemm_part = take(4 * 2 * p.gemm_part_floats);
     p.rowloss = take(4 * std::max<int64_t>(n, 1));
+    p.rowflag = take(4 * std::max<int64_t>(n, 1));
     p.total = off;
     return p;
 }
@@ -158,6 +161,10 @@ __bf16* hptr(void* ws, int64_t off) {
 
 float* fptr(void* ws, int64_t off) {
     return reinterpret_cast<float*>(static_cast<char*>(ws) + off);
+}
+
+int32_t* iptr(void* ws, int64_t off) {
+    return reinterpret_cast<int32_t*>(static_cast<char*>(ws) + off);
 }
 
 // ------------------------------------------------------------ internals
@@ -755,6 +762,7 @@ int plan_step(const gcn_dgraph* g, const gcn_model_desc* d, StepLayout* out) {
     out->sp = plan_scratch(n, g->naux, g->nslots, W);
     out->pub.scratch = off;
     out->pub.scratch_bytes = out->sp.total;
+    out->pub.status = out->pub.scratch + out->sp.status;
     out->pub.total_bytes = off + out->sp.total;
     return GCN_OK;
 }
@@ -915,8 +923,28 @@ int gcn_loss(int32_t n, int32_t C, int32_t kind, const float* logits, int64_t ld
     const ScratchPlan sp = plan_scratch(n, 0, 0, C);
     GCN_TRY(check_ws(fn, ws, ws_bytes, sp.total));
     GCN_HIP(launch_loss(n, C, kind, logits, ldz, labels, dlogits, ldd, fptr(ws, sp.rowloss),
-                        loss_out, (hipStream_t)stream),
+                        iptr(ws, sp.rowflag), iptr(ws, sp.status), loss_out,
+                        (hipStream_t)stream),
             fn);
+    return GCN_OK;
+}
+
+int gcn_status_check(const void* status, gcn_stream_t stream) {
+    const char* fn = "gcn_status_check";
+    GCN_CHECK_ARG(status != nullptr && ((uintptr_t)status & 3) == 0,
+                  "%s: status word NULL or not 4-byte aligned", fn);
+    GCN_HIP(hipStreamSynchronize((hipStream_t)stream), fn);
+    int32_t w = 0;
+    GCN_HIP(hipMemcpy(&w, status, sizeof(w), hipMemcpyDeviceToHost), fn);
+    if (w & 1) {
+        set_error("%s: a label is invalid (softmax: class outside [0, C); multi-label: a "
+                  "byte other than 0 or 1); the loss and gradients of that call are wrong", fn);
+        return GCN_E_INVALID_ARG;
+    }
+    if (w & 2) {
+        set_error("%s: the loss is not finite (inf or NaN in the logits or the inputs)", fn);
+        return GCN_E_NONFINITE;
+    }
     return GCN_OK;
 }
 
@@ -1162,7 +1190,8 @@ int train_step_impl(const char* fn, const gcn_dgraph* g, const gcn_model_desc* d
     // split logits are summed (with the bias) inside the loss kernel
     GCN_HIP(launch_loss_parts((int32_t)n, C, d->loss, lg.part, lg.stride, lg.splits, lg.ldp,
                               lg.splits > 1 ? bcls : nullptr, Z, ldC, labels, dZ, ldC,
-                              fptr(scratch, sp.rowloss), loss_out, s,
+                              fptr(scratch, sp.rowloss), iptr(scratch, sp.rowflag),
+                              iptr(scratch, sp.status), loss_out, s,
                               cp.on ? h16(cp.dZ) : nullptr, cp.ld_dz),
             fn);
     // backward (classifier, then Eq. 2a-2c layer by layer)

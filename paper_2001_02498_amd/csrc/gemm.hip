@@ -46,6 +46,10 @@ __device__ __forceinline__ float4 ld4(const float* p) {
     return *reinterpret_cast<const float4*>(p);
 }
 
+// max(x, 0) that keeps a NaN (as IEEE maximum does), so a non-finite input
+// reaches the loss instead of vanishing in a ReLU
+__device__ __forceinline__ float relu(float x) { return x <= 0.f ? 0.f : x; }
+
 __device__ __forceinline__ void zero_from(float4& v, int valid) {
     // keep the first `valid` elements (valid may be <= 0 or >= 4)
     if (valid < 4) v.w = 0.f;
@@ -177,7 +181,7 @@ __device__ __forceinline__ void store_tile(const GemmProblem& P, int split, int 
                     if constexpr (EP == EPI_BIAS_RELU) {
                         if (!P.no_relu) {
 #pragma unroll
-                            for (int t = 0; t < 4; ++t) v[t] = v[t] > 0.f ? v[t] : 0.f;
+                            for (int t = 0; t < 4; ++t) v[t] = relu(v[t]);
                         }
                     }
                 } else if constexpr (EP == EPI_MASK) {
@@ -294,7 +298,7 @@ __device__ __forceinline__ void store_tile_lds(const GemmProblem& P, int split, 
                 if constexpr (EP == EPI_BIAS_RELU) {
                     if (!P.no_relu) {
 #pragma unroll
-                        for (int t = 0; t < 4; ++t) w[t] = w[t] > 0.f ? w[t] : 0.f;
+                        for (int t = 0; t < 4; ++t) w[t] = relu(w[t]);
                     }
                 }
             } else if constexpr (EP == EPI_MASK) {

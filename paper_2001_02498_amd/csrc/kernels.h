@@ -184,17 +184,20 @@ hipError_t launch_to_bf16(const ConvJob* jobs, int njobs, hipStream_t s);
 
 // ---------------------------------------------------------------- loss
 constexpr int kMaxLossVPL = 8;   // classes per lane: C <= 512
+// rowflag [n] (per-row invalid-label flags) and status (one int32: bit 0 an
+// invalid label, bit 1 a non-finite loss, written every call) may be NULL.
 hipError_t launch_loss(int32_t n, int32_t C, int32_t kind, const float* z,
                        int64_t ldz, const void* labels, float* dz,
-                       int64_t ldd, float* rowloss, float* loss_out,
-                       hipStream_t s);
+                       int64_t ldd, float* rowloss, int32_t* rowflag, int32_t* status,
+                       float* loss_out, hipStream_t s);
 // The same with logits = sum of `splits` slices (stride apart, ld ldp) plus
 // bias, written to z_out.
 // dzh != NULL: also a bf16 copy of dz (leading dimension lddh).
 hipError_t launch_loss_parts(int32_t n, int32_t C, int32_t kind, const float* part,
                              int64_t stride, int32_t splits, int64_t ldp, const float* bias,
                              float* z_out, int64_t ldz, const void* labels, float* dz,
-                             int64_t ldd, float* rowloss, float* loss_out, hipStream_t s,
-                             __bf16* dzh = nullptr, int64_t lddh = 0);
+                             int64_t ldd, float* rowloss, int32_t* rowflag, int32_t* status,
+                             float* loss_out, hipStream_t s, __bf16* dzh = nullptr,
+                             int64_t lddh = 0);
 
 }  // namespace gcn

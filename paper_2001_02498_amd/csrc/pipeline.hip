@@ -89,6 +89,11 @@ struct gcn_pipeline {
         b.cap = 0;
     }
 
+    // caller-owned device workspace of the GPU-reducing workers, split
+    // evenly between them (256-byte-aligned shares)
+    char* dev_ws = nullptr;
+    size_t dev_share = 0;
+
     // per-worker device state of the device reduction
     struct DevState {
         bool device = false;   // this worker reduces on the GPU
@@ -97,20 +102,21 @@ struct gcn_pipeline {
         size_t cap = 0;
     };
 
-    void run(bool device_worker) {
+    void run(bool device_worker, int32_t index) {
         DevState ds;
         ds.device = device_worker;
         if (device_worker) {
             (void)hipSetDevice(device);
             if (hipStreamCreate(&ds.stream) != hipSuccess) ds.stream = nullptr;
+            ds.ws = dev_ws + (size_t)index * dev_share;
+            ds.cap = dev_share;
         }
         run_jobs(ds);
-        if (ds.ws) (void)hipFree(ds.ws);
         if (ds.stream) (void)hipStreamDestroy(ds.stream);
     }
 
-    // device reduction with a workspace grown to fit (256-byte aligned by
-    // hipMalloc)
+    // device reduction in the worker's share of the caller's workspace; a
+    // job that needs more fails (nothing is allocated while jobs run)
     int reduce_on_device(gcn_graph_t g, DevState& ds, gcn_reduced_t* r) {
         if (!ds.stream) {
             set_error("gcn_pipeline: worker stream not created");
@@ -120,16 +126,10 @@ struct gcn_pipeline {
         int rc = gcn_redundancy_reduce_device_bytes(g, &rr, &need);
         if (rc) return rc;
         if (need > ds.cap) {
-            if (ds.ws) (void)hipFree(ds.ws);
-            ds.ws = nullptr;
-            ds.cap = 0;
-            const size_t bytes = need + need / 2;
-            if (hipMalloc(&ds.ws, bytes) != hipSuccess) {
-                ds.ws = nullptr;
-                set_error("gcn_pipeline: device workspace of %zu bytes not allocated", bytes);
-                return GCN_E_OOM;
-            }
-            ds.cap = bytes;
+            set_error("gcn_pipeline: the device reduction needs %zu bytes, a worker's share of "
+                      "the pipeline's device workspace is %zu",
+                      need, ds.cap);
+            return GCN_E_WORKSPACE;
         }
         return gcn_redundancy_reduce_device(g, &rr, ds.ws, ds.cap, ds.stream, r);
     }
@@ -257,7 +257,8 @@ extern "C" {
 
 int gcn_pipeline_create_mixed(const gcn_rr_params* params, int32_t seg_len,
                               int32_t host_workers, int32_t device_workers, int32_t depth,
-                              int32_t flags, gcn_pipeline_t* out) {
+                              int32_t flags, void* dev_ws, size_t dev_ws_bytes,
+                              gcn_pipeline_t* out) {
     GCN_CHECK_ARG(params && out, "gcn_pipeline_create: NULL argument");
     GCN_CHECK_ARG(host_workers >= 0 && device_workers >= 0 &&
                       host_workers + device_workers >= 1 && host_workers + device_workers <= 256,
@@ -270,6 +271,12 @@ int gcn_pipeline_create_mixed(const gcn_rr_params* params, int32_t seg_len,
                   "gcn_pipeline_create: seg_len outside [1, 65536]");
     GCN_CHECK_ARG((flags & ~GCN_PIPE_PINNED) == 0, "gcn_pipeline_create: unknown flags 0x%x",
                   flags);
+    const size_t share =
+        device_workers > 0 ? dev_ws_bytes / (size_t)device_workers / 256 * 256 : 0;
+    GCN_CHECK_ARG(device_workers == 0 ||
+                      (dev_ws != nullptr && ((uintptr_t)dev_ws & 255) == 0 && share > 0),
+                  "gcn_pipeline_create: GPU-reducing workers need a 256-byte-aligned device "
+                  "workspace of at least 256 bytes each");
     try {
         auto* p = new gcn_pipeline;
         p->rr = *params;
@@ -277,13 +284,17 @@ int gcn_pipeline_create_mixed(const gcn_rr_params* params, int32_t seg_len,
         p->depth = depth;
         p->pinned = (flags & GCN_PIPE_PINNED) != 0;
         p->device_reduce = device_workers > 0;
+        p->dev_ws = static_cast<char*>(dev_ws);
+        p->dev_share = share;
         if (p->device_reduce && hipGetDevice(&p->device) != hipSuccess) {
             delete p;
             set_error("gcn_pipeline_create: no current GPU for the device reduction");
             return GCN_E_HIP;
         }
-        for (int32_t i = 0; i < device_workers; ++i) p->workers.emplace_back([p] { p->run(true); });
-        for (int32_t i = 0; i < host_workers; ++i) p->workers.emplace_back([p] { p->run(false); });
+        for (int32_t i = 0; i < device_workers; ++i)
+            p->workers.emplace_back([p, i] { p->run(true, i); });
+        for (int32_t i = 0; i < host_workers; ++i)
+            p->workers.emplace_back([p, i] { p->run(false, i); });
         *out = p;
         return GCN_OK;
     } catch (const std::exception& e) {
@@ -293,13 +304,14 @@ int gcn_pipeline_create_mixed(const gcn_rr_params* params, int32_t seg_len,
 }
 
 int gcn_pipeline_create(const gcn_rr_params* params, int32_t seg_len, int32_t workers,
-                        int32_t depth, int32_t flags, gcn_pipeline_t* out) {
+                        int32_t depth, int32_t flags, void* dev_ws, size_t dev_ws_bytes,
+                        gcn_pipeline_t* out) {
     GCN_CHECK_ARG((flags & ~(GCN_PIPE_PINNED | GCN_PIPE_DEVICE_REDUCE)) == 0,
                   "gcn_pipeline_create: unknown flags 0x%x", flags);
     GCN_CHECK_ARG(workers >= 1 && workers <= 256, "gcn_pipeline_create: workers outside [1, 256]");
     const bool dev = (flags & GCN_PIPE_DEVICE_REDUCE) != 0;
     return gcn_pipeline_create_mixed(params, seg_len, dev ? 0 : workers, dev ? workers : 0, depth,
-                                     flags & GCN_PIPE_PINNED, out);
+                                     flags & GCN_PIPE_PINNED, dev_ws, dev_ws_bytes, out);
 }
 
 int gcn_pipeline_submit(gcn_pipeline_t p, int64_t n_full, const int64_t* src,

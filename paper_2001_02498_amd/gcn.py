@@ -26,6 +26,7 @@ E_INVALID_ARG = -1
 E_HIP = -2
 E_OOM = -3
 E_UNSUPPORTED = -4
+E_NONFINITE = -7
 E_WORKSPACE = -5
 E_INTERNAL = -6
 MAX_ROUNDS = 64
@@ -43,7 +44,7 @@ OPT_MOMENTUM = 1
 OPT_ADAM = 2
 AGG_MEAN = 0
 AGG_TRANSPOSED = 1
-ABI_VERSION = 5
+ABI_VERSION = 6
 
 _i32, _i64, _f32 = C.c_int32, C.c_int64, C.c_float
 _vp, _sz = C.c_void_p, C.c_size_t
@@ -94,7 +95,8 @@ class WsLayout(C.Structure):
                 ("logits", _i64), ("dlogits", _i64), ("ld_C", _i64),
                 ("G", _i64 * MAX_LAYERS),
                 ("scratch", _i64), ("scratch_bytes", _i64), ("total_bytes", _i64),
-                ("ah_bytes", _i64), ("H16", _i64 * MAX_LAYERS), ("G16", _i64 * MAX_LAYERS)]
+                ("ah_bytes", _i64), ("H16", _i64 * MAX_LAYERS), ("G16", _i64 * MAX_LAYERS),
+                ("status", _i64)]
 
 
 def _proto(name, args, res=C.c_int):
@@ -175,6 +177,7 @@ _prof_enable = _proto("gcn_profile_enable", [_i32])
 _prof_disable = _proto("gcn_profile_disable", [])
 _prof_read = _proto("gcn_profile_read", [C.POINTER(ProfileEntry), _i32, _pi32, _i32])
 _read_probe = _proto("gcn_read_probe", [_vp, _sz, _vp, _vp])
+_status_check = _proto("gcn_status_check", [_vp, _vp])
 READ_PROBE_SINK = 16384
 
 class PipelineInfo(C.Structure):
@@ -186,9 +189,9 @@ class PipelineInfo(C.Structure):
 
 
 _pipe_create = _proto("gcn_pipeline_create", [C.POINTER(RrParams), _i32, _i32, _i32, _i32,
-                                              C.POINTER(_vp)])
+                                              _vp, _sz, C.POINTER(_vp)])
 _pipe_create_mixed = _proto("gcn_pipeline_create_mixed", [C.POINTER(RrParams), _i32, _i32, _i32,
-                                                          _i32, _i32, C.POINTER(_vp)])
+                                                          _i32, _i32, _vp, _sz, C.POINTER(_vp)])
 _pipe_submit = _proto("gcn_pipeline_submit", [_vp, _i64, _vp, _vp, _i64, _vp, _i64,
                                               C.POINTER(_i64)])
 _pipe_submit_sample = _proto("gcn_pipeline_submit_sample", [_vp, _vp, _i32, _i32, C.c_uint64,
@@ -211,6 +214,7 @@ EXPORTS = [
     "gcn_profile_read", "gcn_pipeline_create", "gcn_pipeline_submit", "gcn_pipeline_next",
     "gcn_pipeline_release", "gcn_pipeline_destroy", "gcn_pipeline_submit_sample",
     "gcn_pipeline_create_mixed", "gcn_read_probe", "gcn_aggregate_noalloc",
+    "gcn_status_check",
 ]
 
 
@@ -239,10 +243,12 @@ class Graph:
     def __init__(self, handle):
         self._h = _vp(handle)
 
-    def __del__(self):
+    def __del__(self, _free=_graph_free, _null=_vp):
+        # the free function is bound as a default: at interpreter teardown
+        # the module's globals may already be gone
         if getattr(self, "_h", None) and self._h.value:
-            _graph_free(self._h)
-            self._h = _vp()
+            _free(self._h)
+            self._h = _null()
 
     def _info(self):
         n, nnz = _i32(), _i64()
@@ -321,10 +327,10 @@ class Reduced:
     def __init__(self, handle):
         self._h = _vp(handle)
 
-    def __del__(self):
+    def __del__(self, _free=_reduced_free, _null=_vp):
         if getattr(self, "_h", None) and self._h.value:
-            _reduced_free(self._h)
-            self._h = _vp()
+            _free(self._h)
+            self._h = _null()
 
     def info(self):
         n, naux, rounds, nnz = _i32(), _i32(), _i32(), _i64()
@@ -357,6 +363,15 @@ def redundancy_reduce_device_bytes(g: Graph, theta=2, max_rounds=5, max_aux=-1) 
     b = _sz()
     _check(_reduce_dev_bytes(g._h, C.byref(p), C.byref(b)))
     return b.value
+
+
+def device_reduce_bytes(graphs, workers=1, theta=2, max_rounds=5, max_aux=-1) -> int:
+    """Device workspace for `workers` GPU-reducing pipeline workers that can
+    each reduce any of `graphs`: workers x the largest
+    gcn_redundancy_reduce_device_bytes, in 256-byte-aligned shares."""
+    need = max([redundancy_reduce_device_bytes(g, theta, max_rounds, max_aux) for g in graphs]
+               + [256])
+    return int(workers) * ((need + 255) // 256 * 256)
 
 
 def redundancy_reduce_device(g: Graph, ws, theta=2, max_rounds=5, max_aux=-1,
@@ -577,6 +592,14 @@ def profile_read(reset=True):
             for i in range(min(cnt.value, 32))}
 
 
+def status_check(ws, offset=0, stream=None):
+    """gcn_status_check on the status word at byte `offset` of the device
+    buffer `ws` (0 for gcn_loss's ws; layout.status for a training step's):
+    raises GcnError (E_INVALID_ARG: an invalid label; E_NONFINITE: the loss
+    was not finite) after waiting for the stream."""
+    _check(_status_check(_vp(ws.data_ptr() + int(offset)), _stream(stream)))
+
+
 def read_probe(buf, sink, stream=None):
     """One streaming read of every byte of the device tensor `buf`
     (gcn_read_probe); `sink`: device float32 tensor of READ_PROBE_SINK."""
@@ -595,21 +618,28 @@ class Pipeline:
     """Host worker pool preparing graph images in submission order."""
 
     def __init__(self, theta=2, max_rounds=5, max_aux=-1, seg_len=0, workers=4, depth=8,
-                 pinned=True, num_threads=1, device_reduce=False, device_workers=None):
+                 pinned=True, num_threads=1, device_reduce=False, device_workers=None,
+                 device_ws=None):
         """`workers` threads reducing on the host (on the GPU with
         device_reduce); device_workers > 0 adds that many GPU-reducing
-        workers beside `workers` host ones."""
+        workers beside `workers` host ones. GPU-reducing workers share
+        `device_ws` (a 256-byte-aligned device uint8 tensor, e.g. from
+        alloc_ws, kept alive by the pipeline), split evenly between them:
+        size it with device_reduce_bytes()."""
         p = RrParams(int(theta), int(max_rounds), int(max_aux), int(num_threads), 0)
         self._h = _vp()
         self._borrowed = {}   # job id -> full graph a sampled job reads
+        self._dev_ws = device_ws
+        ws_ptr = _ptr(device_ws) if device_ws is not None else None
+        ws_bytes = device_ws.numel() if device_ws is not None else 0
         if device_workers is not None:
             _check(_pipe_create_mixed(C.byref(p), int(seg_len), int(workers), int(device_workers),
-                                      int(depth), PIPE_PINNED if pinned else 0,
+                                      int(depth), PIPE_PINNED if pinned else 0, ws_ptr, ws_bytes,
                                       C.byref(self._h)))
             return
         flags = (PIPE_PINNED if pinned else 0) | (PIPE_DEVICE_REDUCE if device_reduce else 0)
-        _check(_pipe_create(C.byref(p), int(seg_len), int(workers), int(depth), flags,
-                            C.byref(self._h)))
+        _check(_pipe_create(C.byref(p), int(seg_len), int(workers), int(depth), flags, ws_ptr,
+                            ws_bytes, C.byref(self._h)))
 
     def submit(self, n_full, src, dst, vertices=None):
         src = np.ascontiguousarray(src, dtype=np.int64)
@@ -642,11 +672,14 @@ class Pipeline:
     def release(self, job_id):
         _check(_pipe_release(self._h, int(job_id)))
 
-    def close(self):
+    def close(self, _destroy=_pipe_destroy, _null=_vp):
+        # (the library functions are bound as defaults: __del__ may run
+        # while the interpreter tears this module's globals down)
         if getattr(self, "_h", None) and self._h.value:
-            _pipe_destroy(self._h)   # joins the workers: no job reads a graph after this
-            self._h = _vp()
+            _destroy(self._h)   # joins the workers: no job reads a graph after this
+            self._h = _null()
         self._borrowed = {}
+        self._dev_ws = None
 
     def __del__(self):
         self.close()

@@ -64,13 +64,18 @@ def test_pipelined_stream_matches_sequential(device_reduce):
     comp = torch.cuda.current_stream()
     slot_free = [None, None]
     held = collections.deque()
+    # the GPU-reducing workers' device workspace, sized up front
+    gs = [gcn.subgraph_build(wl.n, inp.src, inp.dst) for inp in inps]
+    rr = dict(theta=wl.theta, max_rounds=wl.rounds, max_aux=wl.max_aux)
     if device_reduce == "mixed":
         # two host and two GPU-reducing workers share the queue
-        pipe = gcn.Pipeline(theta=wl.theta, max_rounds=wl.rounds, max_aux=wl.max_aux,
-                            workers=2, device_workers=2, depth=4, pinned=True)
+        dws = gcn.alloc_ws(gcn.device_reduce_bytes(gs, 2, **rr))
+        pipe = gcn.Pipeline(**rr, workers=2, device_workers=2, depth=4, pinned=True,
+                            device_ws=dws)
     else:
-        pipe = gcn.Pipeline(theta=wl.theta, max_rounds=wl.rounds, max_aux=wl.max_aux,
-                            workers=3, depth=4, pinned=True, device_reduce=device_reduce)
+        dws = gcn.alloc_ws(gcn.device_reduce_bytes(gs, 3, **rr)) if device_reduce else None
+        pipe = gcn.Pipeline(**rr, workers=3, depth=4, pinned=True, device_reduce=device_reduce,
+                            device_ws=dws)
     try:
         for inp in inps:
             pipe.submit(wl.n, inp.src, inp.dst)

@@ -149,9 +149,16 @@ def test_sampled_jobs_reduced_on_gpu_match_host(mode):
     full = gcn.subgraph_build(30000, fi.src, fi.dst)
     jobs = [(60, 2000, wl.sample_seed(i), wl.max_steps) for i in range(5)]
 
+    # the GPU-reducing workers' device workspace, sized up front from the
+    # same walks taken on the host
+    rr = dict(theta=wl.theta, max_rounds=wl.rounds, max_aux=wl.max_aux)
+    gs = [gcn.subgraph_induce(full, gcn.sample_frontier(full, *j)[0]) for j in jobs]
+    dws = gcn.alloc_ws(gcn.device_reduce_bytes(gs, 2, **rr))
+
     def buffers(**kw):
-        pipe = gcn.Pipeline(theta=wl.theta, max_rounds=wl.rounds, max_aux=wl.max_aux, depth=3,
-                            pinned=True, **kw)
+        if kw.get("device_reduce") or kw.get("device_workers"):
+            kw["device_ws"] = dws
+        pipe = gcn.Pipeline(**rr, depth=3, pinned=True, **kw)
         out = []
         try:
             for j in jobs:

@@ -3,6 +3,7 @@ packing subgraphs ahead of the device) on the CPU: results in submission
 order, images identical to direct packing, failures reported per job, and
 the hold limit that keeps a misused pipeline from waiting forever."""
 import ctypes
+import os
 
 import numpy as np
 import pytest
@@ -10,6 +11,7 @@ import pytest
 from paper_2001_02498_amd import synth
 
 gcn = pytest.importorskip("paper_2001_02498_amd.gcn")
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 
 
 def _direct_image(n, src, dst, theta, rounds, seg_len):
@@ -142,3 +144,30 @@ def test_mixed_pipeline_host_only_and_rejects():
     for hw, dw in ((0, 0), (-1, 1), (200, 100)):
         with pytest.raises(gcn.GcnError):
             gcn.Pipeline(workers=hw, device_workers=dw, pinned=False)
+
+
+def test_device_workers_need_a_workspace():
+    # GPU-reducing workers take their device workspace from the caller up
+    # front; without one the pipeline is refused before any worker starts
+    for kw in (dict(device_workers=1), dict(device_reduce=True)):
+        with pytest.raises(gcn.GcnError) as e:
+            gcn.Pipeline(workers=1, pinned=False, **kw)
+        assert e.value.code == gcn.E_INVALID_ARG
+        assert "device workspace" in str(e.value)
+
+
+def test_handles_survive_interpreter_teardown():
+    # graphs, reductions and pipelines still alive at exit are freed by
+    # their __del__ after the module's globals are gone, without errors
+    import subprocess
+    import sys
+    code = ("import numpy as np\n"
+            "from paper_2001_02498_amd import gcn\n"
+            "g = gcn.subgraph_build(4, np.array([0, 1, 2]), np.array([1, 2, 3]))\n"
+            "r = gcn.redundancy_reduce(g, theta=0)\n"
+            "p = gcn.Pipeline(workers=1, pinned=False)\n"
+            "keep = [g, r, p]\n")
+    out = subprocess.run([sys.executable, "-c", code], capture_output=True, text=True,
+                         cwd=ROOT, timeout=120)
+    assert out.returncode == 0, out.stderr
+    assert "Exception ignored" not in out.stderr and "Error" not in out.stderr, out.stderr
