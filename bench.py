@@ -969,11 +969,7 @@ def run_sampled(args):
     gcn.profile_disable()
     print(f"[bench] device only: {gpu_ms:.3f} ms/step", file=sys.stderr, flush=True)
 
-    # Phase B: the overlapped schedule (GPU-reducing workers get a device
-    # workspace share each, sized up front for the largest subgraph)
-    dev_share = gcn.device_reduce_bytes(
-        [gcn.subgraph_build(wl.n, inp.src, inp.dst) for inp in inps], 1, theta=wl.theta,
-        max_rounds=wl.rounds, max_aux=wl.max_aux)
+    # Phase B: the overlapped schedule
     slots = [gcn.alloc_ws(img_bytes) for _ in range(2)]
     copy = torch.cuda.Stream()
     comp = torch.cuda.current_stream()
