@@ -50,6 +50,16 @@ __device__ __forceinline__ float4 ld4(const float* p) {
 // reaches the loss instead of vanishing in a ReLU
 __device__ __forceinline__ float relu(float x) { return x <= 0.f ? 0.f : x; }
 
+// Whole K steps [kbeg, kbeg + nfull * BK) of a K-concatenated operand load
+// from one per-step base plus fixed per-thread offsets when the
+// concatenation point lies past them (a one-part operand has it at K), or
+// on a K-step boundary between parts of equal leading dimension (kbeg is a
+// multiple of BK).
+__device__ __forceinline__ bool concat_fast(int ksplit, int kbeg, int nfull, int64_t ld1,
+                                            int64_t ld0) {
+    return ksplit >= kbeg + nfull * BK || (ksplit % BK == 0 && ld1 == ld0);
+}
+
 __device__ __forceinline__ void zero_from(float4& v, int valid) {
     // keep the first `valid` elements (valid may be <= 0 or >= 4)
     if (valid < 4) v.w = 0.f;
@@ -525,10 +535,10 @@ __global__ __launch_bounds__(kThreads, 2) void gemm_kernel(GemmBatch batch) {
     // boundary between parts of equal leading dimension, a whole K step
     // loads from a uniform per-step base plus fixed per-thread offsets and
     // stores without masking.
-    const bool fast_tile = BVEC && !(ones && Areal >= m0 && Areal < m0 + TBM) &&
-                           (AL == A_KM || (ksplitA % BK == 0 && P.lda1 == lda0)) &&
-                           (BL == B_KN || (ksplitB % BK == 0 && P.ldb1 == ldb0));
     const int nfull = (kend - kbeg) / BK;
+    const bool fast_tile = BVEC && !(ones && Areal >= m0 && Areal < m0 + TBM) &&
+                           (AL == A_KM || concat_fast(ksplitA, kbeg, nfull, P.lda1, lda0)) &&
+                           (BL == B_KN || concat_fast(ksplitB, kbeg, nfull, P.ldb1, ldb0));
     int64_t oa[kQA], ob[kQB];
 #pragma unroll
     for (int q = 0; q < kQA; ++q) {
@@ -834,10 +844,10 @@ __global__ __launch_bounds__(kThreads, 2) void gemm_bf16_kernel(GemmBatch batch)
     // boundary between parts of equal leading dimension, every whole K step
     // then needs no per-element work besides the bf16 conversion; the last
     // (partial) steps and every other tile take the masked path.
-    const bool fast_tile = BVEC && !(ones && Areal >= m0 && Areal < m0 + BM) &&
-                           (AL == A_KM || (ksplitA % BK == 0 && P.lda1 == lda0)) &&
-                           (BL == B_KN || (ksplitB % BK == 0 && P.ldb1 == ldb0));
     const int nfull = (kend - kbeg) / BK;   // whole K steps of this split
+    const bool fast_tile = BVEC && !(ones && Areal >= m0 && Areal < m0 + BM) &&
+                           (AL == A_KM || concat_fast(ksplitA, kbeg, nfull, P.lda1, lda0)) &&
+                           (BL == B_KN || concat_fast(ksplitB, kbeg, nfull, P.ldb1, ldb0));
     // Fast loads address element (row, k) of an operand as a base pointer
     // that depends only on the K step (uniform: scalar registers) plus a
     // per-thread offset fixed for the whole loop. Both parts of a
@@ -1118,10 +1128,10 @@ __global__ __launch_bounds__(kThreads, 2) void gemm_h16_kernel(GemmBatch batch) 
     // whole K steps then load from a per-step base plus fixed per-thread
     // offsets (rows / columns outside the operand clamped into it: they
     // only feed outputs the epilogue drops).
-    const bool fast_tile = !(ones && Areal >= m0 && Areal < m0 + BM) &&
-                           (AL == A_KM || (ksplitA % BK == 0 && P.hlda1 == lda0)) &&
-                           (BL == B_KN || (ksplitB % BK == 0 && P.hldb1 == ldb0));
     const int nfull = (kend - kbeg) / BK;
+    const bool fast_tile = !(ones && Areal >= m0 && Areal < m0 + BM) &&
+                           (AL == A_KM || concat_fast(ksplitA, kbeg, nfull, P.hlda1, lda0)) &&
+                           (BL == B_KN || concat_fast(ksplitB, kbeg, nfull, P.hldb1, ldb0));
     int64_t oa[kQ16], ob[kQ16];
 #pragma unroll
     for (int q = 0; q < kQ16; ++q) {
