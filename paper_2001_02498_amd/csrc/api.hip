@@ -291,7 +291,9 @@ int do_classifier_fwd(const char* fn, int32_t n, int32_t K, int32_t C,
         p.hldb0 = p.hldb1 = ldwb;
     }
     // A few output tiles cannot fill the GPU: split K, then sum the slices
-    // (with the bias) either here or inside the loss kernel.
+    // (with the bias) either here or inside the loss kernel. (32-row tiles
+    // without slices were slower here: a K step then holds too few MFMAs
+    // per wavefront to cover the loads of H two steps ahead.)
     const int64_t tiles = (int64_t)((n + 127) / 128) * ((C + 127) / 128);
     int32_t splits = 1, kchunk = 0;
     if (tiles < 192) gemm_split_plan(n, C, K, 1, &splits, &kchunk);
@@ -318,10 +320,11 @@ int do_classifier_fwd(const char* fn, int32_t n, int32_t K, int32_t C,
     return GCN_OK;
 }
 
-// dW = A^T B over K = n rows with split-K slices in scratch slot `which`.
+// dW = A^T B over K = n rows with split-K slices in scratch slot `which`,
+// planned for output tiles of tm x 128.
 GemmProblem dw_problem(int32_t n, int32_t Mw, bool ones, int32_t N,
                        const float* A, int64_t lda, const float* B, int64_t ldb,
-                       float* part, int32_t nprob) {
+                       float* part, int32_t nprob, int32_t tm = 128) {
     GemmProblem p = gp_zero();
     p.M = Mw + (ones ? 1 : 0);
     p.N = N;
@@ -331,7 +334,8 @@ GemmProblem dw_problem(int32_t n, int32_t Mw, bool ones, int32_t N,
     p.ones_row = ones ? 1 : 0;
     p.B0 = p.B1 = B;
     p.ldb0 = p.ldb1 = ldb;
-    gemm_split_plan(p.M, p.N, p.K, nprob, &p.splits, &p.kchunk);
+    gemm_split_plan_tiles((int64_t)((p.M + tm - 1) / tm) * ((p.N + 127) / 128) * nprob, p.K,
+                          &p.splits, &p.kchunk);
     p.C = part;
     p.ldc = r4(N);
     p.part_stride = (int64_t)p.M * p.ldc;
@@ -430,10 +434,14 @@ int do_classifier_bwd(const char* fn, int32_t n, int32_t K, int32_t C,
         b.p[0] = p;
         GCN_HIP(launch_gemm(b, A_MK, B_NK, EPI_MASK, ROLE_CLS_DX, bf16, s), fn);
     }
+    // fp32: 32 x 128 tiles (fewer K slices to write and sum than 128-row
+    // tiles of a classifier-wide product)
     GemmBatch b;
     std::memset(&b, 0, sizeof(b));
     b.nprob = 1;
-    b.p[0] = dw_problem(n, K, bc != nullptr, C, H, ldh, dZ, ldd, fptr(ws, sp.gemm_part), 1);
+    b.tbm = bf16 ? 0 : 32;
+    b.p[0] = dw_problem(n, K, bc != nullptr, C, H, ldh, dZ, ldd, fptr(ws, sp.gemm_part), 1,
+                        bf16 ? 128 : 32);
     if (c) {
         b.p[0].hA0 = b.p[0].hA1 = c->H;
         b.p[0].hlda0 = b.p[0].hlda1 = c->ldh;

@@ -343,16 +343,21 @@ __device__ __forceinline__ void store_tile_lds(const GemmProblem& P, int split, 
 
 // A rows are always 16-byte aligned (checked on the host); BVEC selects
 // float4 or element loads for B (the classifier weight has any width C).
-// Tile shape: each wavefront of the 2 x 2 grid owns MB x NB accumulators of
-// 32 x 32, so the tile is (64 MB) x (64 NB): 128 x 128 by default, 128 x 64
-// where the launch planner finds that it spreads the tiles more evenly over
-// the CUs (launch_gemm).
+// Tile shape: the four wavefronts form a WM x (4 / WM) grid and each owns
+// MB x NB accumulators of 32 x 32, so the tile is (32 MB WM) x (32 NB 4/WM):
+// 128 x 128 by default, 128 x 64 where the launch planner finds that it
+// spreads the tiles more evenly over the CUs, and 32 x 128 (one row of
+// wavefronts, one accumulator each) for the classifier's weight gradient,
+// whose M is the classifier's input width and N its class count
+// (launch_gemm).
 template <ALayout AL, BLayout BL, Epilogue EP, bool BVEC, GemmRole ROLE, bool HALF = false,
-          int MB = 2, int NB = 2>
+          int MB = 2, int NB = 2, int WM = 2>
 __global__ __launch_bounds__(kThreads, 2) void gemm_kernel(GemmBatch batch) {
-    constexpr int TBM = 64 * MB, TBN = 64 * NB;
+    static_assert(WM == 1 || WM == 2 || WM == 4, "four wavefronts per workgroup");
+    constexpr int WN = 4 / WM;
+    constexpr int TBM = 32 * MB * WM, TBN = 32 * NB * WN;
     static_assert(TBM <= BM && TBN <= BN, "operand buffers are sized for 128 x 128");
-    static_assert(!HALF || (MB == 2 && NB == 2), "half-row mode is for 128 x 128 tiles");
+    static_assert(!HALF || (MB == 2 && NB == 2 && WM == 2), "half-row mode is for 128 x 128 tiles");
     // float4 quads per operand and K step, and the K-major layout of each
     // operand: quads per K row, K rows covered per quad index, LDS stride
     constexpr int kQA = BK * TBM / 4 / kThreads, kQB = BK * TBN / 4 / kThreads;
@@ -360,8 +365,16 @@ __global__ __launch_bounds__(kThreads, 2) void gemm_kernel(GemmBatch batch) {
     constexpr int kKStepA = kThreads / kQRA, kKStepB = kThreads / kQRB;
     constexpr int kColStrideA = TBM + 4, kColStrideB = TBN + 4;
     static_assert(kQA * kKStepA == BK && kQB * kKStepB == BK, "K-major quads cover BK rows");
-    // [buffer][A | B] operand tiles
-    __shared__ __attribute__((aligned(16))) float smem[2][2][kOperandFloats];
+    // operand buffers: [buffer][A | B]; 128-row tiles keep both at the
+    // 128 x 128 size (two workgroups per CU), a 32-row tile sizes each for
+    // its own operand
+    constexpr int kSA = TBM == BM ? kOperandFloats
+                                  : (AL == A_MK ? TBM * kRowStride : BK * kColStrideA);
+    constexpr int kSB = TBM == BM ? kOperandFloats
+                                  : (BL == B_NK ? TBN * kRowStride : BK * kColStrideB);
+    __shared__ __attribute__((aligned(16))) float smem[2 * (kSA + kSB)];
+    auto sA = [&](int buf) -> float* { return smem + buf * (kSA + kSB); };
+    auto sB = [&](int buf) -> float* { return smem + buf * (kSA + kSB) + kSA; };
 
     const TileInfo ti = decode_tile<TBM, TBN>(batch);
     const GemmProblem& P = batch.p[ti.pi];
@@ -370,7 +383,7 @@ __global__ __launch_bounds__(kThreads, 2) void gemm_kernel(GemmBatch batch) {
 
     const int t = threadIdx.x;
     const int lane = t & 63, wave = t >> 6;
-    const int wm = wave >> 1, wn = wave & 1;
+    const int wm = wave / WN, wn = wave % WN;
     const int half = lane >> 5, l32 = lane & 31;
     // HALF (every row of the product within the tile's first 64): both
     // wavefront rows work on rows 0-63, each on two of the four K groups
@@ -463,8 +476,8 @@ __global__ __launch_bounds__(kThreads, 2) void gemm_kernel(GemmBatch batch) {
         constexpr int kQM = kQA > kQB ? kQA : kQB;
 #pragma unroll
         for (int q = 0; q < kQM; ++q) {
-            if (q < kQA) *reinterpret_cast<float4*>(&smem[buf][0][a_slot(q)]) = finish(ra[set][q]);
-            if (q < kQB) *reinterpret_cast<float4*>(&smem[buf][1][b_slot(q)]) = finish(rb[set][q]);
+            if (q < kQA) *reinterpret_cast<float4*>(&sA(buf)[a_slot(q)]) = finish(ra[set][q]);
+            if (q < kQB) *reinterpret_cast<float4*>(&sB(buf)[b_slot(q)]) = finish(rb[set][q]);
         }
     };
 
@@ -594,8 +607,8 @@ __global__ __launch_bounds__(kThreads, 2) void gemm_kernel(GemmBatch batch) {
     auto sstore_full = [&](int buf, int set) {
 #pragma unroll
         for (int q = 0; q < kQMax; ++q) {
-            if (q < kQA) *reinterpret_cast<float4*>(&smem[buf][0][a_slot(q)]) = ra[set][q].v;
-            if (q < kQB) *reinterpret_cast<float4*>(&smem[buf][1][b_slot(q)]) = rb[set][q].v;
+            if (q < kQA) *reinterpret_cast<float4*>(&sA(buf)[a_slot(q)]) = ra[set][q].v;
+            if (q < kQB) *reinterpret_cast<float4*>(&sB(buf)[b_slot(q)]) = rb[set][q].v;
         }
     };
     // quads of a set filled by whole-step loads, for a masked store
@@ -619,8 +632,8 @@ __global__ __launch_bounds__(kThreads, 2) void gemm_kernel(GemmBatch batch) {
     // steps kt + 1 and kt + 2 are whole steps of a fast tile.
     auto kstep = [&](int kt, int set, auto FULL) {
         const int buf = kt & 1;
-        const float* As = smem[buf][0];
-        const float* Bs = smem[buf][1];
+        const float* As = sA(buf);
+        const float* Bs = sB(buf);
         const int kload = kbeg + (kt + 2) * BK;   // past kend near the end: empty quads
         // group 0: next group's fragments, the global loads of step kt + 2
         frag(As, Bs, 1, 1);
@@ -666,7 +679,7 @@ __global__ __launch_bounds__(kThreads, 2) void gemm_kernel(GemmBatch batch) {
         __syncthreads();
         // group 3: its fragments are already in registers, so the next
         // step's first LDS reads are hidden behind these MFMAs
-        if (more) frag(smem[buf ^ 1][0], smem[buf ^ 1][1], 0, 0);
+        if (more) frag(sA(buf ^ 1), sB(buf ^ 1), 0, 0);
         mfma_group(1);
         __builtin_amdgcn_sched_barrier(0);
     };
@@ -674,8 +687,8 @@ __global__ __launch_bounds__(kThreads, 2) void gemm_kernel(GemmBatch batch) {
     // interleaved with them as above
     auto kstep_half = [&](int kt, int set, auto FULL) __attribute__((always_inline)) {
         const int buf = kt & 1;
-        const float* As = smem[buf][0];
-        const float* Bs = smem[buf][1];
+        const float* As = sA(buf);
+        const float* Bs = sB(buf);
         const int kload = kbeg + (kt + 2) * BK;
         frag(As, Bs, g0 + 1, 1);
         const float* const sa = step_base_a(kload);
@@ -707,7 +720,7 @@ __global__ __launch_bounds__(kThreads, 2) void gemm_kernel(GemmBatch batch) {
         }
         __builtin_amdgcn_sched_barrier(0);
         __syncthreads();
-        if (more) frag(smem[buf ^ 1][0], smem[buf ^ 1][1], g0, 0);
+        if (more) frag(sA(buf ^ 1), sB(buf ^ 1), g0, 0);
     };
     auto step = [&](int kt, int set, auto FULL) __attribute__((always_inline)) {
         if constexpr (HALF)
@@ -729,7 +742,7 @@ __global__ __launch_bounds__(kThreads, 2) void gemm_kernel(GemmBatch batch) {
     }
     if (nk > 0) {
         __syncthreads();
-        frag(smem[0][0], smem[0][1], g0, 0);
+        frag(sA(0), sB(0), g0, 0);
     }
     int kt = 0;
     if (fast_start) {
@@ -750,7 +763,7 @@ __global__ __launch_bounds__(kThreads, 2) void gemm_kernel(GemmBatch batch) {
         // the second wavefront row's sums join the first's (fixed order);
         // its own rows (64-127) lie outside the product and store nothing
         __syncthreads();
-        float* red = &smem[0][0][0];
+        float* red = smem;
         auto at = [&](int i, int j, int r) { return ((wn * 4 + i * 2 + j) * 16 + r) * 64 + lane; };
         static_assert(!HALF || MB * NB == 4, "half-row reduction layout");
         if (wm == 1) {
@@ -1437,13 +1450,16 @@ hipError_t launch_splitk_finish(const float* part, int64_t part_stride, int64_t 
 
 void gemm_split_plan(int32_t M, int32_t N, int32_t K, int32_t nprob, int32_t* splits,
                      int32_t* kchunk) {
+    gemm_split_plan_tiles((int64_t)((M + BM - 1) / BM) * ((N + BN - 1) / BN) * std::max(nprob, 1),
+                          K, splits, kchunk);
+}
+
+void gemm_split_plan_tiles(int64_t tiles, int32_t K, int32_t* splits, int32_t* kchunk) {
     // Two workgroups fit per CU: pick the smallest split whose tile count
     // fills the 512 resident slots of the 256 CUs to >= 90 %, keeping >= 2 K
     // steps per split and at most 512 slices in all (the scratch bound of the
     // partial sums).
     constexpr int64_t kSlots = 512;
-    const int64_t tiles = (int64_t)((M + BM - 1) / BM) * ((N + BN - 1) / BN) *
-                          std::max(nprob, 1);
     const int64_t smax = std::max<int64_t>(1, std::min<int64_t>(32, K / (2 * BK)));
     int64_t best = 1;
     double best_eff = -1.0;
@@ -1495,13 +1511,19 @@ bool gemm_narrow_tiles(const GemmBatch& b) {
 
 hipError_t launch_gemm(GemmBatch& b, ALayout al, BLayout bl, Epilogue ep, GemmRole role,
                        bool bf16, hipStream_t s) {
-    // 128 x 64 tiles: fp32 kernel, one pass over K, row-contiguous A
-    const bool nb1 = !bf16 && ep != EPI_PARTIAL && al == A_MK && gemm_narrow_tiles(b);
+    // 32 x 128 tiles where the caller asks for them (fp32, classifier
+    // products); else 128 x 64 tiles: fp32 kernel, one pass over K,
+    // row-contiguous A
+    if (b.tbm != 0 && b.tbm != BM && b.tbm != 32) return hipErrorInvalidValue;
+    const bool small = !bf16 && b.tbm == 32;
+    if (small && role != ROLE_CLS_DW) return hipErrorInvalidValue;
+    const bool nb1 = !small && !bf16 && ep != EPI_PARTIAL && al == A_MK && gemm_narrow_tiles(b);
+    const int tbm = small ? 32 : BM;
     const int tbn = nb1 ? 64 : BN;
     int total = 0;
     for (int i = 0; i < b.nprob; ++i) {
         GemmProblem& p = b.p[i];
-        p.tiles_m = (p.M + BM - 1) / BM;
+        p.tiles_m = (p.M + tbm - 1) / tbm;
         p.tiles_n = (p.N + tbn - 1) / tbn;
         if (ep != EPI_PARTIAL) {
             p.splits = 1;
@@ -1574,13 +1596,23 @@ hipError_t launch_gemm(GemmBatch& b, ALayout al, BLayout bl, Epilogue ep, GemmRo
 #define GCN_GEMM_CASE(AL_, BL_, EP_, ROLE_)                                          \
     if (al == AL_ && bl == BL_ && ep == EP_ && role == ROLE_) {                       \
         constexpr bool kNarrowOk = EP_ != EPI_PARTIAL && AL_ == A_MK;                 \
+        constexpr bool kSmallOk = ROLE_ == ROLE_CLS_DW;                             \
         if (copies)                                                                  \
             gemm_h16_kernel<AL_, BL_, EP_, ROLE_><<<grid, block, 0, s>>>(b);          \
         else if (bf16 && bvec)                                                       \
             gemm_bf16_kernel<AL_, BL_, EP_, true, ROLE_><<<grid, block, 0, s>>>(b);   \
         else if (bf16)                                                               \
             gemm_bf16_kernel<AL_, BL_, EP_, false, ROLE_><<<grid, block, 0, s>>>(b);  \
-        else if (bvec && half_m && EP_ == EPI_PARTIAL && AL_ == A_KM)                 \
+        else if (small) {                                                            \
+            if constexpr (kSmallOk) {                                                \
+                if (bvec)                                                            \
+                    gemm_kernel<AL_, BL_, EP_, true, ROLE_, false, 1, 1, 1>           \
+                        <<<grid, block, 0, s>>>(b);                                  \
+                else                                                                 \
+                    gemm_kernel<AL_, BL_, EP_, false, ROLE_, false, 1, 1, 1>          \
+                        <<<grid, block, 0, s>>>(b);                                  \
+            }                                                                        \
+        } else if (bvec && half_m && EP_ == EPI_PARTIAL && AL_ == A_KM)                 \
             gemm_kernel<AL_, BL_, EP_, true, ROLE_, true><<<grid, block, 0, s>>>(b);  \
         else if (nb1) {                                                              \
             if constexpr (kNarrowOk) {                                               \

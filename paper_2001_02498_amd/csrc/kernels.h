@@ -105,6 +105,10 @@ struct GemmBatch {
     GemmProblem p[kMaxProblems];
     int32_t nprob;
     int32_t total_tiles;
+    // tile rows asked for by the caller: 0 (the planner's 128-row tiles) or
+    // 32 (32 x 128 tiles of the fp32 kernel, the classifier's weight
+    // gradient only; the bf16 kernels always take 128)
+    int32_t tbm;
 };
 
 // Split-K plan for `nprob` problems of one shape launched together
@@ -113,6 +117,8 @@ struct GemmBatch {
 // non-empty when K > 0.
 void gemm_split_plan(int32_t M, int32_t N, int32_t K, int32_t nprob, int32_t* splits,
                      int32_t* kchunk);
+// The same for `tiles` output tiles of any shape.
+void gemm_split_plan_tiles(int64_t tiles, int32_t K, int32_t* splits, int32_t* kchunk);
 
 // Which product of the step a launch computes (its own kernel name and
 // timing class; the code depends only on layouts and epilogue).
