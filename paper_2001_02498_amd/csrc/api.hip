@@ -516,8 +516,12 @@ int do_layer_bwd(const char* fn, const gcn_dgraph* g, int32_t F, int32_t h,
     float* part0 = fptr(ws, sp.gemm_part);
     float* part1 = part0 + sp.gemm_part_floats;
     const bool ones = bias != nullptr;
-    b.p[0] = dw_problem(n, F, ones, h, H_in, ld_in, G, ldg, part0, 2);
-    b.p[1] = dw_problem(n, F, ones, h, AH, ld_ah, G + h, ldg, part1, 2);
+    // fp32 first layer: 32 x 128 tiles (M = f_in + bias row is padded to a
+    // multiple of 32 instead of 128, and needs fewer K slices)
+    const int tm = (first && !bf16) ? 32 : 128;
+    b.tbm = tm == 32 ? 32 : 0;
+    b.p[0] = dw_problem(n, F, ones, h, H_in, ld_in, G, ldg, part0, 2, tm);
+    b.p[1] = dw_problem(n, F, ones, h, AH, ld_ah, G + h, ldg, part1, 2, tm);
     if (c) {
         for (int i = 0; i < 2; ++i) {
             b.p[i].hA0 = b.p[i].hA1 = i == 0 ? c->Hin : c->AH;
@@ -648,8 +652,10 @@ int do_layer_bwd_narrow(const char* fn, const gcn_dgraph* g, int32_t F, int32_t 
     b.nprob = 2;
     float* part0 = fptr(ws, sp.gemm_part);
     float* part1 = part0 + sp.gemm_part_floats;
-    b.p[0] = dw_problem(n, F, false, h, H_in, ld_in, G, ldg, part0, 2);
-    b.p[1] = dw_problem(n, F, false, h, H_in, ld_in, T, ldt, part1, 2);
+    const int tm = (first && !bf16) ? 32 : 128;   // as in the paper order
+    b.tbm = tm == 32 ? 32 : 0;
+    b.p[0] = dw_problem(n, F, false, h, H_in, ld_in, G, ldg, part0, 2, tm);
+    b.p[1] = dw_problem(n, F, false, h, H_in, ld_in, T, ldt, part1, 2, tm);
     if (c) {
         for (int i = 0; i < 2; ++i) {
             b.p[i].hA0 = b.p[i].hA1 = c->Hin;

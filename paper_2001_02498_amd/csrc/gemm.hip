@@ -347,9 +347,9 @@ __device__ __forceinline__ void store_tile_lds(const GemmProblem& P, int split, 
 // MB x NB accumulators of 32 x 32, so the tile is (32 MB WM) x (32 NB 4/WM):
 // 128 x 128 by default, 128 x 64 where the launch planner finds that it
 // spreads the tiles more evenly over the CUs, and 32 x 128 (one row of
-// wavefronts, one accumulator each) for the classifier's weight gradient,
-// whose M is the classifier's input width and N its class count
-// (launch_gemm).
+// wavefronts, one accumulator each) for the weight gradients of the
+// classifier (M its input width, N its class count) and of the first layer
+// (M = f_in): less padding of M and fewer K slices to sum (launch_gemm).
 template <ALayout AL, BLayout BL, Epilogue EP, bool BVEC, GemmRole ROLE, bool HALF = false,
           int MB = 2, int NB = 2, int WM = 2>
 __global__ __launch_bounds__(kThreads, 2) void gemm_kernel(GemmBatch batch) {
@@ -1516,7 +1516,7 @@ hipError_t launch_gemm(GemmBatch& b, ALayout al, BLayout bl, Epilogue ep, GemmRo
     // row-contiguous A
     if (b.tbm != 0 && b.tbm != BM && b.tbm != 32) return hipErrorInvalidValue;
     const bool small = !bf16 && b.tbm == 32;
-    if (small && role != ROLE_CLS_DW) return hipErrorInvalidValue;
+    if (small && role != ROLE_CLS_DW && role != ROLE_DW_IN) return hipErrorInvalidValue;
     const bool nb1 = !small && !bf16 && ep != EPI_PARTIAL && al == A_MK && gemm_narrow_tiles(b);
     const int tbm = small ? 32 : BM;
     const int tbn = nb1 ? 64 : BN;
@@ -1596,7 +1596,7 @@ hipError_t launch_gemm(GemmBatch& b, ALayout al, BLayout bl, Epilogue ep, GemmRo
 #define GCN_GEMM_CASE(AL_, BL_, EP_, ROLE_)                                          \
     if (al == AL_ && bl == BL_ && ep == EP_ && role == ROLE_) {                       \
         constexpr bool kNarrowOk = EP_ != EPI_PARTIAL && AL_ == A_MK;                 \
-        constexpr bool kSmallOk = ROLE_ == ROLE_CLS_DW;                             \
+        constexpr bool kSmallOk = ROLE_ == ROLE_CLS_DW || ROLE_ == ROLE_DW_IN;      \
         if (copies)                                                                  \
             gemm_h16_kernel<AL_, BL_, EP_, ROLE_><<<grid, block, 0, s>>>(b);          \
         else if (bf16 && bvec)                                                       \
