@@ -291,12 +291,15 @@ int do_classifier_fwd(const char* fn, int32_t n, int32_t K, int32_t C,
         p.hldb0 = p.hldb1 = ldwb;
     }
     // A few output tiles cannot fill the GPU: split K, then sum the slices
-    // (with the bias) either here or inside the loss kernel. (32-row tiles
-    // without slices were slower here: a K step then holds too few MFMAs
-    // per wavefront to cover the loads of H two steps ahead.)
-    const int64_t tiles = (int64_t)((n + 127) / 128) * ((C + 127) / 128);
+    // (with the bias) either here or inside the loss kernel. fp32 takes
+    // 64 x 128 tiles: twice the row tiles, so half the slices to write and
+    // sum. (32-row tiles without slices were slower: a K step then holds
+    // too few MFMAs per wavefront to cover the loads of H two steps ahead.)
+    const int tm = bf16 ? 128 : 64;
+    b.tbm = bf16 ? 0 : 64;
+    const int64_t tiles = (int64_t)((n + tm - 1) / tm) * ((C + 127) / 128);
     int32_t splits = 1, kchunk = 0;
-    if (tiles < 192) gemm_split_plan(n, C, K, 1, &splits, &kchunk);
+    if (tiles < (bf16 ? 192 : 256)) gemm_split_plan_tiles(tiles, K, &splits, &kchunk);
     if (splits > 1) {
         p.splits = splits;
         p.kchunk = kchunk;

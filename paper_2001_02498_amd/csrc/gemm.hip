@@ -346,10 +346,12 @@ __device__ __forceinline__ void store_tile_lds(const GemmProblem& P, int split, 
 // Tile shape: the four wavefronts form a WM x (4 / WM) grid and each owns
 // MB x NB accumulators of 32 x 32, so the tile is (32 MB WM) x (32 NB 4/WM):
 // 128 x 128 by default, 128 x 64 where the launch planner finds that it
-// spreads the tiles more evenly over the CUs, and 32 x 128 (one row of
+// spreads the tiles more evenly over the CUs, 32 x 128 (one row of
 // wavefronts, one accumulator each) for the weight gradients of the
 // classifier (M its input width, N its class count) and of the first layer
-// (M = f_in): less padding of M and fewer K slices to sum (launch_gemm).
+// (M = f_in): less padding of M and fewer K slices to sum, and 64 x 128 for
+// the classifier's logits (N = C): twice the row tiles of 128 x 128, so
+// half the K slices (launch_gemm).
 template <ALayout AL, BLayout BL, Epilogue EP, bool BVEC, GemmRole ROLE, bool HALF = false,
           int MB = 2, int NB = 2, int WM = 2>
 __global__ __launch_bounds__(kThreads, 2) void gemm_kernel(GemmBatch batch) {
@@ -1511,14 +1513,18 @@ bool gemm_narrow_tiles(const GemmBatch& b) {
 
 hipError_t launch_gemm(GemmBatch& b, ALayout al, BLayout bl, Epilogue ep, GemmRole role,
                        bool bf16, hipStream_t s) {
-    // 32 x 128 tiles where the caller asks for them (fp32, classifier
-    // products); else 128 x 64 tiles: fp32 kernel, one pass over K,
-    // row-contiguous A
-    if (b.tbm != 0 && b.tbm != BM && b.tbm != 32) return hipErrorInvalidValue;
+    // 32 x 128 or 64 x 128 tiles where the caller asks for them (fp32: the
+    // weight gradients of the classifier and the first layer, the
+    // classifier's logits); else 128 x 64 tiles where they spread better:
+    // fp32 kernel, one pass over K, row-contiguous A
+    if (b.tbm != 0 && b.tbm != BM && b.tbm != 32 && b.tbm != 64) return hipErrorInvalidValue;
     const bool small = !bf16 && b.tbm == 32;
+    const bool mid = !bf16 && b.tbm == 64;
     if (small && role != ROLE_CLS_DW && role != ROLE_DW_IN) return hipErrorInvalidValue;
-    const bool nb1 = !small && !bf16 && ep != EPI_PARTIAL && al == A_MK && gemm_narrow_tiles(b);
-    const int tbm = small ? 32 : BM;
+    if (mid && role != ROLE_CLS_FWD) return hipErrorInvalidValue;
+    const bool nb1 =
+        !small && !mid && !bf16 && ep != EPI_PARTIAL && al == A_MK && gemm_narrow_tiles(b);
+    const int tbm = small ? 32 : mid ? 64 : BM;
     const int tbn = nb1 ? 64 : BN;
     int total = 0;
     for (int i = 0; i < b.nprob; ++i) {
@@ -1597,6 +1603,7 @@ hipError_t launch_gemm(GemmBatch& b, ALayout al, BLayout bl, Epilogue ep, GemmRo
     if (al == AL_ && bl == BL_ && ep == EP_ && role == ROLE_) {                       \
         constexpr bool kNarrowOk = EP_ != EPI_PARTIAL && AL_ == A_MK;                 \
         constexpr bool kSmallOk = ROLE_ == ROLE_CLS_DW || ROLE_ == ROLE_DW_IN;      \
+        constexpr bool kMidOk = ROLE_ == ROLE_CLS_FWD;                               \
         if (copies)                                                                  \
             gemm_h16_kernel<AL_, BL_, EP_, ROLE_><<<grid, block, 0, s>>>(b);          \
         else if (bf16 && bvec)                                                       \
@@ -1610,6 +1617,15 @@ hipError_t launch_gemm(GemmBatch& b, ALayout al, BLayout bl, Epilogue ep, GemmRo
                         <<<grid, block, 0, s>>>(b);                                  \
                 else                                                                 \
                     gemm_kernel<AL_, BL_, EP_, false, ROLE_, false, 1, 1, 1>          \
+                        <<<grid, block, 0, s>>>(b);                                  \
+            }                                                                        \
+        } else if (mid) {                                                            \
+            if constexpr (kMidOk) {                                                  \
+                if (bvec)                                                            \
+                    gemm_kernel<AL_, BL_, EP_, true, ROLE_, false, 1, 2, 2>           \
+                        <<<grid, block, 0, s>>>(b);                                  \
+                else                                                                 \
+                    gemm_kernel<AL_, BL_, EP_, false, ROLE_, false, 1, 2, 2>          \
                         <<<grid, block, 0, s>>>(b);                                  \
             }                                                                        \
         } else if (bvec && half_m && EP_ == EPI_PARTIAL && AL_ == A_KM)                 \

@@ -105,10 +105,10 @@ struct GemmBatch {
     GemmProblem p[kMaxProblems];
     int32_t nprob;
     int32_t total_tiles;
-    // tile rows asked for by the caller: 0 (the planner's 128-row tiles) or
-    // 32 (32 x 128 tiles of the fp32 kernel, the weight gradients of the
-    // classifier and of the first layer only; the bf16 kernels always take
-    // 128)
+    // tile rows asked for by the caller: 0 (the planner's 128-row tiles),
+    // 32 (32 x 128 tiles of the fp32 kernel: the weight gradients of the
+    // classifier and of the first layer) or 64 (64 x 128, fp32: the
+    // classifier's logits); the bf16 kernels always take 128
     int32_t tbm;
 };
 

@@ -51,10 +51,12 @@ def test_layer_fwd(n, F, h, bias):
 
 
 # (the weight gradient runs on 32 x 128 tiles: the cases cover a ragged
-# last row tile holding the bias row, two column tiles and a short M)
+# last row tile holding the bias row, two column tiles and a short M; the
+# logits on 64 x 128 tiles, with K slices below 256 row tiles and without
+# them at n = 17000)
 @pytest.mark.parametrize("n,K,C,bias", [(1000, 256, 121, True), (333, 64, 16, False),
                                         (129, 1024, 41, False), (700, 96, 200, True),
-                                        (2000, 36, 7, True)])
+                                        (2000, 36, 7, True), (17000, 64, 10, True)])
 def test_classifier_fwd_loss_bwd(n, K, C, bias):
     need_gpu()
     say("classifier", n, K, C, bias)
