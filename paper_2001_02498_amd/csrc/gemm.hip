@@ -219,23 +219,27 @@ __device__ __forceinline__ void store_tile(const GemmProblem& P, int split, int 
     }
 }
 
-// Epilogue through LDS: the wavefront's 64 x 64 block goes to `stage` (its
-// own 2176 floats of the freed operand buffers) 32 rows at a time, and is
-// read back so that each load and store instruction covers four whole
-// 256-byte row runs (16 lanes per row) instead of 32 rows x 32 bytes.
-// HC: also the bf16 copy. The caller has synchronised the workgroup.
-template <Epilogue EP, bool HC>
+// Epilogue through LDS: the wavefront's 64 x (32 NB) block goes to `stage`
+// (its own 32 x (32 NB + 4) floats of the freed operand buffers) 32 rows at
+// a time, and is read back so that each load and store instruction covers
+// whole row runs of 32 NB floats (8 NB lanes per row) instead of 32 rows x
+// 32 bytes. HC: also the bf16 copy. The caller has synchronised the
+// workgroup.
+template <Epilogue EP, bool HC, int NB = 2>
 __device__ __forceinline__ void store_tile_lds(const GemmProblem& P, int split, int mw, int nw,
                                                int half, int l32, int lane, float* stage,
-                                               const floatx16 (&acc)[2][2]) {
-    constexpr int kSS = 64 + 4;   // staged row stride, floats
+                                               const floatx16 (&acc)[2][NB]) {
+    constexpr int kSS = 32 * NB + 4;   // staged row stride, floats
+    constexpr int kLPR = 8 * NB;       // lanes per staged row
+    constexpr int kRPP = 64 / kLPR;    // rows per read-back pass
+    constexpr int kPass = 32 / kRPP;
     float* C = P.C;
     if constexpr (EP == EPI_PARTIAL) C += (int64_t)split * P.part_stride;
     const bool cvec = ((reinterpret_cast<uintptr_t>(C) | (uintptr_t)(P.ldc * 4)) & 15) == 0;
     const bool mvec =
         EP == EPI_MASK &&
         ((reinterpret_cast<uintptr_t>(P.mask) | (uintptr_t)(P.ldmask * 4)) & 15) == 0;
-    const int c = 4 * (lane & 15);   // this lane's four columns of the block
+    const int c = 4 * (lane % kLPR);   // this lane's four columns of the block
     const int n = nw + c;
     const bool whole = n + 4 <= P.N;
     float bv[4] = {0.f, 0.f, 0.f, 0.f};
@@ -249,19 +253,19 @@ __device__ __forceinline__ void store_tile_lds(const GemmProblem& P, int split, 
     for (int bi = 0; bi < 2; ++bi) {
         // lane (l32, half): row l32, columns 32 bj + 8 g + 4 half .. + 3
 #pragma unroll
-        for (int bj = 0; bj < 2; ++bj)
+        for (int bj = 0; bj < NB; ++bj)
 #pragma unroll
             for (int g = 0; g < 4; ++g)
                 *reinterpret_cast<float4*>(&stage[l32 * kSS + 32 * bj + 8 * g + 4 * half]) =
                     make_float4(acc[bi][bj][4 * g], acc[bi][bj][4 * g + 1],
                                 acc[bi][bj][4 * g + 2], acc[bi][bj][4 * g + 3]);
         __syncthreads();
-        // lane l: rows l / 16 + 4 k of the 32, columns c .. c + 3
-        float v[8][4];
-        float mk[8][4];
+        // lane l: rows l / kLPR + kRPP k of the 32, columns c .. c + 3
+        float v[kPass][4];
+        float mk[kPass][4];
 #pragma unroll
-        for (int k = 0; k < 8; ++k) {
-            const int r = (lane >> 4) + 4 * k;
+        for (int k = 0; k < kPass; ++k) {
+            const int r = lane / kLPR + kRPP * k;
             const float4 q = *reinterpret_cast<const float4*>(&stage[r * kSS + c]);
             v[k][0] = q.x, v[k][1] = q.y, v[k][2] = q.z, v[k][3] = q.w;
             if constexpr (EP == EPI_MASK && HC) {
@@ -296,8 +300,8 @@ __device__ __forceinline__ void store_tile_lds(const GemmProblem& P, int split, 
         }
         __syncthreads();   // the stage is rewritten by the next pass
 #pragma unroll
-        for (int k = 0; k < 8; ++k) {
-            const int m = mw + 32 * bi + (lane >> 4) + 4 * k;
+        for (int k = 0; k < kPass; ++k) {
+            const int m = mw + 32 * bi + lane / kLPR + kRPP * k;
             if (m >= P.M || n >= P.N) continue;
             float* w = v[k];
             if constexpr (EP == EPI_BIAS_RELU || EP == EPI_BIAS) {
@@ -1096,12 +1100,15 @@ __device__ __forceinline__ u32x4 ld16(const __bf16* p) {
     return *reinterpret_cast<const u32x4*>(p);
 }
 
-template <ALayout AL, BLayout BL, Epilogue EP, GemmRole ROLE>
+template <ALayout AL, BLayout BL, Epilogue EP, GemmRole ROLE, int NB = 2>
 __global__ __launch_bounds__(kThreads, 2) void gemm_h16_kernel(GemmBatch batch) {
+    // tile 128 x (64 NB): each wavefront of the 2 x 2 grid owns 2 x NB
+    // accumulators of 32 x 32
+    constexpr int TBN = 64 * NB;
     // [buffer][A | B] operand tiles
     __shared__ __attribute__((aligned(16))) __bf16 hs[2][2][kOp16];
 
-    const TileInfo ti = decode_tile(batch);
+    const TileInfo ti = decode_tile<BM, TBN>(batch);
     const GemmProblem& P = batch.p[ti.pi];
     const int split = ti.split, m0 = ti.m0, n0 = ti.n0;
     const int kbeg = ti.kbeg, kend = ti.kend, nk = ti.nk;
@@ -1120,23 +1127,28 @@ __global__ __launch_bounds__(kThreads, 2) void gemm_h16_kernel(GemmBatch batch) 
     const int ksplitA = P.ksplitA, ksplitB = P.ksplitB;
     const int64_t lda0 = P.hlda0, ldb0 = P.hldb0;
 
-    // Thread t moves kQ16 chunks of 8 bf16 per operand and K step:
+    // Thread t moves kQ16 (A) / kQB chunks (B) of 8 bf16 per K step:
     //   K-contiguous: row t / 4 + 64 q, K offset 8 (t % 4)
-    //   K-major:      K row t / 16 + 16 q, columns 8 (t % 16) .. + 7
+    //   K-major:      K row t / kCPK + kKStep q, columns 8 (t % kCPK) .. + 7
+    //                 (kCPK = 16 chunks per 128 columns, 8 per 64 for B)
     constexpr int kCPR = BK / 8, kRowStep = kThreads / kCPR;
     constexpr int kCPK = BM / 8, kKStep = kThreads / kCPK;
+    constexpr int kQB = BK * TBN / 8 / kThreads;
+    constexpr int kCPKB = TBN / 8, kKStepB = kThreads / kCPKB;
     static_assert(kQ16 * kRowStep == BM && kQ16 * kKStep == BK, "chunks cover the tile");
+    static_assert(kQB * kRowStep == TBN && kQB * kKStepB == BK, "chunks cover the B tile");
     const int rk = 8 * (t % kCPR);
-    const int kq = t / kCPK;
-    const int ac = m0 + 8 * (t % kCPK), bc = n0 + 8 * (t % kCPK);
-    int sofs_a[kQ16], sofs_b[kQ16];   // LDS element offsets of the chunks
+    const int kq = t / kCPK, kqB = t / kCPKB;
+    const int ac = m0 + 8 * (t % kCPK), bc = n0 + 8 * (t % kCPKB);
+    int sofs_a[kQ16], sofs_b[kQB];   // LDS element offsets of the chunks
 #pragma unroll
-    for (int q = 0; q < kQ16; ++q) {
+    for (int q = 0; q < kQ16; ++q)
         sofs_a[q] = AL == A_MK ? (t / kCPR + kRowStep * q) * kRS16 + rk
                                : (kq + kKStep * q) * kKS16 + 8 * (t % kCPK);
+#pragma unroll
+    for (int q = 0; q < kQB; ++q)
         sofs_b[q] = BL == B_NK ? (t / kCPR + kRowStep * q) * kRS16 + rk
-                               : (kq + kKStep * q) * kKS16 + 8 * (t % kCPK);
-    }
+                               : (kqB + kKStepB * q) * kKS16 + 8 * (t % kCPKB);
 
     // Fast tiles: no appended row of ones here and the K concatenation
     // point on a K-step boundary between parts of equal leading dimension;
@@ -1147,7 +1159,7 @@ __global__ __launch_bounds__(kThreads, 2) void gemm_h16_kernel(GemmBatch batch) 
     const bool fast_tile = !(ones && Areal >= m0 && Areal < m0 + BM) &&
                            (AL == A_KM || concat_fast(ksplitA, kbeg, nfull, P.hlda1, lda0)) &&
                            (BL == B_KN || concat_fast(ksplitB, kbeg, nfull, P.hldb1, ldb0));
-    int64_t oa[kQ16], ob[kQ16];
+    int64_t oa[kQ16], ob[kQB];
 #pragma unroll
     for (int q = 0; q < kQ16; ++q) {
         if constexpr (AL == A_MK) {
@@ -1156,15 +1168,18 @@ __global__ __launch_bounds__(kThreads, 2) void gemm_h16_kernel(GemmBatch batch) 
         } else {
             oa[q] = (int64_t)(kq + kKStep * q) * lda0 + (ac < Areal ? ac : 0);
         }
+    }
+#pragma unroll
+    for (int q = 0; q < kQB; ++q) {
         if constexpr (BL == B_NK) {
             const int r = n0 + t / kCPR + kRowStep * q;
             ob[q] = (int64_t)(r < N ? r : 0) * ldb0 + rk;
         } else {
-            ob[q] = (int64_t)(kq + kKStep * q) * ldb0 + (bc < N ? bc : 0);
+            ob[q] = (int64_t)(kqB + kKStepB * q) * ldb0 + (bc < N ? bc : 0);
         }
     }
 
-    HChunk ra[2][kQ16], rb[2][kQ16];
+    HChunk ra[2][kQ16], rb[2][kQB];
     auto gload_full = [&](int set, int k0) {
         const __bf16* sa;
         const __bf16* sb;
@@ -1179,14 +1194,19 @@ __global__ __launch_bounds__(kThreads, 2) void gemm_h16_kernel(GemmBatch batch) 
 #pragma unroll
         for (int q = 0; q < kQ16; ++q) {
             ra[set][q].v = ld16(sa + oa[q]);
-            rb[set][q].v = ld16(sb + ob[q]);
+            if (q < kQB) rb[set][q].v = ld16(sb + ob[q]);
         }
     };
     auto mark_full = [&](int set) {
 #pragma unroll
         for (int q = 0; q < kQ16; ++q) {
-            ra[set][q].valid = rb[set][q].valid = 8;
-            ra[set][q].one = rb[set][q].one = -1;
+            ra[set][q].valid = 8;
+            ra[set][q].one = -1;
+        }
+#pragma unroll
+        for (int q = 0; q < kQB; ++q) {
+            rb[set][q].valid = 8;
+            rb[set][q].one = -1;
         }
     };
     // a K-contiguous chunk (row r, K offset k) of a possibly concatenated operand
@@ -1213,12 +1233,13 @@ __global__ __launch_bounds__(kThreads, 2) void gemm_h16_kernel(GemmBatch batch) 
                 a.one = (ones && krow && Areal - ac >= 0 && Areal - ac < 8) ? Areal - ac : -1;
                 a.v = ld16(a.valid > 0 ? A0 + (int64_t)k * lda0 + ac : A0);
             }
+            if (q >= kQB) continue;
             HChunk& b = rb[set][q];
             if constexpr (BL == B_NK) {
                 row_chunk(b, B0, P.hB1, ldb0, P.hldb1, ksplitB, n0 + t / kCPR + kRowStep * q, N,
                           k0 + rk);
             } else {
-                const int k = k0 + kq + kKStep * q;
+                const int k = k0 + kqB + kKStepB * q;
                 b.valid = (k < kend && bc < N) ? min(8, N - bc) : 0;
                 b.one = -1;
                 b.v = ld16(b.valid > 0 ? B0 + (int64_t)k * ldb0 + bc : B0);
@@ -1231,15 +1252,17 @@ __global__ __launch_bounds__(kThreads, 2) void gemm_h16_kernel(GemmBatch batch) 
 #pragma unroll
         for (int q = 0; q < kQ16; ++q) {
             *reinterpret_cast<u32x4*>(&As[sofs_a[q]]) = full ? ra[set][q].v : finish16(ra[set][q]);
-            *reinterpret_cast<u32x4*>(&Bs[sofs_b[q]]) = full ? rb[set][q].v : finish16(rb[set][q]);
+            if (q < kQB)
+                *reinterpret_cast<u32x4*>(&Bs[sofs_b[q]]) =
+                    full ? rb[set][q].v : finish16(rb[set][q]);
         }
     };
 
-    floatx16 acc[2][2];
+    floatx16 acc[2][NB];
 #pragma unroll
     for (int i = 0; i < 2; ++i)
 #pragma unroll
-        for (int j = 0; j < 2; ++j)
+        for (int j = 0; j < NB; ++j)
 #pragma unroll
             for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
@@ -1256,19 +1279,19 @@ __global__ __launch_bounds__(kThreads, 2) void gemm_h16_kernel(GemmBatch batch) 
             __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4)(S + (k0 + 4) * kKS16 + c));
         return __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
     };
-    bf16x8 fa[2][2], fb[2][2];
+    bf16x8 fa[2][2], fb[2][NB];
     auto frag = [&](int buf, int ks, int fslot) {
 #pragma unroll
         for (int i = 0; i < 2; ++i) {
             fa[fslot][i] = frag_op(hs[buf][0], AL == A_KM, wm * 64 + i * 32, ks);
-            fb[fslot][i] = frag_op(hs[buf][1], BL == B_KN, wn * 64 + i * 32, ks);
+            if (i < NB) fb[fslot][i] = frag_op(hs[buf][1], BL == B_KN, wn * 32 * NB + i * 32, ks);
         }
     };
     auto mfma = [&](int fslot) {
 #pragma unroll
         for (int i = 0; i < 2; ++i)
 #pragma unroll
-            for (int j = 0; j < 2; ++j)
+            for (int j = 0; j < NB; ++j)
                 acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fb[fslot][j], fa[fslot][i],
                                                                     acc[i][j], 0, 0, 0);
     };
@@ -1328,11 +1351,10 @@ __global__ __launch_bounds__(kThreads, 2) void gemm_h16_kernel(GemmBatch batch) 
 
     __syncthreads();   // every fragment read done: the operand buffers become the stage
     constexpr int kStage = 2 * 2 * kOp16 / 2 / 4;   // floats per wavefront
-    static_assert(kStage >= 32 * (64 + 4), "a 32 x 64 block fits each wavefront's share");
+    static_assert(kStage >= 32 * (32 * NB + 4), "a 32 x 32 NB block fits each wavefront's share");
     float* stage = reinterpret_cast<float*>(&hs[0][0][0]) + wave * kStage;
-    store_tile_lds<EP, EP == EPI_BIAS_RELU || EP == EPI_MASK>(P, split, m0 + wm * 64,
-                                                              n0 + wn * 64, half, l32, lane,
-                                                              stage, acc);
+    store_tile_lds<EP, EP == EPI_BIAS_RELU || EP == EPI_MASK, NB>(
+        P, split, m0 + wm * 64, n0 + wn * 32 * NB, half, l32, lane, stage, acc);
 }
 
 // Rounding of fp32 matrices to bf16 copies: one thread per 8 output
@@ -1493,7 +1515,11 @@ void gemm_split_plan_tiles(int64_t tiles, int32_t K, int32_t* splits, int32_t* k
 // CU with a single tile charged 30 % (nothing overlaps its start and end).
 // yelp10k's 10,000 x 1,024 outputs: 632 tiles of 128 x 128 (3 per CU,
 // 2.47 on average) or 1,264 of 128 x 64 (5 per CU, 4.94 on average).
-bool gemm_narrow_tiles(const GemmBatch& b) {
+// The bf16 copies kernel charges its narrow tile 22 % instead (two MFMAs
+// per three fragment reads against four per four, on a kernel whose LDS
+// reads already pace it; fitted to yelp10k's launches), so there it only
+// pays where 128 x 128 tiles leave CUs idle.
+bool gemm_narrow_tiles(const GemmBatch& b, double narrow_eff) {
     constexpr int64_t kCUs = 256;
     int64_t t2 = 0, t1 = 0;
     for (int i = 0; i < b.nprob; ++i) {
@@ -1508,7 +1534,7 @@ bool gemm_narrow_tiles(const GemmBatch& b) {
         const int64_t per_cu = (tiles + kCUs - 1) / kCUs;
         return per_cu * area / eff * (tiles <= kCUs ? 1.3 : 1.0);
     };
-    return cost(t1, 128.0 * 64.0, 0.95) < cost(t2, 128.0 * 128.0, 1.0);
+    return cost(t1, 128.0 * 64.0, narrow_eff) < cost(t2, 128.0 * 128.0, 1.0);
 }
 
 hipError_t launch_gemm(GemmBatch& b, ALayout al, BLayout bl, Epilogue ep, GemmRole role,
@@ -1522,8 +1548,11 @@ hipError_t launch_gemm(GemmBatch& b, ALayout al, BLayout bl, Epilogue ep, GemmRo
     const bool mid = !bf16 && b.tbm == 64;
     if (small && role != ROLE_CLS_DW && role != ROLE_DW_IN) return hipErrorInvalidValue;
     if (mid && role != ROLE_CLS_FWD) return hipErrorInvalidValue;
-    const bool nb1 =
-        !small && !mid && !bf16 && ep != EPI_PARTIAL && al == A_MK && gemm_narrow_tiles(b);
+    // bf16 with operand copies in every problem: the copies kernel
+    bool copies = bf16;
+    for (int i = 0; i < b.nprob; ++i) copies = copies && b.p[i].hA0 && b.p[i].hB0;
+    const bool nb1 = !small && !mid && (!bf16 || copies) && ep != EPI_PARTIAL && al == A_MK &&
+                     gemm_narrow_tiles(b, bf16 ? 0.78 : 0.95);
     const int tbm = small ? 32 : mid ? 64 : BM;
     const int tbn = nb1 ? 64 : BN;
     int total = 0;
@@ -1560,9 +1589,6 @@ hipError_t launch_gemm(GemmBatch& b, ALayout al, BLayout bl, Epilogue ep, GemmRo
     static const int kKinds16[] = {K_GEMM_FWD_BF16, K_GEMM_CLS_BF16, K_GEMM_DX_BF16,
                                    K_GEMM_CLS_DX_BF16, K_GEMM_DW_BF16, K_GEMM_CLS_DW_BF16,
                                    K_GEMM_FWD_IN_BF16, K_GEMM_DW_IN_BF16};
-    // bf16 with operand copies in every problem: the copies kernel
-    bool copies = bf16;
-    for (int i = 0; i < b.nprob; ++i) copies = copies && b.p[i].hA0 && b.p[i].hB0;
     if (copies) {
         auto ok16 = [](const __bf16* q, int64_t ld) {
             return q == nullptr || (((uintptr_t)q & 15) == 0 && (ld & 7) == 0);
@@ -1604,9 +1630,14 @@ hipError_t launch_gemm(GemmBatch& b, ALayout al, BLayout bl, Epilogue ep, GemmRo
         constexpr bool kNarrowOk = EP_ != EPI_PARTIAL && AL_ == A_MK;                 \
         constexpr bool kSmallOk = ROLE_ == ROLE_CLS_DW || ROLE_ == ROLE_DW_IN;      \
         constexpr bool kMidOk = ROLE_ == ROLE_CLS_FWD;                               \
-        if (copies)                                                                  \
-            gemm_h16_kernel<AL_, BL_, EP_, ROLE_><<<grid, block, 0, s>>>(b);          \
-        else if (bf16 && bvec)                                                       \
+        if (copies) {                                                                \
+            if (nb1) {                                                               \
+                if constexpr (kNarrowOk)                                             \
+                    gemm_h16_kernel<AL_, BL_, EP_, ROLE_, 1><<<grid, block, 0, s>>>(b);\
+            } else {                                                                 \
+                gemm_h16_kernel<AL_, BL_, EP_, ROLE_><<<grid, block, 0, s>>>(b);      \
+            }                                                                        \
+        } else if (bf16 && bvec)                                                       \
             gemm_bf16_kernel<AL_, BL_, EP_, true, ROLE_><<<grid, block, 0, s>>>(b);   \
         else if (bf16)                                                               \
             gemm_bf16_kernel<AL_, BL_, EP_, false, ROLE_><<<grid, block, 0, s>>>(b);  \
