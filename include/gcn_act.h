@@ -215,15 +215,16 @@ void gcn_reduced_free(gcn_reduced_t r);
  * the pair counts of Algorithm 1 per vertex in LDS counters; the pairs
  * above theta sorted by (count descending, smaller id, larger id); the
  * greedy scan of Algorithm 2 under the max_aux cap; the list rewrite of
- * Algorithm 3, one wavefront per list. Synchronous: uploads the lists,
+ * Algorithm 3, one workgroup per list. Synchronous: uploads the lists,
  * runs on `stream` (synchronising it twice per round to size the next
  * launches), downloads the result, and returns.
  *   ws, ws_bytes  device workspace, 256-byte aligned, of at least
  *                 gcn_redundancy_reduce_device_bytes(g, params) bytes;
  *                 caller-owned, reusable once the call returned
  *   num_threads   ignored
- * Limits: fewer than 65536 vertex ids (original plus pair sums) in any
- * round (GCN_E_UNSUPPORTED beyond).
+ * Limits: fewer than 524288 (2^19) vertex ids (original plus pair sums)
+ * in any round, and pair counts below 65536 (GCN_E_UNSUPPORTED beyond;
+ * the host reduction has neither limit).
  * Errors: GCN_E_INVALID_ARG (as gcn_redundancy_reduce, or a NULL /
  * misaligned workspace); GCN_E_WORKSPACE; GCN_E_UNSUPPORTED; GCN_E_HIP;
  * GCN_E_INTERNAL (a device-side capacity or range check failed); GCN_E_OOM.

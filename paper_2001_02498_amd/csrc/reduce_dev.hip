@@ -4,9 +4,9 @@
 // One round:
 //   Algorithm 1  transposed index of the lists (which lists hold each id and
 //                where), then one workgroup per id x counts, in 16-bit LDS
-//                counters, every larger id y that follows x in a list holding
-//                x; pairs above the threshold leave as 64-bit keys ordered
-//                by (weight descending, x, y).
+//                counters (65,536 ids per pass), every larger id y that
+//                follows x in a list holding x; pairs above the threshold
+//                leave as 64-bit keys ordered by (weight descending, x, y).
 //   Algorithm 2  the keys are radix-sorted (rocPRIM); one workgroup scans
 //                them in blocks, drops pairs with a used endpoint in
 //                parallel and takes the rest in key order with one thread:
@@ -40,7 +40,11 @@ constexpr int kGreedyThreads = 1024;
 constexpr int kGreedyPer = 4;                         // keys per thread per block
 constexpr int kGreedyBurst = 256;                     // survivors taken between refilters
 constexpr int kGreedyBlock = kGreedyThreads * kGreedyPer;
-constexpr int kMaxIds = 65536;                        // 16-bit counters, 20-bit key fields
+// ids per reduction: the greedy scan's used set fills at most 64 KB of LDS
+// (beside its 64 KB of survivor buffers); pair keys hold 20-bit ids
+constexpr int kMaxIds = 1 << 19;
+// ids counted per pass of Algorithm 1: 16-bit counters in 128 KB of LDS
+constexpr int kCountWindow = 65536;
 
 // Device-side counters of one round (and the error flag).
 struct RoundCounters {
@@ -57,7 +61,8 @@ struct DevState {
     long long naux;             // pairs taken in all rounds so far
     int done;                   // a round took no pair, or the budget is spent
     int error;                  // 1: candidate capacity, 2: id out of range,
-                                // 3: ids reach the 16-bit counter range
+                                // 3: ids reach kMaxIds, or a pair count
+                                //    exceeds 16 bits
     RoundCounters round[GCN_MAX_ROUNDS];
 };
 
@@ -158,14 +163,31 @@ __global__ __launch_bounds__(kBlock) void tfill_kernel(int n, const int32_t* __r
 }
 
 // One workgroup per id x (grid-stride): counts, for every y > x, the lists
-// holding both, in 16-bit counters packed two per LDS word (a count never
-// reaches 2^16: it is at most the number of lists); pairs whose count
-// exceeds theta (and 1: weight-1 pairs are no edges of G_a) are emitted.
-// The parts of the lists after x are staged (start, prefix of lengths) in
-// LDS, kCountStage lists at a time, and all threads sweep their
-// concatenation, so a hub with thousands of lists keeps every lane busy.
+// holding both, in 16-bit counters packed two per LDS word; pairs whose
+// count exceeds theta (and 1: weight-1 pairs are no edges of G_a) are
+// emitted. The ids are counted in windows of kCountWindow (one window when
+// there are fewer ids); a window takes, by binary search, the stretch of
+// every (sorted) list tail that falls in it. The parts of the lists after x
+// are staged (start, prefix of lengths) in LDS, kCountStage lists at a
+// time, and all threads sweep their concatenation, so a hub with thousands
+// of lists keeps every lane busy. A count is at most the number of lists:
+// with 65,535 lists or more a counter that would pass 16 bits is reported
+// (error 3) instead of wrapping.
 constexpr int kCountThreads = 512;
 constexpr int kCountStage = 1024;
+
+// first index in [b, e) of the ascending array a whose value is >= v
+__device__ __forceinline__ int lower_bound_dev(const int32_t* __restrict__ a, int b, int e,
+                                               int v) {
+    while (b < e) {
+        const int mid = (b + e) >> 1;
+        if (a[mid] < v)
+            b = mid + 1;
+        else
+            e = mid;
+    }
+    return b;
+}
 
 __global__ __launch_bounds__(kCountThreads) void count_pairs_kernel(
     int n, int theta, const int32_t* __restrict__ rowptr, const int32_t* __restrict__ col,
@@ -178,114 +200,134 @@ __global__ __launch_bounds__(kCountThreads) void count_pairs_kernel(
     __shared__ int32_t s_wave[kCountThreads / 64];
     if (st->done) return;
     const int ncols = n + (int)st->naux;
-    if (ncols >= kMaxIds) {   // pair keys hold 16-bit ids
+    if (ncols >= kMaxIds) {   // pair keys and the greedy scan's used set
         if (threadIdx.x == 0 && blockIdx.x == 0) st->error = 3;
         return;
     }
     RoundCounters* rc = &st->round[round];
-    const int nw = (ncols + 1) / 2;
+    const bool windowed = ncols > kCountWindow;
+    const int win = windowed ? kCountWindow : ncols;
+    const bool check = n >= 65535;   // counts can reach 2^16 only with that many lists
     const int t = threadIdx.x, lane = t % 64, wave = t / 64;
-    for (int i = t; i < nw; i += kCountThreads) cnt[i] = 0;
+    for (int i = t; i < (win + 1) / 2; i += kCountThreads) cnt[i] = 0;
     __syncthreads();
     for (int x = blockIdx.x; x < ncols; x += gridDim.x) {
         const int tb = tptr[x], te = tptr[x + 1];
         if (te - tb < 2) continue;   // uniform: x in fewer than two lists
-        for (int kb = tb; kb < te; kb += kCountStage) {
-            const int m = min(kCountStage, te - kb);
-            // thread t stages lists 2t, 2t + 1 of this pass
-            int len[2], sum = 0;
-            for (int j = 0; j < 2; ++j) {
-                const int i = 2 * t + j;
-                len[j] = 0;
-                if (i < m) {
-                    const int k = kb + i, w = tlist[k];
-                    const int st = rowptr[w] + tpos[k] + 1;
-                    s_start[i] = st;
-                    len[j] = rowptr[w + 1] - st;
+        // the windows [y0, y0 + win) holding ids above x
+        for (int y0 = windowed ? (x + 1) / win * win : 0; y0 < ncols; y0 += win) {
+            const int y1 = min(ncols, y0 + win);
+            const int nw = (y1 - y0 + 1) / 2;
+            for (int kb = tb; kb < te; kb += kCountStage) {
+                const int m = min(kCountStage, te - kb);
+                // thread t stages lists 2t, 2t + 1 of this pass
+                int len[2], sum = 0;
+                for (int j = 0; j < 2; ++j) {
+                    const int i = 2 * t + j;
+                    len[j] = 0;
+                    if (i < m) {
+                        const int k = kb + i, w = tlist[k];
+                        int b = rowptr[w] + tpos[k] + 1, e = rowptr[w + 1];
+                        if (windowed) {
+                            b = lower_bound_dev(col, b, e, y0);
+                            e = lower_bound_dev(col, b, e, y1);
+                        }
+                        s_start[i] = b;
+                        len[j] = e - b;
+                    }
+                    sum += len[j];
                 }
-                sum += len[j];
+                int incl = sum;
+                for (int off = 1; off < 64; off <<= 1) {
+                    const int v = __shfl_up(incl, off);
+                    if (lane >= off) incl += v;
+                }
+                if (lane == 63) s_wave[wave] = incl;
+                __syncthreads();
+                int before = 0;
+                for (int v = 0; v < wave; ++v) before += s_wave[v];
+                int run = before + incl - sum;
+                for (int j = 0; j < 2; ++j) {
+                    const int i = 2 * t + j;
+                    if (i < m) s_off[i] = run;
+                    run += len[j];
+                }
+                if (t == kCountThreads - 1) s_off[m] = run;   // total (run after the last thread)
+                __syncthreads();
+                const int total = s_off[m];
+                int k = 0;
+                for (int v = t; v < total; v += kCountThreads) {
+                    // the staged list holding visit v: the last k with s_off[k] <= v
+                    int lo = k, hi = m - 1;
+                    while (lo < hi) {
+                        const int mid = (lo + hi + 1) >> 1;
+                        if (s_off[mid] <= v)
+                            lo = mid;
+                        else
+                            hi = mid - 1;
+                    }
+                    k = lo;
+                    const int y = col[s_start[k] + (v - s_off[k])] - y0;
+                    if ((unsigned)y < (unsigned)(y1 - y0)) {
+                        const int sh = (y & 1) * 16;
+                        if (check) {
+                            const uint32_t old = atomicAdd(&cnt[y >> 1], 1u << sh);
+                            if (((old >> sh) & 0xFFFFu) == 0xFFFFu) st->error = 3;
+                        } else {
+                            atomicAdd(&cnt[y >> 1], 1u << sh);
+                        }
+                    }
+                }
+                __syncthreads();
             }
-            int incl = sum;
+            // Emit the pairs of x in the window (counters of y > x, from
+            // the word holding x + 1): count them, reserve one range of
+            // slots for the workgroup, then write each thread's pairs at
+            // its prefix and clear.
+            const int w0 = x + 1 > y0 ? (x + 1 - y0) >> 1 : 0;
+            auto emits = [&](uint32_t v, int wd, int h) {
+                const int y = y0 + 2 * wd + h;
+                const uint32_t c = (v >> (16 * h)) & 0xFFFFu;
+                return y > x && (int)c > theta && c >= 2;
+            };
+            int mine = 0;
+            for (int wd = w0 + t; wd < nw; wd += kCountThreads) {
+                const uint32_t v = cnt[wd];
+                if (v) mine += emits(v, wd, 0) + emits(v, wd, 1);
+            }
+            int incl = mine;
             for (int off = 1; off < 64; off <<= 1) {
                 const int v = __shfl_up(incl, off);
                 if (lane >= off) incl += v;
             }
             if (lane == 63) s_wave[wave] = incl;
             __syncthreads();
+            __shared__ unsigned long long s_base;
+            if (t == 0) {
+                int tot = 0;
+                for (int v = 0; v < kCountThreads / 64; ++v) tot += s_wave[v];
+                s_base = tot ? atomicAdd(&rc->ncand, (unsigned long long)tot) : 0ull;
+            }
+            __syncthreads();
             int before = 0;
             for (int v = 0; v < wave; ++v) before += s_wave[v];
-            int run = before + incl - sum;
-            for (int j = 0; j < 2; ++j) {
-                const int i = 2 * t + j;
-                if (i < m) s_off[i] = run;
-                run += len[j];
-            }
-            if (t == kCountThreads - 1) s_off[m] = run;   // total (run after the last thread)
-            __syncthreads();
-            const int total = s_off[m];
-            int k = 0;
-            for (int v = t; v < total; v += kCountThreads) {
-                // the staged list holding visit v: the last k with s_off[k] <= v
-                int lo = k, hi = m - 1;
-                while (lo < hi) {
-                    const int mid = (lo + hi + 1) >> 1;
-                    if (s_off[mid] <= v)
-                        lo = mid;
+            unsigned long long slot = s_base + (unsigned long long)(before + incl - mine);
+            for (int wd = w0 + t; wd < nw; wd += kCountThreads) {
+                const uint32_t v = cnt[wd];
+                if (!v) continue;
+                cnt[wd] = 0;
+                for (int h = 0; h < 2; ++h) {
+                    if (!emits(v, wd, h)) continue;
+                    if ((int64_t)slot < cap)
+                        cand[slot] = cand_key((v >> (16 * h)) & 0xFFFFu, (uint32_t)x,
+                                              (uint32_t)(y0 + 2 * wd + h));
                     else
-                        hi = mid - 1;
+                        st->error = 1;
+                    ++slot;
                 }
-                k = lo;
-                const int y = col[s_start[k] + (v - s_off[k])];
-                if (y < ncols) atomicAdd(&cnt[y >> 1], 1u << ((y & 1) * 16));
             }
             __syncthreads();
         }
-        // Emit the pairs of x (counters of y > x, from the word holding
-        // x + 1): count them, reserve one range of slots for the workgroup,
-        // then write each thread's pairs at its prefix and clear.
-        const int w0 = (x + 1) >> 1;
-        auto emits = [&](uint32_t v, int wd, int h) {
-            const int y = 2 * wd + h;
-            const uint32_t c = (v >> (16 * h)) & 0xFFFFu;
-            return y > x && (int)c > theta && c >= 2;
-        };
-        int mine = 0;
-        for (int wd = w0 + t; wd < nw; wd += kCountThreads) {
-            const uint32_t v = cnt[wd];
-            if (v) mine += emits(v, wd, 0) + emits(v, wd, 1);
-        }
-        int incl = mine;
-        for (int off = 1; off < 64; off <<= 1) {
-            const int v = __shfl_up(incl, off);
-            if (lane >= off) incl += v;
-        }
-        if (lane == 63) s_wave[wave] = incl;
-        __syncthreads();
-        __shared__ unsigned long long s_base;
-        if (t == 0) {
-            int tot = 0;
-            for (int v = 0; v < kCountThreads / 64; ++v) tot += s_wave[v];
-            s_base = tot ? atomicAdd(&rc->ncand, (unsigned long long)tot) : 0ull;
-        }
-        __syncthreads();
-        int before = 0;
-        for (int v = 0; v < wave; ++v) before += s_wave[v];
-        unsigned long long slot = s_base + (unsigned long long)(before + incl - mine);
-        for (int wd = w0 + t; wd < nw; wd += kCountThreads) {
-            const uint32_t v = cnt[wd];
-            if (!v) continue;
-            cnt[wd] = 0;
-            for (int h = 0; h < 2; ++h) {
-                if (!emits(v, wd, h)) continue;
-                if ((int64_t)slot < cap)
-                    cand[slot] = cand_key((v >> (16 * h)) & 0xFFFFu, (uint32_t)x,
-                                          (uint32_t)(2 * wd + h));
-                else
-                    st->error = 1;
-                ++slot;
-            }
-        }
-        __syncthreads();
     }
 }
 
@@ -314,7 +356,7 @@ __device__ __forceinline__ int lanes_below(uint64_t m) {
 __global__ __launch_bounds__(kGreedyThreads) void greedy_kernel(
     const uint64_t* __restrict__ keys, int64_t nc, int n, int64_t max_aux, int64_t pairs_cap,
     int32_t* __restrict__ all_pairs, DevState* st, int round) {
-    __shared__ uint32_t used[kMaxIds / 32];
+    extern __shared__ uint32_t used[];   // (ncols + 31) / 32 words
     __shared__ uint64_t surv[2][kGreedyBlock];
     __shared__ int32_t wave_sum[kGreedyThreads / 64];
     __shared__ int stop;
@@ -337,13 +379,13 @@ __global__ __launch_bounds__(kGreedyThreads) void greedy_kernel(
     auto is_used = [&](uint32_t v) { return (used[v >> 5] >> (v & 31)) & 1u; };
     // both endpoints free (no short-circuit: no branch, both reads in flight)
     auto free_pair = [&](uint64_t key) {
-        const uint32_t x = (uint32_t)(key >> 20) & 0xFFFFu, y = (uint32_t)key & 0xFFFFu;
+        const uint32_t x = (uint32_t)(key >> 20) & 0xFFFFFu, y = (uint32_t)key & 0xFFFFFu;
         return (is_used(x) | is_used(y)) == 0u;
     };
     // Keys of the next block are loaded while this one is filtered and
-    // taken. Loads are unconditional (clamped index); a key past nc is
-    // replaced by all ones only when its block is used, so nothing waits
-    // for a load before then.
+    // taken. Loads are unconditional (clamped index, so every key read is a
+    // real one with ids below ncols); a slot past nc is dropped by its
+    // index only, so nothing waits for a load before its block is used.
     auto load_raw = [&](int64_t i) { return keys[i < nc ? i : nc - 1]; };
     uint64_t k_raw[kGreedyPer];
 #pragma unroll
@@ -354,15 +396,12 @@ __global__ __launch_bounds__(kGreedyThreads) void greedy_kernel(
 #pragma unroll
         for (int j = 0; j < kGreedyPer; ++j) {
             const int64_t i = base + (int64_t)t * kGreedyPer + j;
-            k[j] = i < nc ? k_raw[j] : ~0ull;
+            k[j] = k_raw[j];
+            live[j] = i < nc;
             k_raw[j] = load_raw(i + kGreedyBlock);
         }
 #pragma unroll
-        for (int j = 0; j < kGreedyPer; ++j) {
-            // keys past nc are all ones: their ids exceed ncols
-            const uint32_t x = (uint32_t)(k[j] >> 20) & 0xFFFFFu, y = (uint32_t)k[j] & 0xFFFFFu;
-            live[j] = (x < (uint32_t)ncols) & (y < (uint32_t)ncols) & free_pair(k[j]);
-        }
+        for (int j = 0; j < kGreedyPer; ++j) live[j] = live[j] & free_pair(k[j]);
         // survivors keep their order (thread-major, then j): the prefix
         // inside a wave from one ballot per key slot, across waves from the
         // per-wave totals
@@ -775,7 +814,7 @@ int redundancy_reduce_device(const int32_t* rowptr_h, const int32_t* col_h, int6
                "cursor");
         tfill_kernel<<<waves_grid(n), kBlock, 0, s>>>((int)n, rowptr[cur], col[cur], I(dp.tcur),
                                                        I(dp.tlist), I(dp.tpos), dst);
-        const size_t lds = 4 * (size_t)((std::min<int64_t>(nc_ub, kMaxIds) + 1) / 2);
+        const size_t lds = 4 * (size_t)((std::min<int64_t>(nc_ub, kCountWindow) + 1) / 2);
         if (lds > 48 * 1024)
             GCN_DR(hipFuncSetAttribute((const void*)count_pairs_kernel,
                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds),
@@ -793,7 +832,8 @@ int redundancy_reduce_device(const int32_t* rowptr_h, const int32_t* col_h, int6
             set_error("gcn_redundancy_reduce_device: %s in round %d",
                       hs.error == 1   ? "candidate capacity exceeded"
                       : hs.error == 2 ? "list id out of range"
-                                      : "ids reach the device reduction's 16-bit range",
+                                      : "ids reach the device reduction's range (2^19) or a "
+                                        "pair count exceeds 16 bits",
                       round + 1);
             return hs.error == 3 ? GCN_E_UNSUPPORTED : GCN_E_INTERNAL;
         }
@@ -806,8 +846,14 @@ int redundancy_reduce_device(const int32_t* rowptr_h, const int32_t* col_h, int6
         GCN_DR(rocprim::radix_sort_keys(base + dp.sort, tmp, keys_in, keys_out, (unsigned)nc, 0,
                                         56, s),
                "candidate sort");
-        greedy_kernel<<<1, kGreedyThreads, 0, s>>>(keys_out, nc, (int)n, p->max_aux,
-                                                   dp.pairs_cap, pairs, dst, round);
+        // the used set: one bit per id issued so far
+        const size_t used = 4 * (size_t)((n + naux_known + 31) / 32);
+        if (used > 48 * 1024)
+            GCN_DR(hipFuncSetAttribute((const void*)greedy_kernel,
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)used),
+                   "matching LDS");
+        greedy_kernel<<<1, kGreedyThreads, used, s>>>(keys_out, nc, (int)n, p->max_aux,
+                                                      dp.pairs_cap, pairs, dst, round);
         GCN_DR(hipGetLastError(), "matching");
         // Algorithm 3: rewrite every list (a round that took no pair
         // copies the lists unchanged)
@@ -816,6 +862,14 @@ int redundancy_reduce_device(const int32_t* rowptr_h, const int32_t* col_h, int6
                               dp.pairs_cap - naux_known);
         const int nxt = cur ^ 1;
         const size_t bits = 4 * (size_t)((std::min<int64_t>(n + naux_known, kMaxIds) + 31) / 32);
+        if (bits > 48 * 1024) {
+            GCN_DR(hipFuncSetAttribute((const void*)rewrite_count_kernel,
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)bits),
+                   "rewrite LDS");
+            GCN_DR(hipFuncSetAttribute((const void*)rewrite_fill_kernel,
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)bits),
+                   "rewrite LDS");
+        }
         set_partner_kernel<<<items_grid(budget_ub), kBlock, 0, s>>>(pairs, (int)n, dst, round,
                                                                     I(dp.partner), I(dp.newid), 0);
         rewrite_count_kernel<<<(unsigned)n, kRowThreads, bits, s>>>(

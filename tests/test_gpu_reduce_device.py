@@ -109,3 +109,27 @@ def test_device_reduction_edges_and_errors():
     with pytest.raises(gcn.GcnError) as ei:
         gcn.redundancy_reduce_device(g, gcn.alloc_ws(need // 2 // 256 * 256 or 256))
     assert ei.value.code == gcn.E_WORKSPACE
+
+
+def test_device_reduction_beyond_16bit_ids():
+    """More ids than 16-bit counters cover: Algorithm 1 counts in windows of
+    65,536 ids (from the first round at n = 70,000, with the 16-bit counter
+    overflow check on; from the second round at n = 65,400, whose first
+    round's pair sums push the ids past 65,536)."""
+    need_gpu()
+    from paper_2001_02498_amd import gcn
+    for n, oracle in ((70000, True), (65400, False)):
+        wl = synth.small_workload(n, 4, 2, 8, 8, 4, synth.SOFTMAX_CE, (n,))
+        inp = synth.make_inputs(wl)
+        kw = dict(theta=2, max_rounds=5)
+        say("device reduction", n, len(inp.src), "oracle", oracle)
+        if oracle:
+            host, dev = _both(gcn, n, inp.src, inp.dst, **kw)
+        else:
+            g = gcn.subgraph_build(n, inp.src, inp.dst)
+            host = gcn.redundancy_reduce(g, **kw).info()
+            ws = gcn.alloc_ws(gcn.redundancy_reduce_device_bytes(g, **kw))
+            dev = gcn.redundancy_reduce_device(g, ws, **kw).info()
+        _same(host, dev)
+        assert n + dev["round_offsets"][1] > 65536 and dev["rounds"] >= 2
+

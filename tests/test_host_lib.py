@@ -318,3 +318,16 @@ def test_reduction_large_theta_matches_oracle(theta):
     red = gcn.redundancy_reduce(gcn.subgraph_build(52, src, dst), theta=theta, max_rounds=3)
     info = _compare_reduction(red, ora)
     assert info["naux"] == (1 if theta < 50 else 0)
+
+
+def test_reduction_32bit_counters_matches_oracle():
+    # 70,000 lists: the host counts pairs in 32-bit counters (16-bit ones
+    # serve fewer than 65,536 lists); bit-exact with the oracle over 5 rounds
+    wl = synth.small_workload(70000, 4, 2, 8, 8, 4, synth.SOFTMAX_CE, (70000,))
+    inp = synth.make_inputs(wl)
+    rp, cl = gr.subgraph_build(wl.n, inp.src, inp.dst)
+    ora = rd.reduce(rp, cl, theta=2, max_rounds=5)
+    red = gcn.redundancy_reduce(gcn.subgraph_build(wl.n, inp.src, inp.dst), theta=2,
+                                max_rounds=5)
+    info = _compare_reduction(red, ora)
+    assert info["naux"] > 0 and info["rounds"] >= 2
