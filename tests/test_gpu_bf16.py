@@ -171,6 +171,18 @@ def test_step_bf16_copies_ragged(L, loss, bias):
     check_step(run, tol=BF16_TOL)
 
 
+def test_step_bf16_copies_large_n():
+    """n = 25,000: the logits' 196 row tiles need no K slices, so the bf16
+    copies kernel writes them with its bias epilogue on 128 x 64 tiles (the
+    other steps here split K for the logits)."""
+    need_gpu()
+    from paper_2001_02498_amd import gcn
+    wl = synth.small_workload(25000, 6, 2, 24, 16, 10, synth.SOFTMAX_CE, (25000,))
+    run = StepRun(wl, bias=True, precision=gcn.PREC_BF16).run()
+    assert run.layout.ah_bytes == 2
+    check_step(run, tol=BF16_TOL)
+
+
 def test_step_bf16_without_copies():
     """h not a multiple of 8: the step's products round fp32 operands."""
     need_gpu()
