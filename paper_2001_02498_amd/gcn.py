@@ -19,6 +19,16 @@ LIB_PATH = os.path.join(_HERE, "_lib", "libgcnact.so")
 if not os.path.exists(LIB_PATH):
     raise ImportError(f"{LIB_PATH} is missing: build it with "
                       "`python -m paper_2001_02498_amd.build`")
+# One HIP runtime per process: torch's. torch's libraries name their bundled
+# runtime `libamdhip64.so` while the library names `libamdhip64.so.7`; with
+# torch loaded first the library's dependency resolves to torch's copy (same
+# soname), but loaded first itself it maps the system copy and torch then
+# maps a second runtime, which cannot open the GPU the first holds (and
+# torch's stream handles would belong to the other runtime).
+try:
+    import torch  # noqa: F401
+except ImportError:
+    pass
 _lib = C.CDLL(LIB_PATH)
 
 OK = 0

@@ -23,6 +23,26 @@ def _declared_symbols():
     return sorted(set(re.findall(r"\b(gcn_[a-z_]+)\s*\(", txt)))
 
 
+def test_one_hip_runtime_per_process():
+    """Importing the binding before torch must not leave two HIP runtimes
+    mapped (the library's and torch's bundled one): the second cannot open
+    the GPU. Checked in a fresh interpreter from its memory map."""
+    import subprocess
+    import sys
+    code = ("import paper_2001_02498_amd.gcn, torch\n"
+            "paths = set()\n"
+            "for line in open('/proc/self/maps'):\n"
+            "    f = line.split()[-1]\n"
+            "    if 'libamdhip64' in f:\n"
+            "        paths.add(f)\n"
+            "print(len(paths), sorted(paths))\n")
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    r = subprocess.run([sys.executable, "-c", code], capture_output=True, text=True,
+                       timeout=600, cwd=root)
+    assert r.returncode == 0, r.stderr[-2000:]
+    assert r.stdout.split()[0] == "1", r.stdout
+
+
 def test_library_exports_every_declared_symbol():
     lib = ctypes.CDLL(gcn.LIB_PATH)
     syms = _declared_symbols()
