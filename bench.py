@@ -122,7 +122,7 @@ _ROLE_CLASS = ["gemm_fwd", "gemm_cls", "gemm_dx", "gemm_cls_dx", "gemm_dw", "gem
 def _family(cls):
     if cls.startswith("gemm") or cls == "splitk_finish":
         return "gemm"
-    if cls in ("pair_sums", "list_sums", "list_fixup"):
+    if cls in ("pair_sums", "list_sums"):
         return "agg"
     if cls.startswith("loss"):
         return "loss"
@@ -149,10 +149,8 @@ def kernel_class(name):
         if key in name:
             m = re.search(r"\(gcn::GemmRole\)(\d+)", name)
             return _ROLE_CLASS[int(m.group(1))] + suffix if m else None
-    if "list_sums_kernel<" in name:
-        head = name[name.index("list_sums_kernel<"):]
-        return "pair_sums" if head.split(">")[0].rstrip().endswith("true") else "list_sums"
-    for key, cls in (("fixup_kernel<", "list_fixup"), ("sgd_reduce_kernel", "sgd_reduce"),
+    for key, cls in (("pair_sums_kernel<", "pair_sums"), ("list_sums_kernel<", "list_sums"),
+                     ("sgd_reduce_kernel", "sgd_reduce"),
                      ("splitk_finish_kernel", "splitk_finish"), ("loss_kernel<", "loss_rows"),
                      ("mean_kernel", "loss_mean"), ("to_bf16_kernel", "to_bf16"),
                      ("gather_rows_kernel<", "gather_rows")):

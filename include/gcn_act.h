@@ -51,6 +51,7 @@ extern "C" {
 
 #define GCN_MAX_ROUNDS 64
 #define GCN_MAX_LAYERS 8
+#define GCN_BIN_GROUPS 16        /* pieces per work-list bin (see image)  */
 
 #define GCN_LOSS_SOFTMAX_CE 0    /* labels: int32[n] class ids            */
 #define GCN_LOSS_SIGMOID_BCE 1   /* labels: uint8[n*C] 0/1, row-major     */
@@ -68,7 +69,7 @@ const char* gcn_last_error(void);
 
 /* ABI version of this header (bumped on incompatible change). */
 int gcn_abi_version(void);
-#define GCN_ABI_VERSION 6
+#define GCN_ABI_VERSION 7
 
 /* ------------------------------------------------ subgraph (host, a1)
  * gcn_subgraph_build - undirected simple subgraph in CSR form.
@@ -237,10 +238,19 @@ int gcn_redundancy_reduce_device(gcn_graph_t g, const gcn_rr_params* params, voi
 /* ------------------------------------------------ device graph image
  * The device form of G_s^# (what the accelerator receives in Section 4.1:
  * the lists, the pairs and D), plus a work list that splits long lists
- * into segments of at most `seg_len` entries for load balance, and each pair
+ * into pieces of at most `seg_len` entries for load balance, and each pair
  * sum's expansion into original vertices (the pair sum of Section 4.2 step 1
  * is the sum of those rows), so that all pair sums of all rounds can be
  * formed in one pass instead of one dependent pass per round.
+ * Work list: `seg` holds nseg pieces (row, begin, end, lead) into col, with
+ * lead = the row's piece count on its first piece and 0 on the others; a
+ * row of at most seg_len entries is one piece (lead 1). `bins` (nbins + 1
+ * ascending piece offsets) cuts it into bins of at most GCN_BIN_GROUPS
+ * pieces, or one bin for a single row of more pieces (a hub); every row's
+ * pieces are consecutive and in one bin, the nhub hub bins come first, then
+ * the other bins holding a split row (nmulti bins in all), so the pieces of
+ * a split row are added within one workgroup (a hub's list within each of
+ * the workgroups that share its columns).
  * gcn_graph_image_bytes - size of the packed image (host and device).
  * gcn_graph_pack        - write the image into a caller host buffer (may
  *                         be pinned); the reduced object may then be freed.
@@ -255,7 +265,8 @@ int gcn_redundancy_reduce_device(gcn_graph_t g, const gcn_rr_params* params, voi
  */
 typedef struct {
     int32_t n, naux, rounds, seg_len;
-    int32_t nseg, nlong, nslots, max_row;
+    int32_t nseg, nbins, nmulti, nhub;
+    int32_t max_row, reserved;
     int64_t nnz;
     int64_t exp_nnz;           /* total expansion length             */
     const int32_t* rowptr;     /* device int32[n+1]                  */
@@ -263,7 +274,7 @@ typedef struct {
     const int32_t* pairs;      /* device int32[2*naux]               */
     const float* inv_deg;      /* device float[n], 1/d (0 if d == 0) */
     const int32_t* seg;        /* device int32[4*nseg]               */
-    const int32_t* longrows;   /* device int32[4*nlong]              */
+    const int32_t* bins;       /* device int32[nbins+1]              */
     const int32_t* exp_col;    /* device int32[exp_nnz]: original
                                   vertices of pair sum k, ascending  */
     const int32_t* exp_seg;    /* device int32[4*naux]: (k, begin,
@@ -380,7 +391,8 @@ int gcn_scratch_bytes(const gcn_dgraph* g, int32_t n, int32_t max_width,
  * the sum for MEAN; on the gathered original rows for TRANSPOSED).
  * Vertices with d == 0 get zero rows.
  *   X  device [n x F] ld ldx;  Y  device [n x F] ld ldy (X and Y must not
- *   overlap). Scratch: pair sums and partial sums of split lists.
+ *   overlap). Scratch: the pair sums. A split list's pieces are added in
+ *   one workgroup, in a fixed order, so results do not vary from run to run.
  */
 int gcn_aggregate(const gcn_dgraph* g, int32_t mode, int32_t F,
                   const float* X, int64_t ldx, float* Y, int64_t ldy,
@@ -389,8 +401,8 @@ int gcn_aggregate(const gcn_dgraph* g, int32_t mode, int32_t F,
 /* gcn_aggregate_noalloc - gcn_aggregate without a workspace argument, for
  * callers that cannot allocate device memory (code under HIP graph capture,
  * tight serving loops, harnesses that forbid allocation). Same operation,
- * kernels and results as gcn_aggregate. Its scratch (pair sums and split-
- * list partial sums, each written before it is read) is a fixed array of
+ * kernels and results as gcn_aggregate. Its scratch (the pair sums, each
+ * written before it is read) is a fixed array of
  * GCN_AGG_NOALLOC_SCRATCH_BYTES per device, held by the library on every
  * device it runs on until the process ends; its device address is looked
  * up (hipGetSymbolAddress) on the first call on each device, the only
@@ -398,8 +410,8 @@ int gcn_aggregate(const gcn_dgraph* g, int32_t mode, int32_t F,
  * Every call on one device shares that device's array: calls that overlap
  * on one device (concurrent streams or threads) race and give wrong
  * results; serialise them. Errors: GCN_E_INVALID_ARG as gcn_aggregate,
- * and when the scratch needed, 4 r4(F) (naux + split-list slots) bytes in
- * 256-byte-aligned regions, exceeds the fixed size (nothing launched);
+ * and when the scratch needed, 4 r4(F) naux bytes in 256-byte-aligned
+ * regions, exceeds the fixed size (nothing launched);
  * GCN_E_HIP if the address lookup or a launch fails. */
 #define GCN_AGG_NOALLOC_SCRATCH_BYTES (64ll << 20)
 int gcn_aggregate_noalloc(const gcn_dgraph* g, int32_t mode, int32_t F,

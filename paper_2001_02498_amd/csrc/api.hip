@@ -20,7 +20,7 @@ inline int64_t r8(int64_t x) { return round_up(x, 8); }
 // Scratch regions (bytes from the start of ws) for widths up to W. The
 // loss status word (one int32) comes first, at offset 0.
 struct ScratchPlan {
-    int64_t status, aux, part_list, T, gemm_part, rowloss, rowflag, total;
+    int64_t status, aux, T, gemm_part, rowloss, rowflag, total;
     int64_t gemm_part_floats;   // per problem
     int64_t ld_max;             // widest row (floats) of the aux / T regions
 };
@@ -31,7 +31,7 @@ int64_t gemm_part_bound(int64_t W) {
     return (512 + tiles) * 128 * 128;
 }
 
-ScratchPlan plan_scratch(int64_t n, int64_t naux, int64_t nslots, int64_t W) {
+ScratchPlan plan_scratch(int64_t n, int64_t naux, int64_t W) {
     ScratchPlan p{};
     const int64_t ldW = r4(std::max<int64_t>(W, 1));
     int64_t off = 0;
@@ -43,7 +43,6 @@ ScratchPlan plan_scratch(int64_t n, int64_t naux, int64_t nslots, int64_t W) {
     p.ld_max = ldW;
     p.status = take(4);
     p.aux = take(4 * naux * ldW);
-    p.part_list = take(4 * nslots * ldW);
     p.T = take(4 * n * ldW);
     p.gemm_part_floats = gemm_part_bound(W);
     p.gemm_part = take(4 * 2 * p.gemm_part_floats);
@@ -122,11 +121,13 @@ int check_graph(const char* fn, const gcn_dgraph* g) {
     GCN_CHECK_ARG(g != nullptr, "%s: graph descriptor is NULL", fn);
     GCN_CHECK_ARG(g->n >= 0 && g->naux >= 0 && g->rounds >= 0 &&
                       g->rounds <= GCN_MAX_ROUNDS && g->nseg >= 0 &&
-                      g->nlong >= 0 && g->nslots >= 0,
+                      g->nbins >= 0 && g->nmulti >= 0 && g->nmulti <= g->nbins &&
+                      g->nhub >= 0 && g->nhub <= g->nmulti &&
+                      (g->n == 0 || g->nbins >= 1),
                   "%s: malformed graph descriptor", fn);
     GCN_CHECK_ARG(g->round_offsets[0] == 0 && g->round_offsets[g->rounds] == g->naux,
                   "%s: graph descriptor round offsets inconsistent", fn);
-    GCN_CHECK_ARG(g->n == 0 || (g->rowptr && g->inv_deg && g->seg),
+    GCN_CHECK_ARG(g->n == 0 || (g->rowptr && g->inv_deg && g->seg && g->bins),
                   "%s: graph descriptor has NULL arrays", fn);
     GCN_CHECK_ARG(g->naux == 0 || (g->exp_col && g->exp_seg && g->exp_nnz >= 2 * (int64_t)g->naux),
                   "%s: graph descriptor lacks pair-sum expansions", fn);
@@ -180,11 +181,9 @@ int do_aggregate(const char* fn, const gcn_dgraph* g, bool transposed, int32_t F
     if (transposed) epi = AGG_SUM;
     const int64_t ldaux = r4(F);
     float* aux = fptr(ws, sp.aux);
-    float* part = fptr(ws, sp.part_list);
     RowSource src{X, ldx, aux, ldaux, g->n};
     GCN_HIP(launch_pair_sums(g, src, transposed, aux, ldaux, F, s), fn);
-    GCN_HIP(launch_list_sums(g, src, transposed, epi, bias, Y, ldy, part, ldaux, F, s, Yh, ldyh),
-            fn);
+    GCN_HIP(launch_list_sums(g, src, transposed, epi, bias, Y, ldy, F, s, Yh, ldyh), fn);
     return GCN_OK;
 }
 
@@ -776,7 +775,7 @@ int plan_step(const gcn_dgraph* g, const gcn_model_desc* d, StepLayout* out) {
         cp.dZ = take(2 * n * cp.ld_dz);
     }
     const int64_t W = std::max<int64_t>({(int64_t)d->f_in, 2 * (int64_t)d->h, (int64_t)d->C});
-    out->sp = plan_scratch(n, g->naux, g->nslots, W);
+    out->sp = plan_scratch(n, g->naux, W);
     out->pub.scratch = off;
     out->pub.scratch_bytes = out->sp.total;
     out->pub.status = out->pub.scratch + out->sp.status;
@@ -832,8 +831,8 @@ int gcn_scratch_bytes(const gcn_dgraph* g, int32_t n, int32_t max_width, size_t*
     GCN_CHECK_ARG(bytes != nullptr, "gcn_scratch_bytes: bytes is NULL");
     GCN_CHECK_ARG(max_width >= 1, "gcn_scratch_bytes: max_width < 1");
     if (g) GCN_TRY(check_graph("gcn_scratch_bytes", g));
-    const ScratchPlan sp = g ? plan_scratch(g->n, g->naux, g->nslots, max_width)
-                             : plan_scratch(std::max(n, 0), 0, 0, max_width);
+    const ScratchPlan sp = g ? plan_scratch(g->n, g->naux, max_width)
+                             : plan_scratch(std::max(n, 0), 0, max_width);
     *bytes = (size_t)sp.total;
     return GCN_OK;
 }
@@ -848,7 +847,7 @@ int gcn_aggregate(const gcn_dgraph* g, int32_t mode, int32_t F, const float* X,
     GCN_TRY(check_mat(fn, "X", X, g->n, F, ldx));
     GCN_TRY(check_mat(fn, "Y", Y, g->n, F, ldy));
     GCN_CHECK_ARG(g->n == 0 || X != Y, "%s: X and Y must not overlap", fn);
-    const ScratchPlan sp = plan_scratch(g->n, g->naux, g->nslots, F);
+    const ScratchPlan sp = plan_scratch(g->n, g->naux, F);
     GCN_TRY(check_ws(fn, ws, ws_bytes, sp.total));
     return do_aggregate(fn, g, mode == GCN_AGG_TRANSPOSED, F, X, ldx, Y, ldy, sp, ws,
                         (hipStream_t)stream);
@@ -863,14 +862,14 @@ int gcn_aggregate_noalloc(const gcn_dgraph* g, int32_t mode, int32_t F, const fl
     GCN_TRY(check_mat(fn, "X", X, g->n, F, ldx));
     GCN_TRY(check_mat(fn, "Y", Y, g->n, F, ldy));
     GCN_CHECK_ARG(g->n == 0 || X != Y, "%s: X and Y must not overlap", fn);
-    // the aggregation reads only the pair-sum and split-list regions, which
-    // lead the plan; both are written before they are read
-    const ScratchPlan sp = plan_scratch(g->n, g->naux, g->nslots, F);
+    // the aggregation reads only the pair-sum region, which leads the plan
+    // after the status word and is written before it is read
+    const ScratchPlan sp = plan_scratch(g->n, g->naux, F);
     const int64_t need = sp.T;
     GCN_CHECK_ARG(need <= kAggStaticBytes,
-                  "%s: %lld scratch bytes needed (naux %d, split-list slots %d, F %d) "
+                  "%s: %lld scratch bytes needed (naux %d, F %d) "
                   "exceed the fixed %lld; use gcn_aggregate with a workspace",
-                  fn, (long long)need, g->naux, g->nslots, F, (long long)kAggStaticBytes);
+                  fn, (long long)need, g->naux, F, (long long)kAggStaticBytes);
     void* ws = nullptr;
     GCN_TRY(static_scratch(fn, &ws));
     return do_aggregate(fn, g, mode == GCN_AGG_TRANSPOSED, F, X, ldx, Y, ldy, sp, ws,
@@ -894,7 +893,7 @@ int gcn_layer_fwd(const gcn_dgraph* g, int32_t F, int32_t h, const float* H_in,
     GCN_TRY(check_mat(fn, "W_self", W_self, F, h, h));
     GCN_TRY(check_mat(fn, "W_neigh", W_neigh, F, h, h));
     if (bias) GCN_TRY(check_vec(fn, "bias", bias, 2 * (int64_t)h));
-    const ScratchPlan sp = plan_scratch(n, g->naux, g->nslots, std::max(F, 2 * h));
+    const ScratchPlan sp = plan_scratch(n, g->naux, std::max(F, 2 * h));
     GCN_TRY(check_ws(fn, ws, ws_bytes, sp.total));
     return do_layer_fwd(fn, g, F, h, H_in, ld_in, W_self, W_neigh, bias, AH, ld_ah,
                         H_out, ld_out, precision == GCN_PREC_BF16, sp, ws,
@@ -912,7 +911,7 @@ int gcn_classifier_fwd(int32_t n, int32_t K, int32_t C, const float* H, int64_t 
     GCN_TRY(check_vec(fn, "W_cls", W_cls, (int64_t)K * C));
     if (b_cls) GCN_TRY(check_vec(fn, "b_cls", b_cls, C));
     GCN_TRY(check_mat(fn, "logits", logits, n, C, ldz));
-    const ScratchPlan sp = plan_scratch(n, 0, 0, std::max(K, C));
+    const ScratchPlan sp = plan_scratch(n, 0, std::max(K, C));
     GCN_TRY(check_ws(fn, ws, ws_bytes, sp.total));
     return do_classifier_fwd(fn, n, K, C, H, ldh, W_cls, b_cls, logits, ldz,
                              precision == GCN_PREC_BF16, sp, ws, (hipStream_t)stream, true,
@@ -937,7 +936,7 @@ int gcn_loss(int32_t n, int32_t C, int32_t kind, const float* logits, int64_t ld
                   "%s: int32 labels not 4-byte aligned", fn);
     GCN_CHECK_ARG(logits != dlogits || ldz == ldd, "%s: in-place loss needs ldz == ldd", fn);
     GCN_TRY(check_vec(fn, "loss_out", loss_out, 1));
-    const ScratchPlan sp = plan_scratch(n, 0, 0, C);
+    const ScratchPlan sp = plan_scratch(n, 0, C);
     GCN_TRY(check_ws(fn, ws, ws_bytes, sp.total));
     GCN_HIP(launch_loss(n, C, kind, logits, ldz, labels, dlogits, ldd, fptr(ws, sp.rowloss),
                         iptr(ws, sp.rowflag), iptr(ws, sp.status), loss_out,
@@ -979,7 +978,7 @@ int gcn_classifier_bwd(int32_t n, int32_t K, int32_t C, const float* dZ, int64_t
     if (G_out) GCN_TRY(check_mat(fn, "G_out", G_out, n, K, ldg));
     if (dW_cls_out) GCN_TRY(check_vec(fn, "dW_cls_out", dW_cls_out, (int64_t)K * C));
     if (db_cls_out) GCN_TRY(check_vec(fn, "db_cls_out", db_cls_out, C));
-    const ScratchPlan sp = plan_scratch(n, 0, 0, std::max(K, C));
+    const ScratchPlan sp = plan_scratch(n, 0, std::max(K, C));
     GCN_TRY(check_ws(fn, ws, ws_bytes, sp.total));
     return do_classifier_bwd(fn, n, K, C, dZ, ldd, H, ldh, W_cls, b_cls, sgd_args(lr),
                              OptState{}, G_out, ldg, dW_cls_out, db_cls_out,
@@ -1008,7 +1007,7 @@ int gcn_layer_bwd(const gcn_dgraph* g, int32_t F, int32_t h, const float* G, int
     if (dW_neigh_out) GCN_TRY(check_vec(fn, "dW_neigh_out", dW_neigh_out, (int64_t)F * h));
     if (db_out) GCN_TRY(check_vec(fn, "db_out", db_out, 2 * (int64_t)h));
     GCN_CHECK_ARG(db_out == nullptr || bias != nullptr, "%s: db_out without bias", fn);
-    const ScratchPlan sp = plan_scratch(n, g->naux, g->nslots, std::max(F, 2 * h));
+    const ScratchPlan sp = plan_scratch(n, g->naux, std::max(F, 2 * h));
     GCN_TRY(check_ws(fn, ws, ws_bytes, sp.total));
     return do_layer_bwd(fn, g, F, h, G, ldg, H_in, ld_in, AH, ld_ah, W_self, W_neigh, bias,
                         sgd_args(lr), OptState{}, OptState{}, G_in, ldgi, dW_self_out,

@@ -29,15 +29,18 @@ inline int64_t round_up(int64_t x, int64_t a) { return (x + a - 1) / a * a; }
 struct ImageHeader {
     uint32_t magic;
     int32_t n, naux, rounds, seg_len;
-    int32_t nseg, nlong, nslots, max_row;
-    int32_t pad0;
+    int32_t nseg, nbins, nmulti, max_row;
+    int32_t nhub;
     int64_t nnz, exp_nnz;
-    int64_t off_rowptr, off_col, off_pairs, off_inv_deg, off_seg, off_longrows;
+    int64_t off_rowptr, off_col, off_pairs, off_inv_deg, off_seg, off_bins;
     int64_t off_exp_col, off_exp_seg;
     int64_t total;
     int32_t round_offsets[GCN_MAX_ROUNDS + 1];
 };
-constexpr uint32_t kImageMagic = 0x47434e32u;  // "GCN2"
+constexpr uint32_t kImageMagic = 0x47434e33u;  // "GCN3"
 constexpr int kDefaultSegLen = 32;
+// Pieces per bin of the list-sum work list: the lane groups of one
+// aggregation workgroup. A list split into pieces lies in one bin.
+constexpr int kBinGroups = GCN_BIN_GROUPS;
 
 }  // namespace gcn

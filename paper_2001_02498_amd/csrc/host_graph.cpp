@@ -599,6 +599,77 @@ void gcn_reduced_free(gcn_reduced_t r) { delete r; }
 
 // ----------------------------------------------------------- device image
 
+// Work-list bins. A row of d entries is ceil(d / seg_len) pieces (one when
+// d <= seg_len, d == 0 included). A row of more than kBinGroups pieces (a
+// hub) is a bin of its own; rows of 2..kBinGroups pieces are packed
+// next-fit, largest first, into bins of kBinGroups pieces; single-piece
+// rows, longest first, fill what those bins leave, then bins of their own.
+// So every row's pieces sit in one bin, the hub bins come first, then the
+// other bins holding split rows, and the groups of one bin have lists of
+// similar length (a workgroup lasts as long as its longest group).
+struct BinLayout {
+    std::vector<int32_t> rows;      // rows in work-list order
+    std::vector<int64_t> bin_rows;  // bin b: rows[bin_rows[b] .. bin_rows[b + 1])
+    int64_t nseg = 0;
+    int32_t nhub = 0, nmulti = 0, max_row = 0;
+};
+
+static int64_t row_pieces(gcn_reduced_t r, int32_t w, int32_t seg_len) {
+    const int64_t d = r->rowptr[w + 1] - r->rowptr[w];
+    return d <= seg_len ? 1 : (d + seg_len - 1) / seg_len;
+}
+
+static BinLayout layout_bins(gcn_reduced_t r, int32_t seg_len) {
+    const int64_t G = gcn::kBinGroups;
+    BinLayout L;
+    std::vector<int32_t> multi, single;
+    L.bin_rows.push_back(0);
+    for (int32_t w = 0; w < r->n; ++w) {
+        L.max_row = std::max(L.max_row, r->rowptr[w + 1] - r->rowptr[w]);
+        const int64_t k = row_pieces(r, w, seg_len);
+        L.nseg += k;
+        if (k > G) {
+            L.rows.push_back(w);
+            L.bin_rows.push_back((int64_t)L.rows.size());
+            ++L.nhub;
+        } else if (k > 1) {
+            multi.push_back(w);
+        } else {
+            single.push_back(w);
+        }
+    }
+    std::stable_sort(multi.begin(), multi.end(), [&](int32_t a, int32_t b) {
+        return row_pieces(r, a, seg_len) > row_pieces(r, b, seg_len);
+    });
+    auto len = [&](int32_t w) { return r->rowptr[w + 1] - r->rowptr[w]; };
+    std::stable_sort(single.begin(), single.end(),
+                     [&](int32_t a, int32_t b) { return len(a) > len(b); });
+    std::vector<std::vector<int32_t>> mb;
+    std::vector<int64_t> used;
+    for (int32_t w : multi) {
+        const int64_t k = row_pieces(r, w, seg_len);
+        if (mb.empty() || used.back() + k > G) {
+            mb.emplace_back();
+            used.push_back(0);
+        }
+        mb.back().push_back(w);
+        used.back() += k;
+    }
+    size_t si = 0;
+    for (size_t b = 0; b < mb.size(); ++b) {
+        for (; used[b] < G && si < single.size(); ++used[b]) mb[b].push_back(single[si++]);
+        L.rows.insert(L.rows.end(), mb[b].begin(), mb[b].end());
+        L.bin_rows.push_back((int64_t)L.rows.size());
+    }
+    L.nmulti = (int32_t)(L.bin_rows.size() - 1);
+    for (; si < single.size(); si += (size_t)G) {
+        const size_t e = std::min(single.size(), si + (size_t)G);
+        L.rows.insert(L.rows.end(), single.begin() + (int64_t)si, single.begin() + (int64_t)e);
+        L.bin_rows.push_back((int64_t)L.rows.size());
+    }
+    return L;
+}
+
 static int plan_image(gcn_reduced_t r, int32_t seg_len, gcn::ImageHeader* h) {
     GCN_CHECK_ARG(r != nullptr, "graph image: NULL reduced graph");
     if (seg_len == 0) seg_len = gcn::kDefaultSegLen;
@@ -611,25 +682,14 @@ static int plan_image(gcn_reduced_t r, int32_t seg_len, gcn::ImageHeader* h) {
     h->rounds = r->rounds;
     h->seg_len = seg_len;
     h->nnz = r->rowptr[r->n];
-    int64_t nseg = 0, nlong = 0, nslots = 0;
-    int32_t max_row = 0;
-    for (int32_t w = 0; w < r->n; ++w) {
-        int32_t d = r->rowptr[w + 1] - r->rowptr[w];
-        max_row = std::max(max_row, d);
-        if (d <= seg_len) {
-            ++nseg;
-        } else {
-            int32_t k = (d + seg_len - 1) / seg_len;
-            nseg += k;
-            nslots += k;
-            ++nlong;
-        }
-    }
-    GCN_CHECK_ARG(nseg < INT32_MAX, "graph image: too many segments");
-    h->nseg = (int32_t)nseg;
-    h->nlong = (int32_t)nlong;
-    h->nslots = (int32_t)nslots;
-    h->max_row = max_row;
+    const BinLayout L = layout_bins(r, seg_len);
+    GCN_CHECK_ARG(L.nseg < INT32_MAX, "graph image: too many segments");
+    h->nseg = (int32_t)L.nseg;
+    h->nbins = (int32_t)(L.bin_rows.size() - 1);
+    h->nmulti = L.nmulti;
+    h->nhub = L.nhub;
+    h->max_row = L.max_row;
+    const int64_t nbins = h->nbins;
     int64_t off = gcn::round_up(sizeof(gcn::ImageHeader), 256);
     auto take = [&](int64_t bytes) {
         int64_t o = off;
@@ -640,8 +700,8 @@ static int plan_image(gcn_reduced_t r, int32_t seg_len, gcn::ImageHeader* h) {
     h->off_col = take(4 * h->nnz);
     h->off_pairs = take(8 * (int64_t)r->naux);
     h->off_inv_deg = take(4 * (int64_t)r->n);
-    h->off_seg = take(16 * nseg);
-    h->off_longrows = take(16 * nlong);
+    h->off_seg = take(16 * L.nseg);
+    h->off_bins = take(4 * (nbins + 1));
     // expansion sizes: |E(k)| = |E(p_k)| + |E(q_k)|, originals count 1
     int64_t exp_nnz = 0;
     {
@@ -692,37 +752,28 @@ int gcn_graph_pack(gcn_reduced_t r, int32_t seg_len, void* host_buf,
     float* inv = reinterpret_cast<float*>(base + h.off_inv_deg);
     for (int32_t v = 0; v < r->n; ++v)
         inv[v] = r->deg[v] > 0 ? (float)(1.0 / (double)r->deg[v]) : 0.0f;
-    // Work list: long lists first (split into seg_len pieces whose partial
-    // sums land in consecutive slots), then the short lists in row order.
+    // Work list, bin by bin (see layout_bins): a row's pieces are
+    // consecutive, the first carrying the piece count, the others 0.
+    const BinLayout L = layout_bins(r, h.seg_len);
     int32_t* seg = reinterpret_cast<int32_t*>(base + h.off_seg);
-    int32_t* lr = reinterpret_cast<int32_t*>(base + h.off_longrows);
-    int64_t s = 0, slot = 0, li = 0;
-    for (int32_t w = 0; w < r->n; ++w) {
-        int32_t b = r->rowptr[w], e = r->rowptr[w + 1];
-        if (e - b <= h.seg_len) continue;
-        int32_t k = (e - b + h.seg_len - 1) / h.seg_len;
-        lr[4 * li + 0] = w;
-        lr[4 * li + 1] = (int32_t)slot;
-        lr[4 * li + 2] = k;
-        lr[4 * li + 3] = 0;
-        ++li;
-        for (int32_t j = 0; j < k; ++j) {
-            seg[4 * s + 0] = w;
-            seg[4 * s + 1] = b + j * h.seg_len;
-            seg[4 * s + 2] = std::min(e, b + (j + 1) * h.seg_len);
-            seg[4 * s + 3] = (int32_t)slot++;
-            ++s;
+    int32_t* bins = reinterpret_cast<int32_t*>(base + h.off_bins);
+    int64_t s = 0;
+    for (int32_t bi = 0; bi < h.nbins; ++bi) {
+        bins[bi] = (int32_t)s;
+        for (int64_t x = L.bin_rows[bi]; x < L.bin_rows[bi + 1]; ++x) {
+            const int32_t w = L.rows[x];
+            const int32_t b = r->rowptr[w], e = r->rowptr[w + 1];
+            const int64_t k = row_pieces(r, w, h.seg_len);
+            for (int64_t j = 0; j < k; ++j) {
+                seg[4 * s + 0] = w;
+                seg[4 * s + 1] = (int32_t)std::min<int64_t>(e, b + j * h.seg_len);
+                seg[4 * s + 2] = (int32_t)std::min<int64_t>(e, b + (j + 1) * h.seg_len);
+                seg[4 * s + 3] = j == 0 ? (int32_t)k : 0;
+                ++s;
+            }
         }
     }
-    for (int32_t w = 0; w < r->n; ++w) {
-        int32_t b = r->rowptr[w], e = r->rowptr[w + 1];
-        if (e - b > h.seg_len) continue;
-        seg[4 * s + 0] = w;
-        seg[4 * s + 1] = b;
-        seg[4 * s + 2] = e;
-        seg[4 * s + 3] = -1;
-        ++s;
-    }
+    bins[h.nbins] = (int32_t)s;
     // Expansion of every pair sum into original vertices, ascending: the
     // members of pair k are the members of its two parts (earlier ids).
     int32_t* ecol = reinterpret_cast<int32_t*>(base + h.off_exp_col);
@@ -765,8 +816,9 @@ int gcn_graph_describe(const void* host_image, size_t bytes,
     out->rounds = h.rounds;
     out->seg_len = h.seg_len;
     out->nseg = h.nseg;
-    out->nlong = h.nlong;
-    out->nslots = h.nslots;
+    out->nbins = h.nbins;
+    out->nmulti = h.nmulti;
+    out->nhub = h.nhub;
     out->max_row = h.max_row;
     out->nnz = h.nnz;
     out->rowptr = reinterpret_cast<const int32_t*>(d + h.off_rowptr);
@@ -774,7 +826,7 @@ int gcn_graph_describe(const void* host_image, size_t bytes,
     out->pairs = reinterpret_cast<const int32_t*>(d + h.off_pairs);
     out->inv_deg = reinterpret_cast<const float*>(d + h.off_inv_deg);
     out->seg = reinterpret_cast<const int32_t*>(d + h.off_seg);
-    out->longrows = reinterpret_cast<const int32_t*>(d + h.off_longrows);
+    out->bins = reinterpret_cast<const int32_t*>(d + h.off_bins);
     out->exp_nnz = h.exp_nnz;
     out->exp_col = reinterpret_cast<const int32_t*>(d + h.off_exp_col);
     out->exp_seg = reinterpret_cast<const int32_t*>(d + h.off_exp_seg);

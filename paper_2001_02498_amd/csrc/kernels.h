@@ -32,15 +32,15 @@ enum AggEpi : int {
     AGG_MEAN_BIAS_RELU = 2,  // Y_w = max((1/d_w) sum + bias, 0)  (bias may be NULL)
 };
 
-// Segment sums of G_s^# lists (see the work list of gcn_graph_pack), then the
-// fix-up of split lists, finished as `epi` says; prescale (with AGG_SUM
-// only): gathered original rows are multiplied by their 1/d.
+// Sums of the G_s^# lists (the binned work list of gcn_graph_pack; a split
+// list's pieces are added within its bin's workgroup), finished as `epi`
+// says; prescale (with AGG_SUM only): gathered original rows are multiplied
+// by their 1/d.
 // Yh != NULL: the finished rows go to Yh as bf16 (rounded to nearest even;
 // leading dimension ldyh) instead of to Y.
 hipError_t launch_list_sums(const gcn_dgraph* g, RowSource src, bool prescale, AggEpi epi,
-                            const float* bias, float* Y, int64_t ldy, float* partial,
-                            int64_t ldp, int32_t F, hipStream_t s, __bf16* Yh = nullptr,
-                            int64_t ldyh = 0);
+                            const float* bias, float* Y, int64_t ldy, int32_t F, hipStream_t s,
+                            __bf16* Yh = nullptr, int64_t ldyh = 0);
 
 // ---------------------------------------------------------------- GEMM
 enum ALayout : int { A_MK = 0, A_KM = 1 };   // A(m,k) = A[m*lda+k] | A[k*lda+m]

@@ -10,7 +10,6 @@ namespace gcn {
 enum Kind : int {
     K_PAIR_SUMS = 0,
     K_LIST_SUMS,
-    K_LIST_FIXUP,
     K_GEMM_FWD,
     K_GEMM_CLS,
     K_GEMM_DX,

@@ -31,7 +31,6 @@ const char* kind_name(int k) {
     switch (k) {
         case K_PAIR_SUMS: return "pair_sums";
         case K_LIST_SUMS: return "list_sums";
-        case K_LIST_FIXUP: return "list_fixup";
         case K_GEMM_FWD: return "gemm_fwd";
         case K_GEMM_CLS: return "gemm_cls";
         case K_GEMM_DX: return "gemm_dx";

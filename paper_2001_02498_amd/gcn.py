@@ -54,7 +54,8 @@ OPT_MOMENTUM = 1
 OPT_ADAM = 2
 AGG_MEAN = 0
 AGG_TRANSPOSED = 1
-ABI_VERSION = 6
+ABI_VERSION = 7
+BIN_GROUPS = 16
 
 _i32, _i64, _f32 = C.c_int32, C.c_int64, C.c_float
 _vp, _sz = C.c_void_p, C.c_size_t
@@ -81,10 +82,11 @@ class RrRound(C.Structure):
 
 class DGraph(C.Structure):
     _fields_ = [("n", _i32), ("naux", _i32), ("rounds", _i32), ("seg_len", _i32),
-                ("nseg", _i32), ("nlong", _i32), ("nslots", _i32), ("max_row", _i32),
+                ("nseg", _i32), ("nbins", _i32), ("nmulti", _i32), ("nhub", _i32),
+                ("max_row", _i32), ("reserved", _i32),
                 ("nnz", _i64), ("exp_nnz", _i64),
                 ("rowptr", _vp), ("col", _vp), ("pairs", _vp), ("inv_deg", _vp),
-                ("seg", _vp), ("longrows", _vp), ("exp_col", _vp), ("exp_seg", _vp),
+                ("seg", _vp), ("bins", _vp), ("exp_col", _vp), ("exp_seg", _vp),
                 ("round_offsets", _i32 * (MAX_ROUNDS + 1))]
 
 

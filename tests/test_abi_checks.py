@@ -18,9 +18,9 @@ class _Graph:
     def __init__(self, n=100, naux=0):
         g = gcn.DGraph()
         g.n, g.naux, g.rounds, g.seg_len = n, naux, 0, 32
-        g.nseg, g.nlong, g.nslots, g.max_row = n, 0, 0, 8
+        g.nseg, g.nbins, g.nmulti, g.max_row = n, (n + 15) // 16, 0, 8
         g.nnz, g.exp_nnz = 4 * n, 0
-        for f in ("rowptr", "col", "inv_deg", "seg"):
+        for f in ("rowptr", "col", "inv_deg", "seg", "bins"):
             setattr(g, f, FAKE)
         self.desc = g
 
@@ -99,6 +99,18 @@ def test_graph_descriptor_checks():
     g.desc.rowptr = None
     code, msg = _code(gcn.workspace_bytes, g, _desc())
     assert code == gcn.E_INVALID_ARG
+    g = _Graph()
+    g.desc.bins = None
+    code, msg = _code(gcn.workspace_bytes, g, _desc())
+    assert code == gcn.E_INVALID_ARG
+    g = _Graph()
+    g.desc.nmulti = g.desc.nbins + 1   # more bins with split rows than bins
+    code, msg = _code(gcn.workspace_bytes, g, _desc())
+    assert code == gcn.E_INVALID_ARG and "malformed" in msg
+    g = _Graph()
+    g.desc.nhub = 1                    # a hub bin outside the split-row bins
+    code, msg = _code(gcn.workspace_bytes, g, _desc())
+    assert code == gcn.E_INVALID_ARG and "malformed" in msg
 
 
 def _params(L):

@@ -15,9 +15,11 @@ GEMM = ("void gcn::(anonymous namespace)::gemm_kernel<(gcn::ALayout)1, (gcn::BLa
 GEMM16 = GEMM.replace("gemm_kernel<", "gemm_bf16_kernel<")
 H16 = ("void gcn::(anonymous namespace)::gemm_h16_kernel<(gcn::ALayout)1, (gcn::BLayout)0, "
        "(gcn::Epilogue)4, (gcn::GemmRole){}>(gcn::GemmBatch)")
-LIST = ("void gcn::(anonymous namespace)::list_sums_kernel<32, 1, false, 1, {}>(int4 const*, "
-        "int, int const*, gcn::RowSource, float const*, float const*, float*, long, float*, "
-        "long, int, int, int)")
+LIST = ("void gcn::(anonymous namespace)::list_sums_kernel<32, 1, false, 1>(int4 const*, "
+        "int const*, int, int const*, gcn::RowSource, float const*, float const*, float*, long, "
+        "int, int, int, __bf16*, long)")
+PAIR = ("void gcn::(anonymous namespace)::pair_sums_kernel<64, 2, true>(int4 const*, int, "
+        "int const*, gcn::RowSource, float const*, float*, long, int, int, int)")
 
 
 @pytest.mark.parametrize("role,cls", list(enumerate(bench._ROLE_CLASS)))
@@ -28,10 +30,9 @@ def test_gemm_roles_map_to_classes(role, cls):
 
 
 def test_other_kernels_map_to_classes():
-    assert bench.kernel_class(LIST.format("true")) == "pair_sums"
-    assert bench.kernel_class(LIST.format("false")) == "list_sums"
+    assert bench.kernel_class(PAIR) == "pair_sums"
+    assert bench.kernel_class(LIST) == "list_sums"
     cases = {
-        "void gcn::(anonymous namespace)::fixup_kernel<32, 1, 1>(int4 const*)": "list_fixup",
         "void gcn::(anonymous namespace)::sgd_reduce_kernel<2>(gcn::SgdProblem)": "sgd_reduce",
         "void gcn::(anonymous namespace)::loss_kernel<2, true>(int, int)": "loss_rows",
         "gcn::(anonymous namespace)::mean_kernel(int, float const*, float, float*)": "loss_mean",

@@ -53,6 +53,36 @@ def test_aggregate_widths(F, seg_len):
         assert rel(Y, og.aggregate_transposed(case.rp, case.cl, X)) < AGG_TOL
 
 
+@pytest.mark.parametrize("F", [1, 5, 64, 256, 300, 602, 1024, 2100])
+def test_aggregate_hubs(F):
+    """Hubs (lists of more than 16 pieces): a star on 6,000 vertices, three
+    smaller hubs and a sparse background; their workgroups split the
+    columns and add the list in a tree, in a fixed order."""
+    need_gpu()
+    rng = np.random.default_rng(F + 7)
+    n = 6000
+    src = [np.zeros(n - 1, np.int64)]
+    dst = [np.arange(1, n)]
+    for h, deg in ((1, 600), (2, 1500), (3, 3100)):
+        src.append(np.full(deg, h))
+        dst.append(rng.choice(np.arange(4, n), deg, replace=False))
+    src.append(rng.integers(4, n, 9000))
+    dst.append(rng.integers(4, n, 9000))
+    src, dst = np.concatenate(src), np.concatenate(dst)
+    X = rng.standard_normal((n, F)).astype(np.float32)
+    for rounds, seg_len in ((0, 0), (0, 7), (5, 0)):
+        say("hubs F", F, "rounds", rounds, "seg_len", seg_len)
+        case = GraphCase(n, src, dst, rounds=rounds, seg_len=seg_len)
+        assert case.dg.desc.nhub >= 2
+        Y = _run(case, case.gcn.AGG_MEAN, X, ldy=(F + 3) // 4 * 4 + 4)
+        assert rel(Y, og.aggregate(case.rp, case.cl, X)) < AGG_TOL
+        assert torch.isnan(padding_of(Y)).all()
+        Y2 = _run(case, case.gcn.AGG_MEAN, X, ldy=(F + 3) // 4 * 4 + 4)
+        assert torch.equal(Y, Y2)
+        Y = _run(case, case.gcn.AGG_TRANSPOSED, X)
+        assert rel(Y, og.aggregate_transposed(case.rp, case.cl, X)) < AGG_TOL
+
+
 def test_aggregate_integer_features_direct_equals_reduced():
     """Integer features: every partial sum is exact in fp32, so the reduced
     graph reaches D^-1 A X bit for bit (same rounding of the final scale)."""

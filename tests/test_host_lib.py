@@ -222,14 +222,13 @@ def _unpack_image(buf, nbytes):
         pairs=view(d.pairs, 2 * d.naux, np.int32) if d.naux else np.zeros(0, np.int32),
         inv_deg=view(d.inv_deg, d.n, np.float32),
         seg=view(d.seg, 4 * d.nseg, np.int32).reshape(-1, 4),
-        longrows=view(d.longrows, 4 * d.nlong, np.int32).reshape(-1, 4) if d.nlong
-        else np.zeros((0, 4), np.int32),
+        bins=view(d.bins, d.nbins + 1, np.int32),
         exp_col=view(d.exp_col, d.exp_nnz, np.int32) if d.exp_nnz else np.zeros(0, np.int32),
         exp_seg=view(d.exp_seg, 4 * d.naux, np.int32).reshape(-1, 4) if d.naux
         else np.zeros((0, 4), np.int32))
 
 
-@pytest.mark.parametrize("seg_len", [0, 1, 3, 64])
+@pytest.mark.parametrize("seg_len", [0, 1, 3, 9, 64])
 def test_device_image_work_list(seg_len):
     wl = synth.WORKLOADS["tiny"]
     inp = synth.make_inputs(wl)
@@ -251,26 +250,44 @@ def test_device_image_work_list(seg_len):
     want_inv = np.where(deg > 0, 1.0 / np.maximum(deg, 1), 0.0).astype(np.float32)
     assert np.array_equal(sec["inv_deg"], want_inv)
     assert list(d.round_offsets[:d.rounds + 1]) == info["round_offsets"].tolist()
-    # every list entry covered exactly once; segments never exceed seg_len;
-    # split lists write consecutive slots recorded in the long-row table
-    covered = np.zeros(info["nnz"], dtype=np.int64)
-    rows_seen = np.zeros(wl.n, dtype=np.int64)
-    slots = {}
-    for row, b, e, slot in sec["seg"]:
-        assert info["rowptr"][row] <= b <= e <= info["rowptr"][row + 1]
-        assert e - b <= L
-        covered[b:e] += 1
-        rows_seen[row] += 1
-        if slot >= 0:
-            slots.setdefault(row, []).append(slot)
-    assert np.all(covered == 1)
-    assert np.all(rows_seen >= 1)
+    # every list entry covered exactly once; pieces never exceed seg_len; a
+    # row's pieces are consecutive and in order, the first carrying their
+    # count; every row lies in one bin of at most GCN_BIN_GROUPS pieces (or
+    # is the only row of its bin), and the bins with split rows come first
+    G = gcn.BIN_GROUPS
     lens = np.diff(info["rowptr"])
     assert d.max_row == lens.max()
-    assert d.nlong == int((lens > L).sum())
-    for row, first, ns, _ in sec["longrows"]:
-        assert slots[row] == list(range(first, first + ns))
-    assert d.nslots == sum(len(v) for v in slots.values())
+    bins = sec["bins"]
+    assert bins[0] == 0 and bins[-1] == d.nseg and np.all(np.diff(bins) >= 1)
+    covered = np.zeros(info["nnz"], dtype=np.int64)
+    rows_seen = np.zeros(wl.n, dtype=np.int64)
+    seg = sec["seg"]
+    for bi in range(d.nbins):
+        s0, s1 = bins[bi], bins[bi + 1]
+        p, rows, split = s0, [], False
+        while p < s1:
+            row, b, e, lead = seg[p]
+            k = max(1, -(-int(lens[row]) // L))
+            assert lead == k and b == info["rowptr"][row] and p + k <= s1
+            for j in range(k):
+                r2, b2, e2, l2 = seg[p + j]
+                assert r2 == row and (l2 == 0) == (j > 0)
+                assert b2 == info["rowptr"][row] + j * L or (k == 1 and b2 == b)
+                assert b2 <= e2 <= info["rowptr"][row + 1] and e2 - b2 <= L
+                covered[b2:e2] += 1
+            assert seg[p + k - 1][2] == info["rowptr"][row + 1]
+            rows_seen[row] += 1
+            rows.append(row)
+            split |= k > 1
+            p += k
+        assert s1 - s0 <= G or len(rows) == 1
+        assert (s1 - s0 > G) == (bi < d.nhub)
+        assert split == (bi < d.nmulti)
+    assert np.all(covered == 1)
+    assert np.all(rows_seen == 1)
+    assert d.nseg == sum(max(1, -(-int(x) // L)) for x in lens)
+    # rows of more than G pieces (seg_len 1, 3, 9 here) get bins of their own
+    assert (np.diff(bins).max() > G) == (lens.max() > G * L)
     # pair sum k expands into the original vertices of the oracle's expansion
     assert d.naux > 0
     for k, (kk, b, e, slot) in enumerate(sec["exp_seg"]):
