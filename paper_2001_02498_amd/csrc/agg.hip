@@ -323,10 +323,15 @@ __global__ __launch_bounds__(kBinGroups * GL) void list_sums_kernel(
     constexpr int kRed = (G - 1) * NCH * GL > T ? (G - 1) * NCH * GL : T;
     __shared__ float4 red[kRed];
     if ((int)blockIdx.x < hub_blocks) {
-        const int h = (int)blockIdx.x / hub_slices;
+        // block b runs on XCD b % 8; (hub, slice) pairs are dealt to the
+        // XCDs in contiguous runs, so neighbouring slices, which share
+        // cache lines, share an L2
+        const int b = (int)blockIdx.x;
+        const int q = (b % 8) * (hub_blocks / 8) + b / 8;
+        const int h = q / hub_slices;
         if (h < nhub)
-            hub_row<T, PRE, EPI>(h, (int)blockIdx.x % hub_slices, seg, bins, col, src, inv_deg,
-                                 bias, Y, ldy, F, Yh, ldyh, red);
+            hub_row<T, PRE, EPI>(h, q % hub_slices, seg, bins, col, src, inv_deg, bias, Y, ldy,
+                                 F, Yh, ldyh, red);
         return;
     }
     // hub_blocks is a multiple of 8, so slice b % nsl still runs on XCD b % 8
