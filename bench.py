@@ -145,7 +145,7 @@ def kernel_class(name):
     reports), or None for kernels that are not the library's."""
     import re
     for key, suffix in (("gemm_kernel<", ""), ("gemm_bf16_kernel<", "_bf16"),
-                        ("gemm_h16_kernel<", "_bf16")):
+                        ("gemm_h16_kernel<", "_bf16"), ("gemm_h16s_kernel<", "_bf16")):
         if key in name:
             m = re.search(r"\(gcn::GemmRole\)(\d+)", name)
             return _ROLE_CLASS[int(m.group(1))] + suffix if m else None

@@ -1357,6 +1357,162 @@ __global__ __launch_bounds__(kThreads, 2) void gemm_h16_kernel(GemmBatch batch) 
         P, split, m0 + wm * 64, n0 + wn * 32 * NB, half, l32, lane, stage, acc);
 }
 
+// ------------------------------------------------------------ staged bf16
+// The bf16 copies products of launches whose every K step is whole (K and
+// the K concatenation points multiples of 32, no appended row of ones),
+// with both operands K-contiguous (A [m][k], B [n][k]: the input
+// gradients). The operands go from HBM straight into LDS
+// (global_load_lds_dwordx4: each wavefront instruction moves 1 KB, 16 bytes
+// per lane, to consecutive LDS addresses), kH16Stages K steps in flight, so
+// no register staging limits how far ahead the loads run; three stages of
+// 16 KB leave room for three workgroups per CU. Each stage holds both
+// operands as [row][k] (64-byte rows), unpadded, the four 16-byte chunks
+// of row r at positions chunk ^ ((r / 4) % 4), so that the 128-bit fragment
+// reads of 16 consecutive rows meet no bank conflicts. The loads of a
+// stage land before a workgroup barrier that follows a wait on this
+// wavefront's own outstanding loads. Tile, tile order, the MFMAs and the
+// order they take the K values are those of the copies kernel above, so
+// the products equal its bit for bit; rows outside the operands are clamped
+// into them (they only feed outputs the epilogue drops).
+constexpr int kH16Stages = 3;
+
+template <Epilogue EP, GemmRole ROLE, int NB = 2>
+__global__ __launch_bounds__(kThreads, 2) void gemm_h16s_kernel(GemmBatch batch) {
+    constexpr int TBN = 64 * NB;
+    constexpr int kS = kH16Stages;
+    constexpr int kABytes = BM * BK * 2;               // 8 KB
+    constexpr int kBBytes = TBN * BK * 2;              // 4 KB per NB
+    constexpr int kStageBytes = kABytes + kBBytes;
+    constexpr int kAInst = kABytes / 1024 / 4;         // A loads per wavefront and stage
+    constexpr int kBInst = kBBytes / 1024 / 4;         // B loads per wavefront and stage
+    constexpr int kLoads = kAInst + kBInst;
+    static_assert(kAInst * 4096 == kABytes && kBInst * 4096 == kBBytes, "whole loads");
+    constexpr int kEpiFloats = 4 * 32 * (32 * NB + 4);
+    static_assert(kEpiFloats * 4 <= kS * kStageBytes, "the epilogue stage fits");
+    __shared__ __attribute__((aligned(1024))) char lds[kS * kStageBytes];
+    typedef __attribute__((address_space(3))) void lds_void;
+
+    const TileInfo ti = decode_tile<BM, TBN>(batch);
+    const GemmProblem& P = batch.p[ti.pi];
+    const int split = ti.split, m0 = ti.m0, n0 = ti.n0;
+    const int kbeg = ti.kbeg, nk = ti.nk;
+
+    const int t = threadIdx.x;
+    const int lane = t & 63, wave = t >> 6;
+    const int wm = wave >> 1, wn = wave & 1;
+    const int half = lane >> 5, l32 = lane & 31;
+    const int M = P.M, N = P.N;
+
+    // Per-lane source offsets (elements), fixed for the whole K loop: load i
+    // of this wavefront covers rows 16 (kAInst wave + i) + lane / 4 of A (and
+    // likewise of B), LDS slot lane % 4 of the row receiving chunk
+    // (lane % 4) ^ ((row / 4) % 4)
+    int64_t oa[kAInst], ob[kBInst];
+#pragma unroll
+    for (int i = 0; i < kAInst; ++i) {
+        const int r = 16 * (kAInst * wave + i) + (lane >> 2);
+        const int c = (lane & 3) ^ ((r >> 2) & 3);
+        oa[i] = (int64_t)min(m0 + r, M - 1) * P.hlda0 + 8 * c;
+    }
+#pragma unroll
+    for (int i = 0; i < kBInst; ++i) {
+        const int r = 16 * (kBInst * wave + i) + (lane >> 2);
+        const int c = (lane & 3) ^ ((r >> 2) & 3);
+        ob[i] = (int64_t)min(n0 + r, N - 1) * P.hldb0 + 8 * c;
+    }
+    auto stage_a = [&](int buf) { return lds + buf * kStageBytes; };
+    auto stage_b = [&](int buf) { return lds + buf * kStageBytes + kABytes; };
+    // loads of K step kt into buffer kt % kS (uniform base per step)
+    auto issue = [&](int kt) {
+        const int k0 = kbeg + kt * BK;
+        const __bf16* sa = k0 >= P.ksplitA ? P.hA1 + (k0 - P.ksplitA) : P.hA0 + k0;
+        const __bf16* sb = k0 >= P.ksplitB ? P.hB1 + (k0 - P.ksplitB) : P.hB0 + k0;
+        char* da = stage_a(kt % kS);
+        char* db = stage_b(kt % kS);
+#pragma unroll
+        for (int i = 0; i < kAInst; ++i)
+            __builtin_amdgcn_global_load_lds((const void*)(sa + oa[i]),
+                                             (lds_void*)(da + 1024 * (kAInst * wave + i)), 16, 0,
+                                             0);
+#pragma unroll
+        for (int i = 0; i < kBInst; ++i)
+            __builtin_amdgcn_global_load_lds((const void*)(sb + ob[i]),
+                                             (lds_void*)(db + 1024 * (kBInst * wave + i)), 16, 0,
+                                             0);
+    };
+
+    floatx16 acc[2][NB];
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < NB; ++j)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+
+    // fragment of MFMA step ks: lane half g holds K values 16 ks + 8 g .. + 7
+    // of row base + l32
+    auto frag_rk = [&](const char* S, int base, int ks) -> bf16x8 {
+        const int r = base + l32, c = 2 * ks + half;
+        return *reinterpret_cast<const bf16x8*>(S + 64 * r + 16 * (c ^ ((r >> 2) & 3)));
+    };
+    bf16x8 fa[2][2], fb[2][NB];
+    auto compute = [&](int buf) {
+        const char* As = stage_a(buf);
+        const char* Bs = stage_b(buf);
+#pragma unroll
+        for (int ks = 0; ks < 2; ++ks) {
+#pragma unroll
+            for (int i = 0; i < 2; ++i) fa[ks][i] = frag_rk(As, wm * 64 + i * 32, ks);
+#pragma unroll
+            for (int j = 0; j < NB; ++j) fb[ks][j] = frag_rk(Bs, wn * 32 * NB + j * 32, ks);
+        }
+#pragma unroll
+        for (int ks = 0; ks < 2; ++ks)
+#pragma unroll
+            for (int i = 0; i < 2; ++i)
+#pragma unroll
+                for (int j = 0; j < NB; ++j)
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fb[ks][j], fa[ks][i],
+                                                                        acc[i][j], 0, 0, 0);
+    };
+    // s_waitcnt vmcnt(n), no wait on the other counters (gfx9 encoding)
+#define GCN_WAIT_VM(n) \
+    __builtin_amdgcn_s_waitcnt(((n) & 15) | ((((n) >> 4) & 3) << 14) | (7 << 4) | (15 << 8))
+    // workgroup barrier without the memory fence of __syncthreads (which
+    // would wait for every load in flight); the empty asm statements keep
+    // the compiler from moving LDS accesses across it
+    auto stage_barrier = [] {
+        asm volatile("" ::: "memory");
+        __builtin_amdgcn_s_barrier();
+        asm volatile("" ::: "memory");
+    };
+
+#pragma unroll
+    for (int s0 = 0; s0 < kS - 1; ++s0)
+        if (s0 < nk) issue(s0);
+    int kt = 0;
+    // steady state: step kt lands while steps kt + 1 .. kt + kS - 2 stay in
+    // flight; buffer (kt + kS - 1) % kS was last read in step kt - 1, which
+    // every wavefront finished before this step's barrier
+    for (; kt + kS - 1 < nk; ++kt) {
+        GCN_WAIT_VM((kS - 2) * kLoads);
+        stage_barrier();
+        issue(kt + kS - 1);
+        compute(kt % kS);
+    }
+    // the last steps: everything issued has landed after one wait
+    if (kt < nk) {
+        GCN_WAIT_VM(0);
+        stage_barrier();
+        for (; kt < nk; ++kt) compute(kt % kS);
+    }
+#undef GCN_WAIT_VM
+    __syncthreads();   // every fragment read done: the stages become the epilogue stage
+    float* stage = reinterpret_cast<float*>(lds) + wave * (kEpiFloats / 4);
+    store_tile_lds<EP, EP == EPI_BIAS_RELU || EP == EPI_MASK, NB>(
+        P, split, m0 + wm * 64, n0 + wn * 32 * NB, half, l32, lane, stage, acc);
+}
+
 // Rounding of fp32 matrices to bf16 copies: one thread per 8 output
 // elements of one row, jobs laid end to end (fewer than 2^31 chunks).
 struct ConvBatch {
@@ -1616,6 +1772,16 @@ hipError_t launch_gemm(GemmBatch& b, ALayout al, BLayout bl, Epilogue ep, GemmRo
                      (p.hC ? 2.0 * M * N : 0.0);
         }
     }
+    // the staged copies kernel: every K step whole in every problem, B as
+    // [n][k] (with B as [k][n] its transposing reads made the forward
+    // products slower than the kernel above on every workload measured)
+    bool staged = copies && al == A_MK && bl == B_NK && ep != EPI_PARTIAL;
+    for (int i = 0; i < b.nprob && staged; ++i) {
+        const GemmProblem& p = b.p[i];
+        staged = p.ones_row == 0 && p.K % BK == 0 &&
+                 (p.ksplitA >= p.K || (p.ksplitA % BK == 0 && p.hlda1 == p.hlda0)) &&
+                 (p.ksplitB >= p.K || (p.ksplitB % BK == 0 && p.hldb1 == p.hldb0));
+    }
     const int kind = bf16 ? kKinds16[role] : kKinds[role];
     ProfScope prof(s, kind, flops, bytes);
     bool bvec = true;
@@ -1631,7 +1797,14 @@ hipError_t launch_gemm(GemmBatch& b, ALayout al, BLayout bl, Epilogue ep, GemmRo
         constexpr bool kSmallOk = ROLE_ == ROLE_CLS_DW || ROLE_ == ROLE_DW_IN;      \
         constexpr bool kMidOk = ROLE_ == ROLE_CLS_FWD;                               \
         if (copies) {                                                                \
-            if (nb1) {                                                               \
+            if (staged) {                                                            \
+                if constexpr (kNarrowOk && BL_ == B_NK) {                            \
+                    if (nb1)                                                         \
+                        gemm_h16s_kernel<EP_, ROLE_, 1><<<grid, block, 0, s>>>(b);    \
+                    else                                                             \
+                        gemm_h16s_kernel<EP_, ROLE_, 2><<<grid, block, 0, s>>>(b);    \
+                }                                                                    \
+            } else if (nb1) {                                                        \
                 if constexpr (kNarrowOk)                                             \
                     gemm_h16_kernel<AL_, BL_, EP_, ROLE_, 1><<<grid, block, 0, s>>>(b);\
             } else {                                                                 \

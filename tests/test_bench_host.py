@@ -15,6 +15,8 @@ GEMM = ("void gcn::(anonymous namespace)::gemm_kernel<(gcn::ALayout)1, (gcn::BLa
 GEMM16 = GEMM.replace("gemm_kernel<", "gemm_bf16_kernel<")
 H16 = ("void gcn::(anonymous namespace)::gemm_h16_kernel<(gcn::ALayout)1, (gcn::BLayout)0, "
        "(gcn::Epilogue)4, (gcn::GemmRole){}>(gcn::GemmBatch)")
+H16S = ("void gcn::(anonymous namespace)::gemm_h16s_kernel<(gcn::Epilogue)3, (gcn::GemmRole){}, "
+        "2>(gcn::GemmBatch)")
 LIST = ("void gcn::(anonymous namespace)::list_sums_kernel<32, 1, false, 1>(int4 const*, "
         "int const*, int, int const*, gcn::RowSource, float const*, float const*, float*, long, "
         "int, int, int, __bf16*, long)")
@@ -27,6 +29,7 @@ def test_gemm_roles_map_to_classes(role, cls):
     assert bench.kernel_class(GEMM.format(role)) == cls
     assert bench.kernel_class(GEMM16.format(role)) == cls + "_bf16"
     assert bench.kernel_class(H16.format(role)) == cls + "_bf16"
+    assert bench.kernel_class(H16S.format(role)) == cls + "_bf16"
 
 
 def test_other_kernels_map_to_classes():
