@@ -24,8 +24,10 @@ def _ws(case, W):
     return case.gcn.alloc_ws(case.gcn.scratch_bytes(case.dg, W))
 
 
+# (9000, 64, 256): a 40-row last row tile, two products of 256 columns
 @pytest.mark.parametrize("n,F,h,bias", [(777, 50, 36, False), (1024, 64, 128, True),
-                                        (300, 602, 20, False), (513, 256, 132, True)])
+                                        (300, 602, 20, False), (513, 256, 132, True),
+                                        (9000, 64, 256, True)])
 def test_layer_fwd(n, F, h, bias):
     need_gpu()
     say("layer_fwd", n, F, h, bias)
@@ -119,7 +121,9 @@ def test_classifier_fwd_loss_bwd(n, K, C, bias):
                                               (5000, 64, 128, True, True),
                                               (5000, 63, 72, True, True),
                                               (2000, 65, 40, False, True),
-                                              (4100, 8, 24, False, True)])
+                                              (4100, 8, 24, False, True),
+                                              # a 40-row last row tile
+                                              (9000, 512, 64, True, False)])
 def test_layer_bwd(n, F, h, bias, first):
     need_gpu()
     say("layer_bwd", n, F, h, bias, first)
