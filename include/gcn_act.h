@@ -512,6 +512,10 @@ int gcn_layer_bwd(const gcn_dgraph* g, int32_t F, int32_t h, const float* G,
  *           individual NULL members, to skip)
  *   ws      >= gcn_workspace_bytes(); activations live at the offsets
  *           reported by gcn_workspace_layout (valid after the step).
+ * Every weight is updated by one launch at the end of the backward pass,
+ * after all input gradients have read the weights; each layer's and the
+ * classifier's gradient slices keep a workspace region of their own until
+ * then.
  * order GCN_ORDER_PAPER: every layer aggregates first, D^-1 A (H W_neigh)
  *   as D^-1 A H then times W_neigh (Eq. 1), and keeps AH for Eq. 2b.
  * order GCN_ORDER_NARROW: a layer whose input is wider than h (F > h)

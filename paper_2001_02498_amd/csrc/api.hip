@@ -25,13 +25,36 @@ struct ScratchPlan {
     int64_t ld_max;             // widest row (floats) of the aux / T regions
 };
 
+// Split-K partial sums of product pair `region` (two problems each): the
+// training step keeps every layer's weight gradients (region l) and the
+// classifier's (region L) until its single update launch at the end.
+float* part_region(void* ws, const ScratchPlan& sp, int region) {
+    return reinterpret_cast<float*>(static_cast<char*>(ws) + sp.gemm_part) +
+           (int64_t)region * 2 * sp.gemm_part_floats;
+}
+
+// Weight updates collected over a step for one launch.
+struct SgdList {
+    SgdProblem p[kMaxSgdProblems];
+    int n = 0;
+};
+
+// Launches q[0..nq) now, or appends them to `defer`.
+hipError_t sgd_now_or_later(const SgdProblem* q, int nq, const OptimArgs& oa, SgdList* defer,
+                            hipStream_t s) {
+    if (!defer) return launch_sgd_reduce(q, nq, oa, s);
+    if (defer->n + nq > kMaxSgdProblems) return hipErrorInvalidValue;
+    for (int i = 0; i < nq; ++i) defer->p[defer->n++] = q[i];
+    return hipSuccess;
+}
+
 int64_t gemm_part_bound(int64_t W) {
     // split factor * tiles <= 512 + tiles, each tile 128 x 128 floats
     const int64_t tiles = ((W + 1 + 127) / 128) * ((W + 127) / 128);
     return (512 + tiles) * 128 * 128;
 }
 
-ScratchPlan plan_scratch(int64_t n, int64_t naux, int64_t W) {
+ScratchPlan plan_scratch(int64_t n, int64_t naux, int64_t W, int64_t part_regions = 1) {
     ScratchPlan p{};
     const int64_t ldW = r4(std::max<int64_t>(W, 1));
     int64_t off = 0;
@@ -45,7 +68,7 @@ ScratchPlan plan_scratch(int64_t n, int64_t naux, int64_t W) {
     p.aux = take(4 * naux * ldW);
     p.T = take(4 * n * ldW);
     p.gemm_part_floats = gemm_part_bound(W);
-    p.gemm_part = take(4 * 2 * p.gemm_part_floats);
+    p.gemm_part = take(4 * 2 * p.gemm_part_floats * part_regions);
     p.rowloss = take(4 * std::max<int64_t>(n, 1));
     p.rowflag = take(4 * std::max<int64_t>(n, 1));
     p.total = off;
@@ -403,7 +426,8 @@ int do_classifier_bwd(const char* fn, int32_t n, int32_t K, int32_t C,
                       float* Wc, float* bc, const OptimArgs& oa, const OptState& st,
                       float* G_out, int64_t ldg, float* dWc_out, float* dbc_out, bool bf16,
                       const ScratchPlan& sp, void* ws, hipStream_t s,
-                      const ClsCopies* c = nullptr) {
+                      const ClsCopies* c = nullptr, SgdList* defer = nullptr,
+                      int region = 0) {
     if (G_out) {
         GemmBatch b;
         std::memset(&b, 0, sizeof(b));
@@ -442,7 +466,7 @@ int do_classifier_bwd(const char* fn, int32_t n, int32_t K, int32_t C,
     std::memset(&b, 0, sizeof(b));
     b.nprob = 1;
     b.tbm = bf16 ? 0 : 32;
-    b.p[0] = dw_problem(n, K, bc != nullptr, C, H, ldh, dZ, ldd, fptr(ws, sp.gemm_part), 1,
+    b.p[0] = dw_problem(n, K, bc != nullptr, C, H, ldh, dZ, ldd, part_region(ws, sp, region), 1,
                         bf16 ? 128 : 32);
     if (c) {
         b.p[0].hA0 = b.p[0].hA1 = c->H;
@@ -452,7 +476,7 @@ int do_classifier_bwd(const char* fn, int32_t n, int32_t K, int32_t C,
     }
     GCN_HIP(launch_gemm(b, A_KM, B_KN, EPI_PARTIAL, ROLE_CLS_DW, bf16, s), fn);
     SgdProblem q = with_state(sgd_problem(b.p[0], K, C, Wc, bc, dWc_out, dbc_out), st);
-    GCN_HIP(launch_sgd_reduce(&q, 1, oa, s), fn);
+    GCN_HIP(sgd_now_or_later(&q, 1, oa, defer, s), fn);
     return GCN_OK;
 }
 
@@ -463,7 +487,8 @@ int do_layer_bwd(const char* fn, const gcn_dgraph* g, int32_t F, int32_t h,
                  const OptState& st_neigh, float* G_in, int64_t ldgi,
                  float* dWs_out, float* dWn_out, float* db_out, bool bf16,
                  const ScratchPlan& sp, void* ws, hipStream_t s,
-                 const LayerCopies* c = nullptr, bool first = false) {
+                 const LayerCopies* c = nullptr, bool first = false, SgdList* defer = nullptr,
+                 int region = 0) {
     const int32_t n = g->n;
     if (G_in) {
         // T = A D^-1 G[:, h:]  (Eq. 2c), then G_in = [G_self | T] [W_self; W_neigh]^T;
@@ -515,7 +540,7 @@ int do_layer_bwd(const char* fn, const gcn_dgraph* g, int32_t F, int32_t h,
     GemmBatch b;
     std::memset(&b, 0, sizeof(b));
     b.nprob = 2;
-    float* part0 = fptr(ws, sp.gemm_part);
+    float* part0 = part_region(ws, sp, region);
     float* part1 = part0 + sp.gemm_part_floats;
     const bool ones = bias != nullptr;
     // fp32 first layer: 32 x 128 tiles (M = f_in + bias row is padded to a
@@ -538,7 +563,7 @@ int do_layer_bwd(const char* fn, const gcn_dgraph* g, int32_t F, int32_t h,
         with_state(sgd_problem(b.p[1], F, h, Wn, bias ? bias + h : nullptr, dWn_out,
                                db_out ? db_out + h : nullptr),
                    st_neigh)};
-    GCN_HIP(launch_sgd_reduce(q, 2, oa, s), fn);
+    GCN_HIP(sgd_now_or_later(q, 2, oa, defer, s), fn);
     return GCN_OK;
 }
 
@@ -604,7 +629,7 @@ int do_layer_bwd_narrow(const char* fn, const gcn_dgraph* g, int32_t F, int32_t 
                         const OptState& st_neigh, float* G_in, int64_t ldgi,
                         float* dWs_out, float* dWn_out, bool bf16, const ScratchPlan& sp,
                         void* ws, hipStream_t s, const LayerCopies* c = nullptr,
-                        bool first = false) {
+                        bool first = false, SgdList* defer = nullptr, int region = 0) {
     const int32_t n = g->n;
     float* T = fptr(ws, sp.T);
     const int64_t ldt = ldg <= sp.ld_max ? ldg : r4(h);
@@ -652,7 +677,7 @@ int do_layer_bwd_narrow(const char* fn, const gcn_dgraph* g, int32_t F, int32_t 
     GemmBatch b;
     std::memset(&b, 0, sizeof(b));
     b.nprob = 2;
-    float* part0 = fptr(ws, sp.gemm_part);
+    float* part0 = part_region(ws, sp, region);
     float* part1 = part0 + sp.gemm_part_floats;
     const int tm = (first && !bf16) ? 32 : 128;   // as in the paper order
     b.tbm = tm == 32 ? 32 : 0;
@@ -670,7 +695,7 @@ int do_layer_bwd_narrow(const char* fn, const gcn_dgraph* g, int32_t F, int32_t 
     SgdProblem q[2] = {
         with_state(sgd_problem(b.p[0], F, h, Ws, nullptr, dWs_out, nullptr), st_self),
         with_state(sgd_problem(b.p[1], F, h, Wn, nullptr, dWn_out, nullptr), st_neigh)};
-    GCN_HIP(launch_sgd_reduce(q, 2, oa, s), fn);
+    GCN_HIP(sgd_now_or_later(q, 2, oa, defer, s), fn);
     return GCN_OK;
 }
 
@@ -775,7 +800,7 @@ int plan_step(const gcn_dgraph* g, const gcn_model_desc* d, StepLayout* out) {
         cp.dZ = take(2 * n * cp.ld_dz);
     }
     const int64_t W = std::max<int64_t>({(int64_t)d->f_in, 2 * (int64_t)d->h, (int64_t)d->C});
-    out->sp = plan_scratch(n, g->naux, W);
+    out->sp = plan_scratch(n, g->naux, W, d->L + 1);
     out->pub.scratch = off;
     out->pub.scratch_bytes = out->sp.total;
     out->pub.status = out->pub.scratch + out->sp.status;
@@ -1210,7 +1235,9 @@ int train_step_impl(const char* fn, const gcn_dgraph* g, const gcn_model_desc* d
                               iptr(scratch, sp.status), loss_out, s,
                               cp.on ? h16(cp.dZ) : nullptr, cp.ld_dz),
             fn);
-    // backward (classifier, then Eq. 2a-2c layer by layer)
+    // backward (classifier, then Eq. 2a-2c layer by layer); every weight's
+    // input gradient is formed before the one launch that updates them all
+    SgdList updates;
     float* Gcur = act(sl.pub.G[L - 1]);
     OptState cst;
     if (st1) {
@@ -1230,7 +1257,7 @@ int train_step_impl(const char* fn, const gcn_dgraph* g, const gcn_model_desc* d
                               d->has_bias ? P->b_cls : nullptr, oa, cst, Gcur, ldH,
                               grads ? grads->W_cls : nullptr,
                               grads ? grads->b_cls : nullptr, bf16, sp, scratch, s,
-                              cp.on ? &cc : nullptr));
+                              cp.on ? &cc : nullptr, &updates, L));
     for (int l = L - 1; l >= 0; --l) {
         const int32_t F = l == 0 ? d->f_in : 2 * h;
         const float* Hin = l == 0 ? X : act(sl.H32[l - 1]);
@@ -1243,7 +1270,7 @@ int train_step_impl(const char* fn, const gcn_dgraph* g, const gcn_model_desc* d
                                         layer_state(d, st1, st2, l, 1), Gnext, ldH,
                                         grads ? grads->W_self[l] : nullptr,
                                         grads ? grads->W_neigh[l] : nullptr, bf16, sp, scratch,
-                                        s, cp.on ? &lc : nullptr, l == 0));
+                                        s, cp.on ? &lc : nullptr, l == 0, &updates, l));
             Gcur = Gnext;
             continue;
         }
@@ -1254,9 +1281,10 @@ int train_step_impl(const char* fn, const gcn_dgraph* g, const gcn_model_desc* d
                              Gnext, ldH, grads ? grads->W_self[l] : nullptr,
                              grads ? grads->W_neigh[l] : nullptr,
                              grads ? grads->b[l] : nullptr, bf16, sp, scratch, s,
-                             cp.on ? &lc : nullptr, l == 0));
+                             cp.on ? &lc : nullptr, l == 0, &updates, l));
         Gcur = Gnext;
     }
+    GCN_HIP(launch_sgd_reduce(updates.p, updates.n, oa, s), fn);
     return GCN_OK;
 }
 

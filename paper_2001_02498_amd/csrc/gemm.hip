@@ -1581,15 +1581,22 @@ __device__ __forceinline__ float opt_update(float w, float d, float* s1, float* 
     }
 }
 
+// The weights of one launch laid end to end: problem i covers elements
+// [end[i - 1], end[i]) (end[-1] = 0).
+struct SgdBatch {
+    SgdProblem p[kMaxSgdProblems];
+    int64_t end[kMaxSgdProblems];
+    int32_t n;
+};
+
 template <int KIND>
-__global__ __launch_bounds__(256) void sgd_reduce_kernel(SgdProblem p0, SgdProblem p1,
-                                                         int64_t total0, int64_t total,
-                                                         OptimArgs o) {
+__global__ __launch_bounds__(256) void sgd_reduce_kernel(SgdBatch b, OptimArgs o) {
     const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (idx >= total) return;
-    const bool second = idx >= total0;
-    const SgdProblem& p = second ? p1 : p0;
-    const int64_t e = second ? idx - total0 : idx;
+    if (idx >= b.end[b.n - 1]) return;
+    int i = 0;
+    while (idx >= b.end[i]) ++i;
+    const SgdProblem& p = b.p[i];
+    const int64_t e = idx - (i > 0 ? b.end[i - 1] : 0);
     const int m = (int)(e / p.N), nn = (int)(e % p.N);
     const float* src = p.part + (int64_t)m * p.ldp + nn;
     const float d = sum_slices(src, p.part_stride, p.splits);
@@ -1890,13 +1897,17 @@ hipError_t launch_to_bf16(const ConvJob* jobs, int njobs, hipStream_t s) {
 hipError_t launch_sgd_reduce(const SgdProblem* p, int nprob, const OptimArgs& o,
                              hipStream_t s) {
     if (nprob <= 0) return hipSuccess;
-    auto count = [](const SgdProblem& q) {
-        return (int64_t)(q.Mw + (q.b ? 1 : 0)) * q.N;
-    };
-    const int64_t t0 = count(p[0]);
-    const int64_t total = t0 + (nprob > 1 ? count(p[1]) : 0);
+    if (nprob > kMaxSgdProblems) return hipErrorInvalidValue;
+    SgdBatch batch;
+    std::memset(&batch, 0, sizeof(batch));
+    int64_t total = 0;
+    for (int i = 0; i < nprob; ++i) {
+        batch.p[i] = p[i];
+        total += (int64_t)(p[i].Mw + (p[i].b ? 1 : 0)) * p[i].N;
+        batch.end[i] = total;
+    }
+    batch.n = nprob;
     if (total == 0) return hipSuccess;
-    const SgdProblem second = nprob > 1 ? p[1] : p[0];
     const int64_t blocks = (total + 255) / 256;
     double flops = 0, bytes = 0;
     // state words read and written per weight: momentum 1, Adam 2
@@ -1909,11 +1920,11 @@ hipError_t launch_sgd_reduce(const SgdProblem* p, int nprob, const OptimArgs& o,
     ProfScope prof(s, K_SGD, flops, bytes);
     const dim3 grid((unsigned)blocks), block(256);
     if (o.kind == OPT_ADAM)
-        sgd_reduce_kernel<OPT_ADAM><<<grid, block, 0, s>>>(p[0], second, t0, total, o);
+        sgd_reduce_kernel<OPT_ADAM><<<grid, block, 0, s>>>(batch, o);
     else if (o.kind == OPT_MOMENTUM)
-        sgd_reduce_kernel<OPT_MOMENTUM><<<grid, block, 0, s>>>(p[0], second, t0, total, o);
+        sgd_reduce_kernel<OPT_MOMENTUM><<<grid, block, 0, s>>>(batch, o);
     else
-        sgd_reduce_kernel<OPT_SGD><<<grid, block, 0, s>>>(p[0], second, t0, total, o);
+        sgd_reduce_kernel<OPT_SGD><<<grid, block, 0, s>>>(batch, o);
     return hipGetLastError();
 }
 

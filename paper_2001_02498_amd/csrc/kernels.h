@@ -173,6 +173,9 @@ struct OptimArgs {
     float lr, mu, b1, b2, eps;
     float c1, c2;   // Adam bias corrections 1 / (1 - b1^t), 1 / (1 - b2^t)
 };
+// Up to kMaxSgdProblems weights (both branches of every layer and the
+// classifier) in one launch.
+constexpr int kMaxSgdProblems = 2 * GCN_MAX_LAYERS + 1;
 hipError_t launch_sgd_reduce(const SgdProblem* p, int nprob, const OptimArgs& o,
                              hipStream_t s);
 
