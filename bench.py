@@ -54,7 +54,7 @@ def parse():
     ap.add_argument("--workers", type=int, default=0,
                     help="host preparation threads of the stream workload (0: min(16, cores))")
     ap.add_argument("--stream-len", type=int, default=64)
-    ap.add_argument("--device-workers", type=int, default=4,
+    ap.add_argument("--device-workers", type=int, default=6,
                     help="stream workload: workers of the pipeline that reduces on the GPU")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="also run one plain device copy of this size (HBM counter "
