@@ -224,6 +224,46 @@ std::vector<Candidate> count_pairs(const Lists& L, int theta, int threads) {
     return count_pairs_t<int32_t>(L, theta, threads);
 }
 
+// Candidates in Algorithm 2's order (weight descending, then (x, y)):
+// with weights below 2^16 and ids below 2^24 the order is that of the
+// 64-bit key (65535 - w, x, y), sorted by four stable passes of 16-bit
+// digits, least significant first; a comparison sort otherwise.
+void sort_candidates(std::vector<Candidate>& c, int32_t ncols) {
+    int32_t wmax = 0;
+    for (const Candidate& e : c) wmax = std::max(wmax, e.w);
+    if (wmax >= 65536 || ncols > (1 << 24) || c.size() < 4096) {
+        std::sort(c.begin(), c.end(), [](const Candidate& a, const Candidate& b) {
+            if (a.w != b.w) return a.w > b.w;
+            return a.x != b.x ? a.x < b.x : a.y < b.y;
+        });
+        return;
+    }
+    const size_t n = c.size();
+    std::vector<uint64_t> key(n), tmp(n);
+    for (size_t i = 0; i < n; ++i)
+        key[i] = ((uint64_t)(65535 - c[i].w) << 48) | ((uint64_t)c[i].x << 24) |
+                 (uint64_t)c[i].y;
+    std::vector<uint32_t> count(65536);
+    for (int pass = 0; pass < 4; ++pass) {
+        const int shift = 16 * pass;
+        std::fill(count.begin(), count.end(), 0u);
+        for (size_t i = 0; i < n; ++i) count[(key[i] >> shift) & 0xFFFF]++;
+        uint32_t run = 0;
+        for (uint32_t& k : count) {
+            const uint32_t v = k;
+            k = run;
+            run += v;
+        }
+        for (size_t i = 0; i < n; ++i) tmp[count[(key[i] >> shift) & 0xFFFF]++] = key[i];
+        key.swap(tmp);
+    }
+    for (size_t i = 0; i < n; ++i) {
+        const uint64_t k = key[i];
+        c[i] = {(int32_t)(65535 - (int32_t)(k >> 48)), (int32_t)((k >> 24) & 0xFFFFFF),
+                (int32_t)(k & 0xFFFFFF)};
+    }
+}
+
 // Algorithm 1 after a round whose greedy scan ran to the end of its
 // candidates. Every pair counted above theta then had an endpoint taken
 // (the matching is maximal), and a pair with neither endpoint taken nor new
@@ -291,10 +331,7 @@ std::vector<Candidate> count_touched_t(const Lists& L, int theta, int threads,
     for (auto& v : out) total += v.size();
     all.reserve(total);
     for (auto& v : out) all.insert(all.end(), v.begin(), v.end());
-    std::sort(all.begin(), all.end(), [](const Candidate& a, const Candidate& b) {
-        if (a.w != b.w) return a.w > b.w;
-        return a.x != b.x ? a.x < b.x : a.y < b.y;
-    });
+    sort_candidates(all, ncols);
     return all;
 }
 
