@@ -278,7 +278,8 @@ typedef struct {
     const int32_t* exp_col;    /* device int32[exp_nnz]: original
                                   vertices of pair sum k, ascending  */
     const int32_t* exp_seg;    /* device int32[4*naux]: (k, begin,
-                                  end, -1) into exp_col              */
+                                  end, -1) into exp_col, longest
+                                  expansion first                    */
     int32_t round_offsets[GCN_MAX_ROUNDS + 1];   /* host copy        */
 } gcn_dgraph;
 

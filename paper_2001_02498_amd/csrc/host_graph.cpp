@@ -3,6 +3,7 @@
 // applied in rounds), plus packing of the device image. CPU only: nothing
 // here calls the HIP runtime, so it also builds and runs without a GPU.
 #include <algorithm>
+#include <array>
 #include <atomic>
 #include <cstring>
 #include <exception>
@@ -832,6 +833,19 @@ int gcn_graph_pack(gcn_reduced_t r, int32_t seg_len, void* host_buf,
         eseg[4 * k + 1] = b;
         eseg[4 * k + 2] = pos;
         eseg[4 * k + 3] = -1;
+    }
+    // Longest expansions first (each entry names its pair sum, so the order
+    // is free): the pair sums of the last rounds, the longest, start first
+    // instead of forming the launch's tail.
+    {
+        std::vector<std::array<int32_t, 4>> ent(r->naux);
+        for (int32_t k = 0; k < r->naux; ++k)
+            for (int j = 0; j < 4; ++j) ent[k][j] = eseg[4 * k + j];
+        std::stable_sort(ent.begin(), ent.end(), [](const auto& a, const auto& b) {
+            return a[2] - a[1] > b[2] - b[1];
+        });
+        for (int32_t k = 0; k < r->naux; ++k)
+            for (int j = 0; j < 4; ++j) eseg[4 * k + j] = ent[k][j];
     }
     return GCN_OK;
 }

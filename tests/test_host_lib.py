@@ -290,11 +290,16 @@ def test_device_image_work_list(seg_len):
     assert (np.diff(bins).max() > G) == (lens.max() > G * L)
     # pair sum k expands into the original vertices of the oracle's expansion
     assert d.naux > 0
-    for k, (kk, b, e, slot) in enumerate(sec["exp_seg"]):
-        assert kk == k and slot == -1
-        want = sorted(rd.expand(wl.n + k, wl.n, info["pairs"]))
+    # (entries longest expansion first, each naming its pair sum)
+    eseg = sec["exp_seg"]
+    assert sorted(eseg[:, 0].tolist()) == list(range(d.naux))
+    lens = eseg[:, 2] - eseg[:, 1]
+    assert np.all(np.diff(lens) <= 0)
+    for kk, b, e, slot in eseg:
+        assert slot == -1
+        want = sorted(rd.expand(wl.n + kk, wl.n, info["pairs"]))
         assert sec["exp_col"][b:e].tolist() == want
-    assert sec["exp_seg"][-1][2] == d.exp_nnz
+    assert eseg[:, 2].max() == d.exp_nnz and lens.sum() == d.exp_nnz
     # image corruption is rejected
     bad = buf.copy()
     bad[:4] = 0
