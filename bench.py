@@ -42,6 +42,9 @@ def parse():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="yelp10k")
     ap.add_argument("--profile-steps", type=int, default=10)
+    ap.add_argument("--theta", type=int, default=None,
+                    help="reduction threshold (pairs held by more lists than this are summed "
+                         "ahead); default: the workload's")
     ap.add_argument("--seg-len", type=int, default=0,
                     help="list segment length of the device work list (0: library default)")
     ap.add_argument("--precision", choices=("fp32", "bf16"), default="fp32",
@@ -1241,6 +1244,8 @@ def main():
         print(json.dumps(run_sampled(args)), flush=True)
         return
     wl = synth.WORKLOADS[args.workload]
+    if args.theta is not None:
+        wl = dataclasses.replace(wl, theta=args.theta)
     inp = synth.make_inputs(wl)
     print(f"[bench] workload {wl.name}: inputs ready", file=sys.stderr, flush=True)
 
