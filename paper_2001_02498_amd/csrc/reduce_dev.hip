@@ -9,7 +9,7 @@
 //                leave as 64-bit keys ordered by (weight descending, x, y).
 //   Algorithm 2  the keys are radix-sorted (rocPRIM); one workgroup scans
 //                them in blocks, drops pairs with a used endpoint in
-//                parallel and takes the rest in key order with one thread:
+//                parallel and takes the rest in key order with one wavefront:
 //                the greedy matching under the budget, pair by pair as the
 //                host takes it.
 //   Algorithm 3  every list is rewritten by one workgroup (its ids marked
@@ -430,47 +430,51 @@ __global__ __launch_bounds__(kGreedyThreads) void greedy_kernel(
             const uint64_t* S = surv[buf];
             const int end = min(cnt, pos + kGreedyBurst);
             if (wave == 0) {
-                long long taken = s_taken, wsum = s_wsum;
+                long long taken = s_taken;
+                long long wl = 0;   // weights of this lane's taken pairs
                 bool halt = false;
                 for (int c0 = pos; c0 < end && !halt; c0 += 64) {
                     const int si = c0 + lane;
                     const uint64_t kv = S[si < end ? si : end - 1];
-                    const uint64_t key = si < end ? kv : ~0ull;
-                    const uint32_t x = (uint32_t)(key >> 20) & 0xFFFFFu, y = (uint32_t)key & 0xFFFFFu;
-                    const uint32_t w = 0xFFFFu - (uint32_t)(key >> 40);
-                    bool live = (si < end) & free_pair(kv);
-                    bool took = false;
-                    const long long first = taken;
-                    // the first live pair is taken; later ones sharing an
-                    // endpoint with it drop (register compares only: the
-                    // used set and the output follow after the chunk)
-                    uint64_t m = __ballot(live);
+                    const uint32_t x = (uint32_t)(kv >> 20) & 0xFFFFFu, y = (uint32_t)kv & 0xFFFFFu;
+                    const uint32_t w = 0xFFFFu - (uint32_t)(kv >> 40);
+                    // live lanes as one wave-uniform mask: the first is
+                    // taken and every lane sharing an endpoint with it
+                    // leaves the mask (one compare per lane and a ballot
+                    // per pair; the used set and the output follow after
+                    // the chunk)
+                    uint64_t m = __builtin_amdgcn_ballot_w64((si < end) & free_pair(kv));
+                    uint64_t tm = 0;
+                    const long long room = budget - taken;
+                    long long got = 0;
                     while (m) {
-                        if (taken >= budget) {
+                        if (got >= room) {
                             halt = true;
                             break;
                         }
-                        const int j = __ffsll((long long)m) - 1;
+                        const int j = (int)__builtin_ctzll(m);
                         const uint32_t xj = __builtin_amdgcn_readlane(x, j);
                         const uint32_t yj = __builtin_amdgcn_readlane(y, j);
-                        wsum += __builtin_amdgcn_readlane(w, j);
-                        took |= lane == j;
-                        ++taken;
-                        live = live && lane > j && x != xj && x != yj && y != xj && y != yj;
-                        m = __ballot(live);
+                        tm |= 1ull << j;
+                        ++got;
+                        m &= ~__builtin_amdgcn_ballot_w64((x == xj) | (x == yj) | (y == xj) |
+                                                          (y == yj));
                     }
-                    const uint64_t tm = __ballot(took);
-                    if (took) {
+                    const long long first = taken;
+                    taken += got;
+                    if ((tm >> lane) & 1ull) {
                         const long long r = first + lanes_below(tm);
+                        wl += w;
                         atomicOr(&used[x >> 5], 1u << (x & 31));
                         atomicOr(&used[y >> 5], 1u << (y & 31));
                         pairs[2 * r] = (int32_t)x;
                         pairs[2 * r + 1] = (int32_t)y;
                     }
                 }
+                for (int off = 32; off > 0; off >>= 1) wl += __shfl_xor(wl, off);
                 if (lane == 0) {
                     s_taken = taken;
-                    s_wsum = wsum;
+                    s_wsum += wl;
                     if (halt || taken >= budget) stop = 1;
                 }
             }
