@@ -36,6 +36,7 @@ namespace {
 
 constexpr int kBlock = 256;
 constexpr int kScanThreads = 1024;
+constexpr int kScanPer = 4;                           // consecutive values per thread per tile
 constexpr int kGreedyThreads = 1024;
 constexpr int kGreedyPer = 4;                         // keys per thread per block
 constexpr int kGreedyBurst = 256;                     // survivors taken between refilters
@@ -71,48 +72,72 @@ __device__ __forceinline__ uint64_t cand_key(uint32_t w, uint32_t x, uint32_t y)
 }
 
 // ------------------------------------------------------------------ scan
-// out[0] = 0, out[i + 1] = in[0] + .. + in[i]  (one workgroup); with
-// num_add, also the sum of max(in[i] - 1, 0) (numAdd of Section 3.2 when
-// in holds list lengths)
-__global__ __launch_bounds__(kScanThreads) void scan_kernel(const int32_t* __restrict__ in,
+// out[0] = 0, out[i + 1] = in[0] + .. + in[i] (one workgroup, tiles of
+// kScanPer consecutive values per thread, all loaded before any is used: a
+// scan inside the thread, one across the wavefront by shuffles, one across
+// the 16 wavefront totals); cur, when
+// set, also receives the exclusive prefix out[i] for i < len (it may be
+// in itself: every value is read by the thread that overwrites it, before
+// it does); with num_add, also the sum of max(in[i] - 1, 0) (numAdd of
+// Section 3.2 when in holds list lengths)
+__global__ __launch_bounds__(kScanThreads) void scan_kernel(const int32_t* in,
                                                             int32_t* __restrict__ out, int len,
+                                                            int32_t* cur,
                                                             unsigned long long* num_add,
                                                             long long* total) {
-    __shared__ int32_t part[kScanThreads];
-    __shared__ unsigned long long adds[kScanThreads / 64];
-    const int t = threadIdx.x;
-    const int per = (len + kScanThreads - 1) / kScanThreads;
-    const int b = min(len, t * per), e = min(len, b + per);
-    int32_t s = 0;
+    constexpr int kWaves = kScanThreads / 64;
+    __shared__ int32_t wsum[kWaves];
+    __shared__ unsigned long long adds[kWaves];
+    const int t = threadIdx.x, lane = t % 64, wave = t / 64;
+    int32_t carry = 0;   // sum of the earlier tiles
     unsigned long long a = 0;
-    for (int i = b; i < e; ++i) {
-        s += in[i];
-        a += in[i] > 1 ? (unsigned long long)(in[i] - 1) : 0ull;
+    if (t == 0) out[0] = 0;
+    for (int base = 0; base < len; base += kScanPer * kScanThreads) {
+        const int i0 = base + kScanPer * t;
+        int32_t v[kScanPer], incl[kScanPer];
+#pragma unroll
+        for (int j = 0; j < kScanPer; ++j) v[j] = i0 + j < len ? in[i0 + j] : 0;
+#pragma unroll
+        for (int j = 0; j < kScanPer; ++j) {
+            a += v[j] > 1 ? (unsigned long long)(v[j] - 1) : 0ull;
+            incl[j] = (j ? incl[j - 1] : 0) + v[j];
+        }
+        int32_t inc = incl[kScanPer - 1];
+        for (int off = 1; off < 64; off <<= 1) {
+            const int32_t y = __shfl_up(inc, off);
+            if (lane >= off) inc += y;
+        }
+        if (lane == 63) wsum[wave] = inc;
+        __syncthreads();
+        int32_t before = carry, tile = 0;
+#pragma unroll
+        for (int w = 0; w < kWaves; ++w) {
+            const int32_t x = wsum[w];
+            before += w < wave ? x : 0;
+            tile += x;
+        }
+        const int32_t ex = before + inc - incl[kScanPer - 1];   // values before this thread's
+#pragma unroll
+        for (int j = 0; j < kScanPer; ++j) {
+            if (i0 + j < len) {
+                out[i0 + j + 1] = ex + incl[j];
+                if (cur) cur[i0 + j] = ex + incl[j] - v[j];
+            }
+        }
+        carry += tile;
+        __syncthreads();   // wsum is rewritten by the next tile
     }
     if (num_add) {
         for (int off = 32; off > 0; off >>= 1) a += __shfl_xor(a, off);
-        if (t % 64 == 0) adds[t / 64] = a;
-    }
-    part[t] = s;
-    __syncthreads();
-    if (num_add && t == 0) {
-        unsigned long long tot = 0;
-        for (int w = 0; w < kScanThreads / 64; ++w) tot += adds[w];
-        *num_add = tot;
-    }
-    for (int off = 1; off < kScanThreads; off <<= 1) {
-        const int32_t v = t >= off ? part[t - off] : 0;
+        if (lane == 0) adds[wave] = a;
         __syncthreads();
-        part[t] += v;
-        __syncthreads();
+        if (t == 0) {
+            unsigned long long tot = 0;
+            for (int w = 0; w < kWaves; ++w) tot += adds[w];
+            *num_add = tot;
+        }
     }
-    int32_t run = part[t] - s;   // exclusive prefix of this chunk
-    if (t == 0) out[0] = 0;
-    for (int i = b; i < e; ++i) {
-        run += in[i];
-        out[i + 1] = run;
-    }
-    if (total && t == kScanThreads - 1) *total = part[t];
+    if (total && t == 0) *total = carry;
 }
 
 __global__ void fill_kernel(int32_t* __restrict__ p, int32_t v, int64_t len) {
@@ -159,6 +184,93 @@ __global__ __launch_bounds__(kBlock) void tfill_kernel(int n, const int32_t* __r
         const int k = atomicAdd(&tcur[c], 1);
         tlist[k] = w;
         tpos[k] = e - b;
+    }
+}
+
+// The same two steps with the counts gathered per workgroup first, for id
+// ranges whose counters fit LDS: a workgroup takes kTransLists consecutive
+// lists (one wavefront per list), counts their ids in LDS, then adds each
+// nonzero count to the global one, so an id held by many lists (a hub)
+// costs one global atomic per workgroup instead of one per list. The fill
+// reserves each id's run of slots the same way, then hands the slots out
+// from LDS.
+constexpr int kTransLists = 32;
+constexpr int kTransMaxIds = 16384;   // 64 KB of LDS counters
+
+__device__ __forceinline__ void trans_count(int n, int nc, const int32_t* __restrict__ rowptr,
+                                            const int32_t* __restrict__ col, int32_t* cnt,
+                                            DevState* st) {
+    const int ncols = min(n + (int)st->naux, nc);
+    for (int i = threadIdx.x; i < nc; i += kBlock) cnt[i] = 0;
+    __syncthreads();
+    const int lane = threadIdx.x % 64;
+    const int w1 = min(n, (int)(blockIdx.x + 1) * kTransLists);
+    for (int w = blockIdx.x * kTransLists + threadIdx.x / 64; w < w1; w += kBlock / 64) {
+        for (int e = rowptr[w] + lane; e < rowptr[w + 1]; e += 64) {
+            const int c = col[e];
+            if (c < 0 || c >= ncols) {
+                st->error = 2;
+                continue;
+            }
+            atomicAdd(&cnt[c], 1);
+        }
+    }
+    __syncthreads();
+}
+
+__global__ __launch_bounds__(kBlock) void tcount_lds_kernel(int n, int nc,
+                                                            const int32_t* __restrict__ rowptr,
+                                                            const int32_t* __restrict__ col,
+                                                            int32_t* __restrict__ tcnt,
+                                                            DevState* st) {
+    extern __shared__ int32_t trans_cnt[];
+    if (st->done) return;
+    trans_count(n, nc, rowptr, col, trans_cnt, st);
+    for (int i = threadIdx.x; i < nc; i += kBlock) {
+        const int v = trans_cnt[i];
+        if (v) atomicAdd(&tcnt[i], v);
+    }
+}
+
+__global__ __launch_bounds__(kBlock) void tfill_lds_kernel(int n, int nc,
+                                                           const int32_t* __restrict__ rowptr,
+                                                           const int32_t* __restrict__ col,
+                                                           int32_t* __restrict__ tcur,
+                                                           int32_t* __restrict__ tlist,
+                                                           int32_t* __restrict__ tpos,
+                                                           DevState* st) {
+    extern __shared__ int32_t trans_cnt[];
+    if (st->done) return;
+    trans_count(n, nc, rowptr, col, trans_cnt, st);
+    // this workgroup's slots of id i start where the cursor stood (eight
+    // ids per thread at a time, so their atomics are in flight together)
+    for (int i0 = threadIdx.x; i0 < nc; i0 += 8 * kBlock) {
+        int v[8], r[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+            const int i = i0 + u * kBlock;
+            v[u] = i < nc ? trans_cnt[i] : 0;
+        }
+#pragma unroll
+        for (int u = 0; u < 8; ++u)
+            if (v[u]) r[u] = atomicAdd(&tcur[i0 + u * kBlock], v[u]);
+#pragma unroll
+        for (int u = 0; u < 8; ++u)
+            if (v[u]) trans_cnt[i0 + u * kBlock] = r[u];
+    }
+    __syncthreads();
+    const int ncols = min(n + (int)st->naux, nc);
+    const int lane = threadIdx.x % 64;
+    const int w1 = min(n, (int)(blockIdx.x + 1) * kTransLists);
+    for (int w = blockIdx.x * kTransLists + threadIdx.x / 64; w < w1; w += kBlock / 64) {
+        const int b = rowptr[w];
+        for (int e = b + lane; e < rowptr[w + 1]; e += 64) {
+            const int c = col[e];
+            if (c < 0 || c >= ncols) continue;
+            const int k = atomicAdd(&trans_cnt[c], 1);
+            tlist[k] = w;
+            tpos[k] = e - b;
+        }
     }
 }
 
@@ -811,13 +923,34 @@ int redundancy_reduce_device(const int32_t* rowptr_h, const int32_t* col_h, int6
         const int32_t nc_ub = (int32_t)std::min<int64_t>(ncols_ub, dp.ncols_cap);
         // Algorithm 1: transposed index, then pair counts per id
         fill_kernel<<<items_grid(nc_ub), kBlock, 0, s>>>(I(dp.tcur), 0, nc_ub);
-        tcount_kernel<<<waves_grid(n), kBlock, 0, s>>>((int)n, rowptr[cur], col[cur], I(dp.tcur),
-                                                        dst);
-        scan_kernel<<<1, kScanThreads, 0, s>>>(I(dp.tcur), I(dp.tptr), nc_ub, nullptr, nullptr);
-        GCN_DR(hipMemcpyAsync(I(dp.tcur), I(dp.tptr), 4 * (size_t)nc_ub, hipMemcpyDeviceToDevice, s),
-               "cursor");
-        tfill_kernel<<<waves_grid(n), kBlock, 0, s>>>((int)n, rowptr[cur], col[cur], I(dp.tcur),
-                                                       I(dp.tlist), I(dp.tpos), dst);
+        const bool trans_lds = nc_ub <= kTransMaxIds;
+        const dim3 trans_grid((unsigned)((n + kTransLists - 1) / kTransLists));
+        if (trans_lds && 4 * (size_t)nc_ub > 48 * 1024) {
+            GCN_DR(hipFuncSetAttribute((const void*)tcount_lds_kernel,
+                                       hipFuncAttributeMaxDynamicSharedMemorySize,
+                                       4 * kTransMaxIds),
+                   "transposed index LDS");
+            GCN_DR(hipFuncSetAttribute((const void*)tfill_lds_kernel,
+                                       hipFuncAttributeMaxDynamicSharedMemorySize,
+                                       4 * kTransMaxIds),
+                   "transposed index LDS");
+        }
+        if (trans_lds)
+            tcount_lds_kernel<<<trans_grid, kBlock, 4 * (size_t)nc_ub, s>>>(
+                (int)n, nc_ub, rowptr[cur], col[cur], I(dp.tcur), dst);
+        else
+            tcount_kernel<<<waves_grid(n), kBlock, 0, s>>>((int)n, rowptr[cur], col[cur],
+                                                            I(dp.tcur), dst);
+        // tptr from the counts; the counts become the fill cursors
+        scan_kernel<<<1, kScanThreads, 0, s>>>(I(dp.tcur), I(dp.tptr), nc_ub, I(dp.tcur), nullptr,
+                                               nullptr);
+        if (trans_lds)
+            tfill_lds_kernel<<<trans_grid, kBlock, 4 * (size_t)nc_ub, s>>>(
+                (int)n, nc_ub, rowptr[cur], col[cur], I(dp.tcur), I(dp.tlist), I(dp.tpos), dst);
+        else
+            tfill_kernel<<<waves_grid(n), kBlock, 0, s>>>((int)n, rowptr[cur], col[cur],
+                                                           I(dp.tcur), I(dp.tlist), I(dp.tpos),
+                                                           dst);
         const size_t lds = 4 * (size_t)((std::min<int64_t>(nc_ub, kCountWindow) + 1) / 2);
         if (lds > 48 * 1024)
             GCN_DR(hipFuncSetAttribute((const void*)count_pairs_kernel,
@@ -878,7 +1011,7 @@ int redundancy_reduce_device(const int32_t* rowptr_h, const int32_t* col_h, int6
                                                                     I(dp.partner), I(dp.newid), 0);
         rewrite_count_kernel<<<(unsigned)n, kRowThreads, bits, s>>>(
             (int)n, dst, round, rowptr[cur], col[cur], I(dp.partner), I(dp.rowlen));
-        scan_kernel<<<1, kScanThreads, 0, s>>>(I(dp.rowlen), rowptr[nxt], (int)n,
+        scan_kernel<<<1, kScanThreads, 0, s>>>(I(dp.rowlen), rowptr[nxt], (int)n, nullptr,
                                                &dst->round[round].num_add,
                                                &dst->round[round].nnz);
         rewrite_fill_kernel<<<(unsigned)n, kRowThreads, bits, s>>>(
