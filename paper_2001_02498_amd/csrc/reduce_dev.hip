@@ -542,8 +542,7 @@ __global__ __launch_bounds__(kGreedyThreads) void greedy_kernel(
             const uint64_t* S = surv[buf];
             const int end = min(cnt, pos + kGreedyBurst);
             if (wave == 0) {
-                long long taken = s_taken;
-                long long wl = 0;   // weights of this lane's taken pairs
+                long long taken = s_taken, wsum = s_wsum;
                 bool halt = false;
                 for (int c0 = pos; c0 < end && !halt; c0 += 64) {
                     const int si = c0 + lane;
@@ -567,26 +566,27 @@ __global__ __launch_bounds__(kGreedyThreads) void greedy_kernel(
                         const int j = (int)__builtin_ctzll(m);
                         const uint32_t xj = __builtin_amdgcn_readlane(x, j);
                         const uint32_t yj = __builtin_amdgcn_readlane(y, j);
+                        wsum += __builtin_amdgcn_readlane(w, j);
                         tm |= 1ull << j;
                         ++got;
-                        m &= ~__builtin_amdgcn_ballot_w64((x == xj) | (x == yj) | (y == xj) |
-                                                          (y == yj));
+                        m &= ~(__builtin_amdgcn_ballot_w64(x == xj) |
+                               __builtin_amdgcn_ballot_w64(x == yj) |
+                               __builtin_amdgcn_ballot_w64(y == xj) |
+                               __builtin_amdgcn_ballot_w64(y == yj));
                     }
                     const long long first = taken;
                     taken += got;
                     if ((tm >> lane) & 1ull) {
                         const long long r = first + lanes_below(tm);
-                        wl += w;
                         atomicOr(&used[x >> 5], 1u << (x & 31));
                         atomicOr(&used[y >> 5], 1u << (y & 31));
                         pairs[2 * r] = (int32_t)x;
                         pairs[2 * r + 1] = (int32_t)y;
                     }
                 }
-                for (int off = 32; off > 0; off >>= 1) wl += __shfl_xor(wl, off);
                 if (lane == 0) {
                     s_taken = taken;
-                    s_wsum += wl;
+                    s_wsum = wsum;
                     if (halt || taken >= budget) stop = 1;
                 }
             }
