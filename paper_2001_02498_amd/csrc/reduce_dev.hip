@@ -2,8 +2,9 @@
 // rounds), with results identical to the host version in host_graph.cpp.
 //
 // One round:
-//   Algorithm 1  transposed index of the lists (which lists hold each id and
-//                where), then one workgroup per id x counts, in 16-bit LDS
+//   Algorithm 1  transposed index of the lists (for each id, the stretch
+//                after it in every list holding it), then one workgroup
+//                per id x counts, in 16-bit LDS
 //                counters (65,536 ids per pass), every larger id y that
 //                follows x in a list holding x; pairs above the threshold
 //                leave as 64-bit keys ordered by (weight descending, x, y).
@@ -165,25 +166,27 @@ __global__ __launch_bounds__(kBlock) void tcount_kernel(int n, const int32_t* __
     }
 }
 
-// tlist[k] / tpos[k]: the list holding id c and c's position in it, for k in
-// [tptr[c], tptr[c + 1]) (any order inside: the counts do not depend on it)
+// For k in [tptr[c], tptr[c + 1]), one per list holding id c (any order
+// inside: the counts do not depend on it): tnext[k], the position in col of
+// the entry after c in that list, and tend[k], the list's end, so the pair
+// counting reads the stretch after c without looking up the list.
 __global__ __launch_bounds__(kBlock) void tfill_kernel(int n, const int32_t* __restrict__ rowptr,
                                                        const int32_t* __restrict__ col,
                                                        int32_t* __restrict__ tcur,
-                                                       int32_t* __restrict__ tlist,
-                                                       int32_t* __restrict__ tpos,
+                                                       int32_t* __restrict__ tnext,
+                                                       int32_t* __restrict__ tend,
                                                        const DevState* st) {
     const int w = blockIdx.x * (kBlock / 64) + threadIdx.x / 64;
     const int lane = threadIdx.x % 64;
     if (w >= n || st->done) return;
     const int ncols = n + (int)st->naux;
-    const int b = rowptr[w];
-    for (int e = b + lane; e < rowptr[w + 1]; e += 64) {
+    const int end = rowptr[w + 1];
+    for (int e = rowptr[w] + lane; e < end; e += 64) {
         const int c = col[e];
         if (c < 0 || c >= ncols) continue;
         const int k = atomicAdd(&tcur[c], 1);
-        tlist[k] = w;
-        tpos[k] = e - b;
+        tnext[k] = e + 1;
+        tend[k] = end;
     }
 }
 
@@ -236,8 +239,8 @@ __global__ __launch_bounds__(kBlock) void tfill_lds_kernel(int n, int nc,
                                                            const int32_t* __restrict__ rowptr,
                                                            const int32_t* __restrict__ col,
                                                            int32_t* __restrict__ tcur,
-                                                           int32_t* __restrict__ tlist,
-                                                           int32_t* __restrict__ tpos,
+                                                           int32_t* __restrict__ tnext,
+                                                           int32_t* __restrict__ tend,
                                                            DevState* st) {
     extern __shared__ int32_t trans_cnt[];
     if (st->done) return;
@@ -263,13 +266,13 @@ __global__ __launch_bounds__(kBlock) void tfill_lds_kernel(int n, int nc,
     const int lane = threadIdx.x % 64;
     const int w1 = min(n, (int)(blockIdx.x + 1) * kTransLists);
     for (int w = blockIdx.x * kTransLists + threadIdx.x / 64; w < w1; w += kBlock / 64) {
-        const int b = rowptr[w];
-        for (int e = b + lane; e < rowptr[w + 1]; e += 64) {
+        const int end = rowptr[w + 1];
+        for (int e = rowptr[w] + lane; e < end; e += 64) {
             const int c = col[e];
             if (c < 0 || c >= ncols) continue;
             const int k = atomicAdd(&trans_cnt[c], 1);
-            tlist[k] = w;
-            tpos[k] = e - b;
+            tnext[k] = e + 1;
+            tend[k] = end;
         }
     }
 }
@@ -302,9 +305,9 @@ __device__ __forceinline__ int lower_bound_dev(const int32_t* __restrict__ a, in
 }
 
 __global__ __launch_bounds__(kCountThreads) void count_pairs_kernel(
-    int n, int theta, const int32_t* __restrict__ rowptr, const int32_t* __restrict__ col,
-    const int32_t* __restrict__ tptr, const int32_t* __restrict__ tlist,
-    const int32_t* __restrict__ tpos, uint64_t* __restrict__ cand, int64_t cap,
+    int n, int theta, const int32_t* __restrict__ col,
+    const int32_t* __restrict__ tptr, const int32_t* __restrict__ tnext,
+    const int32_t* __restrict__ tend, uint64_t* __restrict__ cand, int64_t cap,
     DevState* st, int round) {
     extern __shared__ uint32_t cnt[];
     __shared__ int32_t s_start[kCountStage];
@@ -338,8 +341,8 @@ __global__ __launch_bounds__(kCountThreads) void count_pairs_kernel(
                     const int i = 2 * t + j;
                     len[j] = 0;
                     if (i < m) {
-                        const int k = kb + i, w = tlist[k];
-                        int b = rowptr[w] + tpos[k] + 1, e = rowptr[w + 1];
+                        const int k = kb + i;
+                        int b = tnext[k], e = tend[k];
                         if (windowed) {
                             b = lower_bound_dev(col, b, e, y0);
                             e = lower_bound_dev(col, b, e, y1);
@@ -786,7 +789,7 @@ struct DevPlan {
     int64_t n, nnz, pairs_cap, ncols_cap, cand_cap;
     size_t sort_tmp;
     // byte offsets in the workspace
-    size_t rowptr[2], col[2], rowlen, scratch, tptr, tcur, tlist, tpos, partner, newid,
+    size_t rowptr[2], col[2], rowlen, scratch, tptr, tcur, tnext, tend, partner, newid,
         keys_in, keys_out, pairs, counters, sort, total;
 };
 
@@ -829,8 +832,8 @@ int plan(const int32_t* rowptr, int64_t n, const gcn_rr_params* p, DevPlan* dp) 
     dp->scratch = take(4 * (size_t)dp->nnz);
     dp->tptr = take(4 * (size_t)(dp->ncols_cap + 1));
     dp->tcur = take(4 * (size_t)dp->ncols_cap);
-    dp->tlist = take(4 * (size_t)dp->nnz);
-    dp->tpos = take(4 * (size_t)dp->nnz);
+    dp->tnext = take(4 * (size_t)dp->nnz);
+    dp->tend = take(4 * (size_t)dp->nnz);
     dp->partner = take(4 * (size_t)dp->ncols_cap);
     dp->newid = take(4 * (size_t)dp->ncols_cap);
     dp->keys_in = take(8 * (size_t)dp->cand_cap);
@@ -946,10 +949,10 @@ int redundancy_reduce_device(const int32_t* rowptr_h, const int32_t* col_h, int6
                                                nullptr);
         if (trans_lds)
             tfill_lds_kernel<<<trans_grid, kBlock, 4 * (size_t)nc_ub, s>>>(
-                (int)n, nc_ub, rowptr[cur], col[cur], I(dp.tcur), I(dp.tlist), I(dp.tpos), dst);
+                (int)n, nc_ub, rowptr[cur], col[cur], I(dp.tcur), I(dp.tnext), I(dp.tend), dst);
         else
             tfill_kernel<<<waves_grid(n), kBlock, 0, s>>>((int)n, rowptr[cur], col[cur],
-                                                           I(dp.tcur), I(dp.tlist), I(dp.tpos),
+                                                           I(dp.tcur), I(dp.tnext), I(dp.tend),
                                                            dst);
         const size_t lds = 4 * (size_t)((std::min<int64_t>(nc_ub, kCountWindow) + 1) / 2);
         if (lds > 48 * 1024)
@@ -957,9 +960,9 @@ int redundancy_reduce_device(const int32_t* rowptr_h, const int32_t* col_h, int6
                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds),
                    "pair counting LDS");
         const unsigned grid = (unsigned)std::min<int64_t>(nc_ub, 4096);
-        count_pairs_kernel<<<grid, kCountThreads, lds, s>>>((int)n, p->theta, rowptr[cur],
-                                                            col[cur], I(dp.tptr), I(dp.tlist),
-                                                            I(dp.tpos), keys_in, dp.cand_cap,
+        count_pairs_kernel<<<grid, kCountThreads, lds, s>>>((int)n, p->theta, col[cur],
+                                                            I(dp.tptr), I(dp.tnext),
+                                                            I(dp.tend), keys_in, dp.cand_cap,
                                                             dst, round);
         GCN_DR(hipGetLastError(), "pair counting");
         // the one wait of the round: the sort needs the candidate count
