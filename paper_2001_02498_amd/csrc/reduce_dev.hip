@@ -781,6 +781,80 @@ __global__ __launch_bounds__(kRowThreads) void rewrite_fill_kernel(
 
 }  // namespace
 
+// Algorithm 3's rewrite with one wavefront per list, for rounds whose ids
+// and new ids fit a wavefront's share of LDS: the list's ids go to the
+// wave's own bitmap and the pairs it keeps to a bitmap of the round's new
+// ids, so prefixes come from ballots and the new ids are written in
+// increasing order by scanning that bitmap, with no workgroup barrier. A
+// wavefront's LDS operations run in program order, so its clears, marks
+// and reads need no wait between them.
+constexpr int kListsPerGroup = kRowThreads / 64;
+constexpr int kWaveMaxIds = 32768;    // ids before the round (1,024 bitmap words)
+constexpr int kWaveMaxNew = 8192;     // pairs the round may take (256 words)
+
+__global__ __launch_bounds__(kRowThreads) void rewrite_fill_wave_kernel(
+    int n, const DevState* st, int round, const int32_t* __restrict__ rowptr,
+    const int32_t* __restrict__ col, const int32_t* __restrict__ partner,
+    const int32_t* __restrict__ newid, const int32_t* __restrict__ rowptr_new,
+    int32_t* __restrict__ col_new, int wstride, int wids) {
+    extern __shared__ uint32_t wbits[];
+    const int lane = threadIdx.x % 64;
+    const int w = blockIdx.x * kListsPerGroup + threadIdx.x / 64;
+    if (w >= n) return;   // the whole wavefront
+    uint32_t* bits = wbits + (threadIdx.x / 64) * wstride;
+    uint32_t* nbits = bits + wids;   // the round's new ids, from ncols on
+    const long long taken = st->round[round].taken;
+    const int ncols = n + (int)(st->naux - taken);   // ids before the round = first new id
+    const int nnew = (int)((taken + 31) / 32);
+    const int b = rowptr[w], d = rowptr[w + 1] - b;
+    const int out = rowptr_new[w], len = rowptr_new[w + 1] - out;
+    const int kept_total = len - (d - len);
+    const int32_t* row = col + b;
+    for (int i = lane; i < (ncols + 31) / 32; i += 64) bits[i] = 0;
+    for (int i = lane; i < nnew; i += 64) nbits[i] = 0;
+    for (int i = lane; i < d; i += 64) {
+        const int32_t c = row[i];
+        atomicOr(&bits[c >> 5], 1u << (c & 31));
+    }
+    int kept = 0;
+    for (int i0 = 0; i0 < d; i0 += 64) {
+        const int i = i0 + lane;
+        int32_t c = -1, p = -1;
+        if (i < d) {
+            c = row[i];
+            p = partner[c];
+        }
+        const bool pair_in = p >= 0 && has(bits, p);
+        const bool keep = i < d && !pair_in;
+        const uint64_t mk = __ballot(keep);
+        if (keep) col_new[out + kept + lanes_below(mk)] = c;
+        kept += __popcll(mk);
+        if (pair_in && c < p) {
+            const int q = newid[c] - ncols;
+            atomicOr(&nbits[q >> 5], 1u << (q & 31));
+        }
+    }
+    // the new ids after the kept entries, in increasing order
+    int added = 0;
+    for (int j0 = 0; j0 < nnew; j0 += 64) {
+        const int j = j0 + lane;
+        uint32_t word = j < nnew ? nbits[j] : 0u;
+        const int cnt = __popc(word);
+        int incl = cnt;
+        for (int off = 1; off < 64; off <<= 1) {
+            const int y = __shfl_up(incl, off);
+            if (lane >= off) incl += y;
+        }
+        int pos = out + kept_total + added + incl - cnt;
+        while (word) {
+            const int bit = __ffs(word) - 1;
+            col_new[pos++] = ncols + 32 * j + bit;
+            word &= word - 1;
+        }
+        added += __shfl(incl, 63);
+    }
+}
+
 // ------------------------------------------------------------ host driver
 
 namespace {
@@ -1012,14 +1086,27 @@ int redundancy_reduce_device(const int32_t* rowptr_h, const int32_t* col_h, int6
         }
         set_partner_kernel<<<items_grid(budget_ub), kBlock, 0, s>>>(pairs, (int)n, dst, round,
                                                                     I(dp.partner), I(dp.newid), 0);
+        // the rewrite: one wavefront per list where its bitmaps fit, else one
+        // workgroup (the new lengths: one workgroup per list, which measured
+        // faster than a wavefront per list)
+        const bool wave_rows = n + naux_known <= kWaveMaxIds && budget_ub <= kWaveMaxNew;
+        const int wids = (int)((n + naux_known + 31) / 32);
+        const int wstride = wids + (int)((std::max<int64_t>(budget_ub, 0) + 31) / 32);
+        const dim3 wave_grid((unsigned)((n + kListsPerGroup - 1) / kListsPerGroup));
+        const size_t wave_lds = 4 * (size_t)kListsPerGroup * wstride;
         rewrite_count_kernel<<<(unsigned)n, kRowThreads, bits, s>>>(
             (int)n, dst, round, rowptr[cur], col[cur], I(dp.partner), I(dp.rowlen));
         scan_kernel<<<1, kScanThreads, 0, s>>>(I(dp.rowlen), rowptr[nxt], (int)n, nullptr,
                                                &dst->round[round].num_add,
                                                &dst->round[round].nnz);
-        rewrite_fill_kernel<<<(unsigned)n, kRowThreads, bits, s>>>(
-            (int)n, dst, round, rowptr[cur], col[cur], I(dp.partner), I(dp.newid), rowptr[nxt],
-            col[nxt], I(dp.scratch));
+        if (wave_rows)
+            rewrite_fill_wave_kernel<<<wave_grid, kRowThreads, wave_lds, s>>>(
+                (int)n, dst, round, rowptr[cur], col[cur], I(dp.partner), I(dp.newid),
+                rowptr[nxt], col[nxt], wstride, wids);
+        else
+            rewrite_fill_kernel<<<(unsigned)n, kRowThreads, bits, s>>>(
+                (int)n, dst, round, rowptr[cur], col[cur], I(dp.partner), I(dp.newid),
+                rowptr[nxt], col[nxt], I(dp.scratch));
         set_partner_kernel<<<items_grid(budget_ub), kBlock, 0, s>>>(pairs, (int)n, dst, round,
                                                                     I(dp.partner), I(dp.newid), 1);
         GCN_DR(hipGetLastError(), "rewrite");
