@@ -76,11 +76,11 @@ __device__ __forceinline__ uint64_t cand_key(uint32_t w, uint32_t x, uint32_t y)
 // out[0] = 0, out[i + 1] = in[0] + .. + in[i] (one workgroup, tiles of
 // kScanPer consecutive values per thread, all loaded before any is used: a
 // scan inside the thread, one across the wavefront by shuffles, one across
-// the 16 wavefront totals); cur, when
-// set, also receives the exclusive prefix out[i] for i < len (it may be
-// in itself: every value is read by the thread that overwrites it, before
-// it does); with num_add, also the sum of max(in[i] - 1, 0) (numAdd of
-// Section 3.2 when in holds list lengths)
+// the 16 wavefront totals). cur, when set, also receives the exclusive
+// prefix out[i] for i < len; it may be in itself, since every value is
+// read by the thread that overwrites it, before it does. With num_add,
+// also the sum of max(in[i] - 1, 0) (numAdd of Section 3.2 when in holds
+// list lengths).
 __global__ __launch_bounds__(kScanThreads) void scan_kernel(const int32_t* in,
                                                             int32_t* __restrict__ out, int len,
                                                             int32_t* cur,
