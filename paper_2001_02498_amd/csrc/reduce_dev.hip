@@ -461,6 +461,21 @@ __device__ __forceinline__ int lanes_below(uint64_t m) {
                                           __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
 }
 
+// Exclusive prefix (for this wavefront) and total of the greedy scan's 16
+// per-wavefront counts, after the barrier that published them: one LDS
+// read and a four-step scan across lanes 0-15 (one DPP row).
+static_assert(kGreedyThreads == 1024, "the wavefront counts fill one 16-lane DPP row");
+__device__ __forceinline__ void wave_prefix(const int32_t* wave_sum, int wave, int lane,
+                                            int* before, int* total) {
+    int v = lane < 16 ? wave_sum[lane] : 0;
+    v += __builtin_amdgcn_update_dpp(0, v, 0x111, 0xF, 0xF, false);   // row_shr:1
+    v += __builtin_amdgcn_update_dpp(0, v, 0x112, 0xF, 0xF, false);   // row_shr:2
+    v += __builtin_amdgcn_update_dpp(0, v, 0x114, 0xF, 0xF, false);   // row_shr:4
+    v += __builtin_amdgcn_update_dpp(0, v, 0x118, 0xF, 0xF, false);   // row_shr:8
+    *total = __builtin_amdgcn_readlane(v, 15);
+    *before = wave ? __builtin_amdgcn_readlane(v, wave - 1) : 0;
+}
+
 // The greedy matching over keys sorted ascending, i.e. weight descending,
 // then (x, y): a pair is taken when neither endpoint is used, while fewer
 // than `budget` pairs were taken this round. Blocks of keys are first
@@ -529,12 +544,8 @@ __global__ __launch_bounds__(kGreedyThreads) void greedy_kernel(
         }
         if (lane == 0) wave_sum[wave] = wtot;
         lds_barrier();
-        int before = 0, nsurv = 0;
-        for (int w = 0; w < kGreedyThreads / 64; ++w) {
-            const int v = wave_sum[w];
-            before += w < wave ? v : 0;
-            nsurv += v;
-        }
+        int before, nsurv;
+        wave_prefix(wave_sum, wave, lane, &before, &nsurv);
         int wpos = before + excl;
 #pragma unroll
         for (int j = 0; j < kGreedyPer; ++j)
@@ -621,11 +632,8 @@ __global__ __launch_bounds__(kGreedyThreads) void greedy_kernel(
                 }
                 if (lane == 63) wave_sum[wave] = inc;
                 lds_barrier();
-                int before = 0, total = 0;
-                for (int w = 0; w < kGreedyThreads / 64; ++w) {
-                    if (w < wave) before += wave_sum[w];
-                    total += wave_sum[w];
-                }
+                int before, total;
+                wave_prefix(wave_sum, wave, lane, &before, &total);
                 int o = before + inc - a;
                 uint64_t* D = surv[buf ^ 1];
 #pragma unroll
