@@ -1079,9 +1079,11 @@ int redundancy_reduce_device(const int32_t* rowptr_h, const int32_t* col_h, int6
         GCN_DR(hipGetLastError(), "matching");
         // Algorithm 3: rewrite every list (a round that took no pair
         // copies the lists unchanged)
+        // pairs this round can take: within the budget and the capacity,
+        // and a matching over the ids so far has at most half as many
         const int64_t budget_ub =
-            std::min<int64_t>(p->max_aux < 0 ? INT64_MAX : p->max_aux - naux_known,
-                              dp.pairs_cap - naux_known);
+            std::min<int64_t>({p->max_aux < 0 ? INT64_MAX : p->max_aux - naux_known,
+                               dp.pairs_cap - naux_known, (n + naux_known) / 2});
         const int nxt = cur ^ 1;
         const size_t bits = 4 * (size_t)((std::min<int64_t>(n + naux_known, kMaxIds) + 31) / 32);
         if (bits > 48 * 1024) {
