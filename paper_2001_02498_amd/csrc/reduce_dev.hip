@@ -45,6 +45,14 @@ constexpr int kGreedyBlock = kGreedyThreads * kGreedyPer;
 // ids per reduction: the greedy scan's used set fills at most 64 KB of LDS
 // (beside its 64 KB of survivor buffers); pair keys hold 20-bit ids
 constexpr int kMaxIds = 1 << 19;
+// Candidate sort: rocPRIM's merge sort up to kMergeSortMax keys, its
+// onesweep radix sort above (the library's default switches at 2^20)
+#ifndef GCN_MERGE_SORT_MAX
+#define GCN_MERGE_SORT_MAX 262144
+#endif
+constexpr size_t kMergeSortMax = GCN_MERGE_SORT_MAX;
+using SortConfig = rocprim::radix_sort_config<rocprim::default_config, rocprim::default_config,
+                                              rocprim::default_config, kMergeSortMax>;
 // ids counted per pass of Algorithm 1: 16-bit counters in 128 KB of LDS
 constexpr int kCountWindow = 65536;
 
@@ -894,12 +902,19 @@ int plan(const int32_t* rowptr, int64_t n, const gcn_rr_params* p, DevPlan* dp) 
     // every candidate has weight >= max(theta + 1, 2), and the pair visits
     // (sum of C(d, 2) over the lists) never grow from round to round
     dp->cand_cap = std::max<int64_t>(1, visits_of(rowptr, n) / std::max(p->theta + 1, 2));
-    size_t tmp = 0;
-    if (rocprim::radix_sort_keys(nullptr, tmp, (uint64_t*)nullptr, (uint64_t*)nullptr,
-                                 (unsigned)std::min<int64_t>(dp->cand_cap, UINT32_MAX), 0, 56,
-                                 (hipStream_t)0) != hipSuccess)
-        return GCN_E_HIP;
-    dp->sort_tmp = tmp;
+    // the sort's scratch: the most either of its algorithms needs (merge
+    // sort up to kMergeSortMax keys, onesweep above)
+    const int64_t sizes[2] = {std::min<int64_t>(dp->cand_cap, UINT32_MAX),
+                              std::min<int64_t>(dp->cand_cap, (int64_t)kMergeSortMax)};
+    dp->sort_tmp = 0;
+    for (const int64_t sz : sizes) {
+        size_t tmp = 0;
+        if (rocprim::radix_sort_keys<SortConfig>(nullptr, tmp, (uint64_t*)nullptr,
+                                                 (uint64_t*)nullptr, (unsigned)sz, 0, 56,
+                                                 (hipStream_t)0) != hipSuccess)
+            return GCN_E_HIP;
+        dp->sort_tmp = std::max(dp->sort_tmp, tmp);
+    }
     size_t off = 0;
     auto take = [&](size_t bytes) {
         size_t o = off;
@@ -1065,8 +1080,8 @@ int redundancy_reduce_device(const int32_t* rowptr_h, const int32_t* col_h, int6
         if (nc == 0) break;
         // Algorithm 2: sort by (weight descending, x, y), then the greedy scan
         size_t tmp = dp.sort_tmp;
-        GCN_DR(rocprim::radix_sort_keys(base + dp.sort, tmp, keys_in, keys_out, (unsigned)nc, 0,
-                                        56, s),
+        GCN_DR(rocprim::radix_sort_keys<SortConfig>(base + dp.sort, tmp, keys_in, keys_out,
+                                                    (unsigned)nc, 0, 56, s),
                "candidate sort");
         // the used set: one bit per id issued so far
         const size_t used = 4 * (size_t)((n + naux_known + 31) / 32);
