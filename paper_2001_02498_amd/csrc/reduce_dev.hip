@@ -666,19 +666,33 @@ __global__ __launch_bounds__(kGreedyThreads) void greedy_kernel(
 }
 
 // ------------------------------------------------------------ Algorithm 3
-// the pairs of round `round` (the last `taken` of all pairs so far)
-__global__ void set_partner_kernel(const int32_t* __restrict__ all_pairs, int n,
-                                   const DevState* st, int round,
-                                   int32_t* __restrict__ partner, int32_t* __restrict__ newid,
-                                   int reset) {
-    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+// The pairs of round `round` (the last `taken` of all pairs so far) mark
+// their ids with the partner and the pair's new id, after the previous
+// round's marks are cleared (its ids may pair again). One workgroup, so the
+// barrier orders the clears before the marks; nothing reads the marks
+// between one round's rewrite and the next round's marking, and a call
+// starts from cleared arrays.
+__global__ __launch_bounds__(kScanThreads) void set_partner_kernel(
+    const int32_t* __restrict__ all_pairs, int n, const DevState* st, int round,
+    int32_t* __restrict__ partner, int32_t* __restrict__ newid) {
     const long long taken = st->round[round].taken, naux0 = st->naux - taken;
-    if (i >= taken) return;
+    if (round > 0) {
+        const long long prev = st->round[round - 1].taken;
+        const int32_t* pp = all_pairs + 2 * (naux0 - prev);
+        for (long long i = threadIdx.x; i < prev; i += kScanThreads) {
+            const int32_t x = pp[2 * i], y = pp[2 * i + 1];
+            partner[x] = partner[y] = -1;
+            newid[x] = newid[y] = -1;
+        }
+        __syncthreads();
+    }
     const int32_t* pairs = all_pairs + 2 * naux0;
-    const int32_t x = pairs[2 * i], y = pairs[2 * i + 1];
-    partner[x] = reset ? -1 : y;
-    partner[y] = reset ? -1 : x;
-    newid[x] = newid[y] = reset ? -1 : n + (int32_t)(naux0 + i);
+    for (long long i = threadIdx.x; i < taken; i += kScanThreads) {
+        const int32_t x = pairs[2 * i], y = pairs[2 * i + 1];
+        partner[x] = y;
+        partner[y] = x;
+        newid[x] = newid[y] = n + (int32_t)(naux0 + i);
+    }
 }
 
 // One workgroup per list; the list's ids are marked in an LDS bitmap
@@ -1109,8 +1123,8 @@ int redundancy_reduce_device(const int32_t* rowptr_h, const int32_t* col_h, int6
                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)bits),
                    "rewrite LDS");
         }
-        set_partner_kernel<<<items_grid(budget_ub), kBlock, 0, s>>>(pairs, (int)n, dst, round,
-                                                                    I(dp.partner), I(dp.newid), 0);
+        set_partner_kernel<<<1, kScanThreads, 0, s>>>(pairs, (int)n, dst, round, I(dp.partner),
+                                                      I(dp.newid));
         // the rewrite: one wavefront per list where its bitmaps fit, else one
         // workgroup (the new lengths: one workgroup per list, which measured
         // faster than a wavefront per list)
@@ -1132,8 +1146,6 @@ int redundancy_reduce_device(const int32_t* rowptr_h, const int32_t* col_h, int6
             rewrite_fill_kernel<<<(unsigned)n, kRowThreads, bits, s>>>(
                 (int)n, dst, round, rowptr[cur], col[cur], I(dp.partner), I(dp.newid),
                 rowptr[nxt], col[nxt], I(dp.scratch));
-        set_partner_kernel<<<items_grid(budget_ub), kBlock, 0, s>>>(pairs, (int)n, dst, round,
-                                                                    I(dp.partner), I(dp.newid), 1);
         GCN_DR(hipGetLastError(), "rewrite");
         cur = nxt;
         rounds = round + 1;
