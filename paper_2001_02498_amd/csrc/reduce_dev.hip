@@ -85,8 +85,9 @@ __device__ __forceinline__ uint64_t cand_key(uint32_t w, uint32_t x, uint32_t y)
 // kScanPer consecutive values per thread, all loaded before any is used: a
 // scan inside the thread, one across the wavefront by shuffles, one across
 // the 16 wavefront totals). cur, when set, also receives the exclusive
-// prefix out[i] for i < len; it may be in itself, since every value is
-// read by the thread that overwrites it, before it does. With num_add,
+// prefix out[i] wherever in[i] is nonzero; it may be in itself, since every
+// value is read by the thread that overwrites it, before it does (a zero
+// count then stays zero). With num_add,
 // also the sum of max(in[i] - 1, 0) (numAdd of Section 3.2 when in holds
 // list lengths).
 __global__ __launch_bounds__(kScanThreads) void scan_kernel(const int32_t* in,
@@ -130,7 +131,7 @@ __global__ __launch_bounds__(kScanThreads) void scan_kernel(const int32_t* in,
         for (int j = 0; j < kScanPer; ++j) {
             if (i0 + j < len) {
                 out[i0 + j + 1] = ex + incl[j];
-                if (cur) cur[i0 + j] = ex + incl[j] - v[j];
+                if (cur && v[j]) cur[i0 + j] = ex + incl[j] - v[j];
             }
         }
         carry += tile;
@@ -149,9 +150,16 @@ __global__ __launch_bounds__(kScanThreads) void scan_kernel(const int32_t* in,
     if (total && t == 0) *total = carry;
 }
 
-__global__ void fill_kernel(int32_t* __restrict__ p, int32_t v, int64_t len) {
+// A reduction's starting state: no id paired yet, every transposed-index
+// count zero (each round's pair counting zeroes them again as it passes).
+__global__ void init_kernel(int32_t* __restrict__ partner, int32_t* __restrict__ newid,
+                            int32_t* __restrict__ tcnt, int64_t len) {
     const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (i < len) p[i] = v;
+    if (i < len) {
+        partner[i] = -1;
+        newid[i] = -1;
+        tcnt[i] = 0;
+    }
 }
 
 // ------------------------------------------------------------ Algorithm 1
@@ -315,7 +323,8 @@ __device__ __forceinline__ int lower_bound_dev(const int32_t* __restrict__ a, in
 __global__ __launch_bounds__(kCountThreads) void count_pairs_kernel(
     int n, int theta, const int32_t* __restrict__ col,
     const int32_t* __restrict__ tptr, const int32_t* __restrict__ tnext,
-    const int32_t* __restrict__ tend, uint64_t* __restrict__ cand, int64_t cap,
+    const int32_t* __restrict__ tend, int32_t* __restrict__ tcur, uint64_t* __restrict__ cand,
+    int64_t cap,
     DevState* st, int round) {
     extern __shared__ uint32_t cnt[];
     __shared__ int32_t s_start[kCountStage];
@@ -335,6 +344,8 @@ __global__ __launch_bounds__(kCountThreads) void count_pairs_kernel(
     for (int i = t; i < (win + 1) / 2; i += kCountThreads) cnt[i] = 0;
     __syncthreads();
     for (int x = blockIdx.x; x < ncols; x += gridDim.x) {
+        // the fill cursors are done with: zero them as the next round's counts
+        if (t == 0) tcur[x] = 0;
         const int tb = tptr[x], te = tptr[x + 1];
         if (te - tb < 2) continue;   // uniform: x in fewer than two lists
         // the windows [y0, y0 + win) holding ids above x
@@ -1023,8 +1034,8 @@ int redundancy_reduce_device(const int32_t* rowptr_h, const int32_t* col_h, int6
            "upload");
     GCN_DR(hipMemcpyAsync(col[0], col_h, 4 * (size_t)nnz, hipMemcpyHostToDevice, s), "upload");
     GCN_DR(hipMemsetAsync(dst, 0, sizeof(DevState), s), "state");
-    fill_kernel<<<items_grid(dp.ncols_cap), kBlock, 0, s>>>(I(dp.partner), -1, dp.ncols_cap);
-    fill_kernel<<<items_grid(dp.ncols_cap), kBlock, 0, s>>>(I(dp.newid), -1, dp.ncols_cap);
+    init_kernel<<<items_grid(dp.ncols_cap), kBlock, 0, s>>>(I(dp.partner), I(dp.newid),
+                                                             I(dp.tcur), dp.ncols_cap);
     GCN_DR(hipGetLastError(), "init");
 
     // The host knows the ids exactly at each round's wait (after the pair
@@ -1036,7 +1047,6 @@ int redundancy_reduce_device(const int32_t* rowptr_h, const int32_t* col_h, int6
     for (int round = 0; round < p->max_rounds; ++round) {
         const int32_t nc_ub = (int32_t)std::min<int64_t>(ncols_ub, dp.ncols_cap);
         // Algorithm 1: transposed index, then pair counts per id
-        fill_kernel<<<items_grid(nc_ub), kBlock, 0, s>>>(I(dp.tcur), 0, nc_ub);
         const bool trans_lds = nc_ub <= kTransMaxIds;
         const dim3 trans_grid((unsigned)((n + kTransLists - 1) / kTransLists));
         if (trans_lds && 4 * (size_t)nc_ub > 48 * 1024) {
@@ -1073,7 +1083,8 @@ int redundancy_reduce_device(const int32_t* rowptr_h, const int32_t* col_h, int6
         const unsigned grid = (unsigned)std::min<int64_t>(nc_ub, 4096);
         count_pairs_kernel<<<grid, kCountThreads, lds, s>>>((int)n, p->theta, col[cur],
                                                             I(dp.tptr), I(dp.tnext),
-                                                            I(dp.tend), keys_in, dp.cand_cap,
+                                                            I(dp.tend), I(dp.tcur), keys_in,
+                                                            dp.cand_cap,
                                                             dst, round);
         GCN_DR(hipGetLastError(), "pair counting");
         // the one wait of the round: the sort needs the candidate count
